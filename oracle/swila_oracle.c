@@ -1,0 +1,203 @@
+/*
+ * SwiLA reference oracle -- TEST INFRASTRUCTURE, NOT PRODUCT CODE.
+ *
+ * A plain, slow, fp64 CPU implementation of the Switching Linear Attention
+ * recurrence exactly as the paper states it (Sec. 3.2: eq. recurrence,
+ * eq. responsibility, eq. retrieval; App. B.2 for how beta and the two
+ * priors are produced from logits).  Only the tests, the smoke check and the
+ * CPU-baseline leg of the benchmark may load it.  It shares no code, header,
+ * table or helper with the GPU library, and it never calls into it.
+ *
+ * Notation follows the paper.  For one head, the state is J matrices
+ * W_j in R^{Dv x Dk}; row d of W_j is the regression weight w_{jd} in R^{Dk}
+ * of mixture component j for output dimension d (App. B.4, "rows index
+ * output dimensions and columns index key dimensions").  Per token t:
+ *
+ *   pi^k_{jd}  = softmax over j of the key-prior logits          (App. B.2)
+ *   beta_{tjd} = sigmoid(beta logit)                              (App. B.2)
+ *   delta_{tjd} = v_{td} - w_{t-1,jd}^T k_t                       (Sec. 3.2)
+ *   r_{tjd} = pi^k_{jd} exp(-delta^2/2) / sum_j' (same)           (eq. responsibility)
+ *   w_{tjd} = w_{t-1,jd} + beta_{tjd} r_{tjd} delta_{tjd} k_t     (eq. recurrence)
+ *   pi^q_{jd}  = softmax over j of the query-prior logits         (App. B.2)
+ *   o_{td} = sum_j pi^q_{jd} w_{tjd}^T q_t   (updated state)      (eq. retrieval)
+ *
+ * Tensor layouts (row-major, every array is double):
+ *   q, k          [B, T, H, Dk]
+ *   v, o          [B, T, H, Dv]
+ *   *_logit, resp [B, T, H, J, Dv]
+ *   state         [B, H, J, Dk, Dv]   element (b,h,j,i,d) = (W_j)_{d,i}
+ * The state layout is the storage convention of the library under test; the
+ * oracle converts it to its own W[j][d][i] on entry and back on exit.
+ *
+ * Decode (one token with state in and out) is this same function with T = 1.
+ */
+#include <math.h>
+#include <pthread.h>
+#include <stddef.h>
+#include <stdlib.h>
+#include <string.h>
+#include <unistd.h>
+
+typedef struct {
+    int B, H, T, Dk, Dv, J;
+    const double *q, *k, *v, *lb, *lk, *lq, *state_in;
+    double *state_out, *o, *resp, *delta_out;
+    int next_head;              /* work counter, guarded by mu */
+    int status;                 /* first error seen, guarded by mu */
+    pthread_mutex_t mu;
+} job_t;
+
+/* One (b, h) sequence, straight from the definitions above. */
+static int run_head(job_t *a, int b, int h)
+{
+    const int H = a->H, T = a->T, Dk = a->Dk, Dv = a->Dv, J = a->J;
+    double *W = (double *)malloc(sizeof(double) * (size_t)J * Dv * Dk);
+    double *prior = (double *)malloc(sizeof(double) * (size_t)J);
+    double *num = (double *)malloc(sizeof(double) * (size_t)J);
+    double *delta = (double *)malloc(sizeof(double) * (size_t)J);
+    if (!W || !prior || !num || !delta) {
+        free(W); free(prior); free(num); free(delta);
+        return -2;
+    }
+    int rc = 0;
+
+    /* initial state W_0 (zeros when none is given) */
+    for (int j = 0; j < J; ++j)
+        for (int d = 0; d < Dv; ++d)
+            for (int i = 0; i < Dk; ++i) {
+                size_t s = ((((size_t)b * H + h) * J + j) * Dk + i) * Dv + d;
+                W[((size_t)j * Dv + d) * Dk + i] = a->state_in ? a->state_in[s] : 0.0;
+            }
+
+    for (int t = 0; t < T && rc == 0; ++t) {
+        const size_t row = ((size_t)b * T + t) * H + h;
+        const double *kt = a->k + row * Dk;
+        const double *qt = a->q + row * Dk;
+        const double *vt = a->v + row * Dv;
+        const double *lbt = a->lb + row * (size_t)J * Dv;
+        const double *lkt = a->lk + row * (size_t)J * Dv;
+        const double *lqt = a->lq + row * (size_t)J * Dv;
+
+        for (int d = 0; d < Dv; ++d) {
+            /* key-side prior pi^k_{jd} = softmax_j(logit) */
+            double m = -INFINITY, z = 0.0;
+            for (int j = 0; j < J; ++j) m = fmax(m, lkt[(size_t)j * Dv + d]);
+            for (int j = 0; j < J; ++j) z += exp(lkt[(size_t)j * Dv + d] - m);
+            for (int j = 0; j < J; ++j) prior[j] = exp(lkt[(size_t)j * Dv + d] - m) / z;
+
+            /* prediction errors with the previous state */
+            for (int j = 0; j < J; ++j) {
+                const double *w = W + ((size_t)j * Dv + d) * Dk;
+                double pred = 0.0;
+                for (int i = 0; i < Dk; ++i) pred += w[i] * kt[i];
+                delta[j] = vt[d] - pred;
+            }
+
+            /* E-step: responsibilities, pi * N(v; w^T k, 1) normalised over j */
+            double Z = 0.0;
+            for (int j = 0; j < J; ++j) {
+                num[j] = prior[j] * exp(-0.5 * delta[j] * delta[j]);
+                Z += num[j];
+            }
+            if (!(Z > 0.0) || !isfinite(Z)) { rc = -1; break; }
+
+            /* M-step: one gradient step of size beta on the log-likelihood */
+            for (int j = 0; j < J; ++j) {
+                const double r = num[j] / Z;
+                const double beta = 1.0 / (1.0 + exp(-lbt[(size_t)j * Dv + d]));
+                double *w = W + ((size_t)j * Dv + d) * Dk;
+                for (int i = 0; i < Dk; ++i) w[i] += beta * r * delta[j] * kt[i];
+                if (a->resp) a->resp[(row * J + j) * Dv + d] = r;
+                if (a->delta_out) a->delta_out[(row * J + j) * Dv + d] = delta[j];
+            }
+
+            /* retrieval from the updated state, query-side prior softmax_j */
+            m = -INFINITY; z = 0.0;
+            for (int j = 0; j < J; ++j) m = fmax(m, lqt[(size_t)j * Dv + d]);
+            for (int j = 0; j < J; ++j) z += exp(lqt[(size_t)j * Dv + d] - m);
+            double out = 0.0;
+            for (int j = 0; j < J; ++j) {
+                const double pq = exp(lqt[(size_t)j * Dv + d] - m) / z;
+                const double *w = W + ((size_t)j * Dv + d) * Dk;
+                double y = 0.0;
+                for (int i = 0; i < Dk; ++i) y += w[i] * qt[i];
+                out += pq * y;
+            }
+            a->o[row * Dv + d] = out;
+        }
+    }
+
+    if (rc == 0 && a->state_out)
+        for (int j = 0; j < J; ++j)
+            for (int d = 0; d < Dv; ++d)
+                for (int i = 0; i < Dk; ++i) {
+                    size_t s = ((((size_t)b * H + h) * J + j) * Dk + i) * Dv + d;
+                    a->state_out[s] = W[((size_t)j * Dv + d) * Dk + i];
+                }
+
+    free(W); free(prior); free(num); free(delta);
+    return rc;
+}
+
+static void *worker(void *p)
+{
+    job_t *a = (job_t *)p;
+    for (;;) {
+        pthread_mutex_lock(&a->mu);
+        int hh = a->next_head++;
+        int stop = a->status != 0;
+        pthread_mutex_unlock(&a->mu);
+        if (stop || hh >= a->B * a->H) break;
+        int rc = run_head(a, hh / a->H, hh % a->H);
+        if (rc != 0) {
+            pthread_mutex_lock(&a->mu);
+            if (a->status == 0) a->status = rc;
+            pthread_mutex_unlock(&a->mu);
+        }
+    }
+    return NULL;
+}
+
+/*
+ * Forward over T tokens for every (b, h).  state_in may be NULL (zeros);
+ * state_out, resp_out and delta_out may be NULL (not written).  state_out
+ * must not alias state_in.  nthreads <= 0 uses every online core.
+ * Returns 0, -1 if a responsibility normaliser is zero or not finite,
+ * -2 on allocation failure, -3 on bad sizes.
+ */
+int swila_oracle_forward(int B, int H, int T, int Dk, int Dv, int J,
+                         const double *q, const double *k, const double *v,
+                         const double *beta_logit, const double *prior_k_logit,
+                         const double *prior_q_logit, const double *state_in,
+                         double *state_out, double *o, double *resp_out,
+                         double *delta_out, int nthreads)
+{
+    if (B < 0 || H < 0 || T < 0 || Dk <= 0 || Dv <= 0 || J <= 0) return -3;
+    job_t a;
+    memset(&a, 0, sizeof a);
+    a.B = B; a.H = H; a.T = T; a.Dk = Dk; a.Dv = Dv; a.J = J;
+    a.q = q; a.k = k; a.v = v;
+    a.lb = beta_logit; a.lk = prior_k_logit; a.lq = prior_q_logit;
+    a.state_in = state_in; a.state_out = state_out; a.o = o;
+    a.resp = resp_out; a.delta_out = delta_out;
+    pthread_mutex_init(&a.mu, NULL);
+
+    int n = nthreads;
+    if (n <= 0) n = (int)sysconf(_SC_NPROCESSORS_ONLN);
+    if (n < 1) n = 1;
+    if (n > B * H) n = B * H;
+    if (n <= 1) {
+        worker(&a);
+    } else {
+        pthread_t *th = (pthread_t *)malloc(sizeof(pthread_t) * (size_t)n);
+        if (!th) { pthread_mutex_destroy(&a.mu); return -2; }
+        int started = 0;
+        for (int i = 0; i < n; ++i)
+            if (pthread_create(&th[i], NULL, worker, &a) == 0) ++started;
+        if (started == 0) worker(&a);
+        for (int i = 0; i < started; ++i) pthread_join(th[i], NULL);
+        free(th);
+    }
+    pthread_mutex_destroy(&a.mu);
+    return a.status;
+}
