@@ -17,6 +17,7 @@
  *   beta_{tjd} = sigmoid(beta logit)                              (App. B.2)
  *   delta_{tjd} = v_{td} - w_{t-1,jd}^T k_t                       (Sec. 3.2)
  *   r_{tjd} = pi^k_{jd} exp(-delta^2/2) / sum_j' (same)           (eq. responsibility)
+ *             (evaluated with every exp(-delta^2/2) divided by the largest)
  *   w_{tjd} = w_{t-1,jd} + beta_{tjd} r_{tjd} delta_{tjd} k_t     (eq. recurrence)
  *   pi^q_{jd}  = softmax over j of the query-prior logits         (App. B.2)
  *   o_{td} = sum_j pi^q_{jd} w_{tjd}^T q_t   (updated state)      (eq. retrieval)
@@ -93,10 +94,15 @@ static int run_head(job_t *a, int b, int h)
                 delta[j] = vt[d] - pred;
             }
 
-            /* E-step: responsibilities, pi * N(v; w^T k, 1) normalised over j */
+            /* E-step: responsibilities, pi * N(v; w^T k, 1) normalised over j.
+             * Numerator and denominator are both divided by the largest
+             * exp(-delta^2/2), which leaves r unchanged and keeps the
+             * normaliser finite when every exp(-delta^2/2) underflows. */
+            double shift = -INFINITY;
+            for (int j = 0; j < J; ++j) shift = fmax(shift, -0.5 * delta[j] * delta[j]);
             double Z = 0.0;
             for (int j = 0; j < J; ++j) {
-                num[j] = prior[j] * exp(-0.5 * delta[j] * delta[j]);
+                num[j] = prior[j] * exp(-0.5 * delta[j] * delta[j] - shift);
                 Z += num[j];
             }
             if (!(Z > 0.0) || !isfinite(Z)) { rc = -1; break; }

@@ -70,6 +70,19 @@ def pin_bayes_estep(fwd):
         prior = scipy.special.softmax(lk[:, t], axis=2)
         post = prior * like / (prior * like).sum(axis=2, keepdims=True)
         err = max(err, np.max(np.abs(post - r[:, t])))
+    # errors so large that every density underflows in fp64: Bayes' rule in log
+    # space (scipy's normal log-density and a softmax over j)
+    inp = _inp(1, 2, 5, 3, 4, 3, seed=20, state_std=3.0, logit_scale=5.0)
+    inp["v"] = inp["v"] * np.float32(60.0)
+    S = _prefix_states(fwd, inp)
+    r = fwd(*_args(inp), inp["state"], want_resp=True)["resp"]
+    q, k, v, lb, lk, lq = _args(inp)
+    for t in range(k.shape[1]):
+        pred = np.einsum("bhjid,bhi->bhjd", S[t], k[:, t])
+        logpost = (scipy.special.log_softmax(lk[:, t], axis=2)
+                   + scipy.stats.norm.logpdf(v[:, t][:, :, None, :], loc=pred, scale=1.0))
+        post = scipy.special.softmax(logpost, axis=2)
+        err = max(err, np.max(np.abs(post - r[:, t])))
     return err
 
 

@@ -14,7 +14,11 @@ STATE_IDX = "((((size_t)b * H + h) * J + j) * Dk + i) * Dv + d"
 
 # name -> (text in the oracle, replacement, replace every occurrence?)
 MUTATIONS = {
-    "half_dropped_in_estep": ("exp(-0.5 * delta[j] * delta[j])", "exp(-1.0 * delta[j] * delta[j])", False),
+    "half_dropped_in_estep": ("exp(-0.5 * delta[j] * delta[j] - shift)",
+                              "exp(-1.0 * delta[j] * delta[j] - shift)", False),
+    "estep_shift_ignored": ("num[j] = prior[j] * exp(-0.5 * delta[j] * delta[j] - shift);",
+                            "num[j] = prior[j] * exp(-0.5 * delta[j] * delta[j] - shift * j);",
+                            False),
     "delta_sign_flipped": ("delta[j] = vt[d] - pred;", "delta[j] = pred - vt[d];", False),
     "prediction_with_query": ("pred += w[i] * kt[i];", "pred += w[i] * qt[i];", False),
     "prior_dropped": ("num[j] = prior[j] * exp(", "num[j] = 1.0 * exp(", False),
