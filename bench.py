@@ -1,0 +1,188 @@
+"""Benchmark of the SwiLA hot path on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--config 2] [--no-decode] [--no-cpu-baseline]
+
+A step is one swila_forward call over the whole batch of the small
+training-shaped workload (B=4, H=8, T=2048, Dk=Dv=64, J=4, bf16 inputs, fp32
+state), inputs resident in HBM.  value = B*T / seconds per step (tokens/s).
+The same run also times the batched decode workload (B=256, H=16, D=128, J=4,
+512 one-token steps, state updated in place) and reports it under "decode",
+and times the fp64 oracle on the host cores ("cpu_baseline").
+
+Prints one JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = ("SwiLA fwd tokens/sec at B·H·T·D·K; decode steps/sec; "
+          "% HBM/MFMA roofline")
+PEAK_HBM = 8.0e12          # B/s, MI355X HBM3E
+PEAK_VALU_F32 = 157.3e12   # FLOP/s, MI355X fp32 vector (packed); unpacked FMA is half
+PEAK_MFMA_BF16 = 2.5e15    # FLOP/s, MI355X dense bf16 matrix
+
+
+def forward_alg_bytes(B, H, T, Dk, Dv, J, in_bytes=2, out_bytes=2, state_in=False,
+                      state_out=True):
+    """Bytes the forward must move at least once: q, k, v, three logit tensors,
+    the output, and the state (read if given, written if kept)."""
+    per_token_head = in_bytes * (2 * Dk + Dv) + in_bytes * 3 * J * Dv + out_bytes * Dv
+    state = 4 * J * Dk * Dv * B * H
+    return B * H * T * per_token_head + state * (int(state_in) + int(state_out))
+
+
+def forward_alg_flops(B, H, T, Dk, Dv, J):
+    """Two length-Dk dots (w.k, w.q) and one rank-one update per (t, j, d):
+    3 * Dk * J * Dv fused multiply-adds per token and head, 2 FLOP each."""
+    return 2 * 3 * Dk * J * Dv * B * H * T
+
+
+def decode_alg_bytes(B, H, Dk, Dv, J, in_bytes=2, out_bytes=2):
+    """Per step: the state read and written once, one token of inputs, output."""
+    return (2 * 4 * J * Dk * Dv + in_bytes * (2 * Dk + Dv + 3 * J * Dv) + out_bytes * Dv) * B * H
+
+
+def host_cores():
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count() or 1
+    return max(1, min(n, 16))
+
+
+def time_forward(sw, torch, dev, steps, warmup, o, s_out):
+    names = ("q", "k", "v", "lb", "lk", "lq")
+    args = [dev[n] for n in names]
+    for _ in range(warmup):
+        sw.forward(*args, dev["state"], o=o, state_out=s_out)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(steps)]
+    t0 = time.perf_counter()
+    for i in range(steps):
+        ev[i][0].record(stream)
+        sw.forward(*args, dev["state"], o=o, state_out=s_out)
+        ev[i][1].record(stream)
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) / steps
+    kern = sum(a.elapsed_time(b) for a, b in ev) / steps / 1e3
+    return wall, kern
+
+
+def bench_decode(sw, torch, workloads, steps_total, warmup):
+    c = workloads.CONFIGS[4]
+    B, H, Dk, Dv, J = c["B"], c["H"], c["Dk"], c["Dv"], c["J"]
+    st = torch.from_numpy(workloads.decode_initial_state(B, H, Dk, Dv, J)).cuda()
+    inputs = [workloads.decode_step_inputs_torch(t, B, H, Dk, Dv, J) for t in range(steps_total)]
+    o = torch.empty((B, H, Dv), device="cuda", dtype=torch.bfloat16)
+    names = ("q", "k", "v", "lb", "lk", "lq")
+    for t in range(warmup):
+        sw.decode_step(*(inputs[t % steps_total][n] for n in names), st, state_out=st, o=o)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(steps_total)]
+    t0 = time.perf_counter()
+    for t in range(steps_total):
+        ev[t][0].record(stream)
+        sw.decode_step(*(inputs[t][n] for n in names), st, state_out=st, o=o)
+        ev[t][1].record(stream)
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) / steps_total
+    kern = sum(a.elapsed_time(b) for a, b in ev) / steps_total / 1e3
+    nbytes = decode_alg_bytes(B, H, Dk, Dv, J)
+    assert torch.isfinite(st).all().item()
+    return {
+        "workload": "batched decode B=%d H=%d Dk=Dv=%d J=%d, %d one-token steps, bf16 inputs, "
+                    "fp32 state N(0,0.1^2) updated in place" % (B, H, Dk, J, steps_total),
+        "steps_per_s": 1.0 / wall, "tokens_per_s": B / wall, "ms_per_step": wall * 1e3,
+        "roofline": {"bound": "hbm", "achieved": nbytes / kern / 1e9, "peak": PEAK_HBM / 1e9,
+                     "unit": "GB/s", "frac": nbytes / kern / PEAK_HBM, "traffic": None,
+                     "kernel_ms": kern * 1e3, "alg_bytes_per_launch": nbytes},
+    }
+
+
+def cpu_baseline(workloads, inp, cfg):
+    import oracle
+    n = host_cores()
+    names = ("q", "k", "v", "lb", "lk", "lq")
+    oracle.build()
+    t0 = time.perf_counter()
+    oracle.forward(*(inp[x] for x in names), inp["state"], nthreads=n)
+    dt = time.perf_counter() - t0
+    B, T = cfg["B"], cfg["T"]
+    return {"value": B * T / dt, "unit": "tokens/s", "cores": n, "kind": "oracle",
+            "sample": "the whole benchmark batch (B=%d H=%d T=%d), fp64, %d threads, %.1f s"
+                      % (B, cfg["H"], T, n, dt)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 5])
+    ap.add_argument("--decode-steps", type=int, default=512)
+    ap.add_argument("--no-decode", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the SwiLA path has no cross-GPU step; "
+              "run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2609_39034_amd as sw
+    import workloads
+
+    sw.load_library()
+    cfg = workloads.CONFIGS[args.config]
+    B, H, T, Dk, Dv, J = (cfg[x] for x in ("B", "H", "T", "Dk", "Dv", "J"))
+    bf16 = cfg["dtype"] == "bf16"
+    tdt = torch.bfloat16 if bf16 else torch.float32
+    inp = workloads.config_inputs(args.config)
+    dev = workloads.to_torch(inp, "cuda", tdt)
+    o = torch.empty((B, T, H, Dv), device="cuda", dtype=tdt)
+    s_out = torch.empty((B, H, J, Dk, Dv), device="cuda", dtype=torch.float32)
+    wall, kern = time_forward(sw, torch, dev, args.steps, args.warmup, o, s_out)
+
+    eb = 2 if bf16 else 4
+    nbytes = forward_alg_bytes(B, H, T, Dk, Dv, J, eb, eb, dev["state"] is not None, True)
+    nflop = forward_alg_flops(B, H, T, Dk, Dv, J)
+    out = {
+        "metric": METRIC, "value": B * T / wall, "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": wall * 1e3,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "io_dtype": "bf16" if bf16 else "f32", "data": "synthetic",
+        "config": {"workload": "SwiLA forward, %s: B=%d H=%d T=%d Dk=Dv=%d J=%d, %s inputs, "
+                               "fp32 state, zero initial state, seeded"
+                               % (cfg["name"], B, H, T, Dk, J, cfg["dtype"]),
+                   "B": B, "H": H, "T": T, "Dk": Dk, "Dv": Dv, "J": J, "algo": "recurrent"},
+        "roofline": {"bound": "alu", "achieved": nflop / kern / 1e12, "peak": PEAK_VALU_F32 / 1e12,
+                     "unit": "TFLOP/s", "frac": nflop / kern / PEAK_VALU_F32, "traffic": None,
+                     "kernel": "scan_direct_kernel", "kernel_ms": kern * 1e3,
+                     "alg_flop_per_launch": nflop},
+        "roofline_hbm": {"achieved": nbytes / kern / 1e9, "peak": PEAK_HBM / 1e9, "unit": "GB/s",
+                         "frac": nbytes / kern / PEAK_HBM, "alg_bytes_per_launch": nbytes},
+        "head_tokens_per_s": B * H * T / wall,
+    }
+    if not args.no_decode:
+        out["decode"] = bench_decode(sw, torch, workloads, args.decode_steps, args.warmup)
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(workloads, inp, cfg)
+    else:
+        out["cpu_baseline"] = None
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

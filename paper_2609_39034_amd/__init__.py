@@ -1,0 +1,265 @@
+"""SwiLA hot path for MI355X (gfx950): Python binding of libswila.so.
+
+The binding only marshals arguments: it checks tensors, allocates outputs
+with torch (device memory), and calls the C ABI declared in
+``include/swila.h`` with raw device pointers and the current HIP stream.
+Every step of the layer runs in the library's HIP kernels.  There is no
+fallback: if ``libswila.so`` is missing or fails to load, importing the
+library raises.
+
+Entry points (names as in the C ABI):
+  ``forward``            whole sequences       -> swila_forward
+  ``decode_step``        one token per sequence -> swila_decode_step
+  ``state_init``         initial state          -> swila_state_init
+  ``state_bytes``, ``forward_workspace_bytes``, ``version``
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+__all__ = ["forward", "decode_step", "state_init", "state_bytes", "forward_workspace_bytes",
+           "version", "library_path", "SwilaError", "F32", "BF16", "ALGO_AUTO",
+           "ALGO_RECURRENT"]
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "libswila.so")
+
+F32, BF16 = 0, 1
+ALGO_AUTO, ALGO_RECURRENT = 0, 1
+_ALGOS = {"auto": ALGO_AUTO, "recurrent": ALGO_RECURRENT}
+
+OK, EINVAL, EUNSUPPORTED, EHIP = 0, -1, -2, -3
+
+
+class SwilaError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__("swila error %d: %s" % (code, msg))
+        self.code = code
+
+
+class Shape(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in ("B", "H", "T", "Dk", "Dv", "J")]
+
+
+class Opts(ctypes.Structure):
+    _fields_ = [("in_dtype", ctypes.c_int32), ("out_dtype", ctypes.c_int32),
+                ("algo", ctypes.c_int32), ("chunk", ctypes.c_int32),
+                ("max_iters", ctypes.c_int32), ("tol", ctypes.c_float),
+                ("flags", ctypes.c_uint32)]
+
+
+_lib = None
+
+
+def library_path() -> str:
+    return _LIB_PATH
+
+
+def load_library():
+    """The ctypes handle of libswila.so (loaded once).  Raises if it is absent."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        raise ImportError("libswila.so is not built (%s); run __graft_entry__.build() or "
+                          "python -m paper_2609_39034_amd.build" % _LIB_PATH)
+    lib = ctypes.CDLL(_LIB_PATH)
+    vp, sp, op = ctypes.c_void_p, ctypes.POINTER(Shape), ctypes.POINTER(Opts)
+    lib.swila_version.restype = ctypes.c_int
+    lib.swila_version.argtypes = []
+    lib.swila_last_error.restype = ctypes.c_char_p
+    lib.swila_last_error.argtypes = []
+    lib.swila_state_bytes.restype = ctypes.c_size_t
+    lib.swila_state_bytes.argtypes = [sp]
+    lib.swila_state_init.restype = ctypes.c_int
+    lib.swila_state_init.argtypes = [sp, vp, vp, vp]
+    lib.swila_forward_workspace_bytes.restype = ctypes.c_size_t
+    lib.swila_forward_workspace_bytes.argtypes = [sp, op]
+    lib.swila_forward.restype = ctypes.c_int
+    lib.swila_forward.argtypes = [sp, op] + [vp] * 6 + [vp, vp, vp, vp, vp, ctypes.c_size_t, vp, vp]
+    lib.swila_decode_step.restype = ctypes.c_int
+    lib.swila_decode_step.argtypes = [sp, op] + [vp] * 6 + [vp, vp, vp, vp]
+    _lib = lib
+    return lib
+
+
+def _check(rc):
+    if rc != OK:
+        raise SwilaError(rc, load_library().swila_last_error().decode(errors="replace"))
+
+
+def version() -> int:
+    return load_library().swila_version()
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _dtype_code(t):
+    torch = _torch()
+    if t.dtype == torch.bfloat16:
+        return BF16
+    if t.dtype == torch.float32:
+        return F32
+    raise TypeError("inputs must be float32 or bfloat16, got %s" % t.dtype)
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream_handle(stream):
+    torch = _torch()
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _dev_tensor(t, name, dtype=None):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("%s must be a device tensor" % name)
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError("%s must be %s, got %s" % (name, dtype, t.dtype))
+    return t
+
+
+def state_bytes(B, H, Dk, Dv, J) -> int:
+    return load_library().swila_state_bytes(ctypes.byref(Shape(B, H, 0, Dk, Dv, J)))
+
+
+def forward_workspace_bytes(B, H, T, Dk, Dv, J, *, in_dtype=BF16, out_dtype=None,
+                            algo="auto", chunk=0) -> int:
+    opts = Opts(in_dtype, in_dtype if out_dtype is None else out_dtype, _ALGOS[algo], chunk,
+                0, 0.0, 0)
+    return load_library().swila_forward_workspace_bytes(ctypes.byref(Shape(B, H, T, Dk, Dv, J)),
+                                                         ctypes.byref(opts))
+
+
+def state_init(state, src=None, *, stream=None):
+    """state [B,H,J,Dk,Dv] float32 <- copy of src, or zeros when src is None."""
+    torch = _torch()
+    _dev_tensor(state, "state", torch.float32)
+    _dev_tensor(src, "src", torch.float32)
+    if state.dim() != 5:
+        raise ValueError("state must be [B,H,J,Dk,Dv]")
+    if src is not None and src.shape != state.shape:
+        raise ValueError("src shape %s != state shape %s" % (tuple(src.shape), tuple(state.shape)))
+    B, H, J, Dk, Dv = state.shape
+    _check(load_library().swila_state_init(ctypes.byref(Shape(B, H, 0, Dk, Dv, J)), _ptr(state),
+                                           _ptr(src), _stream_handle(stream)))
+    return state
+
+
+def _layer_shapes(q, v, lb, decode):
+    if decode:
+        B, H, Dk = q.shape
+        T = 1
+        Dv = v.shape[-1]
+        J = lb.shape[2]
+    else:
+        B, T, H, Dk = q.shape
+        Dv = v.shape[-1]
+        J = lb.shape[3]
+    return B, H, T, Dk, Dv, J
+
+
+def forward(q, k, v, beta_logit, prior_k_logit, prior_q_logit, state_in=None, *,
+            state_out=True, o=None, out_dtype=None, resp=False, algo="auto", chunk=0,
+            workspace=None, stream=None):
+    """Forward over whole sequences (swila_forward).
+
+    q, k [B,T,H,Dk]; v [B,T,H,Dv]; logits [B,T,H,J,Dv] (one dtype: float32 or
+    bfloat16); state_in [B,H,J,Dk,Dv] float32 or None (zeros).
+    state_out: True to allocate the final state, False to discard it, or a
+    float32 tensor to write (may be state_in itself).  o: optional output
+    tensor; out_dtype defaults to the input dtype.  resp=True also returns the
+    key-side responsibilities [B,T,H,J,Dv] float32.
+    Returns (o, state_out or None) or (o, state_out, resp).
+    """
+    torch = _torch()
+    names = ("q", "k", "v", "beta_logit", "prior_k_logit", "prior_q_logit")
+    ins = [_dev_tensor(t, n) for t, n in zip((q, k, v, beta_logit, prior_k_logit, prior_q_logit),
+                                             names)]
+    code = _dtype_code(q)
+    for t, n in zip(ins, names):
+        if _dtype_code(t) != code:
+            raise TypeError("%s has dtype %s but q has %s" % (n, t.dtype, q.dtype))
+    B, H, T, Dk, Dv, J = _layer_shapes(q, v, beta_logit, decode=False)
+    expect = {"q": (B, T, H, Dk), "k": (B, T, H, Dk), "v": (B, T, H, Dv),
+              "beta_logit": (B, T, H, J, Dv), "prior_k_logit": (B, T, H, J, Dv),
+              "prior_q_logit": (B, T, H, J, Dv)}
+    for t, n in zip(ins, names):
+        if tuple(t.shape) != expect[n]:
+            raise ValueError("%s has shape %s, expected %s" % (n, tuple(t.shape), expect[n]))
+    _dev_tensor(state_in, "state_in", torch.float32)
+    if state_in is not None and tuple(state_in.shape) != (B, H, J, Dk, Dv):
+        raise ValueError("state_in must be [B,H,J,Dk,Dv] = %s" % ((B, H, J, Dk, Dv),))
+    odt = q.dtype if out_dtype is None else out_dtype
+    if o is None:
+        o = torch.empty((B, T, H, Dv), device=q.device, dtype=odt)
+    _dev_tensor(o, "o")
+    if state_out is True:
+        s_out = torch.empty((B, H, J, Dk, Dv), device=q.device, dtype=torch.float32)
+    elif state_out is False or state_out is None:
+        s_out = None
+    else:
+        s_out = _dev_tensor(state_out, "state_out", torch.float32)
+    r = None
+    if resp:
+        r = torch.empty((B, T, H, J, Dv), device=q.device, dtype=torch.float32)
+    opts = Opts(code, _dtype_code(o), _ALGOS[algo], int(chunk), 0, 0.0, 0)
+    ws_ptr, ws_bytes = None, 0
+    if workspace is not None:
+        ws_ptr, ws_bytes = _ptr(workspace), workspace.numel() * workspace.element_size()
+    _check(load_library().swila_forward(
+        ctypes.byref(Shape(B, H, T, Dk, Dv, J)), ctypes.byref(opts),
+        *[_ptr(t) for t in ins], _ptr(state_in), _ptr(s_out), _ptr(o), _ptr(r),
+        ws_ptr, ws_bytes, None, _stream_handle(stream)))
+    return (o, s_out, r) if resp else (o, s_out)
+
+
+def decode_step(q, k, v, beta_logit, prior_k_logit, prior_q_logit, state_in, *,
+                state_out=None, o=None, out_dtype=None, stream=None):
+    """One token per sequence (swila_decode_step).
+
+    q, k [B,H,Dk]; v [B,H,Dv]; logits [B,H,J,Dv]; state_in [B,H,J,Dk,Dv]
+    float32 (None = zeros).  state_out defaults to state_in (updated in place;
+    with state_in None a new tensor is allocated).  Returns (o, state_out).
+    """
+    torch = _torch()
+    names = ("q", "k", "v", "beta_logit", "prior_k_logit", "prior_q_logit")
+    ins = [_dev_tensor(t, n) for t, n in zip((q, k, v, beta_logit, prior_k_logit, prior_q_logit),
+                                             names)]
+    code = _dtype_code(q)
+    for t, n in zip(ins, names):
+        if _dtype_code(t) != code:
+            raise TypeError("%s has dtype %s but q has %s" % (n, t.dtype, q.dtype))
+    B, H, T, Dk, Dv, J = _layer_shapes(q, v, beta_logit, decode=True)
+    expect = {"q": (B, H, Dk), "k": (B, H, Dk), "v": (B, H, Dv), "beta_logit": (B, H, J, Dv),
+              "prior_k_logit": (B, H, J, Dv), "prior_q_logit": (B, H, J, Dv)}
+    for t, n in zip(ins, names):
+        if tuple(t.shape) != expect[n]:
+            raise ValueError("%s has shape %s, expected %s" % (n, tuple(t.shape), expect[n]))
+    _dev_tensor(state_in, "state_in", torch.float32)
+    if state_in is not None and tuple(state_in.shape) != (B, H, J, Dk, Dv):
+        raise ValueError("state_in must be [B,H,J,Dk,Dv] = %s" % ((B, H, J, Dk, Dv),))
+    if state_out is None:
+        state_out = state_in if state_in is not None else torch.empty(
+            (B, H, J, Dk, Dv), device=q.device, dtype=torch.float32)
+    _dev_tensor(state_out, "state_out", torch.float32)
+    odt = q.dtype if out_dtype is None else out_dtype
+    if o is None:
+        o = torch.empty((B, H, Dv), device=q.device, dtype=odt)
+    _dev_tensor(o, "o")
+    opts = Opts(code, _dtype_code(o), ALGO_AUTO, 0, 0, 0.0, 0)
+    _check(load_library().swila_decode_step(
+        ctypes.byref(Shape(B, H, 1, Dk, Dv, J)), ctypes.byref(opts),
+        *[_ptr(t) for t in ins], _ptr(state_in), _ptr(state_out), _ptr(o),
+        _stream_handle(stream)))
+    return o, state_out

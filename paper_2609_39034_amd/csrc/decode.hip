@@ -1,0 +1,202 @@
+// One-token SwiLA decode step (Sec. 3.2 with T = 1): the state is read once
+// from HBM, updated in registers and written once, so the step is bound by HBM
+// bandwidth (state bytes dominate: 2 x J x Dk x Dv x 4 per head and token).
+//
+// Work split.  A block owns one head's block of DB = min(32, Dv) output
+// columns for every component j and key index i: a J x Dk x DB fp32 tile.
+// CL = DB / 4 lanes cover one 128-byte row segment (float4 per lane), so
+// consecutive lanes read consecutive addresses.  Each thread holds 16 rows
+// (i = ig + IG * m, m < 16) of one component j: IG = Dk / 16 row groups per
+// component, J * IG * CL threads per block (at least DB; any extra threads
+// hold no rows and only serve the per-column step).  Per token:
+//   1. every thread forms partial k- and q-dots of its 16 rows for 4 columns;
+//      lanes of the same component and column reduce over row groups;
+//   2. DB threads (one per column) run the E-step over j and the retrieval;
+//   3. every thread applies w += c k to its rows and stores them.
+// state_out may alias state_in: each block reads its whole tile before any
+// write, and tiles of different blocks are disjoint.
+#include "device_common.hpp"
+#include "launch.hpp"
+
+namespace swila {
+namespace {
+
+constexpr int kRows = 16;  // state rows per thread
+
+template <int DK, int J>
+__global__ __launch_bounds__(512) void decode_kernel(LayerArgs a, int DB) {
+    constexpr int IG = DK / kRows;
+    const int CL = DB / 4;
+    const int tid = threadIdx.x;
+    const int cl = tid % CL;
+    const int ig = (tid / CL) % IG;
+    const bool has_rows = tid < J * IG * CL;
+    const int j = has_rows ? tid / (CL * IG) : 0;
+    const int d0 = blockIdx.x * DB;
+    const int h = blockIdx.y, b = blockIdx.z;
+    const int H = a.H, Dv = a.Dv;
+    const bool ibf = a.in_bf16;
+
+    __shared__ float sk[DK], sq[DK];
+    __shared__ float sP[J][32], sY[J][32], sC[J][32];
+    __shared__ float sKQ;
+
+    // state tile rows of this thread
+    const size_t sbase = ((size_t)b * H + h) * J * DK * Dv + (size_t)j * DK * Dv + d0 + cl * 4;
+    float4 st[kRows];
+    if (a.state_in && has_rows) {
+#pragma unroll
+        for (int m = 0; m < kRows; ++m)
+            st[m] = *reinterpret_cast<const float4 *>(a.state_in + sbase + (size_t)(ig + IG * m) * Dv);
+    } else {
+#pragma unroll
+        for (int m = 0; m < kRows; ++m) st[m] = make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+
+    // per-column inputs, fetched early by the column threads
+    const size_t row = (size_t)b * H + h;
+    float vd = 0.f, lb[J], lk[J], lq[J];
+    if (tid < DB) {
+        vd = load1(a.v, row * Dv + d0 + tid, ibf);
+#pragma unroll
+        for (int jj = 0; jj < J; ++jj) {
+            const size_t idx = (row * J + jj) * Dv + d0 + tid;
+            lb[jj] = load1(a.lb, idx, ibf);
+            lk[jj] = load1(a.lk, idx, ibf);
+            lq[jj] = load1(a.lq, idx, ibf);
+        }
+    }
+    for (int i = tid; i < DK; i += blockDim.x) {
+        sk[i] = load1(a.k, row * DK + i, ibf);
+        sq[i] = load1(a.q, row * DK + i, ibf);
+    }
+    __syncthreads();
+
+    // 1. partial dots over this thread's rows
+    float p[4] = {0.f, 0.f, 0.f, 0.f}, y[4] = {0.f, 0.f, 0.f, 0.f}, kq = 0.f;
+#pragma unroll
+    for (int m = 0; m < kRows; ++m) {
+        const float ki = sk[ig + IG * m], qi = sq[ig + IG * m];
+        p[0] = fmaf(st[m].x, ki, p[0]); y[0] = fmaf(st[m].x, qi, y[0]);
+        p[1] = fmaf(st[m].y, ki, p[1]); y[1] = fmaf(st[m].y, qi, y[1]);
+        p[2] = fmaf(st[m].z, ki, p[2]); y[2] = fmaf(st[m].z, qi, y[2]);
+        p[3] = fmaf(st[m].w, ki, p[3]); y[3] = fmaf(st[m].w, qi, y[3]);
+        kq = fmaf(ki, qi, kq);
+    }
+    for (int off = CL; off < CL * IG; off *= 2) {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            p[c] += __shfl_xor(p[c], off);
+            y[c] += __shfl_xor(y[c], off);
+        }
+        kq += __shfl_xor(kq, off);
+    }
+    if (ig == 0 && has_rows) {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            sP[j][cl * 4 + c] = p[c];
+            sY[j][cl * 4 + c] = y[c];
+        }
+        if (j == 0 && cl == 0) sKQ = kq;
+    }
+    __syncthreads();
+
+    // 2. E-step and retrieval, one thread per column
+    if (tid < DB) {
+        float delta[J], e[J];
+        float m = -INFINITY, mq = -INFINITY;
+#pragma unroll
+        for (int jj = 0; jj < J; ++jj) {
+            delta[jj] = vd - sP[jj][tid];
+            e[jj] = lk[jj] - 0.5f * delta[jj] * delta[jj];
+            m = fmaxf(m, e[jj]);
+            mq = fmaxf(mq, lq[jj]);
+        }
+        float z = 0.f, zq = 0.f;
+#pragma unroll
+        for (int jj = 0; jj < J; ++jj) {
+            e[jj] = exp_fast(e[jj] - m);
+            z += e[jj];
+            lq[jj] = exp_fast(lq[jj] - mq);
+            zq += lq[jj];
+        }
+        const float iz = rcp_fast(z), izq = 1.0f / zq, kqv = sKQ;
+        float o = 0.f;
+#pragma unroll
+        for (int jj = 0; jj < J; ++jj) {
+            const float beta = 1.0f / (1.0f + exp_fast(-lb[jj]));
+            const float c = beta * (e[jj] * iz) * delta[jj];
+            sC[jj][tid] = c;
+            o = fmaf(lq[jj] * izq, fmaf(c, kqv, sY[jj][tid]), o);
+        }
+        store1(a.o, row * Dv + d0 + tid, o, a.out_bf16);
+    }
+    __syncthreads();
+
+    // 3. rank-one update of this thread's rows
+    if (a.state_out && has_rows) {
+        const float4 c4 = make_float4(sC[j][cl * 4], sC[j][cl * 4 + 1], sC[j][cl * 4 + 2],
+                                      sC[j][cl * 4 + 3]);
+        float *dst = a.state_out + sbase;
+#pragma unroll
+        for (int m = 0; m < kRows; ++m) {
+            const float ki = sk[ig + IG * m];
+            float4 s = st[m];
+            s.x = fmaf(c4.x, ki, s.x);
+            s.y = fmaf(c4.y, ki, s.y);
+            s.z = fmaf(c4.z, ki, s.z);
+            s.w = fmaf(c4.w, ki, s.w);
+            *reinterpret_cast<float4 *>(dst + (size_t)(ig + IG * m) * Dv) = s;
+        }
+    }
+}
+
+template <int DK, int J>
+hipError_t launch_dk_j(const LayerArgs &a, hipStream_t stream) {
+    const int DB = a.Dv < 32 ? a.Dv : 32;
+    int threads = J * (DK / kRows) * (DB / 4);
+    if (threads < DB) threads = DB;
+    dim3 grid(a.Dv / DB, a.H, a.B);
+    hipLaunchKernelGGL((decode_kernel<DK, J>), grid, dim3(threads), 0, stream, a, DB);
+    return hipGetLastError();
+}
+
+template <int DK>
+hipError_t launch_dk(const LayerArgs &a, hipStream_t stream) {
+    switch (a.J) {
+        case 1: return launch_dk_j<DK, 1>(a, stream);
+        case 2: return launch_dk_j<DK, 2>(a, stream);
+        case 3: return launch_dk_j<DK, 3>(a, stream);
+        case 4: return launch_dk_j<DK, 4>(a, stream);
+        case 8: return launch_dk_j<DK, 8>(a, stream);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+__global__ void state_fill_kernel(float *dst, const float *src, size_t n) {
+    const size_t stride = (size_t)gridDim.x * blockDim.x;
+    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
+        dst[i] = src ? src[i] : 0.0f;
+}
+
+}  // namespace
+
+hipError_t launch_decode(const LayerArgs &a, hipStream_t stream) {
+    switch (a.Dk) {
+        case 16: return launch_dk<16>(a, stream);
+        case 32: return launch_dk<32>(a, stream);
+        case 64: return launch_dk<64>(a, stream);
+        case 128: return launch_dk<128>(a, stream);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+hipError_t launch_state_fill(float *state, const float *src, size_t n, hipStream_t stream) {
+    if (n == 0 || state == src) return hipSuccess;
+    size_t blocks = (n + 255) / 256;
+    if (blocks > 4096) blocks = 4096;
+    hipLaunchKernelGGL(state_fill_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, state, src, n);
+    return hipGetLastError();
+}
+
+}  // namespace swila

@@ -1,0 +1,31 @@
+// Internal launch interface between the C-ABI layer and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace swila {
+
+// Pointers and sizes of one forward or decode call (decode uses T = 1).
+struct LayerArgs {
+    const void *q, *k, *v, *lb, *lk, *lq;  // inputs, fp32 or bf16 (in_bf16)
+    const float *state_in;                 // nullptr = zeros
+    float *state_out;                      // nullptr = not written
+    void *o;                               // fp32 or bf16 (out_bf16)
+    float *resp;                           // nullptr = not written
+    int B, H, T, Dk, Dv, J;
+    bool in_bf16, out_bf16;
+};
+
+// Token-by-token scan with fp32 state in registers.  Returns the HIP status of
+// the launch; hipErrorInvalidValue if the shape has no instantiation.
+hipError_t launch_scan_direct(const LayerArgs &a, hipStream_t stream);
+
+// One-token decode step streaming the state through registers.
+hipError_t launch_decode(const LayerArgs &a, hipStream_t stream);
+
+// state <- src (or zeros when src is nullptr); n floats.
+hipError_t launch_state_fill(float *state, const float *src, size_t n, hipStream_t stream);
+
+}  // namespace swila

@@ -1,0 +1,225 @@
+// Token-by-token SwiLA scan (Sec. 3.2: eq. recurrence, eq. responsibility,
+// eq. retrieval), fp32 state held in VGPRs for the whole sequence.
+//
+// Work split.  Every (b, h, d) output column is independent except that the
+// E-step normalises over the J components of the same d.  One column's state,
+// w_{jd} for all j (J x Dk floats), is spread over L consecutive lanes, each
+// lane holding an S = Dk / L slice of the key dimension for every j.  Per token:
+//   pred_j = w_j . k and y_j = w_j . q   (S FMAs per lane, DPP sum over L lanes)
+//   r      = softmax_j(lk_j - delta_j^2 / 2)   (in-lane over J; see below)
+//   w_j   += beta_j r_j delta_j k          (S FMAs per lane)
+//   o      = sum_j pi^q_j (y_j + c_j (k . q))
+// The key prior pi^k = softmax_j(lk) enters the E-step only through
+// pi^k_j e^{-delta_j^2/2}, so its normaliser cancels and r is a softmax of
+// lk_j - delta_j^2/2.  The retrieval uses the updated state:
+// w_new . q = w_old . q + c (k . q).
+//
+// Inputs are staged through LDS kTC tokens at a time: k and q as fp32 slices
+// padded so the L lanes of a column read distinct banks, and the per-(token,
+// column) scalars beta = sigmoid(logit), lk and pi^q = softmax_j already formed,
+// so the sequential loop does only the dependent arithmetic.
+#include "device_common.hpp"
+#include "launch.hpp"
+
+namespace swila {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kTC = 16;
+constexpr int kMaxCols = 128;  // largest supported Dv
+
+// Columns one block holds: bounded by the block size, the largest Dv, and a
+// 64 KiB budget for the per-(token, column) scalars staged in LDS.
+constexpr int max_cols(int L, int J) {
+    int n = kThreads / L < kMaxCols ? kThreads / L : kMaxCols;
+    while (n > 16 && kTC * (3 * J + 2) * n * 4 > 65536) n /= 2;
+    return n;
+}
+
+template <int DK, int J, int S>
+__global__ __launch_bounds__(kThreads) void scan_direct_kernel(LayerArgs a, int ncol) {
+    constexpr int L = DK / S;             // lanes per output column
+    constexpr int NCM = max_cols(L, J);
+    constexpr int SP = S + 4;             // padded slice stride in LDS
+
+    __shared__ __align__(16) float sK[kTC][L][SP];
+    __shared__ __align__(16) float sQ[kTC][L][SP];
+    __shared__ float sV[kTC][NCM];
+    __shared__ float sBeta[kTC][J][NCM];
+    __shared__ float sLk[kTC][J][NCM];
+    __shared__ float sPq[kTC][J][NCM];
+    __shared__ float sO[kTC][NCM];
+
+    const int tid = threadIdx.x;
+    const int nthr = ncol * L;
+    const int dl = tid / L, l = tid % L;
+    const int d0 = blockIdx.x * ncol;
+    const int h = blockIdx.y, b = blockIdx.z;
+    const int H = a.H, T = a.T, Dv = a.Dv;
+    const int d = d0 + dl;
+    const bool ibf = a.in_bf16, obf = a.out_bf16;
+
+    float w[J][S];
+    const size_t sbase = ((size_t)b * H + h) * J * DK * Dv;
+#pragma unroll
+    for (int j = 0; j < J; ++j)
+#pragma unroll
+        for (int s = 0; s < S; ++s)
+            w[j][s] = a.state_in ? a.state_in[sbase + ((size_t)j * DK + l * S + s) * Dv + d] : 0.0f;
+
+    for (int t0 = 0; t0 < T; t0 += kTC) {
+        const int nt = min(kTC, T - t0);
+        __syncthreads();
+        if (t0 > 0) {  // outputs of the previous (full) round
+            for (int g = tid; g < kTC * ncol; g += nthr) {
+                const int tt = g / ncol, c = g % ncol;
+                store1(a.o, ((size_t)(b * T + t0 - kTC + tt) * H + h) * Dv + d0 + c, sO[tt][c], obf);
+            }
+        }
+        for (int g = tid; g < nt * (DK / 4); g += nthr) {
+            const int tt = g / (DK / 4), i = (g % (DK / 4)) * 4;
+            const size_t off = ((size_t)(b * T + t0 + tt) * H + h) * DK + i;
+            *reinterpret_cast<float4 *>(&sK[tt][i / S][i % S]) = load4(a.k, off, ibf);
+            *reinterpret_cast<float4 *>(&sQ[tt][i / S][i % S]) = load4(a.q, off, ibf);
+        }
+        for (int g = tid; g < nt * ncol; g += nthr) {
+            const int tt = g / ncol, c = g % ncol;
+            const size_t row = (size_t)(b * T + t0 + tt) * H + h;
+            sV[tt][c] = load1(a.v, row * Dv + d0 + c, ibf);
+            float lq[J];
+            float m = -INFINITY;
+#pragma unroll
+            for (int j = 0; j < J; ++j) {
+                const size_t idx = (row * J + j) * Dv + d0 + c;
+                sBeta[tt][j][c] = 1.0f / (1.0f + exp_fast(-load1(a.lb, idx, ibf)));
+                sLk[tt][j][c] = load1(a.lk, idx, ibf);
+                lq[j] = load1(a.lq, idx, ibf);
+                m = fmaxf(m, lq[j]);
+            }
+            float z = 0.0f;
+#pragma unroll
+            for (int j = 0; j < J; ++j) {
+                lq[j] = exp_fast(lq[j] - m);
+                z += lq[j];
+            }
+            const float iz = 1.0f / z;
+#pragma unroll
+            for (int j = 0; j < J; ++j) sPq[tt][j][c] = lq[j] * iz;
+        }
+        __syncthreads();
+
+        for (int tt = 0; tt < nt; ++tt) {
+            float kv[S], qv[S];
+#pragma unroll
+            for (int s = 0; s < S; s += 4) {
+                const float4 x = *reinterpret_cast<const float4 *>(&sK[tt][l][s]);
+                const float4 y = *reinterpret_cast<const float4 *>(&sQ[tt][l][s]);
+                kv[s] = x.x; kv[s + 1] = x.y; kv[s + 2] = x.z; kv[s + 3] = x.w;
+                qv[s] = y.x; qv[s + 1] = y.y; qv[s + 2] = y.z; qv[s + 3] = y.w;
+            }
+            float p[J], y[J];
+            float kq = 0.0f;
+#pragma unroll
+            for (int j = 0; j < J; ++j) {
+                p[j] = 0.0f;
+                y[j] = 0.0f;
+#pragma unroll
+                for (int s = 0; s < S; ++s) {
+                    p[j] = fmaf(w[j][s], kv[s], p[j]);
+                    y[j] = fmaf(w[j][s], qv[s], y[j]);
+                }
+            }
+#pragma unroll
+            for (int s = 0; s < S; ++s) kq = fmaf(kv[s], qv[s], kq);
+#pragma unroll
+            for (int j = 0; j < J; ++j) {
+                p[j] = group_sum<L>(p[j]);
+                y[j] = group_sum<L>(y[j]);
+            }
+            kq = group_sum<L>(kq);
+
+            const float vd = sV[tt][dl];
+            float delta[J], e[J];
+            float m = -INFINITY;
+#pragma unroll
+            for (int j = 0; j < J; ++j) {
+                delta[j] = vd - p[j];
+                e[j] = sLk[tt][j][dl] - 0.5f * delta[j] * delta[j];
+                m = fmaxf(m, e[j]);
+            }
+            float z = 0.0f;
+#pragma unroll
+            for (int j = 0; j < J; ++j) {
+                e[j] = exp_fast(e[j] - m);
+                z += e[j];
+            }
+            const float iz = rcp_fast(z);
+            float o = 0.0f;
+#pragma unroll
+            for (int j = 0; j < J; ++j) {
+                const float r = e[j] * iz;
+                const float c = sBeta[tt][j][dl] * r * delta[j];
+#pragma unroll
+                for (int s = 0; s < S; ++s) w[j][s] = fmaf(c, kv[s], w[j][s]);
+                o = fmaf(sPq[tt][j][dl], fmaf(c, kq, y[j]), o);
+                if (a.resp && l == 0)
+                    a.resp[(((size_t)(b * T + t0 + tt) * H + h) * J + j) * Dv + d] = r;
+            }
+            if (l == 0) sO[tt][dl] = o;
+        }
+    }
+
+    __syncthreads();
+    if (T > 0) {
+        const int tl = ((T - 1) / kTC) * kTC;
+        const int nt = T - tl;
+        for (int g = tid; g < nt * ncol; g += nthr) {
+            const int tt = g / ncol, c = g % ncol;
+            store1(a.o, ((size_t)(b * T + tl + tt) * H + h) * Dv + d0 + c, sO[tt][c], obf);
+        }
+    }
+    if (a.state_out) {
+#pragma unroll
+        for (int j = 0; j < J; ++j)
+#pragma unroll
+            for (int s = 0; s < S; ++s)
+                a.state_out[sbase + ((size_t)j * DK + l * S + s) * Dv + d] = w[j][s];
+    }
+}
+
+template <int DK, int J>
+hipError_t launch_dk_j(const LayerArgs &a, hipStream_t stream) {
+    constexpr int S = (J <= 4) ? (DK < 16 ? DK : 16) : (DK < 8 ? DK : 8);
+    constexpr int L = DK / S;
+    const int ncol = a.Dv < max_cols(L, J) ? a.Dv : max_cols(L, J);
+    dim3 grid(a.Dv / ncol, a.H, a.B);
+    dim3 block(ncol * L);
+    hipLaunchKernelGGL((scan_direct_kernel<DK, J, S>), grid, block, 0, stream, a, ncol);
+    return hipGetLastError();
+}
+
+template <int DK>
+hipError_t launch_dk(const LayerArgs &a, hipStream_t stream) {
+    switch (a.J) {
+        case 1: return launch_dk_j<DK, 1>(a, stream);
+        case 2: return launch_dk_j<DK, 2>(a, stream);
+        case 3: return launch_dk_j<DK, 3>(a, stream);
+        case 4: return launch_dk_j<DK, 4>(a, stream);
+        case 8: return launch_dk_j<DK, 8>(a, stream);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace
+
+hipError_t launch_scan_direct(const LayerArgs &a, hipStream_t stream) {
+    switch (a.Dk) {
+        case 16: return launch_dk<16>(a, stream);
+        case 32: return launch_dk<32>(a, stream);
+        case 64: return launch_dk<64>(a, stream);
+        case 128: return launch_dk<128>(a, stream);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace swila

@@ -1,0 +1,199 @@
+// C ABI of libswila.so: argument checks, then dispatch to the kernels.
+// Every check runs before anything is enqueued, so a failing call leaves the
+// stream untouched.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "launch.hpp"
+#include "swila.h"
+
+namespace {
+
+thread_local char g_err[512];
+
+int fail(int code, const char *fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof g_err, fmt, ap);
+    va_end(ap);
+    return code;
+}
+
+void clear_error() { g_err[0] = 0; }
+
+bool dim_ok(int x) { return x == 16 || x == 32 || x == 64 || x == 128; }
+bool j_ok(int j) { return j == 1 || j == 2 || j == 3 || j == 4 || j == 8; }
+
+int check_shape(const swila_shape *s, bool decode) {
+    if (!s) return fail(SWILA_EINVAL, "shape is NULL");
+    if (s->B < 1 || s->H < 1 || s->T < 0 || s->Dk < 1 || s->Dv < 1 || s->J < 1)
+        return fail(SWILA_EINVAL, "invalid shape B=%d H=%d T=%d Dk=%d Dv=%d J=%d", s->B, s->H,
+                    s->T, s->Dk, s->Dv, s->J);
+    if (decode && s->T != 1) return fail(SWILA_EINVAL, "decode needs T == 1 (got %d)", s->T);
+    if (!dim_ok(s->Dk) || !dim_ok(s->Dv))
+        return fail(SWILA_EUNSUPPORTED, "Dk=%d Dv=%d: supported sizes are 16, 32, 64, 128", s->Dk,
+                    s->Dv);
+    if (!j_ok(s->J)) return fail(SWILA_EUNSUPPORTED, "J=%d: supported are 1, 2, 3, 4, 8", s->J);
+    if (s->B > 65535 || s->H > 65535)
+        return fail(SWILA_EUNSUPPORTED, "B=%d H=%d: at most 65535 each", s->B, s->H);
+    return SWILA_OK;
+}
+
+int check_opts(const swila_opts *o) {
+    if (!o) return fail(SWILA_EINVAL, "opts is NULL");
+    if (o->in_dtype != SWILA_F32 && o->in_dtype != SWILA_BF16)
+        return fail(SWILA_EINVAL, "in_dtype %d is not SWILA_F32 or SWILA_BF16", o->in_dtype);
+    if (o->out_dtype != SWILA_F32 && o->out_dtype != SWILA_BF16)
+        return fail(SWILA_EINVAL, "out_dtype %d is not SWILA_F32 or SWILA_BF16", o->out_dtype);
+    if (o->algo != SWILA_ALGO_AUTO && o->algo != SWILA_ALGO_RECURRENT)
+        return fail(SWILA_EUNSUPPORTED, "algo %d is not available", o->algo);
+    if (o->chunk < 0) return fail(SWILA_EINVAL, "chunk %d < 0", o->chunk);
+    return SWILA_OK;
+}
+
+struct Span {
+    const char *name;
+    const void *p;
+    size_t bytes;
+};
+
+// Pointer present (when required), 16-byte aligned, and disjoint from the
+// given inputs.
+int check_ptr(const Span &s, bool required) {
+    if (!s.p) return required ? fail(SWILA_EINVAL, "%s is NULL", s.name) : SWILA_OK;
+    if (reinterpret_cast<uintptr_t>(s.p) % 16 != 0)
+        return fail(SWILA_EINVAL, "%s is not 16-byte aligned", s.name);
+    return SWILA_OK;
+}
+
+bool overlap(const Span &a, const Span &b) {
+    if (!a.p || !b.p || a.bytes == 0 || b.bytes == 0) return false;
+    const char *a0 = static_cast<const char *>(a.p), *b0 = static_cast<const char *>(b.p);
+    return a0 < b0 + b.bytes && b0 < a0 + a.bytes;
+}
+
+int map_hip(hipError_t e, const char *what) {
+    if (e == hipSuccess) return SWILA_OK;
+    return fail(SWILA_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+// Shared checks of forward and decode; fills the launch arguments.
+int prepare(const swila_shape *shape, const swila_opts *opts, bool decode, const void *q,
+            const void *k, const void *v, const void *lb, const void *lk, const void *lq,
+            const float *state_in, float *state_out, void *o, float *resp,
+            swila::LayerArgs *a) {
+    int rc = check_shape(shape, decode);
+    if (rc) return rc;
+    rc = check_opts(opts);
+    if (rc) return rc;
+    const size_t B = shape->B, H = shape->H, T = shape->T, Dk = shape->Dk, Dv = shape->Dv,
+                 J = shape->J;
+    const size_t ie = opts->in_dtype == SWILA_BF16 ? 2 : 4;
+    const size_t oe = opts->out_dtype == SWILA_BF16 ? 2 : 4;
+    const bool need = T > 0;
+    const Span in[] = {
+        {"q", q, B * T * H * Dk * ie},          {"k", k, B * T * H * Dk * ie},
+        {"v", v, B * T * H * Dv * ie},          {"beta_logit", lb, B * T * H * J * Dv * ie},
+        {"prior_k_logit", lk, B * T * H * J * Dv * ie},
+        {"prior_q_logit", lq, B * T * H * J * Dv * ie},
+        {"state_in", state_in, B * H * J * Dk * Dv * 4},
+    };
+    const int n_in = sizeof in / sizeof in[0];
+    for (int i = 0; i < n_in; ++i) {
+        rc = check_ptr(in[i], need && i < 6);  // state_in may be NULL (zeros)
+        if (rc) return rc;
+    }
+    const Span outs[] = {
+        {"o", o, B * T * H * Dv * oe},
+        {"state_out", state_out, B * H * J * Dk * Dv * 4},
+        {"resp_out", resp, B * T * H * J * Dv * 4},
+    };
+    for (int x = 0; x < 3; ++x) {
+        rc = check_ptr(outs[x], need && x == 0);  // o is required when T > 0
+        if (rc) return rc;
+        for (int i = 0; i < n_in; ++i) {
+            // the state may be updated in place: state_out == state_in exactly
+            if (x == 1 && i == 6 && state_out == state_in) continue;
+            if (overlap(outs[x], in[i]))
+                return fail(SWILA_EINVAL, "%s overlaps %s", outs[x].name, in[i].name);
+        }
+    }
+    if (overlap(outs[0], outs[1]) || overlap(outs[0], outs[2]) || overlap(outs[1], outs[2]))
+        return fail(SWILA_EINVAL, "output tensors overlap");
+    *a = swila::LayerArgs{q, k, v, lb, lk, lq, state_in, state_out, o, resp,
+                          shape->B, shape->H, shape->T, shape->Dk, shape->Dv, shape->J,
+                          opts->in_dtype == SWILA_BF16, opts->out_dtype == SWILA_BF16};
+    return SWILA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int swila_version(void) { return 1; }
+
+const char *swila_last_error(void) { return g_err; }
+
+size_t swila_state_bytes(const swila_shape *s) {
+    if (!s || s->B < 1 || s->H < 1 || s->Dk < 1 || s->Dv < 1 || s->J < 1) return 0;
+    return (size_t)s->B * s->H * s->J * s->Dk * s->Dv * sizeof(float);
+}
+
+int swila_state_init(const swila_shape *shape, float *state, const float *src, void *stream) {
+    clear_error();
+    if (!shape) return fail(SWILA_EINVAL, "shape is NULL");
+    const size_t bytes = swila_state_bytes(shape);
+    if (bytes == 0) return fail(SWILA_EINVAL, "invalid shape");
+    if (!state) return fail(SWILA_EINVAL, "state is NULL");
+    if (reinterpret_cast<uintptr_t>(state) % 16 || reinterpret_cast<uintptr_t>(src) % 16)
+        return fail(SWILA_EINVAL, "state or src is not 16-byte aligned");
+    const Span a{"state", state, bytes}, b{"src", src, bytes};
+    if (src && src != state && overlap(a, b)) return fail(SWILA_EINVAL, "state overlaps src");
+    return map_hip(swila::launch_state_fill(state, src, bytes / sizeof(float),
+                                            static_cast<hipStream_t>(stream)),
+                   "state_init launch");
+}
+
+size_t swila_forward_workspace_bytes(const swila_shape *shape, const swila_opts *opts) {
+    (void)shape;
+    (void)opts;
+    return 0;
+}
+
+int swila_forward(const swila_shape *shape, const swila_opts *opts, const void *q, const void *k,
+                  const void *v, const void *beta_logit, const void *prior_k_logit,
+                  const void *prior_q_logit, const float *state_in, float *state_out, void *o,
+                  float *resp_out, void *workspace, size_t ws_bytes, int32_t *iters_out,
+                  void *stream) {
+    clear_error();
+    (void)workspace;
+    (void)ws_bytes;
+    (void)iters_out;
+    swila::LayerArgs a;
+    int rc = prepare(shape, opts, false, q, k, v, beta_logit, prior_k_logit, prior_q_logit,
+                     state_in, state_out, o, resp_out, &a);
+    if (rc) return rc;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    if (shape->T == 0) {
+        if (!state_out) return SWILA_OK;
+        return map_hip(swila::launch_state_fill(state_out, state_in,
+                                                swila_state_bytes(shape) / sizeof(float), st),
+                       "state copy");
+    }
+    return map_hip(swila::launch_scan_direct(a, st), "scan launch");
+}
+
+int swila_decode_step(const swila_shape *shape, const swila_opts *opts, const void *q,
+                      const void *k, const void *v, const void *beta_logit,
+                      const void *prior_k_logit, const void *prior_q_logit,
+                      const float *state_in, float *state_out, void *o, void *stream) {
+    clear_error();
+    swila::LayerArgs a;
+    int rc = prepare(shape, opts, true, q, k, v, beta_logit, prior_k_logit, prior_q_logit,
+                     state_in, state_out, o, nullptr, &a);
+    if (rc) return rc;
+    return map_hip(swila::launch_decode(a, static_cast<hipStream_t>(stream)), "decode launch");
+}
+
+}  // extern "C"

@@ -1,0 +1,131 @@
+"""The C-ABI library loads, exports every symbol include/swila.h declares, and
+rejects bad arguments before anything is enqueued.  CPU only: every call made
+here is invalid by construction, so no kernel is ever launched."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2609_39034_amd as sw
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "swila.h")
+
+FAKE = ctypes.c_void_p(1 << 20)        # aligned, never dereferenced
+FAKE2 = ctypes.c_void_p(1 << 30)
+
+
+def declared_functions():
+    text = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    return sorted(set(re.findall(r"\b(swila_[a-z_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return sw.load_library()
+
+
+def test_exports_every_declared_symbol(lib):
+    names = declared_functions()
+    assert "swila_forward" in names and "swila_decode_step" in names and "swila_state_init" in names
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_version_and_sizes(lib):
+    assert lib.swila_version() == 1
+    assert sw.state_bytes(2, 3, 64, 32, 4) == 2 * 3 * 4 * 64 * 32 * 4
+    assert lib.swila_state_bytes(None) == 0
+    assert sw.forward_workspace_bytes(4, 8, 2048, 64, 64, 4) == 0
+
+
+def _fwd(lib, shape, opts, ptrs=None, o=FAKE2, state_in=None, state_out=None, resp=None):
+    ptrs = ptrs if ptrs is not None else [ctypes.c_void_p((1 << 20) + (i << 26)) for i in range(6)]
+    rc = lib.swila_forward(None if shape is None else ctypes.byref(shape),
+                           None if opts is None else ctypes.byref(opts), *ptrs, state_in,
+                           state_out, o, resp, None, 0, None, None)
+    return rc, lib.swila_last_error().decode()
+
+
+OPTS = sw.Opts(sw.BF16, sw.BF16, 0, 0, 0, 0.0, 0)
+
+
+@pytest.mark.parametrize("shape,opts,code,text", [
+    (None, OPTS, sw.EINVAL, "shape is NULL"),
+    (sw.Shape(1, 1, 4, 64, 64, 4), None, sw.EINVAL, "opts is NULL"),
+    (sw.Shape(0, 1, 4, 64, 64, 4), OPTS, sw.EINVAL, "invalid shape"),
+    (sw.Shape(1, 1, -1, 64, 64, 4), OPTS, sw.EINVAL, "invalid shape"),
+    (sw.Shape(1, 1, 4, 48, 64, 4), OPTS, sw.EUNSUPPORTED, "Dk=48"),
+    (sw.Shape(1, 1, 4, 64, 256, 4), OPTS, sw.EUNSUPPORTED, "Dv=256"),
+    (sw.Shape(1, 1, 4, 64, 64, 5), OPTS, sw.EUNSUPPORTED, "J=5"),
+    (sw.Shape(70000, 1, 4, 64, 64, 4), OPTS, sw.EUNSUPPORTED, "at most 65535"),
+    (sw.Shape(1, 1, 4, 64, 64, 4), sw.Opts(7, 1, 0, 0, 0, 0.0, 0), sw.EINVAL, "in_dtype"),
+    (sw.Shape(1, 1, 4, 64, 64, 4), sw.Opts(1, 9, 0, 0, 0, 0.0, 0), sw.EINVAL, "out_dtype"),
+    (sw.Shape(1, 1, 4, 64, 64, 4), sw.Opts(1, 1, 99, 0, 0, 0.0, 0), sw.EUNSUPPORTED, "algo"),
+    (sw.Shape(1, 1, 4, 64, 64, 4), sw.Opts(1, 1, 0, -2, 0, 0.0, 0), sw.EINVAL, "chunk"),
+])
+def test_forward_rejects_bad_shapes_and_options(lib, shape, opts, code, text):
+    rc, msg = _fwd(lib, shape, opts)
+    assert rc == code and text in msg
+
+
+def test_forward_rejects_bad_pointers(lib):
+    shape = sw.Shape(1, 2, 8, 64, 64, 4)
+    good = [ctypes.c_void_p((1 << 20) + (i << 26)) for i in range(6)]
+    for i, name in enumerate(("q", "k", "v", "beta_logit", "prior_k_logit", "prior_q_logit")):
+        ptrs = list(good)
+        ptrs[i] = None
+        rc, msg = _fwd(lib, shape, OPTS, ptrs)
+        assert rc == sw.EINVAL and msg == "%s is NULL" % name
+        ptrs[i] = ctypes.c_void_p(good[i].value + 2)
+        rc, msg = _fwd(lib, shape, OPTS, ptrs)
+        assert rc == sw.EINVAL and "%s is not 16-byte aligned" % name in msg
+    rc, msg = _fwd(lib, shape, OPTS, good, o=None)
+    assert rc == sw.EINVAL and msg == "o is NULL"
+    # o overlapping an input
+    rc, msg = _fwd(lib, shape, OPTS, good, o=ctypes.c_void_p(good[2].value + 64))
+    assert rc == sw.EINVAL and "o overlaps v" in msg
+    # state_out overlapping (but not equal to) state_in
+    st = ctypes.c_void_p(1 << 34)
+    rc, msg = _fwd(lib, shape, OPTS, good, state_in=st, state_out=ctypes.c_void_p(st.value + 256))
+    assert rc == sw.EINVAL and "state_out overlaps state_in" in msg
+    # resp_out overlapping o
+    rc, msg = _fwd(lib, shape, OPTS, good, resp=ctypes.c_void_p(FAKE2.value + 16))
+    assert rc == sw.EINVAL and "overlap" in msg
+
+
+def test_decode_requires_one_token(lib):
+    ptrs = [ctypes.c_void_p((1 << 20) + (i << 26)) for i in range(6)]
+    rc = lib.swila_decode_step(ctypes.byref(sw.Shape(4, 2, 2, 64, 64, 4)), ctypes.byref(OPTS),
+                               *ptrs, None, None, FAKE2, None)
+    assert rc == sw.EINVAL and "T == 1" in lib.swila_last_error().decode()
+
+
+def test_state_init_rejects(lib):
+    assert lib.swila_state_init(None, FAKE, None, None) == sw.EINVAL
+    assert lib.swila_state_init(ctypes.byref(sw.Shape(1, 1, 0, 16, 16, 2)), None, None,
+                                None) == sw.EINVAL
+    assert lib.swila_state_init(ctypes.byref(sw.Shape(1, 1, 0, 16, 16, 2)),
+                                ctypes.c_void_p(FAKE.value + 4), None, None) == sw.EINVAL
+    rc = lib.swila_state_init(ctypes.byref(sw.Shape(1, 1, 0, 16, 16, 2)), FAKE,
+                              ctypes.c_void_p(FAKE.value + 64), None)
+    assert rc == sw.EINVAL and "overlaps" in lib.swila_last_error().decode()
+
+
+def test_error_text_is_thread_local_and_cleared(lib):
+    _fwd(lib, None, OPTS)
+    assert lib.swila_last_error() == b"shape is NULL"
+    import threading
+    seen = []
+    t = threading.Thread(target=lambda: seen.append(lib.swila_last_error()))
+    t.start()
+    t.join()
+    assert seen == [b""]
+
+
+def test_python_binding_checks_before_calling():
+    torch = pytest.importorskip("torch")
+    x = torch.zeros(1, 4, 1, 16)
+    with pytest.raises(ValueError, match="device tensor"):
+        sw.forward(x, x, x, x, x, x)

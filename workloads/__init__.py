@@ -41,20 +41,39 @@ CONFIGS = {
 NAMES = ("q", "k", "v", "lb", "lk", "lq")
 
 
-def round_bf16(x):
-    """Round float32 values to the nearest bfloat16 (ties to even); the result
-    is returned as float32.  Inputs must be finite."""
+def round_bf16_reference(x):
+    """Round float32 values to the nearest bfloat16 (ties to even) by bit
+    arithmetic; the result is returned as float32.  Inputs must be finite."""
     b = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
     r = (b + np.uint32(0x7FFF) + ((b >> np.uint32(16)) & np.uint32(1))) & np.uint32(0xFFFF0000)
     return r.view(np.float32)
 
 
+def round_bf16(x):
+    """Round float32 values to the nearest bfloat16 (ties to even), returned as
+    float32: torch's multi-threaded conversion, which the tests check against
+    ``round_bf16_reference``."""
+    import torch
+    t = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32))
+    return t.to(torch.bfloat16).to(torch.float32).numpy()
+
+
 def _finish(x, dtype):
+    if not isinstance(x, np.ndarray):          # a CPU torch tensor
+        import torch
+        x = x.contiguous()
+        if dtype == "bf16":
+            x = x.to(torch.bfloat16).to(torch.float32)
+        return x.numpy()
     x = np.ascontiguousarray(x, dtype=np.float32)
     return round_bf16(x) if dtype == "bf16" else x
 
 
 def _l2norm_last(x):
+    if not isinstance(x, np.ndarray):          # a CPU torch tensor
+        import torch
+        n = x.to(torch.float64).pow(2).sum(dim=-1, keepdim=True).sqrt().clamp_min(1e-12)
+        return (x / n).to(torch.float32)
     n = np.sqrt((x.astype(np.float64) ** 2).sum(axis=-1, keepdims=True))
     return (x / np.maximum(n, 1e-12)).astype(np.float32)
 
@@ -85,22 +104,25 @@ def iid_inputs(B, H, T, Dk, Dv, J, *, dtype="bf16", seed=0, state_std=0.0,
 def _project_tokens(rng, ids, vocab, width, H, Dk, Dv, J, dtype, chunk_tokens=4096):
     """q, k, v and the three logit tensors as linear projections of random token
     embeddings E ~ N(0,1) [vocab, width] with weights N(0, 1/width), so every
-    projected value is close to N(0,1).  ids: [B, T] integer token ids."""
+    projected value is close to N(0,1).  ids: [B, T] integer token ids.
+    Returns CPU torch float32 tensors."""
+    import torch
     B, T = ids.shape
-    E = rng.standard_normal((vocab, width), dtype=np.float32)
+    E = torch.from_numpy(rng.standard_normal((vocab, width), dtype=np.float32))
     widths = [H * Dk, H * Dk, H * Dv, H * J * Dv, H * J * Dv, H * J * Dv]
     scale = np.float32(1.0 / np.sqrt(width))
-    thetas = [rng.standard_normal((width, w), dtype=np.float32) * scale for w in widths]
+    thetas = [torch.from_numpy(rng.standard_normal((width, w), dtype=np.float32) * scale)
+              for w in widths]
     shapes = [(B, T, H, Dk), (B, T, H, Dk), (B, T, H, Dv),
               (B, T, H, J, Dv), (B, T, H, J, Dv), (B, T, H, J, Dv)]
-    outs = [np.empty(s, dtype=np.float32) for s in shapes]
-    flat_ids = ids.reshape(-1)
-    for a in range(0, flat_ids.size, chunk_tokens):
-        sl = slice(a, min(a + chunk_tokens, flat_ids.size))
+    outs = [torch.empty((B * T, w), dtype=torch.float32) for w in widths]
+    flat_ids = torch.from_numpy(ids.reshape(-1))
+    for a in range(0, flat_ids.numel(), chunk_tokens):
+        sl = slice(a, min(a + chunk_tokens, flat_ids.numel()))
         X = E[flat_ids[sl]]
         for o, th in zip(outs, thetas):
-            o.reshape(B * T, -1)[sl] = X @ th
-    return outs
+            torch.matmul(X, th, out=o[sl])
+    return [o.reshape(s) for o, s in zip(outs, shapes)]
 
 
 def lm_inputs(B=8, H=16, T=4096, Dk=128, Dv=128, J=4, *, dtype="bf16", seed=1003,
@@ -135,10 +157,12 @@ def recall_inputs(B=2, H=8, T=16384, Dk=128, Dv=128, J=8, *, dtype="bf16", seed=
         for p in range(pairs):
             ids[b, pos[p]] = pair_ids[p]
             occ[b, pos[p, 1:]] = True
+    import torch
     q, k, v, lb, lk, lq = _project_tokens(rng, ids, vocab, width, H, Dk, Dv, J, dtype)
     k = _l2norm_last(k)
-    noise = rng.standard_normal((B, T, H, Dk), dtype=np.float32) * np.float32(query_noise)
-    q = np.where(occ[:, :, None, None], k + noise, q).astype(np.float32)
+    noise = torch.from_numpy(rng.standard_normal((B, T, H, Dk), dtype=np.float32)
+                             * np.float32(query_noise))
+    q = torch.where(torch.from_numpy(occ)[:, :, None, None], k + noise, q)
     out = {n: _finish(x, dtype) for n, x in zip(NAMES, (q, k, v, lb, lk, lq))}
     out["state"] = None
     return out
