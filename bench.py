@@ -29,6 +29,27 @@ PEAK_HBM = 8.0e12          # B/s, MI355X HBM3E
 PEAK_VALU_F32 = 157.3e12   # FLOP/s, MI355X fp32 vector (packed); unpacked FMA is half
 PEAK_MFMA_BF16 = 2.5e15    # FLOP/s, MI355X dense bf16 matrix
 
+# HBM bytes per launch from rocprofv3 FETCH_SIZE/WRITE_SIZE passes, scaled by the
+# same counters on a plain 1 GiB copy (FETCH x2.0, WRITE x1.0); valid only for the
+# kernel source they were measured on (summary in profiles/).
+MEASURED_TRAFFIC = {
+    ("decode.hip", "769b72fdca36c7f4df23d3fb1d410dc16c3c323568a37067ebabab4fb4b755be"): 2184302284,
+    ("scan_direct.hip", "b38c28c5de8d782d7e8789d36b1d92720d8a6715bdb2781db527a2d9cdf2e1ba"):
+        136540979,
+}
+
+
+def measured_traffic(source):
+    """Counter-measured HBM bytes per launch of the kernel in ``source``, or None
+    when that source has changed since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "paper_2609_39034_amd", "csrc", source)
+    try:
+        digest = hashlib.sha256(open(path, "rb").read()).hexdigest()
+    except OSError:
+        return None
+    return MEASURED_TRAFFIC.get((source, digest))
+
 
 def forward_alg_bytes(B, H, T, Dk, Dv, J, in_bytes=2, out_bytes=2, state_in=False,
                       state_out=True):
@@ -106,7 +127,8 @@ def bench_decode(sw, torch, workloads, steps_total, warmup):
                     "fp32 state N(0,0.1^2) updated in place" % (B, H, Dk, J, steps_total),
         "steps_per_s": 1.0 / wall, "tokens_per_s": B / wall, "ms_per_step": wall * 1e3,
         "roofline": {"bound": "hbm", "achieved": nbytes / kern / 1e9, "peak": PEAK_HBM / 1e9,
-                     "unit": "GB/s", "frac": nbytes / kern / PEAK_HBM, "traffic": None,
+                     "unit": "GB/s", "frac": nbytes / kern / PEAK_HBM,
+                     "traffic": measured_traffic("decode.hip"), "kernel": "decode_kernel",
                      "kernel_ms": kern * 1e3, "alg_bytes_per_launch": nbytes},
     }
 
@@ -134,6 +156,8 @@ def main():
     ap.add_argument("--decode-steps", type=int, default=512)
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only copy 1 GiB device-to-device (scales HBM counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the SwiLA path has no cross-GPU step; "
@@ -144,6 +168,14 @@ def main():
     import paper_2609_39034_amd as sw
     import workloads
 
+    if args.copy_calibration:
+        x = torch.ones(1 << 28, device="cuda")
+        y = torch.empty_like(x)
+        torch.cuda.synchronize()
+        y.copy_(x)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_read": x.numel() * 4, "copy_bytes_written": y.numel() * 4}))
+        return
     sw.load_library()
     cfg = workloads.CONFIGS[args.config]
     B, H, T, Dk, Dv, J = (cfg[x] for x in ("B", "H", "T", "Dk", "Dv", "J"))
@@ -168,7 +200,8 @@ def main():
                                % (cfg["name"], B, H, T, Dk, J, cfg["dtype"]),
                    "B": B, "H": H, "T": T, "Dk": Dk, "Dv": Dv, "J": J, "algo": "recurrent"},
         "roofline": {"bound": "alu", "achieved": nflop / kern / 1e12, "peak": PEAK_VALU_F32 / 1e12,
-                     "unit": "TFLOP/s", "frac": nflop / kern / PEAK_VALU_F32, "traffic": None,
+                     "unit": "TFLOP/s", "frac": nflop / kern / PEAK_VALU_F32,
+                     "traffic": measured_traffic("scan_direct.hip"),
                      "kernel": "scan_direct_kernel", "kernel_ms": kern * 1e3,
                      "alg_flop_per_launch": nflop},
         "roofline_hbm": {"achieved": nbytes / kern / 1e9, "peak": PEAK_HBM / 1e9, "unit": "GB/s",

@@ -170,7 +170,7 @@ def test_decode_steps_match_oracle(Dk, Dv, J, dtype):
 def test_decode_matches_forward_one_token():
     inp = workloads.iid_inputs(4, 3, 1, 128, 128, 4, dtype="f32", seed=50, state_std=0.2)
     od, sd = _decode_steps(inp, "f32", 1)
-    of, sf, _ = gpu_forward(inp, "f32")
+    of, sf = gpu_forward(inp, "f32")[:2]
     assert np.max(np.abs(od - of)) <= 1e-5 * max(1.0, np.abs(of).max())
     assert np.max(np.abs(sd - sf)) <= 1e-5 * max(1.0, np.abs(sf).max())
 
