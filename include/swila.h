@@ -57,8 +57,11 @@ typedef struct swila_shape {
 enum swila_dtype { SWILA_F32 = 0, SWILA_BF16 = 1 };
 
 enum swila_algo {
-    SWILA_ALGO_AUTO = 0,       /* library picks */
-    SWILA_ALGO_RECURRENT = 1   /* token-by-token scan */
+    SWILA_ALGO_AUTO = 0,        /* CHUNK_EXACT for bf16 inputs, RECURRENT for fp32 */
+    SWILA_ALGO_RECURRENT = 1,   /* token-by-token scan on the vector ALUs */
+    SWILA_ALGO_CHUNK_EXACT = 2  /* the same recurrence evaluated 16 tokens at a time with
+                                   the Dk-long products on the matrix cores (bf16 inputs
+                                   only; fp32 operands split into bf16 high + residual) */
 };
 
 typedef struct swila_opts {

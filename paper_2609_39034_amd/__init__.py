@@ -20,14 +20,14 @@ import os
 
 __all__ = ["forward", "decode_step", "state_init", "state_bytes", "forward_workspace_bytes",
            "version", "library_path", "SwilaError", "F32", "BF16", "ALGO_AUTO",
-           "ALGO_RECURRENT"]
+           "ALGO_RECURRENT", "ALGO_CHUNK_EXACT"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB_PATH = os.path.join(_HERE, "libswila.so")
 
 F32, BF16 = 0, 1
-ALGO_AUTO, ALGO_RECURRENT = 0, 1
-_ALGOS = {"auto": ALGO_AUTO, "recurrent": ALGO_RECURRENT}
+ALGO_AUTO, ALGO_RECURRENT, ALGO_CHUNK_EXACT = 0, 1, 2
+_ALGOS = {"auto": ALGO_AUTO, "recurrent": ALGO_RECURRENT, "chunk": ALGO_CHUNK_EXACT}
 
 OK, EINVAL, EUNSUPPORTED, EHIP = 0, -1, -2, -3
 

@@ -15,7 +15,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libswila.so")
-SOURCES = ["swila_api.hip", "scan_direct.hip", "decode.hip"]
+SOURCES = ["swila_api.hip", "scan_direct.hip", "scan_chunk.hip", "decode.hip"]
 ARCH = "gfx950"
 
 # Packed fp32 VALU instructions are turned off for every kernel: the compiler

@@ -50,6 +50,15 @@ __device__ __forceinline__ void store1(void *base, size_t idx, float x, bool bf1
         static_cast<float *>(base)[idx] = x;
 }
 
+// Block barrier that orders LDS traffic only: waits for this wave's LDS
+// operations, then for every wave of the block.  Global loads still in flight
+// (prefetches) are not waited for; the compiler inserts those waits where the
+// loaded registers are used.  The "memory" clobber keeps the compiler from
+// moving memory accesses across it.
+__device__ __forceinline__ void block_sync_lds() {
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
 // DPP lane moves within a row of 16 lanes.
 template <int CTRL>
 __device__ __forceinline__ float dpp_mov(float x) {
@@ -67,6 +76,17 @@ __device__ __forceinline__ float group_sum(float x) {
     if constexpr (L >= 16) x += dpp_mov<0x140>(x); // row_mirror: other half of 16
     if constexpr (L >= 32) x += __shfl_xor(x, 16);
     if constexpr (L >= 64) x += __shfl_xor(x, 32);
+    return x;
+}
+
+// Maximum over each aligned group of L consecutive lanes (L a power of two,
+// at most 16); every lane of the group receives it.
+template <int L>
+__device__ __forceinline__ float group_max(float x) {
+    if constexpr (L >= 2) x = fmaxf(x, dpp_mov<0xb1>(x));
+    if constexpr (L >= 4) x = fmaxf(x, dpp_mov<0x4e>(x));
+    if constexpr (L >= 8) x = fmaxf(x, dpp_mov<0x141>(x));
+    if constexpr (L >= 16) x = fmaxf(x, dpp_mov<0x140>(x));
     return x;
 }
 

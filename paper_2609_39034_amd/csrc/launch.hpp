@@ -22,6 +22,9 @@ struct LayerArgs {
 // the launch; hipErrorInvalidValue if the shape has no instantiation.
 hipError_t launch_scan_direct(const LayerArgs &a, hipStream_t stream);
 
+// Exact chunked scan on the matrix cores; bf16 inputs only.
+hipError_t launch_scan_chunk(const LayerArgs &a, hipStream_t stream);
+
 // One-token decode step streaming the state through registers.
 hipError_t launch_decode(const LayerArgs &a, hipStream_t stream);
 

@@ -46,8 +46,11 @@ int check_opts(const swila_opts *o) {
         return fail(SWILA_EINVAL, "in_dtype %d is not SWILA_F32 or SWILA_BF16", o->in_dtype);
     if (o->out_dtype != SWILA_F32 && o->out_dtype != SWILA_BF16)
         return fail(SWILA_EINVAL, "out_dtype %d is not SWILA_F32 or SWILA_BF16", o->out_dtype);
-    if (o->algo != SWILA_ALGO_AUTO && o->algo != SWILA_ALGO_RECURRENT)
+    if (o->algo != SWILA_ALGO_AUTO && o->algo != SWILA_ALGO_RECURRENT &&
+        o->algo != SWILA_ALGO_CHUNK_EXACT)
         return fail(SWILA_EUNSUPPORTED, "algo %d is not available", o->algo);
+    if (o->algo == SWILA_ALGO_CHUNK_EXACT && o->in_dtype != SWILA_BF16)
+        return fail(SWILA_EUNSUPPORTED, "SWILA_ALGO_CHUNK_EXACT needs bf16 inputs");
     if (o->chunk < 0) return fail(SWILA_EINVAL, "chunk %d < 0", o->chunk);
     return SWILA_OK;
 }
@@ -181,6 +184,9 @@ int swila_forward(const swila_shape *shape, const swila_opts *opts, const void *
                                                 swila_state_bytes(shape) / sizeof(float), st),
                        "state copy");
     }
+    const bool chunk = opts->algo == SWILA_ALGO_CHUNK_EXACT ||
+                       (opts->algo == SWILA_ALGO_AUTO && opts->in_dtype == SWILA_BF16);
+    if (chunk) return map_hip(swila::launch_scan_chunk(a, st), "chunk scan launch");
     return map_hip(swila::launch_scan_direct(a, st), "scan launch");
 }
 

@@ -24,13 +24,13 @@ def to_device(inp, dtype, device="cuda"):
     return workloads.to_torch(inp, device, torch_dtype(dtype))
 
 
-def gpu_forward(inp, dtype, *, out_dtype=None, resp=False, state_out=True):
+def gpu_forward(inp, dtype, *, out_dtype=None, resp=False, state_out=True, algo="auto"):
     import paper_2609_39034_amd as sw
     import torch
     dev = to_device(inp, dtype)
     od = None if out_dtype is None else torch_dtype(out_dtype)
     res = sw.forward(*(dev[n] for n in NAMES), dev["state"], out_dtype=od, resp=resp,
-                     state_out=state_out)
+                     state_out=state_out, algo=algo)
     torch.cuda.synchronize()
     return [None if x is None else x.float().cpu().numpy().astype(np.float64) for x in res]
 

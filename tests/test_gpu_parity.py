@@ -26,8 +26,8 @@ def _oracle(inp, resp=False, b=None, h=None):
     return oracle.forward(*args, st, want_resp=resp)
 
 
-def _check(inp, dtype, resp=True, out_dtype=None):
-    o, s, r = gpu_forward(inp, dtype, resp=True, out_dtype=out_dtype)
+def _check(inp, dtype, resp=True, out_dtype=None, algo="auto"):
+    o, s, r = gpu_forward(inp, dtype, resp=True, out_dtype=out_dtype, algo=algo)
     ref = _oracle(inp, resp=True)
     tol = tol_for(dtype if out_dtype is None else "bf16" if "bf16" in (dtype, out_dtype) else "f32")
     eo, es, er = (head_rel_err(o, ref["o"], "o"), head_rel_err(s, ref["state"], "state"),
@@ -57,6 +57,24 @@ def test_small_shapes(B, H, T, Dk, Dv, J, dtype, std):
     _check(inp, dtype)
 
 
+# every (Dk, J, column block) instantiation of the matrix-core chunk scan, with
+# ragged last chunks, and the token-by-token scan on the same bf16 inputs
+CHUNK = [
+    # B, H, T, Dk, Dv, J, state_std
+    (1, 2, 37, 16, 16, 1, 0.2), (2, 1, 50, 32, 32, 1, 0.0), (1, 1, 70, 64, 128, 1, 0.3),
+    (2, 2, 33, 128, 16, 2, 0.1), (1, 2, 64, 16, 64, 2, 0.0), (1, 1, 45, 64, 32, 3, 0.2),
+    (2, 2, 40, 128, 128, 4, 0.1), (1, 3, 17, 32, 64, 4, 0.0), (2, 1, 31, 64, 16, 8, 0.2),
+    (1, 2, 80, 128, 128, 8, 0.1), (1, 1, 1, 128, 64, 4, 0.3), (1, 1, 16, 16, 128, 3, 0.0),
+]
+
+
+@pytest.mark.parametrize("algo", ["chunk", "recurrent"])
+@pytest.mark.parametrize("B,H,T,Dk,Dv,J,std", CHUNK)
+def test_bf16_algorithms(B, H, T, Dk, Dv, J, std, algo):
+    inp = workloads.iid_inputs(B, H, T, Dk, Dv, J, dtype="bf16", seed=300 + T + J, state_std=std)
+    _check(inp, "bf16", algo=algo)
+
+
 def test_bf16_inputs_fp32_output():
     inp = workloads.iid_inputs(2, 2, 40, 64, 64, 4, dtype="bf16", seed=7, state_std=0.1)
     _check(inp, "bf16", out_dtype="f32")
@@ -75,8 +93,9 @@ def test_config1_tiny():
     _check(workloads.config_inputs(1), "f32")
 
 
-def test_config2_small_full():
-    _check(workloads.config_inputs(2), "bf16")
+@pytest.mark.parametrize("algo", ["chunk", "recurrent"])
+def test_config2_algorithms(algo):
+    _check(workloads.config_inputs(2), "bf16", algo=algo)
 
 
 @pytest.mark.parametrize("cfg,heads", [(3, [(0, 0), (5, 9), (7, 15)]), (5, [(0, 0), (1, 7)])])
@@ -109,29 +128,49 @@ def test_zero_length_copies_state():
     assert torch.count_nonzero(s) == 0
 
 
-def test_state_passing_and_in_place():
+@pytest.mark.parametrize("algo,split", [("recurrent", 19), ("chunk", 32)])
+def test_state_passing_and_in_place(algo, split):
     """Running a sequence in two pieces, passing the state (in place), gives
-    bit-identical outputs and state to one run."""
+    bit-identical outputs and state to one run (for the chunk scan, when the split
+    falls on a chunk boundary, so the rounding order is the same)."""
     import torch
     import paper_2609_39034_amd as sw
     inp = workloads.iid_inputs(2, 2, 45, 64, 64, 4, dtype="bf16", seed=21, state_std=0.1)
     dev = to_device(inp, "bf16")
-    o_all, s_all = sw.forward(*(dev[n] for n in NAMES), dev["state"])
+    o_all, s_all = sw.forward(*(dev[n] for n in NAMES), dev["state"], algo=algo)
     st = dev["state"].clone()
-    o1, _ = sw.forward(*(dev[n][:, :19].contiguous() for n in NAMES), st, state_out=st)
-    o2, _ = sw.forward(*(dev[n][:, 19:].contiguous() for n in NAMES), st, state_out=st)
+    o1, _ = sw.forward(*(dev[n][:, :split].contiguous() for n in NAMES), st, state_out=st,
+                       algo=algo)
+    o2, _ = sw.forward(*(dev[n][:, split:].contiguous() for n in NAMES), st, state_out=st,
+                       algo=algo)
     torch.cuda.synchronize()
     assert torch.equal(torch.cat([o1, o2], dim=1), o_all)
     assert torch.equal(st, s_all)
 
 
-def test_deterministic():
+def test_chunk_state_passing_any_split():
+    """Splitting off a chunk boundary changes only the rounding order."""
+    inp = workloads.iid_inputs(2, 2, 45, 64, 64, 4, dtype="bf16", seed=23, state_std=0.1)
+    whole = gpu_forward(inp, "bf16", algo="chunk")
+    first = {n: (None if inp[n] is None else inp[n][:, :19]) for n in NAMES}
+    first["state"] = inp["state"]
+    o1, s1 = gpu_forward(first, "bf16", algo="chunk")
+    second = {n: inp[n][:, 19:] for n in NAMES}
+    second["state"] = s1.astype(np.float32)
+    o2, s2 = gpu_forward(second, "bf16", algo="chunk")
+    o = np.concatenate([o1, o2], axis=1)
+    assert head_rel_err(o, whole[0], "o") < 1e-2
+    assert head_rel_err(s2, whole[1], "state") < 1e-4
+
+
+@pytest.mark.parametrize("algo", ["chunk", "recurrent"])
+def test_deterministic(algo):
     import torch
     import paper_2609_39034_amd as sw
     inp = workloads.iid_inputs(2, 4, 70, 128, 128, 4, dtype="bf16", seed=22, state_std=0.1)
     dev = to_device(inp, "bf16")
-    a = sw.forward(*(dev[n] for n in NAMES), dev["state"])
-    b = sw.forward(*(dev[n] for n in NAMES), dev["state"])
+    a = sw.forward(*(dev[n] for n in NAMES), dev["state"], algo=algo)
+    b = sw.forward(*(dev[n] for n in NAMES), dev["state"], algo=algo)
     torch.cuda.synchronize()
     assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1])
 
