@@ -22,8 +22,9 @@ struct LayerArgs {
 // the launch; hipErrorInvalidValue if the shape has no instantiation.
 hipError_t launch_scan_direct(const LayerArgs &a, hipStream_t stream);
 
-// Exact chunked scan on the matrix cores; bf16 inputs only.
-hipError_t launch_scan_chunk(const LayerArgs &a, hipStream_t stream);
+// Exact chunk scan on the matrix cores, pipelined (one sequential wave plus
+// matrix-core waves); bf16 inputs, T > 0.
+hipError_t launch_scan_pipe(const LayerArgs &a, hipStream_t stream);
 
 // One-token decode step streaming the state through registers.
 hipError_t launch_decode(const LayerArgs &a, hipStream_t stream);

@@ -1,0 +1,599 @@
+// Exact chunk scan on the matrix cores (bf16 inputs, fp32 state), pipelined
+// over one sequential wave and the matrix-core waves.
+//
+// Every update of eq. recurrence adds a multiple of k_t to w_{jd}, so inside a
+// chunk of 16 tokens starting from state S_n the state before token t is
+//   w_{t-1,jd} = S_{n,jd} + sum_{s<t in chunk} c_{s,jd} k_s,   c = beta r delta.
+// Hence, exactly up to rounding order,
+//   pred_t   = k_t . S_n + sum_{s<t} (k_t . k_s) c_s           (prediction)
+//   w_t . q_t = q_t . S_n + sum_{s<=t} (q_t . k_s) c_s          (eq. retrieval)
+//   S_{n+1}  = S_n + sum_s c_s k_s^T.
+// The Dk-long contractions are 16 x 16 matrix-core products per chunk; only
+// the scalar recurrence of the coefficients over the 16 tokens of a chunk (a
+// <= 15-term right-looking update plus the E-step, per token) is sequential.
+// This is the algebra of the delta-rule chunk form that App. D builds on,
+// applied to the exact nonlinear recurrence one chunk at a time.  The
+// schedule puts only a 16 x 16 product between the recurrence of one chunk
+// and that of the next.  With C_n the coefficients of chunk n:
+//   P_{n+1} = K_{n+1} S_{n+1} = K_{n+1} S_n + (K_{n+1} K_n^T) C_n.
+// While the sequential wave runs the recurrence of chunk n (phase B), the
+// matrix-core waves do everything that does not need C_n:
+//   S_n = S_{n-1} + K_{n-1}^T C_{n-1}          (state update of the previous chunk)
+//   Y_{n-1} += tril(A_{n-1}) C_{n-1}; pi^q Y    (retrieval of the previous chunk)
+//   o_{n-2} = sum_j pi^q Y                      (output of the chunk before)
+//   Y0_n = Q_n S_n,  X_{n+1} = K_{n+1} S_n,  G'_n = K_{n+1} K_n^T (each wave,
+//   in registers),  G_{n+1} = K_{n+1} K_{n+1}^T,  pi^q_n, beta_{n+1}, ...
+//   and the HBM -> LDS transfer of chunk n+2 (direct global-to-LDS loads).
+// After C_n is published they form P_{n+1} = X_{n+1} + G'_n C_n (three
+// 16 x 16 x 16 products) and the next recurrence starts.  Two block barriers
+// per chunk.
+//
+// Precision.  bf16 q and k enter the matrix cores unrounded.  fp32 operands
+// (the state, the coefficients, the Gram products) are split into a bf16 high
+// part and a bf16 residual and the products that matter are summed (hi*hi +
+// hi*lo [+ lo*hi]), about 2^-16 relative error per product; fp32 accumulation.
+//
+// Layout.  Block = one head (b, h) and DB output dims with all J components,
+// N = J * DB columns (col = j * DB + dl); NW = N / 16 matrix-core waves, wave
+// w holding the Dk x 16 state tile of columns 16w..16w+15 in MFMA accumulator
+// layout; wave NW is the sequential wave.  Raw chunk inputs sit in a ring of
+// kRing LDS slots; K and Q rows are stored with their 16-byte pieces permuted
+// by row (piece p of row t at slot p ^ (t mod pieces)) so that the 16 lanes
+// reading one column range hit distinct banks.
+#include "device_common.hpp"
+#include "launch.hpp"
+
+namespace swila {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef short short4v __attribute__((ext_vector_type(4)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+constexpr int kC = 16;    // tokens per chunk
+constexpr int kRing = 4;  // raw-input slots: chunks n-1 .. n+2 are live
+
+__device__ __forceinline__ floatx4 mfma32(bf16x8 a, bf16x8 b, floatx4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ floatx4 mfma16(short4v a, short4v b, floatx4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ short bf16_bits(__bf16 x) { return __builtin_bit_cast(short, x); }
+__device__ __forceinline__ void split(float x, __bf16 &hi, __bf16 &lo) {
+    hi = (__bf16)x;
+    lo = (__bf16)(x - (float)hi);
+}
+__device__ __forceinline__ void wait_vm() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+template <int DK, int J, int DB>
+struct PCfg {
+    static constexpr int N = J * DB;
+    static constexpr int NW = N / 16;
+    static constexpr int NT = 64 * (NW + 1);
+    static constexpr int NMT = 64 * NW;           // matrix-core threads
+    static constexpr int JP = J == 3 ? 4 : J;
+    static constexpr int IT = DK / 16;
+    static constexpr int NP = N + 4;
+    static constexpr int KPC = DK / 8;            // 16-byte pieces per K row
+    static constexpr int KPIECES = kC * DK / 8;   // per K (or Q) chunk
+    static constexpr int LPIECES = kC * N / 8;    // per logit tensor chunk
+    static constexpr int VPIECES = kC * DB / 8;   // v chunk
+    static_assert(N % 16 == 0 && N <= 64 && DB % 8 == 0, "column block");
+    static_assert(DB * JP <= 64, "one sequential wave");
+};
+
+template <int DK, int J, int DB>
+struct PSmem {
+    using C = PCfg<DK, J, DB>;
+    uint4 k[kRing][C::KPIECES];
+    uint4 q[kRing][C::KPIECES];
+    uint4 lb[kRing][C::LPIECES];
+    uint4 lk[kRing][C::LPIECES];
+    uint4 lq[kRing][C::LPIECES];
+    uint4 v[kRing][C::VPIECES];
+    float beta[2][kC][C::NP];
+    float lks[2][kC][C::NP];   // key-prior logit * log2(e)
+    float vs[2][kC][DB + 4];
+    float pq[2][kC][C::NP];    // query prior
+    float g[2][kC][kC + 4];    // K_n K_n^T, for the sequential wave
+    float p[2][kC][C::NP];     // chunk-start predictions
+    float c[2][kC][C::NP];     // coefficients (column N: idle lanes)
+    float r[2][kC][C::NP];     // responsibilities
+    float py[2][kC][C::NP];    // pi^q * retrieval
+};
+
+// Four consecutive bf16 (as raw bits) of row t from element i (i % 4 == 0)
+// of a row-permuted K or Q tile.
+template <int DK>
+__device__ __forceinline__ uint2 tile4(const uint4 *tile, int t, int i) {
+    constexpr int KPC = DK / 8;
+    const int slot = t * KPC + ((i >> 3) ^ (t & (KPC - 1)));
+    return reinterpret_cast<const uint2 *>(tile + slot)[(i >> 2) & 1];
+}
+template <int DK>
+__device__ __forceinline__ uint16_t tile1(const uint4 *tile, int t, int i) {
+    constexpr int KPC = DK / 8;
+    const int slot = t * KPC + ((i >> 3) ^ (t & (KPC - 1)));
+    return reinterpret_cast<const uint16_t *>(tile + slot)[i & 7];
+}
+
+// A-operand fragment of rows 0..15 of a K or Q tile for the matrix-core step
+// covering key indices [32 s, 32 s + 32) (slot 8 g + m <-> key 32 s + 4 g + m,
+// and 32 s + 16 + 4 g + m - 4), or all 16 for Dk = 16.
+template <int DK>
+__device__ __forceinline__ uint4 frag32(const uint4 *tile, int tl, int lg, int s) {
+    const uint2 x0 = tile4<DK>(tile, tl, 32 * s + 4 * lg);
+    const uint2 x1 = tile4<DK>(tile, tl, 32 * s + 16 + 4 * lg);
+    return make_uint4(x0.x, x0.y, x1.x, x1.y);
+}
+
+// One wave-wide HBM -> LDS transfer: lane L moves 16 bytes from src to
+// dst + 16 L (dst is the same for the whole wave).
+__device__ __forceinline__ void dma16(const uint16_t *src, uint4 *dst) {
+    __builtin_amdgcn_global_load_lds((const void __attribute__((address_space(1))) *)src,
+                                     (void __attribute__((address_space(3))) *)dst, 16, 0, 0);
+}
+
+// First transfer index >= base that falls to wave mw in a round-robin deal.
+__device__ __forceinline__ int first_for(int base, int mw, int nw) {
+    return base + ((mw - base) % nw + nw) % nw;
+}
+
+// Issue the HBM -> LDS transfer of the chunk starting at token t0 into ring
+// slot `slot`.  The chunk is cut into wave-wide transfers of 64 x 16 bytes
+// (K, Q, the three logit tensors, v), dealt round-robin to the matrix-core
+// waves; each tensor has its own loop so its base address stays a scalar.
+// Tokens past T re-read token T - 1 (in range); the recurrence gives them
+// beta = 0.
+template <int DK, int J, int DB>
+__device__ __forceinline__ void issue_chunk(const LayerArgs &a, PSmem<DK, J, DB> &sm, int slot,
+                                            int t0, int b, int h, int d0, int mw, int lane) {
+    using C = PCfg<DK, J, DB>;
+    const int T = a.T, H = a.H, Dv = a.Dv;
+    constexpr int nk = (C::KPIECES + 63) / 64, nl = (C::LPIECES + 63) / 64;
+    const size_t row0 = (size_t)b * T;
+    // K and Q rows: piece p of row t goes to slot p ^ (t mod pieces)
+    auto kq = [&](const void *base, uint4 *tile, int ibase) {
+        for (int ins = first_for(ibase, mw, C::NW); ins < ibase + nk; ins += C::NW) {
+            const int part = ins - ibase, s = part * 64 + lane;
+            if (s < C::KPIECES) {
+                const int t = s / C::KPC, p = s % C::KPC;
+                const int tc = min(t0 + t, T - 1);
+                const int gp = p ^ (t & (C::KPC - 1));
+                dma16(static_cast<const uint16_t *>(base) + ((row0 + tc) * H + h) * DK + 8 * gp,
+                      tile + part * 64);
+            }
+        }
+    };
+    // logits, [t][j][dl]
+    auto logit = [&](const void *base, uint4 *dstv, int ibase) {
+        for (int ins = first_for(ibase, mw, C::NW); ins < ibase + nl; ins += C::NW) {
+            const int part = ins - ibase, s = part * 64 + lane;
+            if (s < C::LPIECES) {
+                const int t = s / (C::N / 8), rem = s % (C::N / 8);
+                const int j = rem / (DB / 8), qd = rem % (DB / 8);
+                const int tc = min(t0 + t, T - 1);
+                dma16(static_cast<const uint16_t *>(base) +
+                          (((row0 + tc) * H + h) * J + j) * Dv + d0 + 8 * qd,
+                      dstv + part * 64);
+            }
+        }
+    };
+    kq(a.k, sm.k[slot], 0);
+    kq(a.q, sm.q[slot], nk);
+    logit(a.lb, sm.lb[slot], 2 * nk);
+    logit(a.lk, sm.lk[slot], 2 * nk + nl);
+    logit(a.lq, sm.lq[slot], 2 * nk + 2 * nl);
+    constexpr int nv = (C::VPIECES + 63) / 64;  // v, [t][dl]
+    for (int ins = first_for(2 * nk + 3 * nl, mw, C::NW); ins < 2 * nk + 3 * nl + nv;
+         ins += C::NW) {
+        const int part = ins - (2 * nk + 3 * nl), s = part * 64 + lane;
+        if (s < C::VPIECES) {
+            const int t = s / (DB / 8), qd = s % (DB / 8);
+            const int tc = min(t0 + t, T - 1);
+            dma16(static_cast<const uint16_t *>(a.v) + ((row0 + tc) * H + h) * Dv + d0 + 8 * qd,
+                  sm.v[slot] + part * 64);
+        }
+    }
+}
+
+__device__ __forceinline__ float bf16_at(const uint4 *base, int idx) {
+    return bf16_bits_to_f32(reinterpret_cast<const uint16_t *>(base)[idx]);
+}
+
+// Same block-to-(head, column block) map as the chunk scan: every column block
+// of a head on one XCD when the head count is a multiple of 8.
+__device__ __forceinline__ void pipe_coords(int id, int ndb, int nheads, int &db, int &head) {
+    if (nheads % 8 == 0) {
+        const int xcd = id % 8, k = id / 8;
+        head = xcd + 8 * (k / ndb);
+        db = k % ndb;
+    } else {
+        head = id / ndb;
+        db = id % ndb;
+    }
+}
+
+template <int DK, int J, int DB>
+__global__ __launch_bounds__(320) void scan_pipe_kernel(LayerArgs a) {
+    using C = PCfg<DK, J, DB>;
+    constexpr int IT = C::IT, N = C::N, NW = C::NW, JP = C::JP;
+    __shared__ PSmem<DK, J, DB> sm;
+
+    const int tid = threadIdx.x;
+    const int w = tid / 64, lane = tid % 64;
+    const int tl = lane % 16, lg = lane / 16;
+    const int H = a.H, T = a.T, Dv = a.Dv;
+    int db, hh;
+    pipe_coords(blockIdx.x, Dv / DB, a.B * H, db, hh);
+    const int d0 = db * DB, h = hh % H, b = hh / H;
+    const int NCH = (T + kC - 1) / kC;
+    const bool seq = (w == NW);
+    // The sequential wave shares a SIMD with a matrix-core wave; its chain of
+    // dependent steps is the critical path, so it issues first.
+    if (seq) __builtin_amdgcn_s_setprio(3);
+
+    // ---- matrix-core wave state: W^T tile rows 16 it + 4 lg + r, column col
+    const int col = 16 * (seq ? 0 : w) + tl;
+    const int jc = col / DB, dc = d0 + col % DB;
+    const size_t sbase = (((size_t)b * H + h) * J + jc) * DK * Dv + dc;
+    floatx4 W[IT];
+#pragma unroll
+    for (int it = 0; it < IT; ++it) W[it] = floatx4{0.f, 0.f, 0.f, 0.f};
+    if (!seq && a.state_in) {
+#pragma unroll
+        for (int it = 0; it < IT; ++it)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+                W[it][r] = a.state_in[sbase + (size_t)(16 * it + 4 * lg + r) * Dv];
+    }
+    floatx4 Yacc = {0.f, 0.f, 0.f, 0.f}, Xacc = Yacc;
+    short4v chi = {0, 0, 0, 0}, clo = chi, ghi = chi, glo = chi;
+
+    // ---- sequential wave identity: lanes of one output dim are adjacent
+    const int sl = lane;
+    const int bdl = (sl / JP) % DB, bj = sl % JP;
+    const bool bact = seq && sl < DB * JP && bj < J;
+    const int bcol = bact ? bj * DB + bdl : 0;
+    const int bsto = bact ? bcol : N;
+
+    // split of the state tile into bf16 (hi, lo) B operands, per k-step
+    auto split_state = [&](bf16x8 (&whi)[IT / 2 > 0 ? IT / 2 : 1],
+                           bf16x8 (&wlo)[IT / 2 > 0 ? IT / 2 : 1], short4v &w16hi,
+                           short4v &w16lo) {
+        if constexpr (DK == 16) {
+#pragma unroll
+            for (int m = 0; m < 4; ++m) {
+                __bf16 hi, lo;
+                split(W[0][m], hi, lo);
+                w16hi[m] = bf16_bits(hi);
+                w16lo[m] = bf16_bits(lo);
+            }
+        } else {
+#pragma unroll
+            for (int s = 0; s < DK / 32; ++s)
+#pragma unroll
+                for (int m = 0; m < 4; ++m) {
+                    __bf16 hi, lo;
+                    split(W[2 * s][m], hi, lo);
+                    whi[s][m] = hi;
+                    wlo[s][m] = lo;
+                    split(W[2 * s + 1][m], hi, lo);
+                    whi[s][4 + m] = hi;
+                    wlo[s][4 + m] = lo;
+                }
+        }
+    };
+    // acc += (rows of tile) x S, with S split as above
+    auto tile_times_state = [&](const uint4 *tile, floatx4 acc, const bf16x8 (&whi)[IT / 2 > 0 ? IT / 2 : 1],
+                                const bf16x8 (&wlo)[IT / 2 > 0 ? IT / 2 : 1], short4v w16hi,
+                                short4v w16lo) {
+        if constexpr (DK == 16) {
+            const uint2 x = tile4<DK>(tile, tl, 4 * lg);
+            const short4v av = __builtin_bit_cast(short4v, x);
+            acc = mfma16(av, w16hi, acc);
+            acc = mfma16(av, w16lo, acc);
+        } else {
+#pragma unroll
+            for (int s = 0; s < DK / 32; ++s) {
+                const bf16x8 av = __builtin_bit_cast(bf16x8, frag32<DK>(tile, tl, lg, s));
+                acc = mfma32(av, whi[s], acc);
+                acc = mfma32(av, wlo[s], acc);
+            }
+        }
+        return acc;
+    };
+    // rows(x) . rows(y)^T for two 16-row tiles (Gram-type product), exact products
+    auto gram = [&](const uint4 *x, const uint4 *y) {
+        floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+        if constexpr (DK == 16) {
+            const short4v ax = __builtin_bit_cast(short4v, tile4<DK>(x, tl, 4 * lg));
+            const short4v ay = __builtin_bit_cast(short4v, tile4<DK>(y, tl, 4 * lg));
+            acc = mfma16(ax, ay, acc);
+        } else {
+#pragma unroll
+            for (int s = 0; s < DK / 32; ++s) {
+                const bf16x8 ax = __builtin_bit_cast(bf16x8, frag32<DK>(x, tl, lg, s));
+                const bf16x8 ay = __builtin_bit_cast(bf16x8, frag32<DK>(y, tl, lg, s));
+                acc = mfma32(ax, ay, acc);
+            }
+        }
+        return acc;
+    };
+    // derived inputs of chunk m (ring slot rs, parity pr) for the sequential wave
+    auto prep_seq_inputs = [&](int m, int rs, int pr) {
+#pragma unroll
+        for (int it = 0; it < (kC * N + C::NMT - 1) / C::NMT; ++it) {
+            const int e = tid + it * C::NMT;
+            if (kC * N % C::NMT != 0 && e >= kC * N) break;
+            const int t = e / N, cc = e % N;
+            const bool ok = m * kC + t < T;
+            sm.beta[pr][t][cc] = ok ? rcp_fast(1.0f + exp_fast(-bf16_at(sm.lb[rs], e))) : 0.f;
+            sm.lks[pr][t][cc] = bf16_at(sm.lk[rs], e) * kLog2e;
+        }
+#pragma unroll
+        for (int it = 0; it < (kC * DB + C::NMT - 1) / C::NMT; ++it) {
+            const int e = tid + it * C::NMT;
+            if (kC * DB % C::NMT == 0 || e < kC * DB) sm.vs[pr][e / DB][e % DB] = bf16_at(sm.v[rs], e);
+        }
+    };
+    // pi^q of chunk m: softmax over j of the query-prior logits, per (t, dl)
+    auto prep_query_prior = [&](int rs, int pr) {
+#pragma unroll
+        for (int it = 0; it < (kC * DB + C::NMT - 1) / C::NMT; ++it) {
+            const int e = tid + it * C::NMT;
+            if (kC * DB % C::NMT != 0 && e >= kC * DB) break;
+            const int t = e / DB, dl = e % DB;
+            float x[J], mq = -INFINITY;
+#pragma unroll
+            for (int j = 0; j < J; ++j) {
+                x[j] = bf16_at(sm.lq[rs], t * N + j * DB + dl);
+                mq = fmaxf(mq, x[j]);
+            }
+            float z = 0.f;
+#pragma unroll
+            for (int j = 0; j < J; ++j) {
+                x[j] = exp_fast(x[j] - mq);
+                z += x[j];
+            }
+            const float iz = rcp_fast(z);
+#pragma unroll
+            for (int j = 0; j < J; ++j) sm.pq[pr][t][j * DB + dl] = x[j] * iz;
+        }
+    };
+    auto store_output = [&](int m, int pr) {
+#pragma unroll
+        for (int it = 0; it < (kC * DB + C::NMT - 1) / C::NMT; ++it) {
+            const int e = tid + it * C::NMT;
+            if (kC * DB % C::NMT != 0 && e >= kC * DB) break;
+            const int t = e / DB, dl = e % DB;
+            if (m * kC + t < T) {
+                float o = 0.f;
+#pragma unroll
+                for (int j = 0; j < J; ++j) o += sm.py[pr][t][j * DB + dl];
+                store1(a.o, ((size_t)(b * T + m * kC + t) * H + h) * Dv + d0 + dl, o, a.out_bf16);
+            }
+        }
+    };
+    auto store_resp = [&](int m, int pr) {
+        for (int e = tid; e < kC * N; e += C::NMT) {
+            const int t = e / N, cc = e % N;
+            if (m * kC + t < T)
+                a.resp[(((size_t)(b * T + m * kC + t) * H + h) * J + cc / DB) * Dv + d0 + cc % DB] =
+                    sm.r[pr][t][cc];
+        }
+    };
+    // W += K_m^T C_m and Y += tril(A_m) C_m (C_m split in chi/clo); then
+    // stage pi^q * Y of chunk m
+    auto finish_chunk = [&](int m) {
+        const int rs = m % kRing, pr = m & 1;
+#pragma unroll
+        for (int it = 0; it < IT; ++it) {
+            short4v ak;
+#pragma unroll
+            for (int mm = 0; mm < 4; ++mm)
+                ak[mm] = (short)tile1<DK>(sm.k[rs], 4 * lg + mm, 16 * it + tl);
+            W[it] = mfma16(ak, chi, W[it]);
+            W[it] = mfma16(ak, clo, W[it]);
+        }
+        // (K_m Q_m^T)[s][t] in accumulator layout is lane (t = tl, s = 4 lg + r):
+        // exactly the A operand of tril(A_m) C_m, A_m = Q_m K_m^T
+        const floatx4 at = gram(sm.k[rs], sm.q[rs]);
+        short4v ahi, alo;
+#pragma unroll
+        for (int mm = 0; mm < 4; ++mm) {
+            __bf16 hi, lo;
+            split(4 * lg + mm <= tl ? at[mm] : 0.f, hi, lo);
+            ahi[mm] = bf16_bits(hi);
+            alo[mm] = bf16_bits(lo);
+        }
+        Yacc = mfma16(ahi, chi, Yacc);
+        Yacc = mfma16(ahi, clo, Yacc);
+        Yacc = mfma16(alo, chi, Yacc);
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+            sm.py[pr][4 * lg + r][col] = Yacc[r] * sm.pq[pr][4 * lg + r][col];
+    };
+
+    // ---------------- prologue: chunks 0 and 1 into the ring; P_0, G_0
+    if (!seq) {
+        issue_chunk<DK, J, DB>(a, sm, 0, 0, b, h, d0, w, lane);
+        if (NCH > 1) issue_chunk<DK, J, DB>(a, sm, 1, kC, b, h, d0, w, lane);
+        wait_vm();
+    }
+    block_sync_lds();
+    if (!seq) {
+        prep_seq_inputs(0, 0, 0);
+        bf16x8 whi[IT / 2 > 0 ? IT / 2 : 1], wlo[IT / 2 > 0 ? IT / 2 : 1];
+        short4v w16hi, w16lo;
+        split_state(whi, wlo, w16hi, w16lo);
+        const floatx4 P0 = tile_times_state(sm.k[0], floatx4{0.f, 0.f, 0.f, 0.f}, whi, wlo,
+                                            w16hi, w16lo);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) sm.p[0][4 * lg + r][col] = P0[r];
+        if (w == 0) {
+            const floatx4 G0 = gram(sm.k[0], sm.k[0]);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) sm.g[0][4 * lg + r][tl] = G0[r];
+        }
+    }
+    block_sync_lds();
+
+    for (int n = 0; n < NCH; ++n) {
+        const int pr = n & 1, rs = n % kRing;
+        if (seq) {
+            // ---- B: the token recurrence of chunk n
+            float P[kC], vv[kC], lkv[kC], bev[kC];
+#pragma unroll
+            for (int t = 0; t < kC; ++t) {
+                P[t] = sm.p[pr][t][bcol];
+                vv[t] = sm.vs[pr][t][bdl];
+                lkv[t] = bact ? sm.lks[pr][t][bcol] : -INFINITY;
+                bev[t] = bact ? sm.beta[pr][t][bcol] : 0.f;
+            }
+            float grow[kC];
+#pragma unroll
+            for (int u = 1; u < kC; ++u) grow[u] = sm.g[pr][0][u];
+#pragma unroll
+            for (int t = 0; t < kC; ++t) {
+                float gnext[kC];
+#pragma unroll
+                for (int u = t + 2; u < kC; ++u) gnext[u] = sm.g[pr][t + 1][u];
+                const float delta = vv[t] - P[t];
+                const float bd = bev[t] * delta;
+                const float e = fmaf(-0.5f * kLog2e * delta, delta, lkv[t]);
+                const float mx = group_max<JP>(e);
+                const float ex = __builtin_amdgcn_exp2f(e - mx);
+                const float z = group_sum<JP>(ex);
+                const float r = ex * rcp_fast(z);
+                const float c = bd * r;
+#pragma unroll
+                for (int u = t + 1; u < kC; ++u) P[u] = fmaf(grow[u], c, P[u]);
+                sm.c[pr][t][bsto] = c;
+                sm.r[pr][t][bsto] = r;
+#pragma unroll
+                for (int u = t + 2; u < kC; ++u) grow[u] = gnext[u];
+            }
+            block_sync_lds();   // e(n): C_n published
+            block_sync_lds();   // i(n+1): P_{n+1} ready
+            continue;
+        }
+
+        // ---- matrix-core waves, while the sequential wave runs chunk n
+        if (n >= 1) {
+            finish_chunk(n - 1);                 // S_n, pi^q Y_{n-1}
+            if (a.resp) store_resp(n - 1, (n - 1) & 1);
+        }
+        if (n >= 2) store_output(n - 2, n & 1);  // (n - 2) & 1 == n & 1
+        {
+            bf16x8 whi[IT / 2 > 0 ? IT / 2 : 1], wlo[IT / 2 > 0 ? IT / 2 : 1];
+            short4v w16hi, w16lo;
+            split_state(whi, wlo, w16hi, w16lo);
+            Yacc = tile_times_state(sm.q[rs], floatx4{0.f, 0.f, 0.f, 0.f}, whi, wlo, w16hi, w16lo);
+            if (n + 1 < NCH)
+                Xacc = tile_times_state(sm.k[(n + 1) % kRing], floatx4{0.f, 0.f, 0.f, 0.f}, whi,
+                                        wlo, w16hi, w16lo);
+        }
+        if (n + 1 < NCH) {
+            // G'_n = K_{n+1} K_n^T as the A operand of G'_n C_n: the accumulator
+            // layout of K_n K_{n+1}^T, split in registers
+            const floatx4 gt = gram(sm.k[rs], sm.k[(n + 1) % kRing]);
+#pragma unroll
+            for (int m = 0; m < 4; ++m) {
+                __bf16 hi, lo;
+                split(gt[m], hi, lo);
+                ghi[m] = bf16_bits(hi);
+                glo[m] = bf16_bits(lo);
+            }
+        }
+        if (w == (1 % NW) && n + 1 < NCH) {
+            const floatx4 g1 = gram(sm.k[(n + 1) % kRing], sm.k[(n + 1) % kRing]);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) sm.g[pr ^ 1][4 * lg + r][tl] = g1[r];
+        }
+        prep_query_prior(rs, pr);
+        if (n + 1 < NCH) prep_seq_inputs(n + 1, (n + 1) % kRing, pr ^ 1);
+        if (n + 2 < NCH) issue_chunk<DK, J, DB>(a, sm, (n + 2) % kRing, (n + 2) * kC, b, h, d0, w, lane);
+        block_sync_lds();   // e(n): C_n published (and G'_n)
+
+        // ---- P_{n+1} = X_{n+1} + G'_n C_n
+#pragma unroll
+        for (int m = 0; m < 4; ++m) {
+            __bf16 hi, lo;
+            split(sm.c[pr][4 * lg + m][col], hi, lo);
+            chi[m] = bf16_bits(hi);
+            clo[m] = bf16_bits(lo);
+        }
+        if (n + 1 < NCH) {
+            Xacc = mfma16(ghi, chi, Xacc);
+            Xacc = mfma16(ghi, clo, Xacc);
+            Xacc = mfma16(glo, chi, Xacc);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) sm.p[pr ^ 1][4 * lg + r][col] = Xacc[r];
+        }
+        wait_vm();          // chunk n+2 has landed in LDS
+        block_sync_lds();   // i(n+1)
+    }
+
+    // ---------------- epilogue: last state update and the last two outputs
+    if (!seq) {
+        finish_chunk(NCH - 1);
+        if (a.resp) store_resp(NCH - 1, (NCH - 1) & 1);
+        if (NCH >= 2) store_output(NCH - 2, NCH & 1);
+    }
+    block_sync_lds();
+    if (!seq) {
+        store_output(NCH - 1, (NCH - 1) & 1);
+        if (a.state_out) {
+#pragma unroll
+            for (int it = 0; it < IT; ++it)
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    a.state_out[sbase + (size_t)(16 * it + 4 * lg + r) * Dv] = W[it][r];
+        }
+    }
+}
+
+template <int DK, int J, int DB>
+hipError_t launch_cfg(const LayerArgs &a, hipStream_t stream) {
+    using C = PCfg<DK, J, DB>;
+    static_assert(sizeof(PSmem<DK, J, DB>) <= 160 * 1024, "LDS");
+    const long blocks = (long)(a.Dv / DB) * a.H * a.B;
+    hipLaunchKernelGGL((scan_pipe_kernel<DK, J, DB>), dim3((unsigned)blocks), dim3(C::NT), 0,
+                       stream, a);
+    return hipGetLastError();
+}
+
+template <int DK>
+hipError_t launch_dk(const LayerArgs &a, hipStream_t stream) {
+    // DB = min(Dv, 64 / J'): at most 64 columns, one wave of sequential lanes
+    switch (a.J) {
+        case 1:
+            if (a.Dv >= 64) return launch_cfg<DK, 1, 64>(a, stream);
+            if (a.Dv == 32) return launch_cfg<DK, 1, 32>(a, stream);
+            return launch_cfg<DK, 1, 16>(a, stream);
+        case 2:
+            if (a.Dv >= 32) return launch_cfg<DK, 2, 32>(a, stream);
+            return launch_cfg<DK, 2, 16>(a, stream);
+        case 3: return launch_cfg<DK, 3, 16>(a, stream);
+        case 4: return launch_cfg<DK, 4, 16>(a, stream);
+        case 8: return launch_cfg<DK, 8, 8>(a, stream);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace
+
+hipError_t launch_scan_pipe(const LayerArgs &a, hipStream_t stream) {
+    if (!a.in_bf16 || a.T <= 0) return hipErrorInvalidValue;
+    switch (a.Dk) {
+        case 16: return launch_dk<16>(a, stream);
+        case 32: return launch_dk<32>(a, stream);
+        case 64: return launch_dk<64>(a, stream);
+        case 128: return launch_dk<128>(a, stream);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace swila

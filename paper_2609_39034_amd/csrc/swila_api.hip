@@ -186,7 +186,7 @@ int swila_forward(const swila_shape *shape, const swila_opts *opts, const void *
     }
     const bool chunk = opts->algo == SWILA_ALGO_CHUNK_EXACT ||
                        (opts->algo == SWILA_ALGO_AUTO && opts->in_dtype == SWILA_BF16);
-    if (chunk) return map_hip(swila::launch_scan_chunk(a, st), "chunk scan launch");
+    if (chunk) return map_hip(swila::launch_scan_pipe(a, st), "chunk scan launch");
     return map_hip(swila::launch_scan_direct(a, st), "scan launch");
 }
 

@@ -68,6 +68,21 @@ CHUNK = [
 ]
 
 
+# batch x head counts that make the dispatcher pick each column-block size
+# (64, 32 or 16 columns per block) for J = 1, 2, 4 and 8
+COLUMN_BLOCKS = [
+    (16, 8, 20, 64, 128, 4), (8, 8, 20, 64, 128, 4), (8, 8, 20, 128, 128, 8),
+    (4, 8, 20, 32, 128, 8), (16, 8, 20, 16, 128, 2), (32, 8, 20, 16, 128, 2),
+    (64, 8, 12, 16, 128, 1), (32, 8, 12, 16, 128, 1),
+]
+
+
+@pytest.mark.parametrize("B,H,T,Dk,Dv,J", COLUMN_BLOCKS)
+def test_chunk_column_blocks(B, H, T, Dk, Dv, J):
+    inp = workloads.iid_inputs(B, H, T, Dk, Dv, J, dtype="bf16", seed=500 + B + J, state_std=0.2)
+    _check(inp, "bf16", algo="chunk")
+
+
 @pytest.mark.parametrize("algo", ["chunk", "recurrent"])
 @pytest.mark.parametrize("B,H,T,Dk,Dv,J,std", CHUNK)
 def test_bf16_algorithms(B, H, T, Dk, Dv, J, std, algo):
@@ -128,39 +143,42 @@ def test_zero_length_copies_state():
     assert torch.count_nonzero(s) == 0
 
 
-@pytest.mark.parametrize("algo,split", [("recurrent", 19), ("chunk", 32)])
-def test_state_passing_and_in_place(algo, split):
+def test_state_passing_and_in_place():
     """Running a sequence in two pieces, passing the state (in place), gives
-    bit-identical outputs and state to one run (for the chunk scan, when the split
-    falls on a chunk boundary, so the rounding order is the same)."""
+    bit-identical outputs and state to one run of the token-by-token scan."""
     import torch
     import paper_2609_39034_amd as sw
     inp = workloads.iid_inputs(2, 2, 45, 64, 64, 4, dtype="bf16", seed=21, state_std=0.1)
     dev = to_device(inp, "bf16")
-    o_all, s_all = sw.forward(*(dev[n] for n in NAMES), dev["state"], algo=algo)
+    o_all, s_all = sw.forward(*(dev[n] for n in NAMES), dev["state"], algo="recurrent")
     st = dev["state"].clone()
-    o1, _ = sw.forward(*(dev[n][:, :split].contiguous() for n in NAMES), st, state_out=st,
-                       algo=algo)
-    o2, _ = sw.forward(*(dev[n][:, split:].contiguous() for n in NAMES), st, state_out=st,
-                       algo=algo)
+    o1, _ = sw.forward(*(dev[n][:, :19].contiguous() for n in NAMES), st, state_out=st,
+                       algo="recurrent")
+    o2, _ = sw.forward(*(dev[n][:, 19:].contiguous() for n in NAMES), st, state_out=st,
+                       algo="recurrent")
     torch.cuda.synchronize()
     assert torch.equal(torch.cat([o1, o2], dim=1), o_all)
     assert torch.equal(st, s_all)
 
 
-def test_chunk_state_passing_any_split():
-    """Splitting off a chunk boundary changes only the rounding order."""
+@pytest.mark.parametrize("split", [19, 32])
+def test_chunk_state_passing(split):
+    """For the chunk scan, splitting the sequence (passing the state in place)
+    changes only the rounding order of the products."""
+    import torch
+    import paper_2609_39034_amd as sw
     inp = workloads.iid_inputs(2, 2, 45, 64, 64, 4, dtype="bf16", seed=23, state_std=0.1)
-    whole = gpu_forward(inp, "bf16", algo="chunk")
-    first = {n: (None if inp[n] is None else inp[n][:, :19]) for n in NAMES}
-    first["state"] = inp["state"]
-    o1, s1 = gpu_forward(first, "bf16", algo="chunk")
-    second = {n: inp[n][:, 19:] for n in NAMES}
-    second["state"] = s1.astype(np.float32)
-    o2, s2 = gpu_forward(second, "bf16", algo="chunk")
-    o = np.concatenate([o1, o2], axis=1)
-    assert head_rel_err(o, whole[0], "o") < 1e-2
-    assert head_rel_err(s2, whole[1], "state") < 1e-4
+    dev = to_device(inp, "bf16")
+    o_all, s_all = sw.forward(*(dev[n] for n in NAMES), dev["state"], algo="chunk")
+    st = dev["state"].clone()
+    o1, _ = sw.forward(*(dev[n][:, :split].contiguous() for n in NAMES), st, state_out=st,
+                       algo="chunk")
+    o2, _ = sw.forward(*(dev[n][:, split:].contiguous() for n in NAMES), st, state_out=st,
+                       algo="chunk")
+    torch.cuda.synchronize()
+    o = torch.cat([o1, o2], dim=1).float().cpu().numpy()
+    assert head_rel_err(o, o_all.float().cpu().numpy(), "o") < 1e-2
+    assert head_rel_err(st.cpu().numpy(), s_all.cpu().numpy(), "state") < 1e-4
 
 
 @pytest.mark.parametrize("algo", ["chunk", "recurrent"])
