@@ -36,6 +36,8 @@ MEASURED_TRAFFIC = {
     ("decode.hip", "769b72fdca36c7f4df23d3fb1d410dc16c3c323568a37067ebabab4fb4b755be"): 2184302284,
     ("scan_direct.hip", "b38c28c5de8d782d7e8789d36b1d92720d8a6715bdb2781db527a2d9cdf2e1ba"):
         136540979,
+    ("scan_pipe.hip", "cd75b604f8ebc54e901f0186d51ba3cb20b32f833a09982c1d2cebe8f79251a7"):
+        136596480,
 }
 
 
@@ -188,7 +190,7 @@ def main():
     s_out = torch.empty((B, H, J, Dk, Dv), device="cuda", dtype=torch.float32)
     wall, kern = time_forward(sw, torch, dev, args.steps, args.warmup, o, s_out, args.algo)
     chunk = args.algo == "chunk" or (args.algo == "auto" and bf16)
-    kname, ksrc = (("scan_chunk_kernel", "scan_chunk.hip") if chunk
+    kname, ksrc = (("scan_pipe_kernel", "scan_pipe.hip") if chunk
                    else ("scan_direct_kernel", "scan_direct.hip"))
 
     eb = 2 if bf16 else 4
