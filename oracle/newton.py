@@ -29,7 +29,12 @@ Readings taken where the appendix is silent:
 * The layer output after an iteration is eq. retrieval evaluated on the
   trajectory of that iteration's linear solve.
 * ``g_clamp`` (default off) optionally clips g into an interval; the fixed point
-  does not depend on the Jacobian approximation (App. D.2).
+  does not depend on the Jacobian approximation (App. D.2).  ``"stable"``
+  clips g_t into [0, 2 / |k_t|^2], the widest interval in which every
+  linearised transition I - g k k^T has spectral radius at most 1 (its only
+  eigenvalue other than 1 is 1 - g |k|^2).  Without such a clip, g < 0 makes
+  transitions expansive and the iterates of long sequences overflow before
+  they converge.
 """
 from __future__ import annotations
 
@@ -42,15 +47,22 @@ def _softmax_j(x):
     return e / e.sum(axis=0, keepdims=True)
 
 
-def linearise(pred, v, beta, prior_k, g_clamp=None):
+def linearise(pred, v, beta, prior_k, g_clamp=None, kk=None):
     """Jacobian coefficient g (eq. jacobian_coeff) and effective input p
     (eq. effective_input) around predictions ``pred`` = k_t^T w^{(i)}_{t-1}.
-    pred, beta, prior_k [T,J,Dv]; v [T,Dv].  Returns (g, p, delta, r)."""
+    pred, beta, prior_k [T,J,Dv]; v [T,Dv]; kk [T] = |k_t|^2 (needed for
+    g_clamp="stable").  Returns (g, p, delta, r)."""
     delta = v[:, None, :] - pred
     num = prior_k * np.exp(-0.5 * delta ** 2)
     r = num / num.sum(axis=1, keepdims=True)
     g = beta * r * (1.0 - delta ** 2 * (1.0 - r))
-    if g_clamp is not None:
+    if isinstance(g_clamp, str):
+        if g_clamp != "stable":
+            raise ValueError("g_clamp must be None, (lo, hi) or 'stable'")
+        with np.errstate(divide="ignore"):
+            hi = 2.0 / np.asarray(kk, dtype=np.float64)          # inf for a zero key
+        g = np.minimum(np.maximum(g, 0.0), hi[:, None, None])
+    elif g_clamp is not None:
         g = np.clip(g, g_clamp[0], g_clamp[1])
     p = g * pred + beta * r * delta
     return g, p, delta, r
@@ -82,7 +94,7 @@ def newton_head(q, k, v, lb, lk, lq, W0=None, *, chunk, iters, g_clamp=None, tol
     n_run = 0
     for _ in range(iters):
         # linearisation around the current iterate (App. D.2)
-        g, p, _, _ = linearise(pred, v, beta, prior_k, g_clamp)
+        g, p, _, _ = linearise(pred, v, beta, prior_k, g_clamp, kk=np.einsum("ti,ti->t", k, k))
 
         new_pred = np.zeros_like(pred)
         Wb = W0.copy()                      # boundary state w_[n]

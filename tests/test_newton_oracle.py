@@ -107,3 +107,49 @@ def test_clamped_jacobian_same_fixed_point():
     o, S, _ = newton.newton_forward(*args, inp["state"], chunk=4, iters=9, g_clamp=(0.0, 1.0))
     assert np.max(np.abs(o - seq["o"])) < 1e-10
     assert np.max(np.abs(S - seq["state"])) < 1e-10
+
+
+# The "stable" clamp, g_t in [0, 2 / |k_t|^2]: keys of norm^2 up to ~3 so that
+# the upper bound binds; the fixed point is still the sequential trajectory and
+# the first i predictions are exact after i sweeps (App. D.1-D.2).
+def _scaled_keys(inp, seed):
+    rng = np.random.Generator(np.random.PCG64(seed))
+    k = np.asarray(inp["k"], dtype=np.float64)
+    scale = np.sqrt(rng.uniform(0.5, 3.0, size=k.shape[:3] + (1,)))
+    inp = dict(inp)
+    inp["k"] = k / np.linalg.norm(k, axis=-1, keepdims=True) * scale
+    return inp
+
+
+def test_stable_clamp_fixed_point_and_exact_prefix():
+    inp = _scaled_keys(_inp(1, 1, 12, 4, 3, 3, seed=37, state_std=0.2), seed=38)
+    args = _f64(inp)
+    seq = oracle.forward(*args, inp["state"], want_delta=True)
+    exact_pred = args[2][0, :, 0][:, None, :] - seq["delta"][0, :, 0]
+    o, S, heads = newton.newton_forward(*args, inp["state"], chunk=5, iters=12,
+                                        g_clamp="stable")
+    preds = heads[(0, 0)]["preds"]
+    for i in range(1, 13):
+        assert np.max(np.abs(preds[i][:i] - exact_pred[:i])) < 1e-9, i
+    assert np.max(np.abs(o - seq["o"])) < 1e-9
+    assert np.max(np.abs(S - seq["state"])) < 1e-9
+
+
+def test_stable_clamp_bounds():
+    inp = _scaled_keys(_inp(1, 1, 40, 6, 5, 4, seed=39), seed=40)
+    k = np.asarray(inp["k"], dtype=np.float64)[0, :, 0]
+    kk = np.einsum("ti,ti->t", k, k)
+    rng = np.random.Generator(np.random.PCG64(41))
+    pred = rng.standard_normal((40, 4, 5)) * 3.0          # far from any fixed point
+    v = rng.standard_normal((40, 5))
+    beta = rng.uniform(0.0, 1.0, (40, 4, 5))
+    prior = scipy.special.softmax(rng.standard_normal((40, 4, 5)), axis=1)
+    g0, _, _, _ = newton.linearise(pred, v, beta, prior)
+    g, p, delta, r = newton.linearise(pred, v, beta, prior, "stable", kk=kk)
+    hi = (2.0 / kk)[:, None, None]
+    assert (g0 < 0).any() and (g0 > hi).any()              # both bounds are exercised
+    assert np.all(g >= 0) and np.all(g <= hi)
+    inside = (g0 >= 0) & (g0 <= hi)
+    assert np.array_equal(g[inside], g0[inside])
+    # p keeps its definition with the clamped g (eq. effective_input)
+    assert np.allclose(p, g * pred + beta * r * delta, rtol=0, atol=1e-12)
