@@ -81,11 +81,11 @@ def host_cores():
     return max(1, min(n, 16))
 
 
-def time_forward(sw, torch, dev, steps, warmup, o, s_out, algo):
+def time_forward(sw, torch, dev, steps, warmup, o, s_out, algo, **kw):
     names = ("q", "k", "v", "lb", "lk", "lq")
     args = [dev[n] for n in names]
     for _ in range(warmup):
-        sw.forward(*args, dev["state"], o=o, state_out=s_out, algo=algo)
+        sw.forward(*args, dev["state"], o=o, state_out=s_out, algo=algo, **kw)
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
@@ -93,12 +93,47 @@ def time_forward(sw, torch, dev, steps, warmup, o, s_out, algo):
     t0 = time.perf_counter()
     for i in range(steps):
         ev[i][0].record(stream)
-        sw.forward(*args, dev["state"], o=o, state_out=s_out, algo=algo)
+        sw.forward(*args, dev["state"], o=o, state_out=s_out, algo=algo, **kw)
         ev[i][1].record(stream)
     torch.cuda.synchronize()
     wall = (time.perf_counter() - t0) / steps
     kern = sum(a.elapsed_time(b) for a, b in ev) / steps / 1e3
     return wall, kern
+
+
+def newton_alg_flops(B, H, T, Dk, Dv, J, sweeps, chunk=16):
+    """Matrix-core work of the App. D form as this library evaluates it, each
+    product counted once (the bf16 high/residual split counts against it).
+    Per sweep, per chunk of C tokens and head (N = J * Dv columns):
+    Q S and K S (2 C Dk N), the state update K^T X (C Dk N), the two C x C by
+    C x N products of the forward substitution and the retrieval (2 C^2 N),
+    and the three C x C Gram products (3 C^2 Dk).  The initial guess K W_0
+    (Dk N per token) is counted once.  2 FLOP per multiply-add."""
+    nch = (T + chunk - 1) // chunk
+    per_chunk = 3 * chunk * Dk * J * Dv + 2 * chunk * chunk * J * Dv + 3 * chunk * chunk * Dk
+    return 2 * B * H * (sweeps * nch * per_chunk + T * Dk * J * Dv)
+
+
+def bench_newton(sw, torch, dev, cfg, steps, warmup, o, s_out, tol):
+    B, H, T, Dk, Dv, J = (cfg[x] for x in ("B", "H", "T", "Dk", "Dv", "J"))
+    ws = torch.empty(sw.forward_workspace_bytes(B, H, T, Dk, Dv, J, algo="newton"),
+                     device="cuda", dtype=torch.uint8)
+    it = torch.zeros(2, device="cuda", dtype=torch.int32)
+    wall, kern = time_forward(sw, torch, dev, steps, warmup, o, s_out, "newton", workspace=ws,
+                              tol=tol, max_iters=256, iters_out=it)
+    sweeps, unconverged = (int(x) for x in it.cpu())
+    nflop = newton_alg_flops(B, H, T, Dk, Dv, J, sweeps)
+    return {
+        "workload": "App. D chunkwise quasi-Newton, same batch, tol %g (relative change of "
+                    "the predictions), g clamped to [0, 2/|k|^2]" % tol,
+        "tokens_per_s": B * T / wall, "ms_per_step": wall * 1e3, "sweeps": sweeps,
+        "unconverged_blocks": unconverged,
+        "roofline": {"bound": "mfma", "achieved": nflop / kern / 1e12,
+                     "peak": PEAK_MFMA_BF16 / 1e12, "unit": "TFLOP/s",
+                     "frac": nflop / kern / PEAK_MFMA_BF16, "traffic": None,
+                     "kernel": "scan_pipe_kernel (Newton mode)", "kernel_ms": kern * 1e3,
+                     "alg_flop_per_launch": nflop},
+    }
 
 
 def bench_decode(sw, torch, workloads, steps_total, warmup):
@@ -158,6 +193,8 @@ def main():
     ap.add_argument("--algo", default="auto", choices=["auto", "chunk", "recurrent"])
     ap.add_argument("--decode-steps", type=int, default=512)
     ap.add_argument("--no-decode", action="store_true")
+    ap.add_argument("--no-newton", action="store_true")
+    ap.add_argument("--newton-tol", type=float, default=1e-3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only copy 1 GiB device-to-device (scales HBM counters)")
@@ -220,6 +257,9 @@ def main():
     out.update({
         "head_tokens_per_s": B * H * T / wall,
     })
+    if not args.no_newton and bf16:
+        out["newton"] = bench_newton(sw, torch, dev, cfg, args.steps, args.warmup, o, s_out,
+                                     args.newton_tol)
     if not args.no_decode:
         out["decode"] = bench_decode(sw, torch, workloads, args.decode_steps, args.warmup)
     if not args.no_cpu_baseline:

@@ -59,19 +59,39 @@ enum swila_dtype { SWILA_F32 = 0, SWILA_BF16 = 1 };
 enum swila_algo {
     SWILA_ALGO_AUTO = 0,        /* CHUNK_EXACT for bf16 inputs, RECURRENT for fp32 */
     SWILA_ALGO_RECURRENT = 1,   /* token-by-token scan on the vector ALUs */
-    SWILA_ALGO_CHUNK_EXACT = 2  /* the same recurrence evaluated 16 tokens at a time with
+    SWILA_ALGO_CHUNK_EXACT = 2, /* the same recurrence evaluated 16 tokens at a time with
                                    the Dk-long products on the matrix cores (bf16 inputs
                                    only; fp32 operands split into bf16 high + residual) */
+    SWILA_ALGO_NEWTON = 3       /* App. D: chunkwise parallel quasi-Newton iteration.  Each
+                                   sweep linearises the recurrence around the previous
+                                   sweep's predictions k_t . w_{t-1} (eq. jacobian_coeff,
+                                   eq. effective_input) and solves the linear recurrence
+                                   (eq. linearized) chunk by chunk (App. D.3), on the matrix
+                                   cores like CHUNK_EXACT.  The first sweep linearises
+                                   around w_t = W_0 for all t.  bf16 inputs only; needs a
+                                   workspace; resp_out must be NULL. */
+};
+
+/* opts->flags bits */
+enum swila_flags {
+    SWILA_FLAG_NEWTON_NO_CLAMP = 1  /* SWILA_ALGO_NEWTON: use g of eq. jacobian_coeff as it
+                                       is.  By default g is clamped to [0, 2 / |k_t|^2], which
+                                       keeps every linearised transition I - g k k^T
+                                       non-expansive; the fixed point does not depend on the
+                                       Jacobian approximation (App. D.2). */
 };
 
 typedef struct swila_opts {
     int32_t in_dtype;    /* enum swila_dtype of q, k, v and the three logits */
     int32_t out_dtype;   /* enum swila_dtype of o */
     int32_t algo;        /* enum swila_algo */
-    int32_t chunk;       /* chunk length of chunked forms; 0 = default */
-    int32_t max_iters;   /* reserved, 0 */
-    float tol;           /* reserved, 0 */
-    uint32_t flags;      /* reserved, 0 */
+    int32_t chunk;       /* chunk length of the chunked forms: 0 (default) or 16 */
+    int32_t max_iters;   /* SWILA_ALGO_NEWTON: most sweeps; 0 = 64.  Ignored otherwise. */
+    float tol;           /* SWILA_ALGO_NEWTON: a block of columns stops once the largest
+                            change of its predictions in a sweep is <= tol * max(1, largest
+                            |prediction|); 0 = 1e-3; < 0 = run exactly max_iters sweeps.
+                            Ignored otherwise.  NaN is an error. */
+    uint32_t flags;      /* enum swila_flags; other bits must be 0 */
 } swila_opts;
 
 enum swila_status {
@@ -103,10 +123,16 @@ int swila_state_init(const swila_shape *shape, float *state, const float *src, v
  *   o:         output [B,T,H,Dv], out_dtype.  Must not overlap any input.
  *   resp_out:  NULL, or [B,T,H,J,Dv] fp32 receiving the key-side
  *              responsibilities r_{tjd} (for routing diagnostics).
- *   workspace, ws_bytes: scratch for forms that need it; see
- *              swila_forward_workspace_bytes (0 for the recurrent scan, where
- *              both may be NULL/0).
- *   iters_out: reserved, may be NULL.
+ *   workspace, ws_bytes: device scratch for forms that need it, at least
+ *              swila_forward_workspace_bytes bytes, 16-byte aligned, disjoint
+ *              from every tensor argument (SWILA_ALGO_NEWTON: the predictions
+ *              of the current iterate, overwritten).  Other forms ignore both.
+ *   iters_out: NULL, or a device int32[2] (SWILA_ALGO_NEWTON only; ignored
+ *              otherwise): [0] = the most sweeps any block of columns ran,
+ *              [1] = how many blocks stopped at max_iters without meeting tol
+ *              (0 when tol < 0).  Columns of different output dimensions are
+ *              independent, so each block of them stops on its own test; the
+ *              outputs and W_T are those of each block's last sweep.
  * T == 0 copies state_in (or zeros) to state_out and writes nothing else.
  */
 int swila_forward(const swila_shape *shape, const swila_opts *opts,
@@ -116,7 +142,8 @@ int swila_forward(const swila_shape *shape, const swila_opts *opts,
                   const float *state_in, float *state_out, void *o, float *resp_out,
                   void *workspace, size_t ws_bytes, int32_t *iters_out, void *stream);
 
-/* Workspace bytes swila_forward needs for these options (0 if none). */
+/* Workspace bytes swila_forward needs for these options (0 if none):
+ * SWILA_ALGO_NEWTON needs B*H*J*Dv*(16*ceil(T/16))*4. */
 size_t swila_forward_workspace_bytes(const swila_shape *shape, const swila_opts *opts);
 
 /*

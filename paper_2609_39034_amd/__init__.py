@@ -20,14 +20,16 @@ import os
 
 __all__ = ["forward", "decode_step", "state_init", "state_bytes", "forward_workspace_bytes",
            "version", "library_path", "SwilaError", "F32", "BF16", "ALGO_AUTO",
-           "ALGO_RECURRENT", "ALGO_CHUNK_EXACT"]
+           "ALGO_RECURRENT", "ALGO_CHUNK_EXACT", "ALGO_NEWTON", "FLAG_NEWTON_NO_CLAMP"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB_PATH = os.path.join(_HERE, "libswila.so")
 
 F32, BF16 = 0, 1
-ALGO_AUTO, ALGO_RECURRENT, ALGO_CHUNK_EXACT = 0, 1, 2
-_ALGOS = {"auto": ALGO_AUTO, "recurrent": ALGO_RECURRENT, "chunk": ALGO_CHUNK_EXACT}
+ALGO_AUTO, ALGO_RECURRENT, ALGO_CHUNK_EXACT, ALGO_NEWTON = 0, 1, 2, 3
+_ALGOS = {"auto": ALGO_AUTO, "recurrent": ALGO_RECURRENT, "chunk": ALGO_CHUNK_EXACT,
+          "newton": ALGO_NEWTON}
+FLAG_NEWTON_NO_CLAMP = 1
 
 OK, EINVAL, EUNSUPPORTED, EHIP = 0, -1, -2, -3
 
@@ -135,6 +137,7 @@ def state_bytes(B, H, Dk, Dv, J) -> int:
 
 def forward_workspace_bytes(B, H, T, Dk, Dv, J, *, in_dtype=BF16, out_dtype=None,
                             algo="auto", chunk=0) -> int:
+    """Workspace bytes of swila_forward for this shape and algorithm."""
     opts = Opts(in_dtype, in_dtype if out_dtype is None else out_dtype, _ALGOS[algo], chunk,
                 0, 0.0, 0)
     return load_library().swila_forward_workspace_bytes(ctypes.byref(Shape(B, H, T, Dk, Dv, J)),
@@ -171,7 +174,7 @@ def _layer_shapes(q, v, lb, decode):
 
 def forward(q, k, v, beta_logit, prior_k_logit, prior_q_logit, state_in=None, *,
             state_out=True, o=None, out_dtype=None, resp=False, algo="auto", chunk=0,
-            workspace=None, stream=None):
+            workspace=None, max_iters=0, tol=0.0, clamp=True, iters_out=None, stream=None):
     """Forward over whole sequences (swila_forward).
 
     q, k [B,T,H,Dk]; v [B,T,H,Dv]; logits [B,T,H,J,Dv] (one dtype: float32 or
@@ -180,6 +183,11 @@ def forward(q, k, v, beta_logit, prior_k_logit, prior_q_logit, state_in=None, *,
     float32 tensor to write (may be state_in itself).  o: optional output
     tensor; out_dtype defaults to the input dtype.  resp=True also returns the
     key-side responsibilities [B,T,H,J,Dv] float32.
+    algo: "auto", "recurrent", "chunk" or "newton" (App. D).  For "newton":
+    max_iters (0 = 64), tol (0 = 1e-3, < 0 = exactly max_iters sweeps), clamp
+    (g clamped to [0, 2/|k|^2]), iters_out (None or a device int32 tensor of 2
+    elements: most sweeps of any block, blocks not converged); the workspace
+    is allocated here unless given.
     Returns (o, state_out or None) or (o, state_out, resp).
     """
     torch = _torch()
@@ -213,14 +221,27 @@ def forward(q, k, v, beta_logit, prior_k_logit, prior_q_logit, state_in=None, *,
     r = None
     if resp:
         r = torch.empty((B, T, H, J, Dv), device=q.device, dtype=torch.float32)
-    opts = Opts(code, _dtype_code(o), _ALGOS[algo], int(chunk), 0, 0.0, 0)
+    flags = 0 if clamp else FLAG_NEWTON_NO_CLAMP
+    opts = Opts(code, _dtype_code(o), _ALGOS[algo], int(chunk), int(max_iters), float(tol),
+                flags)
+    shape = Shape(B, H, T, Dk, Dv, J)
+    lib = load_library()
+    if workspace is None:
+        need = lib.swila_forward_workspace_bytes(ctypes.byref(shape), ctypes.byref(opts))
+        if need:
+            workspace = torch.empty(need, device=q.device, dtype=torch.uint8)
     ws_ptr, ws_bytes = None, 0
     if workspace is not None:
+        _dev_tensor(workspace, "workspace")
         ws_ptr, ws_bytes = _ptr(workspace), workspace.numel() * workspace.element_size()
-    _check(load_library().swila_forward(
-        ctypes.byref(Shape(B, H, T, Dk, Dv, J)), ctypes.byref(opts),
+    if iters_out is not None:
+        _dev_tensor(iters_out, "iters_out", torch.int32)
+        if iters_out.numel() < 2:
+            raise ValueError("iters_out needs 2 int32 elements")
+    _check(lib.swila_forward(
+        ctypes.byref(shape), ctypes.byref(opts),
         *[_ptr(t) for t in ins], _ptr(state_in), _ptr(s_out), _ptr(o), _ptr(r),
-        ws_ptr, ws_bytes, None, _stream_handle(stream)))
+        ws_ptr, ws_bytes, _ptr(iters_out), _stream_handle(stream)))
     return (o, s_out, r) if resp else (o, s_out)
 
 

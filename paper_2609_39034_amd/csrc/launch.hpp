@@ -18,6 +18,15 @@ struct LayerArgs {
     bool in_bf16, out_bf16;
 };
 
+// Parameters of the chunkwise quasi-Newton form (App. D).
+struct NewtonArgs {
+    float *pred;        // workspace: predictions of the current iterate, per block
+    int *iters;         // nullptr, or 2 ints: most sweeps of any block, blocks not converged
+    int max_iters;      // sweeps at most (>= 1)
+    float tol;          // stop when the change is <= tol * max(1, |pred|); < 0: max_iters sweeps
+    bool clamp;         // clamp g to [0, 2 / |k_t|^2]
+};
+
 // Token-by-token scan with fp32 state in registers.  Returns the HIP status of
 // the launch; hipErrorInvalidValue if the shape has no instantiation.
 hipError_t launch_scan_direct(const LayerArgs &a, hipStream_t stream);
@@ -25,6 +34,12 @@ hipError_t launch_scan_direct(const LayerArgs &a, hipStream_t stream);
 // Exact chunk scan on the matrix cores, pipelined (one sequential wave plus
 // matrix-core waves); bf16 inputs, T > 0.
 hipError_t launch_scan_pipe(const LayerArgs &a, hipStream_t stream);
+
+// Chunkwise quasi-Newton evaluation (App. D) on the same pipelined kernel;
+// bf16 inputs, T > 0, resp must be nullptr.  na.pred holds
+// newton_workspace_bytes(...) bytes.
+hipError_t launch_newton(const LayerArgs &a, const NewtonArgs &na, hipStream_t stream);
+size_t newton_workspace_bytes(int B, int H, int T, int Dv, int J);
 
 // One-token decode step streaming the state through registers.
 hipError_t launch_decode(const LayerArgs &a, hipStream_t stream);

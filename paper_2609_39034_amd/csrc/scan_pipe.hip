@@ -40,6 +40,23 @@
 // kRing LDS slots; K and Q rows are stored with their 16-byte pieces permuted
 // by row (piece p of row t at slot p ^ (t mod pieces)) so that the 16 lanes
 // reading one column range hit distinct banks.
+//
+// Newton mode (App. D).  The same kernel evaluates the chunkwise quasi-Newton
+// iteration of App. D.1-D.3.  Sweep i linearises the recurrence around the
+// predictions pred^(i)_t = k_t . w^(i)_{t-1} of the previous sweep
+// (eq. jacobian_coeff, eq. effective_input) and solves the linear recurrence
+// eq. linearized exactly, chunk by chunk.  In solve form (per column, the
+// output index d kept):
+//   pred_t = k_t . S_n + sum_{s<t} (k_t . k_s) x_s,   x_t = p_t - g_t pred_t,
+//   S_{n+1} = S_n + sum_s x_s k_s^T,
+// which is the (I - Lambda)^{-1} of eq. aggregate_transition and
+// eq. aggregate_history applied by forward substitution.  The matrix-core
+// schedule above is unchanged; the sequential wave runs the linear step
+// x_t = g_t (pred^(i)_t - pred_t) + beta r delta instead of the E-step.  The
+// predictions of every sweep go to a workspace and are read back, chunk by
+// chunk, by the next sweep.  Each block iterates until the largest change of
+// its predictions is at most tol * max(1, largest prediction), or until
+// max_iters sweeps; outputs and the final state are those of the last sweep.
 #include "device_common.hpp"
 #include "launch.hpp"
 
@@ -79,11 +96,12 @@ struct PCfg {
     static constexpr int KPIECES = kC * DK / 8;   // per K (or Q) chunk
     static constexpr int LPIECES = kC * N / 8;    // per logit tensor chunk
     static constexpr int VPIECES = kC * DB / 8;   // v chunk
+    static constexpr int PPIECES = kC * N / 4;    // fp32 predictions of a chunk (Newton)
     static_assert(N % 16 == 0 && N <= 64 && DB % 8 == 0, "column block");
     static_assert(DB * JP <= 64, "one sequential wave");
 };
 
-template <int DK, int J, int DB>
+template <int DK, int J, int DB, bool NT>
 struct PSmem {
     using C = PCfg<DK, J, DB>;
     uint4 k[kRing][C::KPIECES];
@@ -92,15 +110,17 @@ struct PSmem {
     uint4 lk[kRing][C::LPIECES];
     uint4 lq[kRing][C::LPIECES];
     uint4 v[kRing][C::VPIECES];
-    float beta[2][kC][C::NP];
-    float lks[2][kC][C::NP];   // key-prior logit * log2(e)
-    float vs[2][kC][DB + 4];
+    uint4 pw[NT ? kRing : 1][NT ? C::PPIECES : 1];  // Newton: previous sweep's predictions
+    float beta[2][kC][C::NP];  // exact: beta;  Newton: g (before the clamp)
+    float lks[2][kC][C::NP];   // exact: key-prior logit * log2(e);  Newton: beta r delta
+    float vs[NT ? 1 : 2][kC][DB + 4];
     float pq[2][kC][C::NP];    // query prior
     float g[2][kC][kC + 4];    // K_n K_n^T, for the sequential wave
     float p[2][kC][C::NP];     // chunk-start predictions
     float c[2][kC][C::NP];     // coefficients (column N: idle lanes)
-    float r[2][kC][C::NP];     // responsibilities
+    float r[NT ? 1 : 2][kC][C::NP];  // responsibilities (exact mode)
     float py[2][kC][C::NP];    // pi^q * retrieval
+    int flag;                  // Newton: this sweep met the tolerance
 };
 
 // Four consecutive bf16 (as raw bits) of row t from element i (i % 4 == 0)
@@ -130,7 +150,7 @@ __device__ __forceinline__ uint4 frag32(const uint4 *tile, int tl, int lg, int s
 
 // One wave-wide HBM -> LDS transfer: lane L moves 16 bytes from src to
 // dst + 16 L (dst is the same for the whole wave).
-__device__ __forceinline__ void dma16(const uint16_t *src, uint4 *dst) {
+__device__ __forceinline__ void dma16(const void *src, uint4 *dst) {
     __builtin_amdgcn_global_load_lds((const void __attribute__((address_space(1))) *)src,
                                      (void __attribute__((address_space(3))) *)dst, 16, 0, 0);
 }
@@ -145,10 +165,12 @@ __device__ __forceinline__ int first_for(int base, int mw, int nw) {
 // (K, Q, the three logit tensors, v), dealt round-robin to the matrix-core
 // waves; each tensor has its own loop so its base address stays a scalar.
 // Tokens past T re-read token T - 1 (in range); the recurrence gives them
-// beta = 0.
-template <int DK, int J, int DB>
-__device__ __forceinline__ void issue_chunk(const LayerArgs &a, PSmem<DK, J, DB> &sm, int slot,
-                                            int t0, int b, int h, int d0, int mw, int lane) {
+// beta = 0.  In Newton mode the chunk's predictions from the previous sweep
+// ([kC][N] fp32 at pred + t0 N, the block's workspace) come along.
+template <int DK, int J, int DB, bool NT>
+__device__ __forceinline__ void issue_chunk(const LayerArgs &a, PSmem<DK, J, DB, NT> &sm,
+                                            int slot, int t0, int b, int h, int d0, int mw,
+                                            int lane, const float *pred) {
     using C = PCfg<DK, J, DB>;
     const int T = a.T, H = a.H, Dv = a.Dv;
     constexpr int nk = (C::KPIECES + 63) / 64, nl = (C::LPIECES + 63) / 64;
@@ -196,6 +218,13 @@ __device__ __forceinline__ void issue_chunk(const LayerArgs &a, PSmem<DK, J, DB>
                   sm.v[slot] + part * 64);
         }
     }
+    if constexpr (NT) {
+        constexpr int ib = 2 * nk + 3 * nl + nv, np = (C::PPIECES + 63) / 64;
+        for (int ins = first_for(ib, mw, C::NW); ins < ib + np; ins += C::NW) {
+            const int part = ins - ib, s = part * 64 + lane;
+            if (s < C::PPIECES) dma16(pred + (size_t)t0 * C::N + 4 * s, sm.pw[slot] + part * 64);
+        }
+    }
 }
 
 __device__ __forceinline__ float bf16_at(const uint4 *base, int idx) {
@@ -215,11 +244,11 @@ __device__ __forceinline__ void pipe_coords(int id, int ndb, int nheads, int &db
     }
 }
 
-template <int DK, int J, int DB>
-__global__ __launch_bounds__(320) void scan_pipe_kernel(LayerArgs a) {
+template <int DK, int J, int DB, bool NT>
+__global__ __launch_bounds__(320) void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
     using C = PCfg<DK, J, DB>;
     constexpr int IT = C::IT, N = C::N, NW = C::NW, JP = C::JP;
-    __shared__ PSmem<DK, J, DB> sm;
+    __shared__ PSmem<DK, J, DB, NT> sm;
 
     const int tid = threadIdx.x;
     const int w = tid / 64, lane = tid % 64;
@@ -233,21 +262,31 @@ __global__ __launch_bounds__(320) void scan_pipe_kernel(LayerArgs a) {
     // The sequential wave shares a SIMD with a matrix-core wave; its chain of
     // dependent steps is the critical path, so it issues first.
     if (seq) __builtin_amdgcn_s_setprio(3);
+    // Newton mode: this block's predictions, [NCH * kC][N] fp32
+    float *const pred = NT ? na.pred + ((size_t)hh * (Dv / DB) + db) * NCH * kC * N : nullptr;
 
     // ---- matrix-core wave state: W^T tile rows 16 it + 4 lg + r, column col
     const int col = 16 * (seq ? 0 : w) + tl;
     const int jc = col / DB, dc = d0 + col % DB;
     const size_t sbase = (((size_t)b * H + h) * J + jc) * DK * Dv + dc;
     floatx4 W[IT];
+    auto load_state = [&]() {
 #pragma unroll
-    for (int it = 0; it < IT; ++it) W[it] = floatx4{0.f, 0.f, 0.f, 0.f};
-    if (!seq && a.state_in) {
+        for (int it = 0; it < IT; ++it) W[it] = floatx4{0.f, 0.f, 0.f, 0.f};
+        if (!seq && a.state_in) {
+            // Newton mode reloads W_0 every sweep: an opaque copy of the row
+            // stride keeps the compiler from holding all IT * 4 addresses in
+            // registers across the sweeps.
+            int dv = Dv;
+            asm volatile("" : "+s"(dv));
+            const float *src = a.state_in + sbase + (size_t)(4 * lg) * dv;
 #pragma unroll
-        for (int it = 0; it < IT; ++it)
+            for (int it = 0; it < IT; ++it)
 #pragma unroll
-            for (int r = 0; r < 4; ++r)
-                W[it][r] = a.state_in[sbase + (size_t)(16 * it + 4 * lg + r) * Dv];
-    }
+                for (int r = 0; r < 4; ++r) W[it][r] = src[(size_t)(16 * it + r) * dv];
+        }
+    };
+    load_state();
     floatx4 Yacc = {0.f, 0.f, 0.f, 0.f}, Xacc = Yacc;
     short4v chi = {0, 0, 0, 0}, clo = chi, ghi = chi, glo = chi;
 
@@ -323,19 +362,58 @@ __global__ __launch_bounds__(320) void scan_pipe_kernel(LayerArgs a) {
     };
     // derived inputs of chunk m (ring slot rs, parity pr) for the sequential wave
     auto prep_seq_inputs = [&](int m, int rs, int pr) {
+        if constexpr (!NT) {
 #pragma unroll
-        for (int it = 0; it < (kC * N + C::NMT - 1) / C::NMT; ++it) {
-            const int e = tid + it * C::NMT;
-            if (kC * N % C::NMT != 0 && e >= kC * N) break;
-            const int t = e / N, cc = e % N;
-            const bool ok = m * kC + t < T;
-            sm.beta[pr][t][cc] = ok ? rcp_fast(1.0f + exp_fast(-bf16_at(sm.lb[rs], e))) : 0.f;
-            sm.lks[pr][t][cc] = bf16_at(sm.lk[rs], e) * kLog2e;
-        }
+            for (int it = 0; it < (kC * N + C::NMT - 1) / C::NMT; ++it) {
+                const int e = tid + it * C::NMT;
+                if (kC * N % C::NMT != 0 && e >= kC * N) break;
+                const int t = e / N, cc = e % N;
+                const bool ok = m * kC + t < T;
+                sm.beta[pr][t][cc] = ok ? rcp_fast(1.0f + exp_fast(-bf16_at(sm.lb[rs], e))) : 0.f;
+                sm.lks[pr][t][cc] = bf16_at(sm.lk[rs], e) * kLog2e;
+            }
 #pragma unroll
-        for (int it = 0; it < (kC * DB + C::NMT - 1) / C::NMT; ++it) {
-            const int e = tid + it * C::NMT;
-            if (kC * DB % C::NMT == 0 || e < kC * DB) sm.vs[pr][e / DB][e % DB] = bf16_at(sm.v[rs], e);
+            for (int it = 0; it < (kC * DB + C::NMT - 1) / C::NMT; ++it) {
+                const int e = tid + it * C::NMT;
+                if (kC * DB % C::NMT == 0 || e < kC * DB)
+                    sm.vs[pr][e / DB][e % DB] = bf16_at(sm.v[rs], e);
+            }
+        } else {
+            // Linearisation around the previous sweep's predictions (App. D.2),
+            // per (t, dl) over the J components: delta, r (eq. responsibility),
+            // g (eq. jacobian_coeff) and the part beta r delta of the effective
+            // input (eq. effective_input); the sequential wave adds g pred^(i).
+            const float *po = reinterpret_cast<const float *>(sm.pw[rs]);
+#pragma unroll
+            for (int it = 0; it < (kC * DB + C::NMT - 1) / C::NMT; ++it) {
+                const int e = tid + it * C::NMT;
+                if (kC * DB % C::NMT != 0 && e >= kC * DB) break;
+                const int t = e / DB, dl = e % DB;
+                const bool ok = m * kC + t < T;
+                const float vv = bf16_at(sm.v[rs], e);
+                float dj[J], xj[J], mx = -INFINITY;
+#pragma unroll
+                for (int j = 0; j < J; ++j) {
+                    dj[j] = vv - po[t * N + j * DB + dl];
+                    xj[j] = kLog2e * fmaf(-0.5f * dj[j], dj[j], bf16_at(sm.lk[rs], t * N + j * DB + dl));
+                    mx = fmaxf(mx, xj[j]);
+                }
+                float z = 0.f;
+#pragma unroll
+                for (int j = 0; j < J; ++j) {
+                    xj[j] = __builtin_amdgcn_exp2f(xj[j] - mx);
+                    z += xj[j];
+                }
+                const float iz = rcp_fast(z);
+#pragma unroll
+                for (int j = 0; j < J; ++j) {
+                    const float r = xj[j] * iz;
+                    const float br = sigmoid(bf16_at(sm.lb[rs], t * N + j * DB + dl)) * r;
+                    const float d = dj[j];
+                    sm.beta[pr][t][j * DB + dl] = ok ? br * fmaf(-d * d, 1.f - r, 1.f) : 0.f;
+                    sm.lks[pr][t][j * DB + dl] = ok ? br * d : 0.f;
+                }
+            }
         }
     };
     // pi^q of chunk m: softmax over j of the query-prior logits, per (t, dl)
@@ -377,11 +455,13 @@ __global__ __launch_bounds__(320) void scan_pipe_kernel(LayerArgs a) {
         }
     };
     auto store_resp = [&](int m, int pr) {
-        for (int e = tid; e < kC * N; e += C::NMT) {
-            const int t = e / N, cc = e % N;
-            if (m * kC + t < T)
-                a.resp[(((size_t)(b * T + m * kC + t) * H + h) * J + cc / DB) * Dv + d0 + cc % DB] =
-                    sm.r[pr][t][cc];
+        if constexpr (!NT) {
+            for (int e = tid; e < kC * N; e += C::NMT) {
+                const int t = e / N, cc = e % N;
+                if (m * kC + t < T)
+                    a.resp[(((size_t)(b * T + m * kC + t) * H + h) * J + cc / DB) * Dv + d0 +
+                           cc % DB] = sm.r[pr][t][cc];
+            }
         }
     };
     // W += K_m^T C_m and Y += tril(A_m) C_m (C_m split in chi/clo); then
@@ -416,169 +496,308 @@ __global__ __launch_bounds__(320) void scan_pipe_kernel(LayerArgs a) {
             sm.py[pr][4 * lg + r][col] = Yacc[r] * sm.pq[pr][4 * lg + r][col];
     };
 
-    // ---------------- prologue: chunks 0 and 1 into the ring; P_0, G_0
-    if (!seq) {
-        issue_chunk<DK, J, DB>(a, sm, 0, 0, b, h, d0, w, lane);
-        if (NCH > 1) issue_chunk<DK, J, DB>(a, sm, 1, kC, b, h, d0, w, lane);
-        wait_vm();
-    }
-    block_sync_lds();
-    if (!seq) {
-        prep_seq_inputs(0, 0, 0);
-        bf16x8 whi[IT / 2 > 0 ? IT / 2 : 1], wlo[IT / 2 > 0 ? IT / 2 : 1];
-        short4v w16hi, w16lo;
-        split_state(whi, wlo, w16hi, w16lo);
-        const floatx4 P0 = tile_times_state(sm.k[0], floatx4{0.f, 0.f, 0.f, 0.f}, whi, wlo,
-                                            w16hi, w16lo);
-#pragma unroll
-        for (int r = 0; r < 4; ++r) sm.p[0][4 * lg + r][col] = P0[r];
-        if (w == 0) {
-            const floatx4 G0 = gram(sm.k[0], sm.k[0]);
-#pragma unroll
-            for (int r = 0; r < 4; ++r) sm.g[0][4 * lg + r][tl] = G0[r];
-        }
-    }
-    block_sync_lds();
-
-    for (int n = 0; n < NCH; ++n) {
-        const int pr = n & 1, rs = n % kRing;
-        if (seq) {
-            // ---- B: the token recurrence of chunk n
-            float P[kC], vv[kC], lkv[kC], bev[kC];
-#pragma unroll
-            for (int t = 0; t < kC; ++t) {
-                P[t] = sm.p[pr][t][bcol];
-                vv[t] = sm.vs[pr][t][bdl];
-                lkv[t] = bact ? sm.lks[pr][t][bcol] : -INFINITY;
-                bev[t] = bact ? sm.beta[pr][t][bcol] : 0.f;
-            }
-            float grow[kC];
-#pragma unroll
-            for (int u = 1; u < kC; ++u) grow[u] = sm.g[pr][0][u];
-#pragma unroll
-            for (int t = 0; t < kC; ++t) {
-                float gnext[kC];
-#pragma unroll
-                for (int u = t + 2; u < kC; ++u) gnext[u] = sm.g[pr][t + 1][u];
-                const float delta = vv[t] - P[t];
-                const float bd = bev[t] * delta;
-                const float e = fmaf(-0.5f * kLog2e * delta, delta, lkv[t]);
-                const float mx = group_max<JP>(e);
-                const float ex = __builtin_amdgcn_exp2f(e - mx);
-                const float z = group_sum<JP>(ex);
-                const float r = ex * rcp_fast(z);
-                const float c = bd * r;
-#pragma unroll
-                for (int u = t + 1; u < kC; ++u) P[u] = fmaf(grow[u], c, P[u]);
-                sm.c[pr][t][bsto] = c;
-                sm.r[pr][t][bsto] = r;
-#pragma unroll
-                for (int u = t + 2; u < kC; ++u) grow[u] = gnext[u];
-            }
-            block_sync_lds();   // e(n): C_n published
-            block_sync_lds();   // i(n+1): P_{n+1} ready
-            continue;
-        }
-
-        // ---- matrix-core waves, while the sequential wave runs chunk n
-        if (n >= 1) {
-            finish_chunk(n - 1);                 // S_n, pi^q Y_{n-1}
-            if (a.resp) store_resp(n - 1, (n - 1) & 1);
-        }
-        if (n >= 2) store_output(n - 2, n & 1);  // (n - 2) & 1 == n & 1
-        {
+    if constexpr (NT) {
+        // Iterate 0 (the initial guess w_t = W_0 for every t): pred_t = k_t . W_0,
+        // straight from HBM rows of K, chunk by chunk.
+        if (!seq) {
             bf16x8 whi[IT / 2 > 0 ? IT / 2 : 1], wlo[IT / 2 > 0 ? IT / 2 : 1];
             short4v w16hi, w16lo;
             split_state(whi, wlo, w16hi, w16lo);
-            Yacc = tile_times_state(sm.q[rs], floatx4{0.f, 0.f, 0.f, 0.f}, whi, wlo, w16hi, w16lo);
-            if (n + 1 < NCH)
-                Xacc = tile_times_state(sm.k[(n + 1) % kRing], floatx4{0.f, 0.f, 0.f, 0.f}, whi,
-                                        wlo, w16hi, w16lo);
+            const uint16_t *kb = static_cast<const uint16_t *>(a.k);
+            for (int n = 0; n < NCH; ++n) {
+                const int tc = min(n * kC + tl, T - 1);
+                const uint16_t *row = kb + (((size_t)b * T + tc) * H + h) * DK;
+                floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+                if constexpr (DK == 16) {
+                    const short4v av =
+                        __builtin_bit_cast(short4v, *reinterpret_cast<const uint2 *>(row + 4 * lg));
+                    acc = mfma16(av, w16hi, acc);
+                    acc = mfma16(av, w16lo, acc);
+                } else {
+#pragma unroll
+                    for (int s = 0; s < DK / 32; ++s) {
+                        const uint2 x0 = *reinterpret_cast<const uint2 *>(row + 32 * s + 4 * lg);
+                        const uint2 x1 = *reinterpret_cast<const uint2 *>(row + 32 * s + 16 + 4 * lg);
+                        const bf16x8 av = __builtin_bit_cast(bf16x8, make_uint4(x0.x, x0.y, x1.x, x1.y));
+                        acc = mfma32(av, whi[s], acc);
+                        acc = mfma32(av, wlo[s], acc);
+                    }
+                }
+#pragma unroll
+                for (int r = 0; r < 4; ++r) pred[(size_t)(n * kC + 4 * lg + r) * N + col] = acc[r];
+            }
+            wait_vm();   // stores done before any wave reads them back
         }
-        if (n + 1 < NCH) {
-            // G'_n = K_{n+1} K_n^T as the A operand of G'_n C_n: the accumulator
-            // layout of K_n K_{n+1}^T, split in registers
-            const floatx4 gt = gram(sm.k[rs], sm.k[(n + 1) % kRing]);
+        block_sync_lds();
+    }
+
+    // The two roles run separate loops with the same barriers, so that the
+    // sequential wave's registers and the matrix-core waves' do not add up.
+    if (seq) {
+        int sweeps = 0;
+        bool done = false;
+        while (!done) {
+            ++sweeps;
+            float dmax = 0.f, pmax = 0.f;   // Newton: largest change, largest prediction
+            block_sync_lds();               // prologue: ring filled
+            block_sync_lds();               // prologue: P_0, G_0
+            for (int n = 0; n < NCH; ++n) {
+                const int pr = n & 1;
+                float grow[kC];
+#pragma unroll
+                for (int u = 1; u < kC; ++u) grow[u] = sm.g[pr][0][u];
+                if constexpr (!NT) {
+                    // ---- B: the token recurrence of chunk n
+                    float P[kC], vv[kC], lkv[kC], bev[kC];
+#pragma unroll
+                    for (int t = 0; t < kC; ++t) {
+                        P[t] = sm.p[pr][t][bcol];
+                        vv[t] = sm.vs[pr][t][bdl];
+                        lkv[t] = bact ? sm.lks[pr][t][bcol] : -INFINITY;
+                        bev[t] = bact ? sm.beta[pr][t][bcol] : 0.f;
+                    }
+#pragma unroll
+                    for (int t = 0; t < kC; ++t) {
+                        float gnext[kC];
+#pragma unroll
+                        for (int u = t + 2; u < kC; ++u) gnext[u] = sm.g[pr][t + 1][u];
+                        const float delta = vv[t] - P[t];
+                        const float bd = bev[t] * delta;
+                        const float e = fmaf(-0.5f * kLog2e * delta, delta, lkv[t]);
+                        const float mx = group_max<JP>(e);
+                        const float ex = __builtin_amdgcn_exp2f(e - mx);
+                        const float z = group_sum<JP>(ex);
+                        const float r = ex * rcp_fast(z);
+                        const float c = bd * r;
+#pragma unroll
+                        for (int u = t + 1; u < kC; ++u) P[u] = fmaf(grow[u], c, P[u]);
+                        sm.c[pr][t][bsto] = c;
+                        sm.r[pr][t][bsto] = r;
+#pragma unroll
+                        for (int u = t + 2; u < kC; ++u) grow[u] = gnext[u];
+                    }
+                } else {
+                    // ---- B: forward substitution of the linearised recurrence
+                    // (eq. linearized) over chunk n; g clamped to [0, 2 / |k_t|^2]
+                    // unless disabled
+                    const float *po = reinterpret_cast<const float *>(sm.pw[n % kRing]);
+                    float P[kC], gc[kC], bb[kC], pold[kC];
+                    const float glo_t = na.clamp ? 0.f : -INFINITY;
+#pragma unroll
+                    for (int t = 0; t < kC; ++t) {
+                        P[t] = sm.p[pr][t][bcol];
+                        const float ghi_t = na.clamp ? 2.f * rcp_fast(sm.g[pr][t][t]) : INFINITY;
+                        gc[t] = fminf(fmaxf(sm.beta[pr][t][bcol], glo_t), ghi_t);
+                        bb[t] = sm.lks[pr][t][bcol];
+                        pold[t] = po[t * N + bcol];
+                    }
+#pragma unroll
+                    for (int t = 0; t < kC; ++t) {
+                        float gnext[kC];
+#pragma unroll
+                        for (int u = t + 2; u < kC; ++u) gnext[u] = sm.g[pr][t + 1][u];
+                        const float pt = P[t];
+                        const float x = fmaf(gc[t], pold[t] - pt, bb[t]);
+#pragma unroll
+                        for (int u = t + 1; u < kC; ++u) P[u] = fmaf(grow[u], x, P[u]);
+                        sm.c[pr][t][bsto] = x;
+                        const int tok = n * kC + t;
+                        if (bact) {
+                            pred[(size_t)tok * N + bcol] = pt;
+                            if (tok < T) {
+                                dmax = fmaxf(dmax, fabsf(pt - pold[t]));
+                                pmax = fmaxf(pmax, fabsf(pt));
+                            }
+                        }
+#pragma unroll
+                        for (int u = t + 2; u < kC; ++u) grow[u] = gnext[u];
+                    }
+                }
+                block_sync_lds();   // e(n): C_n published
+                block_sync_lds();   // i(n+1): P_{n+1} ready
+            }
+            block_sync_lds();       // epilogue
+            if constexpr (NT) {
+                // stopping rule, decided here for the whole block
+#pragma unroll
+                for (int off = 32; off >= 1; off >>= 1) {
+                    dmax = fmaxf(dmax, __shfl_xor(dmax, off));
+                    pmax = fmaxf(pmax, __shfl_xor(pmax, off));
+                }
+                if (lane == 0)
+                    sm.flag = (na.tol >= 0.f && dmax <= na.tol * fmaxf(1.f, pmax)) ? 1 : 0;
+                wait_vm();          // this sweep's predictions are in memory
+                block_sync_lds();
+                done = sm.flag != 0 || sweeps >= na.max_iters;   // as the matrix-core waves decide
+            } else {
+                done = true;
+            }
+        }
+        return;
+    }
+
+    int sweeps = 0;
+    bool done = false;
+    while (!done) {
+        ++sweeps;
+        if (NT && sweeps > 1) {
+            load_state();
+            Yacc = floatx4{0.f, 0.f, 0.f, 0.f};
+        }
+        // ---------------- prologue: chunks 0 and 1 into the ring; P_0, G_0
+        // (t0 is an opaque zero so that, in Newton mode, the compiler does not
+        // hoist these transfers' addresses out of the sweep loop and hold them)
+        int t0 = 0;
+        asm volatile("" : "+s"(t0));
+        issue_chunk<DK, J, DB, NT>(a, sm, 0, t0, b, h, d0, w, lane, pred);
+        if (NCH > 1) issue_chunk<DK, J, DB, NT>(a, sm, 1, t0 + kC, b, h, d0, w, lane, pred);
+        wait_vm();
+        block_sync_lds();
+        {
+            prep_seq_inputs(0, 0, 0);
+            bf16x8 whi[IT / 2 > 0 ? IT / 2 : 1], wlo[IT / 2 > 0 ? IT / 2 : 1];
+            short4v w16hi, w16lo;
+            split_state(whi, wlo, w16hi, w16lo);
+            const floatx4 P0 = tile_times_state(sm.k[0], floatx4{0.f, 0.f, 0.f, 0.f}, whi, wlo,
+                                                w16hi, w16lo);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) sm.p[0][4 * lg + r][col] = P0[r];
+            if (w == 0) {
+                const floatx4 G0 = gram(sm.k[0], sm.k[0]);
+#pragma unroll
+                for (int r = 0; r < 4; ++r) sm.g[0][4 * lg + r][tl] = G0[r];
+            }
+        }
+        block_sync_lds();
+
+        for (int n = 0; n < NCH; ++n) {
+            const int pr = n & 1, rs = n % kRing;
+            // ---- matrix-core waves, while the sequential wave runs chunk n
+            if (n >= 1) {
+                finish_chunk(n - 1);                 // S_n, pi^q Y_{n-1}
+                if (a.resp) store_resp(n - 1, (n - 1) & 1);
+            }
+            if (n >= 2) store_output(n - 2, n & 1);  // (n - 2) & 1 == n & 1
+            {
+                bf16x8 whi[IT / 2 > 0 ? IT / 2 : 1], wlo[IT / 2 > 0 ? IT / 2 : 1];
+                short4v w16hi, w16lo;
+                split_state(whi, wlo, w16hi, w16lo);
+                Yacc = tile_times_state(sm.q[rs], floatx4{0.f, 0.f, 0.f, 0.f}, whi, wlo, w16hi,
+                                        w16lo);
+                if (n + 1 < NCH)
+                    Xacc = tile_times_state(sm.k[(n + 1) % kRing], floatx4{0.f, 0.f, 0.f, 0.f},
+                                            whi, wlo, w16hi, w16lo);
+            }
+            if (n + 1 < NCH) {
+                // G'_n = K_{n+1} K_n^T as the A operand of G'_n C_n: the accumulator
+                // layout of K_n K_{n+1}^T, split in registers
+                const floatx4 gt = gram(sm.k[rs], sm.k[(n + 1) % kRing]);
+#pragma unroll
+                for (int m = 0; m < 4; ++m) {
+                    __bf16 hi, lo;
+                    split(gt[m], hi, lo);
+                    ghi[m] = bf16_bits(hi);
+                    glo[m] = bf16_bits(lo);
+                }
+            }
+            if (w == (1 % NW) && n + 1 < NCH) {
+                const floatx4 g1 = gram(sm.k[(n + 1) % kRing], sm.k[(n + 1) % kRing]);
+#pragma unroll
+                for (int r = 0; r < 4; ++r) sm.g[pr ^ 1][4 * lg + r][tl] = g1[r];
+            }
+            prep_query_prior(rs, pr);
+            if (n + 1 < NCH) prep_seq_inputs(n + 1, (n + 1) % kRing, pr ^ 1);
+            if (n + 2 < NCH)
+                issue_chunk<DK, J, DB, NT>(a, sm, (n + 2) % kRing, (n + 2) * kC, b, h, d0, w, lane,
+                                           pred);
+            block_sync_lds();   // e(n): C_n published (and G'_n)
+
+            // ---- P_{n+1} = X_{n+1} + G'_n C_n
 #pragma unroll
             for (int m = 0; m < 4; ++m) {
                 __bf16 hi, lo;
-                split(gt[m], hi, lo);
-                ghi[m] = bf16_bits(hi);
-                glo[m] = bf16_bits(lo);
+                split(sm.c[pr][4 * lg + m][col], hi, lo);
+                chi[m] = bf16_bits(hi);
+                clo[m] = bf16_bits(lo);
             }
-        }
-        if (w == (1 % NW) && n + 1 < NCH) {
-            const floatx4 g1 = gram(sm.k[(n + 1) % kRing], sm.k[(n + 1) % kRing]);
+            if (n + 1 < NCH) {
+                Xacc = mfma16(ghi, chi, Xacc);
+                Xacc = mfma16(ghi, clo, Xacc);
+                Xacc = mfma16(glo, chi, Xacc);
 #pragma unroll
-            for (int r = 0; r < 4; ++r) sm.g[pr ^ 1][4 * lg + r][tl] = g1[r];
+                for (int r = 0; r < 4; ++r) sm.p[pr ^ 1][4 * lg + r][col] = Xacc[r];
+            }
+            wait_vm();          // chunk n+2 has landed in LDS
+            block_sync_lds();   // i(n+1)
         }
-        prep_query_prior(rs, pr);
-        if (n + 1 < NCH) prep_seq_inputs(n + 1, (n + 1) % kRing, pr ^ 1);
-        if (n + 2 < NCH) issue_chunk<DK, J, DB>(a, sm, (n + 2) % kRing, (n + 2) * kC, b, h, d0, w, lane);
-        block_sync_lds();   // e(n): C_n published (and G'_n)
 
-        // ---- P_{n+1} = X_{n+1} + G'_n C_n
-#pragma unroll
-        for (int m = 0; m < 4; ++m) {
-            __bf16 hi, lo;
-            split(sm.c[pr][4 * lg + m][col], hi, lo);
-            chi[m] = bf16_bits(hi);
-            clo[m] = bf16_bits(lo);
-        }
-        if (n + 1 < NCH) {
-            Xacc = mfma16(ghi, chi, Xacc);
-            Xacc = mfma16(ghi, clo, Xacc);
-            Xacc = mfma16(glo, chi, Xacc);
-#pragma unroll
-            for (int r = 0; r < 4; ++r) sm.p[pr ^ 1][4 * lg + r][col] = Xacc[r];
-        }
-        wait_vm();          // chunk n+2 has landed in LDS
-        block_sync_lds();   // i(n+1)
-    }
-
-    // ---------------- epilogue: last state update and the last two outputs
-    if (!seq) {
+        // ---------------- epilogue: last state update and the last two outputs
         finish_chunk(NCH - 1);
         if (a.resp) store_resp(NCH - 1, (NCH - 1) & 1);
         if (NCH >= 2) store_output(NCH - 2, NCH & 1);
-    }
-    block_sync_lds();
-    if (!seq) {
+        block_sync_lds();
         store_output(NCH - 1, (NCH - 1) & 1);
-        if (a.state_out) {
-#pragma unroll
-            for (int it = 0; it < IT; ++it)
-#pragma unroll
-                for (int r = 0; r < 4; ++r)
-                    a.state_out[sbase + (size_t)(16 * it + 4 * lg + r) * Dv] = W[it][r];
+        if constexpr (NT) {
+            block_sync_lds();   // the sequential wave has set the stopping flag
+            const bool met = sm.flag != 0;
+            done = met || sweeps >= na.max_iters;
+            if (done && tid == 0 && na.iters) {
+                atomicMax(na.iters, sweeps);
+                if (!met && na.tol >= 0.f) atomicAdd(na.iters + 1, 1);
+            }
+        } else {
+            done = true;
         }
+    }
+    if (a.state_out) {
+#pragma unroll
+        for (int it = 0; it < IT; ++it)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+                a.state_out[sbase + (size_t)(16 * it + 4 * lg + r) * Dv] = W[it][r];
     }
 }
 
-template <int DK, int J, int DB>
-hipError_t launch_cfg(const LayerArgs &a, hipStream_t stream) {
+__global__ void int_fill_kernel(int *p, int n, int value) {
+    if ((int)threadIdx.x < n) p[threadIdx.x] = value;
+}
+
+template <int DK, int J, int DB, bool NT>
+hipError_t launch_cfg(const LayerArgs &a, const NewtonArgs &na, hipStream_t stream) {
     using C = PCfg<DK, J, DB>;
-    static_assert(sizeof(PSmem<DK, J, DB>) <= 160 * 1024, "LDS");
+    static_assert(sizeof(PSmem<DK, J, DB, NT>) <= 160 * 1024, "LDS");
     const long blocks = (long)(a.Dv / DB) * a.H * a.B;
-    hipLaunchKernelGGL((scan_pipe_kernel<DK, J, DB>), dim3((unsigned)blocks), dim3(C::NT), 0,
-                       stream, a);
+    hipLaunchKernelGGL((scan_pipe_kernel<DK, J, DB, NT>), dim3((unsigned)blocks), dim3(C::NT), 0,
+                       stream, a, na);
     return hipGetLastError();
 }
 
-template <int DK>
-hipError_t launch_dk(const LayerArgs &a, hipStream_t stream) {
+template <int DK, bool NT>
+hipError_t launch_dk(const LayerArgs &a, const NewtonArgs &na, hipStream_t stream) {
     // DB = min(Dv, 64 / J'): at most 64 columns, one wave of sequential lanes
     switch (a.J) {
         case 1:
-            if (a.Dv >= 64) return launch_cfg<DK, 1, 64>(a, stream);
-            if (a.Dv == 32) return launch_cfg<DK, 1, 32>(a, stream);
-            return launch_cfg<DK, 1, 16>(a, stream);
+            if (a.Dv >= 64) return launch_cfg<DK, 1, 64, NT>(a, na, stream);
+            if (a.Dv == 32) return launch_cfg<DK, 1, 32, NT>(a, na, stream);
+            return launch_cfg<DK, 1, 16, NT>(a, na, stream);
         case 2:
-            if (a.Dv >= 32) return launch_cfg<DK, 2, 32>(a, stream);
-            return launch_cfg<DK, 2, 16>(a, stream);
-        case 3: return launch_cfg<DK, 3, 16>(a, stream);
-        case 4: return launch_cfg<DK, 4, 16>(a, stream);
-        case 8: return launch_cfg<DK, 8, 8>(a, stream);
+            if (a.Dv >= 32) return launch_cfg<DK, 2, 32, NT>(a, na, stream);
+            return launch_cfg<DK, 2, 16, NT>(a, na, stream);
+        case 3: return launch_cfg<DK, 3, 16, NT>(a, na, stream);
+        case 4: return launch_cfg<DK, 4, 16, NT>(a, na, stream);
+        case 8: return launch_cfg<DK, 8, 8, NT>(a, na, stream);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+template <bool NT>
+hipError_t launch_mode(const LayerArgs &a, const NewtonArgs &na, hipStream_t stream) {
+    if (!a.in_bf16 || a.T <= 0) return hipErrorInvalidValue;
+    switch (a.Dk) {
+        case 16: return launch_dk<16, NT>(a, na, stream);
+        case 32: return launch_dk<32, NT>(a, na, stream);
+        case 64: return launch_dk<64, NT>(a, na, stream);
+        case 128: return launch_dk<128, NT>(a, na, stream);
         default: return hipErrorInvalidValue;
     }
 }
@@ -586,14 +805,22 @@ hipError_t launch_dk(const LayerArgs &a, hipStream_t stream) {
 }  // namespace
 
 hipError_t launch_scan_pipe(const LayerArgs &a, hipStream_t stream) {
-    if (!a.in_bf16 || a.T <= 0) return hipErrorInvalidValue;
-    switch (a.Dk) {
-        case 16: return launch_dk<16>(a, stream);
-        case 32: return launch_dk<32>(a, stream);
-        case 64: return launch_dk<64>(a, stream);
-        case 128: return launch_dk<128>(a, stream);
-        default: return hipErrorInvalidValue;
+    return launch_mode<false>(a, NewtonArgs{}, stream);
+}
+
+size_t newton_workspace_bytes(int B, int H, int T, int Dv, int J) {
+    const size_t tpad = (size_t)((T + kC - 1) / kC) * kC;
+    return (size_t)B * H * J * Dv * tpad * sizeof(float);
+}
+
+hipError_t launch_newton(const LayerArgs &a, const NewtonArgs &na, hipStream_t stream) {
+    if (!na.pred || na.max_iters < 1) return hipErrorInvalidValue;
+    if (na.iters) {
+        hipLaunchKernelGGL(int_fill_kernel, dim3(1), dim3(64), 0, stream, na.iters, 2, 0);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
     }
+    return launch_mode<true>(a, na, stream);
 }
 
 }  // namespace swila

@@ -47,11 +47,20 @@ int check_opts(const swila_opts *o) {
     if (o->out_dtype != SWILA_F32 && o->out_dtype != SWILA_BF16)
         return fail(SWILA_EINVAL, "out_dtype %d is not SWILA_F32 or SWILA_BF16", o->out_dtype);
     if (o->algo != SWILA_ALGO_AUTO && o->algo != SWILA_ALGO_RECURRENT &&
-        o->algo != SWILA_ALGO_CHUNK_EXACT)
+        o->algo != SWILA_ALGO_CHUNK_EXACT && o->algo != SWILA_ALGO_NEWTON)
         return fail(SWILA_EUNSUPPORTED, "algo %d is not available", o->algo);
     if (o->algo == SWILA_ALGO_CHUNK_EXACT && o->in_dtype != SWILA_BF16)
         return fail(SWILA_EUNSUPPORTED, "SWILA_ALGO_CHUNK_EXACT needs bf16 inputs");
+    if (o->algo == SWILA_ALGO_NEWTON && o->in_dtype != SWILA_BF16)
+        return fail(SWILA_EUNSUPPORTED, "SWILA_ALGO_NEWTON needs bf16 inputs");
     if (o->chunk < 0) return fail(SWILA_EINVAL, "chunk %d < 0", o->chunk);
+    if ((o->algo == SWILA_ALGO_CHUNK_EXACT || o->algo == SWILA_ALGO_NEWTON) && o->chunk != 0 &&
+        o->chunk != 16)
+        return fail(SWILA_EUNSUPPORTED, "chunk %d: the chunked forms use 16 (or 0)", o->chunk);
+    if (o->max_iters < 0) return fail(SWILA_EINVAL, "max_iters %d < 0", o->max_iters);
+    if (o->tol != o->tol) return fail(SWILA_EINVAL, "tol is NaN");
+    if (o->flags & ~(uint32_t)SWILA_FLAG_NEWTON_NO_CLAMP)
+        return fail(SWILA_EINVAL, "unknown flags 0x%x", o->flags);
     return SWILA_OK;
 }
 
@@ -159,9 +168,9 @@ int swila_state_init(const swila_shape *shape, float *state, const float *src, v
 }
 
 size_t swila_forward_workspace_bytes(const swila_shape *shape, const swila_opts *opts) {
-    (void)shape;
-    (void)opts;
-    return 0;
+    if (!shape || !opts || opts->algo != SWILA_ALGO_NEWTON) return 0;
+    if (shape->B < 1 || shape->H < 1 || shape->T < 1 || shape->Dv < 1 || shape->J < 1) return 0;
+    return swila::newton_workspace_bytes(shape->B, shape->H, shape->T, shape->Dv, shape->J);
 }
 
 int swila_forward(const swila_shape *shape, const swila_opts *opts, const void *q, const void *k,
@@ -170,19 +179,55 @@ int swila_forward(const swila_shape *shape, const swila_opts *opts, const void *
                   float *resp_out, void *workspace, size_t ws_bytes, int32_t *iters_out,
                   void *stream) {
     clear_error();
-    (void)workspace;
-    (void)ws_bytes;
-    (void)iters_out;
     swila::LayerArgs a;
     int rc = prepare(shape, opts, false, q, k, v, beta_logit, prior_k_logit, prior_q_logit,
                      state_in, state_out, o, resp_out, &a);
     if (rc) return rc;
     hipStream_t st = static_cast<hipStream_t>(stream);
+    const bool newton = opts->algo == SWILA_ALGO_NEWTON;
+    if (newton && shape->T > 0) {
+        if (resp_out)
+            return fail(SWILA_EUNSUPPORTED, "resp_out is not produced by SWILA_ALGO_NEWTON");
+        const size_t need = swila_forward_workspace_bytes(shape, opts);
+        if (!workspace) return fail(SWILA_EINVAL, "SWILA_ALGO_NEWTON needs a workspace");
+        if (reinterpret_cast<uintptr_t>(workspace) % 16)
+            return fail(SWILA_EINVAL, "workspace is not 16-byte aligned");
+        if (ws_bytes < need)
+            return fail(SWILA_EINVAL, "workspace holds %zu bytes, %zu needed", ws_bytes, need);
+        if (iters_out && reinterpret_cast<uintptr_t>(iters_out) % 4)
+            return fail(SWILA_EINVAL, "iters_out is not 4-byte aligned");
+        const size_t B = shape->B, H = shape->H, T = shape->T, Dk = shape->Dk, Dv = shape->Dv,
+                     J = shape->J;
+        const size_t ie = 2, oe = opts->out_dtype == SWILA_BF16 ? 2 : 4;
+        const Span ws{"workspace", workspace, need}, it{"iters_out", iters_out, 8};
+        const Span all[] = {
+            {"q", q, B * T * H * Dk * ie},          {"k", k, B * T * H * Dk * ie},
+            {"v", v, B * T * H * Dv * ie},          {"beta_logit", beta_logit, B * T * H * J * Dv * ie},
+            {"prior_k_logit", prior_k_logit, B * T * H * J * Dv * ie},
+            {"prior_q_logit", prior_q_logit, B * T * H * J * Dv * ie},
+            {"state_in", state_in, B * H * J * Dk * Dv * 4},
+            {"state_out", state_out, B * H * J * Dk * Dv * 4},
+            {"o", o, B * T * H * Dv * oe},
+        };
+        for (const Span &x : all) {
+            if (overlap(ws, x)) return fail(SWILA_EINVAL, "workspace overlaps %s", x.name);
+            if (overlap(it, x)) return fail(SWILA_EINVAL, "iters_out overlaps %s", x.name);
+        }
+        if (overlap(ws, it)) return fail(SWILA_EINVAL, "iters_out overlaps workspace");
+    }
     if (shape->T == 0) {
         if (!state_out) return SWILA_OK;
         return map_hip(swila::launch_state_fill(state_out, state_in,
                                                 swila_state_bytes(shape) / sizeof(float), st),
                        "state copy");
+    }
+    if (newton) {
+        // App. D defaults: at most 64 sweeps, tolerance 1e-3 (bf16 inputs)
+        swila::NewtonArgs na{static_cast<float *>(workspace), iters_out,
+                             opts->max_iters > 0 ? opts->max_iters : 64,
+                             opts->tol == 0.f ? 1e-3f : opts->tol,
+                             (opts->flags & SWILA_FLAG_NEWTON_NO_CLAMP) == 0};
+        return map_hip(swila::launch_newton(a, na, st), "Newton launch");
     }
     const bool chunk = opts->algo == SWILA_ALGO_CHUNK_EXACT ||
                        (opts->algo == SWILA_ALGO_AUTO && opts->in_dtype == SWILA_BF16);

@@ -38,6 +38,10 @@ def test_version_and_sizes(lib):
     assert sw.state_bytes(2, 3, 64, 32, 4) == 2 * 3 * 4 * 64 * 32 * 4
     assert lib.swila_state_bytes(None) == 0
     assert sw.forward_workspace_bytes(4, 8, 2048, 64, 64, 4) == 0
+    # App. D form: the predictions of one iterate, T padded to whole chunks of 16
+    assert sw.forward_workspace_bytes(4, 8, 2048, 64, 64, 4, algo="newton") == 4 * 8 * 4 * 64 * 2048 * 4
+    assert sw.forward_workspace_bytes(2, 3, 37, 32, 16, 3, algo="newton") == 2 * 3 * 3 * 16 * 48 * 4
+    assert sw.forward_workspace_bytes(2, 3, 0, 32, 16, 3, algo="newton") == 0
 
 
 def _fwd(lib, shape, opts, ptrs=None, o=FAKE2, state_in=None, state_out=None, resp=None):
@@ -64,6 +68,13 @@ OPTS = sw.Opts(sw.BF16, sw.BF16, 0, 0, 0, 0.0, 0)
     (sw.Shape(1, 1, 4, 64, 64, 4), sw.Opts(1, 9, 0, 0, 0, 0.0, 0), sw.EINVAL, "out_dtype"),
     (sw.Shape(1, 1, 4, 64, 64, 4), sw.Opts(1, 1, 99, 0, 0, 0.0, 0), sw.EUNSUPPORTED, "algo"),
     (sw.Shape(1, 1, 4, 64, 64, 4), sw.Opts(1, 1, 0, -2, 0, 0.0, 0), sw.EINVAL, "chunk"),
+    (sw.Shape(1, 1, 4, 64, 64, 4), sw.Opts(0, 0, 3, 0, 0, 0.0, 0), sw.EUNSUPPORTED,
+     "SWILA_ALGO_NEWTON needs bf16"),
+    (sw.Shape(1, 1, 4, 64, 64, 4), sw.Opts(1, 1, 3, 32, 0, 0.0, 0), sw.EUNSUPPORTED, "chunk 32"),
+    (sw.Shape(1, 1, 4, 64, 64, 4), sw.Opts(1, 1, 2, 8, 0, 0.0, 0), sw.EUNSUPPORTED, "chunk 8"),
+    (sw.Shape(1, 1, 4, 64, 64, 4), sw.Opts(1, 1, 3, 0, -1, 0.0, 0), sw.EINVAL, "max_iters"),
+    (sw.Shape(1, 1, 4, 64, 64, 4), sw.Opts(1, 1, 3, 0, 0, float("nan"), 0), sw.EINVAL, "NaN"),
+    (sw.Shape(1, 1, 4, 64, 64, 4), sw.Opts(1, 1, 3, 0, 0, 0.0, 6), sw.EINVAL, "flags"),
 ])
 def test_forward_rejects_bad_shapes_and_options(lib, shape, opts, code, text):
     rc, msg = _fwd(lib, shape, opts)
@@ -93,6 +104,34 @@ def test_forward_rejects_bad_pointers(lib):
     # resp_out overlapping o
     rc, msg = _fwd(lib, shape, OPTS, good, resp=ctypes.c_void_p(FAKE2.value + 16))
     assert rc == sw.EINVAL and "overlap" in msg
+
+
+def test_newton_workspace_checks(lib):
+    shape = sw.Shape(1, 2, 8, 64, 64, 4)
+    opts = sw.Opts(sw.BF16, sw.BF16, sw.ALGO_NEWTON, 0, 0, 0.0, 0)
+    need = lib.swila_forward_workspace_bytes(ctypes.byref(shape), ctypes.byref(opts))
+    assert need == 2 * 4 * 64 * 16 * 4
+    ptrs = [ctypes.c_void_p((1 << 20) + (i << 26)) for i in range(6)]
+    ws = ctypes.c_void_p(1 << 36)
+
+    def call(ws_p, ws_n, iters=None, resp=None):
+        rc = lib.swila_forward(ctypes.byref(shape), ctypes.byref(opts), *ptrs, None, None, FAKE2,
+                               resp, ws_p, ws_n, iters, None)
+        return rc, lib.swila_last_error().decode()
+
+    assert call(None, 0) == (sw.EINVAL, "SWILA_ALGO_NEWTON needs a workspace")
+    rc, msg = call(ws, need - 4)
+    assert rc == sw.EINVAL and "needed" in msg
+    rc, msg = call(ctypes.c_void_p(ws.value + 8), need)
+    assert rc == sw.EINVAL and "workspace is not 16-byte aligned" in msg
+    rc, msg = call(ctypes.c_void_p(ptrs[1].value), need)
+    assert rc == sw.EINVAL and "workspace overlaps k" in msg
+    rc, msg = call(ws, need, iters=ctypes.c_void_p(ws.value + 64))
+    assert rc == sw.EINVAL and "iters_out overlaps workspace" in msg
+    rc, msg = call(ws, need, iters=ctypes.c_void_p(ws.value + need + 2))
+    assert rc == sw.EINVAL and "iters_out is not 4-byte aligned" in msg
+    rc, msg = call(ws, need, resp=ctypes.c_void_p(1 << 37))
+    assert rc == sw.EUNSUPPORTED and "resp_out" in msg
 
 
 def test_decode_requires_one_token(lib):

@@ -1,0 +1,116 @@
+"""Parity of the App. D chunkwise quasi-Newton path (SWILA_ALGO_NEWTON, through
+the C ABI) with the NumPy Newton oracle after a fixed number of sweeps, and
+with the sequential fp64 oracle once it has converged.
+
+Bar: per (b, h), max|gpu - oracle| / max|oracle| <= 2e-2 (bf16 inputs, fp32
+state and accumulation), for the outputs and the final state.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+from gpu_helpers import NAMES, TOL_BF16, head_rel_err, to_device
+from oracle import newton
+
+pytestmark = pytest.mark.gpu
+
+
+def gpu_newton(inp, *, iters, tol=-1.0, clamp=True, in_place=False):
+    import paper_2609_39034_amd as sw
+    import torch
+    dev = to_device(inp, "bf16")
+    it = torch.full((2,), -7, dtype=torch.int32, device="cuda")
+    st = dev["state"]
+    kw = {}
+    if in_place:
+        st = st.clone() if st is not None else None
+        kw["state_out"] = st
+    o, s = sw.forward(*(dev[n] for n in NAMES), st, algo="newton", max_iters=iters, tol=tol,
+                      clamp=clamp, iters_out=it, **kw)
+    torch.cuda.synchronize()
+    return (o.float().cpu().numpy().astype(np.float64), s.cpu().numpy().astype(np.float64),
+            it.cpu().numpy())
+
+
+def _errs(o, s, ref_o, ref_s):
+    return head_rel_err(o, ref_o, "o"), head_rel_err(s, ref_s, "state")
+
+
+NEWTON_SMALL = [
+    # B, H, T, Dk, Dv, J, state_std, sweeps
+    (1, 2, 40, 32, 32, 4, 0.1, 1),
+    (1, 2, 40, 32, 32, 4, 0.1, 4),
+    (2, 1, 37, 64, 16, 3, 0.0, 3),
+    (1, 1, 50, 128, 64, 8, 0.1, 2),
+    (1, 2, 33, 16, 64, 1, 0.2, 2),
+    (1, 1, 20, 128, 128, 2, 0.1, 5),
+    (1, 1, 16, 64, 32, 4, 0.3, 3),
+]
+
+
+@pytest.mark.parametrize("B,H,T,Dk,Dv,J,std,sweeps", NEWTON_SMALL)
+def test_fixed_sweeps_match_newton_oracle(B, H, T, Dk, Dv, J, std, sweeps):
+    inp = workloads.iid_inputs(B, H, T, Dk, Dv, J, dtype="bf16", seed=300 + T + J, state_std=std)
+    o, s, it = gpu_newton(inp, iters=sweeps)
+    ref_o, ref_s, _ = newton.newton_forward(*(inp[n] for n in NAMES), inp["state"], chunk=16,
+                                            iters=sweeps, g_clamp="stable")
+    eo, es = _errs(o, s, ref_o, ref_s)
+    print("sweeps %d: o %.3e state %.3e" % (sweeps, eo, es))
+    assert eo <= TOL_BF16 and es <= TOL_BF16
+    assert it[0] == sweeps and it[1] == 0
+
+
+def test_unclamped_sweeps_match_newton_oracle():
+    inp = workloads.iid_inputs(1, 2, 30, 32, 32, 4, dtype="bf16", seed=321, state_std=0.1)
+    o, s, it = gpu_newton(inp, iters=3, clamp=False)
+    ref_o, ref_s, _ = newton.newton_forward(*(inp[n] for n in NAMES), inp["state"], chunk=16,
+                                            iters=3, g_clamp=None)
+    eo, es = _errs(o, s, ref_o, ref_s)
+    print("o %.3e state %.3e" % (eo, es))
+    assert eo <= TOL_BF16 and es <= TOL_BF16
+
+
+# P13: one component, the linearisation is exact and one sweep is the
+# sequential recurrence
+def test_one_component_one_sweep_is_sequential():
+    inp = workloads.iid_inputs(2, 2, 45, 64, 64, 1, dtype="bf16", seed=322, state_std=0.2)
+    o, s, _ = gpu_newton(inp, iters=1)
+    ref = oracle.forward(*(inp[n] for n in NAMES), inp["state"])
+    eo, es = _errs(o, s, ref["o"], ref["state"])
+    print("o %.3e state %.3e" % (eo, es))
+    assert eo <= TOL_BF16 and es <= TOL_BF16
+
+
+# P11: the converged iterate is the sequential trajectory
+@pytest.mark.parametrize("B,H,T,Dk,Dv,J,std", [
+    (1, 2, 300, 64, 64, 4, 0.0),
+    (2, 1, 129, 128, 32, 8, 0.1),
+])
+def test_converges_to_sequential(B, H, T, Dk, Dv, J, std):
+    inp = workloads.iid_inputs(B, H, T, Dk, Dv, J, dtype="bf16", seed=330 + T, state_std=std)
+    o, s, it = gpu_newton(inp, iters=200, tol=1e-4)
+    ref = oracle.forward(*(inp[n] for n in NAMES), inp["state"])
+    eo, es = _errs(o, s, ref["o"], ref["state"])
+    print("sweeps %d, unconverged blocks %d: o %.3e state %.3e" % (it[0], it[1], eo, es))
+    assert it[1] == 0 and 1 <= it[0] <= 200
+    assert eo <= TOL_BF16 and es <= TOL_BF16
+
+
+def test_state_in_place():
+    inp = workloads.iid_inputs(1, 2, 40, 64, 64, 4, dtype="bf16", seed=340, state_std=0.2)
+    o1, s1, _ = gpu_newton(inp, iters=3)
+    o2, s2, _ = gpu_newton(inp, iters=3, in_place=True)
+    assert np.array_equal(o1, o2) and np.array_equal(s1, s2)
+
+
+# The small training-shaped workload (B=4 H=8 T=2048 D=64 J=4) to convergence,
+# against the sequential oracle on every head.
+def test_config2_converges_to_sequential():
+    inp = workloads.config_inputs(2)
+    o, s, it = gpu_newton(inp, iters=256, tol=1e-3)
+    ref = oracle.forward(*(inp[n] for n in NAMES), inp["state"], nthreads=16)
+    eo, es = _errs(o, s, ref["o"], ref["state"])
+    print("sweeps %d, unconverged blocks %d: o %.3e state %.3e" % (it[0], it[1], eo, es))
+    assert it[1] == 0
+    assert eo <= TOL_BF16 and es <= TOL_BF16
