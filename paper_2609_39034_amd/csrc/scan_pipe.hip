@@ -36,8 +36,8 @@
 // Layout.  Block = one head (b, h) and DB output dims with all J components,
 // N = J * DB columns (col = j * DB + dl); NW = N / 16 matrix-core waves, wave
 // w holding the Dk x 16 state tile of columns 16w..16w+15 in MFMA accumulator
-// layout; wave NW is the sequential wave.  Raw chunk inputs sit in a ring of
-// kRing LDS slots; K and Q rows are stored with their 16-byte pieces permuted
+// layout; wave NW is the sequential wave.  Raw chunk inputs sit in LDS rings
+// of a few chunk slots each; K and Q rows are stored with their 16-byte pieces permuted
 // by row (piece p of row t at slot p ^ (t mod pieces)) so that the 16 lanes
 // reading one column range hit distinct banks.
 //
@@ -68,7 +68,11 @@ typedef short short4v __attribute__((ext_vector_type(4)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
 constexpr int kC = 16;    // tokens per chunk
-constexpr int kRing = 4;  // raw-input slots: chunks n-1 .. n+2 are live
+// LDS ring slots per input, by how long a chunk stays in use after it lands
+// (it lands two chunks ahead of the sequential wave):
+constexpr int kRingKQ = 4;  // K, Q: chunks n-1 .. n+2 (state update, retrieval of n-1)
+constexpr int kRingQP = 3;  // query-prior logits, Newton predictions: n .. n+2
+constexpr int kRingS = 2;   // beta and key-prior logits, v: n+1, n+2 (staged one chunk ahead)
 
 __device__ __forceinline__ floatx4 mfma32(bf16x8 a, bf16x8 b, floatx4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
@@ -81,7 +85,12 @@ __device__ __forceinline__ void split(float x, __bf16 &hi, __bf16 &lo) {
     hi = (__bf16)x;
     lo = (__bf16)(x - (float)hi);
 }
-__device__ __forceinline__ void wait_vm() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+// Wait for this wave's outstanding vector-memory operations (the direct
+// HBM -> LDS transfers among them).  Issued through the builtin so that the
+// compiler's own wait insertion knows the transfers have landed and does not
+// add waits of its own before later LDS reads (such a wait would also wait for
+// every global store in flight).
+__device__ __forceinline__ void wait_vm() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
 template <int DK, int J, int DB>
 struct PCfg {
@@ -104,13 +113,13 @@ struct PCfg {
 template <int DK, int J, int DB, bool NT>
 struct PSmem {
     using C = PCfg<DK, J, DB>;
-    uint4 k[kRing][C::KPIECES];
-    uint4 q[kRing][C::KPIECES];
-    uint4 lb[kRing][C::LPIECES];
-    uint4 lk[kRing][C::LPIECES];
-    uint4 lq[kRing][C::LPIECES];
-    uint4 v[kRing][C::VPIECES];
-    uint4 pw[NT ? kRing : 1][NT ? C::PPIECES : 1];  // Newton: previous sweep's predictions
+    uint4 k[kRingKQ][C::KPIECES];
+    uint4 q[kRingKQ][C::KPIECES];
+    uint4 lb[kRingS][C::LPIECES];
+    uint4 lk[kRingS][C::LPIECES];
+    uint4 lq[kRingQP][C::LPIECES];
+    uint4 v[kRingS][C::VPIECES];
+    uint4 pw[NT ? kRingQP : 1][NT ? C::PPIECES : 1];  // Newton: previous sweep's predictions
     float beta[2][kC][C::NP];  // exact: beta;  Newton: g (before the clamp)
     float lks[2][kC][C::NP];   // exact: key-prior logit * log2(e);  Newton: beta r delta
     float vs[NT ? 1 : 2][kC][DB + 4];
@@ -160,8 +169,8 @@ __device__ __forceinline__ int first_for(int base, int mw, int nw) {
     return base + ((mw - base) % nw + nw) % nw;
 }
 
-// Issue the HBM -> LDS transfer of the chunk starting at token t0 into ring
-// slot `slot`.  The chunk is cut into wave-wide transfers of 64 x 16 bytes
+// Issue the HBM -> LDS transfer of chunk m (starting at token t0) into its
+// ring slots.  The chunk is cut into wave-wide transfers of 64 x 16 bytes
 // (K, Q, the three logit tensors, v), dealt round-robin to the matrix-core
 // waves; each tensor has its own loop so its base address stays a scalar.
 // Tokens past T re-read token T - 1 (in range); the recurrence gives them
@@ -169,66 +178,166 @@ __device__ __forceinline__ int first_for(int base, int mw, int nw) {
 // ([kC][N] fp32 at pred + t0 N, the block's workspace) come along.
 template <int DK, int J, int DB, bool NT>
 __device__ __forceinline__ void issue_chunk(const LayerArgs &a, PSmem<DK, J, DB, NT> &sm,
-                                            int slot, int t0, int b, int h, int d0, int mw,
+                                            int m, int t0, int b, int h, int d0, int mw,
                                             int lane, const float *pred) {
+    const int skq = m % kRingKQ, sqp = m % kRingQP, ss = m % kRingS;
     using C = PCfg<DK, J, DB>;
     const int T = a.T, H = a.H, Dv = a.Dv;
     constexpr int nk = (C::KPIECES + 63) / 64, nl = (C::LPIECES + 63) / 64;
-    const size_t row0 = (size_t)b * T;
-    // K and Q rows: piece p of row t goes to slot p ^ (t mod pieces)
-    auto kq = [&](const void *base, uint4 *tile, int ibase) {
-        for (int ins = first_for(ibase, mw, C::NW); ins < ibase + nk; ins += C::NW) {
-            const int part = ins - ibase, s = part * 64 + lane;
-            if (s < C::KPIECES) {
-                const int t = s / C::KPC, p = s % C::KPC;
-                const int tc = min(t0 + t, T - 1);
-                const int gp = p ^ (t & (C::KPC - 1));
-                dma16(static_cast<const uint16_t *>(base) + ((row0 + tc) * H + h) * DK + 8 * gp,
-                      tile + part * 64);
+    constexpr int nv = (C::VPIECES + 63) / 64;
+    if (t0 + kC <= T) {
+        // Whole chunk in range: a scalar base per tensor (row t0 of this head)
+        // plus a 32-bit per-lane byte offset.
+        const size_t row0 = ((size_t)b * T + t0) * H + h;
+        // K and Q rows: piece p of row t goes to slot p ^ (t mod pieces)
+        auto kq = [&](const void *base, uint4 *tile, int ibase) {
+            const char *src = static_cast<const char *>(base) + row0 * DK * 2;
+            for (int ins = first_for(ibase, mw, C::NW); ins < ibase + nk; ins += C::NW) {
+                const int part = ins - ibase, s = part * 64 + lane;
+                if (s < C::KPIECES) {
+                    const int t = s / C::KPC, p = s % C::KPC, gp = p ^ (t & (C::KPC - 1));
+                    dma16(src + (uint32_t)(t * H * DK * 2 + 16 * gp), tile + part * 64);
+                }
+            }
+        };
+        // logits, [t][j][dl]
+        auto logit = [&](const void *base, uint4 *dstv, int ibase) {
+            const char *src = static_cast<const char *>(base) + (row0 * J * Dv + d0) * 2;
+            for (int ins = first_for(ibase, mw, C::NW); ins < ibase + nl; ins += C::NW) {
+                const int part = ins - ibase, s = part * 64 + lane;
+                if (s < C::LPIECES) {
+                    const int t = s / (C::N / 8), rem = s % (C::N / 8);
+                    const int j = rem / (DB / 8), qd = rem % (DB / 8);
+                    dma16(src + (uint32_t)((t * H * J + j) * Dv * 2 + 16 * qd), dstv + part * 64);
+                }
+            }
+        };
+        kq(a.k, sm.k[skq], 0);
+        kq(a.q, sm.q[skq], nk);
+        logit(a.lb, sm.lb[ss], 2 * nk);
+        logit(a.lk, sm.lk[ss], 2 * nk + nl);
+        logit(a.lq, sm.lq[sqp], 2 * nk + 2 * nl);
+        const char *vsrc = static_cast<const char *>(a.v) + (row0 * Dv + d0) * 2;
+        for (int ins = first_for(2 * nk + 3 * nl, mw, C::NW); ins < 2 * nk + 3 * nl + nv;
+             ins += C::NW) {
+            const int part = ins - (2 * nk + 3 * nl), s = part * 64 + lane;
+            if (s < C::VPIECES) {
+                const int t = s / (DB / 8), qd = s % (DB / 8);
+                dma16(vsrc + (uint32_t)(t * H * Dv * 2 + 16 * qd), sm.v[ss] + part * 64);
             }
         }
-    };
-    // logits, [t][j][dl]
-    auto logit = [&](const void *base, uint4 *dstv, int ibase) {
-        for (int ins = first_for(ibase, mw, C::NW); ins < ibase + nl; ins += C::NW) {
-            const int part = ins - ibase, s = part * 64 + lane;
-            if (s < C::LPIECES) {
-                const int t = s / (C::N / 8), rem = s % (C::N / 8);
-                const int j = rem / (DB / 8), qd = rem % (DB / 8);
-                const int tc = min(t0 + t, T - 1);
-                dma16(static_cast<const uint16_t *>(base) +
-                          (((row0 + tc) * H + h) * J + j) * Dv + d0 + 8 * qd,
-                      dstv + part * 64);
+    } else {
+        const size_t row0 = (size_t)b * T;
+        // K and Q rows: piece p of row t goes to slot p ^ (t mod pieces)
+        auto kq = [&](const void *base, uint4 *tile, int ibase) {
+            for (int ins = first_for(ibase, mw, C::NW); ins < ibase + nk; ins += C::NW) {
+                const int part = ins - ibase, s = part * 64 + lane;
+                if (s < C::KPIECES) {
+                    const int t = s / C::KPC, p = s % C::KPC;
+                    const int tc = min(t0 + t, T - 1);
+                    const int gp = p ^ (t & (C::KPC - 1));
+                    dma16(static_cast<const uint16_t *>(base) + ((row0 + tc) * H + h) * DK + 8 * gp,
+                          tile + part * 64);
+                }
             }
-        }
-    };
-    kq(a.k, sm.k[slot], 0);
-    kq(a.q, sm.q[slot], nk);
-    logit(a.lb, sm.lb[slot], 2 * nk);
-    logit(a.lk, sm.lk[slot], 2 * nk + nl);
-    logit(a.lq, sm.lq[slot], 2 * nk + 2 * nl);
-    constexpr int nv = (C::VPIECES + 63) / 64;  // v, [t][dl]
-    for (int ins = first_for(2 * nk + 3 * nl, mw, C::NW); ins < 2 * nk + 3 * nl + nv;
-         ins += C::NW) {
-        const int part = ins - (2 * nk + 3 * nl), s = part * 64 + lane;
-        if (s < C::VPIECES) {
-            const int t = s / (DB / 8), qd = s % (DB / 8);
-            const int tc = min(t0 + t, T - 1);
-            dma16(static_cast<const uint16_t *>(a.v) + ((row0 + tc) * H + h) * Dv + d0 + 8 * qd,
-                  sm.v[slot] + part * 64);
+        };
+        // logits, [t][j][dl]
+        auto logit = [&](const void *base, uint4 *dstv, int ibase) {
+            for (int ins = first_for(ibase, mw, C::NW); ins < ibase + nl; ins += C::NW) {
+                const int part = ins - ibase, s = part * 64 + lane;
+                if (s < C::LPIECES) {
+                    const int t = s / (C::N / 8), rem = s % (C::N / 8);
+                    const int j = rem / (DB / 8), qd = rem % (DB / 8);
+                    const int tc = min(t0 + t, T - 1);
+                    dma16(static_cast<const uint16_t *>(base) +
+                              (((row0 + tc) * H + h) * J + j) * Dv + d0 + 8 * qd,
+                          dstv + part * 64);
+                }
+            }
+        };
+        kq(a.k, sm.k[skq], 0);
+        kq(a.q, sm.q[skq], nk);
+        logit(a.lb, sm.lb[ss], 2 * nk);
+        logit(a.lk, sm.lk[ss], 2 * nk + nl);
+        logit(a.lq, sm.lq[sqp], 2 * nk + 2 * nl);
+        for (int ins = first_for(2 * nk + 3 * nl, mw, C::NW); ins < 2 * nk + 3 * nl + nv;
+             ins += C::NW) {
+            const int part = ins - (2 * nk + 3 * nl), s = part * 64 + lane;
+            if (s < C::VPIECES) {
+                const int t = s / (DB / 8), qd = s % (DB / 8);
+                const int tc = min(t0 + t, T - 1);
+                dma16(static_cast<const uint16_t *>(a.v) + ((row0 + tc) * H + h) * Dv + d0 + 8 * qd,
+                      sm.v[ss] + part * 64);
+            }
         }
     }
     if constexpr (NT) {
         constexpr int ib = 2 * nk + 3 * nl + nv, np = (C::PPIECES + 63) / 64;
         for (int ins = first_for(ib, mw, C::NW); ins < ib + np; ins += C::NW) {
             const int part = ins - ib, s = part * 64 + lane;
-            if (s < C::PPIECES) dma16(pred + (size_t)t0 * C::N + 4 * s, sm.pw[slot] + part * 64);
+            if (s < C::PPIECES) dma16(pred + (size_t)t0 * C::N + 4 * s, sm.pw[sqp] + part * 64);
         }
     }
 }
 
-__device__ __forceinline__ float bf16_at(const uint4 *base, int idx) {
-    return bf16_bits_to_f32(reinterpret_cast<const uint16_t *>(base)[idx]);
+// Four consecutive bf16 elements (idx % 4 == 0) of an LDS tile, widened.
+__device__ __forceinline__ float4 bf16x4_at(const uint4 *base, int idx) {
+    const uint2 u = *reinterpret_cast<const uint2 *>(reinterpret_cast<const uint16_t *>(base) + idx);
+    return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u),
+                       __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xffff0000u));
+}
+// L consecutive bf16 (L in {1, 2, 4}, element index aligned to L) of an LDS
+// tile, widened; L consecutive floats loaded or stored (aligned to L); L
+// floats rounded to bf16 and stored.
+template <int L>
+__device__ __forceinline__ void bf16_row(const uint4 *base, int idx, float (&x)[L]) {
+    const uint16_t *p = reinterpret_cast<const uint16_t *>(base) + idx;
+    if constexpr (L == 4) {
+        const uint2 u = *reinterpret_cast<const uint2 *>(p);
+        x[0] = __uint_as_float(u.x << 16), x[1] = __uint_as_float(u.x & 0xffff0000u);
+        x[2] = __uint_as_float(u.y << 16), x[3] = __uint_as_float(u.y & 0xffff0000u);
+    } else if constexpr (L == 2) {
+        const uint32_t u = *reinterpret_cast<const uint32_t *>(p);
+        x[0] = __uint_as_float(u << 16), x[1] = __uint_as_float(u & 0xffff0000u);
+    } else {
+        x[0] = __uint_as_float((uint32_t)p[0] << 16);
+    }
+}
+template <int L>
+__device__ __forceinline__ void f32_load(const float *p, float (&x)[L]) {
+    if constexpr (L == 4) {
+        const float4 v = *reinterpret_cast<const float4 *>(p);
+        x[0] = v.x, x[1] = v.y, x[2] = v.z, x[3] = v.w;
+    } else if constexpr (L == 2) {
+        const float2 v = *reinterpret_cast<const float2 *>(p);
+        x[0] = v.x, x[1] = v.y;
+    } else {
+        x[0] = p[0];
+    }
+}
+template <int L>
+__device__ __forceinline__ void f32_row(float *p, const float (&x)[L]) {
+    if constexpr (L == 4)
+        *reinterpret_cast<float4 *>(p) = make_float4(x[0], x[1], x[2], x[3]);
+    else if constexpr (L == 2)
+        *reinterpret_cast<float2 *>(p) = make_float2(x[0], x[1]);
+    else
+        p[0] = x[0];
+}
+template <int L>
+__device__ __forceinline__ void bf16_store(uint16_t *p, const float (&x)[L]) {
+    typedef __bf16 bf16v __attribute__((ext_vector_type(L)));
+    typedef float f32v __attribute__((ext_vector_type(L)));
+    f32v f;
+#pragma unroll
+    for (int u = 0; u < L; ++u) f[u] = x[u];
+    const bf16v hv = __builtin_convertvector(f, bf16v);
+    if constexpr (L == 4)
+        *reinterpret_cast<uint2 *>(p) = __builtin_bit_cast(uint2, hv);
+    else if constexpr (L == 2)
+        *reinterpret_cast<uint32_t *>(p) = __builtin_bit_cast(uint32_t, hv);
+    else
+        p[0] = __builtin_bit_cast(uint16_t, hv);
 }
 
 // Same block-to-(head, column block) map as the chunk scan: every column block
@@ -360,114 +469,151 @@ __global__ __launch_bounds__(320) void scan_pipe_kernel(LayerArgs a, NewtonArgs 
         }
         return acc;
     };
-    // derived inputs of chunk m (ring slot rs, parity pr) for the sequential wave
-    auto prep_seq_inputs = [&](int m, int rs, int pr) {
+    // Per-chunk bookkeeping works on groups of four consecutive columns (or
+    // output dims), so that every thread makes one round trip to LDS.
+    static_assert(kC * N / 4 == C::NMT, "one column group per matrix-core thread");
+    // Work per (t, dl) over the J components (priors, outputs, Newton
+    // linearisation) is spread over every matrix-core thread: PE consecutive
+    // output dims per thread.
+    constexpr int PE = J == 1 ? 4 : J == 2 ? 2 : 1;
+    constexpr int NPG = kC * DB / PE;   // (t, dl) groups per chunk
+    // derived inputs of chunk m (parity pr) for the sequential wave
+    auto prep_seq_inputs = [&](int m, int pr) {
+        const int rs = m % kRingS;
         if constexpr (!NT) {
-#pragma unroll
-            for (int it = 0; it < (kC * N + C::NMT - 1) / C::NMT; ++it) {
-                const int e = tid + it * C::NMT;
-                if (kC * N % C::NMT != 0 && e >= kC * N) break;
-                const int t = e / N, cc = e % N;
-                const bool ok = m * kC + t < T;
-                sm.beta[pr][t][cc] = ok ? rcp_fast(1.0f + exp_fast(-bf16_at(sm.lb[rs], e))) : 0.f;
-                sm.lks[pr][t][cc] = bf16_at(sm.lk[rs], e) * kLog2e;
-            }
-#pragma unroll
-            for (int it = 0; it < (kC * DB + C::NMT - 1) / C::NMT; ++it) {
-                const int e = tid + it * C::NMT;
-                if (kC * DB % C::NMT == 0 || e < kC * DB)
-                    sm.vs[pr][e / DB][e % DB] = bf16_at(sm.v[rs], e);
-            }
+            const int e4 = 4 * tid, t = e4 / N, cc = e4 % N;
+            const bool ok = m * kC + t < T;
+            const float4 lbv = bf16x4_at(sm.lb[rs], e4), lkv = bf16x4_at(sm.lk[rs], e4);
+            const float4 be = ok ? make_float4(sigmoid(lbv.x), sigmoid(lbv.y), sigmoid(lbv.z),
+                                               sigmoid(lbv.w))
+                                 : make_float4(0.f, 0.f, 0.f, 0.f);
+            *reinterpret_cast<float4 *>(&sm.beta[pr][t][cc]) = be;
+            *reinterpret_cast<float4 *>(&sm.lks[pr][t][cc]) =
+                make_float4(lkv.x * kLog2e, lkv.y * kLog2e, lkv.z * kLog2e, lkv.w * kLog2e);
+            if (tid < kC * DB / 4)
+                *reinterpret_cast<float4 *>(&sm.vs[pr][e4 / DB][e4 % DB]) = bf16x4_at(sm.v[rs], e4);
         } else {
             // Linearisation around the previous sweep's predictions (App. D.2),
             // per (t, dl) over the J components: delta, r (eq. responsibility),
             // g (eq. jacobian_coeff) and the part beta r delta of the effective
             // input (eq. effective_input); the sequential wave adds g pred^(i).
-            const float *po = reinterpret_cast<const float *>(sm.pw[rs]);
+            const float *po = reinterpret_cast<const float *>(sm.pw[m % kRingQP]);
 #pragma unroll
-            for (int it = 0; it < (kC * DB + C::NMT - 1) / C::NMT; ++it) {
-                const int e = tid + it * C::NMT;
-                if (kC * DB % C::NMT != 0 && e >= kC * DB) break;
-                const int t = e / DB, dl = e % DB;
+            for (int gi = tid; gi < NPG; gi += C::NMT) {
+                const int e = PE * gi, t = e / DB, dl = e % DB;
                 const bool ok = m * kC + t < T;
-                const float vv = bf16_at(sm.v[rs], e);
-                float dj[J], xj[J], mx = -INFINITY;
+                float vv[PE];
+                bf16_row<PE>(sm.v[rs], e, vv);
+                float dj[J][PE], xj[J][PE], mx[PE], z[PE];
+#pragma unroll
+                for (int u = 0; u < PE; ++u) mx[u] = -INFINITY, z[u] = 0.f;
 #pragma unroll
                 for (int j = 0; j < J; ++j) {
-                    dj[j] = vv - po[t * N + j * DB + dl];
-                    xj[j] = kLog2e * fmaf(-0.5f * dj[j], dj[j], bf16_at(sm.lk[rs], t * N + j * DB + dl));
-                    mx = fmaxf(mx, xj[j]);
+                    float pj[PE], lkj[PE];
+                    f32_load<PE>(po + t * N + j * DB + dl, pj);
+                    bf16_row<PE>(sm.lk[rs], t * N + j * DB + dl, lkj);
+#pragma unroll
+                    for (int u = 0; u < PE; ++u) {
+                        dj[j][u] = vv[u] - pj[u];
+                        xj[j][u] = kLog2e * fmaf(-0.5f * dj[j][u], dj[j][u], lkj[u]);
+                        mx[u] = fmaxf(mx[u], xj[j][u]);
+                    }
                 }
-                float z = 0.f;
+#pragma unroll
+                for (int j = 0; j < J; ++j)
+#pragma unroll
+                    for (int u = 0; u < PE; ++u) {
+                        xj[j][u] = __builtin_amdgcn_exp2f(xj[j][u] - mx[u]);
+                        z[u] += xj[j][u];
+                    }
+#pragma unroll
+                for (int u = 0; u < PE; ++u) z[u] = rcp_fast(z[u]);
 #pragma unroll
                 for (int j = 0; j < J; ++j) {
-                    xj[j] = __builtin_amdgcn_exp2f(xj[j] - mx);
-                    z += xj[j];
-                }
-                const float iz = rcp_fast(z);
+                    float lbj[PE], gv[PE], bv[PE];
+                    bf16_row<PE>(sm.lb[rs], t * N + j * DB + dl, lbj);
 #pragma unroll
-                for (int j = 0; j < J; ++j) {
-                    const float r = xj[j] * iz;
-                    const float br = sigmoid(bf16_at(sm.lb[rs], t * N + j * DB + dl)) * r;
-                    const float d = dj[j];
-                    sm.beta[pr][t][j * DB + dl] = ok ? br * fmaf(-d * d, 1.f - r, 1.f) : 0.f;
-                    sm.lks[pr][t][j * DB + dl] = ok ? br * d : 0.f;
+                    for (int u = 0; u < PE; ++u) {
+                        const float r = xj[j][u] * z[u];
+                        const float br = sigmoid(lbj[u]) * r;
+                        const float d = dj[j][u];
+                        gv[u] = ok ? br * fmaf(-d * d, 1.f - r, 1.f) : 0.f;
+                        bv[u] = ok ? br * d : 0.f;
+                    }
+                    f32_row<PE>(&sm.beta[pr][t][j * DB + dl], gv);
+                    f32_row<PE>(&sm.lks[pr][t][j * DB + dl], bv);
                 }
             }
         }
     };
     // pi^q of chunk m: softmax over j of the query-prior logits, per (t, dl)
-    auto prep_query_prior = [&](int rs, int pr) {
+    auto prep_query_prior = [&](int m, int pr) {
+        const int rs = m % kRingQP;
 #pragma unroll
-        for (int it = 0; it < (kC * DB + C::NMT - 1) / C::NMT; ++it) {
-            const int e = tid + it * C::NMT;
-            if (kC * DB % C::NMT != 0 && e >= kC * DB) break;
-            const int t = e / DB, dl = e % DB;
-            float x[J], mq = -INFINITY;
+        for (int gi = tid; gi < NPG; gi += C::NMT) {
+            const int e = PE * gi, t = e / DB, dl = e % DB;
+            float x[J][PE], mq[PE], z[PE];
 #pragma unroll
-            for (int j = 0; j < J; ++j) {
-                x[j] = bf16_at(sm.lq[rs], t * N + j * DB + dl);
-                mq = fmaxf(mq, x[j]);
-            }
-            float z = 0.f;
+            for (int u = 0; u < PE; ++u) mq[u] = -INFINITY, z[u] = 0.f;
 #pragma unroll
             for (int j = 0; j < J; ++j) {
-                x[j] = exp_fast(x[j] - mq);
-                z += x[j];
-            }
-            const float iz = rcp_fast(z);
+                bf16_row<PE>(sm.lq[rs], t * N + j * DB + dl, x[j]);
 #pragma unroll
-            for (int j = 0; j < J; ++j) sm.pq[pr][t][j * DB + dl] = x[j] * iz;
+                for (int u = 0; u < PE; ++u) mq[u] = fmaxf(mq[u], x[j][u]);
+            }
+#pragma unroll
+            for (int j = 0; j < J; ++j)
+#pragma unroll
+                for (int u = 0; u < PE; ++u) {
+                    x[j][u] = exp_fast(x[j][u] - mq[u]);
+                    z[u] += x[j][u];
+                }
+#pragma unroll
+            for (int u = 0; u < PE; ++u) z[u] = rcp_fast(z[u]);
+#pragma unroll
+            for (int j = 0; j < J; ++j) {
+#pragma unroll
+                for (int u = 0; u < PE; ++u) x[j][u] *= z[u];
+                f32_row<PE>(&sm.pq[pr][t][j * DB + dl], x[j]);
+            }
         }
     };
+    // o of chunk m: sum over j of pi^q * retrieval
     auto store_output = [&](int m, int pr) {
 #pragma unroll
-        for (int it = 0; it < (kC * DB + C::NMT - 1) / C::NMT; ++it) {
-            const int e = tid + it * C::NMT;
-            if (kC * DB % C::NMT != 0 && e >= kC * DB) break;
-            const int t = e / DB, dl = e % DB;
+        for (int gi = tid; gi < NPG; gi += C::NMT) {
+            const int e = PE * gi, t = e / DB, dl = e % DB;
             if (m * kC + t < T) {
-                float o = 0.f;
+                float o[PE], y[PE];
 #pragma unroll
-                for (int j = 0; j < J; ++j) o += sm.py[pr][t][j * DB + dl];
-                store1(a.o, ((size_t)(b * T + m * kC + t) * H + h) * Dv + d0 + dl, o, a.out_bf16);
+                for (int u = 0; u < PE; ++u) o[u] = 0.f;
+#pragma unroll
+                for (int j = 0; j < J; ++j) {
+                    f32_load<PE>(&sm.py[pr][t][j * DB + dl], y);
+#pragma unroll
+                    for (int u = 0; u < PE; ++u) o[u] += y[u];
+                }
+                const size_t idx = (((size_t)b * T + m * kC + t) * H + h) * Dv + d0 + dl;
+                if (a.out_bf16)
+                    bf16_store<PE>(static_cast<uint16_t *>(a.o) + idx, o);
+                else
+                    f32_row<PE>(static_cast<float *>(a.o) + idx, o);
             }
         }
     };
     auto store_resp = [&](int m, int pr) {
         if constexpr (!NT) {
-            for (int e = tid; e < kC * N; e += C::NMT) {
-                const int t = e / N, cc = e % N;
-                if (m * kC + t < T)
-                    a.resp[(((size_t)(b * T + m * kC + t) * H + h) * J + cc / DB) * Dv + d0 +
-                           cc % DB] = sm.r[pr][t][cc];
-            }
+            const int e4 = 4 * tid, t = e4 / N, cc = e4 % N;
+            if (m * kC + t < T)
+                *reinterpret_cast<float4 *>(
+                    a.resp + ((((size_t)b * T + m * kC + t) * H + h) * J + cc / DB) * Dv + d0 +
+                    cc % DB) = *reinterpret_cast<const float4 *>(&sm.r[pr][t][cc]);
         }
     };
     // W += K_m^T C_m and Y += tril(A_m) C_m (C_m split in chi/clo); then
     // stage pi^q * Y of chunk m
     auto finish_chunk = [&](int m) {
-        const int rs = m % kRing, pr = m & 1;
+        const int rs = m % kRingKQ, pr = m & 1;
 #pragma unroll
         for (int it = 0; it < IT; ++it) {
             short4v ak;
@@ -580,7 +726,7 @@ __global__ __launch_bounds__(320) void scan_pipe_kernel(LayerArgs a, NewtonArgs 
                     // ---- B: forward substitution of the linearised recurrence
                     // (eq. linearized) over chunk n; g clamped to [0, 2 / |k_t|^2]
                     // unless disabled
-                    const float *po = reinterpret_cast<const float *>(sm.pw[n % kRing]);
+                    const float *po = reinterpret_cast<const float *>(sm.pw[n % kRingQP]);
                     float P[kC], gc[kC], bb[kC], pold[kC];
                     const float glo_t = na.clamp ? 0.f : -INFINITY;
 #pragma unroll
@@ -654,7 +800,7 @@ __global__ __launch_bounds__(320) void scan_pipe_kernel(LayerArgs a, NewtonArgs 
         wait_vm();
         block_sync_lds();
         {
-            prep_seq_inputs(0, 0, 0);
+            prep_seq_inputs(0, 0);
             bf16x8 whi[IT / 2 > 0 ? IT / 2 : 1], wlo[IT / 2 > 0 ? IT / 2 : 1];
             short4v w16hi, w16lo;
             split_state(whi, wlo, w16hi, w16lo);
@@ -671,7 +817,7 @@ __global__ __launch_bounds__(320) void scan_pipe_kernel(LayerArgs a, NewtonArgs 
         block_sync_lds();
 
         for (int n = 0; n < NCH; ++n) {
-            const int pr = n & 1, rs = n % kRing;
+            const int pr = n & 1, rs = n % kRingKQ, rn = (n + 1) % kRingKQ;
             // ---- matrix-core waves, while the sequential wave runs chunk n
             if (n >= 1) {
                 finish_chunk(n - 1);                 // S_n, pi^q Y_{n-1}
@@ -685,13 +831,13 @@ __global__ __launch_bounds__(320) void scan_pipe_kernel(LayerArgs a, NewtonArgs 
                 Yacc = tile_times_state(sm.q[rs], floatx4{0.f, 0.f, 0.f, 0.f}, whi, wlo, w16hi,
                                         w16lo);
                 if (n + 1 < NCH)
-                    Xacc = tile_times_state(sm.k[(n + 1) % kRing], floatx4{0.f, 0.f, 0.f, 0.f},
+                    Xacc = tile_times_state(sm.k[rn], floatx4{0.f, 0.f, 0.f, 0.f},
                                             whi, wlo, w16hi, w16lo);
             }
             if (n + 1 < NCH) {
                 // G'_n = K_{n+1} K_n^T as the A operand of G'_n C_n: the accumulator
                 // layout of K_n K_{n+1}^T, split in registers
-                const floatx4 gt = gram(sm.k[rs], sm.k[(n + 1) % kRing]);
+                const floatx4 gt = gram(sm.k[rs], sm.k[rn]);
 #pragma unroll
                 for (int m = 0; m < 4; ++m) {
                     __bf16 hi, lo;
@@ -701,15 +847,14 @@ __global__ __launch_bounds__(320) void scan_pipe_kernel(LayerArgs a, NewtonArgs 
                 }
             }
             if (w == (1 % NW) && n + 1 < NCH) {
-                const floatx4 g1 = gram(sm.k[(n + 1) % kRing], sm.k[(n + 1) % kRing]);
+                const floatx4 g1 = gram(sm.k[rn], sm.k[rn]);
 #pragma unroll
                 for (int r = 0; r < 4; ++r) sm.g[pr ^ 1][4 * lg + r][tl] = g1[r];
             }
-            prep_query_prior(rs, pr);
-            if (n + 1 < NCH) prep_seq_inputs(n + 1, (n + 1) % kRing, pr ^ 1);
+            prep_query_prior(n, pr);
+            if (n + 1 < NCH) prep_seq_inputs(n + 1, pr ^ 1);
             if (n + 2 < NCH)
-                issue_chunk<DK, J, DB, NT>(a, sm, (n + 2) % kRing, (n + 2) * kC, b, h, d0, w, lane,
-                                           pred);
+                issue_chunk<DK, J, DB, NT>(a, sm, n + 2, (n + 2) * kC, b, h, d0, w, lane, pred);
             block_sync_lds();   // e(n): C_n published (and G'_n)
 
             // ---- P_{n+1} = X_{n+1} + G'_n C_n
@@ -774,7 +919,9 @@ hipError_t launch_cfg(const LayerArgs &a, const NewtonArgs &na, hipStream_t stre
 
 template <int DK, bool NT>
 hipError_t launch_dk(const LayerArgs &a, const NewtonArgs &na, hipStream_t stream) {
-    // DB = min(Dv, 64 / J'): at most 64 columns, one wave of sequential lanes
+    // At most 64 columns (one wave of sequential lanes).  J = 4 takes 32
+    // columns (DB = 8): twice the blocks, the sequential wave on a SIMD of its
+    // own, and two blocks' LDS fit one compute unit.
     switch (a.J) {
         case 1:
             if (a.Dv >= 64) return launch_cfg<DK, 1, 64, NT>(a, na, stream);
@@ -784,7 +931,7 @@ hipError_t launch_dk(const LayerArgs &a, const NewtonArgs &na, hipStream_t strea
             if (a.Dv >= 32) return launch_cfg<DK, 2, 32, NT>(a, na, stream);
             return launch_cfg<DK, 2, 16, NT>(a, na, stream);
         case 3: return launch_cfg<DK, 3, 16, NT>(a, na, stream);
-        case 4: return launch_cfg<DK, 4, 16, NT>(a, na, stream);
+        case 4: return launch_cfg<DK, 4, 8, NT>(a, na, stream);
         case 8: return launch_cfg<DK, 8, 8, NT>(a, na, stream);
         default: return hipErrorInvalidValue;
     }
