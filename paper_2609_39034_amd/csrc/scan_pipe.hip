@@ -73,6 +73,14 @@ constexpr int kC = 16;    // tokens per chunk
 constexpr int kRingKQ = 4;  // K, Q: chunks n-1 .. n+2 (state update, retrieval of n-1)
 constexpr int kRingQP = 3;  // query-prior logits, Newton predictions: n .. n+2
 constexpr int kRingS = 2;   // beta and key-prior logits, v: n+1, n+2 (staged one chunk ahead)
+constexpr int kTP = kC + 4;  // row of a column-major [column][token] staging array
+
+// The sequential wave works in scaled units: with s^2 = log2(e) / 2,
+// d = s (v - pred) makes the E-step exponent log2(e) (lk - delta^2 / 2) a
+// single fused multiply-add, -d * d + log2(e) lk, and the coefficient
+// s c = beta r d feeds the scaled predictions s pred.
+constexpr float kS = 0.84932180028801904272f;      // sqrt(log2(e) / 2)
+constexpr float kInvS = 1.17741002251547469101f;   // 1 / kS
 
 __device__ __forceinline__ floatx4 mfma32(bf16x8 a, bf16x8 b, floatx4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
@@ -122,10 +130,10 @@ struct PSmem {
     uint4 pw[NT ? kRingQP : 1][NT ? C::PPIECES : 1];  // Newton: previous sweep's predictions
     float beta[2][kC][C::NP];  // exact: beta;  Newton: g (before the clamp)
     float lks[2][kC][C::NP];   // exact: key-prior logit * log2(e);  Newton: beta r delta
-    float vs[NT ? 1 : 2][kC][DB + 4];
+    float vs[NT ? 1 : 2][kC][DB + 4];  // s v
     float pq[2][kC][C::NP];    // query prior
     float g[2][kC][kC + 4];    // K_n K_n^T, for the sequential wave
-    float p[2][kC][C::NP];     // chunk-start predictions
+    float p[2][C::N][kTP];     // chunk-start predictions, [column][token]
     float c[2][kC][C::NP];     // coefficients (column N: idle lanes)
     float r[NT ? 1 : 2][kC][C::NP];  // responsibilities (exact mode)
     float py[2][kC][C::NP];    // pi^q * retrieval
@@ -360,7 +368,8 @@ __global__ __launch_bounds__(320) void scan_pipe_kernel(LayerArgs a, NewtonArgs 
     __shared__ PSmem<DK, J, DB, NT> sm;
 
     const int tid = threadIdx.x;
-    const int w = tid / 64, lane = tid % 64;
+    // the wave index, as a scalar: role branches and transfer slots stay scalar
+    const int w = __builtin_amdgcn_readfirstlane(tid / 64), lane = tid % 64;
     const int tl = lane % 16, lg = lane / 16;
     const int H = a.H, T = a.T, Dv = a.Dv;
     int db, hh;
@@ -368,9 +377,6 @@ __global__ __launch_bounds__(320) void scan_pipe_kernel(LayerArgs a, NewtonArgs 
     const int d0 = db * DB, h = hh % H, b = hh / H;
     const int NCH = (T + kC - 1) / kC;
     const bool seq = (w == NW);
-    // The sequential wave shares a SIMD with a matrix-core wave; its chain of
-    // dependent steps is the critical path, so it issues first.
-    if (seq) __builtin_amdgcn_s_setprio(3);
     // Newton mode: this block's predictions, [NCH * kC][N] fp32
     float *const pred = NT ? na.pred + ((size_t)hh * (Dv / DB) + db) * NCH * kC * N : nullptr;
 
@@ -403,6 +409,8 @@ __global__ __launch_bounds__(320) void scan_pipe_kernel(LayerArgs a, NewtonArgs 
     const int sl = lane;
     const int bdl = (sl / JP) % DB, bj = sl % JP;
     const bool bact = seq && sl < DB * JP && bj < J;
+    const bool bpad = seq && sl < DB * JP && bj >= J;   // padding component (J = 3)
+    const bool want_r = a.resp != nullptr;
     const int bcol = bact ? bj * DB + bdl : 0;
     const int bsto = bact ? bcol : N;
 
@@ -477,21 +485,30 @@ __global__ __launch_bounds__(320) void scan_pipe_kernel(LayerArgs a, NewtonArgs 
     // output dims per thread.
     constexpr int PE = J == 1 ? 4 : J == 2 ? 2 : 1;
     constexpr int NPG = kC * DB / PE;   // (t, dl) groups per chunk
+    // When the groups fill at most half of the threads (J = 8), the query
+    // prior takes the first half and the outputs the second.
+    constexpr int OUT0 = 2 * NPG <= C::NMT ? C::NMT - NPG : 0;
     // derived inputs of chunk m (parity pr) for the sequential wave
     auto prep_seq_inputs = [&](int m, int pr) {
         const int rs = m % kRingS;
         if constexpr (!NT) {
+            // four consecutive columns of token t
             const int e4 = 4 * tid, t = e4 / N, cc = e4 % N;
             const bool ok = m * kC + t < T;
-            const float4 lbv = bf16x4_at(sm.lb[rs], e4), lkv = bf16x4_at(sm.lk[rs], e4);
-            const float4 be = ok ? make_float4(sigmoid(lbv.x), sigmoid(lbv.y), sigmoid(lbv.z),
-                                               sigmoid(lbv.w))
-                                 : make_float4(0.f, 0.f, 0.f, 0.f);
-            *reinterpret_cast<float4 *>(&sm.beta[pr][t][cc]) = be;
-            *reinterpret_cast<float4 *>(&sm.lks[pr][t][cc]) =
-                make_float4(lkv.x * kLog2e, lkv.y * kLog2e, lkv.z * kLog2e, lkv.w * kLog2e);
-            if (tid < kC * DB / 4)
-                *reinterpret_cast<float4 *>(&sm.vs[pr][e4 / DB][e4 % DB]) = bf16x4_at(sm.v[rs], e4);
+            float lbv[4], lkv[4];
+            bf16_row<4>(sm.lb[rs], e4, lbv);
+            bf16_row<4>(sm.lk[rs], e4, lkv);
+#pragma unroll
+            for (int u = 0; u < 4; ++u) lbv[u] = ok ? sigmoid(lbv[u]) : 0.f, lkv[u] *= kLog2e;
+            f32_row<4>(&sm.beta[pr][t][cc], lbv);
+            f32_row<4>(&sm.lks[pr][t][cc], lkv);
+            if (tid < kC * DB / 4) {
+                float vv[4];
+                bf16_row<4>(sm.v[rs], e4, vv);
+#pragma unroll
+                for (int u = 0; u < 4; ++u) vv[u] *= kS;
+                f32_row<4>(&sm.vs[pr][e4 / DB][e4 % DB], vv);
+            }
         } else {
             // Linearisation around the previous sweep's predictions (App. D.2),
             // per (t, dl) over the J components: delta, r (eq. responsibility),
@@ -581,7 +598,8 @@ __global__ __launch_bounds__(320) void scan_pipe_kernel(LayerArgs a, NewtonArgs 
     // o of chunk m: sum over j of pi^q * retrieval
     auto store_output = [&](int m, int pr) {
 #pragma unroll
-        for (int gi = tid; gi < NPG; gi += C::NMT) {
+        for (int gi = tid - OUT0; gi < NPG; gi += C::NMT) {
+            if (gi < 0) break;
             const int e = PE * gi, t = e / DB, dl = e % DB;
             if (m * kC + t < T) {
                 float o[PE], y[PE];
@@ -693,34 +711,77 @@ __global__ __launch_bounds__(320) void scan_pipe_kernel(LayerArgs a, NewtonArgs 
 #pragma unroll
                 for (int u = 1; u < kC; ++u) grow[u] = sm.g[pr][0][u];
                 if constexpr (!NT) {
-                    // ---- B: the token recurrence of chunk n
-                    float P[kC], vv[kC], lkv[kC], bev[kC];
+                    // ---- B: the token recurrence of chunk n, in scaled units.
+                    // The softmax over j runs without subtracting its maximum: for
+                    // logits and errors of ordinary size its sum stays far inside
+                    // the fp32 range.  Should the sum of some column leave
+                    // [2^-100, 2^100] (every component underflowing, or a logit
+                    // beyond about 60), the chunk is run again with the maximum
+                    // subtracted.
+                    float P[kC], P0[kC], vv[kC], lkv[kC], bev[kC];
+#pragma unroll
+                    for (int t = 0; t < kC; t += 4) {
+                        const float4 p4 = *reinterpret_cast<const float4 *>(&sm.p[pr][bcol][t]);
+                        P[t] = kS * p4.x, P[t + 1] = kS * p4.y, P[t + 2] = kS * p4.z, P[t + 3] = kS * p4.w;
+                    }
 #pragma unroll
                     for (int t = 0; t < kC; ++t) {
-                        P[t] = sm.p[pr][t][bcol];
                         vv[t] = sm.vs[pr][t][bdl];
-                        lkv[t] = bact ? sm.lks[pr][t][bcol] : -INFINITY;
-                        bev[t] = bact ? sm.beta[pr][t][bcol] : 0.f;
+                        lkv[t] = sm.lks[pr][t][bcol];
+                        bev[t] = sm.beta[pr][t][bcol];
                     }
+#pragma unroll
+                    for (int t = 0; t < kC; ++t) {
+                        P0[t] = P[t];
+                        // padding component of J = 3: no mass; idle lanes: harmless
+                        lkv[t] = bpad ? -INFINITY : lkv[t];
+                        bev[t] = bact ? bev[t] : 0.f;
+                    }
+                    float zmin = 1.f, zmax = 1.f;
 #pragma unroll
                     for (int t = 0; t < kC; ++t) {
                         float gnext[kC];
 #pragma unroll
                         for (int u = t + 2; u < kC; ++u) gnext[u] = sm.g[pr][t + 1][u];
-                        const float delta = vv[t] - P[t];
-                        const float bd = bev[t] * delta;
-                        const float e = fmaf(-0.5f * kLog2e * delta, delta, lkv[t]);
-                        const float mx = group_max<JP>(e);
-                        const float ex = __builtin_amdgcn_exp2f(e - mx);
+                        const float d = vv[t] - P[t];
+                        const float bd = bev[t] * d;
+                        const float ex = __builtin_amdgcn_exp2f(fmaf(-d, d, lkv[t]));
                         const float z = group_sum<JP>(ex);
-                        const float r = ex * rcp_fast(z);
-                        const float c = bd * r;
+                        const float iz = rcp_fast(z);
+                        const float cs = (bd * ex) * iz;          // s c
 #pragma unroll
-                        for (int u = t + 1; u < kC; ++u) P[u] = fmaf(grow[u], c, P[u]);
-                        sm.c[pr][t][bsto] = c;
-                        sm.r[pr][t][bsto] = r;
+                        for (int u = t + 1; u < kC; ++u) P[u] = fmaf(grow[u], cs, P[u]);
+                        sm.c[pr][t][bsto] = cs * kInvS;
+                        if (want_r) sm.r[pr][t][bsto] = ex * iz;
+                        zmin = fminf(zmin, z);
+                        zmax = fmaxf(zmax, z);
 #pragma unroll
                         for (int u = t + 2; u < kC; ++u) grow[u] = gnext[u];
+                    }
+                    if (__builtin_amdgcn_ballot_w64(bact && !(zmin >= 0x1p-100f && zmax <= 0x1p100f)) != 0) {
+                        // some softmax underflowed: the chunk again, maximum subtracted
+#pragma unroll
+                        for (int u = 1; u < kC; ++u) grow[u] = sm.g[pr][0][u];
+#pragma unroll
+                        for (int t = 0; t < kC; ++t) P[t] = P0[t];
+#pragma unroll
+                        for (int t = 0; t < kC; ++t) {
+                            float gnext[kC];
+#pragma unroll
+                            for (int u = t + 2; u < kC; ++u) gnext[u] = sm.g[pr][t + 1][u];
+                            const float d = vv[t] - P[t];
+                            const float bd = bev[t] * d;
+                            const float e = fmaf(-d, d, lkv[t]);
+                            const float ex = __builtin_amdgcn_exp2f(e - group_max<JP>(e));
+                            const float iz = rcp_fast(group_sum<JP>(ex));
+                            const float cs = (bd * ex) * iz;
+#pragma unroll
+                            for (int u = t + 1; u < kC; ++u) P[u] = fmaf(grow[u], cs, P[u]);
+                            sm.c[pr][t][bsto] = cs * kInvS;
+                            if (want_r) sm.r[pr][t][bsto] = ex * iz;
+#pragma unroll
+                            for (int u = t + 2; u < kC; ++u) grow[u] = gnext[u];
+                        }
                     }
                 } else {
                     // ---- B: forward substitution of the linearised recurrence
@@ -731,7 +792,7 @@ __global__ __launch_bounds__(320) void scan_pipe_kernel(LayerArgs a, NewtonArgs 
                     const float glo_t = na.clamp ? 0.f : -INFINITY;
 #pragma unroll
                     for (int t = 0; t < kC; ++t) {
-                        P[t] = sm.p[pr][t][bcol];
+                        P[t] = sm.p[pr][bcol][t];
                         const float ghi_t = na.clamp ? 2.f * rcp_fast(sm.g[pr][t][t]) : INFINITY;
                         gc[t] = fminf(fmaxf(sm.beta[pr][t][bcol], glo_t), ghi_t);
                         bb[t] = sm.lks[pr][t][bcol];
@@ -806,8 +867,7 @@ __global__ __launch_bounds__(320) void scan_pipe_kernel(LayerArgs a, NewtonArgs 
             split_state(whi, wlo, w16hi, w16lo);
             const floatx4 P0 = tile_times_state(sm.k[0], floatx4{0.f, 0.f, 0.f, 0.f}, whi, wlo,
                                                 w16hi, w16lo);
-#pragma unroll
-            for (int r = 0; r < 4; ++r) sm.p[0][4 * lg + r][col] = P0[r];
+            *reinterpret_cast<float4 *>(&sm.p[0][col][4 * lg]) = make_float4(P0[0], P0[1], P0[2], P0[3]);
             if (w == 0) {
                 const floatx4 G0 = gram(sm.k[0], sm.k[0]);
 #pragma unroll
@@ -853,6 +913,8 @@ __global__ __launch_bounds__(320) void scan_pipe_kernel(LayerArgs a, NewtonArgs 
             }
             prep_query_prior(n, pr);
             if (n + 1 < NCH) prep_seq_inputs(n + 1, pr ^ 1);
+            // issued last: LDS accesses after it in this chunk would make the
+            // compiler wait for these transfers
             if (n + 2 < NCH)
                 issue_chunk<DK, J, DB, NT>(a, sm, n + 2, (n + 2) * kC, b, h, d0, w, lane, pred);
             block_sync_lds();   // e(n): C_n published (and G'_n)
@@ -870,7 +932,7 @@ __global__ __launch_bounds__(320) void scan_pipe_kernel(LayerArgs a, NewtonArgs 
                 Xacc = mfma16(ghi, clo, Xacc);
                 Xacc = mfma16(glo, chi, Xacc);
 #pragma unroll
-                for (int r = 0; r < 4; ++r) sm.p[pr ^ 1][4 * lg + r][col] = Xacc[r];
+                for (int r = 0; r < 4; ++r) sm.p[pr ^ 1][col][4 * lg + r] = Xacc[r];
             }
             wait_vm();          // chunk n+2 has landed in LDS
             block_sync_lds();   // i(n+1)

@@ -104,6 +104,21 @@ def test_extreme_values():
     _check(inp, "f32")
 
 
+@pytest.mark.parametrize("case", ["errors", "logits"])
+def test_extreme_values_chunk(case):
+    """bf16 inputs through the matrix-core scan: errors so large that every
+    component's factor underflows, or logits so large that the unshifted
+    softmax sum overflows; either way the kernel must fall back to the
+    maximum-subtracted E-step for that chunk."""
+    if case == "errors":
+        inp = workloads.iid_inputs(1, 2, 40, 64, 32, 4, dtype="bf16", seed=19, state_std=0.5)
+        inp["v"] = workloads.round_bf16(inp["v"] * 40.0)
+    else:
+        inp = workloads.iid_inputs(1, 2, 40, 64, 32, 4, dtype="bf16", seed=20, state_std=0.5,
+                                   logit_scale=150.0)
+    _check(inp, "bf16")
+
+
 def test_config1_tiny():
     _check(workloads.config_inputs(1), "f32")
 
