@@ -148,11 +148,23 @@ __device__ __forceinline__ uint2 tile4(const uint4 *tile, int t, int i) {
     const int slot = t * KPC + ((i >> 3) ^ (t & (KPC - 1)));
     return reinterpret_cast<const uint2 *>(tile + slot)[(i >> 2) & 1];
 }
+
+// Transposed 16 x 16 block of a row-permuted K tile, as the A operand of a
+// 16x16x16 matrix-core step: lane (tl, lg) receives K[4 lg + mm][16 it + tl],
+// mm = 0..3, from one transposing LDS load.  In each group of 16 lanes the
+// load hands lane i element mm of the 8 bytes addressed by lane 4 mm + i / 4
+// (element i mod 4), so lane (tl, lg) addresses row 4 lg + tl / 4, key
+// indices 16 it + 4 (tl mod 4) .. + 3.
+typedef short short4vs __attribute__((__vector_size__(8)));
 template <int DK>
-__device__ __forceinline__ uint16_t tile1(const uint4 *tile, int t, int i) {
+__device__ __forceinline__ short4v tile_tr(const uint4 *tile, int it, int tl, int lg) {
     constexpr int KPC = DK / 8;
-    const int slot = t * KPC + ((i >> 3) ^ (t & (KPC - 1)));
-    return reinterpret_cast<const uint16_t *>(tile + slot)[i & 7];
+    const int t = 4 * lg + (tl >> 2), q = tl & 3;
+    const int slot = t * KPC + ((2 * it + (q >> 1)) ^ (t & (KPC - 1)));
+    const char *p = reinterpret_cast<const char *>(tile + slot) + 8 * (q & 1);
+    const short4vs v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (__attribute__((address_space(3))) short4vs *)(p));
+    return __builtin_bit_cast(short4v, v);
 }
 
 // A-operand fragment of rows 0..15 of a K or Q tile for the matrix-core step
@@ -634,10 +646,8 @@ __global__ __launch_bounds__(320) void scan_pipe_kernel(LayerArgs a, NewtonArgs 
         const int rs = m % kRingKQ, pr = m & 1;
 #pragma unroll
         for (int it = 0; it < IT; ++it) {
-            short4v ak;
-#pragma unroll
-            for (int mm = 0; mm < 4; ++mm)
-                ak[mm] = (short)tile1<DK>(sm.k[rs], 4 * lg + mm, 16 * it + tl);
+            // A operand K^T: lane (tl, lg) needs K[4 lg + mm][16 it + tl], mm = 0..3
+            const short4v ak = tile_tr<DK>(sm.k[rs], it, tl, lg);
             W[it] = mfma16(ak, chi, W[it]);
             W[it] = mfma16(ak, clo, W[it]);
         }
