@@ -178,10 +178,22 @@ __device__ __forceinline__ uint4 frag32(const uint4 *tile, int tl, int lg, int s
 }
 
 // One wave-wide HBM -> LDS transfer: lane L moves 16 bytes from src to
-// dst + 16 L (dst is the same for the whole wave).
-__device__ __forceinline__ void dma16(const void *src, uint4 *dst) {
-    __builtin_amdgcn_global_load_lds((const void __attribute__((address_space(1))) *)src,
-                                     (void __attribute__((address_space(3))) *)dst, 16, 0, 0);
+// dst + 16 L (dst is the same for the whole wave).  Issued as inline
+// assembly so that the compiler does not track it: it would otherwise wait
+// for every transfer in flight before any later LDS access it cannot prove
+// disjoint, and the transfers could not overlap a chunk's work.  Every wait
+// for them is explicit (wait_vm before the barrier that publishes the data).
+// lds is the LDS byte address of dst (wave-uniform).  M0 carries it; the
+// compiler's value of M0 is saved and restored around the transfer, and
+// writing M0 needs one wait state before the transfer reads it.
+__device__ __forceinline__ void dma16(const void *src, uint32_t lds) {
+    uint32_t saved;
+    asm volatile(
+        "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\ts_nop 0\n\t"
+        "global_load_lds_dwordx4 %2, off\n\ts_mov_b32 m0, %0"
+        : "=&s"(saved)
+        : "s"(__builtin_amdgcn_readfirstlane(lds)), "v"((uint64_t)(uintptr_t)src)
+        : "memory");
 }
 
 // First transfer index >= base that falls to wave mw in a round-robin deal.
@@ -198,8 +210,13 @@ __device__ __forceinline__ int first_for(int base, int mw, int nw) {
 // ([kC][N] fp32 at pred + t0 N, the block's workspace) come along.
 template <int DK, int J, int DB, bool NT>
 __device__ __forceinline__ void issue_chunk(const LayerArgs &a, PSmem<DK, J, DB, NT> &sm,
-                                            int m, int t0, int b, int h, int d0, int mw,
-                                            int lane, const float *pred) {
+                                            uint32_t lds_base, int m, int t0, int b, int h,
+                                            int d0, int mw, int lane, const float *pred) {
+    // LDS byte address of a destination inside sm
+    auto at = [&](const uint4 *dst) {
+        return lds_base + (uint32_t)(reinterpret_cast<const char *>(dst) -
+                                     reinterpret_cast<const char *>(&sm));
+    };
     const int skq = m % kRingKQ, sqp = m % kRingQP, ss = m % kRingS;
     using C = PCfg<DK, J, DB>;
     const int T = a.T, H = a.H, Dv = a.Dv;
@@ -216,7 +233,7 @@ __device__ __forceinline__ void issue_chunk(const LayerArgs &a, PSmem<DK, J, DB,
                 const int part = ins - ibase, s = part * 64 + lane;
                 if (s < C::KPIECES) {
                     const int t = s / C::KPC, p = s % C::KPC, gp = p ^ (t & (C::KPC - 1));
-                    dma16(src + (uint32_t)(t * H * DK * 2 + 16 * gp), tile + part * 64);
+                    dma16(src + (uint32_t)(t * H * DK * 2 + 16 * gp), at(tile + part * 64));
                 }
             }
         };
@@ -228,7 +245,7 @@ __device__ __forceinline__ void issue_chunk(const LayerArgs &a, PSmem<DK, J, DB,
                 if (s < C::LPIECES) {
                     const int t = s / (C::N / 8), rem = s % (C::N / 8);
                     const int j = rem / (DB / 8), qd = rem % (DB / 8);
-                    dma16(src + (uint32_t)((t * H * J + j) * Dv * 2 + 16 * qd), dstv + part * 64);
+                    dma16(src + (uint32_t)((t * H * J + j) * Dv * 2 + 16 * qd), at(dstv + part * 64));
                 }
             }
         };
@@ -243,7 +260,7 @@ __device__ __forceinline__ void issue_chunk(const LayerArgs &a, PSmem<DK, J, DB,
             const int part = ins - (2 * nk + 3 * nl), s = part * 64 + lane;
             if (s < C::VPIECES) {
                 const int t = s / (DB / 8), qd = s % (DB / 8);
-                dma16(vsrc + (uint32_t)(t * H * Dv * 2 + 16 * qd), sm.v[ss] + part * 64);
+                dma16(vsrc + (uint32_t)(t * H * Dv * 2 + 16 * qd), at(sm.v[ss] + part * 64));
             }
         }
     } else {
@@ -257,7 +274,7 @@ __device__ __forceinline__ void issue_chunk(const LayerArgs &a, PSmem<DK, J, DB,
                     const int tc = min(t0 + t, T - 1);
                     const int gp = p ^ (t & (C::KPC - 1));
                     dma16(static_cast<const uint16_t *>(base) + ((row0 + tc) * H + h) * DK + 8 * gp,
-                          tile + part * 64);
+                          at(tile + part * 64));
                 }
             }
         };
@@ -271,7 +288,7 @@ __device__ __forceinline__ void issue_chunk(const LayerArgs &a, PSmem<DK, J, DB,
                     const int tc = min(t0 + t, T - 1);
                     dma16(static_cast<const uint16_t *>(base) +
                               (((row0 + tc) * H + h) * J + j) * Dv + d0 + 8 * qd,
-                          dstv + part * 64);
+                          at(dstv + part * 64));
                 }
             }
         };
@@ -287,7 +304,7 @@ __device__ __forceinline__ void issue_chunk(const LayerArgs &a, PSmem<DK, J, DB,
                 const int t = s / (DB / 8), qd = s % (DB / 8);
                 const int tc = min(t0 + t, T - 1);
                 dma16(static_cast<const uint16_t *>(a.v) + ((row0 + tc) * H + h) * Dv + d0 + 8 * qd,
-                      sm.v[ss] + part * 64);
+                      at(sm.v[ss] + part * 64));
             }
         }
     }
@@ -295,7 +312,7 @@ __device__ __forceinline__ void issue_chunk(const LayerArgs &a, PSmem<DK, J, DB,
         constexpr int ib = 2 * nk + 3 * nl + nv, np = (C::PPIECES + 63) / 64;
         for (int ins = first_for(ib, mw, C::NW); ins < ib + np; ins += C::NW) {
             const int part = ins - ib, s = part * 64 + lane;
-            if (s < C::PPIECES) dma16(pred + (size_t)t0 * C::N + 4 * s, sm.pw[sqp] + part * 64);
+            if (s < C::PPIECES) dma16(pred + (size_t)t0 * C::N + 4 * s, at(sm.pw[sqp] + part * 64));
         }
     }
 }
@@ -378,6 +395,7 @@ __global__ __launch_bounds__(320) void scan_pipe_kernel(LayerArgs a, NewtonArgs 
     using C = PCfg<DK, J, DB>;
     constexpr int IT = C::IT, N = C::N, NW = C::NW, JP = C::JP;
     __shared__ PSmem<DK, J, DB, NT> sm;
+    const uint32_t lds_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void *)&sm;
 
     const int tid = threadIdx.x;
     // the wave index, as a scalar: role branches and transfer slots stay scalar
@@ -866,8 +884,8 @@ __global__ __launch_bounds__(320) void scan_pipe_kernel(LayerArgs a, NewtonArgs 
         // hoist these transfers' addresses out of the sweep loop and hold them)
         int t0 = 0;
         asm volatile("" : "+s"(t0));
-        issue_chunk<DK, J, DB, NT>(a, sm, 0, t0, b, h, d0, w, lane, pred);
-        if (NCH > 1) issue_chunk<DK, J, DB, NT>(a, sm, 1, t0 + kC, b, h, d0, w, lane, pred);
+        issue_chunk<DK, J, DB, NT>(a, sm, lds_base, 0, t0, b, h, d0, w, lane, pred);
+        if (NCH > 1) issue_chunk<DK, J, DB, NT>(a, sm, lds_base, 1, t0 + kC, b, h, d0, w, lane, pred);
         wait_vm();
         block_sync_lds();
         {
@@ -888,6 +906,11 @@ __global__ __launch_bounds__(320) void scan_pipe_kernel(LayerArgs a, NewtonArgs 
 
         for (int n = 0; n < NCH; ++n) {
             const int pr = n & 1, rs = n % kRingKQ, rn = (n + 1) % kRingKQ;
+            // Chunk n+2 first, so that the transfer has the whole chunk to
+            // land; its ring slots held chunks n-2 (K, Q), n (beta and key-prior
+            // logits, v) and n-1 (query-prior logits, predictions), all used up.
+            if (n + 2 < NCH)
+                issue_chunk<DK, J, DB, NT>(a, sm, lds_base, n + 2, (n + 2) * kC, b, h, d0, w, lane, pred);
             // ---- matrix-core waves, while the sequential wave runs chunk n
             if (n >= 1) {
                 finish_chunk(n - 1);                 // S_n, pi^q Y_{n-1}
@@ -923,10 +946,6 @@ __global__ __launch_bounds__(320) void scan_pipe_kernel(LayerArgs a, NewtonArgs 
             }
             prep_query_prior(n, pr);
             if (n + 1 < NCH) prep_seq_inputs(n + 1, pr ^ 1);
-            // issued last: LDS accesses after it in this chunk would make the
-            // compiler wait for these transfers
-            if (n + 2 < NCH)
-                issue_chunk<DK, J, DB, NT>(a, sm, n + 2, (n + 2) * kC, b, h, d0, w, lane, pred);
             block_sync_lds();   // e(n): C_n published (and G'_n)
 
             // ---- P_{n+1} = X_{n+1} + G'_n C_n
