@@ -36,8 +36,8 @@ MEASURED_TRAFFIC = {
     ("decode.hip", "769b72fdca36c7f4df23d3fb1d410dc16c3c323568a37067ebabab4fb4b755be"): 2184302284,
     ("scan_direct.hip", "b38c28c5de8d782d7e8789d36b1d92720d8a6715bdb2781db527a2d9cdf2e1ba"):
         136540979,
-    ("scan_pipe.hip", "cd75b604f8ebc54e901f0186d51ba3cb20b32f833a09982c1d2cebe8f79251a7"):
-        136596480,
+    ("scan_pipe.hip", "5cda4c1befe00ba76f4c4d773bcef2b66597decf1999ae075ca64c8abbb7ea4d"):
+        136676608,
 }
 
 
