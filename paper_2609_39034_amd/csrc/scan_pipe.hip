@@ -98,6 +98,11 @@ __device__ __forceinline__ void split(float x, __bf16 &hi, __bf16 &lo) {
 // compiler's own wait insertion knows the transfers have landed and does not
 // add waits of its own before later LDS reads (such a wait would also wait for
 // every global store in flight).
+template <bool B>
+struct BoolTag {
+    static constexpr bool value = B;
+};
+
 __device__ __forceinline__ void wait_vm() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
 template <int DK, int J, int DB>
@@ -128,13 +133,18 @@ struct PSmem {
     uint4 lq[kRingQP][C::LPIECES];
     uint4 v[kRingS][C::VPIECES];
     uint4 pw[NT ? kRingQP : 1][NT ? C::PPIECES : 1];  // Newton: previous sweep's predictions
-    float beta[2][kC][C::NP];  // exact: beta;  Newton: g (before the clamp)
-    float lks[2][kC][C::NP];   // exact: key-prior logit * log2(e);  Newton: beta r delta
-    float vs[NT ? 1 : 2][kC][DB + 4];  // s v
+    union {
+        float2 sq[2][kC][C::N];     // exact: {beta, log2(e) key-prior logit} per (t, column)
+        struct {
+            float beta[2][kC][C::NP];   // Newton: g (before the clamp)
+            float lks[2][kC][C::NP];    // Newton: beta r delta
+        };
+    };
+    float vs[NT ? 1 : 2][kC][DB + 4];   // exact: s v
     float pq[2][kC][C::NP];    // query prior
     float g[2][kC][kC + 4];    // K_n K_n^T, for the sequential wave
     float p[2][C::N][kTP];     // chunk-start predictions, [column][token]
-    float c[2][kC][C::NP];     // coefficients (column N: idle lanes)
+    float c[2][C::N + 1][kTP];  // coefficients, [column][token] (column N: idle lanes)
     float r[NT ? 1 : 2][kC][C::NP];  // responsibilities (exact mode)
     float py[2][kC][C::NP];    // pi^q * retrieval
     int flag;                  // Newton: this sweep met the tolerance
@@ -522,16 +532,17 @@ __global__ __launch_bounds__(320) void scan_pipe_kernel(LayerArgs a, NewtonArgs 
     auto prep_seq_inputs = [&](int m, int pr) {
         const int rs = m % kRingS;
         if constexpr (!NT) {
-            // four consecutive columns of token t
+            // four consecutive columns (dims dl .. dl+3 of one component) of token t
             const int e4 = 4 * tid, t = e4 / N, cc = e4 % N;
             const bool ok = m * kC + t < T;
             float lbv[4], lkv[4];
             bf16_row<4>(sm.lb[rs], e4, lbv);
             bf16_row<4>(sm.lk[rs], e4, lkv);
-#pragma unroll
-            for (int u = 0; u < 4; ++u) lbv[u] = ok ? sigmoid(lbv[u]) : 0.f, lkv[u] *= kLog2e;
-            f32_row<4>(&sm.beta[pr][t][cc], lbv);
-            f32_row<4>(&sm.lks[pr][t][cc], lkv);
+            float4 *dst = reinterpret_cast<float4 *>(&sm.sq[pr][t][cc]);
+            dst[0] = make_float4(ok ? sigmoid(lbv[0]) : 0.f, lkv[0] * kLog2e,
+                                 ok ? sigmoid(lbv[1]) : 0.f, lkv[1] * kLog2e);
+            dst[1] = make_float4(ok ? sigmoid(lbv[2]) : 0.f, lkv[2] * kLog2e,
+                                 ok ? sigmoid(lbv[3]) : 0.f, lkv[3] * kLog2e);
             if (tid < kC * DB / 4) {
                 float vv[4];
                 bf16_row<4>(sm.v[rs], e4, vv);
@@ -754,9 +765,8 @@ __global__ __launch_bounds__(320) void scan_pipe_kernel(LayerArgs a, NewtonArgs 
                     }
 #pragma unroll
                     for (int t = 0; t < kC; ++t) {
-                        vv[t] = sm.vs[pr][t][bdl];
-                        lkv[t] = sm.lks[pr][t][bcol];
-                        bev[t] = sm.beta[pr][t][bcol];
+                        const float2 x = sm.sq[pr][t][bcol];
+                        bev[t] = x.x, lkv[t] = x.y, vv[t] = sm.vs[pr][t][bdl];
                     }
 #pragma unroll
                     for (int t = 0; t < kC; ++t) {
@@ -765,33 +775,16 @@ __global__ __launch_bounds__(320) void scan_pipe_kernel(LayerArgs a, NewtonArgs 
                         lkv[t] = bpad ? -INFINITY : lkv[t];
                         bev[t] = bact ? bev[t] : 0.f;
                     }
-                    float zmin = 1.f, zmax = 1.f;
-#pragma unroll
-                    for (int t = 0; t < kC; ++t) {
-                        float gnext[kC];
-#pragma unroll
-                        for (int u = t + 2; u < kC; ++u) gnext[u] = sm.g[pr][t + 1][u];
-                        const float d = vv[t] - P[t];
-                        const float bd = bev[t] * d;
-                        const float ex = __builtin_amdgcn_exp2f(fmaf(-d, d, lkv[t]));
-                        const float z = group_sum<JP>(ex);
-                        const float iz = rcp_fast(z);
-                        const float cs = (bd * ex) * iz;          // s c
-#pragma unroll
-                        for (int u = t + 1; u < kC; ++u) P[u] = fmaf(grow[u], cs, P[u]);
-                        sm.c[pr][t][bsto] = cs * kInvS;
-                        if (want_r) sm.r[pr][t][bsto] = ex * iz;
-                        zmin = fminf(zmin, z);
-                        zmax = fmaxf(zmax, z);
-#pragma unroll
-                        for (int u = t + 2; u < kC; ++u) grow[u] = gnext[u];
-                    }
-                    if (__builtin_amdgcn_ballot_w64(bact && !(zmin >= 0x1p-100f && zmax <= 0x1p100f)) != 0) {
-                        // some softmax underflowed: the chunk again, maximum subtracted
-#pragma unroll
-                        for (int u = 1; u < kC; ++u) grow[u] = sm.g[pr][0][u];
-#pragma unroll
-                        for (int t = 0; t < kC; ++t) P[t] = P0[t];
+                    // Software-pipelined: token t updates only P[t+1] at once; its
+                    // other updates (P[u], u > t+1) run during token t+1, between
+                    // the exponential and the sum over j, where they fill the wait.
+                    // The scheduling barriers and the empty asm pins keep the compiler
+                    // from sinking them into the dependent chain of a later token.
+                    // The coefficients go out four tokens at a time; the branch on
+                    // whether r is wanted is taken once per chunk.
+                    auto run = [&](auto want) {
+                        constexpr bool R = decltype(want)::value;
+                        float zmin = 1.f, zmax = 1.f, cprev = 0.f, gprev[kC], cb[4];
 #pragma unroll
                         for (int t = 0; t < kC; ++t) {
                             float gnext[kC];
@@ -799,18 +792,59 @@ __global__ __launch_bounds__(320) void scan_pipe_kernel(LayerArgs a, NewtonArgs 
                             for (int u = t + 2; u < kC; ++u) gnext[u] = sm.g[pr][t + 1][u];
                             const float d = vv[t] - P[t];
                             const float bd = bev[t] * d;
-                            const float e = fmaf(-d, d, lkv[t]);
-                            const float ex = __builtin_amdgcn_exp2f(e - group_max<JP>(e));
-                            const float iz = rcp_fast(group_sum<JP>(ex));
-                            const float cs = (bd * ex) * iz;
+                            const float ex = __builtin_amdgcn_exp2f(fmaf(-d, d, lkv[t]));
+                            __builtin_amdgcn_sched_barrier(0);
+                            if (t >= 1) {
 #pragma unroll
-                            for (int u = t + 1; u < kC; ++u) P[u] = fmaf(grow[u], cs, P[u]);
-                            sm.c[pr][t][bsto] = cs * kInvS;
-                            if (want_r) sm.r[pr][t][bsto] = ex * iz;
+                                for (int u = t + 1; u < kC; ++u) {
+                                    P[u] = fmaf(gprev[u], cprev, P[u]);
+                                    asm volatile("" : "+v"(P[u]));   // computed here, not later
+                                }
+                            }
+                            __builtin_amdgcn_sched_barrier(0);
+                            const float z = group_sum<JP>(ex);
+                            const float iz = rcp_fast(z);
+                            const float cs = (bd * ex) * iz;          // s c
+                            if (t + 1 < kC) P[t + 1] = fmaf(grow[t + 1], cs, P[t + 1]);
+                            cb[t & 3] = cs * kInvS;
+                            if ((t & 3) == 3)
+                                *reinterpret_cast<float4 *>(&sm.c[pr][bsto][t - 3]) =
+                                    make_float4(cb[0], cb[1], cb[2], cb[3]);
+                            if constexpr (R) sm.r[pr][t][bsto] = ex * iz;
+                            zmin = fminf(zmin, z);
+                            zmax = fmaxf(zmax, z);
+                            cprev = cs;
 #pragma unroll
-                            for (int u = t + 2; u < kC; ++u) grow[u] = gnext[u];
+                            for (int u = t + 2; u < kC; ++u) gprev[u] = grow[u], grow[u] = gnext[u];
                         }
-                    }
+                        if (__builtin_amdgcn_ballot_w64(bact && !(zmin >= 0x1p-100f && zmax <= 0x1p100f)) != 0) {
+                            // some softmax underflowed: the chunk again, maximum subtracted
+#pragma unroll
+                            for (int u = 1; u < kC; ++u) grow[u] = sm.g[pr][0][u];
+#pragma unroll
+                            for (int t = 0; t < kC; ++t) P[t] = P0[t];
+#pragma unroll
+                            for (int t = 0; t < kC; ++t) {
+                                float gnext[kC];
+#pragma unroll
+                                for (int u = t + 2; u < kC; ++u) gnext[u] = sm.g[pr][t + 1][u];
+                                const float d = vv[t] - P[t];
+                                const float bd = bev[t] * d;
+                                const float e = fmaf(-d, d, lkv[t]);
+                                const float ex = __builtin_amdgcn_exp2f(e - group_max<JP>(e));
+                                const float iz = rcp_fast(group_sum<JP>(ex));
+                                const float cs = (bd * ex) * iz;
+#pragma unroll
+                                for (int u = t + 1; u < kC; ++u) P[u] = fmaf(grow[u], cs, P[u]);
+                                sm.c[pr][bsto][t] = cs * kInvS;
+                                if constexpr (R) sm.r[pr][t][bsto] = ex * iz;
+#pragma unroll
+                                for (int u = t + 2; u < kC; ++u) grow[u] = gnext[u];
+                            }
+                        }
+                    };
+                    if (want_r) run(BoolTag<true>{});
+                    else run(BoolTag<false>{});
                 } else {
                     // ---- B: forward substitution of the linearised recurrence
                     // (eq. linearized) over chunk n; g clamped to [0, 2 / |k_t|^2]
@@ -835,7 +869,7 @@ __global__ __launch_bounds__(320) void scan_pipe_kernel(LayerArgs a, NewtonArgs 
                         const float x = fmaf(gc[t], pold[t] - pt, bb[t]);
 #pragma unroll
                         for (int u = t + 1; u < kC; ++u) P[u] = fmaf(grow[u], x, P[u]);
-                        sm.c[pr][t][bsto] = x;
+                        sm.c[pr][bsto][t] = x;
                         const int tok = n * kC + t;
                         if (bact) {
                             pred[(size_t)tok * N + bcol] = pt;
@@ -949,12 +983,16 @@ __global__ __launch_bounds__(320) void scan_pipe_kernel(LayerArgs a, NewtonArgs 
             block_sync_lds();   // e(n): C_n published (and G'_n)
 
             // ---- P_{n+1} = X_{n+1} + G'_n C_n
+            {
+                const float4 c4 = *reinterpret_cast<const float4 *>(&sm.c[pr][col][4 * lg]);
+                const float cv[4] = {c4.x, c4.y, c4.z, c4.w};
 #pragma unroll
-            for (int m = 0; m < 4; ++m) {
-                __bf16 hi, lo;
-                split(sm.c[pr][4 * lg + m][col], hi, lo);
-                chi[m] = bf16_bits(hi);
-                clo[m] = bf16_bits(lo);
+                for (int m = 0; m < 4; ++m) {
+                    __bf16 hi, lo;
+                    split(cv[m], hi, lo);
+                    chi[m] = bf16_bits(hi);
+                    clo[m] = bf16_bits(lo);
+                }
             }
             if (n + 1 < NCH) {
                 Xacc = mfma16(ghi, chi, Xacc);
