@@ -16,6 +16,7 @@ from __future__ import annotations
 import argparse
 import json
 import os
+import re
 import sys
 import time
 
@@ -44,13 +45,25 @@ MEASURED_TRAFFIC = {
 def measured_traffic(source):
     """Counter-measured HBM bytes per launch of the kernel in ``source``, or None
     when that source has changed since the counters were taken."""
-    import hashlib
-    path = os.path.join(ROOT, "paper_2609_39034_amd", "csrc", source)
     try:
-        digest = hashlib.sha256(open(path, "rb").read()).hexdigest()
+        digest = kernel_source_digest(source)
     except OSError:
         return None
     return MEASURED_TRAFFIC.get((source, digest))
+
+
+def kernel_source_digest(source):
+    """sha256 over ``source`` and the local headers and fragments it includes
+    (one level of ``#include "..."``), in order."""
+    import hashlib
+    csrc = os.path.join(ROOT, "paper_2609_39034_amd", "csrc")
+    text = open(os.path.join(csrc, source), "rb").read()
+    h = hashlib.sha256(text)
+    for name in re.findall(rb'^\s*#include\s+"([^"]+)"', text, re.M):
+        path = os.path.join(csrc, name.decode())
+        if os.path.exists(path):
+            h.update(open(path, "rb").read())
+    return h.hexdigest()
 
 
 def forward_alg_bytes(B, H, T, Dk, Dv, J, in_bytes=2, out_bytes=2, state_in=False,

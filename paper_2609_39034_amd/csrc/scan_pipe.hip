@@ -74,6 +74,7 @@ constexpr int kRingKQ = 4;  // K, Q: chunks n-1 .. n+2 (state update, retrieval 
 constexpr int kRingQP = 3;  // query-prior logits, Newton predictions: n .. n+2
 constexpr int kRingS = 2;   // beta and key-prior logits, v: n+1, n+2 (staged one chunk ahead)
 constexpr int kTP = kC + 4;  // row of a column-major [column][token] staging array
+constexpr int ceil_div(int a, int b) { return (a + b - 1) / b; }
 
 // The sequential wave works in scaled units: with s^2 = log2(e) / 2,
 // d = s (v - pred) makes the E-step exponent log2(e) (lk - delta^2 / 2) a
@@ -101,6 +102,10 @@ __device__ __forceinline__ void split(float x, __bf16 &hi, __bf16 &lo) {
 template <bool B>
 struct BoolTag {
     static constexpr bool value = B;
+};
+template <int V>
+struct IntTag {
+    static constexpr int value = V;
 };
 
 __device__ __forceinline__ void wait_vm() { __builtin_amdgcn_s_waitcnt(0x0F70); }
@@ -213,12 +218,13 @@ __device__ __forceinline__ int first_for(int base, int mw, int nw) {
 
 // Issue the HBM -> LDS transfer of chunk m (starting at token t0) into its
 // ring slots.  The chunk is cut into wave-wide transfers of 64 x 16 bytes
-// (K, Q, the three logit tensors, v), dealt round-robin to the matrix-core
-// waves; each tensor has its own loop so its base address stays a scalar.
+// (K, Q, the three logit tensors, v), dealt round-robin to the NIW waves that
+// do the block's bookkeeping; each tensor has its own loop so its base address
+// stays a scalar.
 // Tokens past T re-read token T - 1 (in range); the recurrence gives them
 // beta = 0.  In Newton mode the chunk's predictions from the previous sweep
 // ([kC][N] fp32 at pred + t0 N, the block's workspace) come along.
-template <int DK, int J, int DB, bool NT>
+template <int DK, int J, int DB, bool NT, int NIW>
 __device__ __forceinline__ void issue_chunk(const LayerArgs &a, PSmem<DK, J, DB, NT> &sm,
                                             uint32_t lds_base, int m, int t0, int b, int h,
                                             int d0, int mw, int lane, const float *pred) {
@@ -239,7 +245,7 @@ __device__ __forceinline__ void issue_chunk(const LayerArgs &a, PSmem<DK, J, DB,
         // K and Q rows: piece p of row t goes to slot p ^ (t mod pieces)
         auto kq = [&](const void *base, uint4 *tile, int ibase) {
             const char *src = static_cast<const char *>(base) + row0 * DK * 2;
-            for (int ins = first_for(ibase, mw, C::NW); ins < ibase + nk; ins += C::NW) {
+            for (int ins = first_for(ibase, mw, NIW); ins < ibase + nk; ins += NIW) {
                 const int part = ins - ibase, s = part * 64 + lane;
                 if (s < C::KPIECES) {
                     const int t = s / C::KPC, p = s % C::KPC, gp = p ^ (t & (C::KPC - 1));
@@ -250,7 +256,7 @@ __device__ __forceinline__ void issue_chunk(const LayerArgs &a, PSmem<DK, J, DB,
         // logits, [t][j][dl]
         auto logit = [&](const void *base, uint4 *dstv, int ibase) {
             const char *src = static_cast<const char *>(base) + (row0 * J * Dv + d0) * 2;
-            for (int ins = first_for(ibase, mw, C::NW); ins < ibase + nl; ins += C::NW) {
+            for (int ins = first_for(ibase, mw, NIW); ins < ibase + nl; ins += NIW) {
                 const int part = ins - ibase, s = part * 64 + lane;
                 if (s < C::LPIECES) {
                     const int t = s / (C::N / 8), rem = s % (C::N / 8);
@@ -265,8 +271,8 @@ __device__ __forceinline__ void issue_chunk(const LayerArgs &a, PSmem<DK, J, DB,
         logit(a.lk, sm.lk[ss], 2 * nk + nl);
         logit(a.lq, sm.lq[sqp], 2 * nk + 2 * nl);
         const char *vsrc = static_cast<const char *>(a.v) + (row0 * Dv + d0) * 2;
-        for (int ins = first_for(2 * nk + 3 * nl, mw, C::NW); ins < 2 * nk + 3 * nl + nv;
-             ins += C::NW) {
+        for (int ins = first_for(2 * nk + 3 * nl, mw, NIW); ins < 2 * nk + 3 * nl + nv;
+             ins += NIW) {
             const int part = ins - (2 * nk + 3 * nl), s = part * 64 + lane;
             if (s < C::VPIECES) {
                 const int t = s / (DB / 8), qd = s % (DB / 8);
@@ -277,7 +283,7 @@ __device__ __forceinline__ void issue_chunk(const LayerArgs &a, PSmem<DK, J, DB,
         const size_t row0 = (size_t)b * T;
         // K and Q rows: piece p of row t goes to slot p ^ (t mod pieces)
         auto kq = [&](const void *base, uint4 *tile, int ibase) {
-            for (int ins = first_for(ibase, mw, C::NW); ins < ibase + nk; ins += C::NW) {
+            for (int ins = first_for(ibase, mw, NIW); ins < ibase + nk; ins += NIW) {
                 const int part = ins - ibase, s = part * 64 + lane;
                 if (s < C::KPIECES) {
                     const int t = s / C::KPC, p = s % C::KPC;
@@ -290,7 +296,7 @@ __device__ __forceinline__ void issue_chunk(const LayerArgs &a, PSmem<DK, J, DB,
         };
         // logits, [t][j][dl]
         auto logit = [&](const void *base, uint4 *dstv, int ibase) {
-            for (int ins = first_for(ibase, mw, C::NW); ins < ibase + nl; ins += C::NW) {
+            for (int ins = first_for(ibase, mw, NIW); ins < ibase + nl; ins += NIW) {
                 const int part = ins - ibase, s = part * 64 + lane;
                 if (s < C::LPIECES) {
                     const int t = s / (C::N / 8), rem = s % (C::N / 8);
@@ -307,8 +313,8 @@ __device__ __forceinline__ void issue_chunk(const LayerArgs &a, PSmem<DK, J, DB,
         logit(a.lb, sm.lb[ss], 2 * nk);
         logit(a.lk, sm.lk[ss], 2 * nk + nl);
         logit(a.lq, sm.lq[sqp], 2 * nk + 2 * nl);
-        for (int ins = first_for(2 * nk + 3 * nl, mw, C::NW); ins < 2 * nk + 3 * nl + nv;
-             ins += C::NW) {
+        for (int ins = first_for(2 * nk + 3 * nl, mw, NIW); ins < 2 * nk + 3 * nl + nv;
+             ins += NIW) {
             const int part = ins - (2 * nk + 3 * nl), s = part * 64 + lane;
             if (s < C::VPIECES) {
                 const int t = s / (DB / 8), qd = s % (DB / 8);
@@ -320,7 +326,7 @@ __device__ __forceinline__ void issue_chunk(const LayerArgs &a, PSmem<DK, J, DB,
     }
     if constexpr (NT) {
         constexpr int ib = 2 * nk + 3 * nl + nv, np = (C::PPIECES + 63) / 64;
-        for (int ins = first_for(ib, mw, C::NW); ins < ib + np; ins += C::NW) {
+        for (int ins = first_for(ib, mw, NIW); ins < ib + np; ins += NIW) {
             const int part = ins - ib, s = part * 64 + lane;
             if (s < C::PPIECES) dma16(pred + (size_t)t0 * C::N + 4 * s, at(sm.pw[sqp] + part * 64));
         }
@@ -400,8 +406,11 @@ __device__ __forceinline__ void pipe_coords(int id, int ndb, int nheads, int &db
     }
 }
 
-template <int DK, int J, int DB, bool NT>
-__global__ __launch_bounds__(320) void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
+// LDS (over 60 KB a block) allows at most two blocks on a compute unit, so at
+// most two waves share a SIMD: the compiler may use every register for that.
+template <int DK, int J, int DB, bool NT, int NH>
+__global__ __launch_bounds__(512)
+void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
     using C = PCfg<DK, J, DB>;
     constexpr int IT = C::IT, N = C::N, NW = C::NW, JP = C::JP;
     __shared__ PSmem<DK, J, DB, NT> sm;
@@ -417,6 +426,20 @@ __global__ __launch_bounds__(320) void scan_pipe_kernel(LayerArgs a, NewtonArgs 
     const int d0 = db * DB, h = hh % H, b = hh / H;
     const int NCH = (T + kC - 1) / kC;
     const bool seq = (w == NW);
+    // Roles: waves 0 .. NW-1 hold the state tiles (matrix-core products);
+    // wave NW is the sequential wave; with NH > 0, waves NW+1 .. NW+NH do the
+    // per-chunk bookkeeping (transfers, priors, input prep, outputs), which the
+    // tile waves do themselves when NH = 0.
+    const bool tile = w < NW;
+    constexpr int NBW = NH == 0 ? NW : NH;            // bookkeeping waves
+    constexpr int NBT = 64 * NBW;                     // bookkeeping threads
+    const int bw = NH == 0 ? w : w - (NW + 1);        // index among them
+    // The compiler cannot bound bt (the wave index comes from readfirstlane), so
+    // loops strided by NBT count 0 .. ceil(n / NBT) from bt and stop at n: a
+    // trip count it can see, and fully unrolled loops.
+    const int bt = 64 * bw + lane;
+    // the wave that forms the Gram matrix of the next chunk for the sequential wave
+    const bool gwave = NH == 0 ? w == 1 % NW : w == NW + 1;
     // Newton mode: this block's predictions, [NCH * kC][N] fp32
     float *const pred = NT ? na.pred + ((size_t)hh * (Dv / DB) + db) * NCH * kC * N : nullptr;
 
@@ -428,7 +451,7 @@ __global__ __launch_bounds__(320) void scan_pipe_kernel(LayerArgs a, NewtonArgs 
     auto load_state = [&]() {
 #pragma unroll
         for (int it = 0; it < IT; ++it) W[it] = floatx4{0.f, 0.f, 0.f, 0.f};
-        if (!seq && a.state_in) {
+        if (tile && a.state_in) {
             // Newton mode reloads W_0 every sweep: an opaque copy of the row
             // stride keeps the compiler from holding all IT * 4 addresses in
             // registers across the sweeps.
@@ -519,7 +542,6 @@ __global__ __launch_bounds__(320) void scan_pipe_kernel(LayerArgs a, NewtonArgs 
     };
     // Per-chunk bookkeeping works on groups of four consecutive columns (or
     // output dims), so that every thread makes one round trip to LDS.
-    static_assert(kC * N / 4 == C::NMT, "one column group per matrix-core thread");
     // Work per (t, dl) over the J components (priors, outputs, Newton
     // linearisation) is spread over every matrix-core thread: PE consecutive
     // output dims per thread.
@@ -527,13 +549,17 @@ __global__ __launch_bounds__(320) void scan_pipe_kernel(LayerArgs a, NewtonArgs 
     constexpr int NPG = kC * DB / PE;   // (t, dl) groups per chunk
     // When the groups fill at most half of the threads (J = 8), the query
     // prior takes the first half and the outputs the second.
-    constexpr int OUT0 = 2 * NPG <= C::NMT ? C::NMT - NPG : 0;
+    constexpr int OUT0 = 2 * NPG <= NBT ? NBT - NPG : 0;
     // derived inputs of chunk m (parity pr) for the sequential wave
     auto prep_seq_inputs = [&](int m, int pr) {
         const int rs = m % kRingS;
         if constexpr (!NT) {
+#pragma unroll
+          for (int i_ = 0; i_ < ceil_div(kC * N / 4, NBT); ++i_) {
+            const int g4 = bt + i_ * NBT;
+            if (g4 >= kC * N / 4) break;
             // four consecutive columns (dims dl .. dl+3 of one component) of token t
-            const int e4 = 4 * tid, t = e4 / N, cc = e4 % N;
+            const int e4 = 4 * g4, t = e4 / N, cc = e4 % N;
             const bool ok = m * kC + t < T;
             float lbv[4], lkv[4];
             bf16_row<4>(sm.lb[rs], e4, lbv);
@@ -543,13 +569,18 @@ __global__ __launch_bounds__(320) void scan_pipe_kernel(LayerArgs a, NewtonArgs 
                                  ok ? sigmoid(lbv[1]) : 0.f, lkv[1] * kLog2e);
             dst[1] = make_float4(ok ? sigmoid(lbv[2]) : 0.f, lkv[2] * kLog2e,
                                  ok ? sigmoid(lbv[3]) : 0.f, lkv[3] * kLog2e);
-            if (tid < kC * DB / 4) {
+          }
+#pragma unroll
+          for (int i_ = 0; i_ < ceil_div(kC * DB / 4, NBT); ++i_) {
+            const int g4 = bt + i_ * NBT;
+            if (g4 >= kC * DB / 4) break;
+                const int e4 = 4 * g4;
                 float vv[4];
                 bf16_row<4>(sm.v[rs], e4, vv);
 #pragma unroll
                 for (int u = 0; u < 4; ++u) vv[u] *= kS;
                 f32_row<4>(&sm.vs[pr][e4 / DB][e4 % DB], vv);
-            }
+          }
         } else {
             // Linearisation around the previous sweep's predictions (App. D.2),
             // per (t, dl) over the J components: delta, r (eq. responsibility),
@@ -557,7 +588,9 @@ __global__ __launch_bounds__(320) void scan_pipe_kernel(LayerArgs a, NewtonArgs 
             // input (eq. effective_input); the sequential wave adds g pred^(i).
             const float *po = reinterpret_cast<const float *>(sm.pw[m % kRingQP]);
 #pragma unroll
-            for (int gi = tid; gi < NPG; gi += C::NMT) {
+            for (int i_ = 0; i_ < ceil_div(NPG, NBT); ++i_) {
+            const int gi = bt + i_ * NBT;
+            if (gi >= NPG) break;
                 const int e = PE * gi, t = e / DB, dl = e % DB;
                 const bool ok = m * kC + t < T;
                 float vv[PE];
@@ -608,7 +641,9 @@ __global__ __launch_bounds__(320) void scan_pipe_kernel(LayerArgs a, NewtonArgs 
     auto prep_query_prior = [&](int m, int pr) {
         const int rs = m % kRingQP;
 #pragma unroll
-        for (int gi = tid; gi < NPG; gi += C::NMT) {
+        for (int i_ = 0; i_ < ceil_div(NPG, NBT); ++i_) {
+            const int gi = bt + i_ * NBT;
+            if (gi >= NPG) break;
             const int e = PE * gi, t = e / DB, dl = e % DB;
             float x[J][PE], mq[PE], z[PE];
 #pragma unroll
@@ -639,8 +674,9 @@ __global__ __launch_bounds__(320) void scan_pipe_kernel(LayerArgs a, NewtonArgs 
     // o of chunk m: sum over j of pi^q * retrieval
     auto store_output = [&](int m, int pr) {
 #pragma unroll
-        for (int gi = tid - OUT0; gi < NPG; gi += C::NMT) {
-            if (gi < 0) break;
+        for (int i_ = 0; i_ < ceil_div(NPG, NBT); ++i_) {
+            const int gi = bt - OUT0 + i_ * NBT;
+            if (gi < 0 || gi >= NPG) break;   // gi < 0: a thread of the query-prior half
             const int e = PE * gi, t = e / DB, dl = e % DB;
             if (m * kC + t < T) {
                 float o[PE], y[PE];
@@ -662,11 +698,16 @@ __global__ __launch_bounds__(320) void scan_pipe_kernel(LayerArgs a, NewtonArgs 
     };
     auto store_resp = [&](int m, int pr) {
         if constexpr (!NT) {
-            const int e4 = 4 * tid, t = e4 / N, cc = e4 % N;
+#pragma unroll
+          for (int i_ = 0; i_ < ceil_div(kC * N / 4, NBT); ++i_) {
+            const int g4 = bt + i_ * NBT;
+            if (g4 >= kC * N / 4) break;
+            const int e4 = 4 * g4, t = e4 / N, cc = e4 % N;
             if (m * kC + t < T)
                 *reinterpret_cast<float4 *>(
                     a.resp + ((((size_t)b * T + m * kC + t) * H + h) * J + cc / DB) * Dv + d0 +
                     cc % DB) = *reinterpret_cast<const float4 *>(&sm.r[pr][t][cc]);
+          }
         }
     };
     // W += K_m^T C_m and Y += tril(A_m) C_m (C_m split in chi/clo); then
@@ -702,7 +743,7 @@ __global__ __launch_bounds__(320) void scan_pipe_kernel(LayerArgs a, NewtonArgs 
     if constexpr (NT) {
         // Iterate 0 (the initial guess w_t = W_0 for every t): pred_t = k_t . W_0,
         // straight from HBM rows of K, chunk by chunk.
-        if (!seq) {
+        if (tile) {
             bf16x8 whi[IT / 2 > 0 ? IT / 2 : 1], wlo[IT / 2 > 0 ? IT / 2 : 1];
             short4v w16hi, w16lo;
             split_state(whi, wlo, w16hi, w16lo);
@@ -905,130 +946,18 @@ __global__ __launch_bounds__(320) void scan_pipe_kernel(LayerArgs a, NewtonArgs 
         return;
     }
 
-    int sweeps = 0;
-    bool done = false;
-    while (!done) {
-        ++sweeps;
-        if (NT && sweeps > 1) {
-            load_state();
-            Yacc = floatx4{0.f, 0.f, 0.f, 0.f};
-        }
-        // ---------------- prologue: chunks 0 and 1 into the ring; P_0, G_0
-        // (t0 is an opaque zero so that, in Newton mode, the compiler does not
-        // hoist these transfers' addresses out of the sweep loop and hold them)
-        int t0 = 0;
-        asm volatile("" : "+s"(t0));
-        issue_chunk<DK, J, DB, NT>(a, sm, lds_base, 0, t0, b, h, d0, w, lane, pred);
-        if (NCH > 1) issue_chunk<DK, J, DB, NT>(a, sm, lds_base, 1, t0 + kC, b, h, d0, w, lane, pred);
-        wait_vm();
-        block_sync_lds();
-        {
-            prep_seq_inputs(0, 0);
-            bf16x8 whi[IT / 2 > 0 ? IT / 2 : 1], wlo[IT / 2 > 0 ? IT / 2 : 1];
-            short4v w16hi, w16lo;
-            split_state(whi, wlo, w16hi, w16lo);
-            const floatx4 P0 = tile_times_state(sm.k[0], floatx4{0.f, 0.f, 0.f, 0.f}, whi, wlo,
-                                                w16hi, w16lo);
-            *reinterpret_cast<float4 *>(&sm.p[0][col][4 * lg]) = make_float4(P0[0], P0[1], P0[2], P0[3]);
-            if (w == 0) {
-                const floatx4 G0 = gram(sm.k[0], sm.k[0]);
-#pragma unroll
-                for (int r = 0; r < 4; ++r) sm.g[0][4 * lg + r][tl] = G0[r];
-            }
-        }
-        block_sync_lds();
-
-        for (int n = 0; n < NCH; ++n) {
-            const int pr = n & 1, rs = n % kRingKQ, rn = (n + 1) % kRingKQ;
-            // Chunk n+2 first, so that the transfer has the whole chunk to
-            // land; its ring slots held chunks n-2 (K, Q), n (beta and key-prior
-            // logits, v) and n-1 (query-prior logits, predictions), all used up.
-            if (n + 2 < NCH)
-                issue_chunk<DK, J, DB, NT>(a, sm, lds_base, n + 2, (n + 2) * kC, b, h, d0, w, lane, pred);
-            // ---- matrix-core waves, while the sequential wave runs chunk n
-            if (n >= 1) {
-                finish_chunk(n - 1);                 // S_n, pi^q Y_{n-1}
-                if (a.resp) store_resp(n - 1, (n - 1) & 1);
-            }
-            if (n >= 2) store_output(n - 2, n & 1);  // (n - 2) & 1 == n & 1
-            {
-                bf16x8 whi[IT / 2 > 0 ? IT / 2 : 1], wlo[IT / 2 > 0 ? IT / 2 : 1];
-                short4v w16hi, w16lo;
-                split_state(whi, wlo, w16hi, w16lo);
-                Yacc = tile_times_state(sm.q[rs], floatx4{0.f, 0.f, 0.f, 0.f}, whi, wlo, w16hi,
-                                        w16lo);
-                if (n + 1 < NCH)
-                    Xacc = tile_times_state(sm.k[rn], floatx4{0.f, 0.f, 0.f, 0.f},
-                                            whi, wlo, w16hi, w16lo);
-            }
-            if (n + 1 < NCH) {
-                // G'_n = K_{n+1} K_n^T as the A operand of G'_n C_n: the accumulator
-                // layout of K_n K_{n+1}^T, split in registers
-                const floatx4 gt = gram(sm.k[rs], sm.k[rn]);
-#pragma unroll
-                for (int m = 0; m < 4; ++m) {
-                    __bf16 hi, lo;
-                    split(gt[m], hi, lo);
-                    ghi[m] = bf16_bits(hi);
-                    glo[m] = bf16_bits(lo);
-                }
-            }
-            if (w == (1 % NW) && n + 1 < NCH) {
-                const floatx4 g1 = gram(sm.k[rn], sm.k[rn]);
-#pragma unroll
-                for (int r = 0; r < 4; ++r) sm.g[pr ^ 1][4 * lg + r][tl] = g1[r];
-            }
-            prep_query_prior(n, pr);
-            if (n + 1 < NCH) prep_seq_inputs(n + 1, pr ^ 1);
-            block_sync_lds();   // e(n): C_n published (and G'_n)
-
-            // ---- P_{n+1} = X_{n+1} + G'_n C_n
-            {
-                const float4 c4 = *reinterpret_cast<const float4 *>(&sm.c[pr][col][4 * lg]);
-                const float cv[4] = {c4.x, c4.y, c4.z, c4.w};
-#pragma unroll
-                for (int m = 0; m < 4; ++m) {
-                    __bf16 hi, lo;
-                    split(cv[m], hi, lo);
-                    chi[m] = bf16_bits(hi);
-                    clo[m] = bf16_bits(lo);
-                }
-            }
-            if (n + 1 < NCH) {
-                Xacc = mfma16(ghi, chi, Xacc);
-                Xacc = mfma16(ghi, clo, Xacc);
-                Xacc = mfma16(glo, chi, Xacc);
-#pragma unroll
-                for (int r = 0; r < 4; ++r) sm.p[pr ^ 1][col][4 * lg + r] = Xacc[r];
-            }
-            wait_vm();          // chunk n+2 has landed in LDS
-            block_sync_lds();   // i(n+1)
-        }
-
-        // ---------------- epilogue: last state update and the last two outputs
-        finish_chunk(NCH - 1);
-        if (a.resp) store_resp(NCH - 1, (NCH - 1) & 1);
-        if (NCH >= 2) store_output(NCH - 2, NCH & 1);
-        block_sync_lds();
-        store_output(NCH - 1, (NCH - 1) & 1);
-        if constexpr (NT) {
-            block_sync_lds();   // the sequential wave has set the stopping flag
-            const bool met = sm.flag != 0;
-            done = met || sweeps >= na.max_iters;
-            if (done && tid == 0 && na.iters) {
-                atomicMax(na.iters, sweeps);
-                if (!met && na.tol >= 0.f) atomicAdd(na.iters + 1, 1);
-            }
-        } else {
-            done = true;
-        }
-    }
-    if (a.state_out) {
-#pragma unroll
-        for (int it = 0; it < IT; ++it)
-#pragma unroll
-            for (int r = 0; r < 4; ++r)
-                a.state_out[sbase + (size_t)(16 * it + 4 * lg + r) * Dv] = W[it][r];
+    // The matrix-core side, one copy per role: with NH = 0 the tile waves also
+    // do the bookkeeping; with NH > 0 the tile waves and the helper waves run
+    // copies of their own that meet the same barriers.
+    if constexpr (NH == 0) {
+        constexpr bool DT = true, DBK = true;
+#include "scan_pipe_mfma_side.inc"
+    } else if (tile) {
+        constexpr bool DT = true, DBK = false;
+#include "scan_pipe_mfma_side.inc"
+    } else {
+        constexpr bool DT = false, DBK = true;
+#include "scan_pipe_mfma_side.inc"
     }
 }
 
@@ -1039,10 +968,20 @@ __global__ void int_fill_kernel(int *p, int n, int value) {
 template <int DK, int J, int DB, bool NT>
 hipError_t launch_cfg(const LayerArgs &a, const NewtonArgs &na, hipStream_t stream) {
     using C = PCfg<DK, J, DB>;
-    static_assert(sizeof(PSmem<DK, J, DB, NT>) <= 160 * 1024, "LDS");
+    constexpr size_t lds = sizeof(PSmem<DK, J, DB, NT>);
+    static_assert(lds <= 160 * 1024, "LDS");
     const long blocks = (long)(a.Dv / DB) * a.H * a.B;
-    hipLaunchKernelGGL((scan_pipe_kernel<DK, J, DB, NT>), dim3((unsigned)blocks), dim3(C::NT), 0,
-                       stream, a, na);
+    // Enough blocks to put two on every compute unit (LDS permitting): their
+    // waves hide each other's latencies, so the tile waves keep the
+    // bookkeeping.  Otherwise helper waves take it over.
+    constexpr int NH = NT ? 0 : (C::NW < 3 ? C::NW : 3);
+    if (NH == 0 || (blocks >= 512 && lds <= 80 * 1024)) {
+        hipLaunchKernelGGL((scan_pipe_kernel<DK, J, DB, NT, 0>), dim3((unsigned)blocks),
+                           dim3(64 * (C::NW + 1)), 0, stream, a, na);
+    } else {
+        hipLaunchKernelGGL((scan_pipe_kernel<DK, J, DB, NT, NH>), dim3((unsigned)blocks),
+                           dim3(64 * (C::NW + 1 + NH)), 0, stream, a, na);
+    }
     return hipGetLastError();
 }
 
