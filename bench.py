@@ -34,11 +34,9 @@ PEAK_MFMA_BF16 = 2.5e15    # FLOP/s, MI355X dense bf16 matrix
 # same counters on a plain 1 GiB copy (FETCH x2.0, WRITE x1.0); valid only for the
 # kernel source they were measured on (summary in profiles/).
 MEASURED_TRAFFIC = {
-    ("decode.hip", "769b72fdca36c7f4df23d3fb1d410dc16c3c323568a37067ebabab4fb4b755be"): 2184302284,
-    ("scan_direct.hip", "b38c28c5de8d782d7e8789d36b1d92720d8a6715bdb2781db527a2d9cdf2e1ba"):
-        136540979,
-    ("scan_pipe.hip", "5cda4c1befe00ba76f4c4d773bcef2b66597decf1999ae075ca64c8abbb7ea4d"):
-        136676608,
+    ("decode.hip", "d4bb8e3129fba693ae0d7e4f65fe205210ec56e8df246af4a7ff5599efab912f"): 2184301248,
+    ("scan_pipe.hip", "ed7cab280194b1de5538dcc55ed2797bfbd2d49516ae896064a0d63f646563d0"):
+        136662720,
 }
 
 
