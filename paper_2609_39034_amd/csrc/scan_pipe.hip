@@ -139,15 +139,18 @@ struct PSmem {
     uint4 v[kRingS][C::VPIECES];
     uint4 pw[NT ? kRingQP : 1][NT ? C::PPIECES : 1];  // Newton: previous sweep's predictions
     union {
-        float2 sq[2][kC][C::N];     // exact: {beta, log2(e) key-prior logit} per (t, column)
+        // exact: {beta, log2(e) key-prior logit}, [column][token]; a column's
+        // 16 tokens are 128 contiguous bytes, padded so that the sequential
+        // wave's 16-byte reads of adjacent columns fall in distinct banks
+        alignas(16) float2 sq[2][C::N][kC + 2];
         struct {
             float beta[2][kC][C::NP];   // Newton: g (before the clamp)
             float lks[2][kC][C::NP];    // Newton: beta r delta
         };
     };
-    float vs[NT ? 1 : 2][kC][DB + 4];   // exact: s v
+    alignas(16) float vs[NT ? 1 : 2][DB][kC + 4];   // exact: s v, [dim][token]
     float pq[2][kC][C::NP];    // query prior
-    float g[2][kC][kC + 4];    // K_n K_n^T, for the sequential wave
+    alignas(16) float g[2][kC][kC + 4];    // K_n K_n^T, for the sequential wave
     float p[2][C::N][kTP];     // chunk-start predictions, [column][token]
     float c[2][C::N + 1][kTP];  // coefficients, [column][token] (column N: idle lanes)
     float r[NT ? 1 : 2][kC][C::NP];  // responsibilities (exact mode)
@@ -448,6 +451,11 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
     const int jc = col / DB, dc = d0 + col % DB;
     const size_t sbase = (((size_t)b * H + h) * J + jc) * DK * Dv + dc;
     floatx4 W[IT];
+    // Exact mode keeps the state, and with it every product the sequential wave
+    // consumes (predictions, coefficients), in the scaled units s = sqrt(log2(e)/2)
+    // of its recurrence, so that the critical path carries no conversions; the
+    // state is converted on the way in and out, the retrieval by the query prior.
+    constexpr float kWS = NT ? 1.f : kS, kInvWS = NT ? 1.f : kInvS;
     auto load_state = [&]() {
 #pragma unroll
         for (int it = 0; it < IT; ++it) W[it] = floatx4{0.f, 0.f, 0.f, 0.f};
@@ -461,7 +469,7 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
 #pragma unroll
             for (int it = 0; it < IT; ++it)
 #pragma unroll
-                for (int r = 0; r < 4; ++r) W[it][r] = src[(size_t)(16 * it + r) * dv];
+                for (int r = 0; r < 4; ++r) W[it][r] = kWS * src[(size_t)(16 * it + r) * dv];
         }
     };
     load_state();
@@ -564,11 +572,9 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
             float lbv[4], lkv[4];
             bf16_row<4>(sm.lb[rs], e4, lbv);
             bf16_row<4>(sm.lk[rs], e4, lkv);
-            float4 *dst = reinterpret_cast<float4 *>(&sm.sq[pr][t][cc]);
-            dst[0] = make_float4(ok ? sigmoid(lbv[0]) : 0.f, lkv[0] * kLog2e,
-                                 ok ? sigmoid(lbv[1]) : 0.f, lkv[1] * kLog2e);
-            dst[1] = make_float4(ok ? sigmoid(lbv[2]) : 0.f, lkv[2] * kLog2e,
-                                 ok ? sigmoid(lbv[3]) : 0.f, lkv[3] * kLog2e);
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                sm.sq[pr][cc + u][t] = make_float2(ok ? sigmoid(lbv[u]) : 0.f, lkv[u] * kLog2e);
           }
 #pragma unroll
           for (int i_ = 0; i_ < ceil_div(kC * DB / 4, NBT); ++i_) {
@@ -578,8 +584,7 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
                 float vv[4];
                 bf16_row<4>(sm.v[rs], e4, vv);
 #pragma unroll
-                for (int u = 0; u < 4; ++u) vv[u] *= kS;
-                f32_row<4>(&sm.vs[pr][e4 / DB][e4 % DB], vv);
+                for (int u = 0; u < 4; ++u) sm.vs[pr][e4 % DB + u][e4 / DB] = kS * vv[u];
           }
         } else {
             // Linearisation around the previous sweep's predictions (App. D.2),
@@ -662,7 +667,7 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
                     z[u] += x[j][u];
                 }
 #pragma unroll
-            for (int u = 0; u < PE; ++u) z[u] = rcp_fast(z[u]);
+            for (int u = 0; u < PE; ++u) z[u] = kInvWS * rcp_fast(z[u]);
 #pragma unroll
             for (int j = 0; j < J; ++j) {
 #pragma unroll
@@ -783,13 +788,37 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
         while (!done) {
             ++sweeps;
             float dmax = 0.f, pmax = 0.f;   // Newton: largest change, largest prediction
+            // Exact mode: the per-token inputs of the next chunk and the first row
+            // of its Gram matrix, read while the matrix-core waves form its
+            // predictions (between the two barriers), off the critical path.
+            float vvN[kC], lkvN[kC], bevN[kC], growN[kC];
+            auto fetch_inputs = [&](int prn) {
+                // 16-byte reads: few enough to be in flight together
+                const float4 *sq4 = reinterpret_cast<const float4 *>(sm.sq[prn][bcol]);
+                const float4 *vs4 = reinterpret_cast<const float4 *>(sm.vs[prn][bdl]);
+                const float4 *g4 = reinterpret_cast<const float4 *>(sm.g[prn][0]);
+#pragma unroll
+                for (int i = 0; i < kC / 2; ++i) {
+                    const float4 x = sq4[i];
+                    bevN[2 * i] = x.x, lkvN[2 * i] = x.y, bevN[2 * i + 1] = x.z, lkvN[2 * i + 1] = x.w;
+                }
+#pragma unroll
+                for (int i = 0; i < kC / 4; ++i) {
+                    const float4 x = vs4[i], y = g4[i];
+                    vvN[4 * i] = x.x, vvN[4 * i + 1] = x.y, vvN[4 * i + 2] = x.z, vvN[4 * i + 3] = x.w;
+                    growN[4 * i] = y.x, growN[4 * i + 1] = y.y, growN[4 * i + 2] = y.z, growN[4 * i + 3] = y.w;
+                }
+            };
             block_sync_lds();               // prologue: ring filled
             block_sync_lds();               // prologue: P_0, G_0
+            if constexpr (!NT) fetch_inputs(0);
             for (int n = 0; n < NCH; ++n) {
                 const int pr = n & 1;
                 float grow[kC];
+                if constexpr (NT) {
 #pragma unroll
-                for (int u = 1; u < kC; ++u) grow[u] = sm.g[pr][0][u];
+                    for (int u = 1; u < kC; ++u) grow[u] = sm.g[pr][0][u];
+                }
                 if constexpr (!NT) {
                     // ---- B: the token recurrence of chunk n, in scaled units.
                     // The softmax over j runs without subtracting its maximum: for
@@ -798,24 +827,24 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
                     // [2^-100, 2^100] (every component underflowing, or a logit
                     // beyond about 60), the chunk is run again with the maximum
                     // subtracted.
-                    float P[kC], P0[kC], vv[kC], lkv[kC], bev[kC];
-#pragma unroll
-                    for (int t = 0; t < kC; t += 4) {
-                        const float4 p4 = *reinterpret_cast<const float4 *>(&sm.p[pr][bcol][t]);
-                        P[t] = kS * p4.x, P[t + 1] = kS * p4.y, P[t + 2] = kS * p4.z, P[t + 3] = kS * p4.w;
-                    }
+                    float P[kC], vv[kC], lkv[kC], bev[kC];
 #pragma unroll
                     for (int t = 0; t < kC; ++t) {
-                        const float2 x = sm.sq[pr][t][bcol];
-                        bev[t] = x.x, lkv[t] = x.y, vv[t] = sm.vs[pr][t][bdl];
-                    }
-#pragma unroll
-                    for (int t = 0; t < kC; ++t) {
-                        P0[t] = P[t];
                         // padding component of J = 3: no mass; idle lanes: harmless
-                        lkv[t] = bpad ? -INFINITY : lkv[t];
-                        bev[t] = bact ? bev[t] : 0.f;
+                        vv[t] = vvN[t];
+                        lkv[t] = bpad ? -INFINITY : lkvN[t];
+                        bev[t] = bact ? bevN[t] : 0.f;
                     }
+#pragma unroll
+                    for (int u = 1; u < kC; ++u) grow[u] = growN[u];
+                    auto load_pred = [&]() {
+#pragma unroll
+                        for (int t = 0; t < kC; t += 4) {
+                            const float4 p4 = *reinterpret_cast<const float4 *>(&sm.p[pr][bcol][t]);
+                            P[t] = p4.x, P[t + 1] = p4.y, P[t + 2] = p4.z, P[t + 3] = p4.w;
+                        }
+                    };
+                    load_pred();
                     // Software-pipelined: token t updates only P[t+1] at once; its
                     // other updates (P[u], u > t+1) run during token t+1, between
                     // the exponential and the sum over j, where they fill the wait.
@@ -825,12 +854,18 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
                     // whether r is wanted is taken once per chunk.
                     auto run = [&](auto want) {
                         constexpr bool R = decltype(want)::value;
-                        float zmin = 1.f, zmax = 1.f, cprev = 0.f, gprev[kC], cb[4];
+                        // zmin tracks min(z, 1/z): below 2^-100 iff z left the range
+                        float zmin = 1.f, cprev = 0.f, gprev[kC], cb[4];
 #pragma unroll
                         for (int t = 0; t < kC; ++t) {
+                            // row t+1 of G from column t+2 on, in 16-byte reads
                             float gnext[kC];
 #pragma unroll
-                            for (int u = t + 2; u < kC; ++u) gnext[u] = sm.g[pr][t + 1][u];
+                            for (int q4 = (t + 2) / 4; q4 < kC / 4; ++q4) {
+                                const float4 x = *reinterpret_cast<const float4 *>(&sm.g[pr][t + 1][4 * q4]);
+                                gnext[4 * q4] = x.x, gnext[4 * q4 + 1] = x.y;
+                                gnext[4 * q4 + 2] = x.z, gnext[4 * q4 + 3] = x.w;
+                            }
                             const float d = vv[t] - P[t];
                             const float bd = bev[t] * d;
                             const float ex = __builtin_amdgcn_exp2f(fmaf(-d, d, lkv[t]));
@@ -847,23 +882,21 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
                             const float iz = rcp_fast(z);
                             const float cs = (bd * ex) * iz;          // s c
                             if (t + 1 < kC) P[t + 1] = fmaf(grow[t + 1], cs, P[t + 1]);
-                            cb[t & 3] = cs * kInvS;
+                            cb[t & 3] = cs;
                             if ((t & 3) == 3)
                                 *reinterpret_cast<float4 *>(&sm.c[pr][bsto][t - 3]) =
                                     make_float4(cb[0], cb[1], cb[2], cb[3]);
                             if constexpr (R) sm.r[pr][t][bsto] = ex * iz;
-                            zmin = fminf(zmin, z);
-                            zmax = fmaxf(zmax, z);
+                            zmin = fminf(zmin, fminf(z, iz));
                             cprev = cs;
 #pragma unroll
                             for (int u = t + 2; u < kC; ++u) gprev[u] = grow[u], grow[u] = gnext[u];
                         }
-                        if (__builtin_amdgcn_ballot_w64(bact && !(zmin >= 0x1p-100f && zmax <= 0x1p100f)) != 0) {
+                        if (__builtin_amdgcn_ballot_w64(bact && !(zmin >= 0x1p-100f)) != 0) {
                             // some softmax underflowed: the chunk again, maximum subtracted
 #pragma unroll
                             for (int u = 1; u < kC; ++u) grow[u] = sm.g[pr][0][u];
-#pragma unroll
-                            for (int t = 0; t < kC; ++t) P[t] = P0[t];
+                            load_pred();
 #pragma unroll
                             for (int t = 0; t < kC; ++t) {
                                 float gnext[kC];
@@ -877,7 +910,7 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
                                 const float cs = (bd * ex) * iz;
 #pragma unroll
                                 for (int u = t + 1; u < kC; ++u) P[u] = fmaf(grow[u], cs, P[u]);
-                                sm.c[pr][bsto][t] = cs * kInvS;
+                                sm.c[pr][bsto][t] = cs;
                                 if constexpr (R) sm.r[pr][t][bsto] = ex * iz;
 #pragma unroll
                                 for (int u = t + 2; u < kC; ++u) grow[u] = gnext[u];
@@ -924,7 +957,15 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
                     }
                 }
                 block_sync_lds();   // e(n): C_n published
-                block_sync_lds();   // i(n+1): P_{n+1} ready
+                if constexpr (!NT) {
+                    if (n + 1 < NCH) fetch_inputs(pr ^ 1);
+                    // i(n+1), P_{n+1} ready.  This wave has no LDS stores in
+                    // flight here, and nothing rewrites the slots it is reading
+                    // before i(n+2): its reads may land after the barrier.
+                    asm volatile("s_barrier" ::: "memory");
+                } else {
+                    block_sync_lds();   // i(n+1): P_{n+1} ready
+                }
             }
             block_sync_lds();       // epilogue
             if constexpr (NT) {
