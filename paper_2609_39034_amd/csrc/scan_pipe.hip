@@ -866,22 +866,48 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
                                 gnext[4 * q4] = x.x, gnext[4 * q4 + 1] = x.y;
                                 gnext[4 * q4 + 2] = x.z, gnext[4 * q4 + 3] = x.w;
                             }
+                            // The deferred updates of this token (c_{t-1} into P[u],
+                            // u > t) in four parts, one in each latency gap of the
+                            // dependent chain d, exponent, exp2, sum over j, 1 / z,
+                            // P[t+1]; the scheduling barriers keep every part in its
+                            // gap and the empty asm pins keep the compiler from
+                            // sinking the updates into a later token.
+                            auto defer = [&](int part) {
+                                if (t >= 1) {
+                                    const int F = kC - 1 - t;
+                                    const int lo = t + 1 + F * part / 4, hi = t + 1 + F * (part + 1) / 4;
+#pragma unroll
+                                    for (int u = lo; u < hi; ++u) {
+                                        P[u] = fmaf(gprev[u], cprev, P[u]);
+                                        asm volatile("" : "+v"(P[u]));
+                                    }
+                                }
+                            };
                             const float d = vv[t] - P[t];
                             const float bd = bev[t] * d;
                             const float ex = __builtin_amdgcn_exp2f(fmaf(-d, d, lkv[t]));
                             __builtin_amdgcn_sched_barrier(0);
-                            if (t >= 1) {
-#pragma unroll
-                                for (int u = t + 1; u < kC; ++u) {
-                                    P[u] = fmaf(gprev[u], cprev, P[u]);
-                                    asm volatile("" : "+v"(P[u]));   // computed here, not later
-                                }
-                            }
+                            defer(0);
                             __builtin_amdgcn_sched_barrier(0);
-                            const float z = group_sum<JP>(ex);
+                            float z = ex;
+                            if constexpr (JP >= 2) z += dpp_mov<0xb1>(z);   // lane ^ 1
+                            const float bdex = bd * ex;
+                            const float gb = t + 1 < kC ? grow[t + 1] * bdex : 0.f;
+                            __builtin_amdgcn_sched_barrier(0);
+                            defer(1);
+                            __builtin_amdgcn_sched_barrier(0);
+                            if constexpr (JP >= 4) z += dpp_mov<0x4e>(z);   // lane ^ 2
+                            if constexpr (JP >= 8) z += dpp_mov<0x141>(z);  // other quad of 8
+                            if constexpr (JP >= 16) z += dpp_mov<0x140>(z); // other half of 16
+                            __builtin_amdgcn_sched_barrier(0);
+                            defer(2);
+                            __builtin_amdgcn_sched_barrier(0);
                             const float iz = rcp_fast(z);
-                            const float cs = (bd * ex) * iz;          // s c
-                            if (t + 1 < kC) P[t + 1] = fmaf(grow[t + 1], cs, P[t + 1]);
+                            __builtin_amdgcn_sched_barrier(0);
+                            defer(3);
+                            __builtin_amdgcn_sched_barrier(0);
+                            if (t + 1 < kC) P[t + 1] = fmaf(gb, iz, P[t + 1]);
+                            const float cs = bdex * iz;                  // s c
                             cb[t & 3] = cs;
                             if ((t & 3) == 3)
                                 *reinterpret_cast<float4 *>(&sm.c[pr][bsto][t - 3]) =
