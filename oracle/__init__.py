@@ -5,8 +5,10 @@ written from the paper:
 
 * ``forward`` / ``decode_step`` -- the recurrence, E-step and retrieval of
   Sec. 3.2 (eq. recurrence, eq. responsibility, eq. retrieval), with beta and
-  the two priors produced from logits as App. B.2 states.  Backed by the C file
-  ``swila_oracle.c`` next to this module (compiled here with gcc on first use).
+  the two priors produced from logits as App. B.2 states; with gate logits,
+  the temporal priors of Temporal SwiLA (Sec. 3.3, App. B.3).  Backed by the C
+  file ``swila_oracle.c`` next to this module (compiled here with gcc on first
+  use).
 * ``newton`` (submodule) -- the chunkwise parallel quasi-Newton iteration of
   App. D (eqs. jacobian_coeff, effective_input, lambda, aggregate_transition,
   aggregate_history, boundary, parallel_output) in NumPy fp64.
@@ -50,6 +52,8 @@ def load_library(path):
     dp = ctypes.POINTER(ctypes.c_double)
     lib.swila_oracle_forward.argtypes = [ctypes.c_int] * 6 + [dp] * 11 + [ctypes.c_int]
     lib.swila_oracle_forward.restype = ctypes.c_int
+    lib.swila_oracle_forward_temporal.argtypes = [ctypes.c_int] * 6 + [dp] * 15 + [ctypes.c_int]
+    lib.swila_oracle_forward_temporal.restype = ctypes.c_int
     return lib
 
 
@@ -72,6 +76,7 @@ def _ptr(x):
 
 
 def forward(q, k, v, beta_logit, prior_k_logit, prior_q_logit, state_in=None, *,
+            gate_k_logit=None, gate_q_logit=None, prior_in=None,
             nthreads: int = 0, want_resp: bool = False, want_delta: bool = False,
             lib=None):
     """Run the recurrence over a whole sequence.
@@ -82,6 +87,13 @@ def forward(q, k, v, beta_logit, prior_k_logit, prior_q_logit, state_in=None, *,
     ``state`` [B,H,J,Dk,Dv] and, on request, ``resp`` (the key-side
     responsibilities r) and ``delta`` (the prediction errors), both
     [B,T,H,J,Dv].
+
+    Temporal SwiLA (App. B.3): with ``gate_k_logit`` and ``gate_q_logit``
+    ([B,T,H,Dv], both or neither) the priors are the running mixtures of the
+    previous responsibilities (key side) or previous prior (query side) with
+    the new softmax priors; ``prior_in`` is the carried prior state
+    [B,H,2,J,Dv] (part 0: r_{t-1}, part 1: rhobar_{t-1}) or None (uniform 1/J),
+    and the result then also holds ``prior``, the final prior state.
     """
     q, k, v = _f64(q), _f64(k), _f64(v)
     lb, lk, lq = _f64(beta_logit), _f64(prior_k_logit), _f64(prior_q_logit)
@@ -98,12 +110,28 @@ def forward(q, k, v, beta_logit, prior_k_logit, prior_q_logit, state_in=None, *,
     s_out = np.zeros((B, H, J, Dk, Dv))
     resp = np.zeros((B, T, H, J, Dv)) if want_resp else None
     delta = np.zeros((B, T, H, J, Dv)) if want_delta else None
-    rc = (lib or _load()).swila_oracle_forward(
-        B, H, T, Dk, Dv, J, _ptr(q), _ptr(k), _ptr(v), _ptr(lb), _ptr(lk), _ptr(lq),
-        _ptr(s_in), _ptr(s_out), _ptr(o), _ptr(resp), _ptr(delta), int(nthreads))
+    temporal = gate_k_logit is not None or gate_q_logit is not None
+    if temporal:
+        gk, gq, p_in = _f64(gate_k_logit), _f64(gate_q_logit), _f64(prior_in)
+        assert gk is not None and gq is not None, "both gate logits are needed"
+        assert gk.shape == (B, T, H, Dv) and gq.shape == (B, T, H, Dv)
+        if p_in is not None:
+            assert p_in.shape == (B, H, 2, J, Dv)
+        p_out = np.zeros((B, H, 2, J, Dv))
+        rc = (lib or _load()).swila_oracle_forward_temporal(
+            B, H, T, Dk, Dv, J, _ptr(q), _ptr(k), _ptr(v), _ptr(lb), _ptr(lk), _ptr(lq),
+            _ptr(gk), _ptr(gq), _ptr(s_in), _ptr(p_in), _ptr(s_out), _ptr(p_out), _ptr(o),
+            _ptr(resp), _ptr(delta), int(nthreads))
+    else:
+        assert prior_in is None, "prior_in needs the gate logits"
+        rc = (lib or _load()).swila_oracle_forward(
+            B, H, T, Dk, Dv, J, _ptr(q), _ptr(k), _ptr(v), _ptr(lb), _ptr(lk), _ptr(lq),
+            _ptr(s_in), _ptr(s_out), _ptr(o), _ptr(resp), _ptr(delta), int(nthreads))
     if rc != 0:
         raise FloatingPointError("oracle failed with status %d" % rc)
     out = {"o": o, "state": s_out}
+    if temporal:
+        out["prior"] = p_out
     if want_resp:
         out["resp"] = resp
     if want_delta:
@@ -112,11 +140,19 @@ def forward(q, k, v, beta_logit, prior_k_logit, prior_q_logit, state_in=None, *,
 
 
 def decode_step(q, k, v, beta_logit, prior_k_logit, prior_q_logit, state_in, *,
-                nthreads: int = 0):
+                gate_k_logit=None, gate_q_logit=None, prior_in=None, nthreads: int = 0):
     """One token per sequence: q, k [B,H,Dk]; v [B,H,Dv]; logits [B,H,J,Dv];
-    state_in [B,H,J,Dk,Dv].  Returns (o [B,H,Dv], state [B,H,J,Dk,Dv]).
+    state_in [B,H,J,Dk,Dv].  Returns (o [B,H,Dv], state [B,H,J,Dk,Dv]), plus
+    the prior state [B,H,2,J,Dv] for the temporal form (gate logits [B,H,Dv]).
     This is ``forward`` with T = 1."""
+    temporal = gate_k_logit is not None
+    gates = {}
+    if temporal:
+        gates = dict(gate_k_logit=np.asarray(gate_k_logit)[:, None],
+                     gate_q_logit=np.asarray(gate_q_logit)[:, None], prior_in=prior_in)
     r = forward(*(np.asarray(x)[:, None] for x in
                   (q, k, v, beta_logit, prior_k_logit, prior_q_logit)),
-                state_in, nthreads=nthreads)
+                state_in, nthreads=nthreads, **gates)
+    if temporal:
+        return r["o"][:, 0], r["state"], r["prior"]
     return r["o"][:, 0], r["state"]

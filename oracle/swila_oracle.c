@@ -31,6 +31,20 @@
  * oracle converts it to its own W[j][d][i] on entry and back on exit.
  *
  * Decode (one token with state in and out) is this same function with T = 1.
+ *
+ * Temporal SwiLA (Sec. 3.3, App. B.3), when gate logits are given: the two
+ * priors become running mixtures over time, per (j, d),
+ *
+ *   g^k_{td} = sigmoid(gate_k_logit_{td}),  g^q_{td} = sigmoid(gate_q_logit_{td})
+ *   rbar_{tjd}   = (1 - g^k_{td}) r_{t-1,jd}      + g^k_{td} pi^k_{tjd}
+ *   rhobar_{tjd} = (1 - g^q_{td}) rhobar_{t-1,jd} + g^q_{td} pi^q_{tjd}
+ *
+ * and rbar replaces pi^k in the E-step, rhobar replaces pi^q in the retrieval.
+ * Note the key side mixes in the previous token's responsibilities r (the
+ * filtered posterior), the query side its own previous prior.  The carried
+ * pair (r_{t-1}, rhobar_{t-1}) is the "prior state" [B, H, 2, J, Dv]: part 0
+ * is r, part 1 is rhobar.  Without an input prior state both start uniform,
+ * 1/J (the paper gives no initial value).  Gate logits are [B, T, H, Dv].
  */
 #include <math.h>
 #include <pthread.h>
@@ -43,6 +57,8 @@ typedef struct {
     int B, H, T, Dk, Dv, J;
     const double *q, *k, *v, *lb, *lk, *lq, *state_in;
     double *state_out, *o, *resp, *delta_out;
+    const double *gk, *gq, *prior_in;   /* temporal form: gate logits, prior state */
+    double *prior_out;
     int next_head;              /* work counter, guarded by mu */
     int status;                 /* first error seen, guarded by mu */
     pthread_mutex_t mu;
@@ -56,11 +72,21 @@ static int run_head(job_t *a, int b, int h)
     double *prior = (double *)malloc(sizeof(double) * (size_t)J);
     double *num = (double *)malloc(sizeof(double) * (size_t)J);
     double *delta = (double *)malloc(sizeof(double) * (size_t)J);
-    if (!W || !prior || !num || !delta) {
-        free(W); free(prior); free(num); free(delta);
+    const int temporal = a->gk != NULL;
+    /* temporal form: r_{t-1,jd} and rhobar_{t-1,jd}, [j][d] */
+    double *rprev = (double *)malloc(sizeof(double) * (size_t)J * Dv);
+    double *rho = (double *)malloc(sizeof(double) * (size_t)J * Dv);
+    if (!W || !prior || !num || !delta || !rprev || !rho) {
+        free(W); free(prior); free(num); free(delta); free(rprev); free(rho);
         return -2;
     }
     int rc = 0;
+    for (int j = 0; j < J; ++j)
+        for (int d = 0; d < Dv; ++d) {
+            const size_t p = (((size_t)b * H + h) * 2 * J + j) * Dv + d;
+            rprev[(size_t)j * Dv + d] = a->prior_in ? a->prior_in[p] : 1.0 / J;
+            rho[(size_t)j * Dv + d] = a->prior_in ? a->prior_in[p + (size_t)J * Dv] : 1.0 / J;
+        }
 
     /* initial state W_0 (zeros when none is given) */
     for (int j = 0; j < J; ++j)
@@ -85,6 +111,12 @@ static int run_head(job_t *a, int b, int h)
             for (int j = 0; j < J; ++j) m = fmax(m, lkt[(size_t)j * Dv + d]);
             for (int j = 0; j < J; ++j) z += exp(lkt[(size_t)j * Dv + d] - m);
             for (int j = 0; j < J; ++j) prior[j] = exp(lkt[(size_t)j * Dv + d] - m) / z;
+            if (temporal) {
+                /* App. B.3: mix in the previous token's responsibilities */
+                const double g = 1.0 / (1.0 + exp(-a->gk[row * Dv + d]));
+                for (int j = 0; j < J; ++j)
+                    prior[j] = (1.0 - g) * rprev[(size_t)j * Dv + d] + g * prior[j];
+            }
 
             /* prediction errors with the previous state */
             for (int j = 0; j < J; ++j) {
@@ -114,6 +146,7 @@ static int run_head(job_t *a, int b, int h)
                 double *w = W + ((size_t)j * Dv + d) * Dk;
                 for (int i = 0; i < Dk; ++i) w[i] += beta * r * delta[j] * kt[i];
                 if (a->resp) a->resp[(row * J + j) * Dv + d] = r;
+                if (temporal) rprev[(size_t)j * Dv + d] = r;
                 if (a->delta_out) a->delta_out[(row * J + j) * Dv + d] = delta[j];
             }
 
@@ -122,8 +155,15 @@ static int run_head(job_t *a, int b, int h)
             for (int j = 0; j < J; ++j) m = fmax(m, lqt[(size_t)j * Dv + d]);
             for (int j = 0; j < J; ++j) z += exp(lqt[(size_t)j * Dv + d] - m);
             double out = 0.0;
+            const double gq = temporal ? 1.0 / (1.0 + exp(-a->gq[row * Dv + d])) : 0.0;
             for (int j = 0; j < J; ++j) {
-                const double pq = exp(lqt[(size_t)j * Dv + d] - m) / z;
+                double pq = exp(lqt[(size_t)j * Dv + d] - m) / z;
+                if (temporal) {
+                    /* App. B.3: running mixture of the query-side priors */
+                    double *rq = rho + (size_t)j * Dv + d;
+                    *rq = (1.0 - gq) * *rq + gq * pq;
+                    pq = *rq;
+                }
                 const double *w = W + ((size_t)j * Dv + d) * Dk;
                 double y = 0.0;
                 for (int i = 0; i < Dk; ++i) y += w[i] * qt[i];
@@ -140,8 +180,15 @@ static int run_head(job_t *a, int b, int h)
                     size_t s = ((((size_t)b * H + h) * J + j) * Dk + i) * Dv + d;
                     a->state_out[s] = W[((size_t)j * Dv + d) * Dk + i];
                 }
+    if (rc == 0 && temporal && a->prior_out)
+        for (int j = 0; j < J; ++j)
+            for (int d = 0; d < Dv; ++d) {
+                const size_t p = (((size_t)b * H + h) * 2 * J + j) * Dv + d;
+                a->prior_out[p] = rprev[(size_t)j * Dv + d];
+                a->prior_out[p + (size_t)J * Dv] = rho[(size_t)j * Dv + d];
+            }
 
-    free(W); free(prior); free(num); free(delta);
+    free(W); free(prior); free(num); free(delta); free(rprev); free(rho);
     return rc;
 }
 
@@ -164,6 +211,16 @@ static void *worker(void *p)
     return NULL;
 }
 
+static int run_all(job_t *ap, int nthreads);
+int swila_oracle_forward_temporal(int B, int H, int T, int Dk, int Dv, int J,
+                                  const double *q, const double *k, const double *v,
+                                  const double *beta_logit, const double *prior_k_logit,
+                                  const double *prior_q_logit, const double *gate_k_logit,
+                                  const double *gate_q_logit, const double *state_in,
+                                  const double *prior_in, double *state_out,
+                                  double *prior_out, double *o, double *resp_out,
+                                  double *delta_out, int nthreads);
+
 /*
  * Forward over T tokens for every (b, h).  state_in may be NULL (zeros);
  * state_out, resp_out and delta_out may be NULL (not written).  state_out
@@ -178,7 +235,29 @@ int swila_oracle_forward(int B, int H, int T, int Dk, int Dv, int J,
                          double *state_out, double *o, double *resp_out,
                          double *delta_out, int nthreads)
 {
+    return swila_oracle_forward_temporal(B, H, T, Dk, Dv, J, q, k, v, beta_logit,
+                                         prior_k_logit, prior_q_logit, NULL, NULL, state_in,
+                                         NULL, state_out, NULL, o, resp_out, delta_out,
+                                         nthreads);
+}
+
+/*
+ * The same with the temporal priors of App. B.3 when gate_k_logit and
+ * gate_q_logit are given ([B, T, H, Dv]; both or neither).  prior_in is the
+ * prior state [B, H, 2, J, Dv] or NULL (uniform); prior_out receives the
+ * final one, or is NULL.  Without gate logits this is the plain forward.
+ */
+int swila_oracle_forward_temporal(int B, int H, int T, int Dk, int Dv, int J,
+                                  const double *q, const double *k, const double *v,
+                                  const double *beta_logit, const double *prior_k_logit,
+                                  const double *prior_q_logit, const double *gate_k_logit,
+                                  const double *gate_q_logit, const double *state_in,
+                                  const double *prior_in, double *state_out,
+                                  double *prior_out, double *o, double *resp_out,
+                                  double *delta_out, int nthreads)
+{
     if (B < 0 || H < 0 || T < 0 || Dk <= 0 || Dv <= 0 || J <= 0) return -3;
+    if ((gate_k_logit == NULL) != (gate_q_logit == NULL)) return -3;
     job_t a;
     memset(&a, 0, sizeof a);
     a.B = B; a.H = H; a.T = T; a.Dk = Dk; a.Dv = Dv; a.J = J;
@@ -186,12 +265,20 @@ int swila_oracle_forward(int B, int H, int T, int Dk, int Dv, int J,
     a.lb = beta_logit; a.lk = prior_k_logit; a.lq = prior_q_logit;
     a.state_in = state_in; a.state_out = state_out; a.o = o;
     a.resp = resp_out; a.delta_out = delta_out;
+    a.gk = gate_k_logit; a.gq = gate_q_logit;
+    a.prior_in = prior_in; a.prior_out = prior_out;
+    return run_all(&a, nthreads);
+}
+
+static int run_all(job_t *ap, int nthreads)
+{
+    job_t a = *ap;
     pthread_mutex_init(&a.mu, NULL);
 
     int n = nthreads;
     if (n <= 0) n = (int)sysconf(_SC_NPROCESSORS_ONLN);
     if (n < 1) n = 1;
-    if (n > B * H) n = B * H;
+    if (n > a.B * a.H) n = a.B * a.H;
     if (n <= 1) {
         worker(&a);
     } else {

@@ -29,8 +29,8 @@ MUTATIONS = {
     "sigmoid_sign_flipped": ("1.0 / (1.0 + exp(-lbt[", "1.0 / (1.0 + exp(lbt[", False),
     "retrieval_with_key": ("y += w[i] * qt[i];", "y += w[i] * kt[i];", False),
     "query_prior_from_key_logits": ("lqt[", "lkt[", True),
-    "query_prior_unnormalised": ("const double pq = exp(lqt[(size_t)j * Dv + d] - m) / z;",
-                                 "const double pq = exp(lqt[(size_t)j * Dv + d] - m);", False),
+    "query_prior_unnormalised": ("double pq = exp(lqt[(size_t)j * Dv + d] - m) / z;",
+                                 "double pq = exp(lqt[(size_t)j * Dv + d] - m);", False),
     "initial_state_transposed": (STATE_IDX, "((((size_t)b * H + h) * J + j) * Dv + d) * Dk + i", False),
 }
 

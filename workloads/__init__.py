@@ -101,6 +101,24 @@ def iid_inputs(B, H, T, Dk, Dv, J, *, dtype="bf16", seed=0, state_std=0.0,
     return out
 
 
+def temporal_inputs(B, H, T, Dv, J, *, dtype="bf16", seed=0, gate_scale=1.0,
+                    prior_state=False):
+    """Extra inputs of Temporal SwiLA: the key- and query-side gate logits
+    ``gk``, ``gq`` [B, T, H, Dv], i.i.d. N(0, gate_scale^2) (rounded like the
+    other inputs), and, when ``prior_state`` is set, a carried prior state
+    ``prior`` [B, H, 2, J, Dv] fp32 whose two parts are probability vectors
+    over J (normalised exponentials of N(0,1) draws).  Drawn from their own
+    generator, so the base inputs of the same seed are unchanged."""
+    rng = np.random.Generator(np.random.PCG64(seed + 7919))
+    gk = rng.standard_normal((B, T, H, Dv), dtype=np.float32) * np.float32(gate_scale)
+    gq = rng.standard_normal((B, T, H, Dv), dtype=np.float32) * np.float32(gate_scale)
+    out = {"gk": _finish(gk, dtype), "gq": _finish(gq, dtype), "prior": None}
+    if prior_state:
+        e = np.exp(rng.standard_normal((B, H, 2, J, Dv)))
+        out["prior"] = (e / e.sum(axis=3, keepdims=True)).astype(np.float32)
+    return out
+
+
 def _project_tokens(rng, ids, vocab, width, H, Dk, Dv, J, dtype, chunk_tokens=4096):
     """q, k, v and the three logit tensors as linear projections of random token
     embeddings E ~ N(0,1) [vocab, width] with weights N(0, 1/width), so every
