@@ -160,6 +160,57 @@ int swila_decode_step(const swila_shape *shape, const swila_opts *opts,
                       const void *prior_q_logit,
                       const float *state_in, float *state_out, void *o, void *stream);
 
+/*
+ * Temporal SwiLA (Sec. 3.3, App. B.3): the two priors become running mixtures
+ * over time, per (b, h, j, d),
+ *
+ *   g^k_{td}     = sigmoid(gate_k_logit_{td}),  g^q_{td} = sigmoid(gate_q_logit_{td})
+ *   rbar_{tjd}   = (1 - g^k_{td}) r_{t-1,jd}      + g^k_{td} pi^k_{tjd}
+ *   rhobar_{tjd} = (1 - g^q_{td}) rhobar_{t-1,jd} + g^q_{td} pi^q_{tjd}
+ *
+ * rbar replaces pi^k in eq. responsibility and rhobar replaces pi^q in
+ * eq. retrieval.  The key side mixes in the previous token's responsibilities
+ * r_{t-1} (the filtered posterior), the query side its own previous prior.
+ *   gate_k_logit, gate_q_logit: [B,T,H,Dv] (decode: [B,H,Dv]), in_dtype, 16-byte
+ *              aligned; required when T > 0.
+ *   prior_in:  the prior state [B,H,2,J,Dv] fp32 carried from a previous call
+ *              (part 0: r_{t-1}, part 1: rhobar_{t-1}), or NULL for the uniform
+ *              1/J (the paper gives no initial value).
+ *   prior_out: NULL, or the prior state after the last token; may equal
+ *              prior_in (updated in place), otherwise disjoint from everything.
+ * The gate tensors and prior_in must not overlap any output.
+ */
+typedef struct swila_temporal {
+    const void *gate_k_logit;
+    const void *gate_q_logit;
+    const float *prior_in;
+    float *prior_out;
+} swila_temporal;
+
+/*
+ * swila_forward with the temporal priors above.  The other arguments are those
+ * of swila_forward (no workspace: SWILA_ALGO_NEWTON, whose linearisation is
+ * that of the plain recurrence, returns SWILA_EUNSUPPORTED).  The form runs on
+ * the token-by-token scan (SWILA_ALGO_AUTO or SWILA_ALGO_RECURRENT, either
+ * input dtype); SWILA_ALGO_CHUNK_EXACT returns SWILA_EUNSUPPORTED.  T == 0
+ * copies state_in and prior_in (or zeros and 1/J) to the outputs.
+ */
+int swila_forward_temporal(const swila_shape *shape, const swila_opts *opts,
+                           const void *q, const void *k, const void *v,
+                           const void *beta_logit, const void *prior_k_logit,
+                           const void *prior_q_logit, const swila_temporal *temporal,
+                           const float *state_in, float *state_out, void *o,
+                           float *resp_out, void *stream);
+
+/* swila_decode_step with the temporal priors (gate logits [B,H,Dv]); its
+ * result equals swila_forward_temporal with T = 1. */
+int swila_decode_step_temporal(const swila_shape *shape, const swila_opts *opts,
+                               const void *q, const void *k, const void *v,
+                               const void *beta_logit, const void *prior_k_logit,
+                               const void *prior_q_logit, const swila_temporal *temporal,
+                               const float *state_in, float *state_out, void *o,
+                               void *stream);
+
 /* Text of this thread's last error ("" if none). */
 const char *swila_last_error(void);
 

@@ -10,6 +10,8 @@ library raises.
 Entry points (names as in the C ABI):
   ``forward``            whole sequences       -> swila_forward
   ``decode_step``        one token per sequence -> swila_decode_step
+  ``forward_temporal``, ``decode_step_temporal``  Temporal SwiLA (App. B.3)
+                                                -> swila_forward_temporal, ...
   ``state_init``         initial state          -> swila_state_init
   ``state_bytes``, ``forward_workspace_bytes``, ``version``
 """
@@ -18,7 +20,7 @@ from __future__ import annotations
 import ctypes
 import os
 
-__all__ = ["forward", "decode_step", "state_init", "state_bytes", "forward_workspace_bytes",
+__all__ = ["forward", "decode_step", "forward_temporal", "decode_step_temporal", "state_init", "state_bytes", "forward_workspace_bytes",
            "version", "library_path", "SwilaError", "F32", "BF16", "ALGO_AUTO",
            "ALGO_RECURRENT", "ALGO_CHUNK_EXACT", "ALGO_NEWTON", "FLAG_NEWTON_NO_CLAMP"]
 
@@ -49,6 +51,11 @@ class Opts(ctypes.Structure):
                 ("algo", ctypes.c_int32), ("chunk", ctypes.c_int32),
                 ("max_iters", ctypes.c_int32), ("tol", ctypes.c_float),
                 ("flags", ctypes.c_uint32)]
+
+
+class Temporal(ctypes.Structure):
+    _fields_ = [("gate_k_logit", ctypes.c_void_p), ("gate_q_logit", ctypes.c_void_p),
+                ("prior_in", ctypes.c_void_p), ("prior_out", ctypes.c_void_p)]
 
 
 _lib = None
@@ -82,6 +89,11 @@ def load_library():
     lib.swila_forward.argtypes = [sp, op] + [vp] * 6 + [vp, vp, vp, vp, vp, ctypes.c_size_t, vp, vp]
     lib.swila_decode_step.restype = ctypes.c_int
     lib.swila_decode_step.argtypes = [sp, op] + [vp] * 6 + [vp, vp, vp, vp]
+    tp = ctypes.POINTER(Temporal)
+    lib.swila_forward_temporal.restype = ctypes.c_int
+    lib.swila_forward_temporal.argtypes = [sp, op] + [vp] * 6 + [tp, vp, vp, vp, vp, vp]
+    lib.swila_decode_step_temporal.restype = ctypes.c_int
+    lib.swila_decode_step_temporal.argtypes = [sp, op] + [vp] * 6 + [tp, vp, vp, vp, vp]
     _lib = lib
     return lib
 
@@ -284,3 +296,131 @@ def decode_step(q, k, v, beta_logit, prior_k_logit, prior_q_logit, state_in, *,
         *[_ptr(t) for t in ins], _ptr(state_in), _ptr(state_out), _ptr(o),
         _stream_handle(stream)))
     return o, state_out
+
+
+def _temporal_args(gate_k_logit, gate_q_logit, prior_in, prior_out, code, gate_shape,
+                   prior_shape, device):
+    """Checks the temporal tensors; allocates prior_out when it is True."""
+    torch = _torch()
+    for t, n in ((gate_k_logit, "gate_k_logit"), (gate_q_logit, "gate_q_logit")):
+        _dev_tensor(t, n)
+        if _dtype_code(t) != code:
+            raise TypeError("%s must have the dtype of q" % n)
+        if tuple(t.shape) != gate_shape:
+            raise ValueError("%s has shape %s, expected %s" % (n, tuple(t.shape), gate_shape))
+    _dev_tensor(prior_in, "prior_in", torch.float32)
+    if prior_in is not None and tuple(prior_in.shape) != prior_shape:
+        raise ValueError("prior_in must be [B,H,2,J,Dv] = %s" % (prior_shape,))
+    if prior_out is True:
+        prior_out = torch.empty(prior_shape, device=device, dtype=torch.float32)
+    elif prior_out is False or prior_out is None:
+        prior_out = None
+    else:
+        _dev_tensor(prior_out, "prior_out", torch.float32)
+        if tuple(prior_out.shape) != prior_shape:
+            raise ValueError("prior_out must be [B,H,2,J,Dv] = %s" % (prior_shape,))
+    tp = Temporal(gate_k_logit.data_ptr(), gate_q_logit.data_ptr(),
+                  None if prior_in is None else prior_in.data_ptr(),
+                  None if prior_out is None else prior_out.data_ptr())
+    return tp, prior_out
+
+
+def forward_temporal(q, k, v, beta_logit, prior_k_logit, prior_q_logit, gate_k_logit,
+                     gate_q_logit, state_in=None, prior_in=None, *, state_out=True,
+                     prior_out=True, o=None, out_dtype=None, resp=False, algo="auto",
+                     stream=None):
+    """Temporal SwiLA forward (swila_forward_temporal; Sec. 3.3, App. B.3).
+
+    The arguments of ``forward`` plus the gate logits gate_k_logit,
+    gate_q_logit [B,T,H,Dv] (the dtype of q) and the prior state prior_in
+    [B,H,2,J,Dv] float32 (part 0: r_{t-1}, part 1: rhobar_{t-1}; None = 1/J).
+    prior_out: True to allocate, False to discard, or a float32 tensor (may be
+    prior_in).  algo: "auto" or "recurrent".
+    Returns (o, state_out, prior_out) or (o, state_out, prior_out, resp).
+    """
+    torch = _torch()
+    names = ("q", "k", "v", "beta_logit", "prior_k_logit", "prior_q_logit")
+    ins = [_dev_tensor(t, n) for t, n in zip((q, k, v, beta_logit, prior_k_logit, prior_q_logit),
+                                             names)]
+    code = _dtype_code(q)
+    for t, n in zip(ins, names):
+        if _dtype_code(t) != code:
+            raise TypeError("%s has dtype %s but q has %s" % (n, t.dtype, q.dtype))
+    B, H, T, Dk, Dv, J = _layer_shapes(q, v, beta_logit, decode=False)
+    expect = {"q": (B, T, H, Dk), "k": (B, T, H, Dk), "v": (B, T, H, Dv),
+              "beta_logit": (B, T, H, J, Dv), "prior_k_logit": (B, T, H, J, Dv),
+              "prior_q_logit": (B, T, H, J, Dv)}
+    for t, n in zip(ins, names):
+        if tuple(t.shape) != expect[n]:
+            raise ValueError("%s has shape %s, expected %s" % (n, tuple(t.shape), expect[n]))
+    _dev_tensor(state_in, "state_in", torch.float32)
+    if state_in is not None and tuple(state_in.shape) != (B, H, J, Dk, Dv):
+        raise ValueError("state_in must be [B,H,J,Dk,Dv] = %s" % ((B, H, J, Dk, Dv),))
+    tp, p_out = _temporal_args(gate_k_logit, gate_q_logit, prior_in, prior_out, code,
+                               (B, T, H, Dv), (B, H, 2, J, Dv), q.device)
+    odt = q.dtype if out_dtype is None else out_dtype
+    if o is None:
+        o = torch.empty((B, T, H, Dv), device=q.device, dtype=odt)
+    _dev_tensor(o, "o")
+    if state_out is True:
+        s_out = torch.empty((B, H, J, Dk, Dv), device=q.device, dtype=torch.float32)
+    elif state_out is False or state_out is None:
+        s_out = None
+    else:
+        s_out = _dev_tensor(state_out, "state_out", torch.float32)
+    r = None
+    if resp:
+        r = torch.empty((B, T, H, J, Dv), device=q.device, dtype=torch.float32)
+    opts = Opts(code, _dtype_code(o), _ALGOS[algo], 0, 0, 0.0, 0)
+    _check(load_library().swila_forward_temporal(
+        ctypes.byref(Shape(B, H, T, Dk, Dv, J)), ctypes.byref(opts),
+        *[_ptr(t) for t in ins], ctypes.byref(tp), _ptr(state_in), _ptr(s_out), _ptr(o), _ptr(r),
+        _stream_handle(stream)))
+    return (o, s_out, p_out, r) if resp else (o, s_out, p_out)
+
+
+def decode_step_temporal(q, k, v, beta_logit, prior_k_logit, prior_q_logit, gate_k_logit,
+                         gate_q_logit, state_in, prior_in, *, state_out=None, prior_out=None,
+                         o=None, out_dtype=None, stream=None):
+    """One Temporal SwiLA token per sequence (swila_decode_step_temporal).
+
+    The arguments of ``decode_step`` plus gate logits [B,H,Dv] and the prior
+    state prior_in [B,H,2,J,Dv] float32 (None = 1/J).  state_out and prior_out
+    default to the inputs (updated in place), or to new tensors when those are
+    None.  Returns (o, state_out, prior_out).
+    """
+    torch = _torch()
+    names = ("q", "k", "v", "beta_logit", "prior_k_logit", "prior_q_logit")
+    ins = [_dev_tensor(t, n) for t, n in zip((q, k, v, beta_logit, prior_k_logit, prior_q_logit),
+                                             names)]
+    code = _dtype_code(q)
+    for t, n in zip(ins, names):
+        if _dtype_code(t) != code:
+            raise TypeError("%s has dtype %s but q has %s" % (n, t.dtype, q.dtype))
+    B, H, T, Dk, Dv, J = _layer_shapes(q, v, beta_logit, decode=True)
+    expect = {"q": (B, H, Dk), "k": (B, H, Dk), "v": (B, H, Dv), "beta_logit": (B, H, J, Dv),
+              "prior_k_logit": (B, H, J, Dv), "prior_q_logit": (B, H, J, Dv)}
+    for t, n in zip(ins, names):
+        if tuple(t.shape) != expect[n]:
+            raise ValueError("%s has shape %s, expected %s" % (n, tuple(t.shape), expect[n]))
+    _dev_tensor(state_in, "state_in", torch.float32)
+    if state_in is not None and tuple(state_in.shape) != (B, H, J, Dk, Dv):
+        raise ValueError("state_in must be [B,H,J,Dk,Dv] = %s" % ((B, H, J, Dk, Dv),))
+    if state_out is None:
+        state_out = state_in if state_in is not None else torch.empty(
+            (B, H, J, Dk, Dv), device=q.device, dtype=torch.float32)
+    _dev_tensor(state_out, "state_out", torch.float32)
+    if prior_out is None:
+        prior_out = prior_in if prior_in is not None else True
+    tp, p_out = _temporal_args(gate_k_logit, gate_q_logit, prior_in, prior_out, code,
+                               (B, H, Dv), (B, H, 2, J, Dv), q.device)
+    odt = q.dtype if out_dtype is None else out_dtype
+    if o is None:
+        o = torch.empty((B, H, Dv), device=q.device, dtype=odt)
+    _dev_tensor(o, "o")
+    opts = Opts(code, _dtype_code(o), ALGO_AUTO, 0, 0, 0.0, 0)
+    _check(load_library().swila_decode_step_temporal(
+        ctypes.byref(Shape(B, H, 1, Dk, Dv, J)), ctypes.byref(opts),
+        *[_ptr(t) for t in ins], ctypes.byref(tp), _ptr(state_in), _ptr(state_out), _ptr(o),
+        _stream_handle(stream)))
+    return o, state_out, p_out

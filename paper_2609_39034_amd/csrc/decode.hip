@@ -15,6 +15,12 @@
 //   3. every thread applies w += c k to its rows and stores them.
 // state_out may alias state_in: each block reads its whole tile before any
 // write, and tiles of different blocks are disjoint.
+//
+// Temporal SwiLA (TP; App. B.3): the column threads also read the prior state
+// (r_{t-1}, rhobar_{t-1}) of their column, use rbar = (1 - g^k) r_{t-1} +
+// g^k pi^k as the key prior and rhobar = (1 - g^q) rhobar_{t-1} + g^q pi^q as
+// the query prior, and write the new pair (r, rhobar); prior_out may alias
+// prior_in for the same reason as the state.
 #include "device_common.hpp"
 #include "launch.hpp"
 
@@ -23,7 +29,7 @@ namespace {
 
 constexpr int kRows = 16;  // state rows per thread
 
-template <int DK, int J>
+template <int DK, int J, bool TP>
 __global__ __launch_bounds__(512) void decode_kernel(LayerArgs a, int DB) {
     constexpr int IG = DK / kRows;
     const int CL = DB / 4;
@@ -56,6 +62,8 @@ __global__ __launch_bounds__(512) void decode_kernel(LayerArgs a, int DB) {
     // per-column inputs, fetched early by the column threads
     const size_t row = (size_t)b * H + h;
     float vd = 0.f, lb[J], lk[J], lq[J];
+    float gk = 0.f, gq = 0.f, rprev[J], rho[J];   // temporal
+    const size_t pbase = row * 2 * J * Dv + d0 + tid;
     if (tid < DB) {
         vd = load1(a.v, row * Dv + d0 + tid, ibf);
 #pragma unroll
@@ -64,6 +72,15 @@ __global__ __launch_bounds__(512) void decode_kernel(LayerArgs a, int DB) {
             lb[jj] = load1(a.lb, idx, ibf);
             lk[jj] = load1(a.lk, idx, ibf);
             lq[jj] = load1(a.lq, idx, ibf);
+        }
+        if constexpr (TP) {
+            gk = 1.0f / (1.0f + exp_fast(-load1(a.gk, row * Dv + d0 + tid, ibf)));
+            gq = 1.0f / (1.0f + exp_fast(-load1(a.gq, row * Dv + d0 + tid, ibf)));
+#pragma unroll
+            for (int jj = 0; jj < J; ++jj) {
+                rprev[jj] = a.prior_in ? a.prior_in[pbase + (size_t)jj * Dv] : 1.0f / J;
+                rho[jj] = a.prior_in ? a.prior_in[pbase + (size_t)(J + jj) * Dv] : 1.0f / J;
+            }
         }
     }
     for (int i = tid; i < DK; i += blockDim.x) {
@@ -104,32 +121,59 @@ __global__ __launch_bounds__(512) void decode_kernel(LayerArgs a, int DB) {
     // 2. E-step and retrieval, one thread per column
     if (tid < DB) {
         float delta[J], e[J];
-        float m = -INFINITY, mq = -INFINITY;
+        float m = -INFINITY, mq = -INFINITY, mk = -INFINITY;
 #pragma unroll
         for (int jj = 0; jj < J; ++jj) {
             delta[jj] = vd - sP[jj][tid];
-            e[jj] = lk[jj] - 0.5f * delta[jj] * delta[jj];
+            e[jj] = (TP ? 0.0f : lk[jj]) - 0.5f * delta[jj] * delta[jj];
             m = fmaxf(m, e[jj]);
             mq = fmaxf(mq, lq[jj]);
+            mk = fmaxf(mk, lk[jj]);
         }
-        float z = 0.f, zq = 0.f;
+        float z = 0.f, zq = 0.f, zk = 0.f;
 #pragma unroll
         for (int jj = 0; jj < J; ++jj) {
             e[jj] = exp_fast(e[jj] - m);
-            z += e[jj];
             lq[jj] = exp_fast(lq[jj] - mq);
             zq += lq[jj];
+            if constexpr (TP) {
+                lk[jj] = exp_fast(lk[jj] - mk);
+                zk += lk[jj];
+            }
+        }
+        const float izk = TP ? 1.0f / zk : 1.0f;
+#pragma unroll
+        for (int jj = 0; jj < J; ++jj) {
+            // temporal key prior: (1 - g^k) r_{t-1} + g^k pi^k
+            if constexpr (TP) e[jj] *= fmaf(gk, lk[jj] * izk - rprev[jj], rprev[jj]);
+            z += e[jj];
         }
         const float iz = rcp_fast(z), izq = 1.0f / zq, kqv = sKQ;
         float o = 0.f;
 #pragma unroll
         for (int jj = 0; jj < J; ++jj) {
             const float beta = 1.0f / (1.0f + exp_fast(-lb[jj]));
-            const float c = beta * (e[jj] * iz) * delta[jj];
+            const float r = e[jj] * iz;
+            const float c = beta * r * delta[jj];
             sC[jj][tid] = c;
-            o = fmaf(lq[jj] * izq, fmaf(c, kqv, sY[jj][tid]), o);
+            float pq = lq[jj] * izq;
+            if constexpr (TP) {
+                rprev[jj] = r;
+                rho[jj] = fmaf(gq, pq - rho[jj], rho[jj]);   // (1 - g^q) rhobar + g^q pi^q
+                pq = rho[jj];
+            }
+            o = fmaf(pq, fmaf(c, kqv, sY[jj][tid]), o);
         }
         store1(a.o, row * Dv + d0 + tid, o, a.out_bf16);
+        if constexpr (TP) {
+            if (a.prior_out) {
+#pragma unroll
+                for (int jj = 0; jj < J; ++jj) {
+                    a.prior_out[pbase + (size_t)jj * Dv] = rprev[jj];
+                    a.prior_out[pbase + (size_t)(J + jj) * Dv] = rho[jj];
+                }
+            }
+        }
     }
     __syncthreads();
 
@@ -157,7 +201,10 @@ hipError_t launch_dk_j(const LayerArgs &a, hipStream_t stream) {
     int threads = J * (DK / kRows) * (DB / 4);
     if (threads < DB) threads = DB;
     dim3 grid(a.Dv / DB, a.H, a.B);
-    hipLaunchKernelGGL((decode_kernel<DK, J>), grid, dim3(threads), 0, stream, a, DB);
+    if (a.gk)
+        hipLaunchKernelGGL((decode_kernel<DK, J, true>), grid, dim3(threads), 0, stream, a, DB);
+    else
+        hipLaunchKernelGGL((decode_kernel<DK, J, false>), grid, dim3(threads), 0, stream, a, DB);
     return hipGetLastError();
 }
 
@@ -173,10 +220,10 @@ hipError_t launch_dk(const LayerArgs &a, hipStream_t stream) {
     }
 }
 
-__global__ void state_fill_kernel(float *dst, const float *src, size_t n) {
+__global__ void fill_kernel(float *dst, const float *src, size_t n, float value) {
     const size_t stride = (size_t)gridDim.x * blockDim.x;
     for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
-        dst[i] = src ? src[i] : 0.0f;
+        dst[i] = src ? src[i] : value;
 }
 
 }  // namespace
@@ -191,12 +238,17 @@ hipError_t launch_decode(const LayerArgs &a, hipStream_t stream) {
     }
 }
 
-hipError_t launch_state_fill(float *state, const float *src, size_t n, hipStream_t stream) {
-    if (n == 0 || state == src) return hipSuccess;
+hipError_t launch_fill(float *dst, const float *src, size_t n, float value, hipStream_t stream) {
+    if (n == 0 || dst == src) return hipSuccess;
     size_t blocks = (n + 255) / 256;
     if (blocks > 4096) blocks = 4096;
-    hipLaunchKernelGGL(state_fill_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, state, src, n);
+    hipLaunchKernelGGL(fill_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, dst, src, n,
+                       value);
     return hipGetLastError();
+}
+
+hipError_t launch_state_fill(float *state, const float *src, size_t n, hipStream_t stream) {
+    return launch_fill(state, src, n, 0.0f, stream);
 }
 
 }  // namespace swila

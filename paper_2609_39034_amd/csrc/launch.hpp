@@ -16,6 +16,12 @@ struct LayerArgs {
     float *resp;                           // nullptr = not written
     int B, H, T, Dk, Dv, J;
     bool in_bf16, out_bf16;
+    // Temporal SwiLA (App. B.3): gate logits [B,T,H,Dv] (in_bf16 like the other
+    // inputs; both set, or neither for the plain form) and the prior state
+    // [B,H,2,J,Dv] fp32 (part 0: r_{t-1}, part 1: rhobar_{t-1}; nullptr = 1/J).
+    const void *gk = nullptr, *gq = nullptr;
+    const float *prior_in = nullptr;
+    float *prior_out = nullptr;
 };
 
 // Parameters of the chunkwise quasi-Newton form (App. D).
@@ -46,5 +52,8 @@ hipError_t launch_decode(const LayerArgs &a, hipStream_t stream);
 
 // state <- src (or zeros when src is nullptr); n floats.
 hipError_t launch_state_fill(float *state, const float *src, size_t n, hipStream_t stream);
+
+// dst <- src (or the constant value when src is nullptr); n floats.
+hipError_t launch_fill(float *dst, const float *src, size_t n, float value, hipStream_t stream);
 
 }  // namespace swila

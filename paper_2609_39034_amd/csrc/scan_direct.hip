@@ -18,6 +18,14 @@
 // padded so the L lanes of a column read distinct banks, and the per-(token,
 // column) scalars beta = sigmoid(logit), lk and pi^q = softmax_j already formed,
 // so the sequential loop does only the dependent arithmetic.
+//
+// Temporal SwiLA (TP; Sec. 3.3, App. B.3).  The key prior is the gated mixture
+// rbar_j = (1 - g^k) r_{t-1,j} + g^k pi^k_j of the previous token's
+// responsibilities and pi^k = softmax_j(lk), so pi^k is staged normalised and
+// r = rbar_j e^{-delta_j^2/2} / sum (the exponent shifted by its maximum over j);
+// the query prior rhobar_j = (1 - g^q) rhobar_{t-1,j} + g^q pi^q_j replaces
+// pi^q.  Both running priors live in registers, J per column, from the prior
+// state (or 1/J) to the prior state written at the end.
 #include "device_common.hpp"
 #include "launch.hpp"
 
@@ -30,16 +38,16 @@ constexpr int kMaxCols = 128;  // largest supported Dv
 
 // Columns one block holds: bounded by the block size, the largest Dv, and a
 // 64 KiB budget for the per-(token, column) scalars staged in LDS.
-constexpr int max_cols(int L, int J) {
+constexpr int max_cols(int L, int J, bool tp) {
     int n = kThreads / L < kMaxCols ? kThreads / L : kMaxCols;
-    while (n > 16 && kTC * (3 * J + 2) * n * 4 > 65536) n /= 2;
+    while (n > 16 && kTC * (3 * J + (tp ? 4 : 2)) * n * 4 > 65536) n /= 2;
     return n;
 }
 
-template <int DK, int J, int S>
+template <int DK, int J, int S, bool TP>
 __global__ __launch_bounds__(kThreads) void scan_direct_kernel(LayerArgs a, int ncol) {
     constexpr int L = DK / S;             // lanes per output column
-    constexpr int NCM = max_cols(L, J);
+    constexpr int NCM = max_cols(L, J, TP);
     constexpr int SP = S + 4;             // padded slice stride in LDS
 
     __shared__ __align__(16) float sK[kTC][L][SP];
@@ -49,6 +57,7 @@ __global__ __launch_bounds__(kThreads) void scan_direct_kernel(LayerArgs a, int 
     __shared__ float sLk[kTC][J][NCM];
     __shared__ float sPq[kTC][J][NCM];
     __shared__ float sO[kTC][NCM];
+    __shared__ float sG[TP ? 2 : 1][kTC][TP ? NCM : 1];   // temporal: g^k, g^q
 
     const int tid = threadIdx.x;
     const int nthr = ncol * L;
@@ -66,6 +75,16 @@ __global__ __launch_bounds__(kThreads) void scan_direct_kernel(LayerArgs a, int 
 #pragma unroll
         for (int s = 0; s < S; ++s)
             w[j][s] = a.state_in ? a.state_in[sbase + ((size_t)j * DK + l * S + s) * Dv + d] : 0.0f;
+    // temporal: r_{t-1} and rhobar_{t-1} of this column
+    float rprev[J], rho[J];
+    const size_t pbase = ((size_t)b * H + h) * 2 * J * Dv + d;
+    if constexpr (TP) {
+#pragma unroll
+        for (int j = 0; j < J; ++j) {
+            rprev[j] = a.prior_in ? a.prior_in[pbase + (size_t)j * Dv] : 1.0f / J;
+            rho[j] = a.prior_in ? a.prior_in[pbase + (size_t)(J + j) * Dv] : 1.0f / J;
+        }
+    }
 
     for (int t0 = 0; t0 < T; t0 += kTC) {
         const int nt = min(kTC, T - t0);
@@ -86,25 +105,38 @@ __global__ __launch_bounds__(kThreads) void scan_direct_kernel(LayerArgs a, int 
             const int tt = g / ncol, c = g % ncol;
             const size_t row = (size_t)(b * T + t0 + tt) * H + h;
             sV[tt][c] = load1(a.v, row * Dv + d0 + c, ibf);
-            float lq[J];
-            float m = -INFINITY;
+            float lq[J], lk[J];
+            float m = -INFINITY, mk = -INFINITY;
 #pragma unroll
             for (int j = 0; j < J; ++j) {
                 const size_t idx = (row * J + j) * Dv + d0 + c;
                 sBeta[tt][j][c] = 1.0f / (1.0f + exp_fast(-load1(a.lb, idx, ibf)));
-                sLk[tt][j][c] = load1(a.lk, idx, ibf);
+                lk[j] = load1(a.lk, idx, ibf);
                 lq[j] = load1(a.lq, idx, ibf);
                 m = fmaxf(m, lq[j]);
+                mk = fmaxf(mk, lk[j]);
             }
-            float z = 0.0f;
+            float z = 0.0f, zk = 0.0f;
 #pragma unroll
             for (int j = 0; j < J; ++j) {
                 lq[j] = exp_fast(lq[j] - m);
                 z += lq[j];
+                if constexpr (TP) {
+                    lk[j] = exp_fast(lk[j] - mk);
+                    zk += lk[j];
+                }
             }
             const float iz = 1.0f / z;
+            const float izk = TP ? 1.0f / zk : 1.0f;
 #pragma unroll
-            for (int j = 0; j < J; ++j) sPq[tt][j][c] = lq[j] * iz;
+            for (int j = 0; j < J; ++j) {
+                sPq[tt][j][c] = lq[j] * iz;
+                sLk[tt][j][c] = TP ? lk[j] * izk : lk[j];   // temporal: pi^k itself
+            }
+            if constexpr (TP) {
+                sG[0][tt][c] = 1.0f / (1.0f + exp_fast(-load1(a.gk, row * Dv + d0 + c, ibf)));
+                sG[1][tt][c] = 1.0f / (1.0f + exp_fast(-load1(a.gq, row * Dv + d0 + c, ibf)));
+            }
         }
         __syncthreads();
 
@@ -144,13 +176,16 @@ __global__ __launch_bounds__(kThreads) void scan_direct_kernel(LayerArgs a, int 
 #pragma unroll
             for (int j = 0; j < J; ++j) {
                 delta[j] = vd - p[j];
-                e[j] = sLk[tt][j][dl] - 0.5f * delta[j] * delta[j];
+                e[j] = (TP ? 0.0f : sLk[tt][j][dl]) - 0.5f * delta[j] * delta[j];
                 m = fmaxf(m, e[j]);
             }
             float z = 0.0f;
+            const float gk = TP ? sG[0][tt][dl] : 0.0f, gq = TP ? sG[1][tt][dl] : 0.0f;
 #pragma unroll
             for (int j = 0; j < J; ++j) {
                 e[j] = exp_fast(e[j] - m);
+                // temporal key prior: (1 - g^k) r_{t-1} + g^k pi^k
+                if constexpr (TP) e[j] *= fmaf(gk, sLk[tt][j][dl] - rprev[j], rprev[j]);
                 z += e[j];
             }
             const float iz = rcp_fast(z);
@@ -161,7 +196,13 @@ __global__ __launch_bounds__(kThreads) void scan_direct_kernel(LayerArgs a, int 
                 const float c = sBeta[tt][j][dl] * r * delta[j];
 #pragma unroll
                 for (int s = 0; s < S; ++s) w[j][s] = fmaf(c, kv[s], w[j][s]);
-                o = fmaf(sPq[tt][j][dl], fmaf(c, kq, y[j]), o);
+                float pq = sPq[tt][j][dl];
+                if constexpr (TP) {
+                    rprev[j] = r;
+                    rho[j] = fmaf(gq, pq - rho[j], rho[j]);   // (1 - g^q) rhobar + g^q pi^q
+                    pq = rho[j];
+                }
+                o = fmaf(pq, fmaf(c, kq, y[j]), o);
                 if (a.resp && l == 0)
                     a.resp[(((size_t)(b * T + t0 + tt) * H + h) * J + j) * Dv + d] = r;
             }
@@ -185,17 +226,31 @@ __global__ __launch_bounds__(kThreads) void scan_direct_kernel(LayerArgs a, int 
             for (int s = 0; s < S; ++s)
                 a.state_out[sbase + ((size_t)j * DK + l * S + s) * Dv + d] = w[j][s];
     }
+    if constexpr (TP) {
+        if (a.prior_out && l == 0) {
+#pragma unroll
+            for (int j = 0; j < J; ++j) {
+                a.prior_out[pbase + (size_t)j * Dv] = rprev[j];
+                a.prior_out[pbase + (size_t)(J + j) * Dv] = rho[j];
+            }
+        }
+    }
+}
+
+template <int DK, int J, bool TP>
+hipError_t launch_dk_j_tp(const LayerArgs &a, hipStream_t stream) {
+    constexpr int S = (J <= 4) ? (DK < 16 ? DK : 16) : (DK < 8 ? DK : 8);
+    constexpr int L = DK / S;
+    const int ncol = a.Dv < max_cols(L, J, TP) ? a.Dv : max_cols(L, J, TP);
+    dim3 grid(a.Dv / ncol, a.H, a.B);
+    dim3 block(ncol * L);
+    hipLaunchKernelGGL((scan_direct_kernel<DK, J, S, TP>), grid, block, 0, stream, a, ncol);
+    return hipGetLastError();
 }
 
 template <int DK, int J>
 hipError_t launch_dk_j(const LayerArgs &a, hipStream_t stream) {
-    constexpr int S = (J <= 4) ? (DK < 16 ? DK : 16) : (DK < 8 ? DK : 8);
-    constexpr int L = DK / S;
-    const int ncol = a.Dv < max_cols(L, J) ? a.Dv : max_cols(L, J);
-    dim3 grid(a.Dv / ncol, a.H, a.B);
-    dim3 block(ncol * L);
-    hipLaunchKernelGGL((scan_direct_kernel<DK, J, S>), grid, block, 0, stream, a, ncol);
-    return hipGetLastError();
+    return a.gk ? launch_dk_j_tp<DK, J, true>(a, stream) : launch_dk_j_tp<DK, J, false>(a, stream);
 }
 
 template <int DK>

@@ -139,6 +139,63 @@ int prepare(const swila_shape *shape, const swila_opts *opts, bool decode, const
     return SWILA_OK;
 }
 
+// Temporal SwiLA arguments (App. B.3): the two gate-logit tensors (inputs,
+// in_dtype, [B,T,H,Dv]) and the prior state in and out ([B,H,2,J,Dv] fp32).
+// prior_out may equal prior_in; every other pair is disjoint, and none of them
+// overlaps a tensor of the base call.
+int check_temporal(const swila_shape *shape, const swila_opts *opts, const swila_temporal *tp,
+                   const void *q, const void *k, const void *v, const void *lb, const void *lk,
+                   const void *lq, const float *state_in, float *state_out, void *o, float *resp,
+                   swila::LayerArgs *a) {
+    if (!tp) return fail(SWILA_EINVAL, "temporal is NULL");
+    const size_t B = shape->B, H = shape->H, T = shape->T, Dk = shape->Dk, Dv = shape->Dv,
+                 J = shape->J;
+    const size_t ie = opts->in_dtype == SWILA_BF16 ? 2 : 4;
+    const size_t oe = opts->out_dtype == SWILA_BF16 ? 2 : 4;
+    const bool need = T > 0;
+    const Span t_in[] = {
+        {"gate_k_logit", tp->gate_k_logit, B * T * H * Dv * ie},
+        {"gate_q_logit", tp->gate_q_logit, B * T * H * Dv * ie},
+        {"prior_in", tp->prior_in, B * H * 2 * J * Dv * 4},
+    };
+    const Span p_out{"prior_out", tp->prior_out, B * H * 2 * J * Dv * 4};
+    for (int i = 0; i < 3; ++i) {
+        int rc = check_ptr(t_in[i], need && i < 2);
+        if (rc) return rc;
+    }
+    int rc = check_ptr(p_out, false);
+    if (rc) return rc;
+    const Span base_in[] = {
+        {"q", q, B * T * H * Dk * ie},          {"k", k, B * T * H * Dk * ie},
+        {"v", v, B * T * H * Dv * ie},          {"beta_logit", lb, B * T * H * J * Dv * ie},
+        {"prior_k_logit", lk, B * T * H * J * Dv * ie},
+        {"prior_q_logit", lq, B * T * H * J * Dv * ie},
+        {"state_in", state_in, B * H * J * Dk * Dv * 4},
+    };
+    const Span base_out[] = {
+        {"o", o, B * T * H * Dv * oe},
+        {"state_out", state_out, B * H * J * Dk * Dv * 4},
+        {"resp_out", resp, B * T * H * J * Dv * 4},
+    };
+    for (const Span &x : base_out) {
+        for (const Span &t : t_in)
+            if (overlap(t, x)) return fail(SWILA_EINVAL, "%s overlaps %s", t.name, x.name);
+        if (overlap(p_out, x)) return fail(SWILA_EINVAL, "prior_out overlaps %s", x.name);
+    }
+    for (const Span &x : base_in)
+        if (overlap(p_out, x)) return fail(SWILA_EINVAL, "prior_out overlaps %s", x.name);
+    for (int i = 0; i < 3; ++i) {
+        if (i == 2 && tp->prior_out == tp->prior_in) continue;   // updated in place
+        if (overlap(p_out, t_in[i]))
+            return fail(SWILA_EINVAL, "prior_out overlaps %s", t_in[i].name);
+    }
+    a->gk = tp->gate_k_logit;
+    a->gq = tp->gate_q_logit;
+    a->prior_in = tp->prior_in;
+    a->prior_out = tp->prior_out;
+    return SWILA_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -233,6 +290,57 @@ int swila_forward(const swila_shape *shape, const swila_opts *opts, const void *
                        (opts->algo == SWILA_ALGO_AUTO && opts->in_dtype == SWILA_BF16);
     if (chunk) return map_hip(swila::launch_scan_pipe(a, st), "chunk scan launch");
     return map_hip(swila::launch_scan_direct(a, st), "scan launch");
+}
+
+int swila_forward_temporal(const swila_shape *shape, const swila_opts *opts, const void *q,
+                           const void *k, const void *v, const void *beta_logit,
+                           const void *prior_k_logit, const void *prior_q_logit,
+                           const swila_temporal *temporal, const float *state_in,
+                           float *state_out, void *o, float *resp_out, void *stream) {
+    clear_error();
+    swila::LayerArgs a;
+    int rc = prepare(shape, opts, false, q, k, v, beta_logit, prior_k_logit, prior_q_logit,
+                     state_in, state_out, o, resp_out, &a);
+    if (rc) return rc;
+    rc = check_temporal(shape, opts, temporal, q, k, v, beta_logit, prior_k_logit, prior_q_logit,
+                        state_in, state_out, o, resp_out, &a);
+    if (rc) return rc;
+    if (opts->algo == SWILA_ALGO_NEWTON)
+        return fail(SWILA_EUNSUPPORTED,
+                    "SWILA_ALGO_NEWTON linearises the plain recurrence; not the temporal form");
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    if (shape->T == 0) {
+        if (state_out) {
+            rc = map_hip(swila::launch_state_fill(state_out, state_in,
+                                                  swila_state_bytes(shape) / sizeof(float), st),
+                         "state copy");
+            if (rc) return rc;
+        }
+        if (!temporal->prior_out) return SWILA_OK;
+        const size_t n = (size_t)shape->B * shape->H * 2 * shape->J * shape->Dv;
+        return map_hip(swila::launch_fill(temporal->prior_out, temporal->prior_in, n,
+                                          1.0f / shape->J, st),
+                       "prior state copy");
+    }
+    if (opts->algo == SWILA_ALGO_CHUNK_EXACT)
+        return fail(SWILA_EUNSUPPORTED, "the temporal form runs on SWILA_ALGO_RECURRENT");
+    return map_hip(swila::launch_scan_direct(a, st), "scan launch");
+}
+
+int swila_decode_step_temporal(const swila_shape *shape, const swila_opts *opts, const void *q,
+                               const void *k, const void *v, const void *beta_logit,
+                               const void *prior_k_logit, const void *prior_q_logit,
+                               const swila_temporal *temporal, const float *state_in,
+                               float *state_out, void *o, void *stream) {
+    clear_error();
+    swila::LayerArgs a;
+    int rc = prepare(shape, opts, true, q, k, v, beta_logit, prior_k_logit, prior_q_logit,
+                     state_in, state_out, o, nullptr, &a);
+    if (rc) return rc;
+    rc = check_temporal(shape, opts, temporal, q, k, v, beta_logit, prior_k_logit, prior_q_logit,
+                        state_in, state_out, o, nullptr, &a);
+    if (rc) return rc;
+    return map_hip(swila::launch_decode(a, static_cast<hipStream_t>(stream)), "decode launch");
 }
 
 int swila_decode_step(const swila_shape *shape, const swila_opts *opts, const void *q,

@@ -168,3 +168,47 @@ def test_python_binding_checks_before_calling():
     x = torch.zeros(1, 4, 1, 16)
     with pytest.raises(ValueError, match="device tensor"):
         sw.forward(x, x, x, x, x, x)
+
+
+def _fwd_t(lib, tp, shape=None, opts=None, o=FAKE2, state_in=None, state_out=None, resp=None):
+    shape = shape or sw.Shape(1, 2, 8, 64, 64, 4)
+    opts = opts or OPTS
+    ptrs = [ctypes.c_void_p((1 << 20) + (i << 26)) for i in range(6)]
+    rc = lib.swila_forward_temporal(ctypes.byref(shape), ctypes.byref(opts), *ptrs,
+                                    None if tp is None else ctypes.byref(tp), state_in, state_out,
+                                    o, resp, None)
+    return rc, lib.swila_last_error().decode()
+
+
+def test_temporal_argument_checks(lib):
+    gk, gq = (1 << 32), (1 << 32) + (1 << 26)
+    assert _fwd_t(lib, None) == (sw.EINVAL, "temporal is NULL")
+    assert _fwd_t(lib, sw.Temporal(None, gq, None, None)) == (sw.EINVAL, "gate_k_logit is NULL")
+    assert _fwd_t(lib, sw.Temporal(gk, None, None, None)) == (sw.EINVAL, "gate_q_logit is NULL")
+    rc, msg = _fwd_t(lib, sw.Temporal(gk + 2, gq, None, None))
+    assert rc == sw.EINVAL and "gate_k_logit is not 16-byte aligned" in msg
+    # a gate overlapping an output
+    rc, msg = _fwd_t(lib, sw.Temporal(FAKE2.value, gq, None, None))
+    assert rc == sw.EINVAL and "gate_k_logit overlaps o" in msg
+    # prior_out overlapping (not equal to) prior_in; equal is in place and passes the checks
+    pin = 1 << 35
+    rc, msg = _fwd_t(lib, sw.Temporal(gk, gq, pin, pin + 64))
+    assert rc == sw.EINVAL and "prior_out overlaps prior_in" in msg
+    rc, msg = _fwd_t(lib, sw.Temporal(gk, gq, None, gq))
+    assert rc == sw.EINVAL and "prior_out overlaps gate_q_logit" in msg
+    # the App. D linearisation is that of the plain recurrence
+    newton = sw.Opts(sw.BF16, sw.BF16, sw.ALGO_NEWTON, 0, 0, 0.0, 0)
+    rc, msg = _fwd_t(lib, sw.Temporal(gk, gq, None, None), opts=newton)
+    assert rc == sw.EUNSUPPORTED and "NEWTON" in msg
+    chunk = sw.Opts(sw.BF16, sw.BF16, sw.ALGO_CHUNK_EXACT, 0, 0, 0.0, 0)
+    rc, msg = _fwd_t(lib, sw.Temporal(gk, gq, None, None), opts=chunk)
+    assert rc == sw.EUNSUPPORTED
+
+
+def test_temporal_decode_requires_one_token(lib):
+    ptrs = [ctypes.c_void_p((1 << 20) + (i << 26)) for i in range(6)]
+    tp = sw.Temporal(1 << 32, (1 << 32) + (1 << 26), None, None)
+    rc = lib.swila_decode_step_temporal(ctypes.byref(sw.Shape(4, 2, 2, 64, 64, 4)),
+                                        ctypes.byref(OPTS), *ptrs, ctypes.byref(tp), None, None,
+                                        FAKE2, None)
+    assert rc == sw.EINVAL and "T == 1" in lib.swila_last_error().decode()

@@ -1,0 +1,170 @@
+"""Parity of the Temporal SwiLA path (Sec. 3.3, App. B.3) through the C ABI
+with the fp64 oracle: the token-by-token scan and the decode step.
+
+Bar as for the plain form: per (b, h), max|gpu - oracle| / max|oracle| <= 1e-4
+for fp32 inputs and <= 2e-2 for bf16 inputs, for the outputs, the final state,
+the responsibilities and the final prior state.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+from gpu_helpers import NAMES, head_rel_err, to_device, tol_for, torch_dtype
+
+pytestmark = pytest.mark.gpu
+
+
+def _prior_err(x, y):
+    """max |x - y| per (b, h) over the prior state [B,H,2,J,Dv] (values in [0, 1])."""
+    return float(np.abs(np.asarray(x, np.float64) - y).max())
+
+
+def _run_gpu(inp, tmp, dtype, algo="auto", resp=True):
+    import torch
+    import paper_2609_39034_amd as sw
+    dev = to_device(inp, dtype)
+    td = torch_dtype(dtype)
+    gk = torch.from_numpy(tmp["gk"]).to("cuda", td)
+    gq = torch.from_numpy(tmp["gq"]).to("cuda", td)
+    pin = None if tmp["prior"] is None else torch.from_numpy(tmp["prior"]).cuda()
+    res = sw.forward_temporal(*(dev[n] for n in NAMES), gk, gq, dev["state"], pin, resp=resp,
+                              algo=algo)
+    torch.cuda.synchronize()
+    return [x.float().cpu().numpy().astype(np.float64) for x in res]
+
+
+def _run_oracle(inp, tmp):
+    return oracle.forward(*(inp[n] for n in NAMES), inp["state"], gate_k_logit=tmp["gk"],
+                          gate_q_logit=tmp["gq"], prior_in=tmp["prior"], want_resp=True)
+
+
+CASES = [
+    # B, H, T, Dk, Dv, J, dtype, state_std, prior state given, gate scale
+    (1, 1, 64, 16, 16, 2, "f32", 0.0, False, 1.0),
+    (2, 3, 50, 64, 128, 4, "f32", 0.3, True, 1.0),
+    (2, 2, 37, 128, 128, 4, "bf16", 0.1, True, 2.0),
+    (1, 2, 33, 128, 64, 8, "f32", 0.2, True, 1.0),
+    (2, 1, 17, 32, 16, 3, "f32", 0.5, False, 3.0),
+    (1, 3, 21, 16, 32, 1, "f32", 0.5, True, 1.0),
+    (3, 1, 40, 64, 32, 2, "bf16", 0.0, False, 1.0),
+    (1, 1, 1, 128, 128, 4, "f32", 0.2, True, 1.0),
+    (2, 2, 16, 32, 128, 8, "bf16", 0.1, True, 0.5),
+    (1, 2, 70, 64, 64, 4, "bf16", 0.0, False, 1.0),
+]
+
+
+@pytest.mark.parametrize("B,H,T,Dk,Dv,J,dtype,std,with_prior,gs", CASES)
+def test_temporal_forward(B, H, T, Dk, Dv, J, dtype, std, with_prior, gs):
+    seed = 300 + T + J
+    inp = workloads.iid_inputs(B, H, T, Dk, Dv, J, dtype=dtype, seed=seed, state_std=std)
+    tmp = workloads.temporal_inputs(B, H, T, Dv, J, dtype=dtype, seed=seed, gate_scale=gs,
+                                    prior_state=with_prior)
+    o, s, p, r = _run_gpu(inp, tmp, dtype)
+    ref = _run_oracle(inp, tmp)
+    tol = tol_for(dtype)
+    eo, es, er = (head_rel_err(o, ref["o"], "o"), head_rel_err(s, ref["state"], "state"),
+                  head_rel_err(r, ref["resp"], "resp"))
+    ep = _prior_err(p, ref["prior"])
+    print("o %.3e state %.3e resp %.3e prior %.3e (tol %.0e)" % (eo, es, er, ep, tol))
+    assert eo <= tol and es <= tol and er <= tol and ep <= tol
+
+
+def test_temporal_saturated_gates_equal_plain():
+    """Gates at 1 (logit 40, sigmoid 1 in fp32) give the plain recurrence."""
+    import torch
+    import paper_2609_39034_amd as sw
+    B, H, T, D, J = 2, 2, 45, 64, 4
+    inp = workloads.iid_inputs(B, H, T, D, D, J, dtype="f32", seed=77, state_std=0.2)
+    dev = to_device(inp, "f32")
+    g = torch.full((B, T, H, D), 40.0, device="cuda")
+    o_t, s_t, _ = sw.forward_temporal(*(dev[n] for n in NAMES), g, g, dev["state"], None)
+    o_p, s_p = sw.forward(*(dev[n] for n in NAMES), dev["state"], algo="recurrent")
+    torch.cuda.synchronize()
+    eo = head_rel_err(o_t.cpu().numpy(), o_p.cpu().numpy().astype(np.float64), "o")
+    es = head_rel_err(s_t.cpu().numpy(), s_p.cpu().numpy().astype(np.float64), "state")
+    print("o %.3e state %.3e" % (eo, es))
+    assert eo <= 1e-5 and es <= 1e-5
+
+
+def test_temporal_chained_calls():
+    """Two calls chained through the state and the prior state (in place)
+    match the oracle over the whole sequence."""
+    import torch
+    import paper_2609_39034_amd as sw
+    B, H, T, D, J, c = 2, 2, 41, 32, 3, 19
+    inp = workloads.iid_inputs(B, H, T, D, D, J, dtype="f32", seed=88, state_std=0.3)
+    tmp = workloads.temporal_inputs(B, H, T, D, J, dtype="f32", seed=88, prior_state=True)
+    dev = to_device(inp, "f32")
+    gk, gq = torch.from_numpy(tmp["gk"]).cuda(), torch.from_numpy(tmp["gq"]).cuda()
+    st = dev["state"].clone()
+    pr = torch.from_numpy(tmp["prior"]).cuda()
+    outs = []
+    for t0, t1 in ((0, c), (c, T)):
+        sl = [dev[n][:, t0:t1].contiguous() for n in NAMES]
+        o, _, _ = sw.forward_temporal(*sl, gk[:, t0:t1].contiguous(), gq[:, t0:t1].contiguous(),
+                                      st, pr, state_out=st, prior_out=pr)
+        outs.append(o)
+    torch.cuda.synchronize()
+    ref = _run_oracle(inp, tmp)
+    o = torch.cat(outs, dim=1).cpu().numpy()
+    eo, es = head_rel_err(o, ref["o"], "o"), head_rel_err(st.cpu().numpy(), ref["state"], "state")
+    ep = _prior_err(pr.cpu().numpy(), ref["prior"])
+    print("o %.3e state %.3e prior %.3e" % (eo, es, ep))
+    assert eo <= 1e-4 and es <= 1e-4 and ep <= 1e-4
+
+
+def test_temporal_empty_sequence():
+    """T = 0 copies the state and the prior state (1/J when none is given)."""
+    import torch
+    import paper_2609_39034_amd as sw
+    B, H, D, J = 2, 3, 16, 4
+    q = torch.empty((B, 0, H, D), device="cuda")
+    lb = torch.empty((B, 0, H, J, D), device="cuda")
+    g = torch.empty((B, 0, H, D), device="cuda")
+    st = torch.randn((B, H, J, D, D), device="cuda")
+    o, s, p = sw.forward_temporal(q, q, q, lb, lb, lb, g, g, st, None)
+    torch.cuda.synchronize()
+    assert o.numel() == 0
+    assert torch.equal(s, st)
+    assert torch.allclose(p, torch.full_like(p, 1.0 / J))
+
+
+DECODE = [
+    # B, H, Dk, Dv, J, dtype, steps
+    (4, 3, 64, 64, 4, "f32", 3),
+    (3, 2, 128, 128, 4, "bf16", 4),
+    (2, 2, 32, 16, 3, "f32", 3),
+    (2, 1, 16, 32, 8, "bf16", 2),
+    (5, 2, 128, 64, 1, "f32", 2),
+]
+
+
+@pytest.mark.parametrize("B,H,Dk,Dv,J,dtype,steps", DECODE)
+def test_temporal_decode_steps(B, H, Dk, Dv, J, dtype, steps):
+    """Consecutive decode steps, state and prior state updated in place, equal
+    the oracle's forward over those tokens."""
+    import torch
+    import paper_2609_39034_amd as sw
+    seed = 500 + Dk + J
+    inp = workloads.iid_inputs(B, H, steps, Dk, Dv, J, dtype=dtype, seed=seed, state_std=0.1)
+    tmp = workloads.temporal_inputs(B, H, steps, Dv, J, dtype=dtype, seed=seed, prior_state=True)
+    dev = to_device(inp, dtype)
+    td = torch_dtype(dtype)
+    gk = torch.from_numpy(tmp["gk"]).to("cuda", td)
+    gq = torch.from_numpy(tmp["gq"]).to("cuda", td)
+    st = dev["state"].clone()
+    pr = torch.from_numpy(tmp["prior"]).cuda()
+    outs = []
+    for t in range(steps):
+        x = [dev[n][:, t].contiguous() for n in NAMES]
+        o, _, _ = sw.decode_step_temporal(*x, gk[:, t].contiguous(), gq[:, t].contiguous(), st, pr)
+        outs.append(o.float())
+    torch.cuda.synchronize()
+    ref = _run_oracle(inp, tmp)
+    o = torch.stack(outs, dim=1).cpu().numpy()
+    tol = tol_for(dtype)
+    eo, es = head_rel_err(o, ref["o"], "o"), head_rel_err(st.cpu().numpy(), ref["state"], "state")
+    ep = _prior_err(pr.cpu().numpy(), ref["prior"])
+    print("o %.3e state %.3e prior %.3e (tol %.0e)" % (eo, es, ep, tol))
+    assert eo <= tol and es <= tol and ep <= tol
