@@ -190,10 +190,10 @@ typedef struct swila_temporal {
 /*
  * swila_forward with the temporal priors above.  The other arguments are those
  * of swila_forward (no workspace: SWILA_ALGO_NEWTON, whose linearisation is
- * that of the plain recurrence, returns SWILA_EUNSUPPORTED).  The form runs on
- * the token-by-token scan (SWILA_ALGO_AUTO or SWILA_ALGO_RECURRENT, either
- * input dtype); SWILA_ALGO_CHUNK_EXACT returns SWILA_EUNSUPPORTED.  T == 0
- * copies state_in and prior_in (or zeros and 1/J) to the outputs.
+ * that of the plain recurrence, returns SWILA_EUNSUPPORTED).  SWILA_ALGO_AUTO
+ * picks the matrix-core chunk scan for bf16 inputs and the token-by-token scan
+ * for fp32, as swila_forward does.  T == 0 copies state_in and prior_in (or
+ * zeros and 1/J) to the outputs.
  */
 int swila_forward_temporal(const swila_shape *shape, const swila_opts *opts,
                            const void *q, const void *k, const void *v,

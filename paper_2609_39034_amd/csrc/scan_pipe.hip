@@ -128,8 +128,11 @@ struct PCfg {
     static_assert(DB * JP <= 64, "one sequential wave");
 };
 
-template <int DK, int J, int DB, bool NT>
+// MD: 0 exact scan, 1 Newton sweeps (App. D), 2 exact scan of Temporal SwiLA
+// (App. B.3).
+template <int DK, int J, int DB, int MD>
 struct PSmem {
+    static constexpr bool NT = MD == 1, TP = MD == 2;
     using C = PCfg<DK, J, DB>;
     uint4 k[kRingKQ][C::KPIECES];
     uint4 q[kRingKQ][C::KPIECES];
@@ -138,6 +141,8 @@ struct PSmem {
     uint4 lq[kRingQP][C::LPIECES];
     uint4 v[kRingS][C::VPIECES];
     uint4 pw[NT ? kRingQP : 1][NT ? C::PPIECES : 1];  // Newton: previous sweep's predictions
+    uint4 gk[TP ? kRingS : 1][TP ? C::VPIECES : 1];    // temporal: key gate logits, [t][dl]
+    uint4 gq[TP ? kRingQP : 1][TP ? C::VPIECES : 1];   // temporal: query gate logits
     union {
         // exact: {beta, log2(e) key-prior logit}, [column][token]; a column's
         // 16 tokens are 128 contiguous bytes, padded so that the sequential
@@ -149,7 +154,9 @@ struct PSmem {
         };
     };
     alignas(16) float vs[NT ? 1 : 2][DB][kC + 4];   // exact: s v, [dim][token]
-    float pq[2][kC][C::NP];    // query prior
+    alignas(16) float gs[TP ? 2 : 1][TP ? DB : 1][kC + 4];   // temporal: 1 - g^k, [dim][token]
+    float gqs[TP ? 3 : 1][kC][TP ? DB : 1];                  // temporal: g^q, [token][dim]
+    float pq[TP ? 3 : 2][kC][C::NP];    // query prior (temporal: the running prior, 3 slots)
     alignas(16) float g[2][kC][kC + 4];    // K_n K_n^T, for the sequential wave
     float p[2][C::N][kTP];     // chunk-start predictions, [column][token]
     float c[2][C::N + 1][kTP];  // coefficients, [column][token] (column N: idle lanes)
@@ -227,10 +234,11 @@ __device__ __forceinline__ int first_for(int base, int mw, int nw) {
 // Tokens past T re-read token T - 1 (in range); the recurrence gives them
 // beta = 0.  In Newton mode the chunk's predictions from the previous sweep
 // ([kC][N] fp32 at pred + t0 N, the block's workspace) come along.
-template <int DK, int J, int DB, bool NT, int NIW>
-__device__ __forceinline__ void issue_chunk(const LayerArgs &a, PSmem<DK, J, DB, NT> &sm,
+template <int DK, int J, int DB, int MD, int NIW>
+__device__ __forceinline__ void issue_chunk(const LayerArgs &a, PSmem<DK, J, DB, MD> &sm,
                                             uint32_t lds_base, int m, int t0, int b, int h,
                                             int d0, int mw, int lane, const float *pred) {
+    constexpr bool NT = MD == 1, TP = MD == 2;
     // LDS byte address of a destination inside sm
     auto at = [&](const uint4 *dst) {
         return lds_base + (uint32_t)(reinterpret_cast<const char *>(dst) -
@@ -273,14 +281,21 @@ __device__ __forceinline__ void issue_chunk(const LayerArgs &a, PSmem<DK, J, DB,
         logit(a.lb, sm.lb[ss], 2 * nk);
         logit(a.lk, sm.lk[ss], 2 * nk + nl);
         logit(a.lq, sm.lq[sqp], 2 * nk + 2 * nl);
-        const char *vsrc = static_cast<const char *>(a.v) + (row0 * Dv + d0) * 2;
-        for (int ins = first_for(2 * nk + 3 * nl, mw, NIW); ins < 2 * nk + 3 * nl + nv;
-             ins += NIW) {
-            const int part = ins - (2 * nk + 3 * nl), s = part * 64 + lane;
-            if (s < C::VPIECES) {
-                const int t = s / (DB / 8), qd = s % (DB / 8);
-                dma16(vsrc + (uint32_t)(t * H * Dv * 2 + 16 * qd), at(sm.v[ss] + part * 64));
+        // [t][dl] tensors of one value per (token, output dim): v, and the gates
+        auto vrow = [&](const void *base, uint4 *dstv, int ibase) {
+            const char *src = static_cast<const char *>(base) + (row0 * Dv + d0) * 2;
+            for (int ins = first_for(ibase, mw, NIW); ins < ibase + nv; ins += NIW) {
+                const int part = ins - ibase, s = part * 64 + lane;
+                if (s < C::VPIECES) {
+                    const int t = s / (DB / 8), qd = s % (DB / 8);
+                    dma16(src + (uint32_t)(t * H * Dv * 2 + 16 * qd), at(dstv + part * 64));
+                }
             }
+        };
+        vrow(a.v, sm.v[ss], 2 * nk + 3 * nl);
+        if constexpr (TP) {
+            vrow(a.gk, sm.gk[ss], 2 * nk + 3 * nl + nv);
+            vrow(a.gq, sm.gq[sqp], 2 * nk + 3 * nl + 2 * nv);
         }
     } else {
         const size_t row0 = (size_t)b * T;
@@ -316,15 +331,22 @@ __device__ __forceinline__ void issue_chunk(const LayerArgs &a, PSmem<DK, J, DB,
         logit(a.lb, sm.lb[ss], 2 * nk);
         logit(a.lk, sm.lk[ss], 2 * nk + nl);
         logit(a.lq, sm.lq[sqp], 2 * nk + 2 * nl);
-        for (int ins = first_for(2 * nk + 3 * nl, mw, NIW); ins < 2 * nk + 3 * nl + nv;
-             ins += NIW) {
-            const int part = ins - (2 * nk + 3 * nl), s = part * 64 + lane;
-            if (s < C::VPIECES) {
-                const int t = s / (DB / 8), qd = s % (DB / 8);
-                const int tc = min(t0 + t, T - 1);
-                dma16(static_cast<const uint16_t *>(a.v) + ((row0 + tc) * H + h) * Dv + d0 + 8 * qd,
-                      at(sm.v[ss] + part * 64));
+        auto vrow = [&](const void *base, uint4 *dstv, int ibase) {
+            for (int ins = first_for(ibase, mw, NIW); ins < ibase + nv; ins += NIW) {
+                const int part = ins - ibase, s = part * 64 + lane;
+                if (s < C::VPIECES) {
+                    const int t = s / (DB / 8), qd = s % (DB / 8);
+                    const int tc = min(t0 + t, T - 1);
+                    dma16(static_cast<const uint16_t *>(base) + ((row0 + tc) * H + h) * Dv + d0 +
+                              8 * qd,
+                          at(dstv + part * 64));
+                }
             }
+        };
+        vrow(a.v, sm.v[ss], 2 * nk + 3 * nl);
+        if constexpr (TP) {
+            vrow(a.gk, sm.gk[ss], 2 * nk + 3 * nl + nv);
+            vrow(a.gq, sm.gq[sqp], 2 * nk + 3 * nl + 2 * nv);
         }
     }
     if constexpr (NT) {
@@ -411,12 +433,13 @@ __device__ __forceinline__ void pipe_coords(int id, int ndb, int nheads, int &db
 
 // LDS (over 60 KB a block) allows at most two blocks on a compute unit, so at
 // most two waves share a SIMD: the compiler may use every register for that.
-template <int DK, int J, int DB, bool NT, int NH>
+template <int DK, int J, int DB, int MD, int NH>
 __global__ __launch_bounds__(512)
 void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
     using C = PCfg<DK, J, DB>;
     constexpr int IT = C::IT, N = C::N, NW = C::NW, JP = C::JP;
-    __shared__ PSmem<DK, J, DB, NT> sm;
+    constexpr bool NT = MD == 1, TP = MD == 2;
+    __shared__ PSmem<DK, J, DB, MD> sm;
     const uint32_t lds_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void *)&sm;
 
     const int tid = threadIdx.x;
@@ -434,6 +457,7 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
     // per-chunk bookkeeping (transfers, priors, input prep, outputs), which the
     // tile waves do themselves when NH = 0.
     const bool tile = w < NW;
+    const bool book = NH == 0 ? tile : w > NW;        // this wave does the bookkeeping
     constexpr int NBW = NH == 0 ? NW : NH;            // bookkeeping waves
     constexpr int NBT = 64 * NBW;                     // bookkeeping threads
     const int bw = NH == 0 ? w : w - (NW + 1);        // index among them
@@ -481,7 +505,7 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
     const int bdl = (sl / JP) % DB, bj = sl % JP;
     const bool bact = seq && sl < DB * JP && bj < J;
     const bool bpad = seq && sl < DB * JP && bj >= J;   // padding component (J = 3)
-    const bool want_r = a.resp != nullptr;
+    const bool want_r = a.resp != nullptr;   // (the temporal form always keeps r)
     const int bcol = bact ? bj * DB + bdl : 0;
     const int bsto = bact ? bcol : N;
 
@@ -561,7 +585,49 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
     // derived inputs of chunk m (parity pr) for the sequential wave
     auto prep_seq_inputs = [&](int m, int pr) {
         const int rs = m % kRingS;
-        if constexpr (!NT) {
+        if constexpr (TP) {
+            // Temporal (App. B.3), per (t, dl) over the J components: beta,
+            // g^k pi^k (pi^k = softmax_j of the key-prior logits) and 1 - g^k for
+            // the key prior (1 - g^k) r_{t-1} + g^k pi^k the sequential wave
+            // forms; padded tokens carry no mass and keep r_{t-1}.
+#pragma unroll
+            for (int i_ = 0; i_ < ceil_div(NPG, NBT); ++i_) {
+                const int gi = bt + i_ * NBT;
+                if (gi >= NPG) break;
+                const int e = PE * gi, t = e / DB, dl = e % DB;
+                const bool ok = m * kC + t < T;
+                float lbj[J][PE], lkj[J][PE], mk[PE], zk[PE], gv[PE], vv[PE];
+                bf16_row<PE>(sm.gk[rs], e, gv);
+                bf16_row<PE>(sm.v[rs], e, vv);
+#pragma unroll
+                for (int u = 0; u < PE; ++u) mk[u] = -INFINITY, zk[u] = 0.f;
+#pragma unroll
+                for (int j = 0; j < J; ++j) {
+                    bf16_row<PE>(sm.lb[rs], t * N + j * DB + dl, lbj[j]);
+                    bf16_row<PE>(sm.lk[rs], t * N + j * DB + dl, lkj[j]);
+#pragma unroll
+                    for (int u = 0; u < PE; ++u) mk[u] = fmaxf(mk[u], lkj[j][u]);
+                }
+#pragma unroll
+                for (int j = 0; j < J; ++j)
+#pragma unroll
+                    for (int u = 0; u < PE; ++u) {
+                        lkj[j][u] = exp_fast(lkj[j][u] - mk[u]);
+                        zk[u] += lkj[j][u];
+                    }
+#pragma unroll
+                for (int u = 0; u < PE; ++u) {
+                    const float g = ok ? sigmoid(gv[u]) : 0.f;
+                    const float gz = g * rcp_fast(zk[u]);
+#pragma unroll
+                    for (int j = 0; j < J; ++j)
+                        sm.sq[pr][j * DB + dl + u][t] =
+                            make_float2(ok ? sigmoid(lbj[j][u]) : 0.f, gz * lkj[j][u]);
+                    sm.gs[pr][dl + u][t] = 1.f - g;
+                    sm.vs[pr][dl + u][t] = kS * vv[u];
+                }
+            }
+        } else if constexpr (!NT) {
 #pragma unroll
           for (int i_ = 0; i_ < ceil_div(kC * N / 4, NBT); ++i_) {
             const int g4 = bt + i_ * NBT;
@@ -645,6 +711,8 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
     // pi^q of chunk m: softmax over j of the query-prior logits, per (t, dl)
     auto prep_query_prior = [&](int m, int pr) {
         const int rs = m % kRingQP;
+        // temporal: pi^q itself (the scan below forms rhobar and scales it)
+        constexpr float kQS = TP ? 1.f : kInvWS;
 #pragma unroll
         for (int i_ = 0; i_ < ceil_div(NPG, NBT); ++i_) {
             const int gi = bt + i_ * NBT;
@@ -667,12 +735,38 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
                     z[u] += x[j][u];
                 }
 #pragma unroll
-            for (int u = 0; u < PE; ++u) z[u] = kInvWS * rcp_fast(z[u]);
+            for (int u = 0; u < PE; ++u) z[u] = kQS * rcp_fast(z[u]);
 #pragma unroll
             for (int j = 0; j < J; ++j) {
 #pragma unroll
                 for (int u = 0; u < PE; ++u) x[j][u] *= z[u];
                 f32_row<PE>(&sm.pq[pr][t][j * DB + dl], x[j]);
+            }
+            if constexpr (TP) {
+                float gv[PE];
+                bf16_row<PE>(sm.gq[rs], e, gv);
+#pragma unroll
+                for (int u = 0; u < PE; ++u) sm.gqs[pr][t][dl + u] = sigmoid(gv[u]);
+            }
+        }
+    };
+    // Temporal: the running query prior rhobar_t = (1 - g^q_t) rhobar_{t-1} +
+    // g^q_t pi^q_t (App. B.3) over chunk m, one bookkeeping thread per column,
+    // carried in rho from chunk to chunk; written in place of pi^q (scaled like
+    // the plain prior).  Padded tokens leave it unchanged.
+    float rho = 1.f / J;
+    if constexpr (TP) {
+        if (book && bt < N && a.prior_in)
+            rho = a.prior_in[(((size_t)b * H + h) * 2 * J + J + bt / DB) * Dv + d0 + bt % DB];
+    }
+    auto scan_query_prior = [&](int m) {
+        if (bt < N) {
+            const int slot = m % 3, dl = bt % DB;
+#pragma unroll
+            for (int t = 0; t < kC; ++t) {
+                const float pi = sm.pq[slot][t][bt];
+                if (m * kC + t < T) rho = fmaf(sm.gqs[slot][t][dl], pi - rho, rho);
+                sm.pq[slot][t][bt] = kInvWS * rho;
             }
         }
     };
@@ -742,7 +836,7 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
         Yacc = mfma16(alo, chi, Yacc);
 #pragma unroll
         for (int r = 0; r < 4; ++r)
-            sm.py[pr][4 * lg + r][col] = Yacc[r] * sm.pq[pr][4 * lg + r][col];
+            sm.py[pr][4 * lg + r][col] = Yacc[r] * sm.pq[TP ? m % 3 : pr][4 * lg + r][col];
     };
 
     if constexpr (NT) {
@@ -791,7 +885,16 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
             // Exact mode: the per-token inputs of the next chunk and the first row
             // of its Gram matrix, read while the matrix-core waves form its
             // predictions (between the two barriers), off the critical path.
-            float vvN[kC], lkvN[kC], bevN[kC], growN[kC];
+            // Temporal: lkvN holds g^k pi^k and gsN 1 - g^k of the key prior
+            // (1 - g^k) r_{t-1} + g^k pi^k (App. B.3); rprev is r_{t-1} of this
+            // lane's column, carried from chunk to chunk.
+            float vvN[kC], lkvN[kC], bevN[kC], growN[kC], gsN[TP ? kC : 1];
+            float rprev = 0.f;
+            if constexpr (TP) {
+                if (bact)
+                    rprev = a.prior_in ? a.prior_in[(((size_t)b * H + h) * 2 * J + bj) * Dv + d0 + bdl]
+                                       : 1.f / J;
+            }
             auto fetch_inputs = [&](int prn) {
                 // 16-byte reads: few enough to be in flight together
                 const float4 *sq4 = reinterpret_cast<const float4 *>(sm.sq[prn][bcol]);
@@ -807,6 +910,14 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
                     const float4 x = vs4[i], y = g4[i];
                     vvN[4 * i] = x.x, vvN[4 * i + 1] = x.y, vvN[4 * i + 2] = x.z, vvN[4 * i + 3] = x.w;
                     growN[4 * i] = y.x, growN[4 * i + 1] = y.y, growN[4 * i + 2] = y.z, growN[4 * i + 3] = y.w;
+                }
+                if constexpr (TP) {
+                    const float4 *gs4 = reinterpret_cast<const float4 *>(sm.gs[prn][bdl]);
+#pragma unroll
+                    for (int i = 0; i < kC / 4; ++i) {
+                        const float4 x = gs4[i];
+                        gsN[4 * i] = x.x, gsN[4 * i + 1] = x.y, gsN[4 * i + 2] = x.z, gsN[4 * i + 3] = x.w;
+                    }
                 }
             };
             block_sync_lds();               // prologue: ring filled
@@ -827,14 +938,16 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
                     // [2^-100, 2^100] (every component underflowing, or a logit
                     // beyond about 60), the chunk is run again with the maximum
                     // subtracted.
-                    float P[kC], vv[kC], lkv[kC], bev[kC];
+                    float P[kC], vv[kC], lkv[kC], bev[kC], gs[TP ? kC : 1];
 #pragma unroll
                     for (int t = 0; t < kC; ++t) {
                         // padding component of J = 3: no mass; idle lanes: harmless
                         vv[t] = vvN[t];
-                        lkv[t] = bpad ? -INFINITY : lkvN[t];
+                        lkv[t] = bpad ? (TP ? 0.f : -INFINITY) : lkvN[t];
                         bev[t] = bact ? bevN[t] : 0.f;
+                        if constexpr (TP) gs[t] = bpad ? 0.f : gsN[t];
                     }
+                    const float rprev0 = rprev;   // for a rerun of the chunk
 #pragma unroll
                     for (int u = 1; u < kC; ++u) grow[u] = growN[u];
                     auto load_pred = [&]() {
@@ -885,7 +998,11 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
                             };
                             const float d = vv[t] - P[t];
                             const float bd = bev[t] * d;
-                            const float ex = __builtin_amdgcn_exp2f(fmaf(-d, d, lkv[t]));
+                            float ex;
+                            if constexpr (TP)   // key prior (1 - g^k) r_{t-1} + g^k pi^k
+                                ex = fmaf(gs[t], rprev, lkv[t]) * __builtin_amdgcn_exp2f(-d * d);
+                            else
+                                ex = __builtin_amdgcn_exp2f(fmaf(-d, d, lkv[t]));
                             __builtin_amdgcn_sched_barrier(0);
                             defer(0);
                             __builtin_amdgcn_sched_barrier(0);
@@ -912,7 +1029,11 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
                             if ((t & 3) == 3)
                                 *reinterpret_cast<float4 *>(&sm.c[pr][bsto][t - 3]) =
                                     make_float4(cb[0], cb[1], cb[2], cb[3]);
-                            if constexpr (R) sm.r[pr][t][bsto] = ex * iz;
+                            if constexpr (R) {
+                                const float rt = ex * iz;
+                                sm.r[pr][t][bsto] = rt;
+                                if constexpr (TP) rprev = rt;
+                            }
                             zmin = fminf(zmin, fminf(z, iz));
                             cprev = cs;
 #pragma unroll
@@ -923,6 +1044,7 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
 #pragma unroll
                             for (int u = 1; u < kC; ++u) grow[u] = sm.g[pr][0][u];
                             load_pred();
+                            if constexpr (TP) rprev = rprev0;
 #pragma unroll
                             for (int t = 0; t < kC; ++t) {
                                 float gnext[kC];
@@ -930,20 +1052,25 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
                                 for (int u = t + 2; u < kC; ++u) gnext[u] = sm.g[pr][t + 1][u];
                                 const float d = vv[t] - P[t];
                                 const float bd = bev[t] * d;
-                                const float e = fmaf(-d, d, lkv[t]);
-                                const float ex = __builtin_amdgcn_exp2f(e - group_max<JP>(e));
+                                const float e = TP ? (bpad ? -INFINITY : -d * d) : fmaf(-d, d, lkv[t]);
+                                float ex = __builtin_amdgcn_exp2f(e - group_max<JP>(e));
+                                if constexpr (TP) ex *= fmaf(gs[t], rprev, lkv[t]);
                                 const float iz = rcp_fast(group_sum<JP>(ex));
                                 const float cs = (bd * ex) * iz;
 #pragma unroll
                                 for (int u = t + 1; u < kC; ++u) P[u] = fmaf(grow[u], cs, P[u]);
                                 sm.c[pr][bsto][t] = cs;
-                                if constexpr (R) sm.r[pr][t][bsto] = ex * iz;
+                                if constexpr (R) {
+                                    const float rt = ex * iz;
+                                    sm.r[pr][t][bsto] = rt;
+                                    if constexpr (TP) rprev = rt;
+                                }
 #pragma unroll
                                 for (int u = t + 2; u < kC; ++u) grow[u] = gnext[u];
                             }
                         }
                     };
-                    if (want_r) run(BoolTag<true>{});
+                    if (TP || want_r) run(BoolTag<true>{});
                     else run(BoolTag<false>{});
                 } else {
                     // ---- B: forward substitution of the linearised recurrence
@@ -1010,6 +1137,12 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
                 done = true;
             }
         }
+        if constexpr (TP) {
+            // r of the last token: part 0 of the prior state
+            if (bact && a.prior_out)
+                a.prior_out[(((size_t)b * H + h) * 2 * J + bj) * Dv + d0 + bdl] =
+                    sm.r[(NCH - 1) & 1][T - 1 - (NCH - 1) * kC][bsto];
+        }
         return;
     }
 
@@ -1032,54 +1165,56 @@ __global__ void int_fill_kernel(int *p, int n, int value) {
     if ((int)threadIdx.x < n) p[threadIdx.x] = value;
 }
 
-template <int DK, int J, int DB, bool NT>
+template <int DK, int J, int DB, int MD>
 hipError_t launch_cfg(const LayerArgs &a, const NewtonArgs &na, hipStream_t stream) {
     using C = PCfg<DK, J, DB>;
-    constexpr size_t lds = sizeof(PSmem<DK, J, DB, NT>);
+    constexpr size_t lds = sizeof(PSmem<DK, J, DB, MD>);
     static_assert(lds <= 160 * 1024, "LDS");
     const long blocks = (long)(a.Dv / DB) * a.H * a.B;
     // Enough blocks to put two on every compute unit (LDS permitting): their
     // waves hide each other's latencies, so the tile waves keep the
     // bookkeeping.  Otherwise helper waves take it over.
-    constexpr int NH = NT ? 0 : (C::NW < 3 ? C::NW : 3);
+    constexpr int NH = MD == 1 ? 0 : (C::NW < 3 ? C::NW : 3);
     if (NH == 0 || (blocks >= 512 && lds <= 80 * 1024)) {
-        hipLaunchKernelGGL((scan_pipe_kernel<DK, J, DB, NT, 0>), dim3((unsigned)blocks),
+        hipLaunchKernelGGL((scan_pipe_kernel<DK, J, DB, MD, 0>), dim3((unsigned)blocks),
                            dim3(64 * (C::NW + 1)), 0, stream, a, na);
     } else {
-        hipLaunchKernelGGL((scan_pipe_kernel<DK, J, DB, NT, NH>), dim3((unsigned)blocks),
+        hipLaunchKernelGGL((scan_pipe_kernel<DK, J, DB, MD, NH>), dim3((unsigned)blocks),
                            dim3(64 * (C::NW + 1 + NH)), 0, stream, a, na);
     }
     return hipGetLastError();
 }
 
-template <int DK, bool NT>
+template <int DK, int MD>
 hipError_t launch_dk(const LayerArgs &a, const NewtonArgs &na, hipStream_t stream) {
     // At most 64 columns (one wave of sequential lanes).  J = 4 takes 32
     // columns (DB = 8): twice the blocks, the sequential wave on a SIMD of its
     // own, and two blocks' LDS fit one compute unit.
     switch (a.J) {
         case 1:
-            if (a.Dv >= 64) return launch_cfg<DK, 1, 64, NT>(a, na, stream);
-            if (a.Dv == 32) return launch_cfg<DK, 1, 32, NT>(a, na, stream);
-            return launch_cfg<DK, 1, 16, NT>(a, na, stream);
+            // (the temporal form's extra staging does not fit 64 columns of Dk = 128)
+            if constexpr (MD != 2 || DK < 128)
+                if (a.Dv >= 64) return launch_cfg<DK, 1, 64, MD>(a, na, stream);
+            if (a.Dv >= 32) return launch_cfg<DK, 1, 32, MD>(a, na, stream);
+            return launch_cfg<DK, 1, 16, MD>(a, na, stream);
         case 2:
-            if (a.Dv >= 32) return launch_cfg<DK, 2, 32, NT>(a, na, stream);
-            return launch_cfg<DK, 2, 16, NT>(a, na, stream);
-        case 3: return launch_cfg<DK, 3, 16, NT>(a, na, stream);
-        case 4: return launch_cfg<DK, 4, 8, NT>(a, na, stream);
-        case 8: return launch_cfg<DK, 8, 8, NT>(a, na, stream);
+            if (a.Dv >= 32) return launch_cfg<DK, 2, 32, MD>(a, na, stream);
+            return launch_cfg<DK, 2, 16, MD>(a, na, stream);
+        case 3: return launch_cfg<DK, 3, 16, MD>(a, na, stream);
+        case 4: return launch_cfg<DK, 4, 8, MD>(a, na, stream);
+        case 8: return launch_cfg<DK, 8, 8, MD>(a, na, stream);
         default: return hipErrorInvalidValue;
     }
 }
 
-template <bool NT>
+template <int MD>
 hipError_t launch_mode(const LayerArgs &a, const NewtonArgs &na, hipStream_t stream) {
     if (!a.in_bf16 || a.T <= 0) return hipErrorInvalidValue;
     switch (a.Dk) {
-        case 16: return launch_dk<16, NT>(a, na, stream);
-        case 32: return launch_dk<32, NT>(a, na, stream);
-        case 64: return launch_dk<64, NT>(a, na, stream);
-        case 128: return launch_dk<128, NT>(a, na, stream);
+        case 16: return launch_dk<16, MD>(a, na, stream);
+        case 32: return launch_dk<32, MD>(a, na, stream);
+        case 64: return launch_dk<64, MD>(a, na, stream);
+        case 128: return launch_dk<128, MD>(a, na, stream);
         default: return hipErrorInvalidValue;
     }
 }
@@ -1087,7 +1222,8 @@ hipError_t launch_mode(const LayerArgs &a, const NewtonArgs &na, hipStream_t str
 }  // namespace
 
 hipError_t launch_scan_pipe(const LayerArgs &a, hipStream_t stream) {
-    return launch_mode<false>(a, NewtonArgs{}, stream);
+    if (a.gk) return launch_mode<2>(a, NewtonArgs{}, stream);
+    return launch_mode<0>(a, NewtonArgs{}, stream);
 }
 
 size_t newton_workspace_bytes(int B, int H, int T, int Dv, int J) {
@@ -1102,7 +1238,8 @@ hipError_t launch_newton(const LayerArgs &a, const NewtonArgs &na, hipStream_t s
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
-    return launch_mode<true>(a, na, stream);
+    if (a.gk) return hipErrorInvalidValue;   // App. D linearises the plain recurrence
+    return launch_mode<1>(a, na, stream);
 }
 
 }  // namespace swila

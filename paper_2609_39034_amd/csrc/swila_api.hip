@@ -322,8 +322,9 @@ int swila_forward_temporal(const swila_shape *shape, const swila_opts *opts, con
                                           1.0f / shape->J, st),
                        "prior state copy");
     }
-    if (opts->algo == SWILA_ALGO_CHUNK_EXACT)
-        return fail(SWILA_EUNSUPPORTED, "the temporal form runs on SWILA_ALGO_RECURRENT");
+    const bool chunk = opts->algo == SWILA_ALGO_CHUNK_EXACT ||
+                       (opts->algo == SWILA_ALGO_AUTO && opts->in_dtype == SWILA_BF16);
+    if (chunk) return map_hip(swila::launch_scan_pipe(a, st), "chunk scan launch");
     return map_hip(swila::launch_scan_direct(a, st), "scan launch");
 }
 

@@ -200,9 +200,9 @@ def test_temporal_argument_checks(lib):
     newton = sw.Opts(sw.BF16, sw.BF16, sw.ALGO_NEWTON, 0, 0, 0.0, 0)
     rc, msg = _fwd_t(lib, sw.Temporal(gk, gq, None, None), opts=newton)
     assert rc == sw.EUNSUPPORTED and "NEWTON" in msg
-    chunk = sw.Opts(sw.BF16, sw.BF16, sw.ALGO_CHUNK_EXACT, 0, 0, 0.0, 0)
-    rc, msg = _fwd_t(lib, sw.Temporal(gk, gq, None, None), opts=chunk)
-    assert rc == sw.EUNSUPPORTED
+    chunk32 = sw.Opts(sw.F32, sw.F32, sw.ALGO_CHUNK_EXACT, 0, 0, 0.0, 0)
+    rc, msg = _fwd_t(lib, sw.Temporal(gk, gq, None, None), opts=chunk32)
+    assert rc == sw.EUNSUPPORTED and "bf16" in msg
 
 
 def test_temporal_decode_requires_one_token(lib):
