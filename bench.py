@@ -181,6 +181,61 @@ def bench_decode(sw, torch, workloads, steps_total, warmup):
     }
 
 
+def temporal_alg_bytes(B, H, T, Dk, Dv, J, in_bytes=2, out_bytes=2, state_in=False,
+                       state_out=True, prior_in=False, prior_out=True):
+    """The forward's bytes plus the two gate-logit tensors (one value per token,
+    head and output dim each) and the fp32 prior state [B,H,2,J,Dv]."""
+    prior = 4 * 2 * J * Dv * B * H
+    return (forward_alg_bytes(B, H, T, Dk, Dv, J, in_bytes, out_bytes, state_in, state_out)
+            + 2 * in_bytes * Dv * B * H * T + prior * (int(prior_in) + int(prior_out)))
+
+
+def bench_temporal(sw, torch, workloads, dev, cfg, seed, steps, warmup, o, s_out, algo, tdt):
+    """Temporal SwiLA (App. B.3) on the same batch: N(0,1) gate logits, uniform
+    initial priors, final prior state kept."""
+    B, H, T, Dk, Dv, J = (cfg[x] for x in ("B", "H", "T", "Dk", "Dv", "J"))
+    tmp = workloads.temporal_inputs(B, H, T, Dv, J, dtype=cfg["dtype"], seed=seed)
+    gk = torch.from_numpy(tmp["gk"]).to("cuda", tdt)
+    gq = torch.from_numpy(tmp["gq"]).to("cuda", tdt)
+    p_out = torch.empty((B, H, 2, J, Dv), device="cuda", dtype=torch.float32)
+    names = ("q", "k", "v", "lb", "lk", "lq")
+    args = [dev[n] for n in names]
+
+    def step():
+        sw.forward_temporal(*args, gk, gq, dev["state"], None, o=o, state_out=s_out,
+                            prior_out=p_out, algo=algo)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(steps)]
+    t0 = time.perf_counter()
+    for i in range(steps):
+        ev[i][0].record(stream)
+        step()
+        ev[i][1].record(stream)
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) / steps
+    kern = sum(a.elapsed_time(b) for a, b in ev) / steps / 1e3
+    bf16 = cfg["dtype"] == "bf16"
+    eb = 2 if bf16 else 4
+    chunk = algo == "chunk" or (algo == "auto" and bf16)
+    nbytes = temporal_alg_bytes(B, H, T, Dk, Dv, J, eb, eb, dev["state"] is not None, True)
+    return {
+        "workload": "Temporal SwiLA (App. B.3), same batch, N(0,1) gate logits, uniform "
+                    "initial priors, final prior state kept",
+        "tokens_per_s": B * T / wall, "ms_per_step": wall * 1e3,
+        "algo": "chunk_exact" if chunk else "recurrent",
+        "roofline": {"bound": "hbm", "achieved": nbytes / kern / 1e9, "peak": PEAK_HBM / 1e9,
+                     "unit": "GB/s", "frac": nbytes / kern / PEAK_HBM, "traffic": None,
+                     "kernel": ("scan_pipe_kernel (temporal mode)" if chunk
+                                else "scan_direct_kernel (temporal)"),
+                     "kernel_ms": kern * 1e3, "alg_bytes_per_launch": nbytes},
+    }
+
+
 def cpu_baseline(workloads, inp, cfg):
     import oracle
     n = host_cores()
@@ -205,6 +260,7 @@ def main():
     ap.add_argument("--decode-steps", type=int, default=512)
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-newton", action="store_true")
+    ap.add_argument("--no-temporal", action="store_true")
     ap.add_argument("--newton-tol", type=float, default=1e-3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -268,6 +324,9 @@ def main():
     out.update({
         "head_tokens_per_s": B * H * T / wall,
     })
+    if not args.no_temporal:
+        out["temporal"] = bench_temporal(sw, torch, workloads, dev, cfg, 1000 + args.config,
+                                         args.steps, args.warmup, o, s_out, args.algo, tdt)
     if not args.no_newton and bf16:
         out["newton"] = bench_newton(sw, torch, dev, cfg, args.steps, args.warmup, o, s_out,
                                      args.newton_tol)

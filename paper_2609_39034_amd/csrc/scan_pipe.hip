@@ -751,23 +751,31 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
         }
     };
     // Temporal: the running query prior rhobar_t = (1 - g^q_t) rhobar_{t-1} +
-    // g^q_t pi^q_t (App. B.3) over chunk m, one bookkeeping thread per column,
-    // carried in rho from chunk to chunk; written in place of pi^q (scaled like
-    // the plain prior).  Padded tokens leave it unchanged.
+    // g^q_t pi^q_t (App. B.3) over chunk m, one bookkeeping thread per column
+    // (the last N of them, which have the least other work), carried in rho from
+    // chunk to chunk; written in place of pi^q (scaled like the plain prior).
+    // Padded tokens leave it unchanged.  All loads first, then the 16 dependent
+    // steps in registers, then the stores.
+    const int qc = bt - (NBT - N);   // this thread's column in the scan, if >= 0
     float rho = 1.f / J;
     if constexpr (TP) {
-        if (book && bt < N && a.prior_in)
-            rho = a.prior_in[(((size_t)b * H + h) * 2 * J + J + bt / DB) * Dv + d0 + bt % DB];
+        if (book && qc >= 0 && a.prior_in)
+            rho = a.prior_in[(((size_t)b * H + h) * 2 * J + J + qc / DB) * Dv + d0 + qc % DB];
     }
     auto scan_query_prior = [&](int m) {
-        if (bt < N) {
-            const int slot = m % 3, dl = bt % DB;
+        if (qc >= 0) {
+            const int slot = m % 3, dl = qc % DB;
+            float pi[kC], g[kC];
+#pragma unroll
+            for (int t = 0; t < kC; ++t) pi[t] = sm.pq[slot][t][qc], g[t] = sm.gqs[slot][t][dl];
+            const int nt = T - m * kC;   // tokens of this chunk in range
 #pragma unroll
             for (int t = 0; t < kC; ++t) {
-                const float pi = sm.pq[slot][t][bt];
-                if (m * kC + t < T) rho = fmaf(sm.gqs[slot][t][dl], pi - rho, rho);
-                sm.pq[slot][t][bt] = kInvWS * rho;
+                if (t < nt) rho = fmaf(g[t], pi[t] - rho, rho);
+                pi[t] = kInvWS * rho;
             }
+#pragma unroll
+            for (int t = 0; t < kC; ++t) sm.pq[slot][t][qc] = pi[t];
         }
     };
     // o of chunk m: sum over j of pi^q * retrieval
@@ -1174,7 +1182,8 @@ hipError_t launch_cfg(const LayerArgs &a, const NewtonArgs &na, hipStream_t stre
     // Enough blocks to put two on every compute unit (LDS permitting): their
     // waves hide each other's latencies, so the tile waves keep the
     // bookkeeping.  Otherwise helper waves take it over.
-    constexpr int NH = MD == 1 ? 0 : (C::NW < 3 ? C::NW : 3);
+    // (the temporal form has more per-chunk bookkeeping: always three helpers)
+    constexpr int NH = MD == 1 ? 0 : MD == 2 ? 3 : (C::NW < 3 ? C::NW : 3);
     if (NH == 0 || (blocks >= 512 && lds <= 80 * 1024)) {
         hipLaunchKernelGGL((scan_pipe_kernel<DK, J, DB, MD, 0>), dim3((unsigned)blocks),
                            dim3(64 * (C::NW + 1)), 0, stream, a, na);
