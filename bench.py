@@ -51,16 +51,26 @@ def measured_traffic(source):
 
 
 def kernel_source_digest(source):
-    """sha256 over ``source`` and the local headers and fragments it includes
-    (one level of ``#include "..."``), in order."""
+    """sha256 over ``source`` and, recursively and once each, the local headers
+    and fragments it includes (``#include "..."``), in include order."""
     import hashlib
     csrc = os.path.join(ROOT, "paper_2609_39034_amd", "csrc")
-    text = open(os.path.join(csrc, source), "rb").read()
-    h = hashlib.sha256(text)
-    for name in re.findall(rb'^\s*#include\s+"([^"]+)"', text, re.M):
-        path = os.path.join(csrc, name.decode())
-        if os.path.exists(path):
-            h.update(open(path, "rb").read())
+    h = hashlib.sha256()
+    seen = set()
+
+    def add(name):
+        path = os.path.join(csrc, name)
+        if name in seen or not os.path.exists(path):
+            return
+        seen.add(name)
+        text = open(path, "rb").read()
+        h.update(text)
+        for inc in re.findall(rb'^\s*#include\s+"([^"]+)"', text, re.M):
+            add(inc.decode())
+
+    add(source)
+    if source not in seen:
+        raise OSError("no such kernel source: %s" % source)
     return h.hexdigest()
 
 

@@ -15,7 +15,8 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libswila.so")
-SOURCES = ["swila_api.hip", "scan_direct.hip", "scan_pipe.hip", "decode.hip"]
+SOURCES = ["swila_api.hip", "scan_direct.hip", "scan_pipe.hip", "scan_pipe_newton.hip",
+           "scan_pipe_temporal.hip", "decode.hip"]
 ARCH = "gfx950"
 
 # Packed fp32 VALU instructions are turned off for every kernel: the compiler
@@ -35,7 +36,8 @@ def hipcc():
 # Per-file additions.  The chunk scan never relies on NaN semantics (inputs
 # are finite; idle lanes' values are never stored), which lets the compiler
 # fold the cross-lane DPP moves into v_max/v_add.
-EXTRA = {"scan_pipe.hip": ["-fno-honor-nans"]}
+EXTRA = {f: ["-fno-honor-nans"] for f in ("scan_pipe.hip", "scan_pipe_newton.hip",
+                                          "scan_pipe_temporal.hip")}
 
 
 def _compile(src, verbose):

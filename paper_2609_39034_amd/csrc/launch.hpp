@@ -38,8 +38,10 @@ struct NewtonArgs {
 hipError_t launch_scan_direct(const LayerArgs &a, hipStream_t stream);
 
 // Exact chunk scan on the matrix cores, pipelined (one sequential wave plus
-// matrix-core waves); bf16 inputs, T > 0.
+// matrix-core waves); bf16 inputs, T > 0.  With gate logits (a.gk) it runs the
+// temporal form.
 hipError_t launch_scan_pipe(const LayerArgs &a, hipStream_t stream);
+hipError_t launch_scan_pipe_temporal(const LayerArgs &a, hipStream_t stream);
 
 // Chunkwise quasi-Newton evaluation (App. D) on the same pipelined kernel;
 // bf16 inputs, T > 0, resp must be nullptr.  na.pred holds
