@@ -52,8 +52,9 @@ def load_library(path):
     dp = ctypes.POINTER(ctypes.c_double)
     lib.swila_oracle_forward.argtypes = [ctypes.c_int] * 6 + [dp] * 11 + [ctypes.c_int]
     lib.swila_oracle_forward.restype = ctypes.c_int
-    lib.swila_oracle_forward_temporal.argtypes = [ctypes.c_int] * 6 + [dp] * 15 + [ctypes.c_int]
-    lib.swila_oracle_forward_temporal.restype = ctypes.c_int
+    lib.swila_oracle_forward_ext.argtypes = ([ctypes.c_int] * 6 + [dp] * 9 + [ctypes.c_int]
+                                             + [dp] * 7 + [ctypes.c_int])
+    lib.swila_oracle_forward_ext.restype = ctypes.c_int
     return lib
 
 
@@ -76,9 +77,9 @@ def _ptr(x):
 
 
 def forward(q, k, v, beta_logit, prior_k_logit, prior_q_logit, state_in=None, *,
-            gate_k_logit=None, gate_q_logit=None, prior_in=None,
-            nthreads: int = 0, want_resp: bool = False, want_delta: bool = False,
-            lib=None):
+            gate_k_logit=None, gate_q_logit=None, prior_in=None, decay_logit=None,
+            post_decay: bool = False, nthreads: int = 0, want_resp: bool = False,
+            want_delta: bool = False, lib=None):
     """Run the recurrence over a whole sequence.
 
     Shapes: q, k [B,T,H,Dk]; v [B,T,H,Dv]; the three logit tensors
@@ -94,6 +95,11 @@ def forward(q, k, v, beta_logit, prior_k_logit, prior_q_logit, state_in=None, *,
     the new softmax priors; ``prior_in`` is the carried prior state
     [B,H,2,J,Dv] (part 0: r_{t-1}, part 1: rhobar_{t-1}) or None (uniform 1/J),
     and the result then also holds ``prior``, the final prior state.
+
+    Gated SwiLA (App. B.4): with ``decay_logit`` [B,T,H,J,Dk] the state decays by
+    a = sigmoid(decay_logit), one gate per key dimension and component, before
+    the prediction (eq. pre-decay), or after it with ``post_decay`` (eq.
+    post-decay).  It combines with the temporal priors.
     """
     q, k, v = _f64(q), _f64(k), _f64(v)
     lb, lk, lq = _f64(beta_logit), _f64(prior_k_logit), _f64(prior_q_logit)
@@ -111,17 +117,24 @@ def forward(q, k, v, beta_logit, prior_k_logit, prior_q_logit, state_in=None, *,
     resp = np.zeros((B, T, H, J, Dv)) if want_resp else None
     delta = np.zeros((B, T, H, J, Dv)) if want_delta else None
     temporal = gate_k_logit is not None or gate_q_logit is not None
-    if temporal:
+    dec = _f64(decay_logit)
+    if dec is not None:
+        assert dec.shape == (B, T, H, J, Dk)
+    if temporal or dec is not None:
         gk, gq, p_in = _f64(gate_k_logit), _f64(gate_q_logit), _f64(prior_in)
-        assert gk is not None and gq is not None, "both gate logits are needed"
-        assert gk.shape == (B, T, H, Dv) and gq.shape == (B, T, H, Dv)
-        if p_in is not None:
-            assert p_in.shape == (B, H, 2, J, Dv)
-        p_out = np.zeros((B, H, 2, J, Dv))
-        rc = (lib or _load()).swila_oracle_forward_temporal(
+        p_out = None
+        if temporal:
+            assert gk is not None and gq is not None, "both gate logits are needed"
+            assert gk.shape == (B, T, H, Dv) and gq.shape == (B, T, H, Dv)
+            if p_in is not None:
+                assert p_in.shape == (B, H, 2, J, Dv)
+            p_out = np.zeros((B, H, 2, J, Dv))
+        else:
+            assert prior_in is None, "prior_in needs the gate logits"
+        rc = (lib or _load()).swila_oracle_forward_ext(
             B, H, T, Dk, Dv, J, _ptr(q), _ptr(k), _ptr(v), _ptr(lb), _ptr(lk), _ptr(lq),
-            _ptr(gk), _ptr(gq), _ptr(s_in), _ptr(p_in), _ptr(s_out), _ptr(p_out), _ptr(o),
-            _ptr(resp), _ptr(delta), int(nthreads))
+            _ptr(gk), _ptr(gq), _ptr(dec), int(bool(post_decay)), _ptr(s_in), _ptr(p_in),
+            _ptr(s_out), _ptr(p_out), _ptr(o), _ptr(resp), _ptr(delta), int(nthreads))
     else:
         assert prior_in is None, "prior_in needs the gate logits"
         rc = (lib or _load()).swila_oracle_forward(
@@ -140,16 +153,19 @@ def forward(q, k, v, beta_logit, prior_k_logit, prior_q_logit, state_in=None, *,
 
 
 def decode_step(q, k, v, beta_logit, prior_k_logit, prior_q_logit, state_in, *,
-                gate_k_logit=None, gate_q_logit=None, prior_in=None, nthreads: int = 0):
+                gate_k_logit=None, gate_q_logit=None, prior_in=None, decay_logit=None,
+                nthreads: int = 0):
     """One token per sequence: q, k [B,H,Dk]; v [B,H,Dv]; logits [B,H,J,Dv];
     state_in [B,H,J,Dk,Dv].  Returns (o [B,H,Dv], state [B,H,J,Dk,Dv]), plus
-    the prior state [B,H,2,J,Dv] for the temporal form (gate logits [B,H,Dv]).
-    This is ``forward`` with T = 1."""
+    the prior state [B,H,2,J,Dv] for the temporal form (gate logits [B,H,Dv]);
+    decay_logit [B,H,J,Dk] for the gated form.  This is ``forward`` with T = 1."""
     temporal = gate_k_logit is not None
     gates = {}
     if temporal:
         gates = dict(gate_k_logit=np.asarray(gate_k_logit)[:, None],
                      gate_q_logit=np.asarray(gate_q_logit)[:, None], prior_in=prior_in)
+    if decay_logit is not None:
+        gates["decay_logit"] = np.asarray(decay_logit)[:, None]
     r = forward(*(np.asarray(x)[:, None] for x in
                   (q, k, v, beta_logit, prior_k_logit, prior_q_logit)),
                 state_in, nthreads=nthreads, **gates)

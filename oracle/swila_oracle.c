@@ -45,6 +45,19 @@
  * pair (r_{t-1}, rhobar_{t-1}) is the "prior state" [B, H, 2, J, Dv]: part 0
  * is r, part 1 is rhobar.  Without an input prior state both start uniform,
  * 1/J (the paper gives no initial value).  Gate logits are [B, T, H, Dv].
+ *
+ * Gated SwiLA (Sec. 3.4, App. B.4), when decay logits are given: a decay
+ * a_{tj} = sigmoid(decay_logit_{tj}) in [0,1]^{Dk}, one gate per key dimension
+ * and component, tied across the output dims (the form of the paper's
+ * language-model runs).  Pre-decay (eq. pre-decay, the form the paper uses):
+ *
+ *   wbar_{jd}   = a_{tj} (.) w_{t-1,jd}                 (elementwise over i)
+ *   delta_{tjd} = v_{td} - wbar_{jd} . k_t,  r from these errors
+ *   w_{tjd}     = wbar_{jd} + beta r delta k_t
+ *
+ * Post-decay (eq. post-decay; kept here for the J = 1 equivalence the paper
+ * states): delta and r from w_{t-1}, then w_{tjd} = a_{tj} (.) w_{t-1,jd} +
+ * beta r delta k_t.  Decay logits are [B, T, H, J, Dk].
  */
 #include <math.h>
 #include <pthread.h>
@@ -59,6 +72,8 @@ typedef struct {
     double *state_out, *o, *resp, *delta_out;
     const double *gk, *gq, *prior_in;   /* temporal form: gate logits, prior state */
     double *prior_out;
+    const double *decay;                 /* gated form: decay logits */
+    int post_decay;
     int next_head;              /* work counter, guarded by mu */
     int status;                 /* first error seen, guarded by mu */
     pthread_mutex_t mu;
@@ -118,7 +133,15 @@ static int run_head(job_t *a, int b, int h)
                     prior[j] = (1.0 - g) * rprev[(size_t)j * Dv + d] + g * prior[j];
             }
 
-            /* prediction errors with the previous state */
+            /* gated, pre-decay: the state decays before the prediction */
+            if (a->decay && !a->post_decay)
+                for (int j = 0; j < J; ++j) {
+                    double *w = W + ((size_t)j * Dv + d) * Dk;
+                    const double *dl = a->decay + (row * J + j) * (size_t)Dk;
+                    for (int i = 0; i < Dk; ++i) w[i] *= 1.0 / (1.0 + exp(-dl[i]));
+                }
+
+            /* prediction errors with the previous (pre-decay: decayed) state */
             for (int j = 0; j < J; ++j) {
                 const double *w = W + ((size_t)j * Dv + d) * Dk;
                 double pred = 0.0;
@@ -144,6 +167,10 @@ static int run_head(job_t *a, int b, int h)
                 const double r = num[j] / Z;
                 const double beta = 1.0 / (1.0 + exp(-lbt[(size_t)j * Dv + d]));
                 double *w = W + ((size_t)j * Dv + d) * Dk;
+                if (a->decay && a->post_decay) {   /* gated, post-decay */
+                    const double *dl = a->decay + (row * J + j) * (size_t)Dk;
+                    for (int i = 0; i < Dk; ++i) w[i] *= 1.0 / (1.0 + exp(-dl[i]));
+                }
                 for (int i = 0; i < Dk; ++i) w[i] += beta * r * delta[j] * kt[i];
                 if (a->resp) a->resp[(row * J + j) * Dv + d] = r;
                 if (temporal) rprev[(size_t)j * Dv + d] = r;
@@ -212,14 +239,14 @@ static void *worker(void *p)
 }
 
 static int run_all(job_t *ap, int nthreads);
-int swila_oracle_forward_temporal(int B, int H, int T, int Dk, int Dv, int J,
-                                  const double *q, const double *k, const double *v,
-                                  const double *beta_logit, const double *prior_k_logit,
-                                  const double *prior_q_logit, const double *gate_k_logit,
-                                  const double *gate_q_logit, const double *state_in,
-                                  const double *prior_in, double *state_out,
-                                  double *prior_out, double *o, double *resp_out,
-                                  double *delta_out, int nthreads);
+int swila_oracle_forward_ext(int B, int H, int T, int Dk, int Dv, int J,
+                             const double *q, const double *k, const double *v,
+                             const double *beta_logit, const double *prior_k_logit,
+                             const double *prior_q_logit, const double *gate_k_logit,
+                             const double *gate_q_logit, const double *decay_logit,
+                             int post_decay, const double *state_in, const double *prior_in,
+                             double *state_out, double *prior_out, double *o, double *resp_out,
+                             double *delta_out, int nthreads);
 
 /*
  * Forward over T tokens for every (b, h).  state_in may be NULL (zeros);
@@ -235,26 +262,27 @@ int swila_oracle_forward(int B, int H, int T, int Dk, int Dv, int J,
                          double *state_out, double *o, double *resp_out,
                          double *delta_out, int nthreads)
 {
-    return swila_oracle_forward_temporal(B, H, T, Dk, Dv, J, q, k, v, beta_logit,
-                                         prior_k_logit, prior_q_logit, NULL, NULL, state_in,
-                                         NULL, state_out, NULL, o, resp_out, delta_out,
-                                         nthreads);
+    return swila_oracle_forward_ext(B, H, T, Dk, Dv, J, q, k, v, beta_logit, prior_k_logit,
+                                    prior_q_logit, NULL, NULL, NULL, 0, state_in, NULL,
+                                    state_out, NULL, o, resp_out, delta_out, nthreads);
 }
 
 /*
  * The same with the temporal priors of App. B.3 when gate_k_logit and
- * gate_q_logit are given ([B, T, H, Dv]; both or neither).  prior_in is the
+ * gate_q_logit are given ([B, T, H, Dv]; both or neither), and with the
+ * gated decay of App. B.4 when decay_logit is given ([B, T, H, J, Dk];
+ * post_decay selects eq. post-decay instead of eq. pre-decay).  prior_in is the
  * prior state [B, H, 2, J, Dv] or NULL (uniform); prior_out receives the
- * final one, or is NULL.  Without gate logits this is the plain forward.
+ * final one, or is NULL.  Without either this is the plain forward.
  */
-int swila_oracle_forward_temporal(int B, int H, int T, int Dk, int Dv, int J,
-                                  const double *q, const double *k, const double *v,
-                                  const double *beta_logit, const double *prior_k_logit,
-                                  const double *prior_q_logit, const double *gate_k_logit,
-                                  const double *gate_q_logit, const double *state_in,
-                                  const double *prior_in, double *state_out,
-                                  double *prior_out, double *o, double *resp_out,
-                                  double *delta_out, int nthreads)
+int swila_oracle_forward_ext(int B, int H, int T, int Dk, int Dv, int J,
+                             const double *q, const double *k, const double *v,
+                             const double *beta_logit, const double *prior_k_logit,
+                             const double *prior_q_logit, const double *gate_k_logit,
+                             const double *gate_q_logit, const double *decay_logit,
+                             int post_decay, const double *state_in, const double *prior_in,
+                             double *state_out, double *prior_out, double *o, double *resp_out,
+                             double *delta_out, int nthreads)
 {
     if (B < 0 || H < 0 || T < 0 || Dk <= 0 || Dv <= 0 || J <= 0) return -3;
     if ((gate_k_logit == NULL) != (gate_q_logit == NULL)) return -3;
@@ -267,6 +295,7 @@ int swila_oracle_forward_temporal(int B, int H, int T, int Dk, int Dv, int J,
     a.resp = resp_out; a.delta_out = delta_out;
     a.gk = gate_k_logit; a.gq = gate_q_logit;
     a.prior_in = prior_in; a.prior_out = prior_out;
+    a.decay = decay_logit; a.post_decay = post_decay;
     return run_all(&a, nthreads);
 }
 

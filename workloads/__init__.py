@@ -119,6 +119,15 @@ def temporal_inputs(B, H, T, Dv, J, *, dtype="bf16", seed=0, gate_scale=1.0,
     return out
 
 
+def gated_inputs(B, H, T, Dk, J, *, dtype="bf16", seed=0, mean=2.0, scale=1.0):
+    """Extra input of Gated SwiLA: decay logits ``decay`` [B, T, H, J, Dk],
+    i.i.d. N(mean, scale^2) (sigmoid(2) = 0.88 keeps most of the state per
+    token), rounded like the other inputs.  Drawn from their own generator."""
+    rng = np.random.Generator(np.random.PCG64(seed + 104729))
+    d = rng.standard_normal((B, T, H, J, Dk), dtype=np.float32) * np.float32(scale) + np.float32(mean)
+    return {"decay": _finish(d, dtype)}
+
+
 def _project_tokens(rng, ids, vocab, width, H, Dk, Dv, J, dtype, chunk_tokens=4096):
     """q, k, v and the three logit tensors as linear projections of random token
     embeddings E ~ N(0,1) [vocab, width] with weights N(0, 1/width), so every
