@@ -211,6 +211,46 @@ int swila_decode_step_temporal(const swila_shape *shape, const swila_opts *opts,
                                const float *state_in, float *state_out, void *o,
                                void *stream);
 
+/*
+ * Gated SwiLA (Sec. 3.4, App. B.4), in the form of eq. pre-decay with one
+ * gate per key dimension (tied across output dims, as in the paper's language
+ * models): before the prediction of token t the state decays,
+ *
+ *   a_{tj}      = sigmoid(decay_logit_{tj})          in (0, 1)^Dk
+ *   wbar_{jd}   = a_{tj} (.) w_{t-1,jd}              (elementwise over key index i)
+ *   delta_{tjd} = v_{td} - wbar_{jd} . k_t,  r from these errors (eq. responsibility)
+ *   w_{tjd}     = wbar_{jd} + beta r delta k_t
+ *
+ *   decay_logit: [B,T,H,J,Dk] (decode: [B,H,J,Dk]), in_dtype, 16-byte aligned;
+ *                required when T > 0; must not overlap any output.
+ */
+typedef struct swila_gated {
+    const void *decay_logit;
+} swila_gated;
+
+/*
+ * swila_forward with the gated decay above; temporal may be NULL (plain
+ * priors) or the temporal priors of swila_forward_temporal (Gated Temporal
+ * SwiLA).  Runs on the token-by-token scan (SWILA_ALGO_AUTO or
+ * SWILA_ALGO_RECURRENT, either input dtype); SWILA_ALGO_CHUNK_EXACT and
+ * SWILA_ALGO_NEWTON return SWILA_EUNSUPPORTED.  T == 0 copies the states.
+ */
+int swila_forward_gated(const swila_shape *shape, const swila_opts *opts,
+                        const void *q, const void *k, const void *v,
+                        const void *beta_logit, const void *prior_k_logit,
+                        const void *prior_q_logit, const swila_gated *gated,
+                        const swila_temporal *temporal, const float *state_in,
+                        float *state_out, void *o, float *resp_out, void *stream);
+
+/* swila_decode_step with the gated decay (decay logits [B,H,J,Dk]); temporal
+ * may be NULL.  Its result equals swila_forward_gated with T = 1. */
+int swila_decode_step_gated(const swila_shape *shape, const swila_opts *opts,
+                            const void *q, const void *k, const void *v,
+                            const void *beta_logit, const void *prior_k_logit,
+                            const void *prior_q_logit, const swila_gated *gated,
+                            const swila_temporal *temporal, const float *state_in,
+                            float *state_out, void *o, void *stream);
+
 /* Text of this thread's last error ("" if none). */
 const char *swila_last_error(void);
 

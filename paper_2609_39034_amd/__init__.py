@@ -12,6 +12,8 @@ Entry points (names as in the C ABI):
   ``decode_step``        one token per sequence -> swila_decode_step
   ``forward_temporal``, ``decode_step_temporal``  Temporal SwiLA (App. B.3)
                                                 -> swila_forward_temporal, ...
+  ``forward_gated``, ``decode_step_gated``      Gated SwiLA (App. B.4)
+                                                -> swila_forward_gated, ...
   ``state_init``         initial state          -> swila_state_init
   ``state_bytes``, ``forward_workspace_bytes``, ``version``
 """
@@ -20,7 +22,8 @@ from __future__ import annotations
 import ctypes
 import os
 
-__all__ = ["forward", "decode_step", "forward_temporal", "decode_step_temporal", "state_init", "state_bytes", "forward_workspace_bytes",
+__all__ = ["forward", "decode_step", "forward_temporal", "decode_step_temporal",
+           "forward_gated", "decode_step_gated", "state_init", "state_bytes", "forward_workspace_bytes",
            "version", "library_path", "SwilaError", "F32", "BF16", "ALGO_AUTO",
            "ALGO_RECURRENT", "ALGO_CHUNK_EXACT", "ALGO_NEWTON", "FLAG_NEWTON_NO_CLAMP"]
 
@@ -56,6 +59,10 @@ class Opts(ctypes.Structure):
 class Temporal(ctypes.Structure):
     _fields_ = [("gate_k_logit", ctypes.c_void_p), ("gate_q_logit", ctypes.c_void_p),
                 ("prior_in", ctypes.c_void_p), ("prior_out", ctypes.c_void_p)]
+
+
+class Gated(ctypes.Structure):
+    _fields_ = [("decay_logit", ctypes.c_void_p)]
 
 
 _lib = None
@@ -94,6 +101,11 @@ def load_library():
     lib.swila_forward_temporal.argtypes = [sp, op] + [vp] * 6 + [tp, vp, vp, vp, vp, vp]
     lib.swila_decode_step_temporal.restype = ctypes.c_int
     lib.swila_decode_step_temporal.argtypes = [sp, op] + [vp] * 6 + [tp, vp, vp, vp, vp]
+    gp = ctypes.POINTER(Gated)
+    lib.swila_forward_gated.restype = ctypes.c_int
+    lib.swila_forward_gated.argtypes = [sp, op] + [vp] * 6 + [gp, tp, vp, vp, vp, vp, vp]
+    lib.swila_decode_step_gated.restype = ctypes.c_int
+    lib.swila_decode_step_gated.argtypes = [sp, op] + [vp] * 6 + [gp, tp, vp, vp, vp, vp]
     _lib = lib
     return lib
 
@@ -424,3 +436,120 @@ def decode_step_temporal(q, k, v, beta_logit, prior_k_logit, prior_q_logit, gate
         *[_ptr(t) for t in ins], ctypes.byref(tp), _ptr(state_in), _ptr(state_out), _ptr(o),
         _stream_handle(stream)))
     return o, state_out, p_out
+
+
+def _check_inputs(q, k, v, beta_logit, prior_k_logit, prior_q_logit, decode):
+    names = ("q", "k", "v", "beta_logit", "prior_k_logit", "prior_q_logit")
+    ins = [_dev_tensor(t, n) for t, n in zip((q, k, v, beta_logit, prior_k_logit, prior_q_logit),
+                                             names)]
+    code = _dtype_code(q)
+    for t, n in zip(ins, names):
+        if _dtype_code(t) != code:
+            raise TypeError("%s has dtype %s but q has %s" % (n, t.dtype, q.dtype))
+    B, H, T, Dk, Dv, J = _layer_shapes(q, v, beta_logit, decode=decode)
+    if decode:
+        expect = {"q": (B, H, Dk), "k": (B, H, Dk), "v": (B, H, Dv), "beta_logit": (B, H, J, Dv),
+                  "prior_k_logit": (B, H, J, Dv), "prior_q_logit": (B, H, J, Dv)}
+    else:
+        expect = {"q": (B, T, H, Dk), "k": (B, T, H, Dk), "v": (B, T, H, Dv),
+                  "beta_logit": (B, T, H, J, Dv), "prior_k_logit": (B, T, H, J, Dv),
+                  "prior_q_logit": (B, T, H, J, Dv)}
+    for t, n in zip(ins, names):
+        if tuple(t.shape) != expect[n]:
+            raise ValueError("%s has shape %s, expected %s" % (n, tuple(t.shape), expect[n]))
+    return ins, code, (B, H, T, Dk, Dv, J)
+
+
+def _gated_arg(decay_logit, code, shape):
+    _dev_tensor(decay_logit, "decay_logit")
+    if _dtype_code(decay_logit) != code:
+        raise TypeError("decay_logit must have the dtype of q")
+    if tuple(decay_logit.shape) != shape:
+        raise ValueError("decay_logit has shape %s, expected %s"
+                         % (tuple(decay_logit.shape), shape))
+    return Gated(decay_logit.data_ptr())
+
+
+def forward_gated(q, k, v, beta_logit, prior_k_logit, prior_q_logit, decay_logit,
+                  state_in=None, *, gate_k_logit=None, gate_q_logit=None, prior_in=None,
+                  prior_out=True, state_out=True, o=None, out_dtype=None, resp=False,
+                  algo="auto", stream=None):
+    """Gated SwiLA forward (swila_forward_gated; Sec. 3.4, App. B.4, eq. pre-decay).
+
+    The arguments of ``forward`` plus decay_logit [B,T,H,J,Dk] (the dtype of q;
+    a = sigmoid, one gate per key dimension and component).  With gate_k_logit
+    and gate_q_logit the priors are the temporal ones of ``forward_temporal``
+    (Gated Temporal SwiLA), with prior_in / prior_out as there.
+    Returns (o, state_out[, prior_out][, resp]).
+    """
+    torch = _torch()
+    ins, code, (B, H, T, Dk, Dv, J) = _check_inputs(q, k, v, beta_logit, prior_k_logit,
+                                                    prior_q_logit, decode=False)
+    _dev_tensor(state_in, "state_in", torch.float32)
+    if state_in is not None and tuple(state_in.shape) != (B, H, J, Dk, Dv):
+        raise ValueError("state_in must be [B,H,J,Dk,Dv] = %s" % ((B, H, J, Dk, Dv),))
+    gd = _gated_arg(decay_logit, code, (B, T, H, J, Dk))
+    temporal = gate_k_logit is not None or gate_q_logit is not None
+    tp, p_out = None, None
+    if temporal:
+        tp, p_out = _temporal_args(gate_k_logit, gate_q_logit, prior_in, prior_out, code,
+                                   (B, T, H, Dv), (B, H, 2, J, Dv), q.device)
+    odt = q.dtype if out_dtype is None else out_dtype
+    if o is None:
+        o = torch.empty((B, T, H, Dv), device=q.device, dtype=odt)
+    _dev_tensor(o, "o")
+    if state_out is True:
+        s_out = torch.empty((B, H, J, Dk, Dv), device=q.device, dtype=torch.float32)
+    elif state_out is False or state_out is None:
+        s_out = None
+    else:
+        s_out = _dev_tensor(state_out, "state_out", torch.float32)
+    r = torch.empty((B, T, H, J, Dv), device=q.device, dtype=torch.float32) if resp else None
+    opts = Opts(code, _dtype_code(o), _ALGOS[algo], 0, 0, 0.0, 0)
+    _check(load_library().swila_forward_gated(
+        ctypes.byref(Shape(B, H, T, Dk, Dv, J)), ctypes.byref(opts),
+        *[_ptr(t) for t in ins], ctypes.byref(gd), ctypes.byref(tp) if tp is not None else None,
+        _ptr(state_in), _ptr(s_out), _ptr(o), _ptr(r), _stream_handle(stream)))
+    out = (o, s_out)
+    if temporal:
+        out = out + (p_out,)
+    if resp:
+        out = out + (r,)
+    return out
+
+
+def decode_step_gated(q, k, v, beta_logit, prior_k_logit, prior_q_logit, decay_logit, state_in,
+                      *, gate_k_logit=None, gate_q_logit=None, prior_in=None, prior_out=None,
+                      state_out=None, o=None, out_dtype=None, stream=None):
+    """One Gated SwiLA token per sequence (swila_decode_step_gated): the arguments
+    of ``decode_step`` plus decay_logit [B,H,J,Dk], and optionally the temporal
+    gates [B,H,Dv] with the prior state.  state_out and prior_out default to the
+    inputs (updated in place).  Returns (o, state_out[, prior_out])."""
+    torch = _torch()
+    ins, code, (B, H, T, Dk, Dv, J) = _check_inputs(q, k, v, beta_logit, prior_k_logit,
+                                                    prior_q_logit, decode=True)
+    _dev_tensor(state_in, "state_in", torch.float32)
+    if state_in is not None and tuple(state_in.shape) != (B, H, J, Dk, Dv):
+        raise ValueError("state_in must be [B,H,J,Dk,Dv] = %s" % ((B, H, J, Dk, Dv),))
+    if state_out is None:
+        state_out = state_in if state_in is not None else torch.empty(
+            (B, H, J, Dk, Dv), device=q.device, dtype=torch.float32)
+    _dev_tensor(state_out, "state_out", torch.float32)
+    gd = _gated_arg(decay_logit, code, (B, H, J, Dk))
+    temporal = gate_k_logit is not None or gate_q_logit is not None
+    tp, p_out = None, None
+    if temporal:
+        if prior_out is None:
+            prior_out = prior_in if prior_in is not None else True
+        tp, p_out = _temporal_args(gate_k_logit, gate_q_logit, prior_in, prior_out, code,
+                                   (B, H, Dv), (B, H, 2, J, Dv), q.device)
+    odt = q.dtype if out_dtype is None else out_dtype
+    if o is None:
+        o = torch.empty((B, H, Dv), device=q.device, dtype=odt)
+    _dev_tensor(o, "o")
+    opts = Opts(code, _dtype_code(o), ALGO_AUTO, 0, 0, 0.0, 0)
+    _check(load_library().swila_decode_step_gated(
+        ctypes.byref(Shape(B, H, 1, Dk, Dv, J)), ctypes.byref(opts),
+        *[_ptr(t) for t in ins], ctypes.byref(gd), ctypes.byref(tp) if tp is not None else None,
+        _ptr(state_in), _ptr(state_out), _ptr(o), _stream_handle(stream)))
+    return (o, state_out, p_out) if temporal else (o, state_out)

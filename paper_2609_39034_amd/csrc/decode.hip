@@ -21,6 +21,10 @@
 // g^k pi^k as the key prior and rhobar = (1 - g^q) rhobar_{t-1} + g^q pi^q as
 // the query prior, and write the new pair (r, rhobar); prior_out may alias
 // prior_in for the same reason as the state.
+//
+// Gated SwiLA (GT; App. B.4, eq. pre-decay): every thread scales its rows by
+// the decay of its component and key index, a = sigmoid(decay logit), before
+// the dots, so the E-step, update and retrieval all see the decayed state.
 #include "device_common.hpp"
 #include "launch.hpp"
 
@@ -29,7 +33,7 @@ namespace {
 
 constexpr int kRows = 16;  // state rows per thread
 
-template <int DK, int J, bool TP>
+template <int DK, int J, bool TP, bool GT>
 __global__ __launch_bounds__(512) void decode_kernel(LayerArgs a, int DB) {
     constexpr int IG = DK / kRows;
     const int CL = DB / 4;
@@ -86,6 +90,16 @@ __global__ __launch_bounds__(512) void decode_kernel(LayerArgs a, int DB) {
     for (int i = tid; i < DK; i += blockDim.x) {
         sk[i] = load1(a.k, row * DK + i, ibf);
         sq[i] = load1(a.q, row * DK + i, ibf);
+    }
+    if constexpr (GT) {
+        // eq. pre-decay: w_j (.)= a_j, one gate per key index
+        if (has_rows) {
+#pragma unroll
+            for (int m = 0; m < kRows; ++m) {
+                const float g = sigmoid(load1(a.decay, (row * J + j) * DK + ig + IG * m, ibf));
+                st[m].x *= g, st[m].y *= g, st[m].z *= g, st[m].w *= g;
+            }
+        }
     }
     __syncthreads();
 
@@ -201,10 +215,14 @@ hipError_t launch_dk_j(const LayerArgs &a, hipStream_t stream) {
     int threads = J * (DK / kRows) * (DB / 4);
     if (threads < DB) threads = DB;
     dim3 grid(a.Dv / DB, a.H, a.B);
-    if (a.gk)
-        hipLaunchKernelGGL((decode_kernel<DK, J, true>), grid, dim3(threads), 0, stream, a, DB);
+    if (a.decay && a.gk)
+        hipLaunchKernelGGL((decode_kernel<DK, J, true, true>), grid, dim3(threads), 0, stream, a, DB);
+    else if (a.decay)
+        hipLaunchKernelGGL((decode_kernel<DK, J, false, true>), grid, dim3(threads), 0, stream, a, DB);
+    else if (a.gk)
+        hipLaunchKernelGGL((decode_kernel<DK, J, true, false>), grid, dim3(threads), 0, stream, a, DB);
     else
-        hipLaunchKernelGGL((decode_kernel<DK, J, false>), grid, dim3(threads), 0, stream, a, DB);
+        hipLaunchKernelGGL((decode_kernel<DK, J, false, false>), grid, dim3(threads), 0, stream, a, DB);
     return hipGetLastError();
 }
 

@@ -22,6 +22,9 @@ struct LayerArgs {
     const void *gk = nullptr, *gq = nullptr;
     const float *prior_in = nullptr;
     float *prior_out = nullptr;
+    // Gated SwiLA (App. B.4, eq. pre-decay): decay logits [B,T,H,J,Dk] (in_bf16),
+    // a = sigmoid, one gate per key dimension and component; nullptr = no decay.
+    const void *decay = nullptr;
 };
 
 // Parameters of the chunkwise quasi-Newton form (App. D).

@@ -26,6 +26,12 @@
 // the query prior rhobar_j = (1 - g^q) rhobar_{t-1,j} + g^q pi^q_j replaces
 // pi^q.  Both running priors live in registers, J per column, from the prior
 // state (or 1/J) to the prior state written at the end.
+//
+// Gated SwiLA (GT; Sec. 3.4, App. B.4, eq. pre-decay).  Each token first
+// decays the state, w_j (.)= a_{tj} with a = sigmoid(decay logit) one gate per
+// key dimension, and the prediction, E-step, update and retrieval then use the
+// decayed state.  The gates of a token round are formed once, in fp32, into
+// LDS ([token][j][key index], each lane reading its slice).
 #include "device_common.hpp"
 #include "launch.hpp"
 
@@ -44,7 +50,7 @@ constexpr int max_cols(int L, int J, bool tp) {
     return n;
 }
 
-template <int DK, int J, int S, bool TP>
+template <int DK, int J, int S, bool TP, bool GT>
 __global__ __launch_bounds__(kThreads) void scan_direct_kernel(LayerArgs a, int ncol) {
     constexpr int L = DK / S;             // lanes per output column
     constexpr int NCM = max_cols(L, J, TP);
@@ -58,6 +64,7 @@ __global__ __launch_bounds__(kThreads) void scan_direct_kernel(LayerArgs a, int 
     __shared__ float sPq[kTC][J][NCM];
     __shared__ float sO[kTC][NCM];
     __shared__ float sG[TP ? 2 : 1][kTC][TP ? NCM : 1];   // temporal: g^k, g^q
+    __shared__ __align__(16) float sA[GT ? kTC : 1][GT ? J : 1][GT ? DK : 4];   // gated: decay
 
     const int tid = threadIdx.x;
     const int nthr = ncol * L;
@@ -100,6 +107,16 @@ __global__ __launch_bounds__(kThreads) void scan_direct_kernel(LayerArgs a, int 
             const size_t off = ((size_t)(b * T + t0 + tt) * H + h) * DK + i;
             *reinterpret_cast<float4 *>(&sK[tt][i / S][i % S]) = load4(a.k, off, ibf);
             *reinterpret_cast<float4 *>(&sQ[tt][i / S][i % S]) = load4(a.q, off, ibf);
+        }
+        if constexpr (GT) {
+            for (int g = tid; g < nt * J * (DK / 4); g += nthr) {
+                const int tt = g / (J * (DK / 4)), rem = g % (J * (DK / 4));
+                const int j = rem / (DK / 4), i = (rem % (DK / 4)) * 4;
+                const float4 x = load4(
+                    a.decay, (((size_t)(b * T + t0 + tt) * H + h) * J + j) * DK + i, ibf);
+                *reinterpret_cast<float4 *>(&sA[tt][j][i]) =
+                    make_float4(sigmoid(x.x), sigmoid(x.y), sigmoid(x.z), sigmoid(x.w));
+            }
         }
         for (int g = tid; g < nt * ncol; g += nthr) {
             const int tt = g / ncol, c = g % ncol;
@@ -148,6 +165,16 @@ __global__ __launch_bounds__(kThreads) void scan_direct_kernel(LayerArgs a, int 
                 const float4 y = *reinterpret_cast<const float4 *>(&sQ[tt][l][s]);
                 kv[s] = x.x; kv[s + 1] = x.y; kv[s + 2] = x.z; kv[s + 3] = x.w;
                 qv[s] = y.x; qv[s + 1] = y.y; qv[s + 2] = y.z; qv[s + 3] = y.w;
+            }
+            if constexpr (GT) {
+                // eq. pre-decay: the state decays before the prediction
+#pragma unroll
+                for (int j = 0; j < J; ++j)
+#pragma unroll
+                    for (int s = 0; s < S; s += 4) {
+                        const float4 x = *reinterpret_cast<const float4 *>(&sA[tt][j][l * S + s]);
+                        w[j][s] *= x.x, w[j][s + 1] *= x.y, w[j][s + 2] *= x.z, w[j][s + 3] *= x.w;
+                    }
             }
             float p[J], y[J];
             float kq = 0.0f;
@@ -237,20 +264,24 @@ __global__ __launch_bounds__(kThreads) void scan_direct_kernel(LayerArgs a, int 
     }
 }
 
-template <int DK, int J, bool TP>
+template <int DK, int J, bool TP, bool GT>
 hipError_t launch_dk_j_tp(const LayerArgs &a, hipStream_t stream) {
     constexpr int S = (J <= 4) ? (DK < 16 ? DK : 16) : (DK < 8 ? DK : 8);
     constexpr int L = DK / S;
     const int ncol = a.Dv < max_cols(L, J, TP) ? a.Dv : max_cols(L, J, TP);
     dim3 grid(a.Dv / ncol, a.H, a.B);
     dim3 block(ncol * L);
-    hipLaunchKernelGGL((scan_direct_kernel<DK, J, S, TP>), grid, block, 0, stream, a, ncol);
+    hipLaunchKernelGGL((scan_direct_kernel<DK, J, S, TP, GT>), grid, block, 0, stream, a, ncol);
     return hipGetLastError();
 }
 
 template <int DK, int J>
 hipError_t launch_dk_j(const LayerArgs &a, hipStream_t stream) {
-    return a.gk ? launch_dk_j_tp<DK, J, true>(a, stream) : launch_dk_j_tp<DK, J, false>(a, stream);
+    if (a.decay)
+        return a.gk ? launch_dk_j_tp<DK, J, true, true>(a, stream)
+                    : launch_dk_j_tp<DK, J, false, true>(a, stream);
+    return a.gk ? launch_dk_j_tp<DK, J, true, false>(a, stream)
+                : launch_dk_j_tp<DK, J, false, false>(a, stream);
 }
 
 template <int DK>

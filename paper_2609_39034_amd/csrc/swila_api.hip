@@ -196,6 +196,31 @@ int check_temporal(const swila_shape *shape, const swila_opts *opts, const swila
     return SWILA_OK;
 }
 
+// Gated SwiLA argument (App. B.4): the decay logits, an input of in_dtype,
+// [B,T,H,J,Dk]; disjoint from every output.
+int check_gated(const swila_shape *shape, const swila_opts *opts, const swila_gated *gd,
+                const swila_temporal *tp, void *o, float *state_out, float *resp,
+                swila::LayerArgs *a) {
+    if (!gd) return fail(SWILA_EINVAL, "gated is NULL");
+    const size_t B = shape->B, H = shape->H, T = shape->T, Dk = shape->Dk, Dv = shape->Dv,
+                 J = shape->J;
+    const size_t ie = opts->in_dtype == SWILA_BF16 ? 2 : 4;
+    const size_t oe = opts->out_dtype == SWILA_BF16 ? 2 : 4;
+    const Span dec{"decay_logit", gd->decay_logit, B * T * H * J * Dk * ie};
+    int rc = check_ptr(dec, T > 0);
+    if (rc) return rc;
+    const Span outs[] = {
+        {"o", o, B * T * H * Dv * oe},
+        {"state_out", state_out, B * H * J * Dk * Dv * 4},
+        {"resp_out", resp, B * T * H * J * Dv * 4},
+        {"prior_out", tp ? tp->prior_out : nullptr, B * H * 2 * J * Dv * 4},
+    };
+    for (const Span &x : outs)
+        if (overlap(dec, x)) return fail(SWILA_EINVAL, "decay_logit overlaps %s", x.name);
+    a->decay = gd->decay_logit;
+    return SWILA_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -340,6 +365,63 @@ int swila_decode_step_temporal(const swila_shape *shape, const swila_opts *opts,
     if (rc) return rc;
     rc = check_temporal(shape, opts, temporal, q, k, v, beta_logit, prior_k_logit, prior_q_logit,
                         state_in, state_out, o, nullptr, &a);
+    if (rc) return rc;
+    return map_hip(swila::launch_decode(a, static_cast<hipStream_t>(stream)), "decode launch");
+}
+
+int swila_forward_gated(const swila_shape *shape, const swila_opts *opts, const void *q,
+                        const void *k, const void *v, const void *beta_logit,
+                        const void *prior_k_logit, const void *prior_q_logit,
+                        const swila_gated *gated, const swila_temporal *temporal,
+                        const float *state_in, float *state_out, void *o, float *resp_out,
+                        void *stream) {
+    clear_error();
+    swila::LayerArgs a;
+    int rc = prepare(shape, opts, false, q, k, v, beta_logit, prior_k_logit, prior_q_logit,
+                     state_in, state_out, o, resp_out, &a);
+    if (rc) return rc;
+    if (temporal) {
+        rc = check_temporal(shape, opts, temporal, q, k, v, beta_logit, prior_k_logit,
+                            prior_q_logit, state_in, state_out, o, resp_out, &a);
+        if (rc) return rc;
+    }
+    rc = check_gated(shape, opts, gated, temporal, o, state_out, resp_out, &a);
+    if (rc) return rc;
+    if (opts->algo == SWILA_ALGO_NEWTON || opts->algo == SWILA_ALGO_CHUNK_EXACT)
+        return fail(SWILA_EUNSUPPORTED, "the gated form runs on SWILA_ALGO_RECURRENT");
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    if (shape->T == 0) {
+        if (state_out) {
+            rc = map_hip(swila::launch_state_fill(state_out, state_in,
+                                                  swila_state_bytes(shape) / sizeof(float), st),
+                         "state copy");
+            if (rc) return rc;
+        }
+        if (!temporal || !temporal->prior_out) return SWILA_OK;
+        const size_t n = (size_t)shape->B * shape->H * 2 * shape->J * shape->Dv;
+        return map_hip(swila::launch_fill(temporal->prior_out, temporal->prior_in, n,
+                                          1.0f / shape->J, st),
+                       "prior state copy");
+    }
+    return map_hip(swila::launch_scan_direct(a, st), "scan launch");
+}
+
+int swila_decode_step_gated(const swila_shape *shape, const swila_opts *opts, const void *q,
+                            const void *k, const void *v, const void *beta_logit,
+                            const void *prior_k_logit, const void *prior_q_logit,
+                            const swila_gated *gated, const swila_temporal *temporal,
+                            const float *state_in, float *state_out, void *o, void *stream) {
+    clear_error();
+    swila::LayerArgs a;
+    int rc = prepare(shape, opts, true, q, k, v, beta_logit, prior_k_logit, prior_q_logit,
+                     state_in, state_out, o, nullptr, &a);
+    if (rc) return rc;
+    if (temporal) {
+        rc = check_temporal(shape, opts, temporal, q, k, v, beta_logit, prior_k_logit,
+                            prior_q_logit, state_in, state_out, o, nullptr, &a);
+        if (rc) return rc;
+    }
+    rc = check_gated(shape, opts, gated, temporal, o, state_out, nullptr, &a);
     if (rc) return rc;
     return map_hip(swila::launch_decode(a, static_cast<hipStream_t>(stream)), "decode launch");
 }

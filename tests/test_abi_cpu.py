@@ -212,3 +212,29 @@ def test_temporal_decode_requires_one_token(lib):
                                         ctypes.byref(OPTS), *ptrs, ctypes.byref(tp), None, None,
                                         FAKE2, None)
     assert rc == sw.EINVAL and "T == 1" in lib.swila_last_error().decode()
+
+
+def test_gated_argument_checks(lib):
+    shape = sw.Shape(1, 2, 8, 64, 64, 4)
+    ptrs = [ctypes.c_void_p((1 << 20) + (i << 26)) for i in range(6)]
+    dec = 1 << 33
+
+    def call(gd, tp=None, opts=OPTS, o=FAKE2):
+        rc = lib.swila_forward_gated(ctypes.byref(shape), ctypes.byref(opts), *ptrs,
+                                     None if gd is None else ctypes.byref(gd),
+                                     None if tp is None else ctypes.byref(tp), None, None, o,
+                                     None, None)
+        return rc, lib.swila_last_error().decode()
+
+    assert call(None) == (sw.EINVAL, "gated is NULL")
+    assert call(sw.Gated(None)) == (sw.EINVAL, "decay_logit is NULL")
+    rc, msg = call(sw.Gated(dec + 4))
+    assert rc == sw.EINVAL and "decay_logit is not 16-byte aligned" in msg
+    rc, msg = call(sw.Gated(FAKE2.value))
+    assert rc == sw.EINVAL and "decay_logit overlaps o" in msg
+    chunk = sw.Opts(sw.BF16, sw.BF16, sw.ALGO_CHUNK_EXACT, 0, 0, 0.0, 0)
+    rc, msg = call(sw.Gated(dec), opts=chunk)
+    assert rc == sw.EUNSUPPORTED and "RECURRENT" in msg
+    # temporal arguments are checked too when given
+    rc, msg = call(sw.Gated(dec), tp=sw.Temporal(None, 1 << 32, None, None))
+    assert rc == sw.EINVAL and msg == "gate_k_logit is NULL"

@@ -1,0 +1,126 @@
+"""Parity of the Gated SwiLA path (Sec. 3.4, App. B.4, eq. pre-decay with one
+gate per key dimension) through the C ABI with the fp64 oracle: the
+token-by-token scan and the decode step, alone and with the temporal priors.
+
+Bar as for the plain form: per (b, h), max|gpu - oracle| / max|oracle| <= 1e-4
+for fp32 inputs and <= 2e-2 for bf16 inputs (outputs, final state,
+responsibilities, prior state).
+"""
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+from gpu_helpers import NAMES, head_rel_err, to_device, tol_for, torch_dtype
+
+pytestmark = pytest.mark.gpu
+
+
+def _t(x, dtype):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(x)).to("cuda", torch_dtype(dtype))
+
+
+CASES = [
+    # B, H, T, Dk, Dv, J, dtype, state_std, temporal, decay mean
+    (1, 1, 64, 16, 16, 2, "f32", 0.0, False, 2.0),
+    (2, 3, 50, 64, 128, 4, "f32", 0.3, False, 1.0),
+    (2, 2, 37, 128, 128, 4, "bf16", 0.1, False, 2.0),
+    (1, 2, 33, 128, 64, 8, "f32", 0.2, True, 2.0),
+    (2, 1, 17, 32, 16, 3, "f32", 0.5, False, 0.0),
+    (1, 3, 21, 16, 32, 1, "f32", 0.5, True, 3.0),
+    (3, 1, 40, 64, 32, 2, "bf16", 0.0, True, 2.0),
+    (1, 1, 1, 128, 128, 4, "f32", 0.2, False, 2.0),
+    (2, 2, 16, 32, 128, 8, "bf16", 0.1, False, 1.0),
+]
+
+
+@pytest.mark.parametrize("B,H,T,Dk,Dv,J,dtype,std,temporal,mean", CASES)
+def test_gated_forward(B, H, T, Dk, Dv, J, dtype, std, temporal, mean):
+    import torch
+    import paper_2609_39034_amd as sw
+    seed = 400 + T + J
+    inp = workloads.iid_inputs(B, H, T, Dk, Dv, J, dtype=dtype, seed=seed, state_std=std)
+    dec = workloads.gated_inputs(B, H, T, Dk, J, dtype=dtype, seed=seed, mean=mean)["decay"]
+    dev = to_device(inp, dtype)
+    kw, okw = {}, {}
+    if temporal:
+        tmp = workloads.temporal_inputs(B, H, T, Dv, J, dtype=dtype, seed=seed, prior_state=True)
+        kw = dict(gate_k_logit=_t(tmp["gk"], dtype), gate_q_logit=_t(tmp["gq"], dtype),
+                  prior_in=torch.from_numpy(tmp["prior"]).cuda())
+        okw = dict(gate_k_logit=tmp["gk"], gate_q_logit=tmp["gq"], prior_in=tmp["prior"])
+    res = sw.forward_gated(*(dev[n] for n in NAMES), _t(dec, dtype), dev["state"], resp=True, **kw)
+    torch.cuda.synchronize()
+    res = [x.float().cpu().numpy().astype(np.float64) for x in res]
+    ref = oracle.forward(*(inp[n] for n in NAMES), inp["state"], decay_logit=dec, want_resp=True,
+                         **okw)
+    tol = tol_for(dtype)
+    eo, es = head_rel_err(res[0], ref["o"], "o"), head_rel_err(res[1], ref["state"], "state")
+    er = head_rel_err(res[-1], ref["resp"], "resp")
+    ep = float(np.abs(res[2] - ref["prior"]).max()) if temporal else 0.0
+    print("o %.3e state %.3e resp %.3e prior %.3e (tol %.0e)" % (eo, es, er, ep, tol))
+    assert eo <= tol and es <= tol and er <= tol and ep <= tol
+
+
+def test_gated_saturated_equals_plain():
+    """A decay gate at 1 (logit 40) gives the plain recurrence."""
+    import torch
+    import paper_2609_39034_amd as sw
+    B, H, T, D, J = 2, 2, 45, 64, 4
+    inp = workloads.iid_inputs(B, H, T, D, D, J, dtype="f32", seed=79, state_std=0.2)
+    dev = to_device(inp, "f32")
+    dec = torch.full((B, T, H, J, D), 40.0, device="cuda")
+    o_g, s_g = sw.forward_gated(*(dev[n] for n in NAMES), dec, dev["state"])
+    o_p, s_p = sw.forward(*(dev[n] for n in NAMES), dev["state"], algo="recurrent")
+    torch.cuda.synchronize()
+    eo = head_rel_err(o_g.cpu().numpy(), o_p.cpu().numpy().astype(np.float64), "o")
+    es = head_rel_err(s_g.cpu().numpy(), s_p.cpu().numpy().astype(np.float64), "state")
+    print("o %.3e state %.3e" % (eo, es))
+    assert eo <= 1e-6 and es <= 1e-6
+
+
+DECODE = [
+    # B, H, Dk, Dv, J, dtype, steps, temporal
+    (4, 3, 64, 64, 4, "f32", 3, False),
+    (3, 2, 128, 128, 4, "bf16", 4, True),
+    (2, 2, 32, 16, 3, "f32", 3, True),
+    (2, 1, 16, 32, 8, "bf16", 2, False),
+    (5, 2, 128, 64, 1, "f32", 2, False),
+]
+
+
+@pytest.mark.parametrize("B,H,Dk,Dv,J,dtype,steps,temporal", DECODE)
+def test_gated_decode_steps(B, H, Dk, Dv, J, dtype, steps, temporal):
+    """Consecutive gated decode steps, state (and prior state) in place, equal the
+    oracle's forward over those tokens."""
+    import torch
+    import paper_2609_39034_amd as sw
+    seed = 600 + Dk + J
+    inp = workloads.iid_inputs(B, H, steps, Dk, Dv, J, dtype=dtype, seed=seed, state_std=0.1)
+    dec = workloads.gated_inputs(B, H, steps, Dk, J, dtype=dtype, seed=seed)["decay"]
+    dev = to_device(inp, dtype)
+    st = dev["state"].clone()
+    okw = {}
+    pr = None
+    if temporal:
+        tmp = workloads.temporal_inputs(B, H, steps, Dv, J, dtype=dtype, seed=seed,
+                                        prior_state=True)
+        pr = torch.from_numpy(tmp["prior"]).cuda()
+        okw = dict(gate_k_logit=tmp["gk"], gate_q_logit=tmp["gq"], prior_in=tmp["prior"])
+    outs = []
+    for t in range(steps):
+        x = [dev[n][:, t].contiguous() for n in NAMES]
+        kw = {}
+        if temporal:
+            kw = dict(gate_k_logit=_t(tmp["gk"][:, t], dtype), gate_q_logit=_t(tmp["gq"][:, t], dtype),
+                      prior_in=pr)
+        res = sw.decode_step_gated(*x, _t(dec[:, t], dtype), st, **kw)
+        outs.append(res[0].float())
+    torch.cuda.synchronize()
+    ref = oracle.forward(*(inp[n] for n in NAMES), inp["state"], decay_logit=dec, **okw)
+    o = torch.stack(outs, dim=1).cpu().numpy()
+    tol = tol_for(dtype)
+    eo, es = head_rel_err(o, ref["o"], "o"), head_rel_err(st.cpu().numpy(), ref["state"], "state")
+    ep = float(np.abs(pr.cpu().numpy() - ref["prior"]).max()) if temporal else 0.0
+    print("o %.3e state %.3e prior %.3e (tol %.0e)" % (eo, es, ep, tol))
+    assert eo <= tol and es <= tol and ep <= tol
