@@ -34,9 +34,11 @@ PEAK_MFMA_BF16 = 2.5e15    # FLOP/s, MI355X dense bf16 matrix
 # same counters on a plain 1 GiB copy (FETCH x2.0, WRITE x1.0); valid only for the
 # kernel source they were measured on (summary in profiles/).
 MEASURED_TRAFFIC = {
-    ("decode.hip", "d4bb8e3129fba693ae0d7e4f65fe205210ec56e8df246af4a7ff5599efab912f"): 2184301248,
-    ("scan_pipe.hip", "ed7cab280194b1de5538dcc55ed2797bfbd2d49516ae896064a0d63f646563d0"):
-        136662720,
+    ("decode.hip", "17cda266f6fb5ff92e54ad1b1e645c9ce379946f7ede393facaad11ebd01f546"): 2184300368,
+    ("scan_pipe.hip", "c7ef4e85ac79240fa947b91459c2aef53e021ec3e0d575bc781f8d2969cead69"):
+        136668672,
+    ("scan_pipe_temporal.hip", "066ea19bbb3b339720d4545d0ff436cf74e564f2160979d0ede03be1e7cf9af4"):
+        153628224,
 }
 
 
@@ -239,11 +241,81 @@ def bench_temporal(sw, torch, workloads, dev, cfg, seed, steps, warmup, o, s_out
         "tokens_per_s": B * T / wall, "ms_per_step": wall * 1e3,
         "algo": "chunk_exact" if chunk else "recurrent",
         "roofline": {"bound": "hbm", "achieved": nbytes / kern / 1e9, "peak": PEAK_HBM / 1e9,
-                     "unit": "GB/s", "frac": nbytes / kern / PEAK_HBM, "traffic": None,
+                     "unit": "GB/s", "frac": nbytes / kern / PEAK_HBM,
+                     "traffic": measured_traffic("scan_pipe_temporal.hip") if chunk else None,
                      "kernel": ("scan_pipe_kernel (temporal mode)" if chunk
                                 else "scan_direct_kernel (temporal)"),
                      "kernel_ms": kern * 1e3, "alg_bytes_per_launch": nbytes},
     }
+
+
+def bench_gated(sw, torch, workloads, dev, cfg, seed, steps, warmup, o, s_out, tdt):
+    """Gated SwiLA (App. B.4, eq. pre-decay, one gate per key dimension) on the
+    same batch: decay logits N(2, 1), through the token-by-token scan."""
+    B, H, T, Dk, Dv, J = (cfg[x] for x in ("B", "H", "T", "Dk", "Dv", "J"))
+    dec = workloads.gated_inputs(B, H, T, Dk, J, dtype=cfg["dtype"], seed=seed)["decay"]
+    dec = torch.from_numpy(dec).to("cuda", tdt)
+    names = ("q", "k", "v", "lb", "lk", "lq")
+    args = [dev[n] for n in names]
+
+    def step():
+        sw.forward_gated(*args, dec, dev["state"], o=o, state_out=s_out)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(steps)]
+    t0 = time.perf_counter()
+    for i in range(steps):
+        ev[i][0].record(stream)
+        step()
+        ev[i][1].record(stream)
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) / steps
+    kern = sum(a.elapsed_time(b) for a, b in ev) / steps / 1e3
+    eb = 2 if cfg["dtype"] == "bf16" else 4
+    nbytes = (forward_alg_bytes(B, H, T, Dk, Dv, J, eb, eb, dev["state"] is not None, True)
+              + eb * J * Dk * B * H * T)
+    # the method's FMAs plus the decay: one multiply per state element and token
+    nflop = forward_alg_flops(B, H, T, Dk, Dv, J) + J * Dk * Dv * B * H * T
+    return {
+        "workload": "Gated SwiLA (App. B.4, pre-decay, one gate per key dim), same batch, "
+                    "decay logits N(2,1), token-by-token scan",
+        "tokens_per_s": B * T / wall, "ms_per_step": wall * 1e3, "algo": "recurrent",
+        "roofline": {"bound": "alu", "achieved": nflop / kern / 1e12,
+                     "peak": PEAK_VALU_F32 / 1e12, "unit": "TFLOP/s",
+                     "frac": nflop / kern / PEAK_VALU_F32, "traffic": None,
+                     "kernel": "scan_direct_kernel (gated)", "kernel_ms": kern * 1e3,
+                     "alg_flop_per_launch": nflop, "alg_bytes_per_launch": nbytes},
+    }
+
+
+def newton_study(sw, torch, workloads, steps, tol):
+    """The paper's only chunked measurement (App. D.2): batch 16, T = 4096, 8 heads,
+    D = 64, J = 4, synthetic N(0,1) inputs.  Runs the App. D form to tolerance and
+    the exact chunk scan on the same batch, and compares their outputs."""
+    B, H, T, Dk, Dv, J = 16, 8, 4096, 64, 64, 4
+    inp = workloads.iid_inputs(B, H, T, Dk, Dv, J, dtype="bf16", seed=1042)
+    dev = workloads.to_torch(inp, "cuda", torch.bfloat16)
+    o = torch.empty((B, T, H, Dv), device="cuda", dtype=torch.bfloat16)
+    s_out = torch.empty((B, H, J, Dk, Dv), device="cuda", dtype=torch.float32)
+    wall_x, kern_x = time_forward(sw, torch, dev, steps, 1, o, s_out, "chunk")
+    o_x, s_x = o.float().clone(), s_out.clone()
+    cfg = {"B": B, "H": H, "T": T, "Dk": Dk, "Dv": Dv, "J": J}
+    res = bench_newton(sw, torch, dev, cfg, steps, 1, o, s_out, tol)
+    torch.cuda.synchronize()
+    diff_o = ((o.float() - o_x).abs().amax() / o_x.abs().amax()).item()
+    diff_s = ((s_out - s_x).abs().amax() / s_x.abs().amax()).item()
+    res.update({
+        "workload": "App. D study: B=16 H=8 T=4096 Dk=Dv=64 J=4, bf16 N(0,1) inputs, tol %g"
+                    % tol,
+        "exact_chunk_ms": wall_x * 1e3, "exact_chunk_kernel_ms": kern_x * 1e3,
+        "newton_over_exact": res["ms_per_step"] / (wall_x * 1e3),
+        "max_rel_diff_vs_exact": {"o": diff_o, "state": diff_s},
+    })
+    return res
 
 
 def cpu_baseline(workloads, inp, cfg):
@@ -271,6 +343,9 @@ def main():
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-newton", action="store_true")
     ap.add_argument("--no-temporal", action="store_true")
+    ap.add_argument("--no-gated", action="store_true")
+    ap.add_argument("--newton-study", action="store_true",
+                    help="only the App. D measurement at B=16 H=8 T=4096 D=64 J=4")
     ap.add_argument("--newton-tol", type=float, default=1e-3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -294,6 +369,10 @@ def main():
         print(json.dumps({"copy_bytes_read": x.numel() * 4, "copy_bytes_written": y.numel() * 4}))
         return
     sw.load_library()
+    if args.newton_study:
+        print(json.dumps({"newton_study": newton_study(sw, torch, workloads, args.steps,
+                                                        args.newton_tol)}), flush=True)
+        return
     cfg = workloads.CONFIGS[args.config]
     B, H, T, Dk, Dv, J = (cfg[x] for x in ("B", "H", "T", "Dk", "Dv", "J"))
     bf16 = cfg["dtype"] == "bf16"
@@ -337,6 +416,9 @@ def main():
     if not args.no_temporal:
         out["temporal"] = bench_temporal(sw, torch, workloads, dev, cfg, 1000 + args.config,
                                          args.steps, args.warmup, o, s_out, args.algo, tdt)
+    if not args.no_gated:
+        out["gated"] = bench_gated(sw, torch, workloads, dev, cfg, 1000 + args.config,
+                                   args.steps, args.warmup, o, s_out, tdt)
     if not args.no_newton and bf16:
         out["newton"] = bench_newton(sw, torch, dev, cfg, args.steps, args.warmup, o, s_out,
                                      args.newton_tol)
