@@ -981,8 +981,9 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
                     // whether r is wanted is taken once per chunk.
                     auto run = [&](auto want) {
                         constexpr bool R = decltype(want)::value;
-                        // zmin tracks min(z, 1/z): below 2^-100 iff z left the range
-                        float zmin = 1.f, cprev = 0.f, gprev[kC], cb[4];
+                        // chk sums z * (1/z): not finite iff some z is 0, infinite or
+                        // not a number (every component underflowed, or overflowed)
+                        float chk = 0.f, cprev = 0.f, gprev[kC], cb[4];
 #pragma unroll
                         for (int t = 0; t < kC; ++t) {
                             // row t+1 of G from column t+2 on, in 16-byte reads
@@ -1048,12 +1049,18 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
                                 sm.r[pr][t][bsto] = rt;
                                 if constexpr (TP) rprev = rt;
                             }
-                            zmin = fminf(zmin, fminf(z, iz));
+                            chk = fmaf(z, iz, chk);
                             cprev = cs;
 #pragma unroll
                             for (int u = t + 2; u < kC; ++u) gprev[u] = grow[u], grow[u] = gnext[u];
                         }
-                        if (__builtin_amdgcn_ballot_w64(bact && !(zmin >= 0x1p-100f)) != 0) {
+                        // (an integer test on bits the compiler cannot trace back to a
+                        // float: the file is compiled without NaN semantics, and would
+                        // otherwise reduce the test to |chk| == inf)
+                        uint32_t chk_bits = __float_as_uint(chk);
+                        asm volatile("" : "+v"(chk_bits));
+                        const bool bad = (chk_bits & 0x7f800000u) == 0x7f800000u;
+                        if (__builtin_amdgcn_ballot_w64(bact && bad) != 0) {
                             // some softmax underflowed: the chunk again, maximum subtracted
 #pragma unroll
                             for (int u = 1; u < kC; ++u) grow[u] = sm.g[pr][0][u];
