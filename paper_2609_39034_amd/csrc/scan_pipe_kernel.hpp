@@ -471,6 +471,12 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
     // loops strided by NBT count 0 .. ceil(n / NBT) from bt and stop at n: a
     // trip count it can see, and fully unrolled loops.
     const int bt = 64 * bw + lane;
+    // The loops below deal n items over the NBT bookkeeping threads; when n is
+    // not a multiple of NBT the first threads take one item more.  Each loop
+    // starts its deal at a different bookkeeping wave (brot(k)), so those extra
+    // items fall on different waves.  (Called only by bookkeeping threads, for
+    // which 0 <= bt < NBT.)
+    auto brot = [&](int k) { return (bt + (k % NBW) * 64) % NBT; };
     // the wave that forms the Gram matrix of the next chunk for the sequential wave
     const bool gwave = NH == 0 ? w == 1 % NW : w == NW + 1;
     // Newton mode: this block's predictions, [NCH * kC][N] fp32
@@ -598,7 +604,7 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
             // forms; padded tokens carry no mass and keep r_{t-1}.
 #pragma unroll
             for (int i_ = 0; i_ < ceil_div(NPG, NBT); ++i_) {
-                const int gi = bt + i_ * NBT;
+                const int gi = brot(0) + i_ * NBT;
                 if (gi >= NPG) break;
                 const int e = PE * gi, t = e / DB, dl = e % DB;
                 const bool ok = m * kC + t < T;
@@ -636,7 +642,7 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
         } else if constexpr (!NT) {
 #pragma unroll
           for (int i_ = 0; i_ < ceil_div(kC * N / 4, NBT); ++i_) {
-            const int g4 = bt + i_ * NBT;
+            const int g4 = brot(0) + i_ * NBT;
             if (g4 >= kC * N / 4) break;
             // four consecutive columns (dims dl .. dl+3 of one component) of token t
             const int e4 = 4 * g4, t = e4 / N, cc = e4 % N;
@@ -650,7 +656,7 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
           }
 #pragma unroll
           for (int i_ = 0; i_ < ceil_div(kC * DB / 4, NBT); ++i_) {
-            const int g4 = bt + i_ * NBT;
+            const int g4 = brot(1) + i_ * NBT;
             if (g4 >= kC * DB / 4) break;
                 const int e4 = 4 * g4;
                 float vv[4];
@@ -666,7 +672,7 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
             const float *po = reinterpret_cast<const float *>(sm.pw[m % kRingQP]);
 #pragma unroll
             for (int i_ = 0; i_ < ceil_div(NPG, NBT); ++i_) {
-            const int gi = bt + i_ * NBT;
+            const int gi = brot(0) + i_ * NBT;
             if (gi >= NPG) break;
                 const int e = PE * gi, t = e / DB, dl = e % DB;
                 const bool ok = m * kC + t < T;
@@ -721,7 +727,7 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
         constexpr float kQS = TP ? 1.f : kInvWS;
 #pragma unroll
         for (int i_ = 0; i_ < ceil_div(NPG, NBT); ++i_) {
-            const int gi = bt + i_ * NBT;
+            const int gi = (OUT0 ? bt : brot(2)) + i_ * NBT;
             if (gi >= NPG) break;
             const int e = PE * gi, t = e / DB, dl = e % DB;
             float x[J][PE], mq[PE], z[PE];
@@ -788,7 +794,7 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
     auto store_output = [&](int m, int pr) {
 #pragma unroll
         for (int i_ = 0; i_ < ceil_div(NPG, NBT); ++i_) {
-            const int gi = bt - OUT0 + i_ * NBT;
+            const int gi = (OUT0 ? bt - OUT0 : brot(1)) + i_ * NBT;
             if (gi < 0 || gi >= NPG) break;   // gi < 0: a thread of the query-prior half
             const int e = PE * gi, t = e / DB, dl = e % DB;
             if (m * kC + t < T) {
@@ -813,7 +819,7 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
         if constexpr (!NT) {
 #pragma unroll
           for (int i_ = 0; i_ < ceil_div(kC * N / 4, NBT); ++i_) {
-            const int g4 = bt + i_ * NBT;
+            const int g4 = brot(2) + i_ * NBT;
             if (g4 >= kC * N / 4) break;
             const int e4 = 4 * g4, t = e4 / N, cc = e4 % N;
             if (m * kC + t < T)
@@ -1223,7 +1229,14 @@ hipError_t launch_dk(const LayerArgs &a, const NewtonArgs &na, hipStream_t strea
             if (a.Dv >= 32) return launch_cfg<DK, 2, 32, MD>(a, na, stream);
             return launch_cfg<DK, 2, 16, MD>(a, na, stream);
         case 3: return launch_cfg<DK, 3, 16, MD>(a, na, stream);
-        case 4: return launch_cfg<DK, 4, 8, MD>(a, na, stream);
+        case 4:
+            // With enough heads to fill the chip twice over at 32 columns, 64
+            // columns per block halve the blocks: the sequential wave's time per
+            // token does not depend on its column count, so fewer, wider blocks
+            // finish the batch in fewer rounds.
+            if ((long)(a.Dv / 8) * a.H * a.B >= 512 && a.Dv >= 16)
+                return launch_cfg<DK, 4, 16, MD>(a, na, stream);
+            return launch_cfg<DK, 4, 8, MD>(a, na, stream);
         case 8: return launch_cfg<DK, 8, 8, MD>(a, na, stream);
         default: return hipErrorInvalidValue;
     }
