@@ -46,6 +46,7 @@ NEWTON_SMALL = [
     (1, 2, 33, 16, 64, 1, 0.2, 2),
     (1, 1, 20, 128, 128, 2, 0.1, 5),
     (1, 1, 16, 64, 32, 4, 0.3, 3),
+    (4, 8, 20, 64, 128, 4, 0.1, 2),   # 512 blocks at 32 columns: the 64-column blocks
 ]
 
 
