@@ -124,3 +124,26 @@ def test_gated_decode_steps(B, H, Dk, Dv, J, dtype, steps, temporal):
     ep = float(np.abs(pr.cpu().numpy() - ref["prior"]).max()) if temporal else 0.0
     print("o %.3e state %.3e prior %.3e (tol %.0e)" % (eo, es, ep, tol))
     assert eo <= tol and es <= tol and ep <= tol
+
+
+def test_gated_config2_sampled_heads():
+    """The c2 batch, as the benchmark times it, through the gated form (decay
+    logits N(2,1)); the oracle on sampled heads."""
+    import torch
+    import paper_2609_39034_amd as sw
+    inp = workloads.config_inputs(2)
+    c = workloads.CONFIGS[2]
+    B, H, T, Dk, J = c["B"], c["H"], c["T"], c["Dk"], c["J"]
+    dec = workloads.gated_inputs(B, H, T, Dk, J, dtype="bf16", seed=1002)["decay"]
+    dev = to_device(inp, "bf16")
+    o, s, r = sw.forward_gated(*(dev[n] for n in NAMES), _t(dec, "bf16"), None, resp=True)
+    torch.cuda.synchronize()
+    o, s, r = (x.float().cpu().numpy().astype(np.float64) for x in (o, s, r))
+    for b, h in [(0, 0), (3, 7), (2, 4)]:
+        sub = [inp[n][b:b + 1, :, h:h + 1] for n in NAMES]
+        ref = oracle.forward(*sub, None, decay_logit=dec[b:b + 1, :, h:h + 1], want_resp=True)
+        eo = head_rel_err(o[b:b + 1, :, h:h + 1], ref["o"], "o")
+        es = head_rel_err(s[b:b + 1, h:h + 1], ref["state"], "state")
+        er = head_rel_err(r[b:b + 1, :, h:h + 1], ref["resp"], "resp")
+        print("head (%d,%d): o %.3e state %.3e resp %.3e" % (b, h, eo, es, er))
+        assert eo <= 2e-2 and es <= 2e-2 and er <= 2e-2

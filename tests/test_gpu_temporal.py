@@ -237,3 +237,30 @@ def test_temporal_chunk_extreme_errors():
     er, ep = head_rel_err(r, ref["resp"], "resp"), _prior_err(p, ref["prior"])
     print("o %.3e state %.3e resp %.3e prior %.3e" % (eo, es, er, ep))
     assert eo <= 2e-2 and es <= 2e-2 and er <= 2e-2 and ep <= 2e-2
+
+
+@pytest.mark.parametrize("cfg,heads", [(2, [(0, 0), (3, 7)]), (3, [(0, 0), (7, 15)]),
+                                       (5, [(1, 7)])])
+def test_temporal_standard_configs_sampled_heads(cfg, heads):
+    """The standard batches, in the launch shape the benchmark times, through the
+    temporal chunk scan with N(0,1) gate logits; the oracle on sampled heads."""
+    inp = workloads.config_inputs(cfg)
+    c = workloads.CONFIGS[cfg]
+    B, H, T, Dv, J = c["B"], c["H"], c["T"], c["Dv"], c["J"]
+    tmp = workloads.temporal_inputs(B, H, T, Dv, J, dtype="bf16", seed=1000 + cfg)
+    o, s, p, r = _run_gpu(inp, tmp, "bf16", algo="auto")
+    for b, h in heads:
+        sub = {n: inp[n][b:b + 1, :, h:h + 1] for n in NAMES}
+        sub["state"] = None
+        st = {"gk": tmp["gk"][b:b + 1, :, h:h + 1], "gq": tmp["gq"][b:b + 1, :, h:h + 1],
+              "prior": None}
+        ref = _run_oracle(sub, st)
+        eo = head_rel_err(o[b:b + 1, :, h:h + 1], ref["o"], "o")
+        es = head_rel_err(s[b:b + 1, h:h + 1], ref["state"], "state")
+        er = head_rel_err(r[b:b + 1, :, h:h + 1], ref["resp"], "resp")
+        ep = _prior_err(p[b:b + 1, h:h + 1], ref["prior"])
+        print("cfg %d head (%d,%d): o %.3e state %.3e resp %.3e prior %.3e"
+              % (cfg, b, h, eo, es, er, ep))
+        assert eo <= 2e-2 and es <= 2e-2 and er <= 2e-2 and ep <= 2e-2
+    assert np.all(np.isfinite(o)) and np.all(np.isfinite(s))
+    assert np.max(np.abs(p.sum(axis=3) - 1.0)) < 1e-4
