@@ -30,26 +30,42 @@ PEAK_HBM = 8.0e12          # B/s, MI355X HBM3E
 PEAK_VALU_F32 = 157.3e12   # FLOP/s, MI355X fp32 vector (packed); unpacked FMA is half
 PEAK_MFMA_BF16 = 2.5e15    # FLOP/s, MI355X dense bf16 matrix
 
-# HBM bytes per launch from rocprofv3 FETCH_SIZE/WRITE_SIZE passes, scaled by the
-# same counters on a plain 1 GiB copy (FETCH x2.0, WRITE x1.0); valid only for the
-# kernel source they were measured on (summary in profiles/).
+# Counter-measured HBM bytes per launch (FETCH_SIZE and WRITE_SIZE, each scaled by
+# what the counter reads for a plain copy of known size), keyed by the kernel's
+# source, the workload it ran and the digest of the source at measurement.
 MEASURED_TRAFFIC = {
-    ("decode.hip", "17cda266f6fb5ff92e54ad1b1e645c9ce379946f7ede393facaad11ebd01f546"): 2184300368,
-    ("scan_pipe.hip", "c7ef4e85ac79240fa947b91459c2aef53e021ec3e0d575bc781f8d2969cead69"):
-        136668672,
-    ("scan_pipe_temporal.hip", "066ea19bbb3b339720d4545d0ff436cf74e564f2160979d0ede03be1e7cf9af4"):
-        153628224,
+    ("decode.hip", "decode B=256 H=16 Dk=Dv=128 J=4",
+     "17cda266f6fb5ff92e54ad1b1e645c9ce379946f7ede393facaad11ebd01f546"): 2184242900,
+    ("scan_pipe.hip", "forward B=4 H=8 T=2048 Dk=Dv=64 J=4",
+     "ee7a4ca4b00165323d4a9dc5846f10bf5c09e5a849802ad9e324f9631b5ab7fa"): 136726401,
+    ("scan_pipe.hip", "forward B=8 H=16 T=4096 Dk=Dv=128 J=4",
+     "ee7a4ca4b00165323d4a9dc5846f10bf5c09e5a849802ad9e324f9631b5ab7fa"): 2197260709,
+    ("scan_pipe_temporal.hip", "temporal B=4 H=8 T=2048 Dk=Dv=64 J=4",
+     "48c89ce7f844cea710a7d5e924b56a12657a6c07052831106e0ab66ba5bbc3fb"): 153644932,
+    ("scan_direct.hip", "forward B=4 H=8 T=2048 Dk=Dv=64 J=4",
+     "5de1a35dd71be1f470fe061ddb917b715329bd932696870143ce84c2a0ef94d8"): 136531576,
+    ("scan_direct.hip", "gated B=4 H=8 T=2048 Dk=Dv=64 J=4",
+     "5de1a35dd71be1f470fe061ddb917b715329bd932696870143ce84c2a0ef94d8"): 170095083,
 }
 
 
-def measured_traffic(source):
-    """Counter-measured HBM bytes per launch of the kernel in ``source``, or None
-    when that source has changed since the counters were taken."""
+def workload_key(kind, B, H, T, Dk, Dv, J):
+    """The MEASURED_TRAFFIC key of a workload: its kind and sizes."""
+    dims = "Dk=Dv=%d" % Dk if Dk == Dv else "Dk=%d Dv=%d" % (Dk, Dv)
+    if kind == "decode":
+        return "decode B=%d H=%d %s J=%d" % (B, H, dims, J)
+    return "%s B=%d H=%d T=%d %s J=%d" % (kind, B, H, T, dims, J)
+
+
+def measured_traffic(source, workload):
+    """Counter-measured HBM bytes per launch of the kernel in ``source`` on
+    ``workload`` (a ``workload_key``), or None when that source has changed since
+    the counters were taken or the workload was not measured."""
     try:
         digest = kernel_source_digest(source)
     except OSError:
         return None
-    return MEASURED_TRAFFIC.get((source, digest))
+    return MEASURED_TRAFFIC.get((source, workload, digest))
 
 
 def kernel_source_digest(source):
@@ -188,7 +204,9 @@ def bench_decode(sw, torch, workloads, steps_total, warmup):
         "steps_per_s": 1.0 / wall, "tokens_per_s": B / wall, "ms_per_step": wall * 1e3,
         "roofline": {"bound": "hbm", "achieved": nbytes / kern / 1e9, "peak": PEAK_HBM / 1e9,
                      "unit": "GB/s", "frac": nbytes / kern / PEAK_HBM,
-                     "traffic": measured_traffic("decode.hip"), "kernel": "decode_kernel",
+                     "traffic": measured_traffic("decode.hip",
+                                                 workload_key("decode", B, H, 1, Dk, Dv, J)),
+                     "kernel": "decode_kernel",
                      "kernel_ms": kern * 1e3, "alg_bytes_per_launch": nbytes},
     }
 
@@ -242,7 +260,9 @@ def bench_temporal(sw, torch, workloads, dev, cfg, seed, steps, warmup, o, s_out
         "algo": "chunk_exact" if chunk else "recurrent",
         "roofline": {"bound": "hbm", "achieved": nbytes / kern / 1e9, "peak": PEAK_HBM / 1e9,
                      "unit": "GB/s", "frac": nbytes / kern / PEAK_HBM,
-                     "traffic": measured_traffic("scan_pipe_temporal.hip") if chunk else None,
+                     "traffic": (measured_traffic("scan_pipe_temporal.hip",
+                                                  workload_key("temporal", B, H, T, Dk, Dv, J))
+                                 if chunk else None),
                      "kernel": ("scan_pipe_kernel (temporal mode)" if chunk
                                 else "scan_direct_kernel (temporal)"),
                      "kernel_ms": kern * 1e3, "alg_bytes_per_launch": nbytes},
@@ -286,7 +306,9 @@ def bench_gated(sw, torch, workloads, dev, cfg, seed, steps, warmup, o, s_out, t
         "tokens_per_s": B * T / wall, "ms_per_step": wall * 1e3, "algo": "recurrent",
         "roofline": {"bound": "alu", "achieved": nflop / kern / 1e12,
                      "peak": PEAK_VALU_F32 / 1e12, "unit": "TFLOP/s",
-                     "frac": nflop / kern / PEAK_VALU_F32, "traffic": None,
+                     "frac": nflop / kern / PEAK_VALU_F32,
+                     "traffic": measured_traffic("scan_direct.hip",
+                                                 workload_key("gated", B, H, T, Dk, Dv, J)),
                      "kernel": "scan_direct_kernel (gated)", "kernel_ms": kern * 1e3,
                      "alg_flop_per_launch": nflop, "alg_bytes_per_launch": nbytes},
     }
@@ -401,7 +423,8 @@ def main():
                    "algo": "chunk_exact" if chunk else "recurrent"},
     }
     hbm = {"bound": "hbm", "achieved": nbytes / kern / 1e9, "peak": PEAK_HBM / 1e9,
-           "unit": "GB/s", "frac": nbytes / kern / PEAK_HBM, "traffic": measured_traffic(ksrc),
+           "unit": "GB/s", "frac": nbytes / kern / PEAK_HBM,
+           "traffic": measured_traffic(ksrc, workload_key("forward", B, H, T, Dk, Dv, J)),
            "kernel": kname, "kernel_ms": kern * 1e3, "alg_bytes_per_launch": nbytes}
     alu = {"bound": "alu", "achieved": nflop / kern / 1e12, "peak": PEAK_VALU_F32 / 1e12,
            "unit": "TFLOP/s", "frac": nflop / kern / PEAK_VALU_F32, "kernel": kname,
