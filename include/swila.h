@@ -251,6 +251,42 @@ int swila_decode_step_gated(const swila_shape *shape, const swila_opts *opts,
                             const swila_temporal *temporal, const float *state_in,
                             float *state_out, void *o, void *stream);
 
+/*
+ * Backward pass of swila_forward (plain form; Sec. 3.2: eq. recurrence,
+ * eq. responsibility, eq. retrieval, with the logits of App. B.2): the exact
+ * gradient of a scalar loss L through the forward, for training.  The paper
+ * trains through the sequential evaluation and gives no backward formulas;
+ * this is the chain rule of that forward, evaluated in fp32.
+ *   q, k, v, beta_logit, prior_k_logit, prior_q_logit, state_in: the forward's
+ *              inputs, as in swila_forward (state_in NULL = zeros).
+ *   grad_o:    dL/do [B,T,H,Dv], out_dtype; required when T > 0.
+ *   grad_state_out: dL/dW_T [B,H,J,Dk,Dv] fp32, or NULL for zeros.
+ *   grad_q, grad_k: [B,T,H,Dk] fp32;  grad_v: [B,T,H,Dv] fp32;
+ *   grad_beta_logit, grad_prior_k_logit, grad_prior_q_logit: [B,T,H,J,Dv] fp32
+ *              (all six required when T > 0, overwritten).
+ *   grad_state_in: dL/dW_0 [B,H,J,Dk,Dv] fp32, or NULL to discard it.
+ *   workspace, ws_bytes: at least swila_backward_workspace_bytes bytes,
+ *              16-byte aligned; holds the recomputed errors delta and the state
+ *              every 32 tokens, and is overwritten.
+ * Every output, the workspace and the inputs are pairwise disjoint.  The
+ * algorithm field of opts is ignored: the backward recomputes the forward
+ * with the token-by-token scan.  T == 0 copies grad_state_out (or zeros) to
+ * grad_state_in.
+ */
+int swila_backward(const swila_shape *shape, const swila_opts *opts,
+                   const void *q, const void *k, const void *v,
+                   const void *beta_logit, const void *prior_k_logit,
+                   const void *prior_q_logit, const float *state_in,
+                   const void *grad_o, const float *grad_state_out,
+                   float *grad_q, float *grad_k, float *grad_v,
+                   float *grad_beta_logit, float *grad_prior_k_logit,
+                   float *grad_prior_q_logit, float *grad_state_in,
+                   void *workspace, size_t ws_bytes, void *stream);
+
+/* Workspace bytes swila_backward needs (0 if shape is NULL or invalid):
+ * 2*B*T*H*J*Dv*4 + 2*B*H*ceil(T/32)*J*Dk*Dv*4, each part rounded up to 256. */
+size_t swila_backward_workspace_bytes(const swila_shape *shape);
+
 /* Text of this thread's last error ("" if none). */
 const char *swila_last_error(void);
 

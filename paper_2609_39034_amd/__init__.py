@@ -23,7 +23,8 @@ import ctypes
 import os
 
 __all__ = ["forward", "decode_step", "forward_temporal", "decode_step_temporal",
-           "forward_gated", "decode_step_gated", "state_init", "state_bytes", "forward_workspace_bytes",
+           "forward_gated", "decode_step_gated", "backward", "backward_workspace_bytes",
+           "state_init", "state_bytes", "forward_workspace_bytes",
            "version", "library_path", "SwilaError", "F32", "BF16", "ALGO_AUTO",
            "ALGO_RECURRENT", "ALGO_CHUNK_EXACT", "ALGO_NEWTON", "FLAG_NEWTON_NO_CLAMP"]
 
@@ -106,6 +107,11 @@ def load_library():
     lib.swila_forward_gated.argtypes = [sp, op] + [vp] * 6 + [gp, tp, vp, vp, vp, vp, vp]
     lib.swila_decode_step_gated.restype = ctypes.c_int
     lib.swila_decode_step_gated.argtypes = [sp, op] + [vp] * 6 + [gp, tp, vp, vp, vp, vp]
+    lib.swila_backward_workspace_bytes.restype = ctypes.c_size_t
+    lib.swila_backward_workspace_bytes.argtypes = [sp]
+    lib.swila_backward.restype = ctypes.c_int
+    lib.swila_backward.argtypes = [sp, op] + [vp] * 6 + [vp, vp, vp] + [vp] * 7 + [
+        vp, ctypes.c_size_t, vp]
     _lib = lib
     return lib
 
@@ -267,6 +273,64 @@ def forward(q, k, v, beta_logit, prior_k_logit, prior_q_logit, state_in=None, *,
         *[_ptr(t) for t in ins], _ptr(state_in), _ptr(s_out), _ptr(o), _ptr(r),
         ws_ptr, ws_bytes, _ptr(iters_out), _stream_handle(stream)))
     return (o, s_out, r) if resp else (o, s_out)
+
+
+def backward_workspace_bytes(B, H, T, Dk, Dv, J) -> int:
+    shape = Shape(B, H, T, Dk, Dv, J)
+    return int(load_library().swila_backward_workspace_bytes(ctypes.byref(shape)))
+
+
+def backward(q, k, v, beta_logit, prior_k_logit, prior_q_logit, state_in, grad_o,
+             grad_state=None, *, grad_state_in=True, workspace=None, stream=None):
+    """Gradients of the plain forward (swila_backward).
+
+    The forward's inputs as for ``forward`` (state_in may be None), grad_o =
+    dL/do [B,T,H,Dv] (its dtype is the forward's output dtype), grad_state =
+    dL/dW_T float32 or None.  Returns (dq, dk, dv, dbeta_logit, dprior_k_logit,
+    dprior_q_logit, dstate_in), every gradient float32 (dstate_in None when
+    grad_state_in is False).  The workspace is allocated here unless given.
+    """
+    torch = _torch()
+    names = ("q", "k", "v", "beta_logit", "prior_k_logit", "prior_q_logit")
+    ins = [_dev_tensor(t, n) for t, n in zip((q, k, v, beta_logit, prior_k_logit, prior_q_logit),
+                                             names)]
+    code = _dtype_code(q)
+    for t, n in zip(ins, names):
+        if _dtype_code(t) != code:
+            raise TypeError("%s has dtype %s but q has %s" % (n, t.dtype, q.dtype))
+    B, H, T, Dk, Dv, J = _layer_shapes(q, v, beta_logit, decode=False)
+    expect = {"q": (B, T, H, Dk), "k": (B, T, H, Dk), "v": (B, T, H, Dv),
+              "beta_logit": (B, T, H, J, Dv), "prior_k_logit": (B, T, H, J, Dv),
+              "prior_q_logit": (B, T, H, J, Dv)}
+    for t, n in zip(ins, names):
+        if tuple(t.shape) != expect[n]:
+            raise ValueError("%s has shape %s, expected %s" % (n, tuple(t.shape), expect[n]))
+    _dev_tensor(state_in, "state_in", torch.float32)
+    _dev_tensor(grad_state, "grad_state", torch.float32)
+    for t, n in ((state_in, "state_in"), (grad_state, "grad_state")):
+        if t is not None and tuple(t.shape) != (B, H, J, Dk, Dv):
+            raise ValueError("%s must be [B,H,J,Dk,Dv] = %s" % (n, (B, H, J, Dk, Dv)))
+    _dev_tensor(grad_o, "grad_o")
+    if tuple(grad_o.shape) != (B, T, H, Dv):
+        raise ValueError("grad_o must be [B,T,H,Dv] = %s" % ((B, T, H, Dv),))
+    f32 = dict(device=q.device, dtype=torch.float32)
+    grads = [torch.empty((B, T, H, Dk), **f32), torch.empty((B, T, H, Dk), **f32),
+             torch.empty((B, T, H, Dv), **f32)] + [
+        torch.empty((B, T, H, J, Dv), **f32) for _ in range(3)]
+    ds = torch.empty((B, H, J, Dk, Dv), **f32) if grad_state_in else None
+    shape = Shape(B, H, T, Dk, Dv, J)
+    opts = Opts(code, _dtype_code(grad_o), _ALGOS["auto"], 0, 0, 0.0, 0)
+    lib = load_library()
+    if workspace is None:
+        workspace = torch.empty(max(1, lib.swila_backward_workspace_bytes(ctypes.byref(shape))),
+                                device=q.device, dtype=torch.uint8)
+    _dev_tensor(workspace, "workspace")
+    _check(lib.swila_backward(
+        ctypes.byref(shape), ctypes.byref(opts), *[_ptr(t) for t in ins], _ptr(state_in),
+        _ptr(grad_o), _ptr(grad_state), *[_ptr(t) for t in grads], _ptr(ds),
+        _ptr(workspace), workspace.numel() * workspace.element_size(),
+        _stream_handle(stream)))
+    return tuple(grads) + (ds,)
 
 
 def decode_step(q, k, v, beta_logit, prior_k_logit, prior_q_logit, state_in, *,

@@ -16,7 +16,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libswila.so")
 SOURCES = ["swila_api.hip", "scan_direct.hip", "scan_pipe.hip", "scan_pipe_newton.hip",
-           "scan_pipe_temporal.hip", "decode.hip"]
+           "scan_pipe_temporal.hip", "decode.hip", "scan_backward.hip"]
 ARCH = "gfx950"
 
 # Packed fp32 VALU instructions are turned off for every kernel: the compiler

@@ -25,6 +25,28 @@ struct LayerArgs {
     // Gated SwiLA (App. B.4, eq. pre-decay): decay logits [B,T,H,J,Dk] (in_bf16),
     // a = sigmoid, one gate per key dimension and component; nullptr = no decay.
     const void *decay = nullptr;
+    // Backward support (token-by-token scan only): delta_{tjd} per token
+    // ([B,T,H,J,Dv] fp32) and the state before every kBwdChunk-th token
+    // ([B,H,NCH,Dv,J,Dk] fp32, NCH = ceil(T / kBwdChunk)); nullptr = not written.
+    float *delta_out = nullptr;
+    float *ckpt = nullptr;
+};
+
+// Tokens per checkpoint interval of the backward pass.
+constexpr int kBwdChunk = 32;
+
+// Pointers and sizes of one backward call: the forward's inputs (f.o, f.resp,
+// f.state_out unused), the loss gradients of its outputs, the input gradients
+// (fp32) and the workspace.
+struct BackwardArgs {
+    LayerArgs f;
+    const void *grad_o;          // [B,T,H,Dv], bf16 when f.out_bf16
+    const float *grad_state;     // [B,H,J,Dk,Dv]; nullptr = zeros
+    float *dq, *dk, *dv;         // [B,T,H,Dk], [B,T,H,Dk], [B,T,H,Dv]
+    float *dlb, *dlk, *dlq;      // [B,T,H,J,Dv]
+    float *dstate;               // [B,H,J,Dk,Dv]; nullptr = not written
+    float *delta, *dpred;        // workspace, [B,T,H,J,Dv] each
+    float *wck, *eck;            // workspace, [B,H,NCH,Dv,J,Dk] each
 };
 
 // Parameters of the chunkwise quasi-Newton form (App. D).
@@ -51,6 +73,15 @@ hipError_t launch_scan_pipe_temporal(const LayerArgs &a, hipStream_t stream);
 // newton_workspace_bytes(...) bytes.
 hipError_t launch_newton(const LayerArgs &a, const NewtonArgs &na, hipStream_t stream);
 size_t newton_workspace_bytes(int B, int H, int T, int Dv, int J);
+
+// Token-by-token forward that writes a.delta_out and a.ckpt (both required)
+// and no output or final state: the first step of the backward pass.
+hipError_t launch_scan_direct_aux(const LayerArgs &a, hipStream_t stream);
+
+// Backward pass of the plain forward (every pointer of b set except
+// b.grad_state and b.dstate, which may be nullptr; T > 0).
+hipError_t launch_backward(const BackwardArgs &b, hipStream_t stream);
+size_t backward_workspace_bytes(int B, int H, int T, int Dk, int Dv, int J);
 
 // One-token decode step streaming the state through registers.
 hipError_t launch_decode(const LayerArgs &a, hipStream_t stream);

@@ -1,0 +1,467 @@
+// Backward pass of the plain SwiLA forward (Sec. 3.2: eq. recurrence,
+// eq. responsibility, eq. retrieval; beta and the priors from logits as in
+// App. B.2): the gradients of a loss L with respect to q, k, v, the three
+// logit tensors and the initial state, given dL/do and dL/dW_T.  The paper
+// trains through its sequential evaluation; this is the exact gradient of
+// that forward, in three launches.
+//
+// 1. Forward recompute (the token-by-token scan in its AX mode): delta_{tjd}
+//    of every token and the state W_n before every kBwdChunk-th token.
+//
+// 2. Reverse scan, one (b, h, d) column per L lanes as in the forward, with
+//    G_{jd} = dL/dw_{t,jd} in registers (each lane a key slice).  Per token,
+//    in reverse:
+//      dy_j = do pi^q_j;  G_j += dy_j q_t;  dc_j = G_j . k_t
+//      r = softmax_j(lk - delta^2/2) and beta recomputed from delta and logits
+//      dlb_j = dc_j r_j delta_j beta_j (1 - beta_j)
+//      dr_j = dc_j beta_j delta_j;  da_j = r_j (dr_j - sum_i r_i dr_i) = dlk_j
+//      ddelta_j = dc_j beta_j r_j - delta_j da_j;  dv = sum_j ddelta_j
+//      dpred_j = -ddelta_j;  G_j += dpred_j k_t          (now dL/dw_{t-1,jd})
+//    It writes dv, dlb, dlk, dpred, dL/dW_0 (G after token 0), and E_n, the
+//    part of dL/dw at the last token of chunk n that comes from later tokens.
+//
+// 3. Chunk pass, one block per (b, h, chunk of kBwdChunk tokens), no
+//    sequential dependence.  Inside chunk n, with S = W_n, columns col = (j, d)
+//    and per-(token, column) scalars C = c = beta r delta, P = dpred, Y = dy:
+//      w_t     = S + sum_{s<=t} C_s k_s,     w_{t-1} = S + sum_{s<t} C_s k_s
+//      G_t     = E_n + sum_{s>t} P_s k_s + sum_{s>=t} Y_s q_s
+//    so the two sums over columns that need the per-token state become
+//      dq_t = Y_t.S + sum_{s<=t} (Y_t.C_s) k_s
+//      dk_t = C_t.E_n + P_t.S + sum_{s>t} (C_t.P_s) k_s + sum_{s<t} (P_t.C_s) k_s
+//             + sum_{s>=t} (C_t.Y_s) q_s
+//    (X_t.Z_s = sum over columns of X_{t,col} Z_{s,col}), contractions of
+//    chunk-sized operands, and y_{tjd} = w_{t,jd} . q_t for the query-prior
+//    gradient dlq_j = pi^q_j do (y_j - sum_i pi^q_i y_i) is
+//    Q S + tril(Q K^T) C.  Column tiles of all J components of DT output dims
+//    stream through LDS; the chunk's K, Q and its Gram products stay there.
+#include "device_common.hpp"
+#include "launch.hpp"
+
+namespace swila {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kTC = 16;           // tokens staged per round of the reverse scan
+constexpr int kMaxCols = 128;
+constexpr int kCB = kBwdChunk;    // tokens per chunk of the chunk pass
+
+constexpr int rev_cols(int L, int J) {
+    int n = kThreads / L < kMaxCols ? kThreads / L : kMaxCols;
+    while (n > 16 && kTC * (4 * J + 1) * n * 4 > 65536) n /= 2;
+    return n;
+}
+
+template <int DK, int J, int S>
+__global__ __launch_bounds__(kThreads) void scan_reverse_kernel(BackwardArgs a, int ncol) {
+    constexpr int L = DK / S;             // lanes per output column
+    constexpr int NCM = rev_cols(L, J);
+    constexpr int SP = S + 4;
+
+    __shared__ __align__(16) float sK[kTC][L][SP];
+    __shared__ __align__(16) float sQ[kTC][L][SP];
+    __shared__ float sDo[kTC][NCM];
+    __shared__ float sDelta[kTC][J][NCM];
+    __shared__ float sBeta[kTC][J][NCM];
+    __shared__ float sLk[kTC][J][NCM];
+    __shared__ float sPq[kTC][J][NCM];
+
+    const LayerArgs &f = a.f;
+    const int tid = threadIdx.x;
+    const int nthr = ncol * L;
+    const int dl = tid / L, l = tid % L;
+    const int d0 = blockIdx.x * ncol;
+    const int h = blockIdx.y, b = blockIdx.z;
+    const int H = f.H, T = f.T, Dv = f.Dv;
+    const int d = d0 + dl;
+    const bool ibf = f.in_bf16, obf = f.out_bf16;
+    const int NCH = (T + kCB - 1) / kCB;
+
+    float G[J][S];
+    const size_t sbase = ((size_t)b * H + h) * J * DK * Dv;
+#pragma unroll
+    for (int j = 0; j < J; ++j)
+#pragma unroll
+        for (int s = 0; s < S; ++s)
+            G[j][s] = a.grad_state ? a.grad_state[sbase + ((size_t)j * DK + l * S + s) * Dv + d]
+                                   : 0.0f;
+
+    const int nr = (T + kTC - 1) / kTC;
+    for (int rr = nr - 1; rr >= 0; --rr) {
+        const int t0 = rr * kTC;
+        const int nt = min(kTC, T - t0);
+        __syncthreads();
+        for (int g = tid; g < nt * (DK / 4); g += nthr) {
+            const int tt = g / (DK / 4), i = (g % (DK / 4)) * 4;
+            const size_t off = ((size_t)(b * T + t0 + tt) * H + h) * DK + i;
+            *reinterpret_cast<float4 *>(&sK[tt][i / S][i % S]) = load4(f.k, off, ibf);
+            *reinterpret_cast<float4 *>(&sQ[tt][i / S][i % S]) = load4(f.q, off, ibf);
+        }
+        for (int g = tid; g < nt * ncol; g += nthr) {
+            const int tt = g / ncol, c = g % ncol;
+            const size_t row = (size_t)(b * T + t0 + tt) * H + h;
+            sDo[tt][c] = load1(a.grad_o, row * Dv + d0 + c, obf);
+            float lq[J];
+            float m = -INFINITY;
+#pragma unroll
+            for (int j = 0; j < J; ++j) {
+                const size_t idx = (row * J + j) * Dv + d0 + c;
+                sDelta[tt][j][c] = a.delta[idx];
+                sBeta[tt][j][c] = 1.0f / (1.0f + exp_fast(-load1(f.lb, idx, ibf)));
+                sLk[tt][j][c] = load1(f.lk, idx, ibf);
+                lq[j] = load1(f.lq, idx, ibf);
+                m = fmaxf(m, lq[j]);
+            }
+            float z = 0.0f;
+#pragma unroll
+            for (int j = 0; j < J; ++j) {
+                lq[j] = exp_fast(lq[j] - m);
+                z += lq[j];
+            }
+            const float iz = 1.0f / z;
+#pragma unroll
+            for (int j = 0; j < J; ++j) sPq[tt][j][c] = lq[j] * iz;
+        }
+        __syncthreads();
+
+        for (int tt = nt - 1; tt >= 0; --tt) {
+            const int t = t0 + tt;
+            if (t % kCB == kCB - 1 || t == T - 1) {
+                // E_n: dL/dw_t from the tokens after t (the last token of chunk n)
+                float *ck = a.eck + ((((size_t)b * H + h) * NCH + t / kCB) * Dv + d) * J * DK;
+#pragma unroll
+                for (int j = 0; j < J; ++j)
+#pragma unroll
+                    for (int s = 0; s < S; s += 4)
+                        *reinterpret_cast<float4 *>(ck + j * DK + l * S + s) =
+                            make_float4(G[j][s], G[j][s + 1], G[j][s + 2], G[j][s + 3]);
+            }
+            float kv[S], qv[S];
+#pragma unroll
+            for (int s = 0; s < S; s += 4) {
+                const float4 x = *reinterpret_cast<const float4 *>(&sK[tt][l][s]);
+                const float4 y = *reinterpret_cast<const float4 *>(&sQ[tt][l][s]);
+                kv[s] = x.x; kv[s + 1] = x.y; kv[s + 2] = x.z; kv[s + 3] = x.w;
+                qv[s] = y.x; qv[s + 1] = y.y; qv[s + 2] = y.z; qv[s + 3] = y.w;
+            }
+            const float dov = sDo[tt][dl];
+            // retrieval: o = sum_j pi^q_j w_{t,j} . q_t adds dy_j q_t to G_j
+            float dc[J];
+#pragma unroll
+            for (int j = 0; j < J; ++j) {
+                const float dy = dov * sPq[tt][j][dl];
+                float acc = 0.0f;
+#pragma unroll
+                for (int s = 0; s < S; ++s) {
+                    G[j][s] = fmaf(dy, qv[s], G[j][s]);
+                    acc = fmaf(G[j][s], kv[s], acc);
+                }
+                dc[j] = acc;
+            }
+#pragma unroll
+            for (int j = 0; j < J; ++j) dc[j] = group_sum<L>(dc[j]);
+
+            // r of token t from its errors, as in the forward
+            float delta[J], e[J];
+            float m = -INFINITY;
+#pragma unroll
+            for (int j = 0; j < J; ++j) {
+                delta[j] = sDelta[tt][j][dl];
+                e[j] = sLk[tt][j][dl] - 0.5f * delta[j] * delta[j];
+                m = fmaxf(m, e[j]);
+            }
+            float z = 0.0f;
+#pragma unroll
+            for (int j = 0; j < J; ++j) {
+                e[j] = exp_fast(e[j] - m);
+                z += e[j];
+            }
+            const float iz = 1.0f / z;
+            float r[J], dr[J];
+            float sdr = 0.0f;
+#pragma unroll
+            for (int j = 0; j < J; ++j) {
+                r[j] = J == 1 ? 1.0f : e[j] * iz;
+                dr[j] = dc[j] * sBeta[tt][j][dl] * delta[j];
+                sdr = fmaf(r[j], dr[j], sdr);
+            }
+            const size_t row = (size_t)(b * T + t) * H + h;
+            float dvv = 0.0f;
+#pragma unroll
+            for (int j = 0; j < J; ++j) {
+                const float beta = sBeta[tt][j][dl];
+                // (J = 1: a softmax over one component is constant; written as
+                // 0 because the contracted dr - sum r dr leaves a rounding residue)
+                const float da = J == 1 ? 0.0f : r[j] * (dr[j] - sdr);
+                const float ddelta = dc[j] * beta * r[j] - delta[j] * da;
+                dvv += ddelta;
+                const float dpred = -ddelta;
+#pragma unroll
+                for (int s = 0; s < S; ++s) G[j][s] = fmaf(dpred, kv[s], G[j][s]);
+                if (l == 0) {
+                    const size_t idx = (row * J + j) * Dv + d;
+                    a.dlb[idx] = dc[j] * r[j] * delta[j] * beta * (1.0f - beta);
+                    a.dlk[idx] = da;
+                    a.dpred[idx] = dpred;
+                }
+            }
+            if (l == 0) a.dv[row * Dv + d] = dvv;
+        }
+    }
+    if (a.dstate) {
+#pragma unroll
+        for (int j = 0; j < J; ++j)
+#pragma unroll
+            for (int s = 0; s < S; ++s)
+                a.dstate[sbase + ((size_t)j * DK + l * S + s) * Dv + d] = G[j][s];
+    }
+}
+
+template <int DK, int J>
+__global__ __launch_bounds__(kThreads) void bwd_chunk_kernel(BackwardArgs a) {
+    constexpr int DT = J == 3 ? 4 : 16 / J;   // output dims per column tile
+    constexpr int NCT = J * DT;               // columns per tile, all J of each dim
+    constexpr int KP = DK + 1, CP = NCT + 1, GP = kCB + 1;
+    constexpr int NE = kCB * DK / kThreads;   // (token, key index) entries per thread
+    constexpr int NG = kCB * kCB / kThreads;  // Gram entries per thread
+    static_assert(NE >= 1 && NG >= 1 && kCB * DK % kThreads == 0, "tile sizes");
+
+    __shared__ float sK[kCB][KP], sQ[kCB][KP];
+    __shared__ float sQK[kCB][GP], sA[kCB][GP], sB[kCB][GP];
+    __shared__ float sS[NCT][KP], sE[NCT][KP];
+    __shared__ float sC[kCB][CP], sP[kCB][CP], sY[kCB][CP], sPq[kCB][CP], sYv[kCB][CP];
+    __shared__ float sDo[kCB][DT];
+
+    const LayerArgs &f = a.f;
+    const int n = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+    const int tid = threadIdx.x;
+    const int H = f.H, T = f.T, Dv = f.Dv;
+    const int NCH = (T + kCB - 1) / kCB;
+    const int t0 = n * kCB, nt = min(kCB, T - t0);
+    const bool ibf = f.in_bf16, obf = f.out_bf16;
+
+    for (int g = tid; g < kCB * DK; g += kThreads) {
+        const int t = g / DK, i = g % DK;
+        float kv = 0.0f, qv = 0.0f;
+        if (t < nt) {
+            const size_t off = ((size_t)(b * T + t0 + t) * H + h) * DK + i;
+            kv = load1(f.k, off, ibf);
+            qv = load1(f.q, off, ibf);
+        }
+        sK[t][i] = kv;
+        sQ[t][i] = qv;
+    }
+    __syncthreads();
+    for (int g = tid; g < kCB * kCB; g += kThreads) {
+        const int t = g / kCB, s = g % kCB;
+        float acc = 0.0f;
+#pragma unroll 8
+        for (int i = 0; i < DK; ++i) acc = fmaf(sQ[t][i], sK[s][i], acc);
+        sQK[t][s] = acc;
+    }
+
+    float dq[NE], dk[NE], ga[NG], gb[NG];
+#pragma unroll
+    for (int m = 0; m < NE; ++m) dq[m] = dk[m] = 0.0f;
+#pragma unroll
+    for (int m = 0; m < NG; ++m) ga[m] = gb[m] = 0.0f;
+
+    // checkpoints of this chunk, [Dv][J][DK]
+    const size_t ck0 = (((size_t)b * H + h) * NCH + n) * Dv * J * DK;
+    for (int dt0 = 0; dt0 < Dv; dt0 += DT) {
+        __syncthreads();   // the previous tile is consumed (first pass: Q K^T is done)
+        for (int g = tid; g < DT * J * DK; g += kThreads) {
+            const int dd = g / (J * DK), j = (g / DK) % J, i = g % DK;
+            const size_t src = ck0 + (size_t)dt0 * J * DK + g;
+            sS[j * DT + dd][i] = a.wck[src];
+            sE[j * DT + dd][i] = a.eck[src];
+        }
+        for (int g = tid; g < kCB * DT; g += kThreads) {
+            const int t = g / DT, dd = g % DT;
+            if (t < nt) {
+                const size_t row = (size_t)(b * T + t0 + t) * H + h;
+                const float dov = load1(a.grad_o, row * Dv + dt0 + dd, obf);
+                float delta[J], e[J], lq[J];
+                float m = -INFINITY, mq = -INFINITY;
+#pragma unroll
+                for (int j = 0; j < J; ++j) {
+                    const size_t idx = (row * J + j) * Dv + dt0 + dd;
+                    delta[j] = a.delta[idx];
+                    e[j] = load1(f.lk, idx, ibf) - 0.5f * delta[j] * delta[j];
+                    lq[j] = load1(f.lq, idx, ibf);
+                    m = fmaxf(m, e[j]);
+                    mq = fmaxf(mq, lq[j]);
+                }
+                float z = 0.0f, zq = 0.0f;
+#pragma unroll
+                for (int j = 0; j < J; ++j) {
+                    e[j] = exp_fast(e[j] - m);
+                    z += e[j];
+                    lq[j] = exp_fast(lq[j] - mq);
+                    zq += lq[j];
+                }
+                const float iz = 1.0f / z, izq = 1.0f / zq;
+#pragma unroll
+                for (int j = 0; j < J; ++j) {
+                    const size_t idx = (row * J + j) * Dv + dt0 + dd;
+                    const float beta = 1.0f / (1.0f + exp_fast(-load1(f.lb, idx, ibf)));
+                    const float pq = J == 1 ? 1.0f : lq[j] * izq;
+                    sC[t][j * DT + dd] = beta * (J == 1 ? 1.0f : e[j] * iz) * delta[j];
+                    sP[t][j * DT + dd] = a.dpred[idx];
+                    sPq[t][j * DT + dd] = pq;
+                    sY[t][j * DT + dd] = dov * pq;
+                }
+                sDo[t][dd] = dov;
+            } else {
+#pragma unroll
+                for (int j = 0; j < J; ++j) {
+                    sC[t][j * DT + dd] = 0.0f;
+                    sP[t][j * DT + dd] = 0.0f;
+                    sPq[t][j * DT + dd] = 0.0f;
+                    sY[t][j * DT + dd] = 0.0f;
+                }
+                sDo[t][dd] = 0.0f;
+            }
+        }
+        __syncthreads();
+
+        // Y S into dq; P S + C E into dk
+#pragma unroll
+        for (int m = 0; m < NE; ++m) {
+            const int e = tid + kThreads * m, t = e / DK, i = e % DK;
+            float aq = dq[m], ak = dk[m];
+#pragma unroll
+            for (int cc = 0; cc < NCT; ++cc) {
+                const float sv = sS[cc][i];
+                aq = fmaf(sY[t][cc], sv, aq);
+                ak = fmaf(sP[t][cc], sv, ak);
+                ak = fmaf(sC[t][cc], sE[cc][i], ak);
+            }
+            dq[m] = aq;
+            dk[m] = ak;
+        }
+        // Gram products over the columns: ga[t][s] = Y_t.C_s, gb[t][s] = C_t.P_s
+#pragma unroll
+        for (int m = 0; m < NG; ++m) {
+            const int e = tid + kThreads * m, t = e / kCB, s = e % kCB;
+            float x = ga[m], y = gb[m];
+#pragma unroll
+            for (int cc = 0; cc < NCT; ++cc) {
+                x = fmaf(sY[t][cc], sC[s][cc], x);
+                y = fmaf(sC[t][cc], sP[s][cc], y);
+            }
+            ga[m] = x;
+            gb[m] = y;
+        }
+        // y_t = w_t . q_t = S q_t + sum_{s<=t} (q_t . k_s) C_s
+        for (int g = tid; g < kCB * NCT; g += kThreads) {
+            const int t = g / NCT, cc = g % NCT;
+            float acc = 0.0f;
+#pragma unroll 8
+            for (int i = 0; i < DK; ++i) acc = fmaf(sQ[t][i], sS[cc][i], acc);
+            for (int s = 0; s <= t; ++s) acc = fmaf(sQK[t][s], sC[s][cc], acc);
+            sYv[t][cc] = acc;
+        }
+        __syncthreads();
+        for (int g = tid; g < nt * DT; g += kThreads) {
+            const int t = g / DT, dd = g % DT;
+            const float dov = sDo[t][dd];
+            float mean = 0.0f;
+#pragma unroll
+            for (int j = 0; j < J; ++j) mean = fmaf(sPq[t][j * DT + dd], sYv[t][j * DT + dd], mean);
+            const size_t row = (size_t)(b * T + t0 + t) * H + h;
+#pragma unroll
+            for (int j = 0; j < J; ++j)
+                a.dlq[(row * J + j) * Dv + dt0 + dd] =
+                    J == 1 ? 0.0f : sPq[t][j * DT + dd] * dov * (sYv[t][j * DT + dd] - mean);
+        }
+    }
+
+    // the intra-chunk terms
+#pragma unroll
+    for (int m = 0; m < NG; ++m) {
+        const int e = tid + kThreads * m, t = e / kCB, s = e % kCB;
+        sA[t][s] = ga[m];
+        sB[t][s] = gb[m];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int m = 0; m < NE; ++m) {
+        const int e = tid + kThreads * m, t = e / DK, i = e % DK;
+        if (t >= nt) continue;
+        float aq = dq[m], ak = dk[m];
+        for (int s = 0; s < kCB; ++s) {
+            const float kv = sK[s][i], qv = sQ[s][i];
+            if (s <= t) aq = fmaf(sA[t][s], kv, aq);   // (Y_t . C_s) k_s
+            if (s > t) ak = fmaf(sB[t][s], kv, ak);    // (C_t . P_s) k_s
+            if (s < t) ak = fmaf(sB[s][t], kv, ak);    // (P_t . C_s) k_s
+            if (s >= t) ak = fmaf(sA[s][t], qv, ak);   // (C_t . Y_s) q_s
+        }
+        const size_t off = ((size_t)(b * T + t0 + t) * H + h) * DK + i;
+        a.dq[off] = aq;
+        a.dk[off] = ak;
+    }
+}
+
+template <int DK, int J>
+hipError_t launch_bwd_dk_j(const BackwardArgs &a, hipStream_t stream) {
+    constexpr int S = (J <= 4) ? (DK < 16 ? DK : 16) : (DK < 8 ? DK : 8);
+    constexpr int L = DK / S;
+    const LayerArgs &f = a.f;
+    LayerArgs fa = f;
+    fa.o = nullptr;
+    fa.state_out = nullptr;
+    fa.resp = nullptr;
+    fa.delta_out = a.delta;
+    fa.ckpt = a.wck;
+    hipError_t e = launch_scan_direct_aux(fa, stream);
+    if (e != hipSuccess) return e;
+    const int ncol = f.Dv < rev_cols(L, J) ? f.Dv : rev_cols(L, J);
+    hipLaunchKernelGGL((scan_reverse_kernel<DK, J, S>), dim3(f.Dv / ncol, f.H, f.B),
+                       dim3(ncol * L), 0, stream, a, ncol);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int NCH = (f.T + kCB - 1) / kCB;
+    hipLaunchKernelGGL((bwd_chunk_kernel<DK, J>), dim3(NCH, f.H, f.B), dim3(kThreads), 0, stream,
+                       a);
+    return hipGetLastError();
+}
+
+template <int DK>
+hipError_t launch_bwd_dk(const BackwardArgs &a, hipStream_t stream) {
+    switch (a.f.J) {
+        case 1: return launch_bwd_dk_j<DK, 1>(a, stream);
+        case 2: return launch_bwd_dk_j<DK, 2>(a, stream);
+        case 3: return launch_bwd_dk_j<DK, 3>(a, stream);
+        case 4: return launch_bwd_dk_j<DK, 4>(a, stream);
+        case 8: return launch_bwd_dk_j<DK, 8>(a, stream);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace
+
+size_t backward_workspace_bytes(int B, int H, int T, int Dk, int Dv, int J) {
+    const size_t nch = ((size_t)T + kCB - 1) / kCB;
+    const size_t per_tok = (size_t)B * T * H * J * Dv * sizeof(float);
+    const size_t ck = (size_t)B * H * nch * Dv * J * Dk * sizeof(float);
+    auto up = [](size_t x) { return (x + 255) / 256 * 256; };
+    return 2 * up(per_tok) + 2 * up(ck);
+}
+
+hipError_t launch_backward(const BackwardArgs &a, hipStream_t stream) {
+    const LayerArgs &f = a.f;
+    if (f.T < 1 || f.gk || f.decay || !a.grad_o || !a.dq || !a.dk || !a.dv || !a.dlb || !a.dlk ||
+        !a.dlq || !a.delta || !a.dpred || !a.wck || !a.eck)
+        return hipErrorInvalidValue;
+    if ((f.Dv / (f.J == 3 ? 4 : 16 / f.J)) * (f.J == 3 ? 4 : 16 / f.J) != f.Dv)
+        return hipErrorInvalidValue;
+    switch (f.Dk) {
+        case 16: return launch_bwd_dk<16>(a, stream);
+        case 32: return launch_bwd_dk<32>(a, stream);
+        case 64: return launch_bwd_dk<64>(a, stream);
+        case 128: return launch_bwd_dk<128>(a, stream);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace swila

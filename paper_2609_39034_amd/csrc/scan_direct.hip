@@ -32,6 +32,10 @@
 // key dimension, and the prediction, E-step, update and retrieval then use the
 // decayed state.  The gates of a token round are formed once, in fp32, into
 // LDS ([token][j][key index], each lane reading its slice).
+//
+// Backward support (AX): the same plain scan writes delta_{tjd} of every token
+// and the state before every kBwdChunk-th token (layout [.., chunk, d, j, i], so
+// that each lane stores its key slice contiguously), and no output.
 #include "device_common.hpp"
 #include "launch.hpp"
 
@@ -50,8 +54,9 @@ constexpr int max_cols(int L, int J, bool tp) {
     return n;
 }
 
-template <int DK, int J, int S, bool TP, bool GT>
+template <int DK, int J, int S, bool TP, bool GT, bool AX>
 __global__ __launch_bounds__(kThreads) void scan_direct_kernel(LayerArgs a, int ncol) {
+    static_assert(kBwdChunk % kTC == 0, "checkpoints fall on round starts");
     constexpr int L = DK / S;             // lanes per output column
     constexpr int NCM = max_cols(L, J, TP);
     constexpr int SP = S + 4;             // padded slice stride in LDS
@@ -95,8 +100,20 @@ __global__ __launch_bounds__(kThreads) void scan_direct_kernel(LayerArgs a, int 
 
     for (int t0 = 0; t0 < T; t0 += kTC) {
         const int nt = min(kTC, T - t0);
+        if constexpr (AX) {
+            if (t0 % kBwdChunk == 0) {   // the state before token t0
+                const int NCH = (T + kBwdChunk - 1) / kBwdChunk;
+                float *ck = a.ckpt + ((((size_t)b * H + h) * NCH + t0 / kBwdChunk) * Dv + d) * J * DK;
+#pragma unroll
+                for (int j = 0; j < J; ++j)
+#pragma unroll
+                    for (int s = 0; s < S; s += 4)
+                        *reinterpret_cast<float4 *>(ck + j * DK + l * S + s) =
+                            make_float4(w[j][s], w[j][s + 1], w[j][s + 2], w[j][s + 3]);
+            }
+        }
         __syncthreads();
-        if (t0 > 0) {  // outputs of the previous (full) round
+        if (!AX && t0 > 0) {  // outputs of the previous (full) round
             for (int g = tid; g < kTC * ncol; g += nthr) {
                 const int tt = g / ncol, c = g % ncol;
                 store1(a.o, ((size_t)(b * T + t0 - kTC + tt) * H + h) * Dv + d0 + c, sO[tt][c], obf);
@@ -232,13 +249,15 @@ __global__ __launch_bounds__(kThreads) void scan_direct_kernel(LayerArgs a, int 
                 o = fmaf(pq, fmaf(c, kq, y[j]), o);
                 if (a.resp && l == 0)
                     a.resp[(((size_t)(b * T + t0 + tt) * H + h) * J + j) * Dv + d] = r;
+                if (AX && l == 0)
+                    a.delta_out[(((size_t)(b * T + t0 + tt) * H + h) * J + j) * Dv + d] = delta[j];
             }
             if (l == 0) sO[tt][dl] = o;
         }
     }
 
     __syncthreads();
-    if (T > 0) {
+    if (!AX && T > 0) {
         const int tl = ((T - 1) / kTC) * kTC;
         const int nt = T - tl;
         for (int g = tid; g < nt * ncol; g += nthr) {
@@ -264,14 +283,14 @@ __global__ __launch_bounds__(kThreads) void scan_direct_kernel(LayerArgs a, int 
     }
 }
 
-template <int DK, int J, bool TP, bool GT>
+template <int DK, int J, bool TP, bool GT, bool AX = false>
 hipError_t launch_dk_j_tp(const LayerArgs &a, hipStream_t stream) {
     constexpr int S = (J <= 4) ? (DK < 16 ? DK : 16) : (DK < 8 ? DK : 8);
     constexpr int L = DK / S;
     const int ncol = a.Dv < max_cols(L, J, TP) ? a.Dv : max_cols(L, J, TP);
     dim3 grid(a.Dv / ncol, a.H, a.B);
     dim3 block(ncol * L);
-    hipLaunchKernelGGL((scan_direct_kernel<DK, J, S, TP, GT>), grid, block, 0, stream, a, ncol);
+    hipLaunchKernelGGL((scan_direct_kernel<DK, J, S, TP, GT, AX>), grid, block, 0, stream, a, ncol);
     return hipGetLastError();
 }
 
@@ -296,6 +315,18 @@ hipError_t launch_dk(const LayerArgs &a, hipStream_t stream) {
     }
 }
 
+template <int DK>
+hipError_t launch_aux_dk(const LayerArgs &a, hipStream_t stream) {
+    switch (a.J) {
+        case 1: return launch_dk_j_tp<DK, 1, false, false, true>(a, stream);
+        case 2: return launch_dk_j_tp<DK, 2, false, false, true>(a, stream);
+        case 3: return launch_dk_j_tp<DK, 3, false, false, true>(a, stream);
+        case 4: return launch_dk_j_tp<DK, 4, false, false, true>(a, stream);
+        case 8: return launch_dk_j_tp<DK, 8, false, false, true>(a, stream);
+        default: return hipErrorInvalidValue;
+    }
+}
+
 }  // namespace
 
 hipError_t launch_scan_direct(const LayerArgs &a, hipStream_t stream) {
@@ -304,6 +335,17 @@ hipError_t launch_scan_direct(const LayerArgs &a, hipStream_t stream) {
         case 32: return launch_dk<32>(a, stream);
         case 64: return launch_dk<64>(a, stream);
         case 128: return launch_dk<128>(a, stream);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+hipError_t launch_scan_direct_aux(const LayerArgs &a, hipStream_t stream) {
+    if (!a.delta_out || !a.ckpt || a.gk || a.decay) return hipErrorInvalidValue;
+    switch (a.Dk) {
+        case 16: return launch_aux_dk<16>(a, stream);
+        case 32: return launch_aux_dk<32>(a, stream);
+        case 64: return launch_aux_dk<64>(a, stream);
+        case 128: return launch_aux_dk<128>(a, stream);
         default: return hipErrorInvalidValue;
     }
 }

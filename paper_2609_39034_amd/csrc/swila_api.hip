@@ -438,4 +438,96 @@ int swila_decode_step(const swila_shape *shape, const swila_opts *opts, const vo
     return map_hip(swila::launch_decode(a, static_cast<hipStream_t>(stream)), "decode launch");
 }
 
+size_t swila_backward_workspace_bytes(const swila_shape *s) {
+    if (!s || s->B < 1 || s->H < 1 || s->T < 0 || s->Dk < 1 || s->Dv < 1 || s->J < 1) return 0;
+    return swila::backward_workspace_bytes(s->B, s->H, s->T, s->Dk, s->Dv, s->J);
+}
+
+int swila_backward(const swila_shape *shape, const swila_opts *opts, const void *q,
+                   const void *k, const void *v, const void *beta_logit,
+                   const void *prior_k_logit, const void *prior_q_logit, const float *state_in,
+                   const void *grad_o, const float *grad_state_out, float *grad_q, float *grad_k,
+                   float *grad_v, float *grad_beta_logit, float *grad_prior_k_logit,
+                   float *grad_prior_q_logit, float *grad_state_in, void *workspace,
+                   size_t ws_bytes, void *stream) {
+    clear_error();
+    int rc = check_shape(shape, false);
+    if (rc) return rc;
+    rc = check_opts(opts);
+    if (rc) return rc;
+    const size_t B = shape->B, H = shape->H, T = shape->T, Dk = shape->Dk, Dv = shape->Dv,
+                 J = shape->J;
+    const size_t ie = opts->in_dtype == SWILA_BF16 ? 2 : 4;
+    const size_t oe = opts->out_dtype == SWILA_BF16 ? 2 : 4;
+    const bool need = T > 0;
+    const size_t nst = B * H * J * Dk * Dv * 4;
+    const Span in[] = {
+        {"q", q, B * T * H * Dk * ie},          {"k", k, B * T * H * Dk * ie},
+        {"v", v, B * T * H * Dv * ie},          {"beta_logit", beta_logit, B * T * H * J * Dv * ie},
+        {"prior_k_logit", prior_k_logit, B * T * H * J * Dv * ie},
+        {"prior_q_logit", prior_q_logit, B * T * H * J * Dv * ie},
+        {"grad_o", grad_o, B * T * H * Dv * oe},
+        {"state_in", state_in, nst},
+        {"grad_state_out", grad_state_out, nst},
+    };
+    for (int i = 0; i < 9; ++i) {
+        rc = check_ptr(in[i], need && i < 7);   // the two states may be NULL (zeros)
+        if (rc) return rc;
+    }
+    const size_t need_ws = swila_backward_workspace_bytes(shape);
+    const Span outs[] = {
+        {"grad_q", grad_q, B * T * H * Dk * 4},
+        {"grad_k", grad_k, B * T * H * Dk * 4},
+        {"grad_v", grad_v, B * T * H * Dv * 4},
+        {"grad_beta_logit", grad_beta_logit, B * T * H * J * Dv * 4},
+        {"grad_prior_k_logit", grad_prior_k_logit, B * T * H * J * Dv * 4},
+        {"grad_prior_q_logit", grad_prior_q_logit, B * T * H * J * Dv * 4},
+        {"grad_state_in", grad_state_in, nst},
+        {"workspace", workspace, need_ws},
+    };
+    const int n_out = sizeof outs / sizeof outs[0];
+    for (int x = 0; x < n_out; ++x) {
+        rc = check_ptr(outs[x], need && x != 6);   // grad_state_in may be NULL
+        if (rc) return rc;
+        for (int i = 0; i < 9; ++i)
+            if (overlap(outs[x], in[i]))
+                return fail(SWILA_EINVAL, "%s overlaps %s", outs[x].name, in[i].name);
+        for (int y = 0; y < x; ++y)
+            if (overlap(outs[x], outs[y]))
+                return fail(SWILA_EINVAL, "%s overlaps %s", outs[x].name, outs[y].name);
+    }
+    if (need && ws_bytes < need_ws)
+        return fail(SWILA_EINVAL, "workspace holds %zu bytes, %zu needed", ws_bytes, need_ws);
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    if (T == 0) {
+        if (!grad_state_in) return SWILA_OK;
+        return map_hip(swila::launch_state_fill(grad_state_in, grad_state_out, nst / 4, st),
+                       "state copy");
+    }
+    // workspace: delta, dpred ([B,T,H,J,Dv]); state checkpoints W_n, E_n
+    const size_t nch = (T + swila::kBwdChunk - 1) / swila::kBwdChunk;
+    auto up = [](size_t x) { return (x + 255) / 256 * 256; };
+    char *ws = static_cast<char *>(workspace);
+    const size_t per_tok = up(B * T * H * J * Dv * 4), ck = up(B * H * nch * Dv * J * Dk * 4);
+    swila::BackwardArgs ba;
+    ba.f = swila::LayerArgs{q, k, v, beta_logit, prior_k_logit, prior_q_logit, state_in,
+                            nullptr, nullptr, nullptr, shape->B, shape->H, shape->T,
+                            shape->Dk, shape->Dv, shape->J,
+                            opts->in_dtype == SWILA_BF16, opts->out_dtype == SWILA_BF16};
+    ba.grad_o = grad_o;
+    ba.grad_state = grad_state_out;
+    ba.dq = grad_q;
+    ba.dk = grad_k;
+    ba.dv = grad_v;
+    ba.dlb = grad_beta_logit;
+    ba.dlk = grad_prior_k_logit;
+    ba.dlq = grad_prior_q_logit;
+    ba.dstate = grad_state_in;
+    ba.delta = reinterpret_cast<float *>(ws);
+    ba.dpred = reinterpret_cast<float *>(ws + per_tok);
+    ba.wck = reinterpret_cast<float *>(ws + 2 * per_tok);
+    ba.eck = reinterpret_cast<float *>(ws + 2 * per_tok + ck);
+    return map_hip(swila::launch_backward(ba, st), "backward launch");
+}
+
 }  // extern "C"

@@ -238,3 +238,51 @@ def test_gated_argument_checks(lib):
     # temporal arguments are checked too when given
     rc, msg = call(sw.Gated(dec), tp=sw.Temporal(None, 1 << 32, None, None))
     assert rc == sw.EINVAL and msg == "gate_k_logit is NULL"
+
+
+def test_backward_argument_checks(lib):
+    B, H, T, D, J = 1, 2, 40, 64, 4
+    shape = sw.Shape(B, H, T, D, D, J)
+    need = lib.swila_backward_workspace_bytes(ctypes.byref(shape))
+    per_tok, ck = B * T * H * J * D * 4, B * H * 2 * D * J * D * 4    # ceil(40 / 32) = 2
+    assert need == 2 * ((per_tok + 255) // 256 * 256) + 2 * ((ck + 255) // 256 * 256)
+    assert lib.swila_backward_workspace_bytes(None) == 0
+    ins = [ctypes.c_void_p((1 << 20) + (i << 26)) for i in range(6)]
+    go = ctypes.c_void_p(1 << 33)
+    outs = [ctypes.c_void_p((1 << 34) + (i << 26)) for i in range(6)]
+    ws = ctypes.c_void_p(1 << 36)
+
+    def call(ins=ins, go=go, outs=outs, dstate=None, ws=ws, ws_n=need, shape=shape, sin=None):
+        rc = lib.swila_backward(ctypes.byref(shape), ctypes.byref(OPTS), *ins, sin, go, None,
+                                *outs, dstate, ws, ws_n, None)
+        return rc, lib.swila_last_error().decode()
+
+    for i, name in enumerate(("q", "k", "v", "beta_logit", "prior_k_logit", "prior_q_logit")):
+        bad = list(ins)
+        bad[i] = None
+        assert call(ins=bad) == (sw.EINVAL, "%s is NULL" % name)
+    assert call(go=None) == (sw.EINVAL, "grad_o is NULL")
+    for i, name in enumerate(("grad_q", "grad_k", "grad_v", "grad_beta_logit",
+                              "grad_prior_k_logit", "grad_prior_q_logit")):
+        bad = list(outs)
+        bad[i] = None
+        assert call(outs=bad) == (sw.EINVAL, "%s is NULL" % name)
+    assert call(ws=None) == (sw.EINVAL, "workspace is NULL")
+    rc, msg = call(ws_n=need - 4)
+    assert rc == sw.EINVAL and "needed" in msg
+    rc, msg = call(ws=ctypes.c_void_p(ws.value + 8))
+    assert rc == sw.EINVAL and "workspace is not 16-byte aligned" in msg
+    bad = list(outs)
+    bad[1] = ctypes.c_void_p(ins[2].value + 64)
+    rc, msg = call(outs=bad)
+    assert rc == sw.EINVAL and "grad_k overlaps v" in msg
+    bad = list(outs)
+    bad[4] = ctypes.c_void_p(outs[3].value + 256)
+    rc, msg = call(outs=bad)
+    assert rc == sw.EINVAL and "grad_prior_k_logit overlaps grad_beta_logit" in msg
+    rc, msg = call(ws=ctypes.c_void_p(outs[0].value))
+    assert rc == sw.EINVAL and "workspace overlaps grad_q" in msg
+    rc, msg = call(dstate=ctypes.c_void_p(go.value + 16))
+    assert rc == sw.EINVAL and "grad_state_in overlaps grad_o" in msg
+    rc, msg = call(shape=sw.Shape(B, H, T, 48, 64, J))
+    assert rc == sw.EUNSUPPORTED
