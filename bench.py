@@ -5,9 +5,11 @@
 A step is one swila_forward call over the whole batch of the small
 training-shaped workload (B=4, H=8, T=2048, Dk=Dv=64, J=4, bf16 inputs, fp32
 state), inputs resident in HBM.  value = B*T / seconds per step (tokens/s).
-The same run also times the batched decode workload (B=256, H=16, D=128, J=4,
-512 one-token steps, state updated in place) and reports it under "decode",
-and times the fp64 oracle on the host cores ("cpu_baseline").
+The same run also times the temporal, gated and App. D Newton forms and the
+backward pass on that batch ("temporal", "gated", "newton", "backward"), the
+batched decode workload (B=256, H=16, D=128, J=4, 512 one-token steps, state
+updated in place) under "decode", and the fp64 oracle on the host cores
+("cpu_baseline").
 
 Prints one JSON line.
 """
@@ -269,6 +271,69 @@ def bench_temporal(sw, torch, workloads, dev, cfg, seed, steps, warmup, o, s_out
     }
 
 
+def backward_alg_flops(B, H, T, Dk, Dv, J):
+    """Multiply-adds of the gradient per token, head, component and output dim,
+    each Dk long: the forward's three (the state and errors are recomputed), the
+    reverse recurrence's three (dy q and dpred k into dL/dw, dc = dL/dw . k), the
+    query and key gradients' three (dy . w_t, c . dL/dw, dpred . w_{t-1}) and the
+    retrieval y = w_t . q for the query-prior gradient.  2 FLOP each."""
+    return 2 * 10 * Dk * J * Dv * B * H * T
+
+
+def backward_alg_bytes(B, H, T, Dk, Dv, J, in_bytes=2, go_bytes=2):
+    """The forward's inputs and dL/do read once; the six fp32 input gradients
+    written once; dL/dW_0 written (zero initial state: no state read)."""
+    per_token_head = (in_bytes * (2 * Dk + Dv + 3 * J * Dv) + go_bytes * Dv
+                      + 4 * (2 * Dk + Dv + 3 * J * Dv))
+    return B * H * T * per_token_head + 4 * J * Dk * Dv * B * H
+
+
+def bench_backward(sw, torch, dev, cfg, steps, warmup):
+    """The backward pass (swila_backward) on the same batch: dL/do ~ N(0,1) in the
+    input dtype, no state gradient.  One step is one call: the forward
+    recompute, the reverse scan and the chunk pass."""
+    B, H, T, Dk, Dv, J = (cfg[x] for x in ("B", "H", "T", "Dk", "Dv", "J"))
+    names = ("q", "k", "v", "lb", "lk", "lq")
+    args = [dev[n] for n in names]
+    g = torch.Generator(device="cuda")
+    g.manual_seed(4242)
+    go = torch.randn((B, T, H, Dv), device="cuda", generator=g).to(dev["q"].dtype)
+    ws = torch.empty(sw.backward_workspace_bytes(B, H, T, Dk, Dv, J), device="cuda",
+                     dtype=torch.uint8)
+
+    def step():
+        return sw.backward(*args, dev["state"], go, None, workspace=ws)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(steps)]
+    t0 = time.perf_counter()
+    for i in range(steps):
+        ev[i][0].record(stream)
+        step()
+        ev[i][1].record(stream)
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) / steps
+    kern = sum(a.elapsed_time(b) for a, b in ev) / steps / 1e3
+    eb = dev["q"].element_size()
+    nflop = backward_alg_flops(B, H, T, Dk, Dv, J)
+    nbytes = backward_alg_bytes(B, H, T, Dk, Dv, J, eb, eb)
+    return {
+        "workload": "backward of the plain forward (exact gradient), same batch, dL/do "
+                    "N(0,1), zero initial state, no final-state gradient",
+        "tokens_per_s": B * T / wall, "ms_per_step": wall * 1e3,
+        "roofline": {"bound": "alu", "achieved": nflop / kern / 1e12,
+                     "peak": PEAK_VALU_F32 / 1e12, "unit": "TFLOP/s",
+                     "frac": nflop / kern / PEAK_VALU_F32, "traffic": None,
+                     "kernel": "swila_backward (forward recompute, reverse scan, chunk pass)",
+                     "kernel_ms": kern * 1e3, "alg_flop_per_launch": nflop,
+                     "alg_bytes_per_launch": nbytes},
+    }
+
+
 def bench_gated(sw, torch, workloads, dev, cfg, seed, steps, warmup, o, s_out, tdt):
     """Gated SwiLA (App. B.4, eq. pre-decay, one gate per key dimension) on the
     same batch: decay logits N(2, 1), through the token-by-token scan."""
@@ -366,6 +431,7 @@ def main():
     ap.add_argument("--no-newton", action="store_true")
     ap.add_argument("--no-temporal", action="store_true")
     ap.add_argument("--no-gated", action="store_true")
+    ap.add_argument("--no-backward", action="store_true")
     ap.add_argument("--newton-study", action="store_true",
                     help="only the App. D measurement at B=16 H=8 T=4096 D=64 J=4")
     ap.add_argument("--newton-tol", type=float, default=1e-3)
@@ -442,6 +508,8 @@ def main():
     if not args.no_gated:
         out["gated"] = bench_gated(sw, torch, workloads, dev, cfg, 1000 + args.config,
                                    args.steps, args.warmup, o, s_out, tdt)
+    if not args.no_backward:
+        out["backward"] = bench_backward(sw, torch, dev, cfg, args.steps, args.warmup)
     if not args.no_newton and bf16:
         out["newton"] = bench_newton(sw, torch, dev, cfg, args.steps, args.warmup, o, s_out,
                                      args.newton_tol)

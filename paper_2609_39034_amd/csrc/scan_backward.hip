@@ -29,11 +29,14 @@
 //      dq_t = Y_t.S + sum_{s<=t} (Y_t.C_s) k_s
 //      dk_t = C_t.E_n + P_t.S + sum_{s>t} (C_t.P_s) k_s + sum_{s<t} (P_t.C_s) k_s
 //             + sum_{s>=t} (C_t.Y_s) q_s
-//    (X_t.Z_s = sum over columns of X_{t,col} Z_{s,col}), contractions of
-//    chunk-sized operands, and y_{tjd} = w_{t,jd} . q_t for the query-prior
-//    gradient dlq_j = pi^q_j do (y_j - sum_i pi^q_i y_i) is
-//    Q S + tril(Q K^T) C.  Column tiles of all J components of DT output dims
-//    stream through LDS; the chunk's K, Q and its Gram products stay there.
+//    (X_t.Z_s = sum over columns of X_{t,col} Z_{s,col}): contractions of
+//    chunk-sized operands.  The query-prior logit gradient needs the
+//    retrievals y_{tjd} = w_{t,jd} . q_t = (Q S + tril(Q K^T) C)_{t,col}:
+//    dlq_j = pi^q_j do (y_j - sum_i pi^q_i y_i).  Column tiles of all J
+//    components of DT output dims stream through LDS; each thread accumulates a
+//    TM x TN block of (token, key index) outputs in registers, and the
+//    intra-chunk sums become three masked C x C coefficient matrices applied to
+//    the chunk's K and Q at the end.
 #include "device_common.hpp"
 #include "launch.hpp"
 
@@ -45,6 +48,8 @@ constexpr int kTC = 16;           // tokens staged per round of the reverse scan
 constexpr int kMaxCols = 128;
 constexpr int kCB = kBwdChunk;    // tokens per chunk of the chunk pass
 
+// Columns of one reverse-scan block: bounded by the block size, the largest Dv
+// and 64 KiB of staged per-(token, column) inputs.
 constexpr int rev_cols(int L, int J) {
     int n = kThreads / L < kMaxCols ? kThreads / L : kMaxCols;
     while (n > 16 && kTC * (4 * J + 1) * n * 4 > 65536) n /= 2;
@@ -216,19 +221,45 @@ __global__ __launch_bounds__(kThreads) void scan_reverse_kernel(BackwardArgs a, 
     }
 }
 
+// Output dims per column tile of the chunk pass: tiles of all J components of
+// DT dims, 16 to 32 columns.
+template <int J>
+constexpr int chunk_tile_dims() { return J == 1 ? 16 : J == 3 ? 8 : 32 / J; }
+
+template <int N>
+__device__ __forceinline__ void lds_vec(const float *p, float (&v)[N]) {
+    if constexpr (N == 4) {
+        const float4 x = *reinterpret_cast<const float4 *>(p);
+        v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
+    } else {
+        const float2 x = *reinterpret_cast<const float2 *>(p);
+        v[0] = x.x; v[1] = x.y;
+    }
+}
+
 template <int DK, int J>
 __global__ __launch_bounds__(kThreads) void bwd_chunk_kernel(BackwardArgs a) {
-    constexpr int DT = J == 3 ? 4 : 16 / J;   // output dims per column tile
-    constexpr int NCT = J * DT;               // columns per tile, all J of each dim
-    constexpr int KP = DK + 1, CP = NCT + 1, GP = kCB + 1;
-    constexpr int NE = kCB * DK / kThreads;   // (token, key index) entries per thread
-    constexpr int NG = kCB * kCB / kThreads;  // Gram entries per thread
-    static_assert(NE >= 1 && NG >= 1 && kCB * DK % kThreads == 0, "tile sizes");
+    constexpr int DT = chunk_tile_dims<J>();
+    constexpr int NCT = J * DT;               // columns per tile
+    constexpr int NO = kCB * DK / kThreads;   // (token, key index) outputs per thread
+    constexpr int TN = NO < 4 ? NO : 4;       // consecutive key indices per thread
+    constexpr int TM = NO / TN;               // tokens per thread
+    constexpr int NIB = DK / TN;
+    static_assert(TN >= 2 && NIB * (kCB / TM) == kThreads, "thread tiling");
+    static_assert(kCB * kCB == 4 * kThreads, "Gram tiling: 4 entries per thread");
+    constexpr int KP = DK + 4, GP = kCB + 4, CP = NCT + 1;   // row pitches (16-byte rows)
 
-    __shared__ float sK[kCB][KP], sQ[kCB][KP];
-    __shared__ float sQK[kCB][GP], sA[kCB][GP], sB[kCB][GP];
-    __shared__ float sS[NCT][KP], sE[NCT][KP];
-    __shared__ float sC[kCB][CP], sP[kCB][CP], sY[kCB][CP], sPq[kCB][CP], sYv[kCB][CP];
+    __shared__ __align__(16) float sK[kCB][KP];
+    __shared__ __align__(16) float sQ[kCB][KP];
+    __shared__ __align__(16) float sS[NCT][KP];
+    __shared__ __align__(16) float sE[NCT][KP];
+    __shared__ float sC[kCB][CP], sP[kCB][CP], sY[kCB][CP];
+    __shared__ __align__(16) float sCt[NCT][GP];   // C and P transposed: [column][token]
+    __shared__ __align__(16) float sPt[NCT][GP];
+    __shared__ float sA[kCB][GP], sB[kCB][GP];
+    __shared__ __align__(16) float sM[3][kCB][GP]; // masked intra-chunk coefficients
+    __shared__ float sQK[kCB][GP];                 // q_t . k_s
+    __shared__ float sPq[kCB][CP], sYv[kCB][CP];   // pi^q and the retrievals y
     __shared__ float sDo[kCB][DT];
 
     const LayerArgs &f = a.f;
@@ -238,45 +269,64 @@ __global__ __launch_bounds__(kThreads) void bwd_chunk_kernel(BackwardArgs a) {
     const int NCH = (T + kCB - 1) / kCB;
     const int t0 = n * kCB, nt = min(kCB, T - t0);
     const bool ibf = f.in_bf16, obf = f.out_bf16;
+    const int i0 = (tid % NIB) * TN, tA = (tid / NIB) * TM;   // this thread's outputs
+    const int gt = tid / 8, gs = (tid % 8) * 4;               // its Gram entries
+    const int gt8 = tid % 8;                                  // its retrieval columns
 
-    for (int g = tid; g < kCB * DK; g += kThreads) {
-        const int t = g / DK, i = g % DK;
-        float kv = 0.0f, qv = 0.0f;
+    for (int g = tid; g < kCB * (DK / 4); g += kThreads) {
+        const int t = g / (DK / 4), i = (g % (DK / 4)) * 4;
+        float4 kv = make_float4(0.f, 0.f, 0.f, 0.f), qv = kv;
         if (t < nt) {
             const size_t off = ((size_t)(b * T + t0 + t) * H + h) * DK + i;
-            kv = load1(f.k, off, ibf);
-            qv = load1(f.q, off, ibf);
+            kv = load4(f.k, off, ibf);
+            qv = load4(f.q, off, ibf);
         }
-        sK[t][i] = kv;
-        sQ[t][i] = qv;
+        *reinterpret_cast<float4 *>(&sK[t][i]) = kv;
+        *reinterpret_cast<float4 *>(&sQ[t][i]) = qv;
     }
     __syncthreads();
-    for (int g = tid; g < kCB * kCB; g += kThreads) {
-        const int t = g / kCB, s = g % kCB;
-        float acc = 0.0f;
-#pragma unroll 8
-        for (int i = 0; i < DK; ++i) acc = fmaf(sQ[t][i], sK[s][i], acc);
-        sQK[t][s] = acc;
+    {   // Q K^T: row gt, columns gt8 + 8 x
+        float qk[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
+        for (int i = 0; i < DK; i += 4) {
+            float qv[4];
+            lds_vec<4>(&sQ[gt][i], qv);
+#pragma unroll
+            for (int x = 0; x < 4; ++x) {
+                float kv[4];
+                lds_vec<4>(&sK[gt8 + 8 * x][i], kv);
+#pragma unroll
+                for (int z = 0; z < 4; ++z) qk[x] = fmaf(qv[z], kv[z], qk[x]);
+            }
+        }
+#pragma unroll
+        for (int x = 0; x < 4; ++x) sQK[gt][gt8 + 8 * x] = qk[x];
     }
 
-    float dq[NE], dk[NE], ga[NG], gb[NG];
+    float dq[TM][TN], dk[TM][TN], ga[4], gb[4];
 #pragma unroll
-    for (int m = 0; m < NE; ++m) dq[m] = dk[m] = 0.0f;
+    for (int m = 0; m < TM; ++m)
 #pragma unroll
-    for (int m = 0; m < NG; ++m) ga[m] = gb[m] = 0.0f;
+        for (int x = 0; x < TN; ++x) dq[m][x] = dk[m][x] = 0.0f;
+#pragma unroll
+    for (int x = 0; x < 4; ++x) ga[x] = gb[x] = 0.0f;
 
     // checkpoints of this chunk, [Dv][J][DK]
     const size_t ck0 = (((size_t)b * H + h) * NCH + n) * Dv * J * DK;
     for (int dt0 = 0; dt0 < Dv; dt0 += DT) {
-        __syncthreads();   // the previous tile is consumed (first pass: Q K^T is done)
-        for (int g = tid; g < DT * J * DK; g += kThreads) {
-            const int dd = g / (J * DK), j = (g / DK) % J, i = g % DK;
-            const size_t src = ck0 + (size_t)dt0 * J * DK + g;
-            sS[j * DT + dd][i] = a.wck[src];
-            sE[j * DT + dd][i] = a.eck[src];
+        __syncthreads();   // the previous tile is consumed
+        for (int g = tid; g < DT * J * (DK / 4); g += kThreads) {
+            const int e = 4 * g;
+            const int dd = e / (J * DK), j = (e / DK) % J, i = e % DK;
+            const size_t src = ck0 + (size_t)dt0 * J * DK + e;
+            *reinterpret_cast<float4 *>(&sS[j * DT + dd][i]) =
+                *reinterpret_cast<const float4 *>(a.wck + src);
+            *reinterpret_cast<float4 *>(&sE[j * DT + dd][i]) =
+                *reinterpret_cast<const float4 *>(a.eck + src);
         }
         for (int g = tid; g < kCB * DT; g += kThreads) {
             const int t = g / DT, dd = g % DT;
+            float c[J], p[J], y[J], pq[J];
             if (t < nt) {
                 const size_t row = (size_t)(b * T + t0 + t) * H + h;
                 const float dov = load1(a.grad_o, row * Dv + dt0 + dd, obf);
@@ -304,71 +354,94 @@ __global__ __launch_bounds__(kThreads) void bwd_chunk_kernel(BackwardArgs a) {
                 for (int j = 0; j < J; ++j) {
                     const size_t idx = (row * J + j) * Dv + dt0 + dd;
                     const float beta = 1.0f / (1.0f + exp_fast(-load1(f.lb, idx, ibf)));
-                    const float pq = J == 1 ? 1.0f : lq[j] * izq;
-                    sC[t][j * DT + dd] = beta * (J == 1 ? 1.0f : e[j] * iz) * delta[j];
-                    sP[t][j * DT + dd] = a.dpred[idx];
-                    sPq[t][j * DT + dd] = pq;
-                    sY[t][j * DT + dd] = dov * pq;
+                    c[j] = beta * (J == 1 ? 1.0f : e[j] * iz) * delta[j];
+                    p[j] = a.dpred[idx];
+                    pq[j] = J == 1 ? 1.0f : lq[j] * izq;
+                    y[j] = dov * pq[j];
                 }
                 sDo[t][dd] = dov;
             } else {
 #pragma unroll
-                for (int j = 0; j < J; ++j) {
-                    sC[t][j * DT + dd] = 0.0f;
-                    sP[t][j * DT + dd] = 0.0f;
-                    sPq[t][j * DT + dd] = 0.0f;
-                    sY[t][j * DT + dd] = 0.0f;
-                }
+                for (int j = 0; j < J; ++j) c[j] = p[j] = y[j] = pq[j] = 0.0f;
                 sDo[t][dd] = 0.0f;
+            }
+#pragma unroll
+            for (int j = 0; j < J; ++j) {
+                const int cc = j * DT + dd;
+                sC[t][cc] = c[j];
+                sP[t][cc] = p[j];
+                sY[t][cc] = y[j];
+                sCt[cc][t] = c[j];
+                sPt[cc][t] = p[j];
+                sPq[t][cc] = pq[j];
             }
         }
         __syncthreads();
 
-        // Y S into dq; P S + C E into dk
+        // dq += Y S; dk += P S + C E (this tile's columns)
+#pragma unroll 4
+        for (int cc = 0; cc < NCT; ++cc) {
+            float sv[TN], ev[TN];
+            lds_vec<TN>(&sS[cc][i0], sv);
+            lds_vec<TN>(&sE[cc][i0], ev);
 #pragma unroll
-        for (int m = 0; m < NE; ++m) {
-            const int e = tid + kThreads * m, t = e / DK, i = e % DK;
-            float aq = dq[m], ak = dk[m];
+            for (int m = 0; m < TM; ++m) {
+                const float yv = sY[tA + m][cc], pv = sP[tA + m][cc], cv = sC[tA + m][cc];
 #pragma unroll
-            for (int cc = 0; cc < NCT; ++cc) {
-                const float sv = sS[cc][i];
-                aq = fmaf(sY[t][cc], sv, aq);
-                ak = fmaf(sP[t][cc], sv, ak);
-                ak = fmaf(sC[t][cc], sE[cc][i], ak);
+                for (int x = 0; x < TN; ++x) {
+                    dq[m][x] = fmaf(yv, sv[x], dq[m][x]);
+                    dk[m][x] = fmaf(pv, sv[x], fmaf(cv, ev[x], dk[m][x]));
+                }
             }
-            dq[m] = aq;
-            dk[m] = ak;
         }
-        // Gram products over the columns: ga[t][s] = Y_t.C_s, gb[t][s] = C_t.P_s
+        // Gram products over the columns: ga = Y_t . C_s, gb = C_t . P_s
+#pragma unroll 4
+        for (int cc = 0; cc < NCT; ++cc) {
+            float ct[4], pt[4];
+            lds_vec<4>(&sCt[cc][gs], ct);
+            lds_vec<4>(&sPt[cc][gs], pt);
+            const float yv = sY[gt][cc], cv = sC[gt][cc];
 #pragma unroll
-        for (int m = 0; m < NG; ++m) {
-            const int e = tid + kThreads * m, t = e / kCB, s = e % kCB;
-            float x = ga[m], y = gb[m];
-#pragma unroll
-            for (int cc = 0; cc < NCT; ++cc) {
-                x = fmaf(sY[t][cc], sC[s][cc], x);
-                y = fmaf(sC[t][cc], sP[s][cc], y);
+            for (int x = 0; x < 4; ++x) {
+                ga[x] = fmaf(yv, ct[x], ga[x]);
+                gb[x] = fmaf(cv, pt[x], gb[x]);
             }
-            ga[m] = x;
-            gb[m] = y;
         }
-        // y_t = w_t . q_t = S q_t + sum_{s<=t} (q_t . k_s) C_s
-        for (int g = tid; g < kCB * NCT; g += kThreads) {
-            const int t = g / NCT, cc = g % NCT;
-            float acc = 0.0f;
-#pragma unroll 8
-            for (int i = 0; i < DK; ++i) acc = fmaf(sQ[t][i], sS[cc][i], acc);
-            for (int s = 0; s <= t; ++s) acc = fmaf(sQK[t][s], sC[s][cc], acc);
-            sYv[t][cc] = acc;
+        // retrievals y = Q S + tril(Q K^T) C: row gt, columns gt8 + 8 x
+        if constexpr (J > 1) {
+            constexpr int NY = NCT / 8;
+            float yr[NY];
+#pragma unroll
+            for (int x = 0; x < NY; ++x) yr[x] = 0.0f;
+#pragma unroll 4
+            for (int i = 0; i < DK; i += 4) {
+                float qv[4];
+                lds_vec<4>(&sQ[gt][i], qv);
+#pragma unroll
+                for (int x = 0; x < NY; ++x) {
+                    float sv[4];
+                    lds_vec<4>(&sS[gt8 + 8 * x][i], sv);
+#pragma unroll
+                    for (int z = 0; z < 4; ++z) yr[x] = fmaf(qv[z], sv[z], yr[x]);
+                }
+            }
+            for (int s2 = 0; s2 <= gt; ++s2) {
+                const float qk = sQK[gt][s2];
+#pragma unroll
+                for (int x = 0; x < NY; ++x) yr[x] = fmaf(qk, sC[s2][gt8 + 8 * x], yr[x]);
+            }
+#pragma unroll
+            for (int x = 0; x < NY; ++x) sYv[gt][gt8 + 8 * x] = yr[x];
         }
         __syncthreads();
+        // dL/dlq_j = pi^q_j do (y_j - sum_i pi^q_i y_i); zero for one component
         for (int g = tid; g < nt * DT; g += kThreads) {
             const int t = g / DT, dd = g % DT;
-            const float dov = sDo[t][dd];
+            const size_t row = (size_t)(b * T + t0 + t) * H + h;
             float mean = 0.0f;
 #pragma unroll
             for (int j = 0; j < J; ++j) mean = fmaf(sPq[t][j * DT + dd], sYv[t][j * DT + dd], mean);
-            const size_t row = (size_t)(b * T + t0 + t) * H + h;
+            const float dov = sDo[t][dd];
 #pragma unroll
             for (int j = 0; j < J; ++j)
                 a.dlq[(row * J + j) * Dv + dt0 + dd] =
@@ -376,29 +449,45 @@ __global__ __launch_bounds__(kThreads) void bwd_chunk_kernel(BackwardArgs a) {
         }
     }
 
-    // the intra-chunk terms
+    // the intra-chunk terms, as three masked C x C coefficient matrices
 #pragma unroll
-    for (int m = 0; m < NG; ++m) {
-        const int e = tid + kThreads * m, t = e / kCB, s = e % kCB;
-        sA[t][s] = ga[m];
-        sB[t][s] = gb[m];
+    for (int x = 0; x < 4; ++x) {
+        sA[gt][gs + x] = ga[x];
+        sB[gt][gs + x] = gb[x];
     }
     __syncthreads();
+    for (int g = tid; g < kCB * kCB; g += kThreads) {
+        const int t = g / kCB, s = g % kCB;
+        sM[0][t][s] = s <= t ? sA[t][s] : 0.0f;                          // (Y_t . C_s) k_s
+        sM[1][t][s] = s > t ? sB[t][s] : (s < t ? sB[s][t] : 0.0f);      // (C_t.P_s), (P_t.C_s) k_s
+        sM[2][t][s] = s >= t ? sA[s][t] : 0.0f;                          // (C_t . Y_s) q_s
+    }
+    __syncthreads();
+#pragma unroll 4
+    for (int s = 0; s < kCB; ++s) {
+        float kv[TN], qv[TN];
+        lds_vec<TN>(&sK[s][i0], kv);
+        lds_vec<TN>(&sQ[s][i0], qv);
 #pragma unroll
-    for (int m = 0; m < NE; ++m) {
-        const int e = tid + kThreads * m, t = e / DK, i = e % DK;
-        if (t >= nt) continue;
-        float aq = dq[m], ak = dk[m];
-        for (int s = 0; s < kCB; ++s) {
-            const float kv = sK[s][i], qv = sQ[s][i];
-            if (s <= t) aq = fmaf(sA[t][s], kv, aq);   // (Y_t . C_s) k_s
-            if (s > t) ak = fmaf(sB[t][s], kv, ak);    // (C_t . P_s) k_s
-            if (s < t) ak = fmaf(sB[s][t], kv, ak);    // (P_t . C_s) k_s
-            if (s >= t) ak = fmaf(sA[s][t], qv, ak);   // (C_t . Y_s) q_s
+        for (int m = 0; m < TM; ++m) {
+            const float mq = sM[0][tA + m][s], m1 = sM[1][tA + m][s], m2 = sM[2][tA + m][s];
+#pragma unroll
+            for (int x = 0; x < TN; ++x) {
+                dq[m][x] = fmaf(mq, kv[x], dq[m][x]);
+                dk[m][x] = fmaf(m1, kv[x], fmaf(m2, qv[x], dk[m][x]));
+            }
         }
-        const size_t off = ((size_t)(b * T + t0 + t) * H + h) * DK + i;
-        a.dq[off] = aq;
-        a.dk[off] = ak;
+    }
+#pragma unroll
+    for (int m = 0; m < TM; ++m) {
+        const int t = tA + m;
+        if (t >= nt) continue;
+        const size_t off = ((size_t)(b * T + t0 + t) * H + h) * DK + i0;
+#pragma unroll
+        for (int x = 0; x < TN; ++x) {
+            a.dq[off + x] = dq[m][x];
+            a.dk[off + x] = dk[m][x];
+        }
     }
 }
 
@@ -453,8 +542,7 @@ hipError_t launch_backward(const BackwardArgs &a, hipStream_t stream) {
     if (f.T < 1 || f.gk || f.decay || !a.grad_o || !a.dq || !a.dk || !a.dv || !a.dlb || !a.dlk ||
         !a.dlq || !a.delta || !a.dpred || !a.wck || !a.eck)
         return hipErrorInvalidValue;
-    if ((f.Dv / (f.J == 3 ? 4 : 16 / f.J)) * (f.J == 3 ? 4 : 16 / f.J) != f.Dv)
-        return hipErrorInvalidValue;
+    if (f.Dv % 16 != 0) return hipErrorInvalidValue;   // every column tile divides Dv
     switch (f.Dk) {
         case 16: return launch_bwd_dk<16>(a, stream);
         case 32: return launch_bwd_dk<32>(a, stream);
