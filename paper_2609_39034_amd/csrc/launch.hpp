@@ -25,9 +25,11 @@ struct LayerArgs {
     // Gated SwiLA (App. B.4, eq. pre-decay): decay logits [B,T,H,J,Dk] (in_bf16),
     // a = sigmoid, one gate per key dimension and component; nullptr = no decay.
     const void *decay = nullptr;
-    // Backward support (token-by-token scan only): delta_{tjd} per token
-    // ([B,T,H,J,Dv] fp32) and the state before every kBwdChunk-th token
-    // ([B,H,NCH,Dv,J,Dk] fp32, NCH = ceil(T / kBwdChunk)); nullptr = not written.
+    // Backward support (token-by-token scan in its AX mode, or the chunk scan in
+    // exact mode): delta_{tjd} per token ([B,T,H,J,Dv] fp32; the chunk scan then
+    // writes no responsibilities, and o may be nullptr) and the state before every
+    // kBwdChunk-th token ([B,H,NCH,Dv,J,Dk] fp32, NCH = ceil(T / kBwdChunk));
+    // nullptr = not written.
     float *delta_out = nullptr;
     float *ckpt = nullptr;
 };

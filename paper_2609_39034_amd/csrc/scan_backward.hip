@@ -5,8 +5,10 @@
 // trains through its sequential evaluation; this is the exact gradient of
 // that forward, in three launches.
 //
-// 1. Forward recompute (the token-by-token scan in its AX mode): delta_{tjd}
-//    of every token and the state W_n before every kBwdChunk-th token.
+// 1. Forward recompute: delta_{tjd} of every token and the state W_n before
+//    every kBwdChunk-th token.  bf16 inputs run the matrix-core chunk scan with
+//    these outputs in place of o, fp32 inputs the token-by-token scan in its AX
+//    mode, as their forwards do.
 //
 // 2. Reverse scan, one (b, h, d) column per L lanes as in the forward, with
 //    G_{jd} = dL/dw_{t,jd} in registers (each lane a key slice).  Per token,
@@ -502,7 +504,9 @@ hipError_t launch_bwd_dk_j(const BackwardArgs &a, hipStream_t stream) {
     fa.resp = nullptr;
     fa.delta_out = a.delta;
     fa.ckpt = a.wck;
-    hipError_t e = launch_scan_direct_aux(fa, stream);
+    // bf16 inputs: the matrix-core chunk scan recomputes the forward; fp32 inputs
+    // take the token-by-token scan, as their forward does
+    hipError_t e = f.in_bf16 ? launch_scan_pipe(fa, stream) : launch_scan_direct_aux(fa, stream);
     if (e != hipSuccess) return e;
     const int ncol = f.Dv < rev_cols(L, J) ? f.Dv : rev_cols(L, J);
     hipLaunchKernelGGL((scan_reverse_kernel<DK, J, S>), dim3(f.Dv / ncol, f.H, f.B),

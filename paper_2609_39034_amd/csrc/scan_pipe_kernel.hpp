@@ -517,7 +517,12 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
     const int bdl = (sl / JP) % DB, bj = sl % JP;
     const bool bact = seq && sl < DB * JP && bj < J;
     const bool bpad = seq && sl < DB * JP && bj >= J;   // padding component (J = 3)
-    const bool want_r = a.resp != nullptr;   // (the temporal form always keeps r)
+    // Backward support (exact mode): with delta_out the per-token LDS ring that
+    // carries r for resp carries delta instead, to delta_out, and the tile waves
+    // store the state every second chunk to ckpt.
+    const bool dmode = MD == 0 && a.delta_out != nullptr;
+    float *const rdst = dmode ? a.delta_out : a.resp;
+    const bool want_r = rdst != nullptr;   // (the temporal form always keeps r)
     const int bcol = bact ? bj * DB + bdl : 0;
     const int bsto = bact ? bcol : N;
 
@@ -792,6 +797,7 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
     };
     // o of chunk m: sum over j of pi^q * retrieval
     auto store_output = [&](int m, int pr) {
+        if (!a.o) return;   // (the backward's recompute keeps no output)
 #pragma unroll
         for (int i_ = 0; i_ < ceil_div(NPG, NBT); ++i_) {
             const int gi = (OUT0 ? bt - OUT0 : brot(1)) + i_ * NBT;
@@ -824,10 +830,23 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
             const int e4 = 4 * g4, t = e4 / N, cc = e4 % N;
             if (m * kC + t < T)
                 *reinterpret_cast<float4 *>(
-                    a.resp + ((((size_t)b * T + m * kC + t) * H + h) * J + cc / DB) * Dv + d0 +
+                    rdst + ((((size_t)b * T + m * kC + t) * H + h) * J + cc / DB) * Dv + d0 +
                     cc % DB) = *reinterpret_cast<const float4 *>(&sm.r[pr][t][cc]);
           }
         }
+    };
+    // Backward support: the state before chunk 2 m, unscaled, into
+    // ckpt [B, H, ceil(T / 32), Dv, J, Dk] (rows 16 it + 4 lg .. + 3 of column col)
+    auto store_ckpt = [&](int m) {
+        static_assert(kBwdChunk == 2 * kC, "checkpoints every second chunk");
+        const int NC2 = (T + 2 * kC - 1) / (2 * kC);
+        float *dst = a.ckpt + ((((size_t)b * H + h) * NC2 + m) * Dv + dc) * J * DK +
+                     (size_t)jc * DK + 4 * lg;
+#pragma unroll
+        for (int it = 0; it < IT; ++it)
+            *reinterpret_cast<float4 *>(dst + 16 * it) =
+                make_float4(kInvWS * W[it][0], kInvWS * W[it][1], kInvWS * W[it][2],
+                            kInvWS * W[it][3]);
     };
     // W += K_m^T C_m and Y += tril(A_m) C_m (C_m split in chi/clo); then
     // stage pi^q * Y of chunk m
@@ -1052,7 +1071,7 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
                                     make_float4(cb[0], cb[1], cb[2], cb[3]);
                             if constexpr (R) {
                                 const float rt = ex * iz;
-                                sm.r[pr][t][bsto] = rt;
+                                sm.r[pr][t][bsto] = dmode ? kInvWS * d : rt;
                                 if constexpr (TP) rprev = rt;
                             }
                             chk = fmaf(z, iz, chk);
@@ -1089,7 +1108,7 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
                                 sm.c[pr][bsto][t] = cs;
                                 if constexpr (R) {
                                     const float rt = ex * iz;
-                                    sm.r[pr][t][bsto] = rt;
+                                    sm.r[pr][t][bsto] = dmode ? kInvWS * d : rt;
                                     if constexpr (TP) rprev = rt;
                                 }
 #pragma unroll
