@@ -37,17 +37,15 @@ PEAK_MFMA_BF16 = 2.5e15    # FLOP/s, MI355X dense bf16 matrix
 # source, the workload it ran and the digest of the source at measurement.
 MEASURED_TRAFFIC = {
     ("decode.hip", "decode B=256 H=16 Dk=Dv=128 J=4",
-     "17cda266f6fb5ff92e54ad1b1e645c9ce379946f7ede393facaad11ebd01f546"): 2184242900,
+     "10a280fc4288f38608f27ababeece47b80e697cbc47fd154437db4ebc82836b2"): 2184274349,
     ("scan_pipe.hip", "forward B=4 H=8 T=2048 Dk=Dv=64 J=4",
-     "ee7a4ca4b00165323d4a9dc5846f10bf5c09e5a849802ad9e324f9631b5ab7fa"): 136726401,
+     "c726c889f31a85c4db9ccb59682ba4d02d3cda42e78d9b3dbe342096e3c92e6b"): 136682804,
     ("scan_pipe.hip", "forward B=8 H=16 T=4096 Dk=Dv=128 J=4",
-     "ee7a4ca4b00165323d4a9dc5846f10bf5c09e5a849802ad9e324f9631b5ab7fa"): 2197260709,
+     "c726c889f31a85c4db9ccb59682ba4d02d3cda42e78d9b3dbe342096e3c92e6b"): 2185331085,
     ("scan_pipe_temporal.hip", "temporal B=4 H=8 T=2048 Dk=Dv=64 J=4",
-     "48c89ce7f844cea710a7d5e924b56a12657a6c07052831106e0ab66ba5bbc3fb"): 153644932,
-    ("scan_direct.hip", "forward B=4 H=8 T=2048 Dk=Dv=64 J=4",
-     "099a12cb87aae465addcca2f6cedc2dc92343ec0d0a32245b60c2defffe1cc3f"): 136528440,
+     "a5ffe58c7150c4f1a592fb13502fd103aafa35fb0556c5b5dde60e49b454af9f"): 153641430,
     ("scan_direct.hip", "gated B=4 H=8 T=2048 Dk=Dv=64 J=4",
-     "099a12cb87aae465addcca2f6cedc2dc92343ec0d0a32245b60c2defffe1cc3f"): 170093419,
+     "e24f3a5ca0926eaa89c84fac489f603f2c34e519db5730311b0cbcefdb0b0e05"): 170098769,
 }
 
 
