@@ -10,17 +10,16 @@
 //    these outputs in place of o, fp32 inputs the token-by-token scan in its AX
 //    mode, as their forwards do.
 //
-// 2. Reverse scan, one (b, h, d) column per L lanes as in the forward, with
-//    G_{jd} = dL/dw_{t,jd} in registers (each lane a key slice).  Per token,
-//    in reverse:
+// 2. Reverse scan.  With G_{jd} = dL/dw_{t,jd}, per token in reverse:
 //      dy_j = do pi^q_j;  G_j += dy_j q_t;  dc_j = G_j . k_t
 //      r = softmax_j(lk - delta^2/2) and beta recomputed from delta and logits
 //      dlb_j = dc_j r_j delta_j beta_j (1 - beta_j)
 //      dr_j = dc_j beta_j delta_j;  da_j = r_j (dr_j - sum_i r_i dr_i) = dlk_j
 //      ddelta_j = dc_j beta_j r_j - delta_j da_j;  dv = sum_j ddelta_j
 //      dpred_j = -ddelta_j;  G_j += dpred_j k_t          (now dL/dw_{t-1,jd})
-//    It writes dv, dlb, dlk, dpred, dL/dW_0 (G after token 0), and E_n, the
-//    part of dL/dw at the last token of chunk n that comes from later tokens.
+//    evaluated a chunk at a time (reverse_chunk_kernel below).  It writes dv,
+//    dlb, dlk, dpred, dL/dW_0 (G after token 0), and E_n, the part of dL/dw at
+//    the last token of checkpoint interval n that comes from later tokens.
 //
 // 3. Chunk pass, one block per (b, h, chunk of kBwdChunk tokens), no
 //    sequential dependence.  Inside chunk n, with S = W_n, columns col = (j, d)
@@ -46,180 +45,326 @@ namespace swila {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kTC = 16;           // tokens staged per round of the reverse scan
-constexpr int kMaxCols = 128;
 constexpr int kCB = kBwdChunk;    // tokens per chunk of the chunk pass
 
-// Columns of one reverse-scan block: bounded by the block size, the largest Dv
-// and 64 KiB of staged per-(token, column) inputs.
-constexpr int rev_cols(int L, int J) {
-    int n = kThreads / L < kMaxCols ? kThreads / L : kMaxCols;
-    while (n > 16 && kTC * (4 * J + 1) * n * 4 > 65536) n /= 2;
-    return n;
+// The kernels below order only LDS traffic at their barriers (block_sync_lds):
+// a full __syncthreads would also wait for every global load in flight, and
+// with it for the next chunk's prefetch.
+//
+// Raw loads: the bits of one element (a bf16 in the low half, or an fp32), or
+// of four, converted to fp32 only where they are used.  Loading and converting
+// in one step makes each load wait for its data before the next is issued;
+// these let a staging loop issue all of its loads first.
+__device__ __forceinline__ uint32_t raw1(const void *base, size_t idx, bool bf16) {
+    return bf16 ? (uint32_t) static_cast<const uint16_t *>(base)[idx]
+                : static_cast<const uint32_t *>(base)[idx];
+}
+__device__ __forceinline__ float cvt1(uint32_t r, bool bf16) {
+    return __uint_as_float(bf16 ? r << 16 : r);
+}
+__device__ __forceinline__ uint4 raw4(const void *base, size_t idx, bool bf16) {
+    if (bf16) {
+        const uint2 x = *reinterpret_cast<const uint2 *>(static_cast<const uint16_t *>(base) + idx);
+        return make_uint4(x.x, x.y, 0u, 0u);
+    }
+    return *reinterpret_cast<const uint4 *>(static_cast<const float *>(base) + idx);
+}
+__device__ __forceinline__ float4 cvt4(uint4 r, bool bf16) {
+    if (bf16)
+        return make_float4(__uint_as_float(r.x << 16), __uint_as_float(r.x & 0xffff0000u),
+                           __uint_as_float(r.y << 16), __uint_as_float(r.y & 0xffff0000u));
+    return make_float4(__uint_as_float(r.x), __uint_as_float(r.y), __uint_as_float(r.z),
+                       __uint_as_float(r.w));
 }
 
-template <int DK, int J, int S>
-__global__ __launch_bounds__(kThreads) void scan_reverse_kernel(BackwardArgs a, int ncol) {
-    constexpr int L = DK / S;             // lanes per output column
-    constexpr int NCM = rev_cols(L, J);
-    constexpr int SP = S + 4;
+// Chunked reverse scan.  The recurrence of the reverse sweep has the shape of
+// the forward's chunk form run backwards: inside a chunk of kRC tokens, with E
+// the gradient w.r.t. the state after the chunk's last token from the tokens
+// that follow it,
+//   dc_t = k_t . E + sum_{s>=t} (k_t . q_s) dy_s + sum_{s>t} (k_t . k_s) dpred_s
+// and dpred_t is linear in the J values dc_t of its output dim.  So per chunk:
+// the Gram products K K^T, K Q^T and the base K E + triu(K Q^T) Y in parallel;
+// one wave then runs the chunk's tokens in reverse, one lane per column (all J
+// components of DB output dims, J lanes adjacent), with the later tokens'
+// dpred folded in as deferred updates; last E += Q^T Y + K^T P.  Every product
+// is fp32 on the vector ALUs.
+constexpr int kRC = 16;   // tokens per chunk of the reverse scan
 
-    __shared__ __align__(16) float sK[kTC][L][SP];
-    __shared__ __align__(16) float sQ[kTC][L][SP];
-    __shared__ float sDo[kTC][NCM];
-    __shared__ float sDelta[kTC][J][NCM];
-    __shared__ float sBeta[kTC][J][NCM];
-    __shared__ float sLk[kTC][J][NCM];
-    __shared__ float sPq[kTC][J][NCM];
+template <int DK, int J, int DB>
+__global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a) {
+    constexpr int JP = J == 3 ? 4 : J;   // lanes per output dim (J = 3 padded)
+    constexpr int N = J * DB;            // columns, col = j * DB + dd
+    constexpr int NL = JP * DB;          // sequential lanes, lane = dd * JP + j
+    constexpr int KP = DK + 4;           // row pitches keep 16-byte rows
+    constexpr int CP = N + 4, GP = kRC + 4;
+    static_assert(NL <= 64 && kBwdChunk % kRC == 0 && N % 4 == 0, "one sequential wave");
+
+    __shared__ __align__(16) float sE[DK][CP];
+    __shared__ __align__(16) float sK[kRC][KP], sQ[kRC][KP];    // rows t
+    __shared__ __align__(16) float sKt[DK][GP], sQt[DK][GP];    // the same, [i][t]
+    __shared__ __align__(16) float sGkk[kRC][GP];               // k_t . k_s (symmetric)
+    __shared__ __align__(16) float sGkqT[kRC][GP];              // [s][t] = k_t . q_s
+    __shared__ __align__(16) float sBase[kRC][CP], sY[kRC][CP], sP[kRC][CP];
+    __shared__ float sDelta[kRC][CP], sBeta[kRC][CP], sR[kRC][CP];
+    __shared__ float sDlb[kRC][CP], sDlk[kRC][CP], sDv[kRC][DB];
 
     const LayerArgs &f = a.f;
-    const int tid = threadIdx.x;
-    const int nthr = ncol * L;
-    const int dl = tid / L, l = tid % L;
-    const int d0 = blockIdx.x * ncol;
-    const int h = blockIdx.y, b = blockIdx.z;
+    const int tid = threadIdx.x, lane = tid % 64;
+    const int d0 = blockIdx.x * DB, h = blockIdx.y, b = blockIdx.z;
     const int H = f.H, T = f.T, Dv = f.Dv;
-    const int d = d0 + dl;
     const bool ibf = f.in_bf16, obf = f.out_bf16;
-    const int NCH = (T + kCB - 1) / kCB;
-
-    float G[J][S];
+    const int NCH = (T + kRC - 1) / kRC;
+    const int NC2 = (T + kBwdChunk - 1) / kBwdChunk;
+    constexpr int R2 = kBwdChunk / kRC;   // reverse chunks per checkpoint interval
     const size_t sbase = ((size_t)b * H + h) * J * DK * Dv;
-#pragma unroll
-    for (int j = 0; j < J; ++j)
-#pragma unroll
-        for (int s = 0; s < S; ++s)
-            G[j][s] = a.grad_state ? a.grad_state[sbase + ((size_t)j * DK + l * S + s) * Dv + d]
-                                   : 0.0f;
 
-    const int nr = (T + kTC - 1) / kTC;
-    for (int rr = nr - 1; rr >= 0; --rr) {
-        const int t0 = rr * kTC;
-        const int nt = min(kTC, T - t0);
-        __syncthreads();
-        for (int g = tid; g < nt * (DK / 4); g += nthr) {
-            const int tt = g / (DK / 4), i = (g % (DK / 4)) * 4;
-            const size_t off = ((size_t)(b * T + t0 + tt) * H + h) * DK + i;
-            *reinterpret_cast<float4 *>(&sK[tt][i / S][i % S]) = load4(f.k, off, ibf);
-            *reinterpret_cast<float4 *>(&sQ[tt][i / S][i % S]) = load4(f.q, off, ibf);
-        }
-        for (int g = tid; g < nt * ncol; g += nthr) {
-            const int tt = g / ncol, c = g % ncol;
-            const size_t row = (size_t)(b * T + t0 + tt) * H + h;
-            sDo[tt][c] = load1(a.grad_o, row * Dv + d0 + c, obf);
-            float lq[J];
-            float m = -INFINITY;
-#pragma unroll
-            for (int j = 0; j < J; ++j) {
-                const size_t idx = (row * J + j) * Dv + d0 + c;
-                sDelta[tt][j][c] = a.delta[idx];
-                sBeta[tt][j][c] = 1.0f / (1.0f + exp_fast(-load1(f.lb, idx, ibf)));
-                sLk[tt][j][c] = load1(f.lk, idx, ibf);
-                lq[j] = load1(f.lq, idx, ibf);
-                m = fmaxf(m, lq[j]);
-            }
-            float z = 0.0f;
-#pragma unroll
-            for (int j = 0; j < J; ++j) {
-                lq[j] = exp_fast(lq[j] - m);
-                z += lq[j];
-            }
-            const float iz = 1.0f / z;
-#pragma unroll
-            for (int j = 0; j < J; ++j) sPq[tt][j][c] = lq[j] * iz;
-        }
-        __syncthreads();
+    // E = dL/dW_T (or 0), [i][col]
+    for (int e = tid; e < DK * N; e += kThreads) {
+        const int i = e / N, col = e % N, j = col / DB, dd = col % DB;
+        sE[i][col] = a.grad_state ? a.grad_state[sbase + ((size_t)j * DK + i) * Dv + d0 + dd] : 0.0f;
+    }
+    // this lane's column in the sequential wave
+    const int sj = lane % JP, sdd = lane / JP;
+    const bool sact = tid < 64 && lane < NL && sj < J;
+    const int scol = sact ? sj * DB + sdd : 0;
 
-        for (int tt = nt - 1; tt >= 0; --tt) {
-            const int t = t0 + tt;
-            if (t % kCB == kCB - 1 || t == T - 1) {
-                // E_n: dL/dw_t from the tokens after t (the last token of chunk n)
-                float *ck = a.eck + ((((size_t)b * H + h) * NCH + t / kCB) * Dv + d) * J * DK;
+    // Each chunk's HBM inputs are fetched into registers while the previous
+    // (later) chunk computes: K and Q rows as float4, and per (token, output
+    // dim) the J errors and logits and dL/do.
+    constexpr int NKQ = (kRC * (DK / 4) + kThreads - 1) / kThreads;
+    constexpr int NSC = (kRC * DB + kThreads - 1) / kThreads;
+    uint4 pk[NKQ], pq[NKQ];
+    float pdl[NSC][J];
+    uint32_t plk[NSC][J], plq[NSC][J], plb[NSC][J], pdo[NSC];
+    auto fetch = [&](int n) {
+        const int t0 = n * kRC, nt = min(kRC, T - t0);
 #pragma unroll
-                for (int j = 0; j < J; ++j)
-#pragma unroll
-                    for (int s = 0; s < S; s += 4)
-                        *reinterpret_cast<float4 *>(ck + j * DK + l * S + s) =
-                            make_float4(G[j][s], G[j][s + 1], G[j][s + 2], G[j][s + 3]);
+        for (int x = 0; x < NKQ; ++x) {
+            const int e = tid + kThreads * x, t = e / (DK / 4), i = (e % (DK / 4)) * 4;
+            pk[x] = pq[x] = make_uint4(0u, 0u, 0u, 0u);
+            if (e < kRC * (DK / 4) && t < nt) {
+                const size_t off = ((size_t)(b * T + t0 + t) * H + h) * DK + i;
+                pk[x] = raw4(f.k, off, ibf);
+                pq[x] = raw4(f.q, off, ibf);
             }
-            float kv[S], qv[S];
+        }
 #pragma unroll
-            for (int s = 0; s < S; s += 4) {
-                const float4 x = *reinterpret_cast<const float4 *>(&sK[tt][l][s]);
-                const float4 y = *reinterpret_cast<const float4 *>(&sQ[tt][l][s]);
-                kv[s] = x.x; kv[s + 1] = x.y; kv[s + 2] = x.z; kv[s + 3] = x.w;
-                qv[s] = y.x; qv[s + 1] = y.y; qv[s + 2] = y.z; qv[s + 3] = y.w;
-            }
-            const float dov = sDo[tt][dl];
-            // retrieval: o = sum_j pi^q_j w_{t,j} . q_t adds dy_j q_t to G_j
-            float dc[J];
+        for (int x = 0; x < NSC; ++x) {
+            const int e = tid + kThreads * x, t = e / DB, dd = e % DB;
+            pdo[x] = 0u;
 #pragma unroll
             for (int j = 0; j < J; ++j) {
-                const float dy = dov * sPq[tt][j][dl];
-                float acc = 0.0f;
+                pdl[x][j] = 0.0f;
+                plk[x][j] = plq[x][j] = plb[x][j] = 0u;
+            }
+            if (e < kRC * DB && t < nt) {
+                const size_t row = (size_t)(b * T + t0 + t) * H + h;
+                pdo[x] = raw1(a.grad_o, row * Dv + d0 + dd, obf);
 #pragma unroll
-                for (int s = 0; s < S; ++s) {
-                    G[j][s] = fmaf(dy, qv[s], G[j][s]);
-                    acc = fmaf(G[j][s], kv[s], acc);
+                for (int j = 0; j < J; ++j) {
+                    const size_t idx = (row * J + j) * Dv + d0 + dd;
+                    pdl[x][j] = a.delta[idx];
+                    plk[x][j] = raw1(f.lk, idx, ibf);
+                    plq[x][j] = raw1(f.lq, idx, ibf);
+                    plb[x][j] = raw1(f.lb, idx, ibf);
                 }
-                dc[j] = acc;
             }
-#pragma unroll
-            for (int j = 0; j < J; ++j) dc[j] = group_sum<L>(dc[j]);
+        }
+    };
+    fetch(NCH - 1);
 
-            // r of token t from its errors, as in the forward
-            float delta[J], e[J];
-            float m = -INFINITY;
-#pragma unroll
-            for (int j = 0; j < J; ++j) {
-                delta[j] = sDelta[tt][j][dl];
-                e[j] = sLk[tt][j][dl] - 0.5f * delta[j] * delta[j];
-                m = fmaxf(m, e[j]);
+    for (int n = NCH - 1; n >= 0; --n) {
+        const int t0 = n * kRC, nt = min(kRC, T - t0);
+        block_sync_lds();   // E is complete; the previous chunk's staging is consumed
+        // E_m (the gradient from the tokens after checkpoint interval m) before
+        // the interval's last reverse chunk runs: [.., m, d, j, i]
+        if (n % R2 == R2 - 1 || n == NCH - 1) {
+            const int m = n / R2;
+            float *ck = a.eck + (((size_t)b * H + h) * NC2 + m) * Dv * J * DK;
+            for (int e = tid; e < DB * J * DK; e += kThreads) {
+                const int dd = e / (J * DK), j = (e / DK) % J, i = e % DK;
+                ck[(size_t)(d0 + dd) * J * DK + j * DK + i] = sE[i][j * DB + dd];
             }
-            float z = 0.0f;
+        }
 #pragma unroll
-            for (int j = 0; j < J; ++j) {
-                e[j] = exp_fast(e[j] - m);
-                z += e[j];
+        for (int x = 0; x < NKQ; ++x) {
+            const int e = tid + kThreads * x, t = e / (DK / 4), i = (e % (DK / 4)) * 4;
+            if (e >= kRC * (DK / 4)) break;
+            const float4 kv = cvt4(pk[x], ibf), qv = cvt4(pq[x], ibf);
+            *reinterpret_cast<float4 *>(&sK[t][i]) = kv;
+            *reinterpret_cast<float4 *>(&sQ[t][i]) = qv;
+            sKt[i][t] = kv.x, sKt[i + 1][t] = kv.y, sKt[i + 2][t] = kv.z, sKt[i + 3][t] = kv.w;
+            sQt[i][t] = qv.x, sQt[i + 1][t] = qv.y, sQt[i + 2][t] = qv.z, sQt[i + 3][t] = qv.w;
+        }
+#pragma unroll
+        for (int x = 0; x < NSC; ++x) {
+            const int e = tid + kThreads * x, t = e / DB, dd = e % DB;
+            if (e >= kRC * DB) break;
+            float dl[J], ee[J], lq[J], be[J];
+            const float dov = cvt1(pdo[x], obf);
+            if (t < nt) {
+                float m = -INFINITY, mq = -INFINITY;
+#pragma unroll
+                for (int j = 0; j < J; ++j) {
+                    dl[j] = pdl[x][j];
+                    ee[j] = cvt1(plk[x][j], ibf) - 0.5f * dl[j] * dl[j];
+                    lq[j] = cvt1(plq[x][j], ibf);
+                    be[j] = 1.0f / (1.0f + exp_fast(-cvt1(plb[x][j], ibf)));
+                    m = fmaxf(m, ee[j]);
+                    mq = fmaxf(mq, lq[j]);
+                }
+                float z = 0.0f, zq = 0.0f;
+#pragma unroll
+                for (int j = 0; j < J; ++j) {
+                    ee[j] = exp_fast(ee[j] - m);
+                    z += ee[j];
+                    lq[j] = exp_fast(lq[j] - mq);
+                    zq += lq[j];
+                }
+                const float iz = 1.0f / z, izq = 1.0f / zq;
+#pragma unroll
+                for (int j = 0; j < J; ++j) {
+                    ee[j] = J == 1 ? 1.0f : ee[j] * iz;       // r
+                    lq[j] = J == 1 ? 1.0f : lq[j] * izq;      // pi^q
+                }
+            } else {
+#pragma unroll
+                for (int j = 0; j < J; ++j) dl[j] = ee[j] = lq[j] = be[j] = 0.0f;
             }
-            const float iz = 1.0f / z;
-            float r[J], dr[J];
-            float sdr = 0.0f;
 #pragma unroll
             for (int j = 0; j < J; ++j) {
-                r[j] = J == 1 ? 1.0f : e[j] * iz;
-                dr[j] = dc[j] * sBeta[tt][j][dl] * delta[j];
-                sdr = fmaf(r[j], dr[j], sdr);
+                const int col = j * DB + dd;
+                sDelta[t][col] = dl[j];
+                sR[t][col] = ee[j];
+                sBeta[t][col] = be[j];
+                sY[t][col] = dov * lq[j];
             }
-            const size_t row = (size_t)(b * T + t) * H + h;
-            float dvv = 0.0f;
+        }
+        block_sync_lds();
+        if (n > 0) fetch(n - 1);   // lands while this chunk computes
+        // Gram products of the chunk: one (t, s) pair per thread
+        {
+            const int t = tid / kRC, s2 = tid % kRC;
+            float gkk = 0.0f, gkq = 0.0f;
+#pragma unroll 4
+            for (int i = 0; i < DK; i += 4) {
+                const float4 kt = *reinterpret_cast<const float4 *>(&sK[t][i]);
+                const float4 ks = *reinterpret_cast<const float4 *>(&sK[s2][i]);
+                const float4 qs = *reinterpret_cast<const float4 *>(&sQ[s2][i]);
+                gkk = fmaf(kt.x, ks.x, fmaf(kt.y, ks.y, fmaf(kt.z, ks.z, fmaf(kt.w, ks.w, gkk))));
+                gkq = fmaf(kt.x, qs.x, fmaf(kt.y, qs.y, fmaf(kt.z, qs.z, fmaf(kt.w, qs.w, gkq))));
+            }
+            sGkk[t][s2] = gkk;
+            sGkqT[s2][t] = gkq;
+        }
+        block_sync_lds();
+        // base_t = k_t . E + sum_{s>=t} (k_t . q_s) dy_s: four tokens per thread
+        for (int e = tid; e < (kRC / 4) * N; e += kThreads) {
+            const int t4 = (e / N) * 4, col = e % N;
+            float acc[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 8
+            for (int i = 0; i < DK; ++i) {
+                const float4 kv = *reinterpret_cast<const float4 *>(&sKt[i][t4]);
+                const float ev = sE[i][col];
+                acc[0] = fmaf(kv.x, ev, acc[0]);
+                acc[1] = fmaf(kv.y, ev, acc[1]);
+                acc[2] = fmaf(kv.z, ev, acc[2]);
+                acc[3] = fmaf(kv.w, ev, acc[3]);
+            }
+            for (int s2 = t4; s2 < kRC; ++s2) {
+                const float4 gq = *reinterpret_cast<const float4 *>(&sGkqT[s2][t4]);
+                const float yv = sY[s2][col];
+                // only s >= t: token t4 + x takes s2 >= t4 + x
+                acc[0] = fmaf(gq.x, yv, acc[0]);
+                if (s2 >= t4 + 1) acc[1] = fmaf(gq.y, yv, acc[1]);
+                if (s2 >= t4 + 2) acc[2] = fmaf(gq.z, yv, acc[2]);
+                if (s2 >= t4 + 3) acc[3] = fmaf(gq.w, yv, acc[3]);
+            }
 #pragma unroll
-            for (int j = 0; j < J; ++j) {
-                const float beta = sBeta[tt][j][dl];
-                // (J = 1: a softmax over one component is constant; written as
-                // 0 because the contracted dr - sum r dr leaves a rounding residue)
-                const float da = J == 1 ? 0.0f : r[j] * (dr[j] - sdr);
-                const float ddelta = dc[j] * beta * r[j] - delta[j] * da;
-                dvv += ddelta;
+            for (int x = 0; x < 4; ++x) sBase[t4 + x][col] = acc[x];
+        }
+        block_sync_lds();
+        if (tid < 64) {
+            // the chunk's tokens in reverse; dfr[u] collects sum_{s>u} (k_u . k_s) dpred_s
+            float dfr[kRC], vb[kRC], vd[kRC], vbe[kRC], vr[kRC];
+#pragma unroll
+            for (int u = 0; u < kRC; ++u) {
+                dfr[u] = 0.0f;
+                vb[u] = sact ? sBase[u][scol] : 0.0f;
+                vd[u] = sact ? sDelta[u][scol] : 0.0f;
+                vbe[u] = sact ? sBeta[u][scol] : 0.0f;
+                vr[u] = sact ? sR[u][scol] : 0.0f;
+            }
+#pragma unroll
+            for (int t = kRC - 1; t >= 0; --t) {
+                float grow[kRC];   // row t of K K^T (= column t), the part u < t
+#pragma unroll
+                for (int u4 = 0; u4 < (t + 3) / 4; ++u4) {
+                    const float4 x = *reinterpret_cast<const float4 *>(&sGkk[t][4 * u4]);
+                    grow[4 * u4] = x.x, grow[4 * u4 + 1] = x.y;
+                    grow[4 * u4 + 2] = x.z, grow[4 * u4 + 3] = x.w;
+                }
+                const float dc = vb[t] + dfr[t];
+                const float dl = vd[t], be = vbe[t], r = vr[t];
+                const float dr = dc * be * dl;
+                const float sdr = group_sum<JP>(r * dr);
+                const float da = J == 1 ? 0.0f : r * (dr - sdr);
+                const float ddelta = dc * be * r - dl * da;
+                const float dvv = group_sum<JP>(ddelta);
                 const float dpred = -ddelta;
 #pragma unroll
-                for (int s = 0; s < S; ++s) G[j][s] = fmaf(dpred, kv[s], G[j][s]);
-                if (l == 0) {
-                    const size_t idx = (row * J + j) * Dv + d;
-                    a.dlb[idx] = dc[j] * r[j] * delta[j] * beta * (1.0f - beta);
-                    a.dlk[idx] = da;
-                    a.dpred[idx] = dpred;
+                for (int u = 0; u < t; ++u) dfr[u] = fmaf(grow[u], dpred, dfr[u]);
+                if (sact) {
+                    sP[t][scol] = dpred;
+                    sDlb[t][scol] = dc * r * dl * be * (1.0f - be);
+                    sDlk[t][scol] = da;
+                    if (sj == 0) sDv[t][sdd] = dvv;
                 }
             }
-            if (l == 0) a.dv[row * Dv + d] = dvv;
+        }
+        block_sync_lds();
+        // E += Q^T Y + K^T P (E now from the tokens after the previous chunk):
+        // four columns per thread
+        for (int e = tid; e < DK * (N / 4); e += kThreads) {
+            const int i = e / (N / 4), c4 = (e % (N / 4)) * 4;
+            float4 acc = *reinterpret_cast<const float4 *>(&sE[i][c4]);
+#pragma unroll
+            for (int t4 = 0; t4 < kRC; t4 += 4) {
+                const float4 qv = *reinterpret_cast<const float4 *>(&sQt[i][t4]);
+                const float4 kv = *reinterpret_cast<const float4 *>(&sKt[i][t4]);
+                const float qa[4] = {qv.x, qv.y, qv.z, qv.w}, ka[4] = {kv.x, kv.y, kv.z, kv.w};
+#pragma unroll
+                for (int x = 0; x < 4; ++x) {
+                    const float4 y = *reinterpret_cast<const float4 *>(&sY[t4 + x][c4]);
+                    const float4 p = *reinterpret_cast<const float4 *>(&sP[t4 + x][c4]);
+                    acc.x = fmaf(qa[x], y.x, fmaf(ka[x], p.x, acc.x));
+                    acc.y = fmaf(qa[x], y.y, fmaf(ka[x], p.y, acc.y));
+                    acc.z = fmaf(qa[x], y.z, fmaf(ka[x], p.z, acc.z));
+                    acc.w = fmaf(qa[x], y.w, fmaf(ka[x], p.w, acc.w));
+                }
+            }
+            *reinterpret_cast<float4 *>(&sE[i][c4]) = acc;
+        }
+        // the chunk's per-token outputs, coalesced over output dims
+        for (int e = tid; e < nt * J * DB; e += kThreads) {
+            const int t = e / (J * DB), j = (e / DB) % J, dd = e % DB;
+            const int col = j * DB + dd;
+            const size_t idx = (((size_t)(b * T + t0 + t) * H + h) * J + j) * Dv + d0 + dd;
+            a.dlb[idx] = sDlb[t][col];
+            a.dlk[idx] = sDlk[t][col];
+            a.dpred[idx] = sP[t][col];
+        }
+        for (int e = tid; e < nt * DB; e += kThreads) {
+            const int t = e / DB, dd = e % DB;
+            a.dv[((size_t)(b * T + t0 + t) * H + h) * Dv + d0 + dd] = sDv[t][dd];
         }
     }
+    block_sync_lds();
     if (a.dstate) {
-#pragma unroll
-        for (int j = 0; j < J; ++j)
-#pragma unroll
-            for (int s = 0; s < S; ++s)
-                a.dstate[sbase + ((size_t)j * DK + l * S + s) * Dv + d] = G[j][s];
+        for (int e = tid; e < J * DK * DB; e += kThreads) {
+            const int j = e / (DK * DB), i = (e / DB) % DK, dd = e % DB;
+            a.dstate[sbase + ((size_t)j * DK + i) * Dv + d0 + dd] = sE[i][j * DB + dd];
+        }
     }
 }
 
@@ -277,16 +422,16 @@ __global__ __launch_bounds__(kThreads) void bwd_chunk_kernel(BackwardArgs a) {
 
     for (int g = tid; g < kCB * (DK / 4); g += kThreads) {
         const int t = g / (DK / 4), i = (g % (DK / 4)) * 4;
-        float4 kv = make_float4(0.f, 0.f, 0.f, 0.f), qv = kv;
+        uint4 kr = make_uint4(0u, 0u, 0u, 0u), qr = kr;
         if (t < nt) {
             const size_t off = ((size_t)(b * T + t0 + t) * H + h) * DK + i;
-            kv = load4(f.k, off, ibf);
-            qv = load4(f.q, off, ibf);
+            kr = raw4(f.k, off, ibf);
+            qr = raw4(f.q, off, ibf);
         }
-        *reinterpret_cast<float4 *>(&sK[t][i]) = kv;
-        *reinterpret_cast<float4 *>(&sQ[t][i]) = qv;
+        *reinterpret_cast<float4 *>(&sK[t][i]) = cvt4(kr, ibf);
+        *reinterpret_cast<float4 *>(&sQ[t][i]) = cvt4(qr, ibf);
     }
-    __syncthreads();
+    block_sync_lds();
     {   // Q K^T: row gt, columns gt8 + 8 x
         float qk[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll 4
@@ -316,7 +461,7 @@ __global__ __launch_bounds__(kThreads) void bwd_chunk_kernel(BackwardArgs a) {
     // checkpoints of this chunk, [Dv][J][DK]
     const size_t ck0 = (((size_t)b * H + h) * NCH + n) * Dv * J * DK;
     for (int dt0 = 0; dt0 < Dv; dt0 += DT) {
-        __syncthreads();   // the previous tile is consumed
+        block_sync_lds();   // the previous tile is consumed
         for (int g = tid; g < DT * J * (DK / 4); g += kThreads) {
             const int e = 4 * g;
             const int dd = e / (J * DK), j = (e / DK) % J, i = e % DK;
@@ -331,15 +476,24 @@ __global__ __launch_bounds__(kThreads) void bwd_chunk_kernel(BackwardArgs a) {
             float c[J], p[J], y[J], pq[J];
             if (t < nt) {
                 const size_t row = (size_t)(b * T + t0 + t) * H + h;
-                const float dov = load1(a.grad_o, row * Dv + dt0 + dd, obf);
-                float delta[J], e[J], lq[J];
-                float m = -INFINITY, mq = -INFINITY;
+                const uint32_t rdo = raw1(a.grad_o, row * Dv + dt0 + dd, obf);
+                float delta[J], e[J], lq[J], pp[J];
+                uint32_t rlk[J], rlq[J], rlb[J];
 #pragma unroll
                 for (int j = 0; j < J; ++j) {
                     const size_t idx = (row * J + j) * Dv + dt0 + dd;
                     delta[j] = a.delta[idx];
-                    e[j] = load1(f.lk, idx, ibf) - 0.5f * delta[j] * delta[j];
-                    lq[j] = load1(f.lq, idx, ibf);
+                    pp[j] = a.dpred[idx];
+                    rlk[j] = raw1(f.lk, idx, ibf);
+                    rlq[j] = raw1(f.lq, idx, ibf);
+                    rlb[j] = raw1(f.lb, idx, ibf);
+                }
+                const float dov = cvt1(rdo, obf);
+                float m = -INFINITY, mq = -INFINITY;
+#pragma unroll
+                for (int j = 0; j < J; ++j) {
+                    e[j] = cvt1(rlk[j], ibf) - 0.5f * delta[j] * delta[j];
+                    lq[j] = cvt1(rlq[j], ibf);
                     m = fmaxf(m, e[j]);
                     mq = fmaxf(mq, lq[j]);
                 }
@@ -354,10 +508,9 @@ __global__ __launch_bounds__(kThreads) void bwd_chunk_kernel(BackwardArgs a) {
                 const float iz = 1.0f / z, izq = 1.0f / zq;
 #pragma unroll
                 for (int j = 0; j < J; ++j) {
-                    const size_t idx = (row * J + j) * Dv + dt0 + dd;
-                    const float beta = 1.0f / (1.0f + exp_fast(-load1(f.lb, idx, ibf)));
+                    const float beta = 1.0f / (1.0f + exp_fast(-cvt1(rlb[j], ibf)));
                     c[j] = beta * (J == 1 ? 1.0f : e[j] * iz) * delta[j];
-                    p[j] = a.dpred[idx];
+                    p[j] = pp[j];
                     pq[j] = J == 1 ? 1.0f : lq[j] * izq;
                     y[j] = dov * pq[j];
                 }
@@ -378,7 +531,7 @@ __global__ __launch_bounds__(kThreads) void bwd_chunk_kernel(BackwardArgs a) {
                 sPq[t][cc] = pq[j];
             }
         }
-        __syncthreads();
+        block_sync_lds();
 
         // dq += Y S; dk += P S + C E (this tile's columns)
 #pragma unroll 4
@@ -435,7 +588,7 @@ __global__ __launch_bounds__(kThreads) void bwd_chunk_kernel(BackwardArgs a) {
 #pragma unroll
             for (int x = 0; x < NY; ++x) sYv[gt][gt8 + 8 * x] = yr[x];
         }
-        __syncthreads();
+        block_sync_lds();
         // dL/dlq_j = pi^q_j do (y_j - sum_i pi^q_i y_i); zero for one component
         for (int g = tid; g < nt * DT; g += kThreads) {
             const int t = g / DT, dd = g % DT;
@@ -457,14 +610,14 @@ __global__ __launch_bounds__(kThreads) void bwd_chunk_kernel(BackwardArgs a) {
         sA[gt][gs + x] = ga[x];
         sB[gt][gs + x] = gb[x];
     }
-    __syncthreads();
+    block_sync_lds();
     for (int g = tid; g < kCB * kCB; g += kThreads) {
         const int t = g / kCB, s = g % kCB;
         sM[0][t][s] = s <= t ? sA[t][s] : 0.0f;                          // (Y_t . C_s) k_s
         sM[1][t][s] = s > t ? sB[t][s] : (s < t ? sB[s][t] : 0.0f);      // (C_t.P_s), (P_t.C_s) k_s
         sM[2][t][s] = s >= t ? sA[s][t] : 0.0f;                          // (C_t . Y_s) q_s
     }
-    __syncthreads();
+    block_sync_lds();
 #pragma unroll 4
     for (int s = 0; s < kCB; ++s) {
         float kv[TN], qv[TN];
@@ -493,10 +646,19 @@ __global__ __launch_bounds__(kThreads) void bwd_chunk_kernel(BackwardArgs a) {
     }
 }
 
+template <int DK, int J, int DB>
+hipError_t launch_reverse(const BackwardArgs &a, hipStream_t stream) {
+    if constexpr ((J == 3 ? 4 : J) * DB > 64) {
+        return hipErrorInvalidValue;
+    } else {
+        hipLaunchKernelGGL((reverse_chunk_kernel<DK, J, DB>), dim3(a.f.Dv / DB, a.f.H, a.f.B),
+                           dim3(kThreads), 0, stream, a);
+        return hipGetLastError();
+    }
+}
+
 template <int DK, int J>
 hipError_t launch_bwd_dk_j(const BackwardArgs &a, hipStream_t stream) {
-    constexpr int S = (J <= 4) ? (DK < 16 ? DK : 16) : (DK < 8 ? DK : 8);
-    constexpr int L = DK / S;
     const LayerArgs &f = a.f;
     LayerArgs fa = f;
     fa.o = nullptr;
@@ -508,10 +670,19 @@ hipError_t launch_bwd_dk_j(const BackwardArgs &a, hipStream_t stream) {
     // take the token-by-token scan, as their forward does
     hipError_t e = f.in_bf16 ? launch_scan_pipe(fa, stream) : launch_scan_direct_aux(fa, stream);
     if (e != hipSuccess) return e;
-    const int ncol = f.Dv < rev_cols(L, J) ? f.Dv : rev_cols(L, J);
-    hipLaunchKernelGGL((scan_reverse_kernel<DK, J, S>), dim3(f.Dv / ncol, f.H, f.B),
-                       dim3(ncol * L), 0, stream, a, ncol);
-    e = hipGetLastError();
+    // reverse scan: 64 sequential lanes per block (DB = 64 / JP output dims), or
+    // half as many (and twice the blocks) while the grid would leave compute
+    // units idle
+    constexpr int JP = J == 3 ? 4 : J;
+    int db = 64 / JP < f.Dv ? 64 / JP : f.Dv;
+    if ((long)(f.Dv / db) * f.H * f.B < 256 && db >= 16) db /= 2;
+    switch (db) {
+        case 64: e = launch_reverse<DK, J, 64>(a, stream); break;
+        case 32: e = launch_reverse<DK, J, 32>(a, stream); break;
+        case 16: e = launch_reverse<DK, J, 16>(a, stream); break;
+        case 8: e = launch_reverse<DK, J, 8>(a, stream); break;
+        default: return hipErrorInvalidValue;
+    }
     if (e != hipSuccess) return e;
     const int NCH = (f.T + kCB - 1) / kCB;
     hipLaunchKernelGGL((bwd_chunk_kernel<DK, J>), dim3(NCH, f.H, f.B), dim3(kThreads), 0, stream,
