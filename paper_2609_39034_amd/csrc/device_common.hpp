@@ -40,6 +40,32 @@ __device__ __forceinline__ float load1(const void *base, size_t idx, bool bf16) 
     return static_cast<const float *>(base)[idx];
 }
 
+// Raw loads: the bits of one element (a bf16 in the low half, or an fp32), or
+// of four, converted to fp32 only where they are used.  Loading and converting
+// in one step makes each load wait for its data before the next is issued;
+// these let a staging loop issue all of its loads first.
+__device__ __forceinline__ uint32_t raw1(const void *base, size_t idx, bool bf16) {
+    return bf16 ? (uint32_t) static_cast<const uint16_t *>(base)[idx]
+                : static_cast<const uint32_t *>(base)[idx];
+}
+__device__ __forceinline__ float cvt1(uint32_t r, bool bf16) {
+    return __uint_as_float(bf16 ? r << 16 : r);
+}
+__device__ __forceinline__ uint4 raw4(const void *base, size_t idx, bool bf16) {
+    if (bf16) {
+        const uint2 x = *reinterpret_cast<const uint2 *>(static_cast<const uint16_t *>(base) + idx);
+        return make_uint4(x.x, x.y, 0u, 0u);
+    }
+    return *reinterpret_cast<const uint4 *>(static_cast<const float *>(base) + idx);
+}
+__device__ __forceinline__ float4 cvt4(uint4 r, bool bf16) {
+    if (bf16)
+        return make_float4(__uint_as_float(r.x << 16), __uint_as_float(r.x & 0xffff0000u),
+                           __uint_as_float(r.y << 16), __uint_as_float(r.y & 0xffff0000u));
+    return make_float4(__uint_as_float(r.x), __uint_as_float(r.y), __uint_as_float(r.z),
+                       __uint_as_float(r.w));
+}
+
 __device__ __forceinline__ void store1(void *base, size_t idx, float x, bool bf16) {
     if (bf16)
         static_cast<uint16_t *>(base)[idx] = f32_to_bf16_bits(x);

@@ -119,34 +119,83 @@ __global__ __launch_bounds__(kThreads) void scan_direct_kernel(LayerArgs a, int 
                 store1(a.o, ((size_t)(b * T + t0 - kTC + tt) * H + h) * Dv + d0 + c, sO[tt][c], obf);
             }
         }
-        for (int g = tid; g < nt * (DK / 4); g += nthr) {
-            const int tt = g / (DK / 4), i = (g % (DK / 4)) * 4;
-            const size_t off = ((size_t)(b * T + t0 + tt) * H + h) * DK + i;
-            *reinterpret_cast<float4 *>(&sK[tt][i / S][i % S]) = load4(a.k, off, ibf);
-            *reinterpret_cast<float4 *>(&sQ[tt][i / S][i % S]) = load4(a.q, off, ibf);
+        // Staging issues every load of a batch before it converts anything:
+        // loading and converting element by element would make each load wait
+        // for its data before the next one is issued.
+        {   // K and Q rows (at most S / 4 per thread: ncol >= 16)
+            constexpr int NKQ = S / 4;
+            uint4 rk[NKQ], rq[NKQ];
+#pragma unroll
+            for (int x = 0; x < NKQ; ++x) {
+                const int g = tid + x * nthr;
+                if (g < nt * (DK / 4)) {
+                    const int tt = g / (DK / 4), i = (g % (DK / 4)) * 4;
+                    const size_t off = ((size_t)(b * T + t0 + tt) * H + h) * DK + i;
+                    rk[x] = raw4(a.k, off, ibf);
+                    rq[x] = raw4(a.q, off, ibf);
+                }
+            }
+#pragma unroll
+            for (int x = 0; x < NKQ; ++x) {
+                const int g = tid + x * nthr;
+                if (g < nt * (DK / 4)) {
+                    const int tt = g / (DK / 4), i = (g % (DK / 4)) * 4;
+                    *reinterpret_cast<float4 *>(&sK[tt][i / S][i % S]) = cvt4(rk[x], ibf);
+                    *reinterpret_cast<float4 *>(&sQ[tt][i / S][i % S]) = cvt4(rq[x], ibf);
+                }
+            }
         }
-        if constexpr (GT) {
-            for (int g = tid; g < nt * J * (DK / 4); g += nthr) {
-                const int tt = g / (J * (DK / 4)), rem = g % (J * (DK / 4));
-                const int j = rem / (DK / 4), i = (rem % (DK / 4)) * 4;
-                const float4 x = load4(
-                    a.decay, (((size_t)(b * T + t0 + tt) * H + h) * J + j) * DK + i, ibf);
-                *reinterpret_cast<float4 *>(&sA[tt][j][i]) =
-                    make_float4(sigmoid(x.x), sigmoid(x.y), sigmoid(x.z), sigmoid(x.w));
+        if constexpr (GT) {   // decay gates, four rows of four per thread at a time
+            constexpr int ND = J * S / 4;
+            for (int x0 = 0; x0 < ND; x0 += 4) {
+                uint4 rd[4];
+#pragma unroll
+                for (int x = 0; x < 4; ++x) {
+                    const int g = tid + (x0 + x) * nthr;
+                    if (x0 + x < ND && g < nt * J * (DK / 4)) {
+                        const int tt = g / (J * (DK / 4)), rem = g % (J * (DK / 4));
+                        const int j = rem / (DK / 4), i = (rem % (DK / 4)) * 4;
+                        rd[x] = raw4(a.decay, (((size_t)(b * T + t0 + tt) * H + h) * J + j) * DK + i,
+                                     ibf);
+                    }
+                }
+#pragma unroll
+                for (int x = 0; x < 4; ++x) {
+                    const int g = tid + (x0 + x) * nthr;
+                    if (x0 + x < ND && g < nt * J * (DK / 4)) {
+                        const int tt = g / (J * (DK / 4)), rem = g % (J * (DK / 4));
+                        const int j = rem / (DK / 4), i = (rem % (DK / 4)) * 4;
+                        const float4 v4 = cvt4(rd[x], ibf);
+                        *reinterpret_cast<float4 *>(&sA[tt][j][i]) =
+                            make_float4(sigmoid(v4.x), sigmoid(v4.y), sigmoid(v4.z), sigmoid(v4.w));
+                    }
+                }
             }
         }
         for (int g = tid; g < nt * ncol; g += nthr) {
             const int tt = g / ncol, c = g % ncol;
             const size_t row = (size_t)(b * T + t0 + tt) * H + h;
-            sV[tt][c] = load1(a.v, row * Dv + d0 + c, ibf);
+            uint32_t rv, rb[J], rk[J], rq[J], rgk = 0u, rgq = 0u;
+            rv = raw1(a.v, row * Dv + d0 + c, ibf);
+#pragma unroll
+            for (int j = 0; j < J; ++j) {
+                const size_t idx = (row * J + j) * Dv + d0 + c;
+                rb[j] = raw1(a.lb, idx, ibf);
+                rk[j] = raw1(a.lk, idx, ibf);
+                rq[j] = raw1(a.lq, idx, ibf);
+            }
+            if constexpr (TP) {
+                rgk = raw1(a.gk, row * Dv + d0 + c, ibf);
+                rgq = raw1(a.gq, row * Dv + d0 + c, ibf);
+            }
+            sV[tt][c] = cvt1(rv, ibf);
             float lq[J], lk[J];
             float m = -INFINITY, mk = -INFINITY;
 #pragma unroll
             for (int j = 0; j < J; ++j) {
-                const size_t idx = (row * J + j) * Dv + d0 + c;
-                sBeta[tt][j][c] = 1.0f / (1.0f + exp_fast(-load1(a.lb, idx, ibf)));
-                lk[j] = load1(a.lk, idx, ibf);
-                lq[j] = load1(a.lq, idx, ibf);
+                sBeta[tt][j][c] = 1.0f / (1.0f + exp_fast(-cvt1(rb[j], ibf)));
+                lk[j] = cvt1(rk[j], ibf);
+                lq[j] = cvt1(rq[j], ibf);
                 m = fmaxf(m, lq[j]);
                 mk = fmaxf(mk, lk[j]);
             }
@@ -168,8 +217,8 @@ __global__ __launch_bounds__(kThreads) void scan_direct_kernel(LayerArgs a, int 
                 sLk[tt][j][c] = TP ? lk[j] * izk : lk[j];   // temporal: pi^k itself
             }
             if constexpr (TP) {
-                sG[0][tt][c] = 1.0f / (1.0f + exp_fast(-load1(a.gk, row * Dv + d0 + c, ibf)));
-                sG[1][tt][c] = 1.0f / (1.0f + exp_fast(-load1(a.gq, row * Dv + d0 + c, ibf)));
+                sG[0][tt][c] = 1.0f / (1.0f + exp_fast(-cvt1(rgk, ibf)));
+                sG[1][tt][c] = 1.0f / (1.0f + exp_fast(-cvt1(rgq, ibf)));
             }
         }
         __syncthreads();
