@@ -112,7 +112,7 @@ __global__ __launch_bounds__(kThreads) void scan_direct_kernel(LayerArgs a, int 
                             make_float4(w[j][s], w[j][s + 1], w[j][s + 2], w[j][s + 3]);
             }
         }
-        __syncthreads();
+        block_sync_lds();
         if (!AX && t0 > 0) {  // outputs of the previous (full) round
             for (int g = tid; g < kTC * ncol; g += nthr) {
                 const int tt = g / ncol, c = g % ncol;
@@ -121,9 +121,21 @@ __global__ __launch_bounds__(kThreads) void scan_direct_kernel(LayerArgs a, int 
         }
         // Staging issues every load of a batch before it converts anything:
         // loading and converting element by element would make each load wait
-        // for its data before the next one is issued.
-        {   // K and Q rows (at most S / 4 per thread: ncol >= 16)
-            constexpr int NKQ = S / 4;
+        // for its data before the next one is issued.  The block barriers order
+        // LDS traffic only: the global stores of outputs need no ordering here,
+        // and a full barrier would wait for them.
+        {
+            // K and Q rows and the first batch of per-(token, column) scalars are
+            // all issued before anything converts; the decay gates follow in
+            // batches of their own.
+            constexpr int NKQ = S / 4;                // K/Q pieces per thread at most (ncol >= 16)
+            constexpr int ND = GT ? J * S / 4 : 0;    // decay pieces per thread at most
+            constexpr int NI = kTC / L;               // scalar items per thread at most
+            // scalar items loaded together: a register budget over the values
+            // of an item
+            constexpr int NBR = 56 / (1 + 3 * J + (TP ? 2 : 0));
+            constexpr int NB = NBR < 1 ? 1 : (NBR < NI ? NBR : NI);
+            constexpr int NDB = ND < 4 ? ND : 4;      // decay pieces loaded together
             uint4 rk[NKQ], rq[NKQ];
 #pragma unroll
             for (int x = 0; x < NKQ; ++x) {
@@ -135,93 +147,108 @@ __global__ __launch_bounds__(kThreads) void scan_direct_kernel(LayerArgs a, int 
                     rq[x] = raw4(a.q, off, ibf);
                 }
             }
-#pragma unroll
-            for (int x = 0; x < NKQ; ++x) {
+            auto dpiece = [&](int x, int &tt, int &j, int &i) {
                 const int g = tid + x * nthr;
-                if (g < nt * (DK / 4)) {
-                    const int tt = g / (DK / 4), i = (g % (DK / 4)) * 4;
-                    *reinterpret_cast<float4 *>(&sK[tt][i / S][i % S]) = cvt4(rk[x], ibf);
-                    *reinterpret_cast<float4 *>(&sQ[tt][i / S][i % S]) = cvt4(rq[x], ibf);
-                }
-            }
-        }
-        if constexpr (GT) {   // decay gates, four rows of four per thread at a time
-            constexpr int ND = J * S / 4;
-            for (int x0 = 0; x0 < ND; x0 += 4) {
-                uint4 rd[4];
+                tt = g / (J * (DK / 4));
+                const int rem = g % (J * (DK / 4));
+                j = rem / (DK / 4), i = (rem % (DK / 4)) * 4;
+                return g < nt * J * (DK / 4);
+            };
+            for (int i0 = 0; i0 < NI; i0 += NB) {
+                uint32_t rv[NB], rb[NB][J], rlk[NB][J], rlq[NB][J], rgk[NB], rgq[NB];
 #pragma unroll
-                for (int x = 0; x < 4; ++x) {
-                    const int g = tid + (x0 + x) * nthr;
-                    if (x0 + x < ND && g < nt * J * (DK / 4)) {
-                        const int tt = g / (J * (DK / 4)), rem = g % (J * (DK / 4));
-                        const int j = rem / (DK / 4), i = (rem % (DK / 4)) * 4;
-                        rd[x] = raw4(a.decay, (((size_t)(b * T + t0 + tt) * H + h) * J + j) * DK + i,
-                                     ibf);
+                for (int x = 0; x < NB; ++x) {
+                    const int g = tid + (i0 + x) * nthr;
+                    if (g < nt * ncol) {
+                        const int tt = g / ncol, c = g % ncol;
+                        const size_t row = (size_t)(b * T + t0 + tt) * H + h;
+                        rv[x] = raw1(a.v, row * Dv + d0 + c, ibf);
+#pragma unroll
+                        for (int j = 0; j < J; ++j) {
+                            const size_t idx = (row * J + j) * Dv + d0 + c;
+                            rb[x][j] = raw1(a.lb, idx, ibf);
+                            rlk[x][j] = raw1(a.lk, idx, ibf);
+                            rlq[x][j] = raw1(a.lq, idx, ibf);
+                        }
+                        if constexpr (TP) {
+                            rgk[x] = raw1(a.gk, row * Dv + d0 + c, ibf);
+                            rgq[x] = raw1(a.gq, row * Dv + d0 + c, ibf);
+                        }
+                    }
+                }
+                if (i0 == 0) {
+#pragma unroll
+                    for (int x = 0; x < NKQ; ++x) {
+                        const int g = tid + x * nthr;
+                        if (g < nt * (DK / 4)) {
+                            const int tt = g / (DK / 4), i = (g % (DK / 4)) * 4;
+                            *reinterpret_cast<float4 *>(&sK[tt][i / S][i % S]) = cvt4(rk[x], ibf);
+                            *reinterpret_cast<float4 *>(&sQ[tt][i / S][i % S]) = cvt4(rq[x], ibf);
+                        }
                     }
                 }
 #pragma unroll
-                for (int x = 0; x < 4; ++x) {
-                    const int g = tid + (x0 + x) * nthr;
-                    if (x0 + x < ND && g < nt * J * (DK / 4)) {
-                        const int tt = g / (J * (DK / 4)), rem = g % (J * (DK / 4));
-                        const int j = rem / (DK / 4), i = (rem % (DK / 4)) * 4;
-                        const float4 v4 = cvt4(rd[x], ibf);
-                        *reinterpret_cast<float4 *>(&sA[tt][j][i]) =
-                            make_float4(sigmoid(v4.x), sigmoid(v4.y), sigmoid(v4.z), sigmoid(v4.w));
+                for (int x = 0; x < NB; ++x) {
+                    const int g = tid + (i0 + x) * nthr;
+                    if (g >= nt * ncol) continue;
+                    const int tt = g / ncol, c = g % ncol;
+                    sV[tt][c] = cvt1(rv[x], ibf);
+                    float lq[J], lk[J];
+                    float m = -INFINITY, mk = -INFINITY;
+#pragma unroll
+                    for (int j = 0; j < J; ++j) {
+                        sBeta[tt][j][c] = 1.0f / (1.0f + exp_fast(-cvt1(rb[x][j], ibf)));
+                        lk[j] = cvt1(rlk[x][j], ibf);
+                        lq[j] = cvt1(rlq[x][j], ibf);
+                        m = fmaxf(m, lq[j]);
+                        mk = fmaxf(mk, lk[j]);
+                    }
+                    float z = 0.0f, zk = 0.0f;
+#pragma unroll
+                    for (int j = 0; j < J; ++j) {
+                        lq[j] = exp_fast(lq[j] - m);
+                        z += lq[j];
+                        if constexpr (TP) {
+                            lk[j] = exp_fast(lk[j] - mk);
+                            zk += lk[j];
+                        }
+                    }
+                    const float iz = 1.0f / z;
+                    const float izk = TP ? 1.0f / zk : 1.0f;
+#pragma unroll
+                    for (int j = 0; j < J; ++j) {
+                        sPq[tt][j][c] = lq[j] * iz;
+                        sLk[tt][j][c] = TP ? lk[j] * izk : lk[j];   // temporal: pi^k itself
+                    }
+                    if constexpr (TP) {
+                        sG[0][tt][c] = 1.0f / (1.0f + exp_fast(-cvt1(rgk[x], ibf)));
+                        sG[1][tt][c] = 1.0f / (1.0f + exp_fast(-cvt1(rgq[x], ibf)));
+                    }
+                }
+            }
+            if constexpr (GT) {   // decay gates, in batches of their own
+                for (int x0 = 0; x0 < ND; x0 += NDB) {
+                    uint4 rd[NDB];
+#pragma unroll
+                    for (int x = 0; x < NDB; ++x) {
+                        int tt, j, i;
+                        if (x0 + x < ND && dpiece(x0 + x, tt, j, i))
+                            rd[x] = raw4(a.decay, (((size_t)(b * T + t0 + tt) * H + h) * J + j) * DK + i,
+                                         ibf);
+                    }
+#pragma unroll
+                    for (int x = 0; x < NDB; ++x) {
+                        int tt, j, i;
+                        if (x0 + x < ND && dpiece(x0 + x, tt, j, i)) {
+                            const float4 v4 = cvt4(rd[x], ibf);
+                            *reinterpret_cast<float4 *>(&sA[tt][j][i]) = make_float4(
+                                sigmoid(v4.x), sigmoid(v4.y), sigmoid(v4.z), sigmoid(v4.w));
+                        }
                     }
                 }
             }
         }
-        for (int g = tid; g < nt * ncol; g += nthr) {
-            const int tt = g / ncol, c = g % ncol;
-            const size_t row = (size_t)(b * T + t0 + tt) * H + h;
-            uint32_t rv, rb[J], rk[J], rq[J], rgk = 0u, rgq = 0u;
-            rv = raw1(a.v, row * Dv + d0 + c, ibf);
-#pragma unroll
-            for (int j = 0; j < J; ++j) {
-                const size_t idx = (row * J + j) * Dv + d0 + c;
-                rb[j] = raw1(a.lb, idx, ibf);
-                rk[j] = raw1(a.lk, idx, ibf);
-                rq[j] = raw1(a.lq, idx, ibf);
-            }
-            if constexpr (TP) {
-                rgk = raw1(a.gk, row * Dv + d0 + c, ibf);
-                rgq = raw1(a.gq, row * Dv + d0 + c, ibf);
-            }
-            sV[tt][c] = cvt1(rv, ibf);
-            float lq[J], lk[J];
-            float m = -INFINITY, mk = -INFINITY;
-#pragma unroll
-            for (int j = 0; j < J; ++j) {
-                sBeta[tt][j][c] = 1.0f / (1.0f + exp_fast(-cvt1(rb[j], ibf)));
-                lk[j] = cvt1(rk[j], ibf);
-                lq[j] = cvt1(rq[j], ibf);
-                m = fmaxf(m, lq[j]);
-                mk = fmaxf(mk, lk[j]);
-            }
-            float z = 0.0f, zk = 0.0f;
-#pragma unroll
-            for (int j = 0; j < J; ++j) {
-                lq[j] = exp_fast(lq[j] - m);
-                z += lq[j];
-                if constexpr (TP) {
-                    lk[j] = exp_fast(lk[j] - mk);
-                    zk += lk[j];
-                }
-            }
-            const float iz = 1.0f / z;
-            const float izk = TP ? 1.0f / zk : 1.0f;
-#pragma unroll
-            for (int j = 0; j < J; ++j) {
-                sPq[tt][j][c] = lq[j] * iz;
-                sLk[tt][j][c] = TP ? lk[j] * izk : lk[j];   // temporal: pi^k itself
-            }
-            if constexpr (TP) {
-                sG[0][tt][c] = 1.0f / (1.0f + exp_fast(-cvt1(rgk, ibf)));
-                sG[1][tt][c] = 1.0f / (1.0f + exp_fast(-cvt1(rgq, ibf)));
-            }
-        }
-        __syncthreads();
+        block_sync_lds();
 
         for (int tt = 0; tt < nt; ++tt) {
             float kv[S], qv[S];
@@ -305,7 +332,7 @@ __global__ __launch_bounds__(kThreads) void scan_direct_kernel(LayerArgs a, int 
         }
     }
 
-    __syncthreads();
+    block_sync_lds();
     if (!AX && T > 0) {
         const int tl = ((T - 1) / kTC) * kTC;
         const int nt = T - tl;
