@@ -37,15 +37,17 @@ PEAK_MFMA_BF16 = 2.5e15    # FLOP/s, MI355X dense bf16 matrix
 # source, the workload it ran and the digest of the source at measurement.
 MEASURED_TRAFFIC = {
     ("decode.hip", "decode B=256 H=16 Dk=Dv=128 J=4",
-     "10a280fc4288f38608f27ababeece47b80e697cbc47fd154437db4ebc82836b2"): 2184274349,
+     "f4fda514494702a999a7b1e22375b2a5471d72884bde3177212b9c47cf163ed1"): 2184274117,
     ("scan_pipe.hip", "forward B=4 H=8 T=2048 Dk=Dv=64 J=4",
-     "c726c889f31a85c4db9ccb59682ba4d02d3cda42e78d9b3dbe342096e3c92e6b"): 136682804,
+     "10f01378f0054265aedcd58348c2f33bc35c7a6f65720e39895a612a01dc8ec2"): 136679434,
     ("scan_pipe.hip", "forward B=8 H=16 T=4096 Dk=Dv=128 J=4",
-     "c726c889f31a85c4db9ccb59682ba4d02d3cda42e78d9b3dbe342096e3c92e6b"): 2185331085,
+     "10f01378f0054265aedcd58348c2f33bc35c7a6f65720e39895a612a01dc8ec2"): 2185160535,
     ("scan_pipe_temporal.hip", "temporal B=4 H=8 T=2048 Dk=Dv=64 J=4",
-     "a5ffe58c7150c4f1a592fb13502fd103aafa35fb0556c5b5dde60e49b454af9f"): 153641430,
+     "9887c803ed2530004fba32cefc6dacd68ede72a204b510c26d7d8bbbb47b0848"): 153641701,
+    ("scan_direct.hip", "forward B=4 H=8 T=2048 Dk=Dv=64 J=4",
+     "5faf7d932fe465a54b3aa2376f2646d29ee0b7abafda538bd7699b055eb98b45"): 136648715,
     ("scan_direct.hip", "gated B=4 H=8 T=2048 Dk=Dv=64 J=4",
-     "e24f3a5ca0926eaa89c84fac489f603f2c34e519db5730311b0cbcefdb0b0e05"): 170098769,
+     "5faf7d932fe465a54b3aa2376f2646d29ee0b7abafda538bd7699b055eb98b45"): 170375003,
 }
 
 
