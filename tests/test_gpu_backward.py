@@ -130,3 +130,26 @@ def test_backward_config2_sampled_heads():
                 seed=1002, heads=[(0, 0), (3, 7), (2, 4)])
     print(" ".join("%s %.2e" % kv for kv in errs.items()))
     assert all(v <= 2e-2 for v in errs.values()), errs
+
+
+def test_backward_lm_batch_sampled_head():
+    """The LM-shaped batch (B=8 H=16 T=4096 Dk=Dv=128 J=4, bf16; 128 chunks of 32
+    tokens and 64-lane reverse blocks), the oracle on one sampled head (the
+    oracle keeps every token's state: about 2 GB at this size)."""
+    import torch
+    import paper_2609_39034_amd as sw
+    c = workloads.CONFIGS[3]
+    B, H, T, Dk, Dv, J = (c[x] for x in ("B", "H", "T", "Dk", "Dv", "J"))
+    inp = workloads.config_inputs(3)
+    dev = to_device(inp, "bf16")
+    go_dev, go, _ = _seeds(B, H, T, Dv, Dk, J, "bf16", 1003, False)
+    res = sw.backward(*(dev[n] for n in NAMES), None, go_dev, None)
+    torch.cuda.synchronize()
+    b, h = 5, 11
+    got = [x[b:b + 1, :, h:h + 1].cpu().numpy().astype(np.float64) for x in res[:6]]
+    ref = ob.backward(*(inp[n][b:b + 1, :, h:h + 1] for n in NAMES), None,
+                      go[b:b + 1, :, h:h + 1], None)
+    errs = {n: head_rel_err(g, ref[n], KIND[n]) for n, g in zip(GRADS, got)}
+    errs["state"] = head_rel_err(res[6][b:b + 1, h:h + 1].cpu().numpy(), ref["state"], "state")
+    print(" ".join("%s %.2e" % kv for kv in errs.items()))
+    assert all(v <= 2e-2 for v in errs.values()), errs
