@@ -33,6 +33,18 @@ namespace {
 
 constexpr int kRows = 16;  // state rows per thread
 
+// The state streams through once per step: non-temporal loads and stores keep it
+// from displacing lines that are reused (the token's inputs).
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ float4 stream_load(const float *p) {
+    const f32x4 v = __builtin_nontemporal_load(reinterpret_cast<const f32x4 *>(p));
+    return make_float4(v.x, v.y, v.z, v.w);
+}
+__device__ __forceinline__ void stream_store(float *p, float4 x) {
+    f32x4 v = {x.x, x.y, x.z, x.w};
+    __builtin_nontemporal_store(v, reinterpret_cast<f32x4 *>(p));
+}
+
 template <int DK, int J, bool TP, bool GT>
 __global__ __launch_bounds__(512) void decode_kernel(LayerArgs a, int DB) {
     constexpr int IG = DK / kRows;
@@ -57,7 +69,7 @@ __global__ __launch_bounds__(512) void decode_kernel(LayerArgs a, int DB) {
     if (a.state_in && has_rows) {
 #pragma unroll
         for (int m = 0; m < kRows; ++m)
-            st[m] = *reinterpret_cast<const float4 *>(a.state_in + sbase + (size_t)(ig + IG * m) * Dv);
+            st[m] = stream_load(a.state_in + sbase + (size_t)(ig + IG * m) * Dv);
     } else {
 #pragma unroll
         for (int m = 0; m < kRows; ++m) st[m] = make_float4(0.f, 0.f, 0.f, 0.f);
@@ -204,7 +216,7 @@ __global__ __launch_bounds__(512) void decode_kernel(LayerArgs a, int DB) {
             s.y = fmaf(c4.y, ki, s.y);
             s.z = fmaf(c4.z, ki, s.z);
             s.w = fmaf(c4.w, ki, s.w);
-            *reinterpret_cast<float4 *>(dst + (size_t)(ig + IG * m) * Dv) = s;
+            stream_store(dst + (size_t)(ig + IG * m) * Dv, s);
         }
     }
 }
