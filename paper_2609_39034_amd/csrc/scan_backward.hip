@@ -85,8 +85,22 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
 
     const LayerArgs &f = a.f;
     const int tid = threadIdx.x, lane = tid % 64;
-    const int d0 = blockIdx.x * DB, h = blockIdx.y, b = blockIdx.z;
     const int H = f.H, T = f.T, Dv = f.Dv;
+    // Workgroups go to the eight XCDs (each with its own L2) round-robin by
+    // index; every column block of a head is placed on the same XCD, so that
+    // the head's K and Q rows and the shared cache lines of its per-token
+    // scalars are fetched from HBM once.
+    const int NDB = Dv / DB, NH = f.B * H, L = blockIdx.x;
+    int hh, db;
+    if (NH % 8 == 0) {
+        const int xs = L / 8;
+        hh = 8 * (xs / NDB) + L % 8;
+        db = xs % NDB;
+    } else {
+        hh = L / NDB;
+        db = L % NDB;
+    }
+    const int d0 = db * DB, h = hh % H, b = hh / H;
     const bool ibf = f.in_bf16, obf = f.out_bf16;
     const int NCH = (T + kRC - 1) / kRC;
     const int NC2 = (T + kBwdChunk - 1) / kBwdChunk;
@@ -626,8 +640,9 @@ hipError_t launch_reverse(const BackwardArgs &a, hipStream_t stream) {
     if constexpr ((J == 3 ? 4 : J) * DB > 64) {
         return hipErrorInvalidValue;
     } else {
-        hipLaunchKernelGGL((reverse_chunk_kernel<DK, J, DB>), dim3(a.f.Dv / DB, a.f.H, a.f.B),
-                           dim3(kThreads), 0, stream, a);
+        hipLaunchKernelGGL((reverse_chunk_kernel<DK, J, DB>),
+                           dim3((unsigned)((a.f.Dv / DB) * a.f.H * a.f.B)), dim3(kThreads), 0,
+                           stream, a);
         return hipGetLastError();
     }
 }
