@@ -387,16 +387,37 @@ __global__ __launch_bounds__(kThreads) void bwd_chunk_kernel(BackwardArgs a) {
 
     __shared__ __align__(16) float sK[kCB][KP];
     __shared__ __align__(16) float sQ[kCB][KP];
-    __shared__ __align__(16) float sS[NCT][KP];
-    __shared__ __align__(16) float sE[NCT][KP];
-    __shared__ float sC[kCB][CP], sP[kCB][CP], sY[kCB][CP];
-    __shared__ __align__(16) float sCt[NCT][GP];   // C and P transposed: [column][token]
-    __shared__ __align__(16) float sPt[NCT][GP];
-    __shared__ float sA[kCB][GP], sB[kCB][GP];
-    __shared__ __align__(16) float sM[3][kCB][GP]; // masked intra-chunk coefficients
     __shared__ float sQK[kCB][GP];                 // q_t . k_s
-    __shared__ float sPq[kCB][CP], sYv[kCB][CP];   // pi^q and the retrievals y
-    __shared__ float sDo[kCB][DT];
+    // The column tiles' buffers and the final coefficient matrices are never
+    // live together: they share LDS, which keeps two blocks per compute unit.
+    struct TileBufs {
+        alignas(16) float S[NCT][KP], E[NCT][KP];
+        float C[kCB][CP], P[kCB][CP], Y[kCB][CP];
+        alignas(16) float Ct[NCT][GP], Pt[NCT][GP];   // C and P transposed: [column][token]
+        float Pq[kCB][CP], Yv[kCB][CP];               // pi^q and the retrievals y
+        float Do[kCB][DT];
+    };
+    struct EndBufs {
+        float A[kCB][GP], B[kCB][GP];
+        alignas(16) float M[3][kCB][GP];              // masked intra-chunk coefficients
+    };
+    __shared__ union {
+        TileBufs t;
+        EndBufs e;
+    } lds;
+    auto &sS = lds.t.S;
+    auto &sE = lds.t.E;
+    auto &sC = lds.t.C;
+    auto &sP = lds.t.P;
+    auto &sY = lds.t.Y;
+    auto &sCt = lds.t.Ct;
+    auto &sPt = lds.t.Pt;
+    auto &sPq = lds.t.Pq;
+    auto &sYv = lds.t.Yv;
+    auto &sDo = lds.t.Do;
+    auto &sA = lds.e.A;
+    auto &sB = lds.e.B;
+    auto &sM = lds.e.M;
 
     const LayerArgs &f = a.f;
     const int n = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
@@ -593,7 +614,9 @@ __global__ __launch_bounds__(kThreads) void bwd_chunk_kernel(BackwardArgs a) {
         }
     }
 
-    // the intra-chunk terms, as three masked C x C coefficient matrices
+    // the intra-chunk terms, as three masked C x C coefficient matrices (in the
+    // tile buffers' LDS: the last tile is consumed first)
+    block_sync_lds();
 #pragma unroll
     for (int x = 0; x < 4; ++x) {
         sA[gt][gs + x] = ga[x];
