@@ -359,15 +359,43 @@ __global__ __launch_bounds__(kThreads) void scan_direct_kernel(LayerArgs a, int 
     }
 }
 
-template <int DK, int J, bool TP, bool GT, bool AX = false>
-hipError_t launch_dk_j_tp(const LayerArgs &a, hipStream_t stream) {
-    constexpr int S = (J <= 4) ? (DK < 16 ? DK : 16) : (DK < 8 ? DK : 8);
+template <int DK, int J, int S, bool TP, bool GT, bool AX>
+hipError_t launch_s(const LayerArgs &a, hipStream_t stream) {
     constexpr int L = DK / S;
     const int ncol = a.Dv < max_cols(L, J, TP) ? a.Dv : max_cols(L, J, TP);
     dim3 grid(a.Dv / ncol, a.H, a.B);
     dim3 block(ncol * L);
     hipLaunchKernelGGL((scan_direct_kernel<DK, J, S, TP, GT, AX>), grid, block, 0, stream, a, ncol);
     return hipGetLastError();
+}
+
+// Blocks of the launch with S key rows per lane.
+template <int DK, int J, int S, bool TP>
+size_t grid_blocks(const LayerArgs &a) {
+    const int ncol = a.Dv < max_cols(DK / S, J, TP) ? a.Dv : max_cols(DK / S, J, TP);
+    return (size_t)(a.Dv / ncol) * a.H * a.B;
+}
+
+template <int DK, int J, bool TP, bool GT, bool AX = false>
+hipError_t launch_dk_j_tp(const LayerArgs &a, hipStream_t stream) {
+    constexpr int S = (J <= 4) ? (DK < 16 ? DK : 16) : (DK < 8 ? DK : 8);
+    if constexpr (GT) {
+        // The gated form has no chunk scan, so it is the only path for its
+        // batches.  A column's time per token falls with its rows per lane, and
+        // a grid of fewer blocks than compute units leaves the rest idle: halve
+        // S (down to 4 rows, and to at most 16 lanes per column, which keeps
+        // every block at 16 columns or more) while the grid is under 256
+        // blocks.  At B=4 H=8 Dk=Dv=64 J=4 that is S = 4: 128 blocks of 16
+        // columns instead of 32 of 64.
+        constexpr int S2 = S / 2 >= 4 && DK / (S / 2) <= 16 ? S / 2 : S;
+        constexpr int S4 = S2 / 2 >= 4 && DK / (S2 / 2) <= 16 ? S2 / 2 : S2;
+        if (grid_blocks<DK, J, S, TP>(a) < 256) {
+            if (S4 != S2 && grid_blocks<DK, J, S2, TP>(a) < 256)
+                return launch_s<DK, J, S4, TP, GT, AX>(a, stream);
+            if constexpr (S2 != S) return launch_s<DK, J, S2, TP, GT, AX>(a, stream);
+        }
+    }
+    return launch_s<DK, J, S, TP, GT, AX>(a, stream);
 }
 
 template <int DK, int J>
