@@ -98,6 +98,137 @@ __global__ __launch_bounds__(kThreads) void scan_direct_kernel(LayerArgs a, int 
         }
     }
 
+    // Per-(token, column) scalars of one staged item: v, beta = sigmoid, the
+    // key-prior logits (temporal: pi^k itself), pi^q = softmax_j, and the
+    // temporal gates.
+    auto stage_item = [&](int tt, int c, uint32_t rv, const uint32_t *rb, const uint32_t *rlk,
+                          const uint32_t *rlq, uint32_t rgk, uint32_t rgq) {
+        sV[tt][c] = cvt1(rv, ibf);
+        float lq[J], lk[J];
+        float m = -INFINITY, mk = -INFINITY;
+#pragma unroll
+        for (int j = 0; j < J; ++j) {
+            sBeta[tt][j][c] = 1.0f / (1.0f + exp_fast(-cvt1(rb[j], ibf)));
+            lk[j] = cvt1(rlk[j], ibf);
+            lq[j] = cvt1(rlq[j], ibf);
+            m = fmaxf(m, lq[j]);
+            mk = fmaxf(mk, lk[j]);
+        }
+        float z = 0.0f, zk = 0.0f;
+#pragma unroll
+        for (int j = 0; j < J; ++j) {
+            lq[j] = exp_fast(lq[j] - m);
+            z += lq[j];
+            if constexpr (TP) {
+                lk[j] = exp_fast(lk[j] - mk);
+                zk += lk[j];
+            }
+        }
+        const float iz = 1.0f / z;
+        const float izk = TP ? 1.0f / zk : 1.0f;
+#pragma unroll
+        for (int j = 0; j < J; ++j) {
+            sPq[tt][j][c] = lq[j] * iz;
+            sLk[tt][j][c] = TP ? lk[j] * izk : lk[j];
+        }
+        if constexpr (TP) {
+            sG[0][tt][c] = 1.0f / (1.0f + exp_fast(-cvt1(rgk, ibf)));
+            sG[1][tt][c] = 1.0f / (1.0f + exp_fast(-cvt1(rgq, ibf)));
+        }
+    };
+
+    // Prefetch (PF): when the raw loads of a whole 16-token round fit in a
+    // register budget, the loads of round n+1 are issued right after round n
+    // is published to LDS, and so are in flight during round n's token loop;
+    // they are converted and stored at the top of round n+1.  Without PF a
+    // round's loads are issued and converted in batches before its token loop,
+    // and the HBM latency of every batch sits on the sequential path.
+    constexpr int NKQ = S / 4;                // K/Q pieces per thread at most (ncol >= 16)
+    constexpr int ND = GT ? J * S / 4 : 0;    // decay pieces per thread at most
+    constexpr int NI = kTC / L;               // scalar items per thread at most
+    constexpr int NSC = 1 + 3 * J + (TP ? 2 : 0);
+    constexpr bool PF = NKQ * 8 + NI * NSC + ND * 4 <= 128;
+    uint4 pk[PF ? NKQ : 1], pq[PF ? NKQ : 1], pd[PF && ND ? ND : 1];
+    uint32_t pv[PF ? NI : 1], pb[PF ? NI : 1][J], plk[PF ? NI : 1][J], plq[PF ? NI : 1][J];
+    uint32_t pgk[PF ? NI : 1], pgq[PF ? NI : 1];
+    // decay piece x of a thread in a round of un tokens: token, component, key index
+    auto dpiece_n = [&](int x, int un, int &tt, int &j, int &i) {
+        const int g = tid + x * nthr;
+        tt = g / (J * (DK / 4));
+        const int rem = g % (J * (DK / 4));
+        j = rem / (DK / 4), i = (rem % (DK / 4)) * 4;
+        return g < un * J * (DK / 4);
+    };
+    auto issue = [&](int u0) {   // the raw loads of the round that starts at token u0
+        const int un = min(kTC, T - u0);
+#pragma unroll
+        for (int x = 0; x < NKQ; ++x) {
+            const int g = tid + x * nthr;
+            if (g < un * (DK / 4)) {
+                const size_t off = ((size_t)(b * T + u0 + g / (DK / 4)) * H + h) * DK +
+                                   (g % (DK / 4)) * 4;
+                pk[x] = raw4(a.k, off, ibf);
+                pq[x] = raw4(a.q, off, ibf);
+            }
+        }
+#pragma unroll
+        for (int x = 0; x < NI; ++x) {
+            const int g = tid + x * nthr;
+            if (g < un * ncol) {
+                const int tt = g / ncol, c = g % ncol;
+                const size_t row = (size_t)(b * T + u0 + tt) * H + h;
+                pv[x] = raw1(a.v, row * Dv + d0 + c, ibf);
+#pragma unroll
+                for (int j = 0; j < J; ++j) {
+                    const size_t idx = (row * J + j) * Dv + d0 + c;
+                    pb[x][j] = raw1(a.lb, idx, ibf);
+                    plk[x][j] = raw1(a.lk, idx, ibf);
+                    plq[x][j] = raw1(a.lq, idx, ibf);
+                }
+                if constexpr (TP) {
+                    pgk[x] = raw1(a.gk, row * Dv + d0 + c, ibf);
+                    pgq[x] = raw1(a.gq, row * Dv + d0 + c, ibf);
+                }
+            }
+        }
+#pragma unroll
+        for (int x = 0; x < ND; ++x) {
+            int tt, j, i;
+            if (dpiece_n(x, un, tt, j, i))
+                pd[x] = raw4(a.decay, (((size_t)(b * T + u0 + tt) * H + h) * J + j) * DK + i, ibf);
+        }
+    };
+    auto commit = [&](int u0) {   // convert the issued round and store it to LDS
+        const int un = min(kTC, T - u0);
+#pragma unroll
+        for (int x = 0; x < NKQ; ++x) {
+            const int g = tid + x * nthr;
+            if (g < un * (DK / 4)) {
+                const int tt = g / (DK / 4), i = (g % (DK / 4)) * 4;
+                *reinterpret_cast<float4 *>(&sK[tt][i / S][i % S]) = cvt4(pk[x], ibf);
+                *reinterpret_cast<float4 *>(&sQ[tt][i / S][i % S]) = cvt4(pq[x], ibf);
+            }
+        }
+#pragma unroll
+        for (int x = 0; x < NI; ++x) {
+            const int g = tid + x * nthr;
+            if (g < un * ncol)
+                stage_item(g / ncol, g % ncol, pv[x], pb[x], plk[x], plq[x], pgk[x], pgq[x]);
+        }
+#pragma unroll
+        for (int x = 0; x < ND; ++x) {
+            int tt, j, i;
+            if (dpiece_n(x, un, tt, j, i)) {
+                const float4 v4 = cvt4(pd[x], ibf);
+                *reinterpret_cast<float4 *>(&sA[tt][j][i]) = make_float4(
+                    sigmoid(v4.x), sigmoid(v4.y), sigmoid(v4.z), sigmoid(v4.w));
+            }
+        }
+    };
+    if constexpr (PF) {
+        if (T > 0) issue(0);
+    }
+
     for (int t0 = 0; t0 < T; t0 += kTC) {
         const int nt = min(kTC, T - t0);
         if constexpr (AX) {
@@ -124,13 +255,12 @@ __global__ __launch_bounds__(kThreads) void scan_direct_kernel(LayerArgs a, int 
         // for its data before the next one is issued.  The block barriers order
         // LDS traffic only: the global stores of outputs need no ordering here,
         // and a full barrier would wait for them.
-        {
+        if constexpr (PF) {
+            commit(t0);
+        } else {
             // K and Q rows and the first batch of per-(token, column) scalars are
             // all issued before anything converts; the decay gates follow in
             // batches of their own.
-            constexpr int NKQ = S / 4;                // K/Q pieces per thread at most (ncol >= 16)
-            constexpr int ND = GT ? J * S / 4 : 0;    // decay pieces per thread at most
-            constexpr int NI = kTC / L;               // scalar items per thread at most
             // scalar items loaded together: a register budget over the values
             // of an item
             constexpr int NBR = 56 / (1 + 3 * J + (TP ? 2 : 0));
@@ -147,13 +277,7 @@ __global__ __launch_bounds__(kThreads) void scan_direct_kernel(LayerArgs a, int 
                     rq[x] = raw4(a.q, off, ibf);
                 }
             }
-            auto dpiece = [&](int x, int &tt, int &j, int &i) {
-                const int g = tid + x * nthr;
-                tt = g / (J * (DK / 4));
-                const int rem = g % (J * (DK / 4));
-                j = rem / (DK / 4), i = (rem % (DK / 4)) * 4;
-                return g < nt * J * (DK / 4);
-            };
+            auto dpiece = [&](int x, int &tt, int &j, int &i) { return dpiece_n(x, nt, tt, j, i); };
             for (int i0 = 0; i0 < NI; i0 += NB) {
                 uint32_t rv[NB], rb[NB][J], rlk[NB][J], rlq[NB][J], rgk[NB], rgq[NB];
 #pragma unroll
@@ -191,39 +315,7 @@ __global__ __launch_bounds__(kThreads) void scan_direct_kernel(LayerArgs a, int 
                 for (int x = 0; x < NB; ++x) {
                     const int g = tid + (i0 + x) * nthr;
                     if (g >= nt * ncol) continue;
-                    const int tt = g / ncol, c = g % ncol;
-                    sV[tt][c] = cvt1(rv[x], ibf);
-                    float lq[J], lk[J];
-                    float m = -INFINITY, mk = -INFINITY;
-#pragma unroll
-                    for (int j = 0; j < J; ++j) {
-                        sBeta[tt][j][c] = 1.0f / (1.0f + exp_fast(-cvt1(rb[x][j], ibf)));
-                        lk[j] = cvt1(rlk[x][j], ibf);
-                        lq[j] = cvt1(rlq[x][j], ibf);
-                        m = fmaxf(m, lq[j]);
-                        mk = fmaxf(mk, lk[j]);
-                    }
-                    float z = 0.0f, zk = 0.0f;
-#pragma unroll
-                    for (int j = 0; j < J; ++j) {
-                        lq[j] = exp_fast(lq[j] - m);
-                        z += lq[j];
-                        if constexpr (TP) {
-                            lk[j] = exp_fast(lk[j] - mk);
-                            zk += lk[j];
-                        }
-                    }
-                    const float iz = 1.0f / z;
-                    const float izk = TP ? 1.0f / zk : 1.0f;
-#pragma unroll
-                    for (int j = 0; j < J; ++j) {
-                        sPq[tt][j][c] = lq[j] * iz;
-                        sLk[tt][j][c] = TP ? lk[j] * izk : lk[j];   // temporal: pi^k itself
-                    }
-                    if constexpr (TP) {
-                        sG[0][tt][c] = 1.0f / (1.0f + exp_fast(-cvt1(rgk[x], ibf)));
-                        sG[1][tt][c] = 1.0f / (1.0f + exp_fast(-cvt1(rgq[x], ibf)));
-                    }
+                    stage_item(g / ncol, g % ncol, rv[x], rb[x], rlk[x], rlq[x], rgk[x], rgq[x]);
                 }
             }
             if constexpr (GT) {   // decay gates, in batches of their own
@@ -249,6 +341,9 @@ __global__ __launch_bounds__(kThreads) void scan_direct_kernel(LayerArgs a, int 
             }
         }
         block_sync_lds();
+        if constexpr (PF) {
+            if (t0 + kTC < T) issue(t0 + kTC);
+        }
 
         for (int tt = 0; tt < nt; ++tt) {
             float kv[S], qv[S];
