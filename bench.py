@@ -45,9 +45,9 @@ MEASURED_TRAFFIC = {
     ("scan_pipe_temporal.hip", "temporal B=4 H=8 T=2048 Dk=Dv=64 J=4",
      "9887c803ed2530004fba32cefc6dacd68ede72a204b510c26d7d8bbbb47b0848"): 153641701,
     ("scan_direct.hip", "forward B=4 H=8 T=2048 Dk=Dv=64 J=4",
-     "5faf7d932fe465a54b3aa2376f2646d29ee0b7abafda538bd7699b055eb98b45"): 136648715,
+     "7c51058bec0bae8edace2e9cbd9a1c9286328d04345bca4d65b949689aa31cf1"): 136710124,
     ("scan_direct.hip", "gated B=4 H=8 T=2048 Dk=Dv=64 J=4",
-     "5faf7d932fe465a54b3aa2376f2646d29ee0b7abafda538bd7699b055eb98b45"): 170375003,
+     "7c51058bec0bae8edace2e9cbd9a1c9286328d04345bca4d65b949689aa31cf1"): 170045290,
 }
 
 

@@ -74,8 +74,20 @@ __global__ __launch_bounds__(kThreads) void scan_direct_kernel(LayerArgs a, int 
     const int tid = threadIdx.x;
     const int nthr = ncol * L;
     const int dl = tid / L, l = tid % L;
-    const int d0 = blockIdx.x * ncol;
-    const int h = blockIdx.y, b = blockIdx.z;
+    // Workgroups go to the eight XCDs (each with its own L2) round-robin by
+    // linear index.  Every column block of a head is placed on the same XCD, so
+    // that the head's K, Q and decay rows, which each of its column blocks
+    // stages, come from HBM once.
+    const int NDB = gridDim.x, NH = gridDim.y * gridDim.z;
+    const int lin = blockIdx.x + NDB * (blockIdx.y + gridDim.y * blockIdx.z);
+    int hh = blockIdx.y + gridDim.y * blockIdx.z, db = blockIdx.x;
+    if (NDB > 1 && NH % 8 == 0) {
+        const int xs = lin / 8;
+        hh = 8 * (xs / NDB) + lin % 8;
+        db = xs % NDB;
+    }
+    const int d0 = db * ncol;
+    const int h = hh % gridDim.y, b = hh / gridDim.y;
     const int H = a.H, T = a.T, Dv = a.Dv;
     const int d = d0 + dl;
     const bool ibf = a.in_bf16, obf = a.out_bf16;
