@@ -54,8 +54,19 @@ __global__ __launch_bounds__(512) void decode_kernel(LayerArgs a, int DB) {
     const int ig = (tid / CL) % IG;
     const bool has_rows = tid < J * IG * CL;
     const int j = has_rows ? tid / (CL * IG) : 0;
-    const int d0 = blockIdx.x * DB;
-    const int h = blockIdx.y, b = blockIdx.z;
+    // Workgroups go to the eight XCDs round-robin by linear index.  The column
+    // blocks of a head read interleaved pieces of the same state rows (and the
+    // same k, q and decay row); they are all placed on one XCD.
+    const int NDB = gridDim.x, NH = gridDim.y * gridDim.z;
+    const int lin = blockIdx.x + NDB * (blockIdx.y + gridDim.y * blockIdx.z);
+    int hh = blockIdx.y + gridDim.y * blockIdx.z, db = blockIdx.x;
+    if (NDB > 1 && NH % 8 == 0) {
+        const int xs = lin / 8;
+        hh = 8 * (xs / NDB) + lin % 8;
+        db = xs % NDB;
+    }
+    const int d0 = db * DB;
+    const int h = hh % gridDim.y, b = hh / gridDim.y;
     const int H = a.H, Dv = a.Dv;
     const bool ibf = a.in_bf16;
 
