@@ -32,6 +32,11 @@ CASES = [
     (3, 1, 40, 64, 32, 2, "bf16", 0.0, True, 2.0),
     (1, 1, 1, 128, 128, 4, "f32", 0.2, False, 2.0),
     (2, 2, 16, 32, 128, 8, "bf16", 0.1, False, 1.0),
+    # 256 heads: grids of at least 256 blocks keep 16 (J <= 4) or 8 key rows per
+    # lane; the grids above have fewer blocks and take 4 rows per lane
+    (16, 16, 21, 64, 64, 4, "bf16", 0.1, False, 2.0),
+    (16, 16, 18, 64, 64, 4, "f32", 0.2, True, 2.0),
+    (8, 32, 19, 128, 128, 8, "bf16", 0.1, False, 2.0),
 ]
 
 
