@@ -45,9 +45,9 @@ MEASURED_TRAFFIC = {
     ("scan_pipe_temporal.hip", "temporal B=4 H=8 T=2048 Dk=Dv=64 J=4",
      "9887c803ed2530004fba32cefc6dacd68ede72a204b510c26d7d8bbbb47b0848"): 153641701,
     ("scan_direct.hip", "forward B=4 H=8 T=2048 Dk=Dv=64 J=4",
-     "7c51058bec0bae8edace2e9cbd9a1c9286328d04345bca4d65b949689aa31cf1"): 136710124,
+     "b2ce1cc526e4640fa6b81cf07392f72bbffecf57bc60dae42ae2f80182448c84"): 136457010,
     ("scan_direct.hip", "gated B=4 H=8 T=2048 Dk=Dv=64 J=4",
-     "7c51058bec0bae8edace2e9cbd9a1c9286328d04345bca4d65b949689aa31cf1"): 170045290,
+     "b2ce1cc526e4640fa6b81cf07392f72bbffecf57bc60dae42ae2f80182448c84"): 170037867,
 }
 
 
