@@ -486,14 +486,15 @@ size_t grid_blocks(const LayerArgs &a) {
 template <int DK, int J, bool TP, bool GT, bool AX = false>
 hipError_t launch_dk_j_tp(const LayerArgs &a, hipStream_t stream) {
     constexpr int S = (J <= 4) ? (DK < 16 ? DK : 16) : (DK < 8 ? DK : 8);
-    if constexpr (!AX) {
+    {
         // A wave's time per token is bound by its own instruction stream, which
         // shrinks with its rows per lane, and a grid of fewer blocks than
         // compute units leaves the rest idle: halve S (down to 4 rows, and to
         // at most 16 lanes per column, which keeps every block at 16 columns or
         // more) while the grid is under 256 blocks.  At B=4 H=8 Dk=Dv=64 J=4
-        // that is S = 4: 128 blocks of 16 columns instead of 32 of 64.  (The
-        // backward's recompute keeps its layout.)
+        // that is S = 4: 128 blocks of 16 columns instead of 32 of 64.  The
+        // backward's checkpoints store key index l * S + s at its own position,
+        // so their layout does not depend on S.
         constexpr int S2 = S / 2 >= 4 && DK / (S / 2) <= 16 ? S / 2 : S;
         constexpr int S4 = S2 / 2 >= 4 && DK / (S2 / 2) <= 16 ? S2 / 2 : S2;
         if (grid_blocks<DK, J, S, TP>(a) < 256) {
