@@ -45,9 +45,9 @@ MEASURED_TRAFFIC = {
     ("scan_pipe_temporal.hip", "temporal B=4 H=8 T=2048 Dk=Dv=64 J=4",
      "9887c803ed2530004fba32cefc6dacd68ede72a204b510c26d7d8bbbb47b0848"): 153641701,
     ("scan_direct.hip", "forward B=4 H=8 T=2048 Dk=Dv=64 J=4",
-     "b2ce1cc526e4640fa6b81cf07392f72bbffecf57bc60dae42ae2f80182448c84"): 136457010,
+     "9c05f9370e10e3ef0f32f4340d26da5eaba747b2493f558c7db50d1e290eac3e"): 136456434,
     ("scan_direct.hip", "gated B=4 H=8 T=2048 Dk=Dv=64 J=4",
-     "b2ce1cc526e4640fa6b81cf07392f72bbffecf57bc60dae42ae2f80182448c84"): 170037867,
+     "9c05f9370e10e3ef0f32f4340d26da5eaba747b2493f558c7db50d1e290eac3e"): 170042026,
 }
 
 
