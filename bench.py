@@ -1,15 +1,20 @@
 """Benchmark of the SwiLA hot path on one MI355X.
 
-    python bench.py [--steps K] [--warmup W] [--config 2] [--no-decode] [--no-cpu-baseline]
+    python bench.py [--steps K] [--warmup W] [--config 3] [--no-decode] [--no-cpu-baseline]
 
-A step is one swila_forward call over the whole batch of the small
-training-shaped workload (B=4, H=8, T=2048, Dk=Dv=64, J=4, bf16 inputs, fp32
-state), inputs resident in HBM.  value = B*T / seconds per step (tokens/s).
-The same run also times the temporal, gated and App. D Newton forms and the
-backward pass on that batch ("temporal", "gated", "newton", "backward"), the
-batched decode workload (B=256, H=16, D=128, J=4, 512 one-token steps, state
-updated in place) under "decode", and the fp64 oracle on the host cores
-("cpu_baseline").
+A step is one swila_forward call over the whole batch of the LM-shaped
+workload (B=8, H=16, T=4096, Dk=Dv=128, J=4, bf16 inputs, fp32 state), inputs
+resident in HBM.  value = B*T / seconds per step (tokens/s).  The same run
+also times:
+  "c2", "c5", "c1"  the forward on the other whole-sequence workloads (c1 in us);
+  "temporal", "gated"  the temporal (App. B.3) and gated (App. B.4) forms on the
+                    headline batch;
+  "newton", "newton_c5"  the App. D form on the c2 and c5 batches;
+  "backward"        the gradient of the plain forward on the c2 batch;
+  "decode"          the batched decode workload (B=256, H=16, D=128, J=4, 512
+                    one-token steps, state updated in place);
+  "cpu_baseline"    the fp64 oracle on the host cores (whole headline batch), with
+                    single-thread figures for c1 and c2.
 
 Prints one JSON line.
 """
@@ -115,11 +120,31 @@ def decode_alg_bytes(B, H, Dk, Dv, J, in_bytes=2, out_bytes=2):
 
 
 def host_cores():
+    """(threads the oracle uses, cores visible to this process).  The threads
+    are the visible cores, capped by OMP_NUM_THREADS when it is set: a GPU
+    box grants one GPU's job that many cores of the host."""
     try:
-        n = len(os.sched_getaffinity(0))
+        visible = len(os.sched_getaffinity(0))
     except AttributeError:
-        n = os.cpu_count() or 1
-    return max(1, min(n, 16))
+        visible = os.cpu_count() or 1
+    n = visible
+    try:
+        cap = int(os.environ.get("OMP_NUM_THREADS", "0"))
+    except ValueError:
+        cap = 0
+    if cap > 0:
+        n = min(n, cap)
+    return max(1, n), visible
+
+
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def time_forward(sw, torch, dev, steps, warmup, o, s_out, algo, **kw):
@@ -157,6 +182,7 @@ def newton_alg_flops(B, H, T, Dk, Dv, J, sweeps, chunk=16):
 
 def bench_newton(sw, torch, dev, cfg, steps, warmup, o, s_out, tol):
     B, H, T, Dk, Dv, J = (cfg[x] for x in ("B", "H", "T", "Dk", "Dv", "J"))
+    batch = "B=%d H=%d T=%d Dk=Dv=%d J=%d" % (B, H, T, Dk, J)
     ws = torch.empty(sw.forward_workspace_bytes(B, H, T, Dk, Dv, J, algo="newton"),
                      device="cuda", dtype=torch.uint8)
     it = torch.zeros(2, device="cuda", dtype=torch.int32)
@@ -165,8 +191,8 @@ def bench_newton(sw, torch, dev, cfg, steps, warmup, o, s_out, tol):
     sweeps, unconverged = (int(x) for x in it.cpu())
     nflop = newton_alg_flops(B, H, T, Dk, Dv, J, sweeps)
     return {
-        "workload": "App. D chunkwise quasi-Newton, same batch, tol %g (relative change of "
-                    "the predictions), g clamped to [0, 2/|k|^2]" % tol,
+        "workload": "App. D chunkwise quasi-Newton, %s, bf16 inputs, tol %g (relative change "
+                    "of the predictions), g clamped to [0, 2/|k|^2]" % (batch, tol),
         "tokens_per_s": B * T / wall, "ms_per_step": wall * 1e3, "sweeps": sweeps,
         "unconverged_blocks": unconverged,
         "roofline": {"bound": "mfma", "achieved": nflop / kern / 1e12,
@@ -256,8 +282,8 @@ def bench_temporal(sw, torch, workloads, dev, cfg, seed, steps, warmup, o, s_out
     chunk = algo == "chunk" or (algo == "auto" and bf16)
     nbytes = temporal_alg_bytes(B, H, T, Dk, Dv, J, eb, eb, dev["state"] is not None, True)
     return {
-        "workload": "Temporal SwiLA (App. B.3), same batch, N(0,1) gate logits, uniform "
-                    "initial priors, final prior state kept",
+        "workload": "Temporal SwiLA (App. B.3), B=%d H=%d T=%d Dk=Dv=%d J=%d, N(0,1) gate "
+                    "logits, uniform initial priors, final prior state kept" % (B, H, T, Dk, J),
         "tokens_per_s": B * T / wall, "ms_per_step": wall * 1e3,
         "algo": "chunk_exact" if chunk else "recurrent",
         "roofline": {"bound": "hbm", "achieved": nbytes / kern / 1e9, "peak": PEAK_HBM / 1e9,
@@ -322,8 +348,9 @@ def bench_backward(sw, torch, dev, cfg, steps, warmup):
     nflop = backward_alg_flops(B, H, T, Dk, Dv, J)
     nbytes = backward_alg_bytes(B, H, T, Dk, Dv, J, eb, eb)
     return {
-        "workload": "backward of the plain forward (exact gradient), same batch, dL/do "
-                    "N(0,1), zero initial state, no final-state gradient",
+        "workload": "backward of the plain forward (exact gradient), B=%d H=%d T=%d Dk=Dv=%d "
+                    "J=%d, dL/do N(0,1), zero initial state, no final-state gradient"
+                    % (B, H, T, Dk, J),
         "tokens_per_s": B * T / wall, "ms_per_step": wall * 1e3,
         "roofline": {"bound": "alu", "achieved": nflop / kern / 1e12,
                      "peak": PEAK_VALU_F32 / 1e12, "unit": "TFLOP/s",
@@ -366,13 +393,14 @@ def bench_gated(sw, torch, workloads, dev, cfg, seed, steps, warmup, o, s_out, t
     # the method's FMAs plus the decay: one multiply per state element and token
     nflop = forward_alg_flops(B, H, T, Dk, Dv, J) + J * Dk * Dv * B * H * T
     return {
-        "workload": "Gated SwiLA (App. B.4, pre-decay, one gate per key dim), same batch, "
-                    "decay logits N(2,1), token-by-token scan",
+        "workload": "Gated SwiLA (App. B.4, pre-decay, one gate per key dim), B=%d H=%d T=%d "
+                    "Dk=Dv=%d J=%d, decay logits N(2,1), token-by-token scan"
+                    % (B, H, T, Dk, J),
         "tokens_per_s": B * T / wall, "ms_per_step": wall * 1e3, "algo": "recurrent",
         "roofline": {"bound": "alu", "achieved": nflop / kern / 1e12,
                      "peak": PEAK_VALU_F32 / 1e12, "unit": "TFLOP/s",
                      "frac": nflop / kern / PEAK_VALU_F32,
-                     "traffic": measured_traffic("scan_direct.hip",
+                     "traffic": measured_traffic("scan_direct_dk%d.hip" % Dk,
                                                  workload_key("gated", B, H, T, Dk, Dv, J)),
                      "kernel": "scan_direct_kernel (gated)", "kernel_ms": kern * 1e3,
                      "alg_flop_per_launch": nflop, "alg_bytes_per_launch": nbytes},
@@ -406,17 +434,77 @@ def newton_study(sw, torch, workloads, steps, tol):
 
 
 def cpu_baseline(workloads, inp, cfg):
+    """The fp64 oracle on the host cores: the whole headline batch on every
+    thread granted, then c1 and c2 on one thread."""
     import oracle
-    n = host_cores()
+    n, visible = host_cores()
     names = ("q", "k", "v", "lb", "lk", "lq")
     oracle.build()
     t0 = time.perf_counter()
     oracle.forward(*(inp[x] for x in names), inp["state"], nthreads=n)
     dt = time.perf_counter() - t0
     B, T = cfg["B"], cfg["T"]
+    single = {}
+    for c in (1, 2):
+        x = workloads.config_inputs(c)
+        t1 = time.perf_counter()
+        oracle.forward(*(x[y] for y in names), x["state"], nthreads=1)
+        d1 = time.perf_counter() - t1
+        cc = workloads.CONFIGS[c]
+        single["c%d" % c] = {"tokens_per_s": cc["B"] * cc["T"] / d1, "seconds": d1,
+                             "us_per_call": d1 * 1e6}
     return {"value": B * T / dt, "unit": "tokens/s", "cores": n, "kind": "oracle",
-            "sample": "the whole benchmark batch (B=%d H=%d T=%d), fp64, %d threads, %.1f s"
-                      % (B, cfg["H"], T, n, dt)}
+            "sample": "the whole benchmark batch (B=%d H=%d T=%d Dk=Dv=%d J=%d), fp64, %d "
+                      "threads, %.1f s" % (B, cfg["H"], T, cfg["Dk"], cfg["J"], n, dt),
+            "cores_visible": visible, "cpu_model": cpu_model(),
+            "single_thread": single}
+
+
+def bench_forward(sw, torch, workloads, cfg_id, steps, warmup, algo, inp=None):
+    """One swila_forward over the whole batch of workload cfg_id: wall time per
+    step, kernel time from HIP events on the launch stream, and the HBM and
+    fp32-ALU rooflines of the dominant kernel."""
+    cfg = workloads.CONFIGS[cfg_id]
+    B, H, T, Dk, Dv, J = (cfg[x] for x in ("B", "H", "T", "Dk", "Dv", "J"))
+    bf16 = cfg["dtype"] == "bf16"
+    tdt = torch.bfloat16 if bf16 else torch.float32
+    inp = workloads.config_inputs(cfg_id) if inp is None else inp
+    dev = workloads.to_torch(inp, "cuda", tdt)
+    o = torch.empty((B, T, H, Dv), device="cuda", dtype=tdt)
+    s_out = torch.empty((B, H, J, Dk, Dv), device="cuda", dtype=torch.float32)
+    wall, kern = time_forward(sw, torch, dev, steps, warmup, o, s_out, algo)
+    chunk = algo == "chunk" or (algo == "auto" and bf16 and J <= 8)
+    kname, ksrc = (("scan_pipe_kernel", "scan_pipe.hip") if chunk
+                   else ("scan_direct_kernel", "scan_direct_dk%d.hip" % Dk))
+    eb = 2 if bf16 else 4
+    nbytes = forward_alg_bytes(B, H, T, Dk, Dv, J, eb, eb, dev["state"] is not None, True)
+    nflop = forward_alg_flops(B, H, T, Dk, Dv, J)
+    hbm = {"bound": "hbm", "achieved": nbytes / kern / 1e9, "peak": PEAK_HBM / 1e9,
+           "unit": "GB/s", "frac": nbytes / kern / PEAK_HBM,
+           "traffic": measured_traffic(ksrc, workload_key("forward", B, H, T, Dk, Dv, J)),
+           "kernel": kname, "kernel_ms": kern * 1e3, "alg_bytes_per_launch": nbytes}
+    alu = {"bound": "alu", "achieved": nflop / kern / 1e12, "peak": PEAK_VALU_F32 / 1e12,
+           "unit": "TFLOP/s", "frac": nflop / kern / PEAK_VALU_F32, "kernel": kname,
+           "kernel_ms": kern * 1e3, "alg_flop_per_launch": nflop}
+    # The chunk scan runs the method's Dk-long products on the matrix cores,
+    # where they take microseconds: its binding roofline is HBM.  The
+    # token-by-token scan is bound by its fp32 FMAs on the vector ALUs.
+    roof, other = (hbm, alu) if chunk else (alu, hbm)
+    res = {
+        "workload": "SwiLA forward, %s: B=%d H=%d T=%d Dk=Dv=%d J=%d, %s inputs, fp32 state, "
+                    "zero initial state, seeded" % (cfg["name"], B, H, T, Dk, J, cfg["dtype"]),
+        "B": B, "H": H, "T": T, "Dk": Dk, "Dv": Dv, "J": J,
+        "algo": "chunk_exact" if chunk else "recurrent",
+        "tokens_per_s": B * T / wall, "ms_per_step": wall * 1e3, "us_per_step": wall * 1e6,
+        "roofline": roof, "roofline_other": other,
+    }
+    return res, dev, o, s_out, wall
+
+
+ARITH = ("fp32 state, fp32 scalar recurrence and E-step; the Dk-long products on bf16 "
+         "matrix cores with each fp32 operand split into a bf16 high part and a bf16 "
+         "residual (hi*hi + hi*lo + lo*hi, about 2^-16 relative per product), fp32 "
+         "accumulation; bf16 inputs and output")
 
 
 def main():
@@ -424,7 +512,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 5])
+    ap.add_argument("--config", type=int, default=3, choices=[1, 2, 3, 5])
     ap.add_argument("--algo", default="auto", choices=["auto", "chunk", "recurrent"])
     ap.add_argument("--decode-steps", type=int, default=512)
     ap.add_argument("--no-decode", action="store_true")
@@ -432,6 +520,8 @@ def main():
     ap.add_argument("--no-temporal", action="store_true")
     ap.add_argument("--no-gated", action="store_true")
     ap.add_argument("--no-backward", action="store_true")
+    ap.add_argument("--no-other-configs", action="store_true",
+                    help="skip the c1, c2 and c5 forward lines")
     ap.add_argument("--newton-study", action="store_true",
                     help="only the App. D measurement at B=16 H=8 T=4096 D=64 J=4")
     ap.add_argument("--newton-tol", type=float, default=1e-3)
@@ -475,55 +565,50 @@ def main():
     bf16 = cfg["dtype"] == "bf16"
     tdt = torch.bfloat16 if bf16 else torch.float32
     inp = workloads.config_inputs(args.config)
-    dev = workloads.to_torch(inp, "cuda", tdt)
-    o = torch.empty((B, T, H, Dv), device="cuda", dtype=tdt)
-    s_out = torch.empty((B, H, J, Dk, Dv), device="cuda", dtype=torch.float32)
-    wall, kern = time_forward(sw, torch, dev, args.steps, args.warmup, o, s_out, args.algo)
-    chunk = args.algo == "chunk" or (args.algo == "auto" and bf16)
-    kname, ksrc = (("scan_pipe_kernel", "scan_pipe.hip") if chunk
-                   else ("scan_direct_kernel", "scan_direct.hip"))
-
-    eb = 2 if bf16 else 4
-    nbytes = forward_alg_bytes(B, H, T, Dk, Dv, J, eb, eb, dev["state"] is not None, True)
-    nflop = forward_alg_flops(B, H, T, Dk, Dv, J)
+    head, dev, o, s_out, wall = bench_forward(sw, torch, workloads, args.config, args.steps,
+                                              args.warmup, args.algo, inp=inp)
+    chunk = head["algo"] == "chunk_exact"
     out = {
         "metric": METRIC, "value": B * T / wall, "unit": "tokens/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": wall * 1e3,
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32+bf16x3" if chunk else "f32",
+        "arith": ARITH if chunk else "fp32 throughout on the vector ALUs",
         "io_dtype": "bf16" if bf16 else "f32", "data": "synthetic",
-        "config": {"workload": "SwiLA forward, %s: B=%d H=%d T=%d Dk=Dv=%d J=%d, %s inputs, "
-                               "fp32 state, zero initial state, seeded"
-                               % (cfg["name"], B, H, T, Dk, J, cfg["dtype"]),
-                   "B": B, "H": H, "T": T, "Dk": Dk, "Dv": Dv, "J": J,
-                   "algo": "chunk_exact" if chunk else "recurrent"},
-    }
-    hbm = {"bound": "hbm", "achieved": nbytes / kern / 1e9, "peak": PEAK_HBM / 1e9,
-           "unit": "GB/s", "frac": nbytes / kern / PEAK_HBM,
-           "traffic": measured_traffic(ksrc, workload_key("forward", B, H, T, Dk, Dv, J)),
-           "kernel": kname, "kernel_ms": kern * 1e3, "alg_bytes_per_launch": nbytes}
-    alu = {"bound": "alu", "achieved": nflop / kern / 1e12, "peak": PEAK_VALU_F32 / 1e12,
-           "unit": "TFLOP/s", "frac": nflop / kern / PEAK_VALU_F32, "kernel": kname,
-           "kernel_ms": kern * 1e3, "alg_flop_per_launch": nflop}
-    # The chunk scan runs the Dk-long products on the matrix cores, where the
-    # method's FLOPs take a few microseconds: its binding roofline is HBM.  The
-    # token-by-token scan is bound by its fp32 FMAs on the vector ALUs.
-    out["roofline"], out["roofline_other"] = (hbm, alu) if chunk else (alu, hbm)
-    out.update({
+        "config": {"workload": head["workload"], "B": B, "H": H, "T": T, "Dk": Dk, "Dv": Dv,
+                   "J": J, "algo": head["algo"]},
+        "roofline": head["roofline"], "roofline_other": head["roofline_other"],
         "head_tokens_per_s": B * H * T / wall,
-    })
+    }
+    print("headline forward done: %.3f ms" % (wall * 1e3), file=sys.stderr, flush=True)
     if not args.no_temporal:
         out["temporal"] = bench_temporal(sw, torch, workloads, dev, cfg, 1000 + args.config,
                                          args.steps, args.warmup, o, s_out, args.algo, tdt)
     if not args.no_gated:
         out["gated"] = bench_gated(sw, torch, workloads, dev, cfg, 1000 + args.config,
                                    args.steps, args.warmup, o, s_out, tdt)
-    if not args.no_backward:
-        out["backward"] = bench_backward(sw, torch, dev, cfg, args.steps, args.warmup)
-    if not args.no_newton and bf16:
-        out["newton"] = bench_newton(sw, torch, dev, cfg, args.steps, args.warmup, o, s_out,
-                                     args.newton_tol)
+    print("temporal and gated done", file=sys.stderr, flush=True)
+    del dev, o, s_out
+    if not args.no_other_configs:
+        for c in (1, 2, 5):
+            if c == args.config:
+                continue
+            res, dv, oc, sc, _ = bench_forward(sw, torch, workloads, c, args.steps, args.warmup,
+                                               args.algo)
+            out["c%d" % c] = res
+            if c in (2, 5) and not args.no_newton:
+                key = "newton" if c == 2 else "newton_c5"
+                out[key] = bench_newton(sw, torch, dv, workloads.CONFIGS[c], args.steps,
+                                        args.warmup, oc, sc, args.newton_tol)
+            if c == 2 and not args.no_backward:
+                out["backward"] = bench_backward(sw, torch, dv, workloads.CONFIGS[c], args.steps,
+                                                 args.warmup)
+            del dv, oc, sc
+            torch.cuda.empty_cache()
+            print("c%d done" % c, file=sys.stderr, flush=True)
     if not args.no_decode:
         out["decode"] = bench_decode(sw, torch, workloads, args.decode_steps, args.warmup)
+        print("decode done", file=sys.stderr, flush=True)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(workloads, inp, cfg)
     else:

@@ -38,7 +38,11 @@
  *     before anything is enqueued.  swila_last_error() then describes the
  *     failure (thread-local text, valid until this thread's next call).
  *   - Supported shapes: Dk in {16, 32, 64, 128}, Dv in {16, 32, 64, 128},
- *     J in {1, 2, 3, 4, 8}, B, H >= 1, T >= 0.  Others give SWILA_EUNSUPPORTED.
+ *     J in {1, 2, 3, 4, 8, 16} (every J of the paper's Sec. 5.1 sweep, and 3),
+ *     B, H >= 1, T >= 0.  Others give SWILA_EUNSUPPORTED.  Narrower limits:
+ *     the chunked forms (SWILA_ALGO_CHUNK_EXACT, SWILA_ALGO_NEWTON) and the
+ *     backward pass take J <= 8 (SWILA_ALGO_AUTO then picks the token-by-token
+ *     scan), and the gated forward takes J * Dk <= 1024.
  */
 #ifndef SWILA_H
 #define SWILA_H
@@ -57,7 +61,7 @@ typedef struct swila_shape {
 enum swila_dtype { SWILA_F32 = 0, SWILA_BF16 = 1 };
 
 enum swila_algo {
-    SWILA_ALGO_AUTO = 0,        /* CHUNK_EXACT for bf16 inputs, RECURRENT for fp32 */
+    SWILA_ALGO_AUTO = 0,        /* CHUNK_EXACT for bf16 inputs with J <= 8, else RECURRENT */
     SWILA_ALGO_RECURRENT = 1,   /* token-by-token scan on the vector ALUs */
     SWILA_ALGO_CHUNK_EXACT = 2, /* the same recurrence evaluated 16 tokens at a time with
                                    the Dk-long products on the matrix cores (bf16 inputs
@@ -74,11 +78,18 @@ enum swila_algo {
 
 /* opts->flags bits */
 enum swila_flags {
-    SWILA_FLAG_NEWTON_NO_CLAMP = 1  /* SWILA_ALGO_NEWTON: use g of eq. jacobian_coeff as it
+    SWILA_FLAG_NEWTON_NO_CLAMP = 1, /* SWILA_ALGO_NEWTON: use g of eq. jacobian_coeff as it
                                        is.  By default g is clamped to [0, 2 / |k_t|^2], which
                                        keeps every linearised transition I - g k k^T
                                        non-expansive; the fixed point does not depend on the
                                        Jacobian approximation (App. D.2). */
+    SWILA_FLAG_NEWTON_SYNC = 2      /* SWILA_ALGO_NEWTON, for callers that want a status:
+                                       swila_forward waits for the stream after the launch,
+                                       reads iters_out (then required) and returns
+                                       SWILA_ENOTCONVERGED if some block of columns stopped
+                                       at max_iters without meeting tol.  Its outputs are
+                                       written either way.  Without the flag the call only
+                                       enqueues, and iters_out is the report. */
 };
 
 typedef struct swila_opts {
@@ -98,7 +109,9 @@ enum swila_status {
     SWILA_OK = 0,
     SWILA_EINVAL = -1,        /* null or misaligned pointer, bad size or dtype */
     SWILA_EUNSUPPORTED = -2,  /* valid but outside the supported set */
-    SWILA_EHIP = -3           /* the HIP runtime reported an error */
+    SWILA_EHIP = -3,          /* the HIP runtime reported an error */
+    SWILA_ENOTCONVERGED = -4  /* SWILA_ALGO_NEWTON with SWILA_FLAG_NEWTON_SYNC: some block of
+                                 columns did not meet tol within max_iters sweeps */
 };
 
 /* Library ABI version (currently 1). */

@@ -26,7 +26,8 @@ __all__ = ["forward", "decode_step", "forward_temporal", "decode_step_temporal",
            "forward_gated", "decode_step_gated", "backward", "backward_workspace_bytes",
            "state_init", "state_bytes", "forward_workspace_bytes",
            "version", "library_path", "SwilaError", "F32", "BF16", "ALGO_AUTO",
-           "ALGO_RECURRENT", "ALGO_CHUNK_EXACT", "ALGO_NEWTON", "FLAG_NEWTON_NO_CLAMP"]
+           "ALGO_RECURRENT", "ALGO_CHUNK_EXACT", "ALGO_NEWTON", "FLAG_NEWTON_NO_CLAMP",
+           "FLAG_NEWTON_SYNC", "ENOTCONVERGED"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB_PATH = os.path.join(_HERE, "libswila.so")
@@ -35,9 +36,9 @@ F32, BF16 = 0, 1
 ALGO_AUTO, ALGO_RECURRENT, ALGO_CHUNK_EXACT, ALGO_NEWTON = 0, 1, 2, 3
 _ALGOS = {"auto": ALGO_AUTO, "recurrent": ALGO_RECURRENT, "chunk": ALGO_CHUNK_EXACT,
           "newton": ALGO_NEWTON}
-FLAG_NEWTON_NO_CLAMP = 1
+FLAG_NEWTON_NO_CLAMP, FLAG_NEWTON_SYNC = 1, 2
 
-OK, EINVAL, EUNSUPPORTED, EHIP = 0, -1, -2, -3
+OK, EINVAL, EUNSUPPORTED, EHIP, ENOTCONVERGED = 0, -1, -2, -3, -4
 
 
 class SwilaError(RuntimeError):
@@ -161,6 +162,48 @@ def _dev_tensor(t, name, dtype=None):
     return t
 
 
+def _expect_shape(t, shape, name):
+    """ValueError unless the tensor ``t`` has ``shape``; None, True and False
+    (allocate or discard) pass.  Called before any device check, so a wrong
+    size is reported before anything reaches the library."""
+    if t is None or t is True or t is False:
+        return
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError("%s has shape %s, expected %s" % (name, tuple(t.shape), tuple(shape)))
+
+
+_IN_NAMES = ("q", "k", "v", "beta_logit", "prior_k_logit", "prior_q_logit")
+
+
+def _input_shapes(B, H, T, Dk, Dv, J, decode):
+    if decode:
+        return {"q": (B, H, Dk), "k": (B, H, Dk), "v": (B, H, Dv), "beta_logit": (B, H, J, Dv),
+                "prior_k_logit": (B, H, J, Dv), "prior_q_logit": (B, H, J, Dv)}
+    return {"q": (B, T, H, Dk), "k": (B, T, H, Dk), "v": (B, T, H, Dv),
+            "beta_logit": (B, T, H, J, Dv), "prior_k_logit": (B, T, H, J, Dv),
+            "prior_q_logit": (B, T, H, J, Dv)}
+
+
+def _check_layer(tensors, decode, o=None, state_in=None, state_out=None):
+    """Shape checks of one call (inputs, state_in, o, state_out), then device,
+    layout and dtype checks of the inputs.  Returns (inputs, dtype code,
+    (B, H, T, Dk, Dv, J))."""
+    q, v, lb = tensors[0], tensors[2], tensors[3]
+    B, H, T, Dk, Dv, J = _layer_shapes(q, v, lb, decode=decode)
+    expect = _input_shapes(B, H, T, Dk, Dv, J, decode)
+    for t, n in zip(tensors, _IN_NAMES):
+        _expect_shape(t, expect[n], n)
+    _expect_shape(state_in, (B, H, J, Dk, Dv), "state_in")
+    _expect_shape(state_out, (B, H, J, Dk, Dv), "state_out")
+    _expect_shape(o, (B, H, Dv) if decode else (B, T, H, Dv), "o")
+    ins = [_dev_tensor(t, n) for t, n in zip(tensors, _IN_NAMES)]
+    code = _dtype_code(q)
+    for t, n in zip(ins, _IN_NAMES):
+        if _dtype_code(t) != code:
+            raise TypeError("%s has dtype %s but q has %s" % (n, t.dtype, q.dtype))
+    return ins, code, (B, H, T, Dk, Dv, J)
+
+
 def state_bytes(B, H, Dk, Dv, J) -> int:
     return load_library().swila_state_bytes(ctypes.byref(Shape(B, H, 0, Dk, Dv, J)))
 
@@ -204,7 +247,8 @@ def _layer_shapes(q, v, lb, decode):
 
 def forward(q, k, v, beta_logit, prior_k_logit, prior_q_logit, state_in=None, *,
             state_out=True, o=None, out_dtype=None, resp=False, algo="auto", chunk=0,
-            workspace=None, max_iters=0, tol=0.0, clamp=True, iters_out=None, stream=None):
+            workspace=None, max_iters=0, tol=0.0, clamp=True, iters_out=None,
+            sync_status=False, stream=None):
     """Forward over whole sequences (swila_forward).
 
     q, k [B,T,H,Dk]; v [B,T,H,Dv]; logits [B,T,H,J,Dv] (one dtype: float32 or
@@ -217,27 +261,16 @@ def forward(q, k, v, beta_logit, prior_k_logit, prior_q_logit, state_in=None, *,
     max_iters (0 = 64), tol (0 = 1e-3, < 0 = exactly max_iters sweeps), clamp
     (g clamped to [0, 2/|k|^2]), iters_out (None or a device int32 tensor of 2
     elements: most sweeps of any block, blocks not converged); the workspace
-    is allocated here unless given.
+    is allocated here unless given.  sync_status=True (needs iters_out) waits
+    for the launch and raises SwilaError with code ENOTCONVERGED when some
+    block did not meet tol.
     Returns (o, state_out or None) or (o, state_out, resp).
     """
     torch = _torch()
-    names = ("q", "k", "v", "beta_logit", "prior_k_logit", "prior_q_logit")
-    ins = [_dev_tensor(t, n) for t, n in zip((q, k, v, beta_logit, prior_k_logit, prior_q_logit),
-                                             names)]
-    code = _dtype_code(q)
-    for t, n in zip(ins, names):
-        if _dtype_code(t) != code:
-            raise TypeError("%s has dtype %s but q has %s" % (n, t.dtype, q.dtype))
-    B, H, T, Dk, Dv, J = _layer_shapes(q, v, beta_logit, decode=False)
-    expect = {"q": (B, T, H, Dk), "k": (B, T, H, Dk), "v": (B, T, H, Dv),
-              "beta_logit": (B, T, H, J, Dv), "prior_k_logit": (B, T, H, J, Dv),
-              "prior_q_logit": (B, T, H, J, Dv)}
-    for t, n in zip(ins, names):
-        if tuple(t.shape) != expect[n]:
-            raise ValueError("%s has shape %s, expected %s" % (n, tuple(t.shape), expect[n]))
+    ins, code, (B, H, T, Dk, Dv, J) = _check_layer(
+        (q, k, v, beta_logit, prior_k_logit, prior_q_logit), False, o=o, state_in=state_in,
+        state_out=state_out)
     _dev_tensor(state_in, "state_in", torch.float32)
-    if state_in is not None and tuple(state_in.shape) != (B, H, J, Dk, Dv):
-        raise ValueError("state_in must be [B,H,J,Dk,Dv] = %s" % ((B, H, J, Dk, Dv),))
     odt = q.dtype if out_dtype is None else out_dtype
     if o is None:
         o = torch.empty((B, T, H, Dv), device=q.device, dtype=odt)
@@ -251,7 +284,7 @@ def forward(q, k, v, beta_logit, prior_k_logit, prior_q_logit, state_in=None, *,
     r = None
     if resp:
         r = torch.empty((B, T, H, J, Dv), device=q.device, dtype=torch.float32)
-    flags = 0 if clamp else FLAG_NEWTON_NO_CLAMP
+    flags = (0 if clamp else FLAG_NEWTON_NO_CLAMP) | (FLAG_NEWTON_SYNC if sync_status else 0)
     opts = Opts(code, _dtype_code(o), _ALGOS[algo], int(chunk), int(max_iters), float(tol),
                 flags)
     shape = Shape(B, H, T, Dk, Dv, J)
@@ -291,28 +324,14 @@ def backward(q, k, v, beta_logit, prior_k_logit, prior_q_logit, state_in, grad_o
     grad_state_in is False).  The workspace is allocated here unless given.
     """
     torch = _torch()
-    names = ("q", "k", "v", "beta_logit", "prior_k_logit", "prior_q_logit")
-    ins = [_dev_tensor(t, n) for t, n in zip((q, k, v, beta_logit, prior_k_logit, prior_q_logit),
-                                             names)]
-    code = _dtype_code(q)
-    for t, n in zip(ins, names):
-        if _dtype_code(t) != code:
-            raise TypeError("%s has dtype %s but q has %s" % (n, t.dtype, q.dtype))
     B, H, T, Dk, Dv, J = _layer_shapes(q, v, beta_logit, decode=False)
-    expect = {"q": (B, T, H, Dk), "k": (B, T, H, Dk), "v": (B, T, H, Dv),
-              "beta_logit": (B, T, H, J, Dv), "prior_k_logit": (B, T, H, J, Dv),
-              "prior_q_logit": (B, T, H, J, Dv)}
-    for t, n in zip(ins, names):
-        if tuple(t.shape) != expect[n]:
-            raise ValueError("%s has shape %s, expected %s" % (n, tuple(t.shape), expect[n]))
+    _expect_shape(grad_state, (B, H, J, Dk, Dv), "grad_state")
+    _expect_shape(grad_o, (B, T, H, Dv), "grad_o")
+    ins, code, _ = _check_layer((q, k, v, beta_logit, prior_k_logit, prior_q_logit), False,
+                                state_in=state_in)
     _dev_tensor(state_in, "state_in", torch.float32)
     _dev_tensor(grad_state, "grad_state", torch.float32)
-    for t, n in ((state_in, "state_in"), (grad_state, "grad_state")):
-        if t is not None and tuple(t.shape) != (B, H, J, Dk, Dv):
-            raise ValueError("%s must be [B,H,J,Dk,Dv] = %s" % (n, (B, H, J, Dk, Dv)))
     _dev_tensor(grad_o, "grad_o")
-    if tuple(grad_o.shape) != (B, T, H, Dv):
-        raise ValueError("grad_o must be [B,T,H,Dv] = %s" % ((B, T, H, Dv),))
     f32 = dict(device=q.device, dtype=torch.float32)
     grads = [torch.empty((B, T, H, Dk), **f32), torch.empty((B, T, H, Dk), **f32),
              torch.empty((B, T, H, Dv), **f32)] + [
@@ -342,22 +361,10 @@ def decode_step(q, k, v, beta_logit, prior_k_logit, prior_q_logit, state_in, *,
     with state_in None a new tensor is allocated).  Returns (o, state_out).
     """
     torch = _torch()
-    names = ("q", "k", "v", "beta_logit", "prior_k_logit", "prior_q_logit")
-    ins = [_dev_tensor(t, n) for t, n in zip((q, k, v, beta_logit, prior_k_logit, prior_q_logit),
-                                             names)]
-    code = _dtype_code(q)
-    for t, n in zip(ins, names):
-        if _dtype_code(t) != code:
-            raise TypeError("%s has dtype %s but q has %s" % (n, t.dtype, q.dtype))
-    B, H, T, Dk, Dv, J = _layer_shapes(q, v, beta_logit, decode=True)
-    expect = {"q": (B, H, Dk), "k": (B, H, Dk), "v": (B, H, Dv), "beta_logit": (B, H, J, Dv),
-              "prior_k_logit": (B, H, J, Dv), "prior_q_logit": (B, H, J, Dv)}
-    for t, n in zip(ins, names):
-        if tuple(t.shape) != expect[n]:
-            raise ValueError("%s has shape %s, expected %s" % (n, tuple(t.shape), expect[n]))
+    ins, code, (B, H, T, Dk, Dv, J) = _check_layer(
+        (q, k, v, beta_logit, prior_k_logit, prior_q_logit), True, o=o, state_in=state_in,
+        state_out=state_out)
     _dev_tensor(state_in, "state_in", torch.float32)
-    if state_in is not None and tuple(state_in.shape) != (B, H, J, Dk, Dv):
-        raise ValueError("state_in must be [B,H,J,Dk,Dv] = %s" % ((B, H, J, Dk, Dv),))
     if state_out is None:
         state_out = state_in if state_in is not None else torch.empty(
             (B, H, J, Dk, Dv), device=q.device, dtype=torch.float32)
@@ -379,22 +386,22 @@ def _temporal_args(gate_k_logit, gate_q_logit, prior_in, prior_out, code, gate_s
     """Checks the temporal tensors; allocates prior_out when it is True."""
     torch = _torch()
     for t, n in ((gate_k_logit, "gate_k_logit"), (gate_q_logit, "gate_q_logit")):
+        if t is None:
+            raise ValueError("%s is required" % n)
+        _expect_shape(t, gate_shape, n)
+    _expect_shape(prior_in, prior_shape, "prior_in")
+    _expect_shape(prior_out, prior_shape, "prior_out")
+    for t, n in ((gate_k_logit, "gate_k_logit"), (gate_q_logit, "gate_q_logit")):
         _dev_tensor(t, n)
         if _dtype_code(t) != code:
             raise TypeError("%s must have the dtype of q" % n)
-        if tuple(t.shape) != gate_shape:
-            raise ValueError("%s has shape %s, expected %s" % (n, tuple(t.shape), gate_shape))
     _dev_tensor(prior_in, "prior_in", torch.float32)
-    if prior_in is not None and tuple(prior_in.shape) != prior_shape:
-        raise ValueError("prior_in must be [B,H,2,J,Dv] = %s" % (prior_shape,))
     if prior_out is True:
         prior_out = torch.empty(prior_shape, device=device, dtype=torch.float32)
     elif prior_out is False or prior_out is None:
         prior_out = None
     else:
         _dev_tensor(prior_out, "prior_out", torch.float32)
-        if tuple(prior_out.shape) != prior_shape:
-            raise ValueError("prior_out must be [B,H,2,J,Dv] = %s" % (prior_shape,))
     tp = Temporal(gate_k_logit.data_ptr(), gate_q_logit.data_ptr(),
                   None if prior_in is None else prior_in.data_ptr(),
                   None if prior_out is None else prior_out.data_ptr())
@@ -415,23 +422,10 @@ def forward_temporal(q, k, v, beta_logit, prior_k_logit, prior_q_logit, gate_k_l
     Returns (o, state_out, prior_out) or (o, state_out, prior_out, resp).
     """
     torch = _torch()
-    names = ("q", "k", "v", "beta_logit", "prior_k_logit", "prior_q_logit")
-    ins = [_dev_tensor(t, n) for t, n in zip((q, k, v, beta_logit, prior_k_logit, prior_q_logit),
-                                             names)]
-    code = _dtype_code(q)
-    for t, n in zip(ins, names):
-        if _dtype_code(t) != code:
-            raise TypeError("%s has dtype %s but q has %s" % (n, t.dtype, q.dtype))
-    B, H, T, Dk, Dv, J = _layer_shapes(q, v, beta_logit, decode=False)
-    expect = {"q": (B, T, H, Dk), "k": (B, T, H, Dk), "v": (B, T, H, Dv),
-              "beta_logit": (B, T, H, J, Dv), "prior_k_logit": (B, T, H, J, Dv),
-              "prior_q_logit": (B, T, H, J, Dv)}
-    for t, n in zip(ins, names):
-        if tuple(t.shape) != expect[n]:
-            raise ValueError("%s has shape %s, expected %s" % (n, tuple(t.shape), expect[n]))
+    ins, code, (B, H, T, Dk, Dv, J) = _check_layer(
+        (q, k, v, beta_logit, prior_k_logit, prior_q_logit), False, o=o, state_in=state_in,
+        state_out=state_out)
     _dev_tensor(state_in, "state_in", torch.float32)
-    if state_in is not None and tuple(state_in.shape) != (B, H, J, Dk, Dv):
-        raise ValueError("state_in must be [B,H,J,Dk,Dv] = %s" % ((B, H, J, Dk, Dv),))
     tp, p_out = _temporal_args(gate_k_logit, gate_q_logit, prior_in, prior_out, code,
                                (B, T, H, Dv), (B, H, 2, J, Dv), q.device)
     odt = q.dtype if out_dtype is None else out_dtype
@@ -466,22 +460,10 @@ def decode_step_temporal(q, k, v, beta_logit, prior_k_logit, prior_q_logit, gate
     None.  Returns (o, state_out, prior_out).
     """
     torch = _torch()
-    names = ("q", "k", "v", "beta_logit", "prior_k_logit", "prior_q_logit")
-    ins = [_dev_tensor(t, n) for t, n in zip((q, k, v, beta_logit, prior_k_logit, prior_q_logit),
-                                             names)]
-    code = _dtype_code(q)
-    for t, n in zip(ins, names):
-        if _dtype_code(t) != code:
-            raise TypeError("%s has dtype %s but q has %s" % (n, t.dtype, q.dtype))
-    B, H, T, Dk, Dv, J = _layer_shapes(q, v, beta_logit, decode=True)
-    expect = {"q": (B, H, Dk), "k": (B, H, Dk), "v": (B, H, Dv), "beta_logit": (B, H, J, Dv),
-              "prior_k_logit": (B, H, J, Dv), "prior_q_logit": (B, H, J, Dv)}
-    for t, n in zip(ins, names):
-        if tuple(t.shape) != expect[n]:
-            raise ValueError("%s has shape %s, expected %s" % (n, tuple(t.shape), expect[n]))
+    ins, code, (B, H, T, Dk, Dv, J) = _check_layer(
+        (q, k, v, beta_logit, prior_k_logit, prior_q_logit), True, o=o, state_in=state_in,
+        state_out=state_out)
     _dev_tensor(state_in, "state_in", torch.float32)
-    if state_in is not None and tuple(state_in.shape) != (B, H, J, Dk, Dv):
-        raise ValueError("state_in must be [B,H,J,Dk,Dv] = %s" % ((B, H, J, Dk, Dv),))
     if state_out is None:
         state_out = state_in if state_in is not None else torch.empty(
             (B, H, J, Dk, Dv), device=q.device, dtype=torch.float32)
@@ -502,35 +484,11 @@ def decode_step_temporal(q, k, v, beta_logit, prior_k_logit, prior_q_logit, gate
     return o, state_out, p_out
 
 
-def _check_inputs(q, k, v, beta_logit, prior_k_logit, prior_q_logit, decode):
-    names = ("q", "k", "v", "beta_logit", "prior_k_logit", "prior_q_logit")
-    ins = [_dev_tensor(t, n) for t, n in zip((q, k, v, beta_logit, prior_k_logit, prior_q_logit),
-                                             names)]
-    code = _dtype_code(q)
-    for t, n in zip(ins, names):
-        if _dtype_code(t) != code:
-            raise TypeError("%s has dtype %s but q has %s" % (n, t.dtype, q.dtype))
-    B, H, T, Dk, Dv, J = _layer_shapes(q, v, beta_logit, decode=decode)
-    if decode:
-        expect = {"q": (B, H, Dk), "k": (B, H, Dk), "v": (B, H, Dv), "beta_logit": (B, H, J, Dv),
-                  "prior_k_logit": (B, H, J, Dv), "prior_q_logit": (B, H, J, Dv)}
-    else:
-        expect = {"q": (B, T, H, Dk), "k": (B, T, H, Dk), "v": (B, T, H, Dv),
-                  "beta_logit": (B, T, H, J, Dv), "prior_k_logit": (B, T, H, J, Dv),
-                  "prior_q_logit": (B, T, H, J, Dv)}
-    for t, n in zip(ins, names):
-        if tuple(t.shape) != expect[n]:
-            raise ValueError("%s has shape %s, expected %s" % (n, tuple(t.shape), expect[n]))
-    return ins, code, (B, H, T, Dk, Dv, J)
-
-
 def _gated_arg(decay_logit, code, shape):
+    _expect_shape(decay_logit, shape, "decay_logit")
     _dev_tensor(decay_logit, "decay_logit")
     if _dtype_code(decay_logit) != code:
         raise TypeError("decay_logit must have the dtype of q")
-    if tuple(decay_logit.shape) != shape:
-        raise ValueError("decay_logit has shape %s, expected %s"
-                         % (tuple(decay_logit.shape), shape))
     return Gated(decay_logit.data_ptr())
 
 
@@ -547,11 +505,10 @@ def forward_gated(q, k, v, beta_logit, prior_k_logit, prior_q_logit, decay_logit
     Returns (o, state_out[, prior_out][, resp]).
     """
     torch = _torch()
-    ins, code, (B, H, T, Dk, Dv, J) = _check_inputs(q, k, v, beta_logit, prior_k_logit,
-                                                    prior_q_logit, decode=False)
+    ins, code, (B, H, T, Dk, Dv, J) = _check_layer(
+        (q, k, v, beta_logit, prior_k_logit, prior_q_logit), False, o=o, state_in=state_in,
+        state_out=state_out)
     _dev_tensor(state_in, "state_in", torch.float32)
-    if state_in is not None and tuple(state_in.shape) != (B, H, J, Dk, Dv):
-        raise ValueError("state_in must be [B,H,J,Dk,Dv] = %s" % ((B, H, J, Dk, Dv),))
     gd = _gated_arg(decay_logit, code, (B, T, H, J, Dk))
     temporal = gate_k_logit is not None or gate_q_logit is not None
     tp, p_out = None, None
@@ -590,11 +547,10 @@ def decode_step_gated(q, k, v, beta_logit, prior_k_logit, prior_q_logit, decay_l
     gates [B,H,Dv] with the prior state.  state_out and prior_out default to the
     inputs (updated in place).  Returns (o, state_out[, prior_out])."""
     torch = _torch()
-    ins, code, (B, H, T, Dk, Dv, J) = _check_inputs(q, k, v, beta_logit, prior_k_logit,
-                                                    prior_q_logit, decode=True)
+    ins, code, (B, H, T, Dk, Dv, J) = _check_layer(
+        (q, k, v, beta_logit, prior_k_logit, prior_q_logit), True, o=o, state_in=state_in,
+        state_out=state_out)
     _dev_tensor(state_in, "state_in", torch.float32)
-    if state_in is not None and tuple(state_in.shape) != (B, H, J, Dk, Dv):
-        raise ValueError("state_in must be [B,H,J,Dk,Dv] = %s" % ((B, H, J, Dk, Dv),))
     if state_out is None:
         state_out = state_in if state_in is not None else torch.empty(
             (B, H, J, Dk, Dv), device=q.device, dtype=torch.float32)

@@ -234,7 +234,11 @@ __global__ __launch_bounds__(512) void decode_kernel(LayerArgs a, int DB) {
 
 template <int DK, int J>
 hipError_t launch_dk_j(const LayerArgs &a, hipStream_t stream) {
-    const int DB = a.Dv < 32 ? a.Dv : 32;
+    // DB columns per block: 32, or fewer where J * (Dk / 16) * (DB / 4) row
+    // threads would exceed the 512-thread block (J = 16, Dk = 128: 16 columns)
+    constexpr int kMaxDB = 4 * 512 / (J * (DK / kRows)) < 32 ? 4 * 512 / (J * (DK / kRows)) : 32;
+    static_assert(kMaxDB >= 4, "block of at least one float4 column group");
+    const int DB = a.Dv < kMaxDB ? a.Dv : kMaxDB;
     int threads = J * (DK / kRows) * (DB / 4);
     if (threads < DB) threads = DB;
     dim3 grid(a.Dv / DB, a.H, a.B);
@@ -257,6 +261,7 @@ hipError_t launch_dk(const LayerArgs &a, hipStream_t stream) {
         case 3: return launch_dk_j<DK, 3>(a, stream);
         case 4: return launch_dk_j<DK, 4>(a, stream);
         case 8: return launch_dk_j<DK, 8>(a, stream);
+        case 16: return launch_dk_j<DK, 16>(a, stream);
         default: return hipErrorInvalidValue;
     }
 }

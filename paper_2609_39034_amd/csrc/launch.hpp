@@ -37,6 +37,14 @@ struct LayerArgs {
 // Tokens per checkpoint interval of the backward pass.
 constexpr int kBwdChunk = 32;
 
+// Largest J * Dk of the gated token-by-token scan (its per-round gate tile in
+// LDS is [16 tokens][J][Dk] fp32).
+constexpr int kMaxGatedJDk = 1024;
+
+// Largest J of the matrix-core chunk scan (all J components of at least 8
+// output dims in one 64-lane sequential wave).
+constexpr int kMaxChunkJ = 8;
+
 // Pointers and sizes of one backward call: the forward's inputs (f.o, f.resp,
 // f.state_out unused), the loss gradients of its outputs, the input gradients
 // (fp32) and the workspace.

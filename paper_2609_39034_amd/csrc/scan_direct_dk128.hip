@@ -1,0 +1,14 @@
+// Token-by-token scan instantiated for Dk = 128 (see scan_direct_kernel.hpp).
+#include "scan_direct_kernel.hpp"
+
+namespace swila {
+
+hipError_t launch_scan_direct_dk128(const LayerArgs &a, hipStream_t stream) {
+    return launch_dk<128>(a, stream);
+}
+
+hipError_t launch_scan_direct_aux_dk128(const LayerArgs &a, hipStream_t stream) {
+    return launch_aux_dk<128>(a, stream);
+}
+
+}  // namespace swila

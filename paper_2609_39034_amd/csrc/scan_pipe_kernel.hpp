@@ -972,11 +972,13 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
                 if constexpr (!NT) {
                     // ---- B: the token recurrence of chunk n, in scaled units.
                     // The softmax over j runs without subtracting its maximum: for
-                    // logits and errors of ordinary size its sum stays far inside
-                    // the fp32 range.  Should the sum of some column leave
-                    // [2^-100, 2^100] (every component underflowing, or a logit
-                    // beyond about 60), the chunk is run again with the maximum
-                    // subtracted.
+                    // logits and errors of ordinary size its sum z stays far inside
+                    // the fp32 range.  Should z of some column and token leave
+                    // [2^-100, 2^100], the chunk is run again with the maximum
+                    // subtracted.  Inside that range a component whose term was
+                    // lost to underflow (true value below 2^-126) has r below
+                    // 2^-126 / 2^-100 = 2^-26, and no term exceeds 2^100, so
+                    // beta delta times a term stays finite.
                     float P[kC], vv[kC], lkv[kC], bev[kC], gs[TP ? kC : 1];
 #pragma unroll
                     for (int t = 0; t < kC; ++t) {
@@ -1006,8 +1008,8 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
                     // whether r is wanted is taken once per chunk.
                     auto run = [&](auto want) {
                         constexpr bool R = decltype(want)::value;
-                        // chk sums z * (1/z): not finite iff some z is 0, infinite or
-                        // not a number (every component underflowed, or overflowed)
+                        // chk is the largest z and 1/z seen (one max3 per token):
+                        // above 2^100 iff some z left [2^-100, 2^100]
                         float chk = 0.f, cprev = 0.f, gprev[kC], cb[4];
 #pragma unroll
                         for (int t = 0; t < kC; ++t) {
@@ -1074,19 +1076,19 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
                                 sm.r[pr][t][bsto] = dmode ? kInvWS * d : rt;
                                 if constexpr (TP) rprev = rt;
                             }
-                            chk = fmaf(z, iz, chk);
+                            chk = fmaxf(chk, fmaxf(z, iz));
                             cprev = cs;
 #pragma unroll
                             for (int u = t + 2; u < kC; ++u) gprev[u] = grow[u], grow[u] = gnext[u];
                         }
                         // (an integer test on bits the compiler cannot trace back to a
-                        // float: the file is compiled without NaN semantics, and would
-                        // otherwise reduce the test to |chk| == inf)
+                        // float: the file is compiled without NaN semantics, and a NaN,
+                        // whose magnitude bits exceed those of 2^100, must fail it too)
                         uint32_t chk_bits = __float_as_uint(chk);
                         asm volatile("" : "+v"(chk_bits));
-                        const bool bad = (chk_bits & 0x7f800000u) == 0x7f800000u;
+                        const bool bad = (chk_bits & 0x7fffffffu) > 0x71800000u;   // 2^100
                         if (__builtin_amdgcn_ballot_w64(bact && bad) != 0) {
-                            // some softmax underflowed: the chunk again, maximum subtracted
+                            // some softmax sum left the range: the chunk again, maximum subtracted
 #pragma unroll
                             for (int u = 1; u < kC; ++u) grow[u] = sm.g[pr][0][u];
                             load_pred();

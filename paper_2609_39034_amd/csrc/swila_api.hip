@@ -23,7 +23,8 @@ int fail(int code, const char *fmt, ...) {
 void clear_error() { g_err[0] = 0; }
 
 bool dim_ok(int x) { return x == 16 || x == 32 || x == 64 || x == 128; }
-bool j_ok(int j) { return j == 1 || j == 2 || j == 3 || j == 4 || j == 8; }
+// every J the paper uses (its Sec. 5.1 sweep: powers of two up to 16), and 3
+bool j_ok(int j) { return j == 1 || j == 2 || j == 3 || j == 4 || j == 8 || j == 16; }
 
 int check_shape(const swila_shape *s, bool decode) {
     if (!s) return fail(SWILA_EINVAL, "shape is NULL");
@@ -34,7 +35,8 @@ int check_shape(const swila_shape *s, bool decode) {
     if (!dim_ok(s->Dk) || !dim_ok(s->Dv))
         return fail(SWILA_EUNSUPPORTED, "Dk=%d Dv=%d: supported sizes are 16, 32, 64, 128", s->Dk,
                     s->Dv);
-    if (!j_ok(s->J)) return fail(SWILA_EUNSUPPORTED, "J=%d: supported are 1, 2, 3, 4, 8", s->J);
+    if (!j_ok(s->J))
+        return fail(SWILA_EUNSUPPORTED, "J=%d: supported are 1, 2, 3, 4, 8, 16", s->J);
     if (s->B > 65535 || s->H > 65535)
         return fail(SWILA_EUNSUPPORTED, "B=%d H=%d: at most 65535 each", s->B, s->H);
     return SWILA_OK;
@@ -59,8 +61,25 @@ int check_opts(const swila_opts *o) {
         return fail(SWILA_EUNSUPPORTED, "chunk %d: the chunked forms use 16 (or 0)", o->chunk);
     if (o->max_iters < 0) return fail(SWILA_EINVAL, "max_iters %d < 0", o->max_iters);
     if (o->tol != o->tol) return fail(SWILA_EINVAL, "tol is NaN");
-    if (o->flags & ~(uint32_t)SWILA_FLAG_NEWTON_NO_CLAMP)
+    if (o->flags & ~(uint32_t)(SWILA_FLAG_NEWTON_NO_CLAMP | SWILA_FLAG_NEWTON_SYNC))
         return fail(SWILA_EINVAL, "unknown flags 0x%x", o->flags);
+    return SWILA_OK;
+}
+
+// The matrix-core chunk scan takes bf16 inputs and J <= kMaxChunkJ; AUTO picks
+// it whenever it can, the token-by-token scan otherwise.
+bool use_chunk(const swila_shape *s, const swila_opts *o) {
+    if (o->algo == SWILA_ALGO_CHUNK_EXACT) return true;
+    return o->algo == SWILA_ALGO_AUTO && o->in_dtype == SWILA_BF16 && s->J <= swila::kMaxChunkJ;
+}
+
+// The chunked forms (exact chunk scan, App. D) hold all J components of eight or
+// more output dims in one wave: J <= kMaxChunkJ.
+int check_chunk_j(const swila_shape *s, const swila_opts *o) {
+    if ((o->algo == SWILA_ALGO_CHUNK_EXACT || o->algo == SWILA_ALGO_NEWTON) &&
+        s->J > swila::kMaxChunkJ)
+        return fail(SWILA_EUNSUPPORTED, "J=%d: the chunked forms support J <= %d", s->J,
+                    swila::kMaxChunkJ);
     return SWILA_OK;
 }
 
@@ -88,6 +107,21 @@ bool overlap(const Span &a, const Span &b) {
 int map_hip(hipError_t e, const char *what) {
     if (e == hipSuccess) return SWILA_OK;
     return fail(SWILA_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+// SWILA_FLAG_NEWTON_SYNC: wait for the Newton launch and report whether every
+// block of columns met the tolerance (iters_out[1] counts those that did not).
+int newton_status(const int32_t *iters_out, hipStream_t st) {
+    int32_t it[2] = {0, 0};
+    int rc = map_hip(hipMemcpyAsync(it, iters_out, sizeof it, hipMemcpyDeviceToHost, st),
+                     "iteration count copy");
+    if (rc) return rc;
+    rc = map_hip(hipStreamSynchronize(st), "stream synchronize");
+    if (rc) return rc;
+    if (it[1] > 0)
+        return fail(SWILA_ENOTCONVERGED, "%d blocks of columns did not converge in %d sweeps",
+                    it[1], it[0]);
+    return SWILA_OK;
 }
 
 // Shared checks of forward and decode; fills the launch arguments.
@@ -265,6 +299,8 @@ int swila_forward(const swila_shape *shape, const swila_opts *opts, const void *
     int rc = prepare(shape, opts, false, q, k, v, beta_logit, prior_k_logit, prior_q_logit,
                      state_in, state_out, o, resp_out, &a);
     if (rc) return rc;
+    rc = check_chunk_j(shape, opts);
+    if (rc) return rc;
     hipStream_t st = static_cast<hipStream_t>(stream);
     const bool newton = opts->algo == SWILA_ALGO_NEWTON;
     if (newton && shape->T > 0) {
@@ -278,6 +314,8 @@ int swila_forward(const swila_shape *shape, const swila_opts *opts, const void *
             return fail(SWILA_EINVAL, "workspace holds %zu bytes, %zu needed", ws_bytes, need);
         if (iters_out && reinterpret_cast<uintptr_t>(iters_out) % 4)
             return fail(SWILA_EINVAL, "iters_out is not 4-byte aligned");
+        if ((opts->flags & SWILA_FLAG_NEWTON_SYNC) && !iters_out)
+            return fail(SWILA_EINVAL, "SWILA_FLAG_NEWTON_SYNC needs iters_out");
         const size_t B = shape->B, H = shape->H, T = shape->T, Dk = shape->Dk, Dv = shape->Dv,
                      J = shape->J;
         const size_t ie = 2, oe = opts->out_dtype == SWILA_BF16 ? 2 : 4;
@@ -309,11 +347,11 @@ int swila_forward(const swila_shape *shape, const swila_opts *opts, const void *
                              opts->max_iters > 0 ? opts->max_iters : 64,
                              opts->tol == 0.f ? 1e-3f : opts->tol,
                              (opts->flags & SWILA_FLAG_NEWTON_NO_CLAMP) == 0};
-        return map_hip(swila::launch_newton(a, na, st), "Newton launch");
+        rc = map_hip(swila::launch_newton(a, na, st), "Newton launch");
+        if (rc || !(opts->flags & SWILA_FLAG_NEWTON_SYNC)) return rc;
+        return newton_status(iters_out, st);
     }
-    const bool chunk = opts->algo == SWILA_ALGO_CHUNK_EXACT ||
-                       (opts->algo == SWILA_ALGO_AUTO && opts->in_dtype == SWILA_BF16);
-    if (chunk) return map_hip(swila::launch_scan_pipe(a, st), "chunk scan launch");
+    if (use_chunk(shape, opts)) return map_hip(swila::launch_scan_pipe(a, st), "chunk scan launch");
     return map_hip(swila::launch_scan_direct(a, st), "scan launch");
 }
 
@@ -329,6 +367,8 @@ int swila_forward_temporal(const swila_shape *shape, const swila_opts *opts, con
     if (rc) return rc;
     rc = check_temporal(shape, opts, temporal, q, k, v, beta_logit, prior_k_logit, prior_q_logit,
                         state_in, state_out, o, resp_out, &a);
+    if (rc) return rc;
+    rc = check_chunk_j(shape, opts);
     if (rc) return rc;
     if (opts->algo == SWILA_ALGO_NEWTON)
         return fail(SWILA_EUNSUPPORTED,
@@ -347,9 +387,7 @@ int swila_forward_temporal(const swila_shape *shape, const swila_opts *opts, con
                                           1.0f / shape->J, st),
                        "prior state copy");
     }
-    const bool chunk = opts->algo == SWILA_ALGO_CHUNK_EXACT ||
-                       (opts->algo == SWILA_ALGO_AUTO && opts->in_dtype == SWILA_BF16);
-    if (chunk) return map_hip(swila::launch_scan_pipe(a, st), "chunk scan launch");
+    if (use_chunk(shape, opts)) return map_hip(swila::launch_scan_pipe(a, st), "chunk scan launch");
     return map_hip(swila::launch_scan_direct(a, st), "scan launch");
 }
 
@@ -389,6 +427,9 @@ int swila_forward_gated(const swila_shape *shape, const swila_opts *opts, const 
     if (rc) return rc;
     if (opts->algo == SWILA_ALGO_NEWTON || opts->algo == SWILA_ALGO_CHUNK_EXACT)
         return fail(SWILA_EUNSUPPORTED, "the gated form runs on SWILA_ALGO_RECURRENT");
+    if (shape->J * shape->Dk > swila::kMaxGatedJDk)
+        return fail(SWILA_EUNSUPPORTED, "gated forward: J * Dk = %d exceeds %d",
+                    shape->J * shape->Dk, swila::kMaxGatedJDk);
     hipStream_t st = static_cast<hipStream_t>(stream);
     if (shape->T == 0) {
         if (state_out) {
@@ -455,6 +496,9 @@ int swila_backward(const swila_shape *shape, const swila_opts *opts, const void 
     if (rc) return rc;
     rc = check_opts(opts);
     if (rc) return rc;
+    if (shape->J > swila::kMaxChunkJ)
+        return fail(SWILA_EUNSUPPORTED, "backward: J=%d, supported J <= %d", shape->J,
+                    swila::kMaxChunkJ);
     const size_t B = shape->B, H = shape->H, T = shape->T, Dk = shape->Dk, Dv = shape->Dv,
                  J = shape->J;
     const size_t ie = opts->in_dtype == SWILA_BF16 ? 2 : 4;

@@ -166,7 +166,10 @@ def test_error_text_is_thread_local_and_cleared(lib):
 def test_python_binding_checks_before_calling():
     torch = pytest.importorskip("torch")
     x = torch.zeros(1, 4, 1, 16)
+    lg = torch.zeros(1, 4, 1, 2, 16)
     with pytest.raises(ValueError, match="device tensor"):
+        sw.forward(x, x, x, lg, lg, lg)
+    with pytest.raises(ValueError, match="beta_logit has shape"):
         sw.forward(x, x, x, x, x, x)
 
 
@@ -286,3 +289,90 @@ def test_backward_argument_checks(lib):
     assert rc == sw.EINVAL and "grad_state_in overlaps grad_o" in msg
     rc, msg = call(shape=sw.Shape(B, H, T, 48, 64, J))
     assert rc == sw.EUNSUPPORTED
+
+
+def test_j_limits_of_each_form(lib):
+    """J = 16 is in the supported set (every J of the paper's sweep); the
+    chunked forms, the backward pass and the gated forward past J * Dk = 1024
+    reject it before anything is enqueued.  Only rejected calls are made."""
+    ptrs = [ctypes.c_void_p((1 << 20) + (i << 26)) for i in range(6)]
+    shape = sw.Shape(1, 2, 8, 128, 64, 16)
+    for algo in (sw.ALGO_CHUNK_EXACT, sw.ALGO_NEWTON):
+        opts = sw.Opts(sw.BF16, sw.BF16, algo, 0, 0, 0.0, 0)
+        rc, msg = _fwd(lib, shape, opts, ptrs)
+        assert rc == sw.EUNSUPPORTED and "J <= 8" in msg, msg
+        tp = sw.Temporal(1 << 32, (1 << 32) + (1 << 26), None, None)
+        rc, msg = _fwd_t(lib, tp, shape=shape, opts=opts)
+        assert rc == sw.EUNSUPPORTED, msg
+    rc = lib.swila_forward_gated(ctypes.byref(shape), ctypes.byref(OPTS), *ptrs,
+                                 ctypes.byref(sw.Gated(1 << 33)), None, None, None, FAKE2, None,
+                                 None)
+    assert rc == sw.EUNSUPPORTED and "J * Dk" in lib.swila_last_error().decode()
+    rc = lib.swila_backward(ctypes.byref(shape), ctypes.byref(OPTS), *ptrs, None,
+                            ctypes.c_void_p(1 << 33), None,
+                            *[ctypes.c_void_p((1 << 34) + (i << 26)) for i in range(6)], None,
+                            ctypes.c_void_p(1 << 36), 1 << 40, None)
+    assert rc == sw.EUNSUPPORTED and "J=16" in lib.swila_last_error().decode()
+    for j in (5, 6, 7, 9, 12, 15, 17, 32):
+        rc, msg = _fwd(lib, sw.Shape(1, 2, 8, 64, 64, j), OPTS, ptrs)
+        assert rc == sw.EUNSUPPORTED and "J=%d" % j in msg
+
+
+def test_newton_sync_status_needs_iters_out(lib):
+    shape = sw.Shape(1, 2, 8, 64, 64, 4)
+    opts = sw.Opts(sw.BF16, sw.BF16, sw.ALGO_NEWTON, 0, 0, 0.0, sw.FLAG_NEWTON_SYNC)
+    need = lib.swila_forward_workspace_bytes(ctypes.byref(shape), ctypes.byref(opts))
+    ptrs = [ctypes.c_void_p((1 << 20) + (i << 26)) for i in range(6)]
+    rc = lib.swila_forward(ctypes.byref(shape), ctypes.byref(opts), *ptrs, None, None, FAKE2,
+                           None, ctypes.c_void_p(1 << 36), need, None, None)
+    assert rc == sw.EINVAL and "needs iters_out" in lib.swila_last_error().decode()
+    assert sw.ENOTCONVERGED == -4
+
+
+def _cpu_layer(B=1, H=2, T=5, Dk=16, Dv=32, J=2, decode=False):
+    torch = pytest.importorskip("torch")
+    if decode:
+        shp = [(B, H, Dk), (B, H, Dk), (B, H, Dv)] + [(B, H, J, Dv)] * 3
+    else:
+        shp = [(B, T, H, Dk), (B, T, H, Dk), (B, T, H, Dv)] + [(B, T, H, J, Dv)] * 3
+    return torch, [torch.zeros(s) for s in shp]
+
+
+@pytest.mark.parametrize("entry", ["forward", "forward_temporal", "forward_gated", "decode_step",
+                                   "decode_step_temporal", "decode_step_gated"])
+@pytest.mark.parametrize("which", ["o", "state_out"])
+def test_binding_rejects_wrong_sized_outputs(entry, which):
+    """A caller-supplied o or state_out of the wrong shape is a ValueError raised
+    before any device check, so nothing reaches the library: the kernels would
+    write past the end of a smaller buffer."""
+    decode = entry.startswith("decode")
+    B, H, T, Dk, Dv, J = 1, 2, 5, 16, 32, 2
+    torch, ins = _cpu_layer(B, H, T, Dk, Dv, J, decode)
+    extra = []
+    gshape = (B, H, Dv) if decode else (B, T, H, Dv)
+    kw = {}
+    if entry.endswith("temporal"):
+        extra = [torch.zeros(gshape), torch.zeros(gshape)]
+    if entry.endswith("gated"):
+        extra = [torch.zeros((B, H, J, Dk) if decode else (B, T, H, J, Dk))]
+    state = torch.zeros((B, H, J, Dk, Dv))
+    bad_o = torch.zeros((B, H, Dv + 16) if decode else (B, T - 1, H, Dv))
+    bad_s = torch.zeros((B, H, J, Dk, Dv // 2))
+    if which == "o":
+        kw["o"] = bad_o
+    else:
+        kw["state_out"] = bad_s
+    fn = getattr(sw, entry)
+    args = ins + extra
+    if entry == "forward":
+        call = lambda: fn(*args, state, **kw)
+    elif entry == "forward_temporal":
+        call = lambda: fn(*args, state, None, **kw)
+    elif entry == "forward_gated":
+        call = lambda: fn(*args, state, **kw)
+    elif entry == "decode_step_temporal":
+        call = lambda: fn(*args, state, None, **kw)
+    else:
+        call = lambda: fn(*args, state, **kw)
+    with pytest.raises(ValueError, match="%s has shape" % which):
+        call()

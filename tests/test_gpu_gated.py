@@ -37,6 +37,9 @@ CASES = [
     (16, 16, 21, 64, 64, 4, "bf16", 0.1, False, 2.0),
     (16, 16, 18, 64, 64, 4, "f32", 0.2, True, 2.0),
     (8, 32, 19, 128, 128, 8, "bf16", 0.1, False, 2.0),
+    # J = 16 (J * Dk <= 1024: its gate tile fits LDS)
+    (1, 2, 37, 64, 64, 16, "f32", 0.1, False, 2.0),
+    (2, 1, 20, 16, 32, 16, "bf16", 0.2, True, 1.0),
 ]
 
 
@@ -91,6 +94,8 @@ DECODE = [
     (2, 2, 32, 16, 3, "f32", 3, True),
     (2, 1, 16, 32, 8, "bf16", 2, False),
     (5, 2, 128, 64, 1, "f32", 2, False),
+    (2, 2, 128, 128, 16, "bf16", 3, True),
+    (3, 1, 64, 32, 16, "f32", 2, False),
 ]
 
 
@@ -131,9 +136,9 @@ def test_gated_decode_steps(B, H, Dk, Dv, J, dtype, steps, temporal):
     assert eo <= tol and es <= tol and ep <= tol
 
 
-def test_gated_config2_sampled_heads():
+def test_gated_config2_every_head():
     """The c2 batch, as the benchmark times it, through the gated form (decay
-    logits N(2,1)); the oracle on sampled heads."""
+    logits N(2,1)); the oracle on every head."""
     import torch
     import paper_2609_39034_amd as sw
     inp = workloads.config_inputs(2)
@@ -144,11 +149,9 @@ def test_gated_config2_sampled_heads():
     o, s, r = sw.forward_gated(*(dev[n] for n in NAMES), _t(dec, "bf16"), None, resp=True)
     torch.cuda.synchronize()
     o, s, r = (x.float().cpu().numpy().astype(np.float64) for x in (o, s, r))
-    for b, h in [(0, 0), (3, 7), (2, 4)]:
-        sub = [inp[n][b:b + 1, :, h:h + 1] for n in NAMES]
-        ref = oracle.forward(*sub, None, decay_logit=dec[b:b + 1, :, h:h + 1], want_resp=True)
-        eo = head_rel_err(o[b:b + 1, :, h:h + 1], ref["o"], "o")
-        es = head_rel_err(s[b:b + 1, h:h + 1], ref["state"], "state")
-        er = head_rel_err(r[b:b + 1, :, h:h + 1], ref["resp"], "resp")
-        print("head (%d,%d): o %.3e state %.3e resp %.3e" % (b, h, eo, es, er))
-        assert eo <= 2e-2 and es <= 2e-2 and er <= 2e-2
+    ref = oracle.forward(*(inp[n] for n in NAMES), None, decay_logit=dec, want_resp=True)
+    eo = head_rel_err(o, ref["o"], "o")
+    es = head_rel_err(s, ref["state"], "state")
+    er = head_rel_err(r, ref["resp"], "resp")
+    print("worst head: o %.3e state %.3e resp %.3e" % (eo, es, er))
+    assert eo <= 2e-2 and es <= 2e-2 and er <= 2e-2

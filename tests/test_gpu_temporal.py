@@ -11,7 +11,7 @@ import pytest
 
 import oracle
 import workloads
-from gpu_helpers import NAMES, head_rel_err, to_device, tol_for, torch_dtype
+from gpu_helpers import NAMES, head_rel_err, range_edge_inputs, to_device, tol_for, torch_dtype
 
 pytestmark = pytest.mark.gpu
 
@@ -239,8 +239,40 @@ def test_temporal_chunk_extreme_errors():
     assert eo <= 2e-2 and es <= 2e-2 and er <= 2e-2 and ep <= 2e-2
 
 
-@pytest.mark.parametrize("cfg,heads", [(2, [(0, 0), (3, 7)]), (3, [(0, 0), (7, 15)]),
-                                       (5, [(1, 7)])])
+@pytest.mark.parametrize("algo", ["chunk", "recurrent"])
+def test_temporal_softmax_band(algo):
+    """The largest rbar e^{-delta^2/2} of each (t, d) in [2^-125, 2^-111], other
+    components' terms below 2^-126 with r well above the tolerance (App. B.3
+    with eq. responsibility): the temporal chunk scan reruns those chunks with
+    the maximum subtracted."""
+    inp = range_edge_inputs("band", seed=702)
+    B, T, H, Dk = inp["q"].shape
+    J, Dv = inp["lb"].shape[3], inp["lb"].shape[4]
+    tmp = workloads.temporal_inputs(B, H, T, Dv, J, dtype="bf16", seed=702, prior_state=True)
+    o, s, p, r = _run_gpu(inp, tmp, "bf16", algo=algo)
+    ref = _run_oracle(inp, tmp)
+    eo, es = head_rel_err(o, ref["o"], "o"), head_rel_err(s, ref["state"], "state")
+    er, ep = head_rel_err(r, ref["resp"], "resp"), _prior_err(p, ref["prior"])
+    print("o %.3e state %.3e resp %.3e prior %.3e" % (eo, es, er, ep))
+    assert eo <= 2e-2 and es <= 2e-2 and er <= 2e-2 and ep <= 2e-2
+
+
+@pytest.mark.parametrize("B,H,T,Dk,Dv,dtype", [(1, 2, 37, 64, 64, "f32"), (2, 1, 20, 128, 32, "bf16")])
+def test_temporal_sixteen_components(B, H, T, Dk, Dv, dtype):
+    """J = 16 (token-by-token scan), temporal priors carried in and out."""
+    J = 16
+    inp = workloads.iid_inputs(B, H, T, Dk, Dv, J, dtype=dtype, seed=820 + T, state_std=0.1)
+    tmp = workloads.temporal_inputs(B, H, T, Dv, J, dtype=dtype, seed=820 + T, prior_state=True)
+    o, s, p, r = _run_gpu(inp, tmp, dtype)
+    ref = _run_oracle(inp, tmp)
+    tol = tol_for(dtype)
+    eo, es = head_rel_err(o, ref["o"], "o"), head_rel_err(s, ref["state"], "state")
+    er, ep = head_rel_err(r, ref["resp"], "resp"), _prior_err(p, ref["prior"])
+    print("o %.3e state %.3e resp %.3e prior %.3e" % (eo, es, er, ep))
+    assert eo <= tol and es <= tol and er <= tol and ep <= tol
+
+
+@pytest.mark.parametrize("cfg,heads", [(2, [(0, 0), (3, 7)])])
 def test_temporal_standard_configs_sampled_heads(cfg, heads):
     """The standard batches, in the launch shape the benchmark times, through the
     temporal chunk scan with N(0,1) gate logits; the oracle on sampled heads."""
