@@ -180,19 +180,24 @@ def newton_alg_flops(B, H, T, Dk, Dv, J, sweeps, chunk=16):
     return 2 * B * H * (sweeps * nch * per_chunk + T * Dk * J * Dv)
 
 
-def bench_newton(sw, torch, dev, cfg, steps, warmup, o, s_out, tol):
+def bench_newton(sw, torch, dev, cfg, steps, warmup, o, s_out, tol, unnormalized=False,
+                 clamp=True):
     B, H, T, Dk, Dv, J = (cfg[x] for x in ("B", "H", "T", "Dk", "Dv", "J"))
     batch = "B=%d H=%d T=%d Dk=Dv=%d J=%d" % (B, H, T, Dk, J)
     ws = torch.empty(sw.forward_workspace_bytes(B, H, T, Dk, Dv, J, algo="newton"),
                      device="cuda", dtype=torch.uint8)
     it = torch.zeros(2, device="cuda", dtype=torch.int32)
     wall, kern = time_forward(sw, torch, dev, steps, warmup, o, s_out, "newton", workspace=ws,
-                              tol=tol, max_iters=256, iters_out=it)
+                              tol=tol, max_iters=256, iters_out=it, unnormalized=unnormalized,
+                              clamp=clamp)
     sweeps, unconverged = (int(x) for x in it.cpu())
     nflop = newton_alg_flops(B, H, T, Dk, Dv, J, sweeps)
+    form = ("App. D.2's unnormalised-responsibility variant (exact Jacobian)" if unnormalized
+            else "App. D chunkwise quasi-Newton")
+    jac = "g clamped to [0, 2/|k|^2]" if clamp else "g unclamped"
     return {
-        "workload": "App. D chunkwise quasi-Newton, %s, bf16 inputs, tol %g (relative change "
-                    "of the predictions), g clamped to [0, 2/|k|^2]" % (batch, tol),
+        "workload": "%s, %s, bf16 inputs, tol %g (relative change of the predictions), %s"
+                    % (form, batch, tol, jac),
         "tokens_per_s": B * T / wall, "ms_per_step": wall * 1e3, "sweeps": sweeps,
         "unconverged_blocks": unconverged,
         "roofline": {"bound": "mfma", "achieved": nflop / kern / 1e12,
@@ -409,8 +414,11 @@ def bench_gated(sw, torch, workloads, dev, cfg, seed, steps, warmup, o, s_out, t
 
 def newton_study(sw, torch, workloads, steps, tol):
     """The paper's only chunked measurement (App. D.2): batch 16, T = 4096, 8 heads,
-    D = 64, J = 4, synthetic N(0,1) inputs.  Runs the App. D form to tolerance and
-    the exact chunk scan on the same batch, and compares their outputs."""
+    D = 64, J = 4, synthetic N(0,1) inputs.  Runs the exact chunk scan, the App. D
+    form, and App. D.2's unnormalised-responsibility variant (clamped and with
+    its exact Jacobian unclamped) to tolerance on the same batch.  The variant is
+    a different recurrence: only the normalised form is compared with the exact
+    chunk scan."""
     B, H, T, Dk, Dv, J = 16, 8, 4096, 64, 64, 4
     inp = workloads.iid_inputs(B, H, T, Dk, Dv, J, dtype="bf16", seed=1042)
     dev = workloads.to_torch(inp, "cuda", torch.bfloat16)
@@ -430,6 +438,14 @@ def newton_study(sw, torch, workloads, steps, tol):
         "newton_over_exact": res["ms_per_step"] / (wall_x * 1e3),
         "max_rel_diff_vs_exact": {"o": diff_o, "state": diff_s},
     })
+    variants = {}
+    for name, clamp in (("unnormalized_clamped", True), ("unnormalized_exact_jacobian", False)):
+        v = bench_newton(sw, torch, dev, cfg, steps, 1, o, s_out, tol, unnormalized=True,
+                         clamp=clamp)
+        variants[name] = {x: v[x] for x in ("workload", "ms_per_step", "sweeps",
+                                             "unconverged_blocks")}
+        variants[name]["mfma_frac"] = v["roofline"]["frac"]
+    res["variants"] = variants
     return res
 
 

@@ -83,13 +83,21 @@ enum swila_flags {
                                        keeps every linearised transition I - g k k^T
                                        non-expansive; the fixed point does not depend on the
                                        Jacobian approximation (App. D.2). */
-    SWILA_FLAG_NEWTON_SYNC = 2      /* SWILA_ALGO_NEWTON, for callers that want a status:
+    SWILA_FLAG_NEWTON_SYNC = 2,     /* SWILA_ALGO_NEWTON, for callers that want a status:
                                        swila_forward waits for the stream after the launch,
                                        reads iters_out (then required) and returns
                                        SWILA_ENOTCONVERGED if some block of columns stopped
                                        at max_iters without meeting tol.  Its outputs are
                                        written either way.  Without the flag the call only
                                        enqueues, and iters_out is the report. */
+    SWILA_FLAG_UNNORMALIZED = 4     /* SWILA_ALGO_NEWTON only (other algorithms and entry
+                                       points return SWILA_EUNSUPPORTED): evaluate App. D.2's
+                                       variant of the recurrence whose responsibilities drop
+                                       the denominator of eq. responsibility,
+                                       r = pi^k exp(-delta^2/2).  Its Jacobian is exact,
+                                       g = beta r (1 - delta^2), so the sweeps are Newton's
+                                       method proper.  It is a different recurrence: the
+                                       outputs are those of the variant. */
 };
 
 typedef struct swila_opts {

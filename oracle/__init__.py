@@ -52,7 +52,7 @@ def load_library(path):
     dp = ctypes.POINTER(ctypes.c_double)
     lib.swila_oracle_forward.argtypes = [ctypes.c_int] * 6 + [dp] * 11 + [ctypes.c_int]
     lib.swila_oracle_forward.restype = ctypes.c_int
-    lib.swila_oracle_forward_ext.argtypes = ([ctypes.c_int] * 6 + [dp] * 9 + [ctypes.c_int]
+    lib.swila_oracle_forward_ext.argtypes = ([ctypes.c_int] * 6 + [dp] * 9 + [ctypes.c_int] * 2
                                              + [dp] * 7 + [ctypes.c_int])
     lib.swila_oracle_forward_ext.restype = ctypes.c_int
     return lib
@@ -78,8 +78,8 @@ def _ptr(x):
 
 def forward(q, k, v, beta_logit, prior_k_logit, prior_q_logit, state_in=None, *,
             gate_k_logit=None, gate_q_logit=None, prior_in=None, decay_logit=None,
-            post_decay: bool = False, nthreads: int = 0, want_resp: bool = False,
-            want_delta: bool = False, lib=None):
+            post_decay: bool = False, unnormalized: bool = False, nthreads: int = 0,
+            want_resp: bool = False, want_delta: bool = False, lib=None):
     """Run the recurrence over a whole sequence.
 
     Shapes: q, k [B,T,H,Dk]; v [B,T,H,Dv]; the three logit tensors
@@ -100,6 +100,9 @@ def forward(q, k, v, beta_logit, prior_k_logit, prior_q_logit, state_in=None, *,
     a = sigmoid(decay_logit), one gate per key dimension and component, before
     the prediction (eq. pre-decay), or after it with ``post_decay`` (eq.
     post-decay).  It combines with the temporal priors.
+
+    ``unnormalized`` (App. D.2): the variant whose responsibilities drop the
+    denominator of eq. responsibility, r = pi^k exp(-delta^2/2); plain form only.
     """
     q, k, v = _f64(q), _f64(k), _f64(v)
     lb, lk, lq = _f64(beta_logit), _f64(prior_k_logit), _f64(prior_q_logit)
@@ -120,7 +123,9 @@ def forward(q, k, v, beta_logit, prior_k_logit, prior_q_logit, state_in=None, *,
     dec = _f64(decay_logit)
     if dec is not None:
         assert dec.shape == (B, T, H, J, Dk)
-    if temporal or dec is not None:
+    if unnormalized and (temporal or dec is not None):
+        raise ValueError("the unnormalised variant is defined for the plain form only")
+    if temporal or dec is not None or unnormalized:
         gk, gq, p_in = _f64(gate_k_logit), _f64(gate_q_logit), _f64(prior_in)
         p_out = None
         if temporal:
@@ -133,7 +138,8 @@ def forward(q, k, v, beta_logit, prior_k_logit, prior_q_logit, state_in=None, *,
             assert prior_in is None, "prior_in needs the gate logits"
         rc = (lib or _load()).swila_oracle_forward_ext(
             B, H, T, Dk, Dv, J, _ptr(q), _ptr(k), _ptr(v), _ptr(lb), _ptr(lk), _ptr(lq),
-            _ptr(gk), _ptr(gq), _ptr(dec), int(bool(post_decay)), _ptr(s_in), _ptr(p_in),
+            _ptr(gk), _ptr(gq), _ptr(dec), int(bool(post_decay)), int(bool(unnormalized)),
+            _ptr(s_in), _ptr(p_in),
             _ptr(s_out), _ptr(p_out), _ptr(o), _ptr(resp), _ptr(delta), int(nthreads))
     else:
         assert prior_in is None, "prior_in needs the gate logits"

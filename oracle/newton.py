@@ -35,6 +35,13 @@ Readings taken where the appendix is silent:
   eigenvalue other than 1 is 1 - g |k|^2).  Without such a clip, g < 0 makes
   transitions expansive and the iterates of long sequences overflow before
   they converge.
+* ``unnormalized`` runs App. D.2's variant of the recurrence whose
+  responsibilities drop the denominator of eq. responsibility,
+  r = pi^k exp(-delta^2/2).  Each (j, d) column is then a recurrence of its own,
+  and its Jacobian I - g k k^T with g = beta r (1 - delta^2) is exact (the
+  derivative of r delta along w is -r (1 - delta^2) k^T), so the iteration is
+  Newton's method proper; its fixed point is the sequential trajectory of the
+  same variant.
 """
 from __future__ import annotations
 
@@ -47,15 +54,20 @@ def _softmax_j(x):
     return e / e.sum(axis=0, keepdims=True)
 
 
-def linearise(pred, v, beta, prior_k, g_clamp=None, kk=None):
+def linearise(pred, v, beta, prior_k, g_clamp=None, kk=None, unnormalized=False):
     """Jacobian coefficient g (eq. jacobian_coeff) and effective input p
     (eq. effective_input) around predictions ``pred`` = k_t^T w^{(i)}_{t-1}.
     pred, beta, prior_k [T,J,Dv]; v [T,Dv]; kk [T] = |k_t|^2 (needed for
-    g_clamp="stable").  Returns (g, p, delta, r)."""
+    g_clamp="stable").  With ``unnormalized``, r has no denominator and g is
+    the exact coefficient of that variant (App. D.2).  Returns (g, p, delta, r)."""
     delta = v[:, None, :] - pred
     num = prior_k * np.exp(-0.5 * delta ** 2)
-    r = num / num.sum(axis=1, keepdims=True)
-    g = beta * r * (1.0 - delta ** 2 * (1.0 - r))
+    if unnormalized:
+        r = num
+        g = beta * r * (1.0 - delta ** 2)
+    else:
+        r = num / num.sum(axis=1, keepdims=True)
+        g = beta * r * (1.0 - delta ** 2 * (1.0 - r))
     if isinstance(g_clamp, str):
         if g_clamp != "stable":
             raise ValueError("g_clamp must be None, (lo, hi) or 'stable'")
@@ -68,7 +80,8 @@ def linearise(pred, v, beta, prior_k, g_clamp=None, kk=None):
     return g, p, delta, r
 
 
-def newton_head(q, k, v, lb, lk, lq, W0=None, *, chunk, iters, g_clamp=None, tol=None):
+def newton_head(q, k, v, lb, lk, lq, W0=None, *, chunk, iters, g_clamp=None, tol=None,
+                unnormalized=False):
     """One head.  q, k [T,Dk]; v [T,Dv]; logits [T,J,Dv]; W0 [J,Dv,Dk] (paper
     layout: W0[j, d] is w_{jd}) or None.
 
@@ -94,7 +107,8 @@ def newton_head(q, k, v, lb, lk, lq, W0=None, *, chunk, iters, g_clamp=None, tol
     n_run = 0
     for _ in range(iters):
         # linearisation around the current iterate (App. D.2)
-        g, p, _, _ = linearise(pred, v, beta, prior_k, g_clamp, kk=np.einsum("ti,ti->t", k, k))
+        g, p, _, _ = linearise(pred, v, beta, prior_k, g_clamp, kk=np.einsum("ti,ti->t", k, k),
+                               unnormalized=unnormalized)
 
         new_pred = np.zeros_like(pred)
         Wb = W0.copy()                      # boundary state w_[n]
@@ -130,7 +144,8 @@ def newton_head(q, k, v, lb, lk, lq, W0=None, *, chunk, iters, g_clamp=None, tol
     return {"o": o, "W": W_end, "preds": preds, "iters": n_run}
 
 
-def newton_forward(q, k, v, lb, lk, lq, state_in=None, *, chunk, iters, g_clamp=None, tol=None):
+def newton_forward(q, k, v, lb, lk, lq, state_in=None, *, chunk, iters, g_clamp=None, tol=None,
+                   unnormalized=False):
     """All heads, in the library's layouts: q, k [B,T,H,Dk]; v [B,T,H,Dv];
     logits [B,T,H,J,Dv]; state [B,H,J,Dk,Dv].  Returns (o [B,T,H,Dv],
     state [B,H,J,Dk,Dv], per-head result dicts)."""
@@ -147,7 +162,8 @@ def newton_forward(q, k, v, lb, lk, lq, state_in=None, *, chunk, iters, g_clamp=
             if state_in is not None:
                 W0 = np.transpose(np.asarray(state_in, dtype=np.float64)[b, h], (0, 2, 1))
             res = newton_head(q[b, :, h], k[b, :, h], v[b, :, h], lb[b, :, h], lk[b, :, h],
-                              lq[b, :, h], W0, chunk=chunk, iters=iters, g_clamp=g_clamp, tol=tol)
+                              lq[b, :, h], W0, chunk=chunk, iters=iters, g_clamp=g_clamp, tol=tol,
+                              unnormalized=unnormalized)
             o[b, :, h] = res["o"]
             S[b, h] = np.transpose(res["W"], (0, 2, 1))
             heads[(b, h)] = res

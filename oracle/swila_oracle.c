@@ -58,6 +58,17 @@
  * Post-decay (eq. post-decay; kept here for the J = 1 equivalence the paper
  * states): delta and r from w_{t-1}, then w_{tjd} = a_{tj} (.) w_{t-1,jd} +
  * beta r delta k_t.  Decay logits are [B, T, H, J, Dk].
+ *
+ * Unnormalised responsibilities (App. D.2), when asked for: the variant of the
+ * recurrence whose Jacobian has no cross-component terms, obtained by dropping
+ * the denominator of eq. responsibility,
+ *
+ *   r_{tjd} = pi^k_{jd} exp(-delta_{tjd}^2 / 2),
+ *
+ * so that the update is beta times the gradient of the mixture likelihood
+ * sum_j pi_j exp(-delta_j^2/2) itself rather than of its logarithm.  Everything
+ * else (prediction, retrieval) is unchanged.  It is defined for the plain form
+ * only.
  */
 #include <math.h>
 #include <pthread.h>
@@ -74,6 +85,7 @@ typedef struct {
     double *prior_out;
     const double *decay;                 /* gated form: decay logits */
     int post_decay;
+    int unnormalized;                    /* App. D.2 variant: r without its normaliser */
     int next_head;              /* work counter, guarded by mu */
     int status;                 /* first error seen, guarded by mu */
     pthread_mutex_t mu;
@@ -162,9 +174,11 @@ static int run_head(job_t *a, int b, int h)
             }
             if (!(Z > 0.0) || !isfinite(Z)) { rc = -1; break; }
 
-            /* M-step: one gradient step of size beta on the log-likelihood */
+            /* M-step: one gradient step of size beta on the log-likelihood
+             * (unnormalised variant: on the likelihood, r without Z) */
             for (int j = 0; j < J; ++j) {
-                const double r = num[j] / Z;
+                double r = num[j] / Z;
+                if (a->unnormalized) r = prior[j] * exp(-0.5 * delta[j] * delta[j]);
                 const double beta = 1.0 / (1.0 + exp(-lbt[(size_t)j * Dv + d]));
                 double *w = W + ((size_t)j * Dv + d) * Dk;
                 if (a->decay && a->post_decay) {   /* gated, post-decay */
@@ -244,7 +258,8 @@ int swila_oracle_forward_ext(int B, int H, int T, int Dk, int Dv, int J,
                              const double *beta_logit, const double *prior_k_logit,
                              const double *prior_q_logit, const double *gate_k_logit,
                              const double *gate_q_logit, const double *decay_logit,
-                             int post_decay, const double *state_in, const double *prior_in,
+                             int post_decay, int unnormalized,
+                             const double *state_in, const double *prior_in,
                              double *state_out, double *prior_out, double *o, double *resp_out,
                              double *delta_out, int nthreads);
 
@@ -263,7 +278,7 @@ int swila_oracle_forward(int B, int H, int T, int Dk, int Dv, int J,
                          double *delta_out, int nthreads)
 {
     return swila_oracle_forward_ext(B, H, T, Dk, Dv, J, q, k, v, beta_logit, prior_k_logit,
-                                    prior_q_logit, NULL, NULL, NULL, 0, state_in, NULL,
+                                    prior_q_logit, NULL, NULL, NULL, 0, 0, state_in, NULL,
                                     state_out, NULL, o, resp_out, delta_out, nthreads);
 }
 
@@ -274,18 +289,22 @@ int swila_oracle_forward(int B, int H, int T, int Dk, int Dv, int J,
  * post_decay selects eq. post-decay instead of eq. pre-decay).  prior_in is the
  * prior state [B, H, 2, J, Dv] or NULL (uniform); prior_out receives the
  * final one, or is NULL.  Without either this is the plain forward.
+ * unnormalized selects App. D.2's unnormalised responsibilities (plain form
+ * only: -3 with gates or decay).
  */
 int swila_oracle_forward_ext(int B, int H, int T, int Dk, int Dv, int J,
                              const double *q, const double *k, const double *v,
                              const double *beta_logit, const double *prior_k_logit,
                              const double *prior_q_logit, const double *gate_k_logit,
                              const double *gate_q_logit, const double *decay_logit,
-                             int post_decay, const double *state_in, const double *prior_in,
+                             int post_decay, int unnormalized,
+                             const double *state_in, const double *prior_in,
                              double *state_out, double *prior_out, double *o, double *resp_out,
                              double *delta_out, int nthreads)
 {
     if (B < 0 || H < 0 || T < 0 || Dk <= 0 || Dv <= 0 || J <= 0) return -3;
     if ((gate_k_logit == NULL) != (gate_q_logit == NULL)) return -3;
+    if (unnormalized && (gate_k_logit || decay_logit)) return -3;
     job_t a;
     memset(&a, 0, sizeof a);
     a.B = B; a.H = H; a.T = T; a.Dk = Dk; a.Dv = Dv; a.J = J;
@@ -296,6 +315,7 @@ int swila_oracle_forward_ext(int B, int H, int T, int Dk, int Dv, int J,
     a.gk = gate_k_logit; a.gq = gate_q_logit;
     a.prior_in = prior_in; a.prior_out = prior_out;
     a.decay = decay_logit; a.post_decay = post_decay;
+    a.unnormalized = unnormalized;
     return run_all(&a, nthreads);
 }
 

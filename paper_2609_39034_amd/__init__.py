@@ -27,7 +27,7 @@ __all__ = ["forward", "decode_step", "forward_temporal", "decode_step_temporal",
            "state_init", "state_bytes", "forward_workspace_bytes",
            "version", "library_path", "SwilaError", "F32", "BF16", "ALGO_AUTO",
            "ALGO_RECURRENT", "ALGO_CHUNK_EXACT", "ALGO_NEWTON", "FLAG_NEWTON_NO_CLAMP",
-           "FLAG_NEWTON_SYNC", "ENOTCONVERGED"]
+           "FLAG_NEWTON_SYNC", "FLAG_UNNORMALIZED", "ENOTCONVERGED"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB_PATH = os.path.join(_HERE, "libswila.so")
@@ -36,7 +36,7 @@ F32, BF16 = 0, 1
 ALGO_AUTO, ALGO_RECURRENT, ALGO_CHUNK_EXACT, ALGO_NEWTON = 0, 1, 2, 3
 _ALGOS = {"auto": ALGO_AUTO, "recurrent": ALGO_RECURRENT, "chunk": ALGO_CHUNK_EXACT,
           "newton": ALGO_NEWTON}
-FLAG_NEWTON_NO_CLAMP, FLAG_NEWTON_SYNC = 1, 2
+FLAG_NEWTON_NO_CLAMP, FLAG_NEWTON_SYNC, FLAG_UNNORMALIZED = 1, 2, 4
 
 OK, EINVAL, EUNSUPPORTED, EHIP, ENOTCONVERGED = 0, -1, -2, -3, -4
 
@@ -248,7 +248,7 @@ def _layer_shapes(q, v, lb, decode):
 def forward(q, k, v, beta_logit, prior_k_logit, prior_q_logit, state_in=None, *,
             state_out=True, o=None, out_dtype=None, resp=False, algo="auto", chunk=0,
             workspace=None, max_iters=0, tol=0.0, clamp=True, iters_out=None,
-            sync_status=False, stream=None):
+            sync_status=False, unnormalized=False, stream=None):
     """Forward over whole sequences (swila_forward).
 
     q, k [B,T,H,Dk]; v [B,T,H,Dv]; logits [B,T,H,J,Dv] (one dtype: float32 or
@@ -263,7 +263,8 @@ def forward(q, k, v, beta_logit, prior_k_logit, prior_q_logit, state_in=None, *,
     elements: most sweeps of any block, blocks not converged); the workspace
     is allocated here unless given.  sync_status=True (needs iters_out) waits
     for the launch and raises SwilaError with code ENOTCONVERGED when some
-    block did not meet tol.
+    block did not meet tol.  unnormalized=True (algo "newton" only) evaluates
+    App. D.2's variant with responsibilities r = pi^k exp(-delta^2/2).
     Returns (o, state_out or None) or (o, state_out, resp).
     """
     torch = _torch()
@@ -284,7 +285,8 @@ def forward(q, k, v, beta_logit, prior_k_logit, prior_q_logit, state_in=None, *,
     r = None
     if resp:
         r = torch.empty((B, T, H, J, Dv), device=q.device, dtype=torch.float32)
-    flags = (0 if clamp else FLAG_NEWTON_NO_CLAMP) | (FLAG_NEWTON_SYNC if sync_status else 0)
+    flags = ((0 if clamp else FLAG_NEWTON_NO_CLAMP) | (FLAG_NEWTON_SYNC if sync_status else 0)
+             | (FLAG_UNNORMALIZED if unnormalized else 0))
     opts = Opts(code, _dtype_code(o), _ALGOS[algo], int(chunk), int(max_iters), float(tol),
                 flags)
     shape = Shape(B, H, T, Dk, Dv, J)

@@ -66,6 +66,7 @@ struct NewtonArgs {
     int max_iters;      // sweeps at most (>= 1)
     float tol;          // stop when the change is <= tol * max(1, |pred|); < 0: max_iters sweeps
     bool clamp;         // clamp g to [0, 2 / |k_t|^2]
+    bool unnorm;        // App. D.2 variant: responsibilities without their normaliser
 };
 
 // Token-by-token scan with fp32 state in registers.  Returns the HIP status of

@@ -683,28 +683,47 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
                 const bool ok = m * kC + t < T;
                 float vv[PE];
                 bf16_row<PE>(sm.v[rs], e, vv);
-                float dj[J][PE], xj[J][PE], mx[PE], z[PE];
+                float dj[J][PE], xj[J][PE], lka[J][PE], mx[PE], z[PE];
 #pragma unroll
                 for (int u = 0; u < PE; ++u) mx[u] = -INFINITY, z[u] = 0.f;
 #pragma unroll
                 for (int j = 0; j < J; ++j) {
-                    float pj[PE], lkj[PE];
+                    float pj[PE];
                     f32_load<PE>(po + t * N + j * DB + dl, pj);
-                    bf16_row<PE>(sm.lk[rs], t * N + j * DB + dl, lkj);
+                    bf16_row<PE>(sm.lk[rs], t * N + j * DB + dl, lka[j]);
 #pragma unroll
                     for (int u = 0; u < PE; ++u) {
                         dj[j][u] = vv[u] - pj[u];
-                        xj[j][u] = kLog2e * fmaf(-0.5f * dj[j][u], dj[j][u], lkj[u]);
+                        xj[j][u] = kLog2e * fmaf(-0.5f * dj[j][u], dj[j][u], lka[j][u]);
                         mx[u] = fmaxf(mx[u], xj[j][u]);
                     }
                 }
+                if (na.unnorm) {
+                    // App. D.2's variant: r = pi^k e^{-delta^2/2} with no
+                    // normaliser, pi^k = softmax_j of the logits; the exponent
+                    // log2(e) (lk - max lk - delta^2/2) is at most 0
 #pragma unroll
-                for (int j = 0; j < J; ++j)
+                    for (int u = 0; u < PE; ++u) mx[u] = -INFINITY;
 #pragma unroll
-                    for (int u = 0; u < PE; ++u) {
-                        xj[j][u] = __builtin_amdgcn_exp2f(xj[j][u] - mx[u]);
-                        z[u] += xj[j][u];
-                    }
+                    for (int j = 0; j < J; ++j)
+#pragma unroll
+                        for (int u = 0; u < PE; ++u) mx[u] = fmaxf(mx[u], lka[j][u]);
+#pragma unroll
+                    for (int j = 0; j < J; ++j)
+#pragma unroll
+                        for (int u = 0; u < PE; ++u) {
+                            z[u] += exp_fast(lka[j][u] - mx[u]);
+                            xj[j][u] = __builtin_amdgcn_exp2f(fmaf(-kLog2e, mx[u], xj[j][u]));
+                        }
+                } else {
+#pragma unroll
+                    for (int j = 0; j < J; ++j)
+#pragma unroll
+                        for (int u = 0; u < PE; ++u) {
+                            xj[j][u] = __builtin_amdgcn_exp2f(xj[j][u] - mx[u]);
+                            z[u] += xj[j][u];
+                        }
+                }
 #pragma unroll
                 for (int u = 0; u < PE; ++u) z[u] = rcp_fast(z[u]);
 #pragma unroll
@@ -716,7 +735,10 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
                         const float r = xj[j][u] * z[u];
                         const float br = sigmoid(lbj[u]) * r;
                         const float d = dj[j][u];
-                        gv[u] = ok ? br * fmaf(-d * d, 1.f - r, 1.f) : 0.f;
+                        // eq. jacobian_coeff; the variant's exact coefficient drops
+                        // the factor 1 - r that the normaliser contributes
+                        const float c1 = na.unnorm ? 1.f : 1.f - r;
+                        gv[u] = ok ? br * fmaf(-d * d, c1, 1.f) : 0.f;
                         bv[u] = ok ? br * d : 0.f;
                     }
                     f32_row<PE>(&sm.beta[pr][t][j * DB + dl], gv);

@@ -61,8 +61,11 @@ int check_opts(const swila_opts *o) {
         return fail(SWILA_EUNSUPPORTED, "chunk %d: the chunked forms use 16 (or 0)", o->chunk);
     if (o->max_iters < 0) return fail(SWILA_EINVAL, "max_iters %d < 0", o->max_iters);
     if (o->tol != o->tol) return fail(SWILA_EINVAL, "tol is NaN");
-    if (o->flags & ~(uint32_t)(SWILA_FLAG_NEWTON_NO_CLAMP | SWILA_FLAG_NEWTON_SYNC))
+    if (o->flags & ~(uint32_t)(SWILA_FLAG_NEWTON_NO_CLAMP | SWILA_FLAG_NEWTON_SYNC |
+                               SWILA_FLAG_UNNORMALIZED))
         return fail(SWILA_EINVAL, "unknown flags 0x%x", o->flags);
+    if ((o->flags & SWILA_FLAG_UNNORMALIZED) && o->algo != SWILA_ALGO_NEWTON)
+        return fail(SWILA_EUNSUPPORTED, "SWILA_FLAG_UNNORMALIZED needs SWILA_ALGO_NEWTON");
     return SWILA_OK;
 }
 
@@ -346,7 +349,8 @@ int swila_forward(const swila_shape *shape, const swila_opts *opts, const void *
         swila::NewtonArgs na{static_cast<float *>(workspace), iters_out,
                              opts->max_iters > 0 ? opts->max_iters : 64,
                              opts->tol == 0.f ? 1e-3f : opts->tol,
-                             (opts->flags & SWILA_FLAG_NEWTON_NO_CLAMP) == 0};
+                             (opts->flags & SWILA_FLAG_NEWTON_NO_CLAMP) == 0,
+                             (opts->flags & SWILA_FLAG_UNNORMALIZED) != 0};
         rc = map_hip(swila::launch_newton(a, na, st), "Newton launch");
         if (rc || !(opts->flags & SWILA_FLAG_NEWTON_SYNC)) return rc;
         return newton_status(iters_out, st);
@@ -401,6 +405,8 @@ int swila_decode_step_temporal(const swila_shape *shape, const swila_opts *opts,
     int rc = prepare(shape, opts, true, q, k, v, beta_logit, prior_k_logit, prior_q_logit,
                      state_in, state_out, o, nullptr, &a);
     if (rc) return rc;
+    if (opts->flags & SWILA_FLAG_UNNORMALIZED)
+        return fail(SWILA_EUNSUPPORTED, "decode evaluates the plain recurrence");
     rc = check_temporal(shape, opts, temporal, q, k, v, beta_logit, prior_k_logit, prior_q_logit,
                         state_in, state_out, o, nullptr, &a);
     if (rc) return rc;
@@ -457,6 +463,8 @@ int swila_decode_step_gated(const swila_shape *shape, const swila_opts *opts, co
     int rc = prepare(shape, opts, true, q, k, v, beta_logit, prior_k_logit, prior_q_logit,
                      state_in, state_out, o, nullptr, &a);
     if (rc) return rc;
+    if (opts->flags & SWILA_FLAG_UNNORMALIZED)
+        return fail(SWILA_EUNSUPPORTED, "decode evaluates the plain recurrence");
     if (temporal) {
         rc = check_temporal(shape, opts, temporal, q, k, v, beta_logit, prior_k_logit,
                             prior_q_logit, state_in, state_out, o, nullptr, &a);
@@ -476,6 +484,8 @@ int swila_decode_step(const swila_shape *shape, const swila_opts *opts, const vo
     int rc = prepare(shape, opts, true, q, k, v, beta_logit, prior_k_logit, prior_q_logit,
                      state_in, state_out, o, nullptr, &a);
     if (rc) return rc;
+    if (opts->flags & SWILA_FLAG_UNNORMALIZED)
+        return fail(SWILA_EUNSUPPORTED, "decode evaluates the plain recurrence");
     return map_hip(swila::launch_decode(a, static_cast<hipStream_t>(stream)), "decode launch");
 }
 
@@ -499,6 +509,8 @@ int swila_backward(const swila_shape *shape, const swila_opts *opts, const void 
     if (shape->J > swila::kMaxChunkJ)
         return fail(SWILA_EUNSUPPORTED, "backward: J=%d, supported J <= %d", shape->J,
                     swila::kMaxChunkJ);
+    if (opts->flags & SWILA_FLAG_UNNORMALIZED)
+        return fail(SWILA_EUNSUPPORTED, "backward: the plain recurrence only");
     const size_t B = shape->B, H = shape->H, T = shape->T, Dk = shape->Dk, Dv = shape->Dv,
                  J = shape->J;
     const size_t ie = opts->in_dtype == SWILA_BF16 ? 2 : 4;

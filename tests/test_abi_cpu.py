@@ -74,7 +74,9 @@ OPTS = sw.Opts(sw.BF16, sw.BF16, 0, 0, 0, 0.0, 0)
     (sw.Shape(1, 1, 4, 64, 64, 4), sw.Opts(1, 1, 2, 8, 0, 0.0, 0), sw.EUNSUPPORTED, "chunk 8"),
     (sw.Shape(1, 1, 4, 64, 64, 4), sw.Opts(1, 1, 3, 0, -1, 0.0, 0), sw.EINVAL, "max_iters"),
     (sw.Shape(1, 1, 4, 64, 64, 4), sw.Opts(1, 1, 3, 0, 0, float("nan"), 0), sw.EINVAL, "NaN"),
-    (sw.Shape(1, 1, 4, 64, 64, 4), sw.Opts(1, 1, 3, 0, 0, 0.0, 6), sw.EINVAL, "flags"),
+    (sw.Shape(1, 1, 4, 64, 64, 4), sw.Opts(1, 1, 3, 0, 0, 0.0, 0x40), sw.EINVAL, "flags"),
+    (sw.Shape(1, 1, 4, 64, 64, 4), sw.Opts(1, 1, 2, 0, 0, 0.0, 4), sw.EUNSUPPORTED,
+     "SWILA_FLAG_UNNORMALIZED needs SWILA_ALGO_NEWTON"),
 ])
 def test_forward_rejects_bad_shapes_and_options(lib, shape, opts, code, text):
     rc, msg = _fwd(lib, shape, opts)
@@ -376,3 +378,19 @@ def test_binding_rejects_wrong_sized_outputs(entry, which):
         call = lambda: fn(*args, state, **kw)
     with pytest.raises(ValueError, match="%s has shape" % which):
         call()
+
+
+def test_unnormalized_flag_is_forward_newton_only(lib):
+    """App. D.2's variant runs only as the App. D form of swila_forward: decode
+    and the backward evaluate the plain recurrence and reject the flag."""
+    ptrs = [ctypes.c_void_p((1 << 20) + (i << 26)) for i in range(6)]
+    opts = sw.Opts(sw.BF16, sw.BF16, sw.ALGO_NEWTON, 0, 0, 0.0, sw.FLAG_UNNORMALIZED)
+    rc = lib.swila_decode_step(ctypes.byref(sw.Shape(4, 2, 1, 64, 64, 4)), ctypes.byref(opts),
+                               *ptrs, None, None, FAKE2, None)
+    assert rc == sw.EUNSUPPORTED and "plain recurrence" in lib.swila_last_error().decode()
+    shape = sw.Shape(1, 2, 8, 64, 64, 4)
+    rc = lib.swila_backward(ctypes.byref(shape), ctypes.byref(opts), *ptrs, None,
+                            ctypes.c_void_p(1 << 33), None,
+                            *[ctypes.c_void_p((1 << 34) + (i << 26)) for i in range(6)], None,
+                            ctypes.c_void_p(1 << 36), 1 << 40, None)
+    assert rc == sw.EUNSUPPORTED and "plain recurrence" in lib.swila_last_error().decode()

@@ -16,7 +16,7 @@ from oracle import newton
 pytestmark = pytest.mark.gpu
 
 
-def gpu_newton(inp, *, iters, tol=-1.0, clamp=True, in_place=False):
+def gpu_newton(inp, *, iters, tol=-1.0, clamp=True, in_place=False, unnormalized=False):
     import paper_2609_39034_amd as sw
     import torch
     dev = to_device(inp, "bf16")
@@ -27,7 +27,7 @@ def gpu_newton(inp, *, iters, tol=-1.0, clamp=True, in_place=False):
         st = st.clone() if st is not None else None
         kw["state_out"] = st
     o, s = sw.forward(*(dev[n] for n in NAMES), st, algo="newton", max_iters=iters, tol=tol,
-                      clamp=clamp, iters_out=it, **kw)
+                      clamp=clamp, iters_out=it, unnormalized=unnormalized, **kw)
     torch.cuda.synchronize()
     return (o.float().cpu().numpy().astype(np.float64), s.cpu().numpy().astype(np.float64),
             it.cpu().numpy())
@@ -113,5 +113,70 @@ def test_config2_converges_to_sequential():
     ref = oracle.forward(*(inp[n] for n in NAMES), inp["state"], nthreads=16)
     eo, es = _errs(o, s, ref["o"], ref["state"])
     print("sweeps %d, unconverged blocks %d: o %.3e state %.3e" % (it[0], it[1], eo, es))
+    assert it[1] == 0
+    assert eo <= TOL_BF16 and es <= TOL_BF16
+
+
+def test_sync_status_reports_non_convergence():
+    """SWILA_FLAG_NEWTON_SYNC: one sweep with a tolerance no block can meet gives
+    SWILA_ENOTCONVERGED (outputs still written); enough sweeps give OK."""
+    import paper_2609_39034_amd as sw
+    import torch
+    inp = workloads.iid_inputs(1, 2, 100, 64, 64, 4, dtype="bf16", seed=350, state_std=0.1)
+    dev = to_device(inp, "bf16")
+    it = torch.zeros(2, dtype=torch.int32, device="cuda")
+    with pytest.raises(sw.SwilaError) as e:
+        sw.forward(*(dev[n] for n in NAMES), dev["state"], algo="newton", max_iters=1, tol=1e-9,
+                   iters_out=it, sync_status=True)
+    assert e.value.code == sw.ENOTCONVERGED
+    assert int(it[0]) == 1 and int(it[1]) > 0
+    sw.forward(*(dev[n] for n in NAMES), dev["state"], algo="newton", max_iters=200, tol=1e-4,
+               iters_out=it, sync_status=True)
+    assert int(it[1]) == 0
+
+
+# ---- App. D.2's unnormalised-responsibility variant (exact Jacobian)
+@pytest.mark.parametrize("B,H,T,Dk,Dv,J,std,sweeps,clamp", [
+    (1, 2, 40, 32, 32, 4, 0.1, 3, True),
+    (2, 1, 37, 64, 16, 3, 0.0, 2, True),
+    (1, 1, 50, 128, 64, 8, 0.1, 2, False),
+    (1, 2, 33, 16, 64, 1, 0.2, 4, False),
+    (4, 8, 20, 64, 128, 4, 0.1, 2, True),
+])
+def test_unnormalized_fixed_sweeps_match_newton_oracle(B, H, T, Dk, Dv, J, std, sweeps, clamp):
+    inp = workloads.iid_inputs(B, H, T, Dk, Dv, J, dtype="bf16", seed=360 + T + J, state_std=std)
+    o, s, it = gpu_newton(inp, iters=sweeps, clamp=clamp, unnormalized=True)
+    ref_o, ref_s, _ = newton.newton_forward(*(inp[n] for n in NAMES), inp["state"], chunk=16,
+                                            iters=sweeps, g_clamp="stable" if clamp else None,
+                                            unnormalized=True)
+    eo, es = _errs(o, s, ref_o, ref_s)
+    print("sweeps %d: o %.3e state %.3e" % (sweeps, eo, es))
+    assert eo <= TOL_BF16 and es <= TOL_BF16
+    assert it[0] == sweeps
+
+
+@pytest.mark.parametrize("clamp", [True, False])
+def test_unnormalized_converges_to_its_sequential_trajectory(clamp):
+    inp = workloads.iid_inputs(2, 2, 300, 64, 64, 4, dtype="bf16", seed=370, state_std=0.0)
+    o, s, it = gpu_newton(inp, iters=200, tol=1e-4, clamp=clamp, unnormalized=True)
+    ref = oracle.forward(*(inp[n] for n in NAMES), inp["state"], unnormalized=True)
+    eo, es = _errs(o, s, ref["o"], ref["state"])
+    print("clamp %s: sweeps %d, unconverged blocks %d: o %.3e state %.3e"
+          % (clamp, it[0], it[1], eo, es))
+    assert it[1] == 0
+    assert eo <= TOL_BF16 and es <= TOL_BF16
+
+
+# The paper's App. D.2 measurement shape: B=16, T=4096, H=8, D=64, J=4, synthetic
+# inputs; both variants to convergence against their sequential oracles on
+# every head.  The paper reports about 10 iterations for either.
+@pytest.mark.parametrize("unnormalized", [False, True])
+def test_study_shape_converges(unnormalized):
+    inp = workloads.iid_inputs(16, 8, 4096, 64, 64, 4, dtype="bf16", seed=1042)
+    o, s, it = gpu_newton(inp, iters=256, tol=1e-3, unnormalized=unnormalized)
+    ref = oracle.forward(*(inp[n] for n in NAMES), inp["state"], unnormalized=unnormalized)
+    eo, es = _errs(o, s, ref["o"], ref["state"])
+    print("study shape, %s: sweeps %d, unconverged blocks %d, worst head: o %.3e state %.3e"
+          % ("unnormalised" if unnormalized else "normalised", it[0], it[1], eo, es))
     assert it[1] == 0
     assert eo <= TOL_BF16 and es <= TOL_BF16

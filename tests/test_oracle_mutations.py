@@ -22,7 +22,7 @@ MUTATIONS = {
     "delta_sign_flipped": ("delta[j] = vt[d] - pred;", "delta[j] = pred - vt[d];", False),
     "prediction_with_query": ("pred += w[i] * kt[i];", "pred += w[i] * qt[i];", False),
     "prior_dropped": ("num[j] = prior[j] * exp(", "num[j] = 1.0 * exp(", False),
-    "responsibility_unnormalised": ("const double r = num[j] / Z;", "const double r = num[j];", False),
+    "responsibility_unnormalised": ("double r = num[j] / Z;", "double r = num[j];", False),
     "beta_dropped": ("w[i] += beta * r * delta[j] * kt[i];", "w[i] += r * delta[j] * kt[i];", False),
     "update_along_query": ("w[i] += beta * r * delta[j] * kt[i];",
                            "w[i] += beta * r * delta[j] * qt[i];", False),
