@@ -182,6 +182,31 @@ int swila_decode_step(const swila_shape *shape, const swila_opts *opts,
                       const float *state_in, float *state_out, void *o, void *stream);
 
 /*
+ * For callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc): swila_forward without
+ * the workspace arguments.  The arguments, results and errors are those of
+ * swila_forward; the forms that need scratch (SWILA_ALGO_NEWTON: the
+ * predictions of the current iterate) use a device array of
+ * SWILA_NOALLOC_SCRATCH_BYTES that the library holds on each GPU it runs on
+ * until the process ends, so the call allocates nothing.
+ *   - Limit: B*H*J*Dv*16*ceil(T/16)*4 <= SWILA_NOALLOC_SCRATCH_BYTES (64 MiB, e.g.
+ *     B=4 H=8 T=2048 Dv=64 J=4) for SWILA_ALGO_NEWTON; larger calls return
+ *     SWILA_EUNSUPPORTED before anything is enqueued.  Other forms need none.
+ *   - The stream must belong to the current device (hipGetDevice).  The first
+ *     call on a device looks up that device's copy of the array.
+ *   - Every call on a GPU shares that GPU's array, which keeps the last call's
+ *     contents (nothing in it needs to start at zero): calls that overlap on one
+ *     GPU, on different streams or threads, race.
+ */
+#define SWILA_NOALLOC_SCRATCH_BYTES (64u << 20)
+int swila_forward_noalloc(const swila_shape *shape, const swila_opts *opts,
+                          const void *q, const void *k, const void *v,
+                          const void *beta_logit, const void *prior_k_logit,
+                          const void *prior_q_logit,
+                          const float *state_in, float *state_out, void *o, float *resp_out,
+                          int32_t *iters_out, void *stream);
+
+/*
  * Temporal SwiLA (Sec. 3.3, App. B.3): the two priors become running mixtures
  * over time, per (b, h, j, d),
  *

@@ -9,6 +9,7 @@ library raises.
 
 Entry points (names as in the C ABI):
   ``forward``            whole sequences       -> swila_forward
+  ``forward_noalloc``    the same, allocating nothing -> swila_forward_noalloc
   ``decode_step``        one token per sequence -> swila_decode_step
   ``forward_temporal``, ``decode_step_temporal``  Temporal SwiLA (App. B.3)
                                                 -> swila_forward_temporal, ...
@@ -22,7 +23,7 @@ from __future__ import annotations
 import ctypes
 import os
 
-__all__ = ["forward", "decode_step", "forward_temporal", "decode_step_temporal",
+__all__ = ["forward", "forward_noalloc", "NOALLOC_SCRATCH_BYTES", "decode_step", "forward_temporal", "decode_step_temporal",
            "forward_gated", "decode_step_gated", "backward", "backward_workspace_bytes",
            "state_init", "state_bytes", "forward_workspace_bytes",
            "version", "library_path", "SwilaError", "F32", "BF16", "ALGO_AUTO",
@@ -96,6 +97,8 @@ def load_library():
     lib.swila_forward_workspace_bytes.argtypes = [sp, op]
     lib.swila_forward.restype = ctypes.c_int
     lib.swila_forward.argtypes = [sp, op] + [vp] * 6 + [vp, vp, vp, vp, vp, ctypes.c_size_t, vp, vp]
+    lib.swila_forward_noalloc.restype = ctypes.c_int
+    lib.swila_forward_noalloc.argtypes = [sp, op] + [vp] * 6 + [vp, vp, vp, vp, vp, vp]
     lib.swila_decode_step.restype = ctypes.c_int
     lib.swila_decode_step.argtypes = [sp, op] + [vp] * 6 + [vp, vp, vp, vp]
     tp = ctypes.POINTER(Temporal)
@@ -308,6 +311,43 @@ def forward(q, k, v, beta_logit, prior_k_logit, prior_q_logit, state_in=None, *,
         *[_ptr(t) for t in ins], _ptr(state_in), _ptr(s_out), _ptr(o), _ptr(r),
         ws_ptr, ws_bytes, _ptr(iters_out), _stream_handle(stream)))
     return (o, s_out, r) if resp else (o, s_out)
+
+
+NOALLOC_SCRATCH_BYTES = 64 << 20
+
+
+def forward_noalloc(q, k, v, beta_logit, prior_k_logit, prior_q_logit, state_in, o, *,
+                    state_out=None, resp=None, algo="auto", chunk=0, max_iters=0, tol=0.0,
+                    clamp=True, iters_out=None, sync_status=False, unnormalized=False,
+                    stream=None):
+    """swila_forward_noalloc: ``forward`` for callers that cannot allocate.  The
+    caller passes every output (o [B,T,H,Dv]; state_out and resp tensors or
+    None; iters_out as for ``forward``); nothing is allocated here or in the
+    library, whose App. D form uses a scratch array of NOALLOC_SCRATCH_BYTES
+    per GPU (larger calls raise with code EUNSUPPORTED).  Calls that overlap on
+    one GPU share that array and race.  Returns (o, state_out)."""
+    torch = _torch()
+    ins, code, (B, H, T, Dk, Dv, J) = _check_layer(
+        (q, k, v, beta_logit, prior_k_logit, prior_q_logit), False, o=o, state_in=state_in,
+        state_out=state_out)
+    _expect_shape(resp, (B, T, H, J, Dv), "resp")
+    _dev_tensor(state_in, "state_in", torch.float32)
+    _dev_tensor(o, "o")
+    _dev_tensor(state_out, "state_out", torch.float32)
+    _dev_tensor(resp, "resp", torch.float32)
+    if iters_out is not None:
+        _dev_tensor(iters_out, "iters_out", torch.int32)
+        if iters_out.numel() < 2:
+            raise ValueError("iters_out needs 2 int32 elements")
+    flags = ((0 if clamp else FLAG_NEWTON_NO_CLAMP) | (FLAG_NEWTON_SYNC if sync_status else 0)
+             | (FLAG_UNNORMALIZED if unnormalized else 0))
+    opts = Opts(code, _dtype_code(o), _ALGOS[algo], int(chunk), int(max_iters), float(tol),
+                flags)
+    _check(load_library().swila_forward_noalloc(
+        ctypes.byref(Shape(B, H, T, Dk, Dv, J)), ctypes.byref(opts), *[_ptr(t) for t in ins],
+        _ptr(state_in), _ptr(state_out), _ptr(o), _ptr(resp), _ptr(iters_out),
+        _stream_handle(stream)))
+    return o, state_out
 
 
 def backward_workspace_bytes(B, H, T, Dk, Dv, J) -> int:

@@ -5,8 +5,16 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <mutex>
+
 #include "launch.hpp"
 #include "swila.h"
+
+// Device scratch of swila_forward_noalloc: each GPU the library runs on holds
+// its own copy until the process ends.  In host code this name is a stand-in,
+// not a device address; host code uses the address hipGetSymbolAddress returns
+// for the current device (scratch_address below).
+static __device__ __align__(256) unsigned char scratch[SWILA_NOALLOC_SCRATCH_BYTES];
 
 namespace {
 
@@ -258,6 +266,30 @@ int check_gated(const swila_shape *shape, const swila_opts *opts, const swila_ga
     return SWILA_OK;
 }
 
+// Address of this device's copy of the scratch array, looked up once per device
+// with that device current.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_at[kMaxDevices];
+
+int scratch_address(void **out) {
+    int dev = 0;
+    int rc = map_hip(hipGetDevice(&dev), "hipGetDevice");
+    if (rc) return rc;
+    if (dev < 0 || dev >= kMaxDevices)
+        return fail(SWILA_EUNSUPPORTED, "device %d: at most %d devices", dev, kMaxDevices);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_at[dev]) {
+        void *p = nullptr;
+        rc = map_hip(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)), "scratch symbol address");
+        if (rc) return rc;
+        if (!p) return fail(SWILA_EHIP, "scratch symbol address is NULL");
+        g_scratch_at[dev] = p;
+    }
+    *out = g_scratch_at[dev];
+    return SWILA_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -357,6 +389,30 @@ int swila_forward(const swila_shape *shape, const swila_opts *opts, const void *
     }
     if (use_chunk(shape, opts)) return map_hip(swila::launch_scan_pipe(a, st), "chunk scan launch");
     return map_hip(swila::launch_scan_direct(a, st), "scan launch");
+}
+
+int swila_forward_noalloc(const swila_shape *shape, const swila_opts *opts, const void *q,
+                          const void *k, const void *v, const void *beta_logit,
+                          const void *prior_k_logit, const void *prior_q_logit,
+                          const float *state_in, float *state_out, void *o, float *resp_out,
+                          int32_t *iters_out, void *stream) {
+    clear_error();
+    if (!shape) return fail(SWILA_EINVAL, "shape is NULL");
+    if (!opts) return fail(SWILA_EINVAL, "opts is NULL");
+    const size_t need = swila_forward_workspace_bytes(shape, opts);
+    if (need > SWILA_NOALLOC_SCRATCH_BYTES)
+        return fail(SWILA_EUNSUPPORTED,
+                    "swila_forward_noalloc: this call needs %zu bytes of scratch, the library "
+                    "holds %zu (B*H*J*Dv*16*ceil(T/16)*4 <= %zu)", need,
+                    (size_t)SWILA_NOALLOC_SCRATCH_BYTES, (size_t)SWILA_NOALLOC_SCRATCH_BYTES);
+    void *ws = nullptr;
+    if (need > 0) {
+        int rc = scratch_address(&ws);
+        if (rc) return rc;
+    }
+    return swila_forward(shape, opts, q, k, v, beta_logit, prior_k_logit, prior_q_logit,
+                         state_in, state_out, o, resp_out, ws,
+                         need > 0 ? (size_t)SWILA_NOALLOC_SCRATCH_BYTES : 0, iters_out, stream);
 }
 
 int swila_forward_temporal(const swila_shape *shape, const swila_opts *opts, const void *q,
