@@ -649,8 +649,12 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
           for (int i_ = 0; i_ < ceil_div(kC * N / 4, NBT); ++i_) {
             const int g4 = brot(0) + i_ * NBT;
             if (g4 >= kC * N / 4) break;
-            // four consecutive columns (dims dl .. dl+3 of one component) of token t
-            const int e4 = 4 * g4, t = e4 / N, cc = e4 % N;
+            // four consecutive columns (dims dl .. dl+3 of one component) of token
+            // t.  Item g4 = 16 a + i takes token i and column group (a + i) mod
+            // N/4: the 16 lanes of a group then read 16 distinct bank pairs of
+            // the logit rows and store to 16 distinct bank pairs of sq (a plain
+            // row-major deal put them on two).
+            const int t = g4 % kC, cc = 4 * ((g4 / kC + t) % (N / 4)), e4 = t * N + cc;
             const bool ok = m * kC + t < T;
             float lbv[4], lkv[4];
             bf16_row<4>(sm.lb[rs], e4, lbv);
