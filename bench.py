@@ -604,6 +604,11 @@ def main():
         out["gated"] = bench_gated(sw, torch, workloads, dev, cfg, 1000 + args.config,
                                    args.steps, args.warmup, o, s_out, tdt)
     print("temporal and gated done", file=sys.stderr, flush=True)
+    if args.config in (2, 5) and not args.no_newton:
+        out["newton" if args.config == 2 else "newton_c5"] = bench_newton(
+            sw, torch, dev, cfg, args.steps, args.warmup, o, s_out, args.newton_tol)
+    if args.config == 2 and not args.no_backward:
+        out["backward"] = bench_backward(sw, torch, dev, cfg, args.steps, args.warmup)
     del dev, o, s_out
     if not args.no_other_configs:
         for c in (1, 2, 5):

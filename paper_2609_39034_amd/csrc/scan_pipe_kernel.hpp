@@ -169,6 +169,7 @@ struct PSmem {
     float r[NT ? 1 : 2][kC][C::NP];  // responsibilities (exact mode)
     float py[2][kC][C::NP];    // pi^q * retrieval
     int flag;                  // Newton: this sweep met the tolerance
+    int near;                  // Newton: its change was within 4 tol (the next may be the last)
 };
 
 // Four consecutive bf16 (as raw bits) of row t from element i (i % 4 == 0)
@@ -481,6 +482,17 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
     const bool gwave = NH == 0 ? w == 1 % NW : w == NW + 1;
     // Newton mode: this block's predictions, [NCH * kC][N] fp32
     float *const pred = NT ? na.pred + ((size_t)hh * (Dv / DB) + db) * NCH * kC * N : nullptr;
+    // Newton mode: only the last sweep's outputs are kept, so a sweep forms the
+    // query side (Q S, the retrieval product, pi^q, the output stores) only when
+    // it can be the last: the max_iters-th sweep, or one that follows a sweep
+    // whose change was within 4 tol.  A sweep that meets tol without it is
+    // followed by one more that has it.  Every role reads the sequential wave's
+    // verdict after the sweep's last barrier and takes the same decision.
+    auto next_sweep = [&](int sweeps, bool &qs, bool &done) {
+        const bool met = sm.flag != 0, near = sm.near != 0;
+        done = (met && qs) || sweeps >= na.max_iters;
+        qs = near || met || sweeps + 1 >= na.max_iters;
+    };
 
     // ---- matrix-core wave state: W^T tile rows 16 it + 4 lg + r, column col
     const int col = 16 * (seq ? 0 : w) + tl;
@@ -876,7 +888,7 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
     };
     // W += K_m^T C_m and Y += tril(A_m) C_m (C_m split in chi/clo); then
     // stage pi^q * Y of chunk m
-    auto finish_chunk = [&](int m) {
+    auto finish_chunk = [&](int m, bool qs) {
         const int rs = m % kRingKQ, pr = m & 1;
 #pragma unroll
         for (int it = 0; it < IT; ++it) {
@@ -885,6 +897,7 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
             W[it] = mfma16(ak, chi, W[it]);
             W[it] = mfma16(ak, clo, W[it]);
         }
+        if (!qs) return;   // (Newton: a sweep without the query side)
         // (K_m Q_m^T)[s][t] in accumulator layout is lane (t = tl, s = 4 lg + r):
         // exactly the A operand of tril(A_m) C_m, A_m = Q_m K_m^T
         const floatx4 at = gram(sm.k[rs], sm.q[rs]);
@@ -943,7 +956,7 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
     // sequential wave's registers and the matrix-core waves' do not add up.
     if (seq) {
         int sweeps = 0;
-        bool done = false;
+        bool done = false, qs = na.max_iters <= 1;
         while (!done) {
             ++sweeps;
             float dmax = 0.f, pmax = 0.f;   // Newton: largest change, largest prediction
@@ -1202,11 +1215,13 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
                     dmax = fmaxf(dmax, __shfl_xor(dmax, off));
                     pmax = fmaxf(pmax, __shfl_xor(pmax, off));
                 }
-                if (lane == 0)
+                if (lane == 0) {
                     sm.flag = (na.tol >= 0.f && dmax <= na.tol * fmaxf(1.f, pmax)) ? 1 : 0;
+                    sm.near = (na.tol >= 0.f && dmax <= 4.f * na.tol * fmaxf(1.f, pmax)) ? 1 : 0;
+                }
                 wait_vm();          // this sweep's predictions are in memory
                 block_sync_lds();
-                done = sm.flag != 0 || sweeps >= na.max_iters;   // as the matrix-core waves decide
+                next_sweep(sweeps, qs, done);   // as the matrix-core waves decide
             } else {
                 done = true;
             }
@@ -1249,14 +1264,18 @@ hipError_t launch_cfg(const LayerArgs &a, const NewtonArgs &na, hipStream_t stre
     // waves hide each other's latencies, so the tile waves keep the
     // bookkeeping.  Otherwise helper waves take it over.
     // (the temporal form has more per-chunk bookkeeping: always three helpers)
-    constexpr int NH = MD == 1 ? 0 : MD == 2 ? 3 : (C::NW < 3 ? C::NW : 3);
-    if (NH == 0 || (blocks >= 512 && lds <= 80 * 1024)) {
-        hipLaunchKernelGGL((scan_pipe_kernel<DK, J, DB, MD, 0>), dim3((unsigned)blocks),
-                           dim3(64 * (C::NW + 1)), 0, stream, a, na);
-    } else {
-        hipLaunchKernelGGL((scan_pipe_kernel<DK, J, DB, MD, NH>), dim3((unsigned)blocks),
-                           dim3(64 * (C::NW + 1 + NH)), 0, stream, a, na);
+    // (a block over 80 KB of LDS is never two to a compute unit: only the
+    // variant with helpers is built for it)
+    constexpr int NH = MD == 2 ? 3 : (C::NW < 3 ? C::NW : 3);
+    if constexpr (lds <= 80 * 1024) {
+        if (blocks >= 512) {
+            hipLaunchKernelGGL((scan_pipe_kernel<DK, J, DB, MD, 0>), dim3((unsigned)blocks),
+                               dim3(64 * (C::NW + 1)), 0, stream, a, na);
+            return hipGetLastError();
+        }
     }
+    hipLaunchKernelGGL((scan_pipe_kernel<DK, J, DB, MD, NH>), dim3((unsigned)blocks),
+                       dim3(64 * (C::NW + 1 + NH)), 0, stream, a, na);
     return hipGetLastError();
 }
 
