@@ -39,7 +39,8 @@
  *     failure (thread-local text, valid until this thread's next call).
  *   - Supported shapes: Dk in {16, 32, 64, 128}, Dv in {16, 32, 64, 128},
  *     J in {1, 2, 3, 4, 8, 16} (every J of the paper's Sec. 5.1 sweep, and 3),
- *     B, H >= 1, T >= 0.  Others give SWILA_EUNSUPPORTED.  Narrower limits:
+ *     1 <= B, H <= 65535 with B * H <= 2^26, T >= 0.  Others give
+ *     SWILA_EUNSUPPORTED.  Narrower limits:
  *     the chunked forms (SWILA_ALGO_CHUNK_EXACT, SWILA_ALGO_NEWTON) and the
  *     backward pass take J <= 8 (SWILA_ALGO_AUTO then picks the token-by-token
  *     scan), and the gated forward takes J * Dk <= 1024.

@@ -31,6 +31,7 @@ int fail(int code, const char *fmt, ...) {
 void clear_error() { g_err[0] = 0; }
 
 bool dim_ok(int x) { return x == 16 || x == 32 || x == 64 || x == 128; }
+constexpr int64_t kMaxHeads = int64_t(1) << 26;
 // every J the paper uses (its Sec. 5.1 sweep: powers of two up to 16), and 3
 bool j_ok(int j) { return j == 1 || j == 2 || j == 3 || j == 4 || j == 8 || j == 16; }
 
@@ -47,6 +48,11 @@ int check_shape(const swila_shape *s, bool decode) {
         return fail(SWILA_EUNSUPPORTED, "J=%d: supported are 1, 2, 3, 4, 8, 16", s->J);
     if (s->B > 65535 || s->H > 65535)
         return fail(SWILA_EUNSUPPORTED, "B=%d H=%d: at most 65535 each", s->B, s->H);
+    // the matrix-core kernels launch (Dv / 8) * B * H blocks or fewer on a 1-D
+    // grid and index heads with 32-bit integers
+    if ((int64_t)s->B * s->H > kMaxHeads)
+        return fail(SWILA_EUNSUPPORTED, "B*H=%lld: at most %lld heads per call",
+                    (long long)s->B * s->H, (long long)kMaxHeads);
     return SWILA_OK;
 }
 

@@ -64,6 +64,7 @@ OPTS = sw.Opts(sw.BF16, sw.BF16, 0, 0, 0, 0.0, 0)
     (sw.Shape(1, 1, 4, 64, 256, 4), OPTS, sw.EUNSUPPORTED, "Dv=256"),
     (sw.Shape(1, 1, 4, 64, 64, 5), OPTS, sw.EUNSUPPORTED, "J=5"),
     (sw.Shape(70000, 1, 4, 64, 64, 4), OPTS, sw.EUNSUPPORTED, "at most 65535"),
+    (sw.Shape(65535, 1025, 4, 64, 64, 4), OPTS, sw.EUNSUPPORTED, "heads per call"),
     (sw.Shape(1, 1, 4, 64, 64, 4), sw.Opts(7, 1, 0, 0, 0, 0.0, 0), sw.EINVAL, "in_dtype"),
     (sw.Shape(1, 1, 4, 64, 64, 4), sw.Opts(1, 9, 0, 0, 0, 0.0, 0), sw.EINVAL, "out_dtype"),
     (sw.Shape(1, 1, 4, 64, 64, 4), sw.Opts(1, 1, 99, 0, 0, 0.0, 0), sw.EUNSUPPORTED, "algo"),

@@ -155,3 +155,17 @@ def test_gated_config2_every_head():
     er = head_rel_err(r, ref["resp"], "resp")
     print("worst head: o %.3e state %.3e resp %.3e" % (eo, es, er))
     assert eo <= 2e-2 and es <= 2e-2 and er <= 2e-2
+
+
+def test_gated_empty_sequence_copies_states():
+    """T = 0 through the gated forward: the states are copied, nothing else."""
+    import torch
+    import paper_2609_39034_amd as sw
+    B, H, D, J = 2, 3, 32, 4
+    q = torch.empty((B, 0, H, D), device="cuda")
+    lb = torch.empty((B, 0, H, J, D), device="cuda")
+    dec = torch.empty((B, 0, H, J, D), device="cuda")
+    s0 = torch.randn((B, H, J, D, D), device="cuda")
+    o, s = sw.forward_gated(q, q, q, lb, lb, lb, dec, s0)
+    torch.cuda.synchronize()
+    assert o.numel() == 0 and torch.equal(s, s0)

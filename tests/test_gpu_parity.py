@@ -171,6 +171,32 @@ def test_state_init_then_forward():
     assert eo <= 2e-2 and es <= 2e-2
 
 
+@pytest.mark.parametrize("B,H", [(65535, 1), (1, 65535)])
+@pytest.mark.parametrize("dtype,algo", [("f32", "recurrent"), ("bf16", "chunk")])
+def test_largest_batch_and_heads(B, H, dtype, algo):
+    """The largest B and H the boundary accepts (65535 each): every head of the
+    grid is computed (T = 3 spans a ragged chunk), then one decode step."""
+    import torch
+    import paper_2609_39034_amd as sw
+    inp = workloads.iid_inputs(B, H, 3, 16, 16, 2, dtype=dtype, seed=830, state_std=0.2)
+    _check(inp, dtype, algo=algo)
+    dev = to_device(inp, dtype)
+    st = dev["state"].clone()
+    o, _ = sw.decode_step(*(dev[n][:, 0].contiguous() for n in NAMES), st, state_out=st)
+    torch.cuda.synchronize()
+    ref = _oracle({n: inp[n][:, :1] for n in NAMES} | {"state": inp["state"]})
+    eo = head_rel_err(o.float().cpu().numpy()[:, None], ref["o"], "o")
+    es = head_rel_err(st.cpu().numpy(), ref["state"], "state")
+    assert eo <= tol_for(dtype) and es <= tol_for(dtype)
+
+
+def test_lm_shape_ragged_sequence():
+    """The LM-shaped head (Dk = Dv = 128, J = 4) over T = 4095: a ragged last
+    chunk at full length, with an initial state, on the chunk scan."""
+    inp = workloads.iid_inputs(2, 4, 4095, 128, 128, 4, dtype="bf16", seed=831, state_std=0.05)
+    _check(inp, "bf16", algo="chunk")
+
+
 def test_config1_tiny():
     _check(workloads.config_inputs(1), "f32")
 
