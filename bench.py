@@ -41,18 +41,20 @@ PEAK_MFMA_BF16 = 2.5e15    # FLOP/s, MI355X dense bf16 matrix
 # what the counter reads for a plain copy of known size), keyed by the kernel's
 # source, the workload it ran and the digest of the source at measurement.
 MEASURED_TRAFFIC = {
-    ("decode.hip", "decode B=256 H=16 Dk=Dv=128 J=4",
-     "61389eba263b4383d29d2a95a508eda272785d4528f176469643084a48b144d7"): 2165221728,
-    ("scan_pipe.hip", "forward B=4 H=8 T=2048 Dk=Dv=64 J=4",
-     "10f01378f0054265aedcd58348c2f33bc35c7a6f65720e39895a612a01dc8ec2"): 136679434,
     ("scan_pipe.hip", "forward B=8 H=16 T=4096 Dk=Dv=128 J=4",
-     "10f01378f0054265aedcd58348c2f33bc35c7a6f65720e39895a612a01dc8ec2"): 2185160535,
-    ("scan_pipe_temporal.hip", "temporal B=4 H=8 T=2048 Dk=Dv=64 J=4",
-     "9887c803ed2530004fba32cefc6dacd68ede72a204b510c26d7d8bbbb47b0848"): 153641701,
-    ("scan_direct.hip", "forward B=4 H=8 T=2048 Dk=Dv=64 J=4",
-     "9c05f9370e10e3ef0f32f4340d26da5eaba747b2493f558c7db50d1e290eac3e"): 136456434,
-    ("scan_direct.hip", "gated B=4 H=8 T=2048 Dk=Dv=64 J=4",
-     "9c05f9370e10e3ef0f32f4340d26da5eaba747b2493f558c7db50d1e290eac3e"): 170042026,
+     "0411c48d19a00b1068fdc899c3b9b2ce423de766c4002d1ad8a0be4831095816"): 2187420876,
+    ("scan_pipe.hip", "forward B=4 H=8 T=2048 Dk=Dv=64 J=4",
+     "0411c48d19a00b1068fdc899c3b9b2ce423de766c4002d1ad8a0be4831095816"): 136691844,
+    ("scan_pipe.hip", "forward B=2 H=8 T=16384 Dk=Dv=128 J=8",
+     "0411c48d19a00b1068fdc899c3b9b2ce423de766c4002d1ad8a0be4831095816"): 2354048188,
+    ("scan_pipe_temporal.hip", "temporal B=8 H=16 T=4096 Dk=Dv=128 J=4",
+     "552bf36e40f3d9d5960c872b5f0f758278e26b89c6a3236891f32c1d39bfd6b1"): 2450490466,
+    ("scan_direct_dk128.hip", "gated B=8 H=16 T=4096 Dk=Dv=128 J=4",
+     "b427757a58067e7408bd320e9708cb725b13ca36c35cdc60190f7ba3a750d634"): 2718133297,
+    ("scan_direct_dk16.hip", "forward B=1 H=1 T=64 Dk=Dv=16 J=2",
+     "b1e50e81270777e46233ef0e983e3dfc6e99576676c141d880e2b428bc014b9c"): 67711,
+    ("decode.hip", "decode B=256 H=16 Dk=Dv=128 J=4",
+     "9780a8085553bafe2ac41143998e6a3b95f3a2e33aa73ea5db1f5adc0e87c8a6"): 2165846719,
 }
 
 

@@ -496,14 +496,19 @@ hipError_t launch_dk_j_tp(const LayerArgs &a, hipStream_t stream) {
         // shrinks with its rows per lane, and a grid of fewer blocks than
         // compute units leaves the rest idle: halve S (down to 4 rows, and to
         // at most 16 lanes per column, which keeps every block at 16 columns or
-        // more) while the grid is under 256 blocks.  At B=4 H=8 Dk=Dv=64 J=4
-        // that is S = 4: 128 blocks of 16 columns instead of 32 of 64.  The
+        // more) while the grid is under 256 blocks.  The gated form rescales
+        // every state row of a lane each token, so its rows cost more than the
+        // wider reductions that fewer rows bring: it halves S while the grid is
+        // under 1024 blocks (four per compute unit).  At B=4 H=8 Dk=Dv=64 J=4
+        // that is S = 4: 128 blocks of 16 columns instead of 32 of 64; gated at
+        // B=8 H=16 Dk=Dv=128 J=4, S = 8: 1024 blocks instead of 512.  The
         // backward's checkpoints store key index l * S + s at its own position,
         // so their layout does not depend on S.
+        constexpr size_t kFill = GT ? 1024 : 256;
         constexpr int S2 = S / 2 >= 4 && DK / (S / 2) <= 16 ? S / 2 : S;
         constexpr int S4 = S2 / 2 >= 4 && DK / (S2 / 2) <= 16 ? S2 / 2 : S2;
-        if (grid_blocks<DK, J, S, TP>(a) < 256) {
-            if (S4 != S2 && grid_blocks<DK, J, S2, TP>(a) < 256)
+        if (grid_blocks<DK, J, S, TP>(a) < kFill) {
+            if (S4 != S2 && grid_blocks<DK, J, S2, TP>(a) < kFill)
                 return launch_s<DK, J, S4, TP, GT, AX>(a, stream);
             if constexpr (S2 != S) return launch_s<DK, J, S2, TP, GT, AX>(a, stream);
         }
