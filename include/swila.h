@@ -313,12 +313,13 @@ int swila_decode_step_gated(const swila_shape *shape, const swila_opts *opts,
  *              (all six required when T > 0, overwritten).
  *   grad_state_in: dL/dW_0 [B,H,J,Dk,Dv] fp32, or NULL to discard it.
  *   workspace, ws_bytes: at least swila_backward_workspace_bytes bytes,
- *              16-byte aligned; holds the recomputed errors delta and the state
- *              every 32 tokens, and is overwritten.
+ *              16-byte aligned; holds the recomputed errors delta, the state
+ *              every 32 tokens and the per-token operands the reverse scan
+ *              hands to the final pass, and is overwritten.
  * Every output, the workspace and the inputs are pairwise disjoint.  The
  * algorithm field of opts is ignored: the backward recomputes the forward
- * with the token-by-token scan.  T == 0 copies grad_state_out (or zeros) to
- * grad_state_in.
+ * with the matrix-core chunk scan for bf16 inputs and the token-by-token scan
+ * for fp32 inputs.  T == 0 copies grad_state_out (or zeros) to grad_state_in.
  */
 int swila_backward(const swila_shape *shape, const swila_opts *opts,
                    const void *q, const void *k, const void *v,
@@ -330,8 +331,9 @@ int swila_backward(const swila_shape *shape, const swila_opts *opts,
                    float *grad_prior_q_logit, float *grad_state_in,
                    void *workspace, size_t ws_bytes, void *stream);
 
-/* Workspace bytes swila_backward needs (0 if shape is NULL or invalid):
- * 2*B*T*H*J*Dv*4 + 2*B*H*ceil(T/32)*J*Dk*Dv*4, each part rounded up to 256. */
+/* Workspace bytes swila_backward needs (0 if shape is NULL or invalid), with
+ * N = ceil(T/32) and each part rounded up to a multiple of 256:
+ * B*T*H*J*Dv*4 + 3*(B*H*N*32*J*Dv*4) + B*H*N*32*Dv*4 + 2*(B*H*N*J*Dk*Dv*4). */
 size_t swila_backward_workspace_bytes(const swila_shape *shape);
 
 /* Text of this thread's last error ("" if none). */

@@ -55,7 +55,12 @@ struct BackwardArgs {
     float *dq, *dk, *dv;         // [B,T,H,Dk], [B,T,H,Dk], [B,T,H,Dv]
     float *dlb, *dlk, *dlq;      // [B,T,H,J,Dv]
     float *dstate;               // [B,H,J,Dk,Dv]; nullptr = not written
-    float *delta, *dpred;        // workspace, [B,T,H,J,Dv] each
+    float *delta;                // workspace, [B,T,H,J,Dv]: the recomputed errors
+    // workspace: the chunk pass's per-(token, column) operands, written by the
+    // reverse scan in the pass's tile order, [B,H,NCH,Dv/DT,kBwdChunk,DT,J] with
+    // DT output dims per tile: c = beta r delta, dpred and pi^q; and dL/do as
+    // [B,H,NCH,Dv/DT,kBwdChunk,DT] fp32
+    float *cpk, *ppk, *qpk, *dopk;
     float *wck, *eck;            // workspace, [B,H,NCH,Dv,J,Dk] each
 };
 

@@ -18,8 +18,10 @@
 //      ddelta_j = dc_j beta_j r_j - delta_j da_j;  dv = sum_j ddelta_j
 //      dpred_j = -ddelta_j;  G_j += dpred_j k_t          (now dL/dw_{t-1,jd})
 //    evaluated a chunk at a time (reverse_chunk_kernel below).  It writes dv,
-//    dlb, dlk, dpred, dL/dW_0 (G after token 0), and E_n, the part of dL/dw at
-//    the last token of checkpoint interval n that comes from later tokens.
+//    dlb, dlk, dL/dW_0 (G after token 0), and E_n, the part of dL/dw at the
+//    last token of checkpoint interval n that comes from later tokens; and, for
+//    the chunk pass, c = beta r delta, dpred, pi^q and dL/do in that pass's tile
+//    order, so that each of its tiles reads one contiguous run per operand.
 //
 // 3. Chunk pass, one block per (b, h, chunk of kBwdChunk tokens), no
 //    sequential dependence.  Inside chunk n, with S = W_n, columns col = (j, d)
@@ -52,6 +54,11 @@ constexpr int kCB = kBwdChunk;    // tokens per chunk of the chunk pass
 // with it for the next chunk's prefetch.  Their staging loads raw bits
 // (raw1, raw4) and converts later.
 
+// Output dims per column tile of the chunk pass: tiles of all J components of
+// DT dims, 16 to 32 columns.
+template <int J>
+constexpr int chunk_tile_dims() { return J == 1 ? 16 : J == 3 ? 8 : 32 / J; }
+
 // Chunked reverse scan.  The recurrence of the reverse sweep has the shape of
 // the forward's chunk form run backwards: inside a chunk of kRC tokens, with E
 // the gradient w.r.t. the state after the chunk's last token from the tokens
@@ -73,6 +80,8 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
     constexpr int KP = DK + 4;           // row pitches keep 16-byte rows
     constexpr int CP = N + 4, GP = kRC + 4;
     static_assert(NL <= 64 && kBwdChunk % kRC == 0 && N % 4 == 0, "one sequential wave");
+    static_assert(DB % chunk_tile_dims<J>() == 0 || chunk_tile_dims<J>() % DB == 0,
+                  "a block covers whole tiles of the chunk pass, or a part of one");
 
     __shared__ __align__(16) float sE[DK][CP];
     __shared__ __align__(16) float sK[kRC][KP], sQ[kRC][KP];    // rows t
@@ -82,6 +91,7 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
     __shared__ __align__(16) float sBase[kRC][CP], sY[kRC][CP], sP[kRC][CP];
     __shared__ float sDelta[kRC][CP], sBeta[kRC][CP], sR[kRC][CP];
     __shared__ float sDlb[kRC][CP], sDlk[kRC][CP], sDv[kRC][DB];
+    __shared__ float sPq[kRC][CP], sDo[kRC][DB];                // pi^q, dL/do
 
     const LayerArgs &f = a.f;
     const int tid = threadIdx.x, lane = tid % 64;
@@ -160,6 +170,27 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
             }
         }
     };
+    // The chunk pass's operands, in its tile order [b, h, interval, tile, token,
+    // dd, j]: the rows of one tile and consecutive tokens are contiguous, so each
+    // store run covers whole lines.  This block's dims cover TW dims of each tile
+    // it touches (all of them, or a part when the block is narrower than a
+    // tile).  Threads first .. first + nthr - 1 store X[t][col] for the chunk's
+    // tokens (trip counts and divisors compile-time; tokens past the end skipped).
+    constexpr int CT = chunk_tile_dims<J>();
+    constexpr int TW = DB < CT ? DB : CT;
+    auto pack_index = [&](int t0, int t, int d) {
+        const size_t pbase = ((size_t)b * H + h) * NC2 + t0 / kBwdChunk;
+        return ((pbase * (Dv / CT) + d / CT) * kBwdChunk + t0 % kBwdChunk + t) * CT + d % CT;
+    };
+    auto pack_store = [&](float *dst, const float (*X)[CP], int t0, int nt, int first, int nthr) {
+        constexpr int NE = kRC * J * DB;
+        for (int e = tid - first; e < NE; e += nthr) {
+            const int j = e % J, w = (e / J) % TW, t = (e / (J * TW)) % kRC,
+                      kk = e / (J * TW * kRC);
+            const int dd = kk * TW + w;
+            if (t < nt) dst[pack_index(t0, t, d0 + dd) * J + j] = X[t][j * DB + dd];
+        }
+    };
     fetch(NCH - 1);
 
     for (int n = NCH - 1; n >= 0; --n) {
@@ -227,7 +258,9 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
                 sR[t][col] = ee[j];
                 sBeta[t][col] = be[j];
                 sY[t][col] = dov * lq[j];
+                sPq[t][col] = lq[j];
             }
+            sDo[t][dd] = dov;
         }
         block_sync_lds();
         if (n > 0) fetch(n - 1);   // lands while this chunk computes
@@ -273,9 +306,23 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
             for (int x = 0; x < 4; ++x) sBase[t4 + x][col] = acc[x];
         }
         block_sync_lds();
+        if (tid >= 64) {
+            // while the sequential wave runs (it stores c = beta r delta and dpred
+            // for the chunk pass), the other waves store pi^q and dL/do
+            pack_store(a.qpk, sPq, t0, nt, 64, kThreads - 64);
+            for (int e = tid - 64; e < kRC * DB; e += kThreads - 64) {
+                const int w = e % TW, t = (e / TW) % kRC, kk = e / (TW * kRC);
+                if (t < nt) a.dopk[pack_index(t0, t, d0 + kk * TW + w)] = sDo[t][kk * TW + w];
+            }
+        }
         if (tid < 64) {
             // the chunk's tokens in reverse; dfr[u] collects sum_{s>u} (k_u . k_s) dpred_s
             float dfr[kRC], vb[kRC], vd[kRC], vbe[kRC], vr[kRC];
+            // this lane's column in the chunk pass's tile order: token t of the
+            // chunk at t * CT * J floats on (tokens past the end land in the
+            // padding of the last interval, inside the buffer)
+            const size_t pl = pack_index(t0, 0, d0 + sdd) * J + sj;
+            float *const cl = a.cpk + pl, *const plp = a.ppk + pl;
 #pragma unroll
             for (int u = 0; u < kRC; ++u) {
                 dfr[u] = 0.0f;
@@ -308,6 +355,8 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
                     sDlb[t][scol] = dc * r * dl * be * (1.0f - be);
                     sDlk[t][scol] = da;
                     if (sj == 0) sDv[t][sdd] = dvv;
+                    cl[t * CT * J] = be * r * dl;
+                    plp[t * CT * J] = dpred;
                 }
             }
         }
@@ -341,7 +390,6 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
             const size_t idx = (((size_t)(b * T + t0 + t) * H + h) * J + j) * Dv + d0 + dd;
             a.dlb[idx] = sDlb[t][col];
             a.dlk[idx] = sDlk[t][col];
-            a.dpred[idx] = sP[t][col];
         }
         for (int e = tid; e < nt * DB; e += kThreads) {
             const int t = e / DB, dd = e % DB;
@@ -357,11 +405,6 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
     }
 }
 
-// Output dims per column tile of the chunk pass: tiles of all J components of
-// DT dims, 16 to 32 columns.
-template <int J>
-constexpr int chunk_tile_dims() { return J == 1 ? 16 : J == 3 ? 8 : 32 / J; }
-
 template <int N>
 __device__ __forceinline__ void lds_vec(const float *p, float (&v)[N]) {
     if constexpr (N == 4) {
@@ -370,6 +413,24 @@ __device__ __forceinline__ void lds_vec(const float *p, float (&v)[N]) {
     } else {
         const float2 x = *reinterpret_cast<const float2 *>(p);
         v[0] = x.x; v[1] = x.y;
+    }
+}
+
+// J consecutive floats from global memory (16-byte loads where J allows).
+template <int J>
+__device__ __forceinline__ void lds_row(const float *p, float (&v)[J]) {
+    if constexpr (J % 4 == 0) {
+#pragma unroll
+        for (int x = 0; x < J; x += 4) {
+            const float4 w = *reinterpret_cast<const float4 *>(p + x);
+            v[x] = w.x; v[x + 1] = w.y; v[x + 2] = w.z; v[x + 3] = w.w;
+        }
+    } else if constexpr (J == 2) {
+        const float2 w = *reinterpret_cast<const float2 *>(p);
+        v[0] = w.x; v[1] = w.y;
+    } else {
+#pragma unroll
+        for (int x = 0; x < J; ++x) v[x] = p[x];
     }
 }
 
@@ -425,7 +486,7 @@ __global__ __launch_bounds__(kThreads) void bwd_chunk_kernel(BackwardArgs a) {
     const int H = f.H, T = f.T, Dv = f.Dv;
     const int NCH = (T + kCB - 1) / kCB;
     const int t0 = n * kCB, nt = min(kCB, T - t0);
-    const bool ibf = f.in_bf16, obf = f.out_bf16;
+    const bool ibf = f.in_bf16;
     const int i0 = (tid % NIB) * TN, tA = (tid / NIB) * TM;   // this thread's outputs
     const int gt = tid / 8, gs = (tid % 8) * 4;               // its Gram entries
     const int gt8 = tid % 8;                                  // its retrieval columns
@@ -481,55 +542,25 @@ __global__ __launch_bounds__(kThreads) void bwd_chunk_kernel(BackwardArgs a) {
             *reinterpret_cast<float4 *>(&sE[j * DT + dd][i]) =
                 *reinterpret_cast<const float4 *>(a.eck + src);
         }
+        // this tile's per-(token, column) operands, contiguous in the reverse
+        // scan's tile order: [token][dd][j]
+        const size_t tb = ((((size_t)b * H + h) * NCH + n) * (Dv / DT) + dt0 / DT) * kCB;
         for (int g = tid; g < kCB * DT; g += kThreads) {
             const int t = g / DT, dd = g % DT;
-            float c[J], p[J], y[J], pq[J];
+            float c[J], p[J], y[J], pq[J], dov = 0.0f;
             if (t < nt) {
-                const size_t row = (size_t)(b * T + t0 + t) * H + h;
-                const uint32_t rdo = raw1(a.grad_o, row * Dv + dt0 + dd, obf);
-                float delta[J], e[J], lq[J], pp[J];
-                uint32_t rlk[J], rlq[J], rlb[J];
+                const size_t row = (tb + t) * DT + dd;
+                lds_row<J>(a.cpk + row * J, c);
+                lds_row<J>(a.ppk + row * J, p);
+                lds_row<J>(a.qpk + row * J, pq);
+                dov = a.dopk[row];
 #pragma unroll
-                for (int j = 0; j < J; ++j) {
-                    const size_t idx = (row * J + j) * Dv + dt0 + dd;
-                    delta[j] = a.delta[idx];
-                    pp[j] = a.dpred[idx];
-                    rlk[j] = raw1(f.lk, idx, ibf);
-                    rlq[j] = raw1(f.lq, idx, ibf);
-                    rlb[j] = raw1(f.lb, idx, ibf);
-                }
-                const float dov = cvt1(rdo, obf);
-                float m = -INFINITY, mq = -INFINITY;
-#pragma unroll
-                for (int j = 0; j < J; ++j) {
-                    e[j] = cvt1(rlk[j], ibf) - 0.5f * delta[j] * delta[j];
-                    lq[j] = cvt1(rlq[j], ibf);
-                    m = fmaxf(m, e[j]);
-                    mq = fmaxf(mq, lq[j]);
-                }
-                float z = 0.0f, zq = 0.0f;
-#pragma unroll
-                for (int j = 0; j < J; ++j) {
-                    e[j] = exp_fast(e[j] - m);
-                    z += e[j];
-                    lq[j] = exp_fast(lq[j] - mq);
-                    zq += lq[j];
-                }
-                const float iz = 1.0f / z, izq = 1.0f / zq;
-#pragma unroll
-                for (int j = 0; j < J; ++j) {
-                    const float beta = 1.0f / (1.0f + exp_fast(-cvt1(rlb[j], ibf)));
-                    c[j] = beta * (J == 1 ? 1.0f : e[j] * iz) * delta[j];
-                    p[j] = pp[j];
-                    pq[j] = J == 1 ? 1.0f : lq[j] * izq;
-                    y[j] = dov * pq[j];
-                }
-                sDo[t][dd] = dov;
+                for (int j = 0; j < J; ++j) y[j] = dov * pq[j];
             } else {
 #pragma unroll
                 for (int j = 0; j < J; ++j) c[j] = p[j] = y[j] = pq[j] = 0.0f;
-                sDo[t][dd] = 0.0f;
             }
+            sDo[t][dd] = dov;
 #pragma unroll
             for (int j = 0; j < J; ++j) {
                 const int cc = j * DT + dd;
@@ -720,15 +751,16 @@ hipError_t launch_bwd_dk(const BackwardArgs &a, hipStream_t stream) {
 size_t backward_workspace_bytes(int B, int H, int T, int Dk, int Dv, int J) {
     const size_t nch = ((size_t)T + kCB - 1) / kCB;
     const size_t per_tok = (size_t)B * T * H * J * Dv * sizeof(float);
+    const size_t pk = (size_t)B * H * nch * kCB * J * Dv * sizeof(float);
     const size_t ck = (size_t)B * H * nch * Dv * J * Dk * sizeof(float);
     auto up = [](size_t x) { return (x + 255) / 256 * 256; };
-    return 2 * up(per_tok) + 2 * up(ck);
+    return up(per_tok) + 3 * up(pk) + up(pk / J) + 2 * up(ck);
 }
 
 hipError_t launch_backward(const BackwardArgs &a, hipStream_t stream) {
     const LayerArgs &f = a.f;
     if (f.T < 1 || f.gk || f.decay || !a.grad_o || !a.dq || !a.dk || !a.dv || !a.dlb || !a.dlk ||
-        !a.dlq || !a.delta || !a.dpred || !a.wck || !a.eck)
+        !a.dlq || !a.delta || !a.cpk || !a.ppk || !a.qpk || !a.dopk || !a.wck || !a.eck)
         return hipErrorInvalidValue;
     if (f.Dv % 16 != 0) return hipErrorInvalidValue;   // every column tile divides Dv
     switch (f.Dk) {

@@ -622,11 +622,15 @@ int swila_backward(const swila_shape *shape, const swila_opts *opts, const void 
         return map_hip(swila::launch_state_fill(grad_state_in, grad_state_out, nst / 4, st),
                        "state copy");
     }
-    // workspace: delta, dpred ([B,T,H,J,Dv]); state checkpoints W_n, E_n
+    // workspace: delta ([B,T,H,J,Dv]); the chunk pass's operands c, dpred, pi^q
+    // and dL/do in its tile order (tokens padded to whole checkpoint intervals);
+    // state checkpoints W_n, E_n
     const size_t nch = (T + swila::kBwdChunk - 1) / swila::kBwdChunk;
     auto up = [](size_t x) { return (x + 255) / 256 * 256; };
     char *ws = static_cast<char *>(workspace);
     const size_t per_tok = up(B * T * H * J * Dv * 4), ck = up(B * H * nch * Dv * J * Dk * 4);
+    const size_t pk = up(B * H * nch * swila::kBwdChunk * J * Dv * 4),
+                 dpk = up(B * H * nch * swila::kBwdChunk * Dv * 4);
     swila::BackwardArgs ba;
     ba.f = swila::LayerArgs{q, k, v, beta_logit, prior_k_logit, prior_q_logit, state_in,
                             nullptr, nullptr, nullptr, shape->B, shape->H, shape->T,
@@ -642,9 +646,14 @@ int swila_backward(const swila_shape *shape, const swila_opts *opts, const void 
     ba.dlq = grad_prior_q_logit;
     ba.dstate = grad_state_in;
     ba.delta = reinterpret_cast<float *>(ws);
-    ba.dpred = reinterpret_cast<float *>(ws + per_tok);
-    ba.wck = reinterpret_cast<float *>(ws + 2 * per_tok);
-    ba.eck = reinterpret_cast<float *>(ws + 2 * per_tok + ck);
+    ws += per_tok;
+    ba.cpk = reinterpret_cast<float *>(ws);
+    ba.ppk = reinterpret_cast<float *>(ws + pk);
+    ba.qpk = reinterpret_cast<float *>(ws + 2 * pk);
+    ba.dopk = reinterpret_cast<float *>(ws + 3 * pk);
+    ws += 3 * pk + dpk;
+    ba.wck = reinterpret_cast<float *>(ws);
+    ba.eck = reinterpret_cast<float *>(ws + ck);
     return map_hip(swila::launch_backward(ba, st), "backward launch");
 }
 

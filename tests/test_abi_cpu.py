@@ -251,7 +251,9 @@ def test_backward_argument_checks(lib):
     shape = sw.Shape(B, H, T, D, D, J)
     need = lib.swila_backward_workspace_bytes(ctypes.byref(shape))
     per_tok, ck = B * T * H * J * D * 4, B * H * 2 * D * J * D * 4    # ceil(40 / 32) = 2
-    assert need == 2 * ((per_tok + 255) // 256 * 256) + 2 * ((ck + 255) // 256 * 256)
+    pk, dpk = B * H * 64 * J * D * 4, B * H * 64 * D * 4                 # 2 x 32 tokens
+    up = lambda x: (x + 255) // 256 * 256
+    assert need == up(per_tok) + 3 * up(pk) + up(dpk) + 2 * up(ck)
     assert lib.swila_backward_workspace_bytes(None) == 0
     ins = [ctypes.c_void_p((1 << 20) + (i << 26)) for i in range(6)]
     go = ctypes.c_void_p(1 << 33)

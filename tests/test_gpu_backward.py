@@ -76,6 +76,8 @@ CASES = [
     (1, 1, 1, 128, 128, 4, "f32", 0.2, True),      # one token
     (2, 2, 96, 32, 128, 8, "bf16", 0.1, True),
     (1, 2, 130, 64, 64, 4, "f32", 0.1, True),      # five chunks, two staging rounds each
+    (1, 2, 45, 32, 16, 1, "f32", 0.2, True),       # reverse blocks of 8 dims, half a tile
+    (2, 1, 70, 64, 16, 2, "bf16", 0.1, False),     # the same with two components
 ]
 
 
