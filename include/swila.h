@@ -43,7 +43,8 @@
  *     SWILA_EUNSUPPORTED.  Narrower limits:
  *     the chunked forms (SWILA_ALGO_CHUNK_EXACT, SWILA_ALGO_NEWTON) and the
  *     backward pass take J <= 8 (SWILA_ALGO_AUTO then picks the token-by-token
- *     scan), and the gated forward takes J * Dk <= 1024.
+ *     scan), and the gated forward takes J * Dk <= 1024 (its chunked form
+ *     J <= 4 and J * Dk <= 256; see swila_forward_gated).
  */
 #ifndef SWILA_H
 #define SWILA_H
@@ -278,9 +279,16 @@ typedef struct swila_gated {
 /*
  * swila_forward with the gated decay above; temporal may be NULL (plain
  * priors) or the temporal priors of swila_forward_temporal (Gated Temporal
- * SwiLA).  Runs on the token-by-token scan (SWILA_ALGO_AUTO or
- * SWILA_ALGO_RECURRENT, either input dtype); SWILA_ALGO_CHUNK_EXACT and
- * SWILA_ALGO_NEWTON return SWILA_EUNSUPPORTED.  T == 0 copies the states.
+ * SwiLA).  Algorithms:
+ *   SWILA_ALGO_CHUNK_EXACT: the same recurrence 16 tokens at a time on the
+ *     matrix cores (App. B.4 with the chunk algebra of the plain form; exact
+ *     up to rounding order).  It takes bf16 inputs, no temporal priors,
+ *     J <= 4 and J * Dk <= 256; other calls return SWILA_EUNSUPPORTED.
+ *   SWILA_ALGO_RECURRENT: the token-by-token scan (either input dtype, with
+ *     or without temporal priors, J * Dk <= 1024).
+ *   SWILA_ALGO_AUTO: CHUNK_EXACT where it applies, else RECURRENT.
+ *   SWILA_ALGO_NEWTON returns SWILA_EUNSUPPORTED.
+ * T == 0 copies the states.
  */
 int swila_forward_gated(const swila_shape *shape, const swila_opts *opts,
                         const void *q, const void *k, const void *v,

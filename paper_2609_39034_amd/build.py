@@ -18,8 +18,8 @@ LIB = os.path.join(PKG, "libswila.so")
 # the largest units first, so that the parallel compile ends soonest
 SOURCES = ["scan_direct_dk128.hip", "scan_direct_dk64.hip", "scan_pipe.hip",
            "scan_pipe_temporal.hip", "scan_direct_dk32.hip", "scan_direct_dk16.hip",
-           "scan_pipe_newton.hip", "decode.hip", "scan_backward.hip", "scan_direct.hip",
-           "swila_api.hip"]
+           "scan_pipe_newton.hip", "scan_gated_chunk.hip", "decode.hip", "scan_backward.hip",
+           "scan_direct.hip", "swila_api.hip"]
 ARCH = "gfx950"
 
 # Packed fp32 VALU instructions are turned off for every kernel: the compiler

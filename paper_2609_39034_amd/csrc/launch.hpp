@@ -82,6 +82,10 @@ hipError_t launch_scan_direct(const LayerArgs &a, hipStream_t stream);
 // matrix-core waves); bf16 inputs, T > 0.  With gate logits (a.gk) it runs the
 // temporal form.
 hipError_t launch_scan_pipe(const LayerArgs &a, hipStream_t stream);
+// Gated SwiLA (App. B.4) in chunks of 16 tokens on the matrix cores: bf16
+// inputs, no temporal priors, J <= 4, J * Dk <= 256 (gated_chunk_supported).
+bool gated_chunk_supported(const LayerArgs &a);
+hipError_t launch_scan_gated_chunk(const LayerArgs &a, hipStream_t stream);
 hipError_t launch_scan_pipe_temporal(const LayerArgs &a, hipStream_t stream);
 
 // Chunkwise quasi-Newton evaluation (App. D) on the same pipelined kernel;

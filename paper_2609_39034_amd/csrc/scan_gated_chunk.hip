@@ -1,0 +1,610 @@
+// Chunk form of Gated SwiLA on the matrix cores (App. B.4, eq. pre-decay with
+// one gate per key dimension, eq. gate-elementwise tied across the output
+// index): bf16 inputs, fp32 state.
+//
+// Per component j and output dim d the recurrence is
+//   w~_t = a_t (.) w_{t-1},   delta_t = v_t - k_t . w~_t,   w_t = w~_t + c_t k_t,
+// c_t = beta r delta (r from eq. responsibility at the decayed state), with
+// a_t = sigmoid(decay logit) in (0,1)^Dk.  Inside a chunk of 16 tokens that
+// starts from S, with L_t = sum_{u<=t} log a_u (per key index, from the chunk
+// start) and E_t = e^{L_t}:
+//   w~_t = E_t (.) S + sum_{s<t} (E_t / E_s) (.) k_s c_s
+//   pred_t  = (k_t (.) E_t) . S + sum_{s<t} G_ts c_s,   G_ts = sum_i k_ti k_si e^{L_ti - L_si}
+//   q_t.w_t = (q_t (.) E_t) . S + sum_{s<=t} QG_ts c_s, QG_ts = sum_i q_ti k_si e^{L_ti - L_si}
+//   S'      = E_C (.) S + sum_s (k_s (.) E_C / E_s) c_s.
+// G and QG are formed as (K (.) E)(K (.) E^-1)^T on the matrix cores while
+// every e^{-L} stays below e^{40}; a chunk whose gates decay further (some
+// L_C < -40) forms them with the per-pair exponent instead.  The scaled
+// operands are fp32: each is split into a bf16 high part and a bf16 residual,
+// and the hi*hi + hi*lo + lo*hi products are summed (about 2^-16 relative per
+// product, fp32 accumulation).  A component's gates differ from the others',
+// so each component has its own Gram matrices and scaled operands: tile wave
+// j holds the state columns of component j.
+//
+// Block = one head (b, h) and DB output dims with all J components (J <= 4,
+// J * Dk <= 256): J tile waves (wave j: the Dk x DB state tile of component j
+// in accumulator registers), one sequential wave (one lane per column, the J
+// components of an output dim in adjacent lanes), three helper waves.  Per
+// chunk n, between two block barriers:
+//   phase A  sequential wave: the chunk's 16-token recurrence -> C_n
+//            tile waves: retrieval of chunk n-1 (needs C_{n-1}); Q_n S_n and
+//              QG_n; the update operand of chunk n; K_{n+1} (.) E_{n+1} and
+//              G_{n+1} for the next recurrence
+//            helper waves: pi^q_n, the output of chunk n-2, and the inputs of
+//              chunk n+2 (HBM -> registers -> LDS, with its L)
+//   phase B  tile waves: S_{n+1} = E_C (.) S_n + U_n^T C_n and
+//              P_{n+1} = (K_{n+1} (.) E_{n+1}) S_{n+1} for the next recurrence;
+//            sequential wave: beta, key-prior logits and v of chunk n+1.
+#include "device_common.hpp"
+#include "launch.hpp"
+
+namespace swila {
+namespace {
+
+typedef short short4v __attribute__((ext_vector_type(4)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+constexpr int kGC = 16;              // tokens per chunk
+constexpr int kGH = 3;               // helper waves
+constexpr float kGramL = -40.0f;     // factorised Gram products while every L >= this
+constexpr int ceil_div_c(int x, int y) { return (x + y - 1) / y; }
+
+__device__ __forceinline__ floatx4 mfma16(short4v a, short4v b, floatx4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b, c, 0, 0, 0);
+}
+
+// Four fp32 values as bf16 high parts and bf16 residuals.
+struct S4 {
+    short4v hi, lo;
+};
+__device__ __forceinline__ S4 split4(float x0, float x1, float x2, float x3) {
+    const float x[4] = {x0, x1, x2, x3};
+    S4 s;
+#pragma unroll
+    for (int m = 0; m < 4; ++m) {
+        const __bf16 h = (__bf16)x[m];
+        s.hi[m] = __builtin_bit_cast(short, h);
+        s.lo[m] = __builtin_bit_cast(short, (__bf16)(x[m] - (float)h));
+    }
+    return s;
+}
+__device__ __forceinline__ S4 split4(floatx4 x) { return split4(x[0], x[1], x[2], x[3]); }
+__device__ __forceinline__ S4 zero4() {
+    S4 s;
+    s.hi = short4v{0, 0, 0, 0};
+    s.lo = short4v{0, 0, 0, 0};
+    return s;
+}
+// a b with both operands split: hi hi + hi lo + lo hi
+__device__ __forceinline__ floatx4 mm3(const S4 &a, const S4 &b, floatx4 acc) {
+    acc = mfma16(a.hi, b.hi, acc);
+    acc = mfma16(a.hi, b.lo, acc);
+    acc = mfma16(a.lo, b.hi, acc);
+    return acc;
+}
+
+__device__ __forceinline__ float bf(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
+
+// log sigmoid(x) = min(x, 0) - log(1 + e^{-|x|})
+__device__ __forceinline__ float log_sigmoid(float x) {
+    const float e = __builtin_amdgcn_exp2f(-fabsf(x) * kLog2e);
+    return fminf(x, 0.0f) - __builtin_amdgcn_logf(1.0f + e) * 0.69314718055994531f;
+}
+
+template <int DK, int J, int DB>
+struct GCfg {
+    static constexpr int IT = DK / 16;       // 16-row key tiles
+    static constexpr int N = J * DB;         // columns, col = j * DB + dd
+    static constexpr int JP = J == 3 ? 4 : J;
+    static constexpr int NWAVE = J + 1 + kGH;
+    static constexpr int KP = DK + 4;        // bf16 row pitch of the K, Q tiles
+    static constexpr int LP = DK + 4;        // fp32 row pitch of L
+    static constexpr int TP = kGC + 4;       // [column][token] row pitch
+    static constexpr int NP = N + 4;         // [token][column] row pitch
+    static_assert(J >= 1 && J <= 4 && J * DK <= 256, "LDS budget of the gated chunk form");
+    static_assert(DB == 8 || DB == 16, "column block");
+    static_assert(DB * JP <= 64, "one sequential wave");
+};
+
+template <int DK, int J, int DB>
+struct GSmem {
+    using C = GCfg<DK, J, DB>;
+    // chunk inputs, chunk m in slot m % 3
+    alignas(16) uint16_t k[3][kGC][C::KP];
+    alignas(16) uint16_t q[3][kGC][C::KP];
+    alignas(16) uint16_t lb[3][kGC][C::N];   // [token][j * DB + dd]
+    alignas(16) uint16_t lk[3][kGC][C::N];
+    alignas(16) uint16_t lq[3][kGC][C::N];
+    alignas(16) uint16_t v[3][kGC][DB];
+    alignas(16) float L[3][J][kGC][C::LP];   // cumulative log gates from the chunk start
+    int fb[3];                               // the chunk's Gram products need the per-pair exponent
+    alignas(16) float gt[2][J][kGC][kGC + 4];   // gt[.][j][s][t] = G_ts (t > s), chunk m in m & 1
+    alignas(16) float p[C::N][C::TP];        // chunk-start predictions [column][token]
+    alignas(16) float c[2][C::N][C::TP];     // coefficients [column][token], chunk m in m & 1
+    float pq[2][kGC][C::NP];                 // pi^q [token][column]
+    float py[2][kGC][C::NP];                 // pi^q * retrieval [token][column]
+};
+
+// Block -> (column block, head): the column blocks of a head on one XCD
+// (workgroups go to the eight XCDs round-robin by index, each with its own L2),
+// so that the head's K, Q and gate rows are fetched from HBM once.
+__device__ __forceinline__ void gated_coords(int id, int ndb, int nheads, int &db, int &head) {
+    if (nheads % 8 == 0) {
+        const int k = id / 8;
+        head = id % 8 + 8 * (k / ndb);
+        db = k % ndb;
+    } else {
+        head = id / ndb;
+        db = id % ndb;
+    }
+}
+
+// Each role runs its whole chunk loop in a branch of its own, so that the
+// registers one role keeps across chunks are not held by the others; every
+// role meets the same block barriers in the same order: three in the prologue,
+// two per chunk (e(n): C_n and chunk n + 2 published; i(n+1): P_{n+1}
+// published), one in the epilogue.
+template <int DK, int J, int DB>
+__global__ __launch_bounds__(512) void scan_gated_chunk_kernel(LayerArgs a) {
+    using C = GCfg<DK, J, DB>;
+    constexpr int IT = C::IT, N = C::N, JP = C::JP;
+    __shared__ GSmem<DK, J, DB> sm;
+
+    const int tid = threadIdx.x;
+    const int w = __builtin_amdgcn_readfirstlane(tid / 64), lane = tid % 64;
+    const int tl = lane % 16, lg = lane / 16;
+    const int H = a.H, T = a.T, Dv = a.Dv;
+    int db, hh;
+    gated_coords(blockIdx.x, Dv / DB, a.B * H, db, hh);
+    const int d0 = db * DB, h = hh % H, b = hh / H;
+    const int NCH = (T + kGC - 1) / kGC;
+
+    if (w < J) {
+        // ================= tile wave j: the state of component j =================
+        // state S^j rows 16 it + 4 lg + r, column tl (a real column when tl < DB)
+        const int tj = w;
+        const bool tvalid = tl < DB;
+        const int tcol = tj * DB + (tvalid ? tl : 0);
+        floatx4 W[IT];
+        S4 Kp[IT];     // K_{m} (.) E_{m} for the next chunk m, A operand (rows t = tl)
+        S4 Kinv[IT];   // K_m (.) E_m^-1 (rows s = tl): B operand of G_m, A operand of QG_m
+        S4 U[IT];      // update operand of chunk n: rows i = 16 it + tl, columns s = 4 lg + m
+        floatx4 Y0 = floatx4{0.f, 0.f, 0.f, 0.f};   // Q S of the chunk whose retrieval is pending
+        S4 QGs = zero4();                           // its tril(QG), A operand
+
+        // X (.) e^{sign L} of the chunk in slot s3, rows tl, key indices 16 it + 4 lg .. + 3
+        auto scaled_rows = [&](const uint16_t (*X)[C::KP], int s3, int it, float sign) {
+            const uint2 raw = *reinterpret_cast<const uint2 *>(&X[tl][16 * it + 4 * lg]);
+            const float4 l = *reinterpret_cast<const float4 *>(&sm.L[s3][tj][tl][16 * it + 4 * lg]);
+            const float f = sign * kLog2e;
+            return split4(__uint_as_float(raw.x << 16) * __builtin_amdgcn_exp2f(f * l.x),
+                          __uint_as_float(raw.x & 0xffff0000u) * __builtin_amdgcn_exp2f(f * l.y),
+                          __uint_as_float(raw.y << 16) * __builtin_amdgcn_exp2f(f * l.z),
+                          __uint_as_float(raw.y & 0xffff0000u) * __builtin_amdgcn_exp2f(f * l.w));
+        };
+        // per-pair exponent: sum_i X[t][i] K[s][i] e^{L_ti - L_si} (chunk in slot s3)
+        auto pair_dot = [&](const uint16_t (*X)[C::KP], int s3, int t, int s) {
+            float acc = 0.0f;
+            for (int i = 0; i < DK; ++i)
+                acc = fmaf(bf(X[t][i]) * bf(sm.k[s3][s][i]),
+                           __builtin_amdgcn_exp2f(kLog2e * (sm.L[s3][tj][t][i] - sm.L[s3][tj][s][i])),
+                           acc);
+            return acc;
+        };
+        // Kp, Kinv and the Gram matrix of chunk m (for the sequential wave)
+        auto gram = [&](int m) {
+            const int s3 = m % 3;
+            const bool pair = sm.fb[s3] != 0;
+            floatx4 g = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int it = 0; it < IT; ++it) {
+                Kp[it] = scaled_rows(sm.k[s3], s3, it, 1.0f);
+                Kinv[it] = pair ? zero4() : scaled_rows(sm.k[s3], s3, it, -1.0f);
+                g = mm3(Kp[it], Kinv[it], g);   // D[t = 4 lg + r][s = tl] = G_ts
+            }
+            if (pair) {
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int t = 4 * lg + r;
+                    g[r] = t > tl ? pair_dot(sm.k[s3], s3, t, tl) : 0.0f;
+                }
+            }
+            *reinterpret_cast<float4 *>(&sm.gt[m & 1][tj][tl][4 * lg]) =
+                make_float4(g[0], g[1], g[2], g[3]);
+        };
+        // chunk-start predictions P = Kp S for the sequential wave
+        auto predict = [&]() {
+            floatx4 pacc = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int it = 0; it < IT; ++it) pacc = mm3(Kp[it], split4(W[it]), pacc);   // D[t][col]
+            if (tvalid)
+                *reinterpret_cast<float4 *>(&sm.p[tcol][4 * lg]) =
+                    make_float4(pacc[0], pacc[1], pacc[2], pacc[3]);
+        };
+        // C of chunk m as the B operand: rows s = 4 lg .. + 3, column tl
+        auto coeffs = [&](int m) {
+            const float4 c4 = *reinterpret_cast<const float4 *>(&sm.c[m & 1][tcol][4 * lg]);
+            return tvalid ? split4(c4.x, c4.y, c4.z, c4.w) : zero4();
+        };
+        // retrieval of chunk m: Y = Y0 + tril(QG) C, times pi^q, to py
+        auto retrieve = [&](int m) {
+            const floatx4 y = mm3(QGs, coeffs(m), Y0);   // D[t = 4 lg + r][col]
+            if (tvalid) {
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int t = 4 * lg + r;
+                    sm.py[m & 1][t][tcol] = sm.pq[m & 1][t][tcol] * y[r];
+                }
+            }
+        };
+        // what chunk n needs besides C_n: Q_n S_n, tril(QG_n), U_n (Kinv holds chunk n's)
+        auto prepare = [&](int n) {
+            const int s3 = n % 3;
+            const bool pair = sm.fb[s3] != 0;
+            floatx4 y0 = floatx4{0.f, 0.f, 0.f, 0.f}, qg = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int it = 0; it < IT; ++it) {
+                const S4 qe = scaled_rows(sm.q[s3], s3, it, 1.0f);   // rows t = tl
+                y0 = mm3(qe, split4(W[it]), y0);                      // D[t = 4 lg + r][col]
+                qg = mm3(Kinv[it], qe, qg);                           // D[s = 4 lg + r][t = tl]
+            }
+            Y0 = y0;
+            // lane (t = tl, lg) holds QG[t][s = 4 lg + r]: the A operand of the retrieval
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int s = 4 * lg + r;
+                if (pair) qg[r] = s <= tl ? pair_dot(sm.q[s3], s3, tl, s) : 0.0f;
+                else if (s > tl) qg[r] = 0.0f;
+            }
+            QGs = split4(qg);
+            // U[i][s] = K[s][i] e^{L_C,i - L_s,i}, i = 16 it + tl, s = 4 lg + m
+#pragma unroll
+            for (int it = 0; it < IT; ++it) {
+                const int i = 16 * it + tl;
+                const float lc = sm.L[s3][tj][kGC - 1][i];
+                float u[4];
+#pragma unroll
+                for (int m = 0; m < 4; ++m) {
+                    const int s = 4 * lg + m;
+                    u[m] = bf(sm.k[s3][s][i]) *
+                           __builtin_amdgcn_exp2f(kLog2e * (lc - sm.L[s3][tj][s][i]));
+                }
+                U[it] = split4(u[0], u[1], u[2], u[3]);
+            }
+        };
+
+#pragma unroll
+        for (int it = 0; it < IT; ++it)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+                W[it][r] = tvalid && a.state_in
+                               ? a.state_in[(((size_t)b * H + h) * J + tj) * DK * Dv +
+                                            (size_t)(16 * it + 4 * lg + r) * Dv + d0 + tl]
+                               : 0.0f;
+        block_sync_lds();   // prologue 1: flags cleared
+        block_sync_lds();   // prologue 2: chunks 0 and 1 in LDS
+        gram(0);            // Kp = K_0 (.) E_0, Kinv = K_0 (.) E_0^-1, G_0
+        predict();          // P_0
+        block_sync_lds();   // prologue 3
+        for (int n = 0; n < NCH; ++n) {
+            // ---- phase A: everything that does not need C_n
+            if (n >= 1) retrieve(n - 1);
+            prepare(n);
+            if (n + 1 < NCH) gram(n + 1);
+            block_sync_lds();   // e(n)
+            // ---- phase B: S_{n+1} = E_C (.) S_n + U_n^T C_n, then P_{n+1}
+            const S4 cb = coeffs(n);
+#pragma unroll
+            for (int it = 0; it < IT; ++it) {
+                const float4 l4 =
+                    *reinterpret_cast<const float4 *>(&sm.L[n % 3][tj][kGC - 1][16 * it + 4 * lg]);
+                W[it][0] *= __builtin_amdgcn_exp2f(kLog2e * l4.x);
+                W[it][1] *= __builtin_amdgcn_exp2f(kLog2e * l4.y);
+                W[it][2] *= __builtin_amdgcn_exp2f(kLog2e * l4.z);
+                W[it][3] *= __builtin_amdgcn_exp2f(kLog2e * l4.w);
+                W[it] = mm3(U[it], cb, W[it]);
+            }
+            if (n + 1 < NCH) predict();
+            block_sync_lds();   // i(n+1)
+        }
+        retrieve(NCH - 1);
+        block_sync_lds();   // epilogue
+        if (tvalid && a.state_out) {
+#pragma unroll
+            for (int it = 0; it < IT; ++it)
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    a.state_out[(((size_t)b * H + h) * J + tj) * DK * Dv +
+                                (size_t)(16 * it + 4 * lg + r) * Dv + d0 + tl] = W[it][r];
+        }
+    } else if (w == J) {
+        // ================= sequential wave: one lane per column =================
+        const int sdd = lane / JP, sj = lane % JP;
+        const bool sact = sdd < DB && sj < J;
+        const int scol = sact ? sj * DB + sdd : 0, gj = sact ? sj : 0;
+        float sbeta[kGC], slk[kGC], sv[kGC];
+        auto seq_inputs = [&](int m) {   // beta, key-prior logits and v of chunk m
+            const int s3 = m % 3, nt = min(kGC, T - m * kGC);
+#pragma unroll
+            for (int t = 0; t < kGC; ++t) {
+                // tokens past the end take beta = 0: no update
+                sbeta[t] = sact && t < nt ? sigmoid(bf(sm.lb[s3][t][scol])) : 0.0f;
+                slk[t] = sact ? bf(sm.lk[s3][t][scol]) : 0.0f;
+                sv[t] = sact ? bf(sm.v[s3][t][sdd]) : 0.0f;
+            }
+        };
+        block_sync_lds();   // prologue 1
+        block_sync_lds();   // prologue 2
+        seq_inputs(0);
+        block_sync_lds();   // prologue 3
+        for (int n = 0; n < NCH; ++n) {
+            const int t0 = n * kGC, nt = min(kGC, T - t0), gs = n & 1;
+            float pacc[kGC], cc[kGC];
+#pragma unroll
+            for (int t4 = 0; t4 < kGC; t4 += 4) {
+                const float4 p4 = *reinterpret_cast<const float4 *>(&sm.p[scol][t4]);
+                pacc[t4] = p4.x, pacc[t4 + 1] = p4.y, pacc[t4 + 2] = p4.z, pacc[t4 + 3] = p4.w;
+            }
+#pragma unroll
+            for (int t = 0; t < kGC; ++t) {
+                const float delta = sv[t] - pacc[t];
+                float r = 1.0f;
+                if constexpr (J > 1) {
+                    // eq. responsibility at the decayed state, over the J lanes of the dim
+                    const float e = sact ? slk[t] - 0.5f * delta * delta : -INFINITY;
+                    const float mx = group_max<JP>(e);
+                    const float ex = sact ? __builtin_amdgcn_exp2f(kLog2e * (e - mx)) : 0.0f;
+                    const float z = group_sum<JP>(ex);
+                    r = sact ? ex * rcp_fast(z) : 0.0f;
+                }
+                const float c = sbeta[t] * r * delta;
+                cc[t] = c;
+                if (a.resp && sact && t < nt)
+                    a.resp[((((size_t)b * T + t0 + t) * H + h) * J + sj) * Dv + d0 + sdd] = r;
+                // the later tokens' predictions: pred_u += G_ut c_t (row t of gt)
+#pragma unroll
+                for (int u4 = 4 * ((t + 1) / 4); u4 < kGC; u4 += 4) {
+                    const float4 g4 = *reinterpret_cast<const float4 *>(&sm.gt[gs][gj][t][u4]);
+                    const float gg[4] = {g4.x, g4.y, g4.z, g4.w};
+#pragma unroll
+                    for (int x = 0; x < 4; ++x)
+                        if (u4 + x > t) pacc[u4 + x] = fmaf(gg[x], c, pacc[u4 + x]);
+                }
+            }
+            if (sact) {
+#pragma unroll
+                for (int t4 = 0; t4 < kGC; t4 += 4)
+                    *reinterpret_cast<float4 *>(&sm.c[n & 1][scol][t4]) =
+                        make_float4(cc[t4], cc[t4 + 1], cc[t4 + 2], cc[t4 + 3]);
+            }
+            block_sync_lds();   // e(n)
+            if (n + 1 < NCH) seq_inputs(n + 1);
+            block_sync_lds();   // i(n+1)
+        }
+        block_sync_lds();   // epilogue
+    } else {
+        // ================= helper waves: inputs, priors, outputs =================
+        const int bt = tid - 64 * (J + 1);
+        constexpr int NBT = 64 * kGH;
+        const bool obf = a.out_bf16;
+        const uint16_t *const Kg = static_cast<const uint16_t *>(a.k);
+        const uint16_t *const Qg = static_cast<const uint16_t *>(a.q);
+        const uint16_t *const Vg = static_cast<const uint16_t *>(a.v);
+        const uint16_t *const LBg = static_cast<const uint16_t *>(a.lb);
+        const uint16_t *const LKg = static_cast<const uint16_t *>(a.lk);
+        const uint16_t *const LQg = static_cast<const uint16_t *>(a.lq);
+        const uint16_t *const Gg = static_cast<const uint16_t *>(a.decay);
+        // one chunk's raw inputs, in registers from fetch to land
+        constexpr int NKQ = ceil_div_c(kGC * DK / 8, NBT);   // uint4 of K (and of Q)
+        constexpr int NLG = ceil_div_c(kGC * N / 8, NBT);    // uint4 of each logit tensor
+        constexpr int NV = ceil_div_c(kGC * DB / 8, NBT);
+        constexpr int NPAIR = ceil_div_c(J * DK, NBT);       // (j, i) gate columns
+        uint4 rk[NKQ], rq[NKQ], rlb[NLG], rlk[NLG], rlq[NLG], rv[NV];
+        uint16_t rg[NPAIR][kGC];
+        auto fetch = [&](int m) {
+            const int t0 = m * kGC, nt = min(kGC, T - t0);
+            const size_t row0 = (size_t)b * T + t0;
+#pragma unroll
+            for (int x = 0; x < NKQ; ++x) {
+                const int e = bt + NBT * x, t = e / (DK / 8), p = e % (DK / 8);
+                rk[x] = rq[x] = make_uint4(0u, 0u, 0u, 0u);
+                if (e < kGC * DK / 8 && t < nt) {
+                    const size_t off = ((row0 + t) * H + h) * DK + 8 * p;
+                    rk[x] = *reinterpret_cast<const uint4 *>(Kg + off);
+                    rq[x] = *reinterpret_cast<const uint4 *>(Qg + off);
+                }
+            }
+#pragma unroll
+            for (int x = 0; x < NLG; ++x) {
+                const int e = bt + NBT * x, t = e / (N / 8), rem = e % (N / 8);
+                const int j = rem / (DB / 8), p = rem % (DB / 8);
+                rlb[x] = rlk[x] = rlq[x] = make_uint4(0u, 0u, 0u, 0u);
+                if (e < kGC * N / 8 && t < nt) {
+                    const size_t off = (((row0 + t) * H + h) * J + j) * Dv + d0 + 8 * p;
+                    rlb[x] = *reinterpret_cast<const uint4 *>(LBg + off);
+                    rlk[x] = *reinterpret_cast<const uint4 *>(LKg + off);
+                    rlq[x] = *reinterpret_cast<const uint4 *>(LQg + off);
+                }
+            }
+#pragma unroll
+            for (int x = 0; x < NV; ++x) {
+                const int e = bt + NBT * x, t = e / (DB / 8), p = e % (DB / 8);
+                rv[x] = make_uint4(0u, 0u, 0u, 0u);
+                if (e < kGC * DB / 8 && t < nt)
+                    rv[x] = *reinterpret_cast<const uint4 *>(Vg + ((row0 + t) * H + h) * Dv + d0 + 8 * p);
+            }
+#pragma unroll
+            for (int x = 0; x < NPAIR; ++x) {
+                const int e = bt + NBT * x;   // (j, i) = (e / DK, e % DK)
+#pragma unroll
+                for (int t = 0; t < kGC; ++t) {
+                    rg[x][t] = 0;
+                    if (e < J * DK && t < nt) rg[x][t] = Gg[((row0 + t) * H + h) * J * DK + e];
+                }
+            }
+        };
+        // chunk m's inputs to its slot, with its cumulative log gates and flag
+        auto land = [&](int m) {
+            const int s3 = m % 3, nt = min(kGC, T - m * kGC);
+#pragma unroll
+            for (int x = 0; x < NKQ; ++x) {
+                const int e = bt + NBT * x, t = e / (DK / 8), p = e % (DK / 8);
+                if (e < kGC * DK / 8) {
+                    // two 8-byte stores: the padded rows are 8-byte aligned
+                    uint2 *dk = reinterpret_cast<uint2 *>(&sm.k[s3][t][8 * p]);
+                    uint2 *dq = reinterpret_cast<uint2 *>(&sm.q[s3][t][8 * p]);
+                    dk[0] = make_uint2(rk[x].x, rk[x].y);
+                    dk[1] = make_uint2(rk[x].z, rk[x].w);
+                    dq[0] = make_uint2(rq[x].x, rq[x].y);
+                    dq[1] = make_uint2(rq[x].z, rq[x].w);
+                }
+            }
+#pragma unroll
+            for (int x = 0; x < NLG; ++x) {
+                const int e = bt + NBT * x, t = e / (N / 8), col8 = e % (N / 8);
+                if (e < kGC * N / 8) {
+                    *reinterpret_cast<uint4 *>(&sm.lb[s3][t][8 * col8]) = rlb[x];
+                    *reinterpret_cast<uint4 *>(&sm.lk[s3][t][8 * col8]) = rlk[x];
+                    *reinterpret_cast<uint4 *>(&sm.lq[s3][t][8 * col8]) = rlq[x];
+                }
+            }
+#pragma unroll
+            for (int x = 0; x < NV; ++x) {
+                const int e = bt + NBT * x, t = e / (DB / 8), p = e % (DB / 8);
+                if (e < kGC * DB / 8) *reinterpret_cast<uint4 *>(&sm.v[s3][t][8 * p]) = rv[x];
+            }
+            bool deep = false;
+#pragma unroll
+            for (int x = 0; x < NPAIR; ++x) {
+                const int e = bt + NBT * x;
+                if (e < J * DK) {
+                    const int j = e / DK, i = e % DK;
+                    float cum = 0.0f;
+#pragma unroll
+                    for (int t = 0; t < kGC; ++t) {
+                        // tokens past the end decay nothing: the chunk's last row
+                        // is the cumulative gate of its last token
+                        if (t < nt) cum += log_sigmoid(bf(rg[x][t]));
+                        sm.L[s3][j][t][i] = cum;
+                    }
+                    deep = deep || !(cum >= kGramL);
+                }
+            }
+            if (deep) sm.fb[s3] = 1;
+        };
+        // pi^q of chunk m: softmax over j of the query-prior logits, per (t, dd)
+        auto priors = [&](int m) {
+            const int s3 = m % 3;
+            for (int e = bt; e < kGC * DB; e += NBT) {
+                const int t = e / DB, dd = e % DB;
+                float x[J], mx = -INFINITY, z = 0.0f;
+#pragma unroll
+                for (int j = 0; j < J; ++j) {
+                    x[j] = bf(sm.lq[s3][t][j * DB + dd]);
+                    mx = fmaxf(mx, x[j]);
+                }
+#pragma unroll
+                for (int j = 0; j < J; ++j) {
+                    x[j] = __builtin_amdgcn_exp2f(kLog2e * (x[j] - mx));
+                    z += x[j];
+                }
+                const float iz = rcp_fast(z);
+#pragma unroll
+                for (int j = 0; j < J; ++j) sm.pq[m & 1][t][j * DB + dd] = J == 1 ? 1.0f : x[j] * iz;
+            }
+        };
+        // output of chunk m: o = sum_j pi^q y
+        auto output = [&](int m) {
+            const int mt0 = m * kGC, nt = min(kGC, T - mt0);
+            for (int e = bt; e < kGC * DB; e += NBT) {
+                const int t = e / DB, dd = e % DB;
+                if (t >= nt) continue;
+                float o = 0.0f;
+#pragma unroll
+                for (int j = 0; j < J; ++j) o += sm.py[m & 1][t][j * DB + dd];
+                store1(a.o, (((size_t)b * T + mt0 + t) * H + h) * Dv + d0 + dd, o, obf);
+            }
+        };
+
+        if (bt < 3) sm.fb[bt] = 0;
+        block_sync_lds();   // prologue 1
+        fetch(0);
+        land(0);
+        if (NCH > 1) {
+            fetch(1);
+            land(1);
+        }
+        block_sync_lds();   // prologue 2
+        if (NCH > 2) fetch(2);
+        block_sync_lds();   // prologue 3
+        for (int n = 0; n < NCH; ++n) {
+            priors(n);
+            if (n >= 2) output(n - 2);
+            // chunk n + 2 lands in the slot of chunk n - 1 (its flag cleared in
+            // phase B of chunk n - 1)
+            if (n + 2 < NCH) land(n + 2);
+            block_sync_lds();   // e(n)
+            if (n + 3 < NCH) fetch(n + 3);
+            // chunk n's slot is free after this phase: chunk n + 3 lands there next
+            if (bt == 0) sm.fb[n % 3] = 0;
+            block_sync_lds();   // i(n+1)
+        }
+        if (NCH >= 2) output(NCH - 2);
+        block_sync_lds();   // epilogue
+        output(NCH - 1);
+    }
+}
+
+template <int DK, int J, int DB>
+hipError_t launch_g(const LayerArgs &a, hipStream_t stream) {
+    using C = GCfg<DK, J, DB>;
+    static_assert(sizeof(GSmem<DK, J, DB>) <= 160 * 1024, "LDS");
+    const long blocks = (long)(a.Dv / DB) * a.H * a.B;
+    hipLaunchKernelGGL((scan_gated_chunk_kernel<DK, J, DB>), dim3((unsigned)blocks),
+                       dim3(64 * C::NWAVE), 0, stream, a);
+    return hipGetLastError();
+}
+
+template <int DK, int J>
+hipError_t launch_gj(const LayerArgs &a, hipStream_t stream) {
+    if constexpr (J * DK > 256) {
+        return hipErrorInvalidValue;
+    } else {
+        // 16 output dims per block once that grid fills the chip; 8 below
+        if (a.Dv % 16 == 0 && (long)(a.Dv / 16) * a.H * a.B >= 256)
+            return launch_g<DK, J, 16>(a, stream);
+        return launch_g<DK, J, 8>(a, stream);
+    }
+}
+
+template <int DK>
+hipError_t launch_gdk(const LayerArgs &a, hipStream_t stream) {
+    switch (a.J) {
+        case 1: return launch_gj<DK, 1>(a, stream);
+        case 2: return launch_gj<DK, 2>(a, stream);
+        case 3: return launch_gj<DK, 3>(a, stream);
+        case 4: return launch_gj<DK, 4>(a, stream);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace
+
+bool gated_chunk_supported(const LayerArgs &a) {
+    return a.in_bf16 && a.decay && !a.gk && !a.delta_out && !a.ckpt && a.J >= 1 && a.J <= 4 &&
+           a.J * a.Dk <= 256 && a.Dv % 8 == 0 &&
+           (a.Dk == 16 || a.Dk == 32 || a.Dk == 64 || a.Dk == 128);
+}
+
+hipError_t launch_scan_gated_chunk(const LayerArgs &a, hipStream_t stream) {
+    if (!gated_chunk_supported(a) || a.T <= 0) return hipErrorInvalidValue;
+    switch (a.Dk) {
+        case 16: return launch_gdk<16>(a, stream);
+        case 32: return launch_gdk<32>(a, stream);
+        case 64: return launch_gdk<64>(a, stream);
+        case 128: return launch_gdk<128>(a, stream);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace swila

@@ -493,9 +493,17 @@ int swila_forward_gated(const swila_shape *shape, const swila_opts *opts, const 
     }
     rc = check_gated(shape, opts, gated, temporal, o, state_out, resp_out, &a);
     if (rc) return rc;
-    if (opts->algo == SWILA_ALGO_NEWTON || opts->algo == SWILA_ALGO_CHUNK_EXACT)
-        return fail(SWILA_EUNSUPPORTED, "the gated form runs on SWILA_ALGO_RECURRENT");
-    if (shape->J * shape->Dk > swila::kMaxGatedJDk)
+    if (opts->algo == SWILA_ALGO_NEWTON)
+        return fail(SWILA_EUNSUPPORTED,
+                    "the gated form runs on SWILA_ALGO_CHUNK_EXACT or SWILA_ALGO_RECURRENT");
+    const bool chunk_ok = swila::gated_chunk_supported(a);
+    if (opts->algo == SWILA_ALGO_CHUNK_EXACT && !chunk_ok)
+        return fail(SWILA_EUNSUPPORTED,
+                    "the gated chunk form takes bf16 inputs without temporal priors, J <= 4 "
+                    "and J * Dk <= 256 (J=%d, Dk=%d)",
+                    shape->J, shape->Dk);
+    const bool use_chunk = chunk_ok && opts->algo != SWILA_ALGO_RECURRENT;
+    if (!use_chunk && shape->J * shape->Dk > swila::kMaxGatedJDk)
         return fail(SWILA_EUNSUPPORTED, "gated forward: J * Dk = %d exceeds %d",
                     shape->J * shape->Dk, swila::kMaxGatedJDk);
     hipStream_t st = static_cast<hipStream_t>(stream);
@@ -512,6 +520,7 @@ int swila_forward_gated(const swila_shape *shape, const swila_opts *opts, const 
                                           1.0f / shape->J, st),
                        "prior state copy");
     }
+    if (use_chunk) return map_hip(swila::launch_scan_gated_chunk(a, st), "gated chunk launch");
     return map_hip(swila::launch_scan_direct(a, st), "scan launch");
 }
 

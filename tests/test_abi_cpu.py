@@ -238,9 +238,22 @@ def test_gated_argument_checks(lib):
     assert rc == sw.EINVAL and "decay_logit is not 16-byte aligned" in msg
     rc, msg = call(sw.Gated(FAKE2.value))
     assert rc == sw.EINVAL and "decay_logit overlaps o" in msg
-    chunk = sw.Opts(sw.BF16, sw.BF16, sw.ALGO_CHUNK_EXACT, 0, 0, 0.0, 0)
-    rc, msg = call(sw.Gated(dec), opts=chunk)
+    newton = sw.Opts(sw.BF16, sw.BF16, sw.ALGO_NEWTON, 0, 0, 0.0, 0)
+    rc, msg = call(sw.Gated(dec), opts=newton)
     assert rc == sw.EUNSUPPORTED and "RECURRENT" in msg
+    # the chunk form: bf16 without temporal priors, J <= 4, J * Dk <= 256 (only
+    # calls it rejects are made here)
+    chunk = sw.Opts(sw.BF16, sw.BF16, sw.ALGO_CHUNK_EXACT, 0, 0, 0.0, 0)
+    rc, msg = call(sw.Gated(dec), opts=chunk,
+                   tp=sw.Temporal(1 << 32, (1 << 32) + (1 << 26), None, None))
+    assert rc == sw.EUNSUPPORTED and "J * Dk <= 256" in msg
+    f32chunk = sw.Opts(sw.F32, sw.F32, sw.ALGO_CHUNK_EXACT, 0, 0, 0.0, 0)
+    rc, msg = call(sw.Gated(dec), opts=f32chunk)
+    assert rc == sw.EUNSUPPORTED and "bf16" in msg
+    shape.Dk = 128
+    rc, msg = call(sw.Gated(dec), opts=chunk)
+    assert rc == sw.EUNSUPPORTED and "J=4, Dk=128" in msg
+    shape.Dk = 64
     # temporal arguments are checked too when given
     rc, msg = call(sw.Gated(dec), tp=sw.Temporal(None, 1 << 32, None, None))
     assert rc == sw.EINVAL and msg == "gate_k_logit is NULL"

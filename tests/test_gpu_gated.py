@@ -1,6 +1,8 @@
 """Parity of the Gated SwiLA path (Sec. 3.4, App. B.4, eq. pre-decay with one
 gate per key dimension) through the C ABI with the fp64 oracle: the
-token-by-token scan and the decode step, alone and with the temporal priors.
+token-by-token scan and the decode step, alone and with the temporal priors,
+and the chunk form on the matrix cores (bf16 inputs, J <= 4, J * Dk <= 256),
+including chunks whose gates decay past the factorised Gram products.
 
 Bar as for the plain form: per (b, h), max|gpu - oracle| / max|oracle| <= 1e-4
 for fp32 inputs and <= 2e-2 for bf16 inputs (outputs, final state,
@@ -57,7 +59,8 @@ def test_gated_forward(B, H, T, Dk, Dv, J, dtype, std, temporal, mean):
         kw = dict(gate_k_logit=_t(tmp["gk"], dtype), gate_q_logit=_t(tmp["gq"], dtype),
                   prior_in=torch.from_numpy(tmp["prior"]).cuda())
         okw = dict(gate_k_logit=tmp["gk"], gate_q_logit=tmp["gq"], prior_in=tmp["prior"])
-    res = sw.forward_gated(*(dev[n] for n in NAMES), _t(dec, dtype), dev["state"], resp=True, **kw)
+    res = sw.forward_gated(*(dev[n] for n in NAMES), _t(dec, dtype), dev["state"], resp=True,
+                           algo="recurrent", **kw)
     torch.cuda.synchronize()
     res = [x.float().cpu().numpy().astype(np.float64) for x in res]
     ref = oracle.forward(*(inp[n] for n in NAMES), inp["state"], decay_logit=dec, want_resp=True,
@@ -136,9 +139,10 @@ def test_gated_decode_steps(B, H, Dk, Dv, J, dtype, steps, temporal):
     assert eo <= tol and es <= tol and ep <= tol
 
 
-def test_gated_config2_every_head():
+@pytest.mark.parametrize("algo", ["chunk", "recurrent"])
+def test_gated_config2_every_head(algo):
     """The c2 batch, as the benchmark times it, through the gated form (decay
-    logits N(2,1)); the oracle on every head."""
+    logits N(2,1)) on either algorithm; the oracle on every head."""
     import torch
     import paper_2609_39034_amd as sw
     inp = workloads.config_inputs(2)
@@ -146,15 +150,130 @@ def test_gated_config2_every_head():
     B, H, T, Dk, J = c["B"], c["H"], c["T"], c["Dk"], c["J"]
     dec = workloads.gated_inputs(B, H, T, Dk, J, dtype="bf16", seed=1002)["decay"]
     dev = to_device(inp, "bf16")
-    o, s, r = sw.forward_gated(*(dev[n] for n in NAMES), _t(dec, "bf16"), None, resp=True)
+    o, s, r = sw.forward_gated(*(dev[n] for n in NAMES), _t(dec, "bf16"), None, resp=True,
+                               algo=algo)
     torch.cuda.synchronize()
     o, s, r = (x.float().cpu().numpy().astype(np.float64) for x in (o, s, r))
     ref = oracle.forward(*(inp[n] for n in NAMES), None, decay_logit=dec, want_resp=True)
     eo = head_rel_err(o, ref["o"], "o")
     es = head_rel_err(s, ref["state"], "state")
     er = head_rel_err(r, ref["resp"], "resp")
-    print("worst head: o %.3e state %.3e resp %.3e" % (eo, es, er))
+    print("%s, worst head: o %.3e state %.3e resp %.3e" % (algo, eo, es, er))
     assert eo <= 2e-2 and es <= 2e-2 and er <= 2e-2
+
+
+# ---- the chunk form (bf16 inputs, J <= 4, J * Dk <= 256)
+CHUNK_CASES = [
+    # B, H, T, Dk, Dv, J, state_std, decay mean
+    (1, 2, 37, 64, 64, 4, 0.1, 2.0),     # ragged third chunk
+    (2, 1, 16, 32, 16, 2, 0.0, 1.0),     # one whole chunk
+    (1, 1, 1, 16, 16, 1, 0.3, 2.0),      # one token
+    (2, 2, 50, 16, 32, 3, 0.2, 0.0),     # J = 3 (padded lanes), a = 1/2 on average
+    (1, 3, 70, 128, 64, 2, 0.1, 2.0),    # Dk = 128
+    (1, 2, 45, 128, 128, 1, 0.2, 3.0),   # J = 1
+    (2, 2, 64, 32, 128, 4, 0.1, 2.0),    # Dv = 128, whole chunks
+    (1, 1, 33, 64, 16, 4, 0.3, -1.0),    # strong decay (some chunks past the factorised form)
+    (8, 8, 40, 64, 64, 4, 0.1, 2.0),     # 256 blocks of 16 output dims
+    (4, 16, 29, 64, 32, 2, 0.2, 2.0),    # 256 blocks of 8 output dims
+]
+
+
+def _chunk_case(B, H, T, Dk, Dv, J, std, mean, seed, dec=None):
+    import torch
+    import paper_2609_39034_amd as sw
+    inp = workloads.iid_inputs(B, H, T, Dk, Dv, J, dtype="bf16", seed=seed, state_std=std)
+    if dec is None:
+        dec = workloads.gated_inputs(B, H, T, Dk, J, dtype="bf16", seed=seed, mean=mean)["decay"]
+    dev = to_device(inp, "bf16")
+    res = sw.forward_gated(*(dev[n] for n in NAMES), _t(dec, "bf16"), dev["state"], resp=True,
+                           algo="chunk")
+    torch.cuda.synchronize()
+    res = [x.float().cpu().numpy().astype(np.float64) for x in res]
+    ref = oracle.forward(*(inp[n] for n in NAMES), inp["state"], decay_logit=dec, want_resp=True)
+    eo, es = head_rel_err(res[0], ref["o"], "o"), head_rel_err(res[1], ref["state"], "state")
+    er = head_rel_err(res[2], ref["resp"], "resp")
+    print("chunk form: o %.3e state %.3e resp %.3e" % (eo, es, er))
+    return eo, es, er
+
+
+@pytest.mark.parametrize("B,H,T,Dk,Dv,J,std,mean", CHUNK_CASES)
+def test_gated_chunk_forward(B, H, T, Dk, Dv, J, std, mean):
+    eo, es, er = _chunk_case(B, H, T, Dk, Dv, J, std, mean, seed=700 + T + J + Dk)
+    assert eo <= 2e-2 and es <= 2e-2 and er <= 2e-2
+
+
+@pytest.mark.parametrize("J,Dk", [(4, 64), (2, 128), (1, 16)])
+def test_gated_chunk_deep_decay(J, Dk):
+    """Eight tokens of gate logit -8 (a = 3.4e-4, log a = -8) in the second chunk
+    take its cumulative log gate to about -64, past the factorised Gram
+    products: that chunk forms them with the per-pair exponent, the others do
+    not."""
+    B, H, T, Dv = 1, 2, 56, 32
+    dec = workloads.gated_inputs(B, H, T, Dk, J, dtype="bf16", seed=770)["decay"]
+    dec[:, 20:28] = -8.0
+    eo, es, er = _chunk_case(B, H, T, Dk, Dv, J, 0.2, 2.0, seed=771, dec=dec)
+    assert eo <= 2e-2 and es <= 2e-2 and er <= 2e-2
+
+
+def test_gated_chunk_all_chunks_deep():
+    """Gate logits around -4 everywhere: every chunk past the factorised form."""
+    eo, es, er = _chunk_case(2, 1, 48, 32, 32, 2, 0.1, -4.0, seed=772)
+    assert eo <= 2e-2 and es <= 2e-2 and er <= 2e-2
+
+
+def test_gated_chunk_saturated_equals_plain_chunk():
+    """Gate logits of 40 (a = 1 in fp32): the gated chunk form gives the plain
+    chunk scan's result, up to the rounding of two different kernels."""
+    import torch
+    import paper_2609_39034_amd as sw
+    B, H, T, D, J = 2, 2, 45, 64, 4
+    inp = workloads.iid_inputs(B, H, T, D, D, J, dtype="bf16", seed=773, state_std=0.2)
+    dev = to_device(inp, "bf16")
+    dec = torch.full((B, T, H, J, D), 40.0, device="cuda", dtype=torch.bfloat16)
+    o_g, s_g = sw.forward_gated(*(dev[n] for n in NAMES), dec, dev["state"], algo="chunk")
+    o_p, s_p = sw.forward(*(dev[n] for n in NAMES), dev["state"], algo="chunk")
+    torch.cuda.synchronize()
+    eo = head_rel_err(o_g.float().cpu().numpy(), o_p.float().cpu().numpy().astype(np.float64), "o")
+    es = head_rel_err(s_g.cpu().numpy(), s_p.cpu().numpy().astype(np.float64), "state")
+    print("o %.3e state %.3e" % (eo, es))
+    assert eo <= 1e-2 and es <= 1e-3
+
+
+def test_gated_chunk_state_chaining():
+    """Two calls, the second starting from the first's final state, equal one
+    call over the whole sequence (the split falls inside a chunk)."""
+    import torch
+    import paper_2609_39034_amd as sw
+    B, H, T, D, J = 1, 2, 53, 64, 4
+    inp = workloads.iid_inputs(B, H, T, D, D, J, dtype="bf16", seed=774, state_std=0.1)
+    dec = _t(workloads.gated_inputs(B, H, T, D, J, dtype="bf16", seed=774)["decay"], "bf16")
+    dev = to_device(inp, "bf16")
+    o, s = sw.forward_gated(*(dev[n] for n in NAMES), dec, dev["state"], algo="chunk")
+    cut = 21
+    first = [dev[n][:, :cut].contiguous() for n in NAMES]
+    second = [dev[n][:, cut:].contiguous() for n in NAMES]
+    o1, s1 = sw.forward_gated(*first, dec[:, :cut].contiguous(), dev["state"], algo="chunk")
+    o2, s2 = sw.forward_gated(*second, dec[:, cut:].contiguous(), s1, algo="chunk")
+    torch.cuda.synchronize()
+    oc = torch.cat([o1, o2], dim=1).float().cpu().numpy().astype(np.float64)
+    eo = head_rel_err(oc, o.float().cpu().numpy().astype(np.float64), "o")
+    es = head_rel_err(s2.cpu().numpy(), s.cpu().numpy().astype(np.float64), "state")
+    print("o %.3e state %.3e" % (eo, es))
+    assert eo <= 1e-2 and es <= 1e-3
+
+
+def test_gated_auto_picks_the_chunk_form():
+    """SWILA_ALGO_AUTO on a shape the chunk form takes gives its result exactly."""
+    import torch
+    import paper_2609_39034_amd as sw
+    B, H, T, D, J = 1, 2, 40, 64, 4
+    inp = workloads.iid_inputs(B, H, T, D, D, J, dtype="bf16", seed=775, state_std=0.1)
+    dec = _t(workloads.gated_inputs(B, H, T, D, J, dtype="bf16", seed=775)["decay"], "bf16")
+    dev = to_device(inp, "bf16")
+    oa, sa = sw.forward_gated(*(dev[n] for n in NAMES), dec, dev["state"])
+    oc, sc = sw.forward_gated(*(dev[n] for n in NAMES), dec, dev["state"], algo="chunk")
+    torch.cuda.synchronize()
+    assert torch.equal(oa, oc) and torch.equal(sa, sc)
 
 
 def test_gated_empty_sequence_copies_states():
