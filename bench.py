@@ -368,9 +368,16 @@ def bench_backward(sw, torch, dev, cfg, steps, warmup):
     }
 
 
+def gated_chunk_form(cfg):
+    """Whether SWILA_ALGO_AUTO runs the gated form in chunks on the matrix cores
+    (bf16 inputs, J <= 4, J * Dk <= 256, no temporal priors)."""
+    return cfg["dtype"] == "bf16" and cfg["J"] <= 4 and cfg["J"] * cfg["Dk"] <= 256
+
+
 def bench_gated(sw, torch, workloads, dev, cfg, seed, steps, warmup, o, s_out, tdt):
     """Gated SwiLA (App. B.4, eq. pre-decay, one gate per key dimension) on the
-    same batch: decay logits N(2, 1), through the token-by-token scan."""
+    same batch: decay logits N(2, 1), SWILA_ALGO_AUTO (the chunk form on the
+    matrix cores where it applies, else the token-by-token scan)."""
     B, H, T, Dk, Dv, J = (cfg[x] for x in ("B", "H", "T", "Dk", "Dv", "J"))
     dec = workloads.gated_inputs(B, H, T, Dk, J, dtype=cfg["dtype"], seed=seed)["decay"]
     dec = torch.from_numpy(dec).to("cuda", tdt)
@@ -399,18 +406,32 @@ def bench_gated(sw, torch, workloads, dev, cfg, seed, steps, warmup, o, s_out, t
               + eb * J * Dk * B * H * T)
     # the method's FMAs plus the decay: one multiply per state element and token
     nflop = forward_alg_flops(B, H, T, Dk, Dv, J) + J * Dk * Dv * B * H * T
+    chunk = gated_chunk_form(cfg)
+    key = workload_key("gated", B, H, T, Dk, Dv, J)
+    alu = {"bound": "alu", "achieved": nflop / kern / 1e12, "peak": PEAK_VALU_F32 / 1e12,
+           "unit": "TFLOP/s", "frac": nflop / kern / PEAK_VALU_F32,
+           "kernel_ms": kern * 1e3, "alg_flop_per_launch": nflop, "alg_bytes_per_launch": nbytes}
+    hbm = {"bound": "hbm", "achieved": nbytes / kern / 1e9, "peak": PEAK_HBM / 1e9,
+           "unit": "GB/s", "frac": nbytes / kern / PEAK_HBM, "kernel_ms": kern * 1e3,
+           "alg_bytes_per_launch": nbytes}
+    if chunk:
+        # the Dk-long products run on the matrix cores: the HBM roofline, as for
+        # the plain chunk scan, with the fp32-ALU figure beside it
+        roof = dict(hbm, kernel="scan_gated_chunk_kernel",
+                    traffic=measured_traffic("scan_gated_chunk.hip", key))
+        other = dict(alu, kernel="scan_gated_chunk_kernel")
+    else:
+        roof = dict(alu, kernel="scan_direct_kernel (gated)",
+                    traffic=measured_traffic("scan_direct_dk%d.hip" % Dk, key))
+        other = None
     return {
         "workload": "Gated SwiLA (App. B.4, pre-decay, one gate per key dim), B=%d H=%d T=%d "
-                    "Dk=Dv=%d J=%d, decay logits N(2,1), token-by-token scan"
-                    % (B, H, T, Dk, J),
-        "tokens_per_s": B * T / wall, "ms_per_step": wall * 1e3, "algo": "recurrent",
-        "roofline": {"bound": "alu", "achieved": nflop / kern / 1e12,
-                     "peak": PEAK_VALU_F32 / 1e12, "unit": "TFLOP/s",
-                     "frac": nflop / kern / PEAK_VALU_F32,
-                     "traffic": measured_traffic("scan_direct_dk%d.hip" % Dk,
-                                                 workload_key("gated", B, H, T, Dk, Dv, J)),
-                     "kernel": "scan_direct_kernel (gated)", "kernel_ms": kern * 1e3,
-                     "alg_flop_per_launch": nflop, "alg_bytes_per_launch": nbytes},
+                    "Dk=Dv=%d J=%d, decay logits N(2,1), %s"
+                    % (B, H, T, Dk, J, "chunks of 16 tokens on the matrix cores" if chunk
+                       else "token-by-token scan"),
+        "tokens_per_s": B * T / wall, "ms_per_step": wall * 1e3,
+        "algo": "chunk_exact" if chunk else "recurrent",
+        "roofline": roof, "roofline_other": other,
     }
 
 
@@ -626,6 +647,10 @@ def main():
             if c == 2 and not args.no_backward:
                 out["backward"] = bench_backward(sw, torch, dv, workloads.CONFIGS[c], args.steps,
                                                  args.warmup)
+            if c == 2 and not args.no_gated:
+                out["gated_c2"] = bench_gated(sw, torch, workloads, dv, workloads.CONFIGS[c],
+                                              1000 + c, args.steps, args.warmup, oc, sc,
+                                              torch.bfloat16)
             del dv, oc, sc
             torch.cuda.empty_cache()
             print("c%d done" % c, file=sys.stderr, flush=True)

@@ -28,10 +28,11 @@
 // chunk n, between two block barriers:
 //   phase A  sequential wave: the chunk's 16-token recurrence -> C_n
 //            tile waves: retrieval of chunk n-1 (needs C_{n-1}); Q_n S_n and
-//              QG_n; the update operand of chunk n; K_{n+1} (.) E_{n+1} and
-//              G_{n+1} for the next recurrence
+//              QG_n; the update operand of chunk n; L of chunk n+1 (wave j:
+//              component j's), K_{n+1} (.) E_{n+1} and G_{n+1} for the next
+//              recurrence
 //            helper waves: pi^q_n, the output of chunk n-2, and the inputs of
-//              chunk n+2 (HBM -> registers -> LDS, with its L)
+//              chunk n+2 (HBM -> registers -> LDS)
 //   phase B  tile waves: S_{n+1} = E_C (.) S_n + U_n^T C_n and
 //              P_{n+1} = (K_{n+1} (.) E_{n+1}) S_{n+1} for the next recurrence;
 //            sequential wave: beta, key-prior logits and v of chunk n+1.
@@ -47,6 +48,11 @@ typedef float floatx4 __attribute__((ext_vector_type(4)));
 constexpr int kGC = 16;              // tokens per chunk
 constexpr int kGH = 3;               // helper waves
 constexpr float kGramL = -40.0f;     // factorised Gram products while every L >= this
+// The sequential wave works in scaled units: with s^2 = log2(e) / 2, d = s (v - pred)
+// makes the E-step exponent log2(e) (lk - delta^2 / 2) a single fused multiply-add,
+// -d * d + log2(e) lk, and the coefficient s c = beta r d feeds s pred.
+constexpr float kS = 0.84932180028801904272f;      // sqrt(log2(e) / 2)
+constexpr float kInvS = 1.17741002251547469101f;   // 1 / kS
 constexpr int ceil_div_c(int x, int y) { return (x + y - 1) / y; }
 
 __device__ __forceinline__ floatx4 mfma16(short4v a, short4v b, floatx4 c) {
@@ -112,14 +118,15 @@ struct GSmem {
     // chunk inputs, chunk m in slot m % 3
     alignas(16) uint16_t k[3][kGC][C::KP];
     alignas(16) uint16_t q[3][kGC][C::KP];
-    alignas(16) uint16_t lb[3][kGC][C::N];   // [token][j * DB + dd]
-    alignas(16) uint16_t lk[3][kGC][C::N];
-    alignas(16) uint16_t lq[3][kGC][C::N];
-    alignas(16) uint16_t v[3][kGC][DB];
-    alignas(16) float L[3][J][kGC][C::LP];   // cumulative log gates from the chunk start
-    int fb[3];                               // the chunk's Gram products need the per-pair exponent
+    alignas(16) uint16_t lq[3][kGC][C::N];   // [token][j * DB + dd]
+    alignas(16) uint16_t g[2][kGC][J * DK];  // decay logits, chunk m in m & 1
+    alignas(16) float L[2][J][kGC][C::LP];   // cumulative log gates from the chunk start, m & 1
+    // for the sequential wave, chunk m in m & 1: {beta, log2(e) key-prior logit}
+    // [column][token] (beta = 0 past the end) and s v [dim][token]
+    alignas(16) float2 sq[2][C::N][kGC + 2];
+    alignas(16) float vs[2][DB][kGC + 4];
     alignas(16) float gt[2][J][kGC][kGC + 4];   // gt[.][j][s][t] = G_ts (t > s), chunk m in m & 1
-    alignas(16) float p[C::N][C::TP];        // chunk-start predictions [column][token]
+    alignas(16) float p[C::N][C::TP];        // chunk-start predictions, times s [column][token]
     alignas(16) float c[2][C::N][C::TP];     // coefficients [column][token], chunk m in m & 1
     float pq[2][kGC][C::NP];                 // pi^q [token][column]
     float py[2][kGC][C::NP];                 // pi^q * retrieval [token][column]
@@ -171,55 +178,94 @@ __global__ __launch_bounds__(512) void scan_gated_chunk_kernel(LayerArgs a) {
         S4 U[IT];      // update operand of chunk n: rows i = 16 it + tl, columns s = 4 lg + m
         floatx4 Y0 = floatx4{0.f, 0.f, 0.f, 0.f};   // Q S of the chunk whose retrieval is pending
         S4 QGs = zero4();                           // its tril(QG), A operand
+        float4 Er[IT];     // E of the next chunk at rows tl, key indices 16 it + 4 lg .. + 3
+        bool deep_n = false, deep_n1 = false;   // chunk n, n+1 past the factorised Gram products
 
-        // X (.) e^{sign L} of the chunk in slot s3, rows tl, key indices 16 it + 4 lg .. + 3
-        auto scaled_rows = [&](const uint16_t (*X)[C::KP], int s3, int it, float sign) {
-            const uint2 raw = *reinterpret_cast<const uint2 *>(&X[tl][16 * it + 4 * lg]);
-            const float4 l = *reinterpret_cast<const float4 *>(&sm.L[s3][tj][tl][16 * it + 4 * lg]);
-            const float f = sign * kLog2e;
-            return split4(__uint_as_float(raw.x << 16) * __builtin_amdgcn_exp2f(f * l.x),
-                          __uint_as_float(raw.x & 0xffff0000u) * __builtin_amdgcn_exp2f(f * l.y),
-                          __uint_as_float(raw.y << 16) * __builtin_amdgcn_exp2f(f * l.z),
-                          __uint_as_float(raw.y & 0xffff0000u) * __builtin_amdgcn_exp2f(f * l.w));
+        // L of chunk m for component tj from its decay logits (lane: key indices
+        // lane, lane + 64, ...); returns whether some L of the chunk is below
+        // the factorised form's range.  Written and read by this wave only.
+        auto log_gates = [&](int m) {
+            const int nt = min(kGC, T - m * kGC);
+            bool deep = false;
+#pragma unroll
+            for (int i0 = 0; i0 < DK; i0 += 64) {
+                // every lane loads its column first (idle lanes column 0), then sums
+                const int i = i0 + lane, ic = DK >= 64 || i < DK ? i : 0;
+                uint16_t x[kGC];
+#pragma unroll
+                for (int t = 0; t < kGC; ++t) x[t] = sm.g[m & 1][t][tj * DK + ic];
+                float cum = 0.0f, l[kGC];
+#pragma unroll
+                for (int t = 0; t < kGC; ++t) {
+                    // tokens past the end decay nothing: the chunk's last row is
+                    // the cumulative gate of its last token
+                    const float ls = log_sigmoid(bf(x[t]));
+                    cum += t < nt ? ls : 0.0f;
+                    l[t] = cum;
+                }
+                if (DK >= 64 || i < DK) {
+#pragma unroll
+                    for (int t = 0; t < kGC; ++t) sm.L[m & 1][tj][t][i] = l[t];
+                    deep = deep || !(cum >= kGramL);
+                }
+            }
+            return __any(deep) != 0;
         };
-        // per-pair exponent: sum_i X[t][i] K[s][i] e^{L_ti - L_si} (chunk in slot s3)
-        auto pair_dot = [&](const uint16_t (*X)[C::KP], int s3, int t, int s) {
+
+        // four bf16 of row tl of X, key indices 16 it + 4 lg .. + 3, times f
+        auto row4 = [&](const uint16_t (*X)[C::KP], int it, float4 f) {
+            const uint2 raw = *reinterpret_cast<const uint2 *>(&X[tl][16 * it + 4 * lg]);
+            return split4(__uint_as_float(raw.x << 16) * f.x,
+                          __uint_as_float(raw.x & 0xffff0000u) * f.y,
+                          __uint_as_float(raw.y << 16) * f.z,
+                          __uint_as_float(raw.y & 0xffff0000u) * f.w);
+        };
+        // e^{sign L} of chunk m at rows tl, key indices 16 it + 4 lg .. + 3
+        auto erow = [&](int m, int it, float sign) {
+            const float4 l = *reinterpret_cast<const float4 *>(&sm.L[m & 1][tj][tl][16 * it + 4 * lg]);
+            const float f = sign * kLog2e;
+            return make_float4(__builtin_amdgcn_exp2f(f * l.x), __builtin_amdgcn_exp2f(f * l.y),
+                               __builtin_amdgcn_exp2f(f * l.z), __builtin_amdgcn_exp2f(f * l.w));
+        };
+        // per-pair exponent: sum_i X[t][i] K[s][i] e^{L_ti - L_si} (chunk m)
+        auto pair_dot = [&](const uint16_t (*X)[C::KP], int m, int t, int s) {
             float acc = 0.0f;
+#pragma unroll 1
             for (int i = 0; i < DK; ++i)
-                acc = fmaf(bf(X[t][i]) * bf(sm.k[s3][s][i]),
-                           __builtin_amdgcn_exp2f(kLog2e * (sm.L[s3][tj][t][i] - sm.L[s3][tj][s][i])),
+                acc = fmaf(bf(X[t][i]) * bf(sm.k[m % 3][s][i]),
+                           __builtin_amdgcn_exp2f(kLog2e * (sm.L[m & 1][tj][t][i] - sm.L[m & 1][tj][s][i])),
                            acc);
             return acc;
         };
-        // Kp, Kinv and the Gram matrix of chunk m (for the sequential wave)
-        auto gram = [&](int m) {
+        // Kp, Kinv, E and the Gram matrix of chunk m (for the sequential wave)
+        auto gram = [&](int m, bool pair) {
             const int s3 = m % 3;
-            const bool pair = sm.fb[s3] != 0;
             floatx4 g = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int it = 0; it < IT; ++it) {
-                Kp[it] = scaled_rows(sm.k[s3], s3, it, 1.0f);
-                Kinv[it] = pair ? zero4() : scaled_rows(sm.k[s3], s3, it, -1.0f);
+                Er[it] = erow(m, it, 1.0f);
+                Kp[it] = row4(sm.k[s3], it, Er[it]);
+                Kinv[it] = pair ? zero4() : row4(sm.k[s3], it, erow(m, it, -1.0f));
                 g = mm3(Kp[it], Kinv[it], g);   // D[t = 4 lg + r][s = tl] = G_ts
             }
             if (pair) {
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
                     const int t = 4 * lg + r;
-                    g[r] = t > tl ? pair_dot(sm.k[s3], s3, t, tl) : 0.0f;
+                    g[r] = t > tl ? pair_dot(sm.k[s3], m, t, tl) : 0.0f;
                 }
             }
             *reinterpret_cast<float4 *>(&sm.gt[m & 1][tj][tl][4 * lg]) =
                 make_float4(g[0], g[1], g[2], g[3]);
         };
-        // chunk-start predictions P = Kp S for the sequential wave
+        // chunk-start predictions P = Kp S for the sequential wave, in its units
         auto predict = [&]() {
             floatx4 pacc = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int it = 0; it < IT; ++it) pacc = mm3(Kp[it], split4(W[it]), pacc);   // D[t][col]
             if (tvalid)
                 *reinterpret_cast<float4 *>(&sm.p[tcol][4 * lg]) =
-                    make_float4(pacc[0], pacc[1], pacc[2], pacc[3]);
+                    make_float4(kS * pacc[0], kS * pacc[1], kS * pacc[2], kS * pacc[3]);
         };
         // C of chunk m as the B operand: rows s = 4 lg .. + 3, column tl
         auto coeffs = [&](int m) {
@@ -237,14 +283,14 @@ __global__ __launch_bounds__(512) void scan_gated_chunk_kernel(LayerArgs a) {
                 }
             }
         };
-        // what chunk n needs besides C_n: Q_n S_n, tril(QG_n), U_n (Kinv holds chunk n's)
-        auto prepare = [&](int n) {
+        // what chunk n needs besides C_n: Q_n S_n, tril(QG_n), U_n (Kinv and Er
+        // hold chunk n's)
+        auto prepare = [&](int n, bool pair) {
             const int s3 = n % 3;
-            const bool pair = sm.fb[s3] != 0;
             floatx4 y0 = floatx4{0.f, 0.f, 0.f, 0.f}, qg = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int it = 0; it < IT; ++it) {
-                const S4 qe = scaled_rows(sm.q[s3], s3, it, 1.0f);   // rows t = tl
+                const S4 qe = row4(sm.q[s3], it, Er[it]);   // Q (.) E, rows t = tl
                 y0 = mm3(qe, split4(W[it]), y0);                      // D[t = 4 lg + r][col]
                 qg = mm3(Kinv[it], qe, qg);                           // D[s = 4 lg + r][t = tl]
             }
@@ -253,7 +299,7 @@ __global__ __launch_bounds__(512) void scan_gated_chunk_kernel(LayerArgs a) {
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const int s = 4 * lg + r;
-                if (pair) qg[r] = s <= tl ? pair_dot(sm.q[s3], s3, tl, s) : 0.0f;
+                if (pair) qg[r] = s <= tl ? pair_dot(sm.q[s3], n, tl, s) : 0.0f;
                 else if (s > tl) qg[r] = 0.0f;
             }
             QGs = split4(qg);
@@ -261,13 +307,13 @@ __global__ __launch_bounds__(512) void scan_gated_chunk_kernel(LayerArgs a) {
 #pragma unroll
             for (int it = 0; it < IT; ++it) {
                 const int i = 16 * it + tl;
-                const float lc = sm.L[s3][tj][kGC - 1][i];
+                const float lc = sm.L[n & 1][tj][kGC - 1][i];
                 float u[4];
 #pragma unroll
                 for (int m = 0; m < 4; ++m) {
                     const int s = 4 * lg + m;
                     u[m] = bf(sm.k[s3][s][i]) *
-                           __builtin_amdgcn_exp2f(kLog2e * (lc - sm.L[s3][tj][s][i]));
+                           __builtin_amdgcn_exp2f(kLog2e * (lc - sm.L[n & 1][tj][s][i]));
                 }
                 U[it] = split4(u[0], u[1], u[2], u[3]);
             }
@@ -281,23 +327,27 @@ __global__ __launch_bounds__(512) void scan_gated_chunk_kernel(LayerArgs a) {
                                ? a.state_in[(((size_t)b * H + h) * J + tj) * DK * Dv +
                                             (size_t)(16 * it + 4 * lg + r) * Dv + d0 + tl]
                                : 0.0f;
-        block_sync_lds();   // prologue 1: flags cleared
+        block_sync_lds();   // prologue 1
         block_sync_lds();   // prologue 2: chunks 0 and 1 in LDS
-        gram(0);            // Kp = K_0 (.) E_0, Kinv = K_0 (.) E_0^-1, G_0
+        deep_n = log_gates(0);
+        gram(0, deep_n);    // Kp = K_0 (.) E_0, Kinv = K_0 (.) E_0^-1, G_0
         predict();          // P_0
         block_sync_lds();   // prologue 3
         for (int n = 0; n < NCH; ++n) {
             // ---- phase A: everything that does not need C_n
             if (n >= 1) retrieve(n - 1);
-            prepare(n);
-            if (n + 1 < NCH) gram(n + 1);
+            prepare(n, deep_n);
+            if (n + 1 < NCH) {
+                deep_n1 = log_gates(n + 1);
+                gram(n + 1, deep_n1);
+            }
             block_sync_lds();   // e(n)
             // ---- phase B: S_{n+1} = E_C (.) S_n + U_n^T C_n, then P_{n+1}
             const S4 cb = coeffs(n);
 #pragma unroll
             for (int it = 0; it < IT; ++it) {
                 const float4 l4 =
-                    *reinterpret_cast<const float4 *>(&sm.L[n % 3][tj][kGC - 1][16 * it + 4 * lg]);
+                    *reinterpret_cast<const float4 *>(&sm.L[n & 1][tj][kGC - 1][16 * it + 4 * lg]);
                 W[it][0] *= __builtin_amdgcn_exp2f(kLog2e * l4.x);
                 W[it][1] *= __builtin_amdgcn_exp2f(kLog2e * l4.y);
                 W[it][2] *= __builtin_amdgcn_exp2f(kLog2e * l4.z);
@@ -305,6 +355,7 @@ __global__ __launch_bounds__(512) void scan_gated_chunk_kernel(LayerArgs a) {
                 W[it] = mm3(U[it], cb, W[it]);
             }
             if (n + 1 < NCH) predict();
+            deep_n = deep_n1;
             block_sync_lds();   // i(n+1)
         }
         retrieve(NCH - 1);
@@ -322,15 +373,22 @@ __global__ __launch_bounds__(512) void scan_gated_chunk_kernel(LayerArgs a) {
         const int sdd = lane / JP, sj = lane % JP;
         const bool sact = sdd < DB && sj < J;
         const int scol = sact ? sj * DB + sdd : 0, gj = sact ? sj : 0;
+        const bool wres = a.resp && sact;
         float sbeta[kGC], slk[kGC], sv[kGC];
-        auto seq_inputs = [&](int m) {   // beta, key-prior logits and v of chunk m
-            const int s3 = m % 3, nt = min(kGC, T - m * kGC);
+        const int vdd = sact ? sdd : 0;
+        // beta, key-prior logits and v of chunk m (idle lanes read column 0)
+        auto seq_inputs = [&](int m) {
 #pragma unroll
-            for (int t = 0; t < kGC; ++t) {
-                // tokens past the end take beta = 0: no update
-                sbeta[t] = sact && t < nt ? sigmoid(bf(sm.lb[s3][t][scol])) : 0.0f;
-                slk[t] = sact ? bf(sm.lk[s3][t][scol]) : 0.0f;
-                sv[t] = sact ? bf(sm.v[s3][t][sdd]) : 0.0f;
+            for (int t2 = 0; t2 < kGC; t2 += 2) {
+                const float4 x = *reinterpret_cast<const float4 *>(&sm.sq[m & 1][scol][t2]);
+                // idle lanes (and the padding component of J = 3) carry no mass
+                sbeta[t2] = sact ? x.x : 0.0f, slk[t2] = sact ? x.y : -INFINITY;
+                sbeta[t2 + 1] = sact ? x.z : 0.0f, slk[t2 + 1] = sact ? x.w : -INFINITY;
+            }
+#pragma unroll
+            for (int t4 = 0; t4 < kGC; t4 += 4) {
+                const float4 x = *reinterpret_cast<const float4 *>(&sm.vs[m & 1][vdd][t4]);
+                sv[t4] = x.x, sv[t4 + 1] = x.y, sv[t4 + 2] = x.z, sv[t4 + 3] = x.w;
             }
         };
         block_sync_lds();   // prologue 1
@@ -339,43 +397,119 @@ __global__ __launch_bounds__(512) void scan_gated_chunk_kernel(LayerArgs a) {
         block_sync_lds();   // prologue 3
         for (int n = 0; n < NCH; ++n) {
             const int t0 = n * kGC, nt = min(kGC, T - t0), gs = n & 1;
-            float pacc[kGC], cc[kGC];
+            // ---- the token recurrence of chunk n, in scaled units.  The softmax
+            // over j runs without subtracting its maximum: for logits and errors
+            // of ordinary size its sum z stays far inside the fp32 range.  Should
+            // z of some column and token leave [2^-100, 2^100], the chunk is run
+            // again with the maximum subtracted (the bound of the plain chunk scan).
+            float P[kGC], cc[kGC], grow[kGC];
+            auto load_pred = [&]() {
 #pragma unroll
-            for (int t4 = 0; t4 < kGC; t4 += 4) {
-                const float4 p4 = *reinterpret_cast<const float4 *>(&sm.p[scol][t4]);
-                pacc[t4] = p4.x, pacc[t4 + 1] = p4.y, pacc[t4 + 2] = p4.z, pacc[t4 + 3] = p4.w;
-            }
+                for (int t4 = 0; t4 < kGC; t4 += 4) {
+                    const float4 p4 = *reinterpret_cast<const float4 *>(&sm.p[scol][t4]);
+                    P[t4] = p4.x, P[t4 + 1] = p4.y, P[t4 + 2] = p4.z, P[t4 + 3] = p4.w;
+                }
+#pragma unroll
+                for (int u4 = 0; u4 < kGC; u4 += 4) {   // row 0 of gt: G_u0
+                    const float4 x = *reinterpret_cast<const float4 *>(&sm.gt[gs][gj][0][u4]);
+                    grow[u4] = x.x, grow[u4 + 1] = x.y, grow[u4 + 2] = x.z, grow[u4 + 3] = x.w;
+                }
+            };
+            load_pred();
+            // Software-pipelined: token t updates only P[t+1] at once; its other
+            // updates (P[u], u > t+1) run during token t+1, in the latency gaps of
+            // its chain, pinned there by scheduling barriers and empty asm.
+            float chk = 0.f, cprev = 0.f, gprev[kGC];
 #pragma unroll
             for (int t = 0; t < kGC; ++t) {
-                const float delta = sv[t] - pacc[t];
-                float r = 1.0f;
-                if constexpr (J > 1) {
-                    // eq. responsibility at the decayed state, over the J lanes of the dim
-                    const float e = sact ? slk[t] - 0.5f * delta * delta : -INFINITY;
-                    const float mx = group_max<JP>(e);
-                    const float ex = sact ? __builtin_amdgcn_exp2f(kLog2e * (e - mx)) : 0.0f;
-                    const float z = group_sum<JP>(ex);
-                    r = sact ? ex * rcp_fast(z) : 0.0f;
+                // row t+1 of gt (G_{u,t+1}) from column t+2 on, in 16-byte reads
+                float gnext[kGC];
+#pragma unroll
+                for (int q4 = (t + 2) / 4; q4 < kGC / 4; ++q4) {
+                    const float4 x = *reinterpret_cast<const float4 *>(&sm.gt[gs][gj][t + 1 < kGC ? t + 1 : t][4 * q4]);
+                    gnext[4 * q4] = x.x, gnext[4 * q4 + 1] = x.y;
+                    gnext[4 * q4 + 2] = x.z, gnext[4 * q4 + 3] = x.w;
                 }
-                const float c = sbeta[t] * r * delta;
-                cc[t] = c;
-                if (a.resp && sact && t < nt)
-                    a.resp[((((size_t)b * T + t0 + t) * H + h) * J + sj) * Dv + d0 + sdd] = r;
-                // the later tokens' predictions: pred_u += G_ut c_t (row t of gt)
+                auto defer = [&](int part) {   // c_{t-1} into P[u], u > t, in four parts
+                    if (t >= 1) {
+                        const int F = kGC - 1 - t;
+                        const int lo = t + 1 + F * part / 4, hi = t + 1 + F * (part + 1) / 4;
 #pragma unroll
-                for (int u4 = 4 * ((t + 1) / 4); u4 < kGC; u4 += 4) {
-                    const float4 g4 = *reinterpret_cast<const float4 *>(&sm.gt[gs][gj][t][u4]);
-                    const float gg[4] = {g4.x, g4.y, g4.z, g4.w};
+                        for (int u = lo; u < hi; ++u) {
+                            P[u] = fmaf(gprev[u], cprev, P[u]);
+                            asm volatile("" : "+v"(P[u]));
+                        }
+                    }
+                };
+                const float d = sv[t] - P[t];
+                const float bd = sbeta[t] * d;
+                const float ex = __builtin_amdgcn_exp2f(fmaf(-d, d, slk[t]));
+                __builtin_amdgcn_sched_barrier(0);
+                defer(0);
+                __builtin_amdgcn_sched_barrier(0);
+                float z = ex;
+                if constexpr (JP >= 2) z += dpp_mov<0xb1>(z);   // lane ^ 1
+                const float bdex = bd * ex;
+                const float gb = t + 1 < kGC ? grow[t + 1] * bdex : 0.f;
+                __builtin_amdgcn_sched_barrier(0);
+                defer(1);
+                __builtin_amdgcn_sched_barrier(0);
+                if constexpr (JP >= 4) z += dpp_mov<0x4e>(z);   // lane ^ 2
+                __builtin_amdgcn_sched_barrier(0);
+                defer(2);
+                __builtin_amdgcn_sched_barrier(0);
+                const float iz = rcp_fast(z);
+                __builtin_amdgcn_sched_barrier(0);
+                defer(3);
+                __builtin_amdgcn_sched_barrier(0);
+                if (t + 1 < kGC) P[t + 1] = fmaf(gb, iz, P[t + 1]);
+                const float cs = bdex * iz;   // s c
+                cc[t] = cs;
+                if (wres) {   // (tokens past the end stay in registers)
+                    if (t < nt)
+                        a.resp[((((size_t)b * T + t0 + t) * H + h) * J + sj) * Dv + d0 + sdd] = ex * iz;
+                }
+                chk = fmaxf(chk, fmaxf(z, iz));
+                cprev = cs;
 #pragma unroll
-                    for (int x = 0; x < 4; ++x)
-                        if (u4 + x > t) pacc[u4 + x] = fmaf(gg[x], c, pacc[u4 + x]);
+                for (int u = t + 2; u < kGC; ++u) gprev[u] = grow[u], grow[u] = gnext[u];
+            }
+            // (an integer test on bits the compiler cannot trace back to a float:
+            // a NaN, whose magnitude bits exceed those of 2^100, must fail it too)
+            uint32_t chk_bits = __float_as_uint(chk);
+            asm volatile("" : "+v"(chk_bits));
+            const bool bad = (chk_bits & 0x7fffffffu) > 0x71800000u;   // 2^100
+            if (__builtin_amdgcn_ballot_w64(sact && bad) != 0) {
+                // some softmax sum left the range: the chunk again, maximum subtracted
+                load_pred();
+#pragma unroll
+                for (int t = 0; t < kGC; ++t) {
+                    float gnext[kGC];
+#pragma unroll
+                    for (int u = t + 2; u < kGC; ++u) gnext[u] = sm.gt[gs][gj][t + 1 < kGC ? t + 1 : t][u];
+                    const float d = sv[t] - P[t];
+                    const float e = fmaf(-d, d, slk[t]);
+                    const float mx = group_max<JP>(e);
+                    const float ex = sact ? __builtin_amdgcn_exp2f(e - mx) : 0.0f;
+                    const float iz = rcp_fast(group_sum<JP>(ex));
+                    const float cs = sact ? sbeta[t] * d * ex * iz : 0.0f;
+#pragma unroll
+                    for (int u = t + 1; u < kGC; ++u) P[u] = fmaf(grow[u], cs, P[u]);
+                    cc[t] = cs;
+                    if (wres) {
+                        if (t < nt)
+                            a.resp[((((size_t)b * T + t0 + t) * H + h) * J + sj) * Dv + d0 + sdd] = ex * iz;
+                    }
+#pragma unroll
+                    for (int u = t + 2; u < kGC; ++u) grow[u] = gnext[u];
                 }
             }
             if (sact) {
 #pragma unroll
                 for (int t4 = 0; t4 < kGC; t4 += 4)
                     *reinterpret_cast<float4 *>(&sm.c[n & 1][scol][t4]) =
-                        make_float4(cc[t4], cc[t4 + 1], cc[t4 + 2], cc[t4 + 3]);
+                        make_float4(kInvS * cc[t4], kInvS * cc[t4 + 1], kInvS * cc[t4 + 2],
+                                    kInvS * cc[t4 + 3]);
             }
             block_sync_lds();   // e(n)
             if (n + 1 < NCH) seq_inputs(n + 1);
@@ -398,99 +532,102 @@ __global__ __launch_bounds__(512) void scan_gated_chunk_kernel(LayerArgs a) {
         constexpr int NKQ = ceil_div_c(kGC * DK / 8, NBT);   // uint4 of K (and of Q)
         constexpr int NLG = ceil_div_c(kGC * N / 8, NBT);    // uint4 of each logit tensor
         constexpr int NV = ceil_div_c(kGC * DB / 8, NBT);
-        constexpr int NPAIR = ceil_div_c(J * DK, NBT);       // (j, i) gate columns
-        uint4 rk[NKQ], rq[NKQ], rlb[NLG], rlk[NLG], rlq[NLG], rv[NV];
-        uint16_t rg[NPAIR][kGC];
+        constexpr int NG = ceil_div_c(kGC * J * DK / 8, NBT);   // uint4 of the decay logits
+        uint4 rk[NKQ], rq[NKQ], rlb[NLG], rlk[NLG], rlq[NLG], rv[NV], rg[NG];
+        // Every thread loads every item it owns, from a clamped row (the last
+        // token of the chunk, the last item): the loads go out back to back,
+        // with no branch each.  land() zeroes what lies past the end, a phase
+        // later, so that nothing here waits for the data.
         auto fetch = [&](int m) {
             const int t0 = m * kGC, nt = min(kGC, T - t0);
             const size_t row0 = (size_t)b * T + t0;
 #pragma unroll
             for (int x = 0; x < NKQ; ++x) {
-                const int e = bt + NBT * x, t = e / (DK / 8), p = e % (DK / 8);
-                rk[x] = rq[x] = make_uint4(0u, 0u, 0u, 0u);
-                if (e < kGC * DK / 8 && t < nt) {
-                    const size_t off = ((row0 + t) * H + h) * DK + 8 * p;
-                    rk[x] = *reinterpret_cast<const uint4 *>(Kg + off);
-                    rq[x] = *reinterpret_cast<const uint4 *>(Qg + off);
-                }
+                const int e = min(bt + NBT * x, kGC * DK / 8 - 1);
+                const int t = min(e / (DK / 8), nt - 1), p = e % (DK / 8);
+                const size_t off = ((row0 + t) * H + h) * DK + 8 * p;
+                rk[x] = *reinterpret_cast<const uint4 *>(Kg + off);
+                rq[x] = *reinterpret_cast<const uint4 *>(Qg + off);
             }
 #pragma unroll
             for (int x = 0; x < NLG; ++x) {
-                const int e = bt + NBT * x, t = e / (N / 8), rem = e % (N / 8);
+                const int e = min(bt + NBT * x, kGC * N / 8 - 1);
+                const int t = min(e / (N / 8), nt - 1), rem = e % (N / 8);
                 const int j = rem / (DB / 8), p = rem % (DB / 8);
-                rlb[x] = rlk[x] = rlq[x] = make_uint4(0u, 0u, 0u, 0u);
-                if (e < kGC * N / 8 && t < nt) {
-                    const size_t off = (((row0 + t) * H + h) * J + j) * Dv + d0 + 8 * p;
-                    rlb[x] = *reinterpret_cast<const uint4 *>(LBg + off);
-                    rlk[x] = *reinterpret_cast<const uint4 *>(LKg + off);
-                    rlq[x] = *reinterpret_cast<const uint4 *>(LQg + off);
-                }
+                const size_t off = (((row0 + t) * H + h) * J + j) * Dv + d0 + 8 * p;
+                rlb[x] = *reinterpret_cast<const uint4 *>(LBg + off);
+                rlk[x] = *reinterpret_cast<const uint4 *>(LKg + off);
+                rlq[x] = *reinterpret_cast<const uint4 *>(LQg + off);
             }
 #pragma unroll
             for (int x = 0; x < NV; ++x) {
-                const int e = bt + NBT * x, t = e / (DB / 8), p = e % (DB / 8);
-                rv[x] = make_uint4(0u, 0u, 0u, 0u);
-                if (e < kGC * DB / 8 && t < nt)
-                    rv[x] = *reinterpret_cast<const uint4 *>(Vg + ((row0 + t) * H + h) * Dv + d0 + 8 * p);
+                const int e = min(bt + NBT * x, kGC * DB / 8 - 1);
+                const int t = min(e / (DB / 8), nt - 1), p = e % (DB / 8);
+                rv[x] = *reinterpret_cast<const uint4 *>(Vg + ((row0 + t) * H + h) * Dv + d0 + 8 * p);
             }
 #pragma unroll
-            for (int x = 0; x < NPAIR; ++x) {
-                const int e = bt + NBT * x;   // (j, i) = (e / DK, e % DK)
-#pragma unroll
-                for (int t = 0; t < kGC; ++t) {
-                    rg[x][t] = 0;
-                    if (e < J * DK && t < nt) rg[x][t] = Gg[((row0 + t) * H + h) * J * DK + e];
-                }
+            for (int x = 0; x < NG; ++x) {
+                const int e = min(bt + NBT * x, kGC * J * DK / 8 - 1);
+                const int t = min(e / (J * DK / 8), nt - 1), p = e % (J * DK / 8);
+                rg[x] = *reinterpret_cast<const uint4 *>(Gg + ((row0 + t) * H + h) * J * DK + 8 * p);
             }
         };
         // chunk m's inputs to its slot, with its cumulative log gates and flag
+        const uint4 zero = make_uint4(0u, 0u, 0u, 0u);
         auto land = [&](int m) {
             const int s3 = m % 3, nt = min(kGC, T - m * kGC);
 #pragma unroll
             for (int x = 0; x < NKQ; ++x) {
                 const int e = bt + NBT * x, t = e / (DK / 8), p = e % (DK / 8);
                 if (e < kGC * DK / 8) {
-                    // two 8-byte stores: the padded rows are 8-byte aligned
+                    // rows past the end are zero; two 8-byte stores (the padded
+                    // rows are 8-byte aligned)
+                    const uint4 kk = t < nt ? rk[x] : zero, qq = t < nt ? rq[x] : zero;
                     uint2 *dk = reinterpret_cast<uint2 *>(&sm.k[s3][t][8 * p]);
                     uint2 *dq = reinterpret_cast<uint2 *>(&sm.q[s3][t][8 * p]);
-                    dk[0] = make_uint2(rk[x].x, rk[x].y);
-                    dk[1] = make_uint2(rk[x].z, rk[x].w);
-                    dq[0] = make_uint2(rq[x].x, rq[x].y);
-                    dq[1] = make_uint2(rq[x].z, rq[x].w);
+                    dk[0] = make_uint2(kk.x, kk.y);
+                    dk[1] = make_uint2(kk.z, kk.w);
+                    dq[0] = make_uint2(qq.x, qq.y);
+                    dq[1] = make_uint2(qq.z, qq.w);
                 }
             }
+            // query-prior logits to the slot; beta = sigmoid(beta logit) and the
+            // key-prior logits, and v, straight to the sequential wave's arrays
+            // (chunk m's pair of them was last read in phase B of chunk m - 3)
 #pragma unroll
             for (int x = 0; x < NLG; ++x) {
                 const int e = bt + NBT * x, t = e / (N / 8), col8 = e % (N / 8);
                 if (e < kGC * N / 8) {
-                    *reinterpret_cast<uint4 *>(&sm.lb[s3][t][8 * col8]) = rlb[x];
-                    *reinterpret_cast<uint4 *>(&sm.lk[s3][t][8 * col8]) = rlk[x];
-                    *reinterpret_cast<uint4 *>(&sm.lq[s3][t][8 * col8]) = rlq[x];
+                    const bool in = t < nt;
+                    *reinterpret_cast<uint4 *>(&sm.lq[s3][t][8 * col8]) = in ? rlq[x] : zero;
+                    const uint32_t bw[4] = {rlb[x].x, rlb[x].y, rlb[x].z, rlb[x].w};
+                    const uint32_t kw[4] = {rlk[x].x, rlk[x].y, rlk[x].z, rlk[x].w};
+#pragma unroll
+                    for (int y = 0; y < 8; ++y) {
+                        const uint16_t hb = (uint16_t)(bw[y / 2] >> (16 * (y % 2)));
+                        const uint16_t hk = (uint16_t)(kw[y / 2] >> (16 * (y % 2)));
+                        sm.sq[m & 1][8 * col8 + y][t] =
+                            make_float2(in ? sigmoid(bf(hb)) : 0.0f, in ? kLog2e * bf(hk) : 0.0f);
+                    }
                 }
             }
 #pragma unroll
             for (int x = 0; x < NV; ++x) {
                 const int e = bt + NBT * x, t = e / (DB / 8), p = e % (DB / 8);
-                if (e < kGC * DB / 8) *reinterpret_cast<uint4 *>(&sm.v[s3][t][8 * p]) = rv[x];
-            }
-            bool deep = false;
+                if (e < kGC * DB / 8) {
+                    const uint32_t vw[4] = {rv[x].x, rv[x].y, rv[x].z, rv[x].w};
 #pragma unroll
-            for (int x = 0; x < NPAIR; ++x) {
-                const int e = bt + NBT * x;
-                if (e < J * DK) {
-                    const int j = e / DK, i = e % DK;
-                    float cum = 0.0f;
-#pragma unroll
-                    for (int t = 0; t < kGC; ++t) {
-                        // tokens past the end decay nothing: the chunk's last row
-                        // is the cumulative gate of its last token
-                        if (t < nt) cum += log_sigmoid(bf(rg[x][t]));
-                        sm.L[s3][j][t][i] = cum;
-                    }
-                    deep = deep || !(cum >= kGramL);
+                    for (int y = 0; y < 8; ++y)
+                        sm.vs[m & 1][8 * p + y][t] =
+                            t < nt ? kS * bf((uint16_t)(vw[y / 2] >> (16 * (y % 2)))) : 0.0f;
                 }
             }
-            if (deep) sm.fb[s3] = 1;
+#pragma unroll
+            for (int x = 0; x < NG; ++x) {
+                const int e = bt + NBT * x, t = e / (J * DK / 8), p = e % (J * DK / 8);
+                if (e < kGC * J * DK / 8)
+                    *reinterpret_cast<uint4 *>(&sm.g[m & 1][t][8 * p]) = t < nt ? rg[x] : zero;
+            }
         };
         // pi^q of chunk m: softmax over j of the query-prior logits, per (t, dd)
         auto priors = [&](int m) {
@@ -526,7 +663,6 @@ __global__ __launch_bounds__(512) void scan_gated_chunk_kernel(LayerArgs a) {
             }
         };
 
-        if (bt < 3) sm.fb[bt] = 0;
         block_sync_lds();   // prologue 1
         fetch(0);
         land(0);
@@ -540,13 +676,11 @@ __global__ __launch_bounds__(512) void scan_gated_chunk_kernel(LayerArgs a) {
         for (int n = 0; n < NCH; ++n) {
             priors(n);
             if (n >= 2) output(n - 2);
-            // chunk n + 2 lands in the slot of chunk n - 1 (its flag cleared in
-            // phase B of chunk n - 1)
+            // chunk n + 2 lands in the slots of chunk n - 1 (its decay logits in
+            // those of chunk n, which the tile waves turned into L last phase)
             if (n + 2 < NCH) land(n + 2);
             block_sync_lds();   // e(n)
             if (n + 3 < NCH) fetch(n + 3);
-            // chunk n's slot is free after this phase: chunk n + 3 lands there next
-            if (bt == 0) sm.fb[n % 3] = 0;
             block_sync_lds();   // i(n+1)
         }
         if (NCH >= 2) output(NCH - 2);
