@@ -42,19 +42,21 @@ PEAK_MFMA_BF16 = 2.5e15    # FLOP/s, MI355X dense bf16 matrix
 # source, the workload it ran and the digest of the source at measurement.
 MEASURED_TRAFFIC = {
     ("scan_pipe.hip", "forward B=8 H=16 T=4096 Dk=Dv=128 J=4",
-     "0411c48d19a00b1068fdc899c3b9b2ce423de766c4002d1ad8a0be4831095816"): 2187420876,
+     "6fc333fc19bb03e99649a170bb3cd97a9e6defdfb8a4d7f4e5967378ea424437"): 2189939206,
     ("scan_pipe.hip", "forward B=4 H=8 T=2048 Dk=Dv=64 J=4",
-     "0411c48d19a00b1068fdc899c3b9b2ce423de766c4002d1ad8a0be4831095816"): 136691844,
+     "6fc333fc19bb03e99649a170bb3cd97a9e6defdfb8a4d7f4e5967378ea424437"): 136863294,
     ("scan_pipe.hip", "forward B=2 H=8 T=16384 Dk=Dv=128 J=8",
-     "0411c48d19a00b1068fdc899c3b9b2ce423de766c4002d1ad8a0be4831095816"): 2354048188,
+     "6fc333fc19bb03e99649a170bb3cd97a9e6defdfb8a4d7f4e5967378ea424437"): 2534394415,
     ("scan_pipe_temporal.hip", "temporal B=8 H=16 T=4096 Dk=Dv=128 J=4",
-     "552bf36e40f3d9d5960c872b5f0f758278e26b89c6a3236891f32c1d39bfd6b1"): 2450490466,
+     "cccc3565bc93a77d940c00ec22e392f9d5416ecb56469aaedb8c4fd185fdd548"): 2450704072,
     ("scan_direct_dk128.hip", "gated B=8 H=16 T=4096 Dk=Dv=128 J=4",
-     "b427757a58067e7408bd320e9708cb725b13ca36c35cdc60190f7ba3a750d634"): 2718133297,
+     "39988c61ffdc92c542a18091834b55f6a71977a11a0302fd3f9580181595ad2b"): 2718134140,
     ("scan_direct_dk16.hip", "forward B=1 H=1 T=64 Dk=Dv=16 J=2",
-     "b1e50e81270777e46233ef0e983e3dfc6e99576676c141d880e2b428bc014b9c"): 67711,
+     "11dc94a786728640b929d058f8600bf4e3c032bd82c288ad3136a45bdd77cb84"): 67583,
     ("decode.hip", "decode B=256 H=16 Dk=Dv=128 J=4",
-     "9780a8085553bafe2ac41143998e6a3b95f3a2e33aa73ea5db1f5adc0e87c8a6"): 2165846719,
+     "885219bbb8497010b554af973a0d14b02c80037d8cb73ffd4fa2afb165c828d7"): 2165212629,
+    ("scan_gated_chunk.hip", "gated B=4 H=8 T=2048 Dk=Dv=64 J=4",
+     "facc5a996b3a946a524b86831f86bc7f517c8906e403536001a496d93ad0d4d6"): 179186388,
 }
 
 
