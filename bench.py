@@ -196,9 +196,10 @@ def bench_newton(sw, torch, dev, cfg, steps, warmup, o, s_out, tol, unnormalized
                               clamp=clamp)
     sweeps, unconverged = (int(x) for x in it.cpu())
     nflop = newton_alg_flops(B, H, T, Dk, Dv, J, sweeps)
-    form = ("App. D.2's unnormalised-responsibility variant (exact Jacobian)" if unnormalized
+    form = ("App. D.2's unnormalised-responsibility variant" if unnormalized
             else "App. D chunkwise quasi-Newton")
-    jac = "g clamped to [0, 2/|k|^2]" if clamp else "g unclamped"
+    jac = ("g clamped to [0, 2/|k|^2]" if clamp
+           else "g unclamped (the exact Jacobian: Newton's method proper)")
     return {
         "workload": "%s, %s, bf16 inputs, tol %g (relative change of the predictions), %s"
                     % (form, batch, tol, jac),
