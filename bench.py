@@ -373,8 +373,8 @@ def bench_backward(sw, torch, dev, cfg, steps, warmup):
 
 def gated_chunk_form(cfg):
     """Whether SWILA_ALGO_AUTO runs the gated form in chunks on the matrix cores
-    (bf16 inputs, J <= 4, J * Dk <= 256, no temporal priors)."""
-    return cfg["dtype"] == "bf16" and cfg["J"] <= 4 and cfg["J"] * cfg["Dk"] <= 256
+    (bf16 inputs, J <= 4, J * Dk <= 512, no temporal priors)."""
+    return cfg["dtype"] == "bf16" and cfg["J"] <= 4 and cfg["J"] * cfg["Dk"] <= 512
 
 
 def bench_gated(sw, torch, workloads, dev, cfg, seed, steps, warmup, o, s_out, tdt):

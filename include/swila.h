@@ -44,7 +44,7 @@
  *     the chunked forms (SWILA_ALGO_CHUNK_EXACT, SWILA_ALGO_NEWTON) and the
  *     backward pass take J <= 8 (SWILA_ALGO_AUTO then picks the token-by-token
  *     scan), and the gated forward takes J * Dk <= 1024 (its chunked form
- *     J <= 4 and J * Dk <= 256; see swila_forward_gated).
+ *     J <= 4 and J * Dk <= 512; see swila_forward_gated).
  */
 #ifndef SWILA_H
 #define SWILA_H
@@ -283,7 +283,7 @@ typedef struct swila_gated {
  *   SWILA_ALGO_CHUNK_EXACT: the same recurrence 16 tokens at a time on the
  *     matrix cores (App. B.4 with the chunk algebra of the plain form; exact
  *     up to rounding order).  It takes bf16 inputs, no temporal priors,
- *     J <= 4 and J * Dk <= 256; other calls return SWILA_EUNSUPPORTED.
+ *     J <= 4 and J * Dk <= 512; other calls return SWILA_EUNSUPPORTED.
  *   SWILA_ALGO_RECURRENT: the token-by-token scan (either input dtype, with
  *     or without temporal priors, J * Dk <= 1024).
  *   SWILA_ALGO_AUTO: CHUNK_EXACT where it applies, else RECURRENT.

@@ -13,29 +13,33 @@
 //   q_t.w_t = (q_t (.) E_t) . S + sum_{s<=t} QG_ts c_s, QG_ts = sum_i q_ti k_si e^{L_ti - L_si}
 //   S'      = E_C (.) S + sum_s (k_s (.) E_C / E_s) c_s.
 // G and QG are formed as (K (.) E)(K (.) E^-1)^T on the matrix cores while
-// every e^{-L} stays below e^{40}; a chunk whose gates decay further (some
-// L_C < -40) forms them with the per-pair exponent instead.  The scaled
-// operands are fp32: each is split into a bf16 high part and a bf16 residual,
-// and the hi*hi + hi*lo + lo*hi products are summed (about 2^-16 relative per
-// product, fp32 accumulation).  A component's gates differ from the others',
-// so each component has its own Gram matrices and scaled operands: tile wave
-// j holds the state columns of component j.
+// every E^-1 stays below e^{40}.  E^-1 is the running product of 1 + e^{-x}
+// over the chunk's decay logits x (1 / sigmoid), one exponential per element,
+// and E its reciprocal; a chunk whose gates decay further (some E^-1_C above
+// e^{40}) forms its cumulative log gates L instead and the Gram products with
+// the per-pair exponent.  The scaled operands are fp32: each is split into a
+// bf16 high part and a bf16 residual, and the hi*hi + hi*lo + lo*hi products
+// are summed (about 2^-16 relative per product, fp32 accumulation).  A
+// component's gates differ from the others', so each component has its own
+// Gram matrices and scaled operands: tile wave j holds the state columns of
+// component j.
 //
 // Block = one head (b, h) and DB output dims with all J components (J <= 4,
-// J * Dk <= 256): J tile waves (wave j: the Dk x DB state tile of component j
+// J * Dk <= 512): J tile waves (wave j: the Dk x DB state tile of component j
 // in accumulator registers), one sequential wave (one lane per column, the J
 // components of an output dim in adjacent lanes), three helper waves.  Per
 // chunk n, between two block barriers:
 //   phase A  sequential wave: the chunk's 16-token recurrence -> C_n
 //            tile waves: retrieval of chunk n-1 (needs C_{n-1}); Q_n S_n and
-//              QG_n; the update operand of chunk n; L of chunk n+1 (wave j:
-//              component j's), K_{n+1} (.) E_{n+1} and G_{n+1} for the next
-//              recurrence
+//              the update operand of chunk n; E^-1 of chunk n+1 (wave j:
+//              component j's), K_{n+1} (.) E_{n+1}, Q_{n+1} (.) E_{n+1},
+//              G_{n+1} for the next recurrence and QG_{n+1}
 //            helper waves: pi^q_n, the output of chunk n-2, and the inputs of
-//              chunk n+2 (HBM -> registers -> LDS)
+//              chunk n+2 but its decay logits (HBM -> registers -> LDS)
 //   phase B  tile waves: S_{n+1} = E_C (.) S_n + U_n^T C_n and
 //              P_{n+1} = (K_{n+1} (.) E_{n+1}) S_{n+1} for the next recurrence;
-//            sequential wave: beta, key-prior logits and v of chunk n+1.
+//            sequential wave: beta, key-prior logits and v of chunk n+1;
+//            helper waves: the decay logits of chunk n+2, the loads of n+3.
 #include "device_common.hpp"
 #include "launch.hpp"
 
@@ -47,7 +51,7 @@ typedef float floatx4 __attribute__((ext_vector_type(4)));
 
 constexpr int kGC = 16;              // tokens per chunk
 constexpr int kGH = 3;               // helper waves
-constexpr float kGramL = -40.0f;     // factorised Gram products while every L >= this
+constexpr float kGramEinv = 2.35385266837019985e17f;   // e^40: factorised Gram products while every E^-1 <= this
 // The sequential wave works in scaled units: with s^2 = log2(e) / 2, d = s (v - pred)
 // makes the E-step exponent log2(e) (lk - delta^2 / 2) a single fused multiply-add,
 // -d * d + log2(e) lk, and the coefficient s c = beta r d feeds s pred.
@@ -104,10 +108,10 @@ struct GCfg {
     static constexpr int JP = J == 3 ? 4 : J;
     static constexpr int NWAVE = J + 1 + kGH;
     static constexpr int KP = DK + 4;        // bf16 row pitch of the K, Q tiles
-    static constexpr int LP = DK + 4;        // fp32 row pitch of L
+    static constexpr int LP = DK + 4;        // fp32 row pitch of E^-1 (or L)
     static constexpr int TP = kGC + 4;       // [column][token] row pitch
     static constexpr int NP = N + 4;         // [token][column] row pitch
-    static_assert(J >= 1 && J <= 4 && J * DK <= 256, "LDS budget of the gated chunk form");
+    static_assert(J >= 1 && J <= 4 && J * DK <= 512, "LDS budget of the gated chunk form");
     static_assert(DB == 8 || DB == 16, "column block");
     static_assert(DB * JP <= 64, "one sequential wave");
 };
@@ -119,8 +123,11 @@ struct GSmem {
     alignas(16) uint16_t k[3][kGC][C::KP];
     alignas(16) uint16_t q[3][kGC][C::KP];
     alignas(16) uint16_t lq[3][kGC][C::N];   // [token][j * DB + dd]
-    alignas(16) uint16_t g[2][kGC][J * DK];  // decay logits, chunk m in m & 1
-    alignas(16) float L[2][J][kGC][C::LP];   // cumulative log gates from the chunk start, m & 1
+    alignas(16) uint16_t g[kGC][J * DK];     // decay logits of the next chunk to take its gates
+    // E^-1 of chunk m (its cumulative log gates L in a deep chunk), written and
+    // read by tile wave j only; E_C, chunk m in m & 1
+    alignas(16) float ei[J][kGC][C::LP];
+    alignas(16) float ec[2][J][DK];
     // for the sequential wave, chunk m in m & 1: {beta, log2(e) key-prior logit}
     // [column][token] (beta = 0 past the end) and s v [dim][token]
     alignas(16) float2 sq[2][C::N][kGC + 2];
@@ -148,7 +155,7 @@ __device__ __forceinline__ void gated_coords(int id, int ndb, int nheads, int &d
 
 // Each role runs its whole chunk loop in a branch of its own, so that the
 // registers one role keeps across chunks are not held by the others; every
-// role meets the same block barriers in the same order: three in the prologue,
+// role meets the same block barriers in the same order: four in the prologue,
 // two per chunk (e(n): C_n and chunk n + 2 published; i(n+1): P_{n+1}
 // published), one in the epilogue.
 template <int DK, int J, int DB>
@@ -172,44 +179,61 @@ __global__ __launch_bounds__(512) void scan_gated_chunk_kernel(LayerArgs a) {
         const int tj = w;
         const bool tvalid = tl < DB;
         const int tcol = tj * DB + (tvalid ? tl : 0);
+        float (*const EI)[C::LP] = sm.ei[tj];
         floatx4 W[IT];
-        S4 Kp[IT];     // K_{m} (.) E_{m} for the next chunk m, A operand (rows t = tl)
-        S4 Kinv[IT];   // K_m (.) E_m^-1 (rows s = tl): B operand of G_m, A operand of QG_m
-        S4 U[IT];      // update operand of chunk n: rows i = 16 it + tl, columns s = 4 lg + m
+        S4 Kp[IT];   // K_m (.) E_m for the next chunk m, A operand (rows t = tl)
+        S4 Qe[IT];   // Q_m (.) E_m of the next chunk whose Q S is pending (rows t = tl)
+        S4 U[IT];    // update operand of chunk n: rows i = 16 it + tl, columns s = 4 lg + m
         floatx4 Y0 = floatx4{0.f, 0.f, 0.f, 0.f};   // Q S of the chunk whose retrieval is pending
-        S4 QGs = zero4();                           // its tril(QG), A operand
-        float4 Er[IT];     // E of the next chunk at rows tl, key indices 16 it + 4 lg .. + 3
+        S4 QGr = zero4();   // its tril(QG), A operand
+        S4 QGq = zero4();   // tril(QG) of the chunk after it
         bool deep_n = false, deep_n1 = false;   // chunk n, n+1 past the factorised Gram products
 
-        // L of chunk m for component tj from its decay logits (lane: key indices
-        // lane, lane + 64, ...); returns whether some L of the chunk is below
-        // the factorised form's range.  Written and read by this wave only.
+        // E^-1 (or, in a deep chunk, L) and E_C of chunk m for component tj from
+        // its decay logits (lane: key indices lane, lane + 64, ...); returns
+        // whether the chunk is deep.
         auto log_gates = [&](int m) {
             const int nt = min(kGC, T - m * kGC);
             bool deep = false;
 #pragma unroll
             for (int i0 = 0; i0 < DK; i0 += 64) {
-                // every lane loads its column first (idle lanes column 0), then sums
+                // every lane loads its column first (idle lanes column 0), then multiplies
                 const int i = i0 + lane, ic = DK >= 64 || i < DK ? i : 0;
-                uint16_t x[kGC];
+                float x[kGC];
 #pragma unroll
-                for (int t = 0; t < kGC; ++t) x[t] = sm.g[m & 1][t][tj * DK + ic];
-                float cum = 0.0f, l[kGC];
+                for (int t = 0; t < kGC; ++t) x[t] = bf(sm.g[t][tj * DK + ic]);
+                // tokens past the end decay nothing: the chunk's last row is the
+                // product over its last token
+                float cum = 1.0f, e[kGC];
 #pragma unroll
                 for (int t = 0; t < kGC; ++t) {
-                    // tokens past the end decay nothing: the chunk's last row is
-                    // the cumulative gate of its last token
-                    const float ls = log_sigmoid(bf(x[t]));
-                    cum += t < nt ? ls : 0.0f;
-                    l[t] = cum;
+                    const float f = 1.0f + __builtin_amdgcn_exp2f(-kLog2e * x[t]);
+                    cum *= t < nt ? f : 1.0f;
+                    e[t] = cum;
                 }
                 if (DK >= 64 || i < DK) {
 #pragma unroll
-                    for (int t = 0; t < kGC; ++t) sm.L[m & 1][tj][t][i] = l[t];
-                    deep = deep || !(cum >= kGramL);
+                    for (int t = 0; t < kGC; ++t) EI[t][i] = e[t];
+                    sm.ec[m & 1][tj][i] = rcp_fast(cum);
+                    deep = deep || !(cum <= kGramEinv);
                 }
             }
-            return __any(deep) != 0;
+            if (__any(deep) == 0) return false;
+            // deep chunk: L = the running sum of log sigmoid, in place of E^-1
+#pragma unroll
+            for (int i0 = 0; i0 < DK; i0 += 64) {
+                const int i = i0 + lane;
+                if (DK >= 64 || i < DK) {
+                    float cum = 0.0f;
+#pragma unroll
+                    for (int t = 0; t < kGC; ++t) {
+                        cum += t < nt ? log_sigmoid(bf(sm.g[t][tj * DK + i])) : 0.0f;
+                        EI[t][i] = cum;
+                    }
+                    sm.ec[m & 1][tj][i] = __builtin_amdgcn_exp2f(kLog2e * cum);
+                }
+            }
+            return true;
         };
 
         // four bf16 of row tl of X, key indices 16 it + 4 lg .. + 3, times f
@@ -220,43 +244,54 @@ __global__ __launch_bounds__(512) void scan_gated_chunk_kernel(LayerArgs a) {
                           __uint_as_float(raw.y << 16) * f.z,
                           __uint_as_float(raw.y & 0xffff0000u) * f.w);
         };
-        // e^{sign L} of chunk m at rows tl, key indices 16 it + 4 lg .. + 3
-        auto erow = [&](int m, int it, float sign) {
-            const float4 l = *reinterpret_cast<const float4 *>(&sm.L[m & 1][tj][tl][16 * it + 4 * lg]);
-            const float f = sign * kLog2e;
-            return make_float4(__builtin_amdgcn_exp2f(f * l.x), __builtin_amdgcn_exp2f(f * l.y),
-                               __builtin_amdgcn_exp2f(f * l.z), __builtin_amdgcn_exp2f(f * l.w));
-        };
-        // per-pair exponent: sum_i X[t][i] K[s][i] e^{L_ti - L_si} (chunk m)
+        // per-pair exponent (deep chunk m, L in EI): sum_i X[t][i] K[s][i] e^{L_ti - L_si}
         auto pair_dot = [&](const uint16_t (*X)[C::KP], int m, int t, int s) {
             float acc = 0.0f;
 #pragma unroll 1
             for (int i = 0; i < DK; ++i)
                 acc = fmaf(bf(X[t][i]) * bf(sm.k[m % 3][s][i]),
-                           __builtin_amdgcn_exp2f(kLog2e * (sm.L[m & 1][tj][t][i] - sm.L[m & 1][tj][s][i])),
-                           acc);
+                           __builtin_amdgcn_exp2f(kLog2e * (EI[t][i] - EI[s][i])), acc);
             return acc;
         };
-        // Kp, Kinv, E and the Gram matrix of chunk m (for the sequential wave)
+        // the operands of chunk m: Kp, Qe, G_m (for the sequential wave) and QG_m
         auto gram = [&](int m, bool pair) {
             const int s3 = m % 3;
-            floatx4 g = floatx4{0.f, 0.f, 0.f, 0.f};
+            floatx4 g = floatx4{0.f, 0.f, 0.f, 0.f}, qg = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int it = 0; it < IT; ++it) {
-                Er[it] = erow(m, it, 1.0f);
-                Kp[it] = row4(sm.k[s3], it, Er[it]);
-                Kinv[it] = pair ? zero4() : row4(sm.k[s3], it, erow(m, it, -1.0f));
-                g = mm3(Kp[it], Kinv[it], g);   // D[t = 4 lg + r][s = tl] = G_ts
+                const float4 x = *reinterpret_cast<const float4 *>(&EI[tl][16 * it + 4 * lg]);
+                float4 er;   // E at rows tl, key indices 16 it + 4 lg .. + 3
+                if (pair) {
+                    er = make_float4(__builtin_amdgcn_exp2f(kLog2e * x.x),
+                                     __builtin_amdgcn_exp2f(kLog2e * x.y),
+                                     __builtin_amdgcn_exp2f(kLog2e * x.z),
+                                     __builtin_amdgcn_exp2f(kLog2e * x.w));
+                } else {
+                    er = make_float4(rcp_fast(x.x), rcp_fast(x.y), rcp_fast(x.z), rcp_fast(x.w));
+                }
+                Kp[it] = row4(sm.k[s3], it, er);
+                Qe[it] = row4(sm.q[s3], it, er);
+                if (!pair) {
+                    const S4 kinv = row4(sm.k[s3], it, x);   // K (.) E^-1, rows s = tl
+                    g = mm3(Kp[it], kinv, g);      // D[t = 4 lg + r][s = tl] = G_ts
+                    qg = mm3(kinv, Qe[it], qg);    // D[s = 4 lg + r][t = tl] = QG_ts
+                }
             }
-            if (pair) {
+            // lane (tl, lg) holds QG[t = tl][s = 4 lg + r]: the A operand of the retrieval
 #pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int t = 4 * lg + r;
+            for (int r = 0; r < 4; ++r) {
+                const int t = 4 * lg + r;   // row of G
+                const int s = 4 * lg + r;   // column of QG
+                if (pair) {
                     g[r] = t > tl ? pair_dot(sm.k[s3], m, t, tl) : 0.0f;
+                    qg[r] = s <= tl ? pair_dot(sm.q[s3], m, tl, s) : 0.0f;
+                } else if (s > tl) {
+                    qg[r] = 0.0f;
                 }
             }
             *reinterpret_cast<float4 *>(&sm.gt[m & 1][tj][tl][4 * lg]) =
                 make_float4(g[0], g[1], g[2], g[3]);
+            QGq = split4(qg);
         };
         // chunk-start predictions P = Kp S for the sequential wave, in its units
         auto predict = [&]() {
@@ -274,7 +309,7 @@ __global__ __launch_bounds__(512) void scan_gated_chunk_kernel(LayerArgs a) {
         };
         // retrieval of chunk m: Y = Y0 + tril(QG) C, times pi^q, to py
         auto retrieve = [&](int m) {
-            const floatx4 y = mm3(QGs, coeffs(m), Y0);   // D[t = 4 lg + r][col]
+            const floatx4 y = mm3(QGr, coeffs(m), Y0);   // D[t = 4 lg + r][col]
             if (tvalid) {
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
@@ -283,37 +318,34 @@ __global__ __launch_bounds__(512) void scan_gated_chunk_kernel(LayerArgs a) {
                 }
             }
         };
-        // what chunk n needs besides C_n: Q_n S_n, tril(QG_n), U_n (Kinv and Er
-        // hold chunk n's)
+        // what chunk n needs besides C_n: Q_n S_n and U_n (Qe, QGq and EI hold
+        // chunk n's)
         auto prepare = [&](int n, bool pair) {
             const int s3 = n % 3;
-            floatx4 y0 = floatx4{0.f, 0.f, 0.f, 0.f}, qg = floatx4{0.f, 0.f, 0.f, 0.f};
+            floatx4 y0 = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int it = 0; it < IT; ++it) {
-                const S4 qe = row4(sm.q[s3], it, Er[it]);   // Q (.) E, rows t = tl
-                y0 = mm3(qe, split4(W[it]), y0);                      // D[t = 4 lg + r][col]
-                qg = mm3(Kinv[it], qe, qg);                           // D[s = 4 lg + r][t = tl]
-            }
+            for (int it = 0; it < IT; ++it) y0 = mm3(Qe[it], split4(W[it]), y0);   // D[t][col]
             Y0 = y0;
-            // lane (t = tl, lg) holds QG[t][s = 4 lg + r]: the A operand of the retrieval
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int s = 4 * lg + r;
-                if (pair) qg[r] = s <= tl ? pair_dot(sm.q[s3], n, tl, s) : 0.0f;
-                else if (s > tl) qg[r] = 0.0f;
-            }
-            QGs = split4(qg);
-            // U[i][s] = K[s][i] e^{L_C,i - L_s,i}, i = 16 it + tl, s = 4 lg + m
+            QGr = QGq;
+            // U[i][s] = K[s][i] E_C,i / E_s,i, i = 16 it + tl, s = 4 lg + m
 #pragma unroll
             for (int it = 0; it < IT; ++it) {
                 const int i = 16 * it + tl;
-                const float lc = sm.L[n & 1][tj][kGC - 1][i];
                 float u[4];
+                if (pair) {
+                    const float lc = EI[kGC - 1][i];
 #pragma unroll
-                for (int m = 0; m < 4; ++m) {
-                    const int s = 4 * lg + m;
-                    u[m] = bf(sm.k[s3][s][i]) *
-                           __builtin_amdgcn_exp2f(kLog2e * (lc - sm.L[n & 1][tj][s][i]));
+                    for (int m = 0; m < 4; ++m) {
+                        const int s = 4 * lg + m;
+                        u[m] = bf(sm.k[s3][s][i]) * __builtin_amdgcn_exp2f(kLog2e * (lc - EI[s][i]));
+                    }
+                } else {
+                    const float ecv = sm.ec[n & 1][tj][i];
+#pragma unroll
+                    for (int m = 0; m < 4; ++m) {
+                        const int s = 4 * lg + m;
+                        u[m] = bf(sm.k[s3][s][i]) * (ecv * EI[s][i]);
+                    }
                 }
                 U[it] = split4(u[0], u[1], u[2], u[3]);
             }
@@ -328,11 +360,12 @@ __global__ __launch_bounds__(512) void scan_gated_chunk_kernel(LayerArgs a) {
                                             (size_t)(16 * it + 4 * lg + r) * Dv + d0 + tl]
                                : 0.0f;
         block_sync_lds();   // prologue 1
-        block_sync_lds();   // prologue 2: chunks 0 and 1 in LDS
+        block_sync_lds();   // prologue 2: chunks 0 and 1 in LDS (the decay logits of 0)
         deep_n = log_gates(0);
-        gram(0, deep_n);    // Kp = K_0 (.) E_0, Kinv = K_0 (.) E_0^-1, G_0
+        gram(0, deep_n);
         predict();          // P_0
-        block_sync_lds();   // prologue 3
+        block_sync_lds();   // prologue 3: the decay logits of chunk 0 read
+        block_sync_lds();   // prologue 4: those of chunk 1 in LDS
         for (int n = 0; n < NCH; ++n) {
             // ---- phase A: everything that does not need C_n
             if (n >= 1) retrieve(n - 1);
@@ -346,12 +379,11 @@ __global__ __launch_bounds__(512) void scan_gated_chunk_kernel(LayerArgs a) {
             const S4 cb = coeffs(n);
 #pragma unroll
             for (int it = 0; it < IT; ++it) {
-                const float4 l4 =
-                    *reinterpret_cast<const float4 *>(&sm.L[n & 1][tj][kGC - 1][16 * it + 4 * lg]);
-                W[it][0] *= __builtin_amdgcn_exp2f(kLog2e * l4.x);
-                W[it][1] *= __builtin_amdgcn_exp2f(kLog2e * l4.y);
-                W[it][2] *= __builtin_amdgcn_exp2f(kLog2e * l4.z);
-                W[it][3] *= __builtin_amdgcn_exp2f(kLog2e * l4.w);
+                const float4 e4 = *reinterpret_cast<const float4 *>(&sm.ec[n & 1][tj][16 * it + 4 * lg]);
+                W[it][0] *= e4.x;
+                W[it][1] *= e4.y;
+                W[it][2] *= e4.z;
+                W[it][3] *= e4.w;
                 W[it] = mm3(U[it], cb, W[it]);
             }
             if (n + 1 < NCH) predict();
@@ -395,6 +427,7 @@ __global__ __launch_bounds__(512) void scan_gated_chunk_kernel(LayerArgs a) {
         block_sync_lds();   // prologue 2
         seq_inputs(0);
         block_sync_lds();   // prologue 3
+        block_sync_lds();   // prologue 4
         for (int n = 0; n < NCH; ++n) {
             const int t0 = n * kGC, nt = min(kGC, T - t0), gs = n & 1;
             // ---- the token recurrence of chunk n, in scaled units.  The softmax
@@ -572,8 +605,13 @@ __global__ __launch_bounds__(512) void scan_gated_chunk_kernel(LayerArgs a) {
                 rg[x] = *reinterpret_cast<const uint4 *>(Gg + ((row0 + t) * H + h) * J * DK + 8 * p);
             }
         };
-        // chunk m's inputs to its slot, with its cumulative log gates and flag
-        const uint4 zero = make_uint4(0u, 0u, 0u, 0u);
+        // r, or zero when !keep (a mask: a select of the whole vector would be
+        // made on addresses and put the registers in scratch memory)
+        auto mask4 = [](const uint4 &r, bool keep) {
+            const uint32_t m = keep ? 0xffffffffu : 0u;
+            return make_uint4(r.x & m, r.y & m, r.z & m, r.w & m);
+        };
+        // chunk m's inputs but its decay logits to its slot
         auto land = [&](int m) {
             const int s3 = m % 3, nt = min(kGC, T - m * kGC);
 #pragma unroll
@@ -582,7 +620,7 @@ __global__ __launch_bounds__(512) void scan_gated_chunk_kernel(LayerArgs a) {
                 if (e < kGC * DK / 8) {
                     // rows past the end are zero; two 8-byte stores (the padded
                     // rows are 8-byte aligned)
-                    const uint4 kk = t < nt ? rk[x] : zero, qq = t < nt ? rq[x] : zero;
+                    const uint4 kk = mask4(rk[x], t < nt), qq = mask4(rq[x], t < nt);
                     uint2 *dk = reinterpret_cast<uint2 *>(&sm.k[s3][t][8 * p]);
                     uint2 *dq = reinterpret_cast<uint2 *>(&sm.q[s3][t][8 * p]);
                     dk[0] = make_uint2(kk.x, kk.y);
@@ -599,7 +637,7 @@ __global__ __launch_bounds__(512) void scan_gated_chunk_kernel(LayerArgs a) {
                 const int e = bt + NBT * x, t = e / (N / 8), col8 = e % (N / 8);
                 if (e < kGC * N / 8) {
                     const bool in = t < nt;
-                    *reinterpret_cast<uint4 *>(&sm.lq[s3][t][8 * col8]) = in ? rlq[x] : zero;
+                    *reinterpret_cast<uint4 *>(&sm.lq[s3][t][8 * col8]) = mask4(rlq[x], in);
                     const uint32_t bw[4] = {rlb[x].x, rlb[x].y, rlb[x].z, rlb[x].w};
                     const uint32_t kw[4] = {rlk[x].x, rlk[x].y, rlk[x].z, rlk[x].w};
 #pragma unroll
@@ -622,11 +660,15 @@ __global__ __launch_bounds__(512) void scan_gated_chunk_kernel(LayerArgs a) {
                             t < nt ? kS * bf((uint16_t)(vw[y / 2] >> (16 * (y % 2)))) : 0.0f;
                 }
             }
+        };
+        // chunk m's decay logits, once the tile waves have taken chunk m - 1's
+        auto land_g = [&](int m) {
+            const int nt = min(kGC, T - m * kGC);
 #pragma unroll
             for (int x = 0; x < NG; ++x) {
                 const int e = bt + NBT * x, t = e / (J * DK / 8), p = e % (J * DK / 8);
                 if (e < kGC * J * DK / 8)
-                    *reinterpret_cast<uint4 *>(&sm.g[m & 1][t][8 * p]) = t < nt ? rg[x] : zero;
+                    *reinterpret_cast<uint4 *>(&sm.g[t][8 * p]) = mask4(rg[x], t < nt);
             }
         };
         // pi^q of chunk m: softmax over j of the query-prior logits, per (t, dd)
@@ -666,20 +708,24 @@ __global__ __launch_bounds__(512) void scan_gated_chunk_kernel(LayerArgs a) {
         block_sync_lds();   // prologue 1
         fetch(0);
         land(0);
+        land_g(0);
         if (NCH > 1) {
             fetch(1);
             land(1);
         }
         block_sync_lds();   // prologue 2
+        block_sync_lds();   // prologue 3: the tile waves have read chunk 0's decay logits
+        if (NCH > 1) land_g(1);
         if (NCH > 2) fetch(2);
-        block_sync_lds();   // prologue 3
+        block_sync_lds();   // prologue 4
         for (int n = 0; n < NCH; ++n) {
             priors(n);
             if (n >= 2) output(n - 2);
-            // chunk n + 2 lands in the slots of chunk n - 1 (its decay logits in
-            // those of chunk n, which the tile waves turned into L last phase)
+            // chunk n + 2 lands in the slots of chunk n - 1
             if (n + 2 < NCH) land(n + 2);
             block_sync_lds();   // e(n)
+            // its decay logits in phase B, when those of chunk n + 1 have been read
+            if (n + 2 < NCH) land_g(n + 2);
             if (n + 3 < NCH) fetch(n + 3);
             block_sync_lds();   // i(n+1)
         }
@@ -701,7 +747,7 @@ hipError_t launch_g(const LayerArgs &a, hipStream_t stream) {
 
 template <int DK, int J>
 hipError_t launch_gj(const LayerArgs &a, hipStream_t stream) {
-    if constexpr (J * DK > 256) {
+    if constexpr (J * DK > 512) {
         return hipErrorInvalidValue;
     } else {
         // 16 output dims per block once that grid fills the chip; 8 below
@@ -726,7 +772,7 @@ hipError_t launch_gdk(const LayerArgs &a, hipStream_t stream) {
 
 bool gated_chunk_supported(const LayerArgs &a) {
     return a.in_bf16 && a.decay && !a.gk && !a.delta_out && !a.ckpt && a.J >= 1 && a.J <= 4 &&
-           a.J * a.Dk <= 256 && a.Dv % 8 == 0 &&
+           a.J * a.Dk <= 512 && a.Dv % 8 == 0 &&
            (a.Dk == 16 || a.Dk == 32 || a.Dk == 64 || a.Dk == 128);
 }
 

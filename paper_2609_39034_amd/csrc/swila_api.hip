@@ -500,7 +500,7 @@ int swila_forward_gated(const swila_shape *shape, const swila_opts *opts, const 
     if (opts->algo == SWILA_ALGO_CHUNK_EXACT && !chunk_ok)
         return fail(SWILA_EUNSUPPORTED,
                     "the gated chunk form takes bf16 inputs without temporal priors, J <= 4 "
-                    "and J * Dk <= 256 (J=%d, Dk=%d)",
+                    "and J * Dk <= 512 (J=%d, Dk=%d)",
                     shape->J, shape->Dk);
     const bool use_chunk = chunk_ok && opts->algo != SWILA_ALGO_RECURRENT;
     if (!use_chunk && shape->J * shape->Dk > swila::kMaxGatedJDk)

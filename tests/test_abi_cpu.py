@@ -241,19 +241,19 @@ def test_gated_argument_checks(lib):
     newton = sw.Opts(sw.BF16, sw.BF16, sw.ALGO_NEWTON, 0, 0, 0.0, 0)
     rc, msg = call(sw.Gated(dec), opts=newton)
     assert rc == sw.EUNSUPPORTED and "RECURRENT" in msg
-    # the chunk form: bf16 without temporal priors, J <= 4, J * Dk <= 256 (only
+    # the chunk form: bf16 without temporal priors, J <= 4, J * Dk <= 512 (only
     # calls it rejects are made here)
     chunk = sw.Opts(sw.BF16, sw.BF16, sw.ALGO_CHUNK_EXACT, 0, 0, 0.0, 0)
     rc, msg = call(sw.Gated(dec), opts=chunk,
                    tp=sw.Temporal(1 << 32, (1 << 32) + (1 << 26), None, None))
-    assert rc == sw.EUNSUPPORTED and "J * Dk <= 256" in msg
+    assert rc == sw.EUNSUPPORTED and "J * Dk <= 512" in msg
     f32chunk = sw.Opts(sw.F32, sw.F32, sw.ALGO_CHUNK_EXACT, 0, 0, 0.0, 0)
     rc, msg = call(sw.Gated(dec), opts=f32chunk)
     assert rc == sw.EUNSUPPORTED and "bf16" in msg
-    shape.Dk = 128
+    shape.J = 8
     rc, msg = call(sw.Gated(dec), opts=chunk)
-    assert rc == sw.EUNSUPPORTED and "J=4, Dk=128" in msg
-    shape.Dk = 64
+    assert rc == sw.EUNSUPPORTED and "J=8, Dk=64" in msg
+    shape.J = 4
     # temporal arguments are checked too when given
     rc, msg = call(sw.Gated(dec), tp=sw.Temporal(None, 1 << 32, None, None))
     assert rc == sw.EINVAL and msg == "gate_k_logit is NULL"

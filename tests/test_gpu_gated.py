@@ -1,7 +1,7 @@
 """Parity of the Gated SwiLA path (Sec. 3.4, App. B.4, eq. pre-decay with one
 gate per key dimension) through the C ABI with the fp64 oracle: the
 token-by-token scan and the decode step, alone and with the temporal priors,
-and the chunk form on the matrix cores (bf16 inputs, J <= 4, J * Dk <= 256),
+and the chunk form on the matrix cores (bf16 inputs, J <= 4, J * Dk <= 512),
 including chunks whose gates decay past the factorised Gram products.
 
 Bar as for the plain form: per (b, h), max|gpu - oracle| / max|oracle| <= 1e-4
@@ -162,7 +162,7 @@ def test_gated_config2_every_head(algo):
     assert eo <= 2e-2 and es <= 2e-2 and er <= 2e-2
 
 
-# ---- the chunk form (bf16 inputs, J <= 4, J * Dk <= 256)
+# ---- the chunk form (bf16 inputs, J <= 4, J * Dk <= 512)
 CHUNK_CASES = [
     # B, H, T, Dk, Dv, J, state_std, decay mean
     (1, 2, 37, 64, 64, 4, 0.1, 2.0),     # ragged third chunk
@@ -175,6 +175,9 @@ CHUNK_CASES = [
     (1, 1, 33, 64, 16, 4, 0.3, -1.0),    # strong decay (some chunks past the factorised form)
     (8, 8, 40, 64, 64, 4, 0.1, 2.0),     # 256 blocks of 16 output dims
     (4, 16, 29, 64, 32, 2, 0.2, 2.0),    # 256 blocks of 8 output dims
+    (1, 2, 37, 128, 128, 4, 0.1, 2.0),   # J * Dk = 512
+    (2, 2, 50, 128, 64, 3, 0.2, 1.0),    # J = 3, Dk = 128
+    (8, 16, 20, 128, 128, 4, 0.1, 2.0),  # 1024 blocks of 16 output dims, J * Dk = 512
 ]
 
 
@@ -202,7 +205,7 @@ def test_gated_chunk_forward(B, H, T, Dk, Dv, J, std, mean):
     assert eo <= 2e-2 and es <= 2e-2 and er <= 2e-2
 
 
-@pytest.mark.parametrize("J,Dk", [(4, 64), (2, 128), (1, 16)])
+@pytest.mark.parametrize("J,Dk", [(4, 64), (2, 128), (1, 16), (4, 128)])
 def test_gated_chunk_deep_decay(J, Dk):
     """Eight tokens of gate logit -8 (a = 3.4e-4, log a = -8) in the second chunk
     take its cumulative log gate to about -64, past the factorised Gram
