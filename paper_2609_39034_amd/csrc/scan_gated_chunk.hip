@@ -63,19 +63,25 @@ __device__ __forceinline__ floatx4 mfma16(short4v a, short4v b, floatx4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b, c, 0, 0, 0);
 }
 
-// Four fp32 values as bf16 high parts and bf16 residuals.
+// Four fp32 values as bf16 high parts (round to nearest) and bf16 residuals,
+// converted two at a time.
 struct S4 {
     short4v hi, lo;
 };
+typedef __bf16 bf16x2v __attribute__((ext_vector_type(2)));
+typedef float floatx2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ void split2(float a, float b, uint32_t &hi, uint32_t &lo) {
+    hi = __builtin_bit_cast(uint32_t, __builtin_convertvector(floatx2{a, b}, bf16x2v));
+    const float ah = __uint_as_float(hi << 16), bh = __uint_as_float(hi & 0xffff0000u);
+    lo = __builtin_bit_cast(uint32_t, __builtin_convertvector(floatx2{a - ah, b - bh}, bf16x2v));
+}
 __device__ __forceinline__ S4 split4(float x0, float x1, float x2, float x3) {
-    const float x[4] = {x0, x1, x2, x3};
+    uint32_t h0, l0, h1, l1;
+    split2(x0, x1, h0, l0);
+    split2(x2, x3, h1, l1);
     S4 s;
-#pragma unroll
-    for (int m = 0; m < 4; ++m) {
-        const __bf16 h = (__bf16)x[m];
-        s.hi[m] = __builtin_bit_cast(short, h);
-        s.lo[m] = __builtin_bit_cast(short, (__bf16)(x[m] - (float)h));
-    }
+    s.hi = __builtin_bit_cast(short4v, make_uint2(h0, h1));
+    s.lo = __builtin_bit_cast(short4v, make_uint2(l0, l1));
     return s;
 }
 __device__ __forceinline__ S4 split4(floatx4 x) { return split4(x[0], x[1], x[2], x[3]); }
@@ -182,11 +188,12 @@ __global__ __launch_bounds__(512) void scan_gated_chunk_kernel(LayerArgs a) {
         float (*const EI)[C::LP] = sm.ei[tj];
         floatx4 W[IT];
         S4 Kp[IT];   // K_m (.) E_m for the next chunk m, A operand (rows t = tl)
-        S4 Qe[IT];   // Q_m (.) E_m of the next chunk whose Q S is pending (rows t = tl)
+        S4 Qe[IT];   // Q_m (.) E_m for the next chunk m (rows t = tl)
         S4 U[IT];    // update operand of chunk n: rows i = 16 it + tl, columns s = 4 lg + m
-        floatx4 Y0 = floatx4{0.f, 0.f, 0.f, 0.f};   // Q S of the chunk whose retrieval is pending
-        S4 QGr = zero4();   // its tril(QG), A operand
-        S4 QGq = zero4();   // tril(QG) of the chunk after it
+        // Q S and tril(QG) (A operand) of the chunk whose retrieval is pending
+        // (r), and of the chunk after it (q)
+        floatx4 Y0r = floatx4{0.f, 0.f, 0.f, 0.f}, Y0q = floatx4{0.f, 0.f, 0.f, 0.f};
+        S4 QGr = zero4(), QGq = zero4();
         bool deep_n = false, deep_n1 = false;   // chunk n, n+1 past the factorised Gram products
 
         // E^-1 (or, in a deep chunk, L) and E_C of chunk m for component tj from
@@ -257,50 +264,59 @@ __global__ __launch_bounds__(512) void scan_gated_chunk_kernel(LayerArgs a) {
         auto gram = [&](int m, bool pair) {
             const int s3 = m % 3;
             floatx4 g = floatx4{0.f, 0.f, 0.f, 0.f}, qg = floatx4{0.f, 0.f, 0.f, 0.f};
+            if (!pair) {
 #pragma unroll
-            for (int it = 0; it < IT; ++it) {
-                const float4 x = *reinterpret_cast<const float4 *>(&EI[tl][16 * it + 4 * lg]);
-                float4 er;   // E at rows tl, key indices 16 it + 4 lg .. + 3
-                if (pair) {
-                    er = make_float4(__builtin_amdgcn_exp2f(kLog2e * x.x),
-                                     __builtin_amdgcn_exp2f(kLog2e * x.y),
-                                     __builtin_amdgcn_exp2f(kLog2e * x.z),
-                                     __builtin_amdgcn_exp2f(kLog2e * x.w));
-                } else {
-                    er = make_float4(rcp_fast(x.x), rcp_fast(x.y), rcp_fast(x.z), rcp_fast(x.w));
-                }
-                Kp[it] = row4(sm.k[s3], it, er);
-                Qe[it] = row4(sm.q[s3], it, er);
-                if (!pair) {
+                for (int it = 0; it < IT; ++it) {
+                    // E^-1 and E at rows tl, key indices 16 it + 4 lg .. + 3
+                    const float4 x = *reinterpret_cast<const float4 *>(&EI[tl][16 * it + 4 * lg]);
+                    const float4 er = make_float4(rcp_fast(x.x), rcp_fast(x.y), rcp_fast(x.z), rcp_fast(x.w));
+                    Kp[it] = row4(sm.k[s3], it, er);
+                    Qe[it] = row4(sm.q[s3], it, er);
                     const S4 kinv = row4(sm.k[s3], it, x);   // K (.) E^-1, rows s = tl
                     g = mm3(Kp[it], kinv, g);      // D[t = 4 lg + r][s = tl] = G_ts
                     qg = mm3(kinv, Qe[it], qg);    // D[s = 4 lg + r][t = tl] = QG_ts
                 }
-            }
-            // lane (tl, lg) holds QG[t = tl][s = 4 lg + r]: the A operand of the retrieval
+                // lane (tl, lg) holds QG[t = tl][s = 4 lg + r]: the A operand of the retrieval
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int t = 4 * lg + r;   // row of G
-                const int s = 4 * lg + r;   // column of QG
-                if (pair) {
+                for (int r = 0; r < 4; ++r)
+                    if (4 * lg + r > tl) qg[r] = 0.0f;
+            } else {
+#pragma unroll
+                for (int it = 0; it < IT; ++it) {
+                    const float4 x = *reinterpret_cast<const float4 *>(&EI[tl][16 * it + 4 * lg]);
+                    const float4 er = make_float4(__builtin_amdgcn_exp2f(kLog2e * x.x),
+                                                  __builtin_amdgcn_exp2f(kLog2e * x.y),
+                                                  __builtin_amdgcn_exp2f(kLog2e * x.z),
+                                                  __builtin_amdgcn_exp2f(kLog2e * x.w));
+                    Kp[it] = row4(sm.k[s3], it, er);
+                    Qe[it] = row4(sm.q[s3], it, er);
+                }
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int t = 4 * lg + r;   // row of G
+                    const int s = 4 * lg + r;   // column of QG
                     g[r] = t > tl ? pair_dot(sm.k[s3], m, t, tl) : 0.0f;
                     qg[r] = s <= tl ? pair_dot(sm.q[s3], m, tl, s) : 0.0f;
-                } else if (s > tl) {
-                    qg[r] = 0.0f;
                 }
             }
             *reinterpret_cast<float4 *>(&sm.gt[m & 1][tj][tl][4 * lg]) =
                 make_float4(g[0], g[1], g[2], g[3]);
             QGq = split4(qg);
         };
-        // chunk-start predictions P = Kp S for the sequential wave, in its units
+        // for the next chunk, from its start state S: the predictions P = Kp S
+        // for the sequential wave, in its units, and Q S (Y0q)
         auto predict = [&]() {
-            floatx4 pacc = floatx4{0.f, 0.f, 0.f, 0.f};
+            floatx4 pacc = floatx4{0.f, 0.f, 0.f, 0.f}, y0 = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int it = 0; it < IT; ++it) pacc = mm3(Kp[it], split4(W[it]), pacc);   // D[t][col]
+            for (int it = 0; it < IT; ++it) {
+                const S4 ws = split4(W[it]);
+                pacc = mm3(Kp[it], ws, pacc);   // D[t][col]
+                y0 = mm3(Qe[it], ws, y0);
+            }
             if (tvalid)
                 *reinterpret_cast<float4 *>(&sm.p[tcol][4 * lg]) =
                     make_float4(kS * pacc[0], kS * pacc[1], kS * pacc[2], kS * pacc[3]);
+            Y0q = y0;
         };
         // C of chunk m as the B operand: rows s = 4 lg .. + 3, column tl
         auto coeffs = [&](int m) {
@@ -309,7 +325,7 @@ __global__ __launch_bounds__(512) void scan_gated_chunk_kernel(LayerArgs a) {
         };
         // retrieval of chunk m: Y = Y0 + tril(QG) C, times pi^q, to py
         auto retrieve = [&](int m) {
-            const floatx4 y = mm3(QGr, coeffs(m), Y0);   // D[t = 4 lg + r][col]
+            const floatx4 y = mm3(QGr, coeffs(m), Y0r);   // D[t = 4 lg + r][col]
             if (tvalid) {
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
@@ -318,36 +334,39 @@ __global__ __launch_bounds__(512) void scan_gated_chunk_kernel(LayerArgs a) {
                 }
             }
         };
-        // what chunk n needs besides C_n: Q_n S_n and U_n (Qe, QGq and EI hold
-        // chunk n's)
+        // what chunk n needs besides C_n: its Q S and tril(QG) for the retrieval
+        // (from Y0q and QGq) and U_n (EI holds chunk n's E^-1 or L)
         auto prepare = [&](int n, bool pair) {
             const int s3 = n % 3;
-            floatx4 y0 = floatx4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int it = 0; it < IT; ++it) y0 = mm3(Qe[it], split4(W[it]), y0);   // D[t][col]
-            Y0 = y0;
+            Y0r = Y0q;
             QGr = QGq;
             // U[i][s] = K[s][i] E_C,i / E_s,i, i = 16 it + tl, s = 4 lg + m
+            if (!pair) {
 #pragma unroll
-            for (int it = 0; it < IT; ++it) {
-                const int i = 16 * it + tl;
-                float u[4];
-                if (pair) {
-                    const float lc = EI[kGC - 1][i];
-#pragma unroll
-                    for (int m = 0; m < 4; ++m) {
-                        const int s = 4 * lg + m;
-                        u[m] = bf(sm.k[s3][s][i]) * __builtin_amdgcn_exp2f(kLog2e * (lc - EI[s][i]));
-                    }
-                } else {
+                for (int it = 0; it < IT; ++it) {
+                    const int i = 16 * it + tl;
                     const float ecv = sm.ec[n & 1][tj][i];
+                    float u[4];
 #pragma unroll
                     for (int m = 0; m < 4; ++m) {
                         const int s = 4 * lg + m;
                         u[m] = bf(sm.k[s3][s][i]) * (ecv * EI[s][i]);
                     }
+                    U[it] = split4(u[0], u[1], u[2], u[3]);
                 }
-                U[it] = split4(u[0], u[1], u[2], u[3]);
+            } else {
+#pragma unroll
+                for (int it = 0; it < IT; ++it) {
+                    const int i = 16 * it + tl;
+                    const float lc = EI[kGC - 1][i];
+                    float u[4];
+#pragma unroll
+                    for (int m = 0; m < 4; ++m) {
+                        const int s = 4 * lg + m;
+                        u[m] = bf(sm.k[s3][s][i]) * __builtin_amdgcn_exp2f(kLog2e * (lc - EI[s][i]));
+                    }
+                    U[it] = split4(u[0], u[1], u[2], u[3]);
+                }
             }
         };
 
@@ -363,7 +382,7 @@ __global__ __launch_bounds__(512) void scan_gated_chunk_kernel(LayerArgs a) {
         block_sync_lds();   // prologue 2: chunks 0 and 1 in LDS (the decay logits of 0)
         deep_n = log_gates(0);
         gram(0, deep_n);
-        predict();          // P_0
+        predict();          // P_0, Q_0 S_0
         block_sync_lds();   // prologue 3: the decay logits of chunk 0 read
         block_sync_lds();   // prologue 4: those of chunk 1 in LDS
         for (int n = 0; n < NCH; ++n) {
@@ -375,7 +394,7 @@ __global__ __launch_bounds__(512) void scan_gated_chunk_kernel(LayerArgs a) {
                 gram(n + 1, deep_n1);
             }
             block_sync_lds();   // e(n)
-            // ---- phase B: S_{n+1} = E_C (.) S_n + U_n^T C_n, then P_{n+1}
+            // ---- phase B: S_{n+1} = E_C (.) S_n + U_n^T C_n, then P_{n+1}, Q_{n+1} S_{n+1}
             const S4 cb = coeffs(n);
 #pragma unroll
             for (int it = 0; it < IT; ++it) {
