@@ -95,10 +95,23 @@ __device__ __forceinline__ floatx4 mfma32(bf16x8 a, bf16x8 b, floatx4 c) {
 __device__ __forceinline__ floatx4 mfma16(short4v a, short4v b, floatx4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b, c, 0, 0, 0);
 }
-__device__ __forceinline__ short bf16_bits(__bf16 x) { return __builtin_bit_cast(short, x); }
-__device__ __forceinline__ void split(float x, __bf16 &hi, __bf16 &lo) {
-    hi = (__bf16)x;
-    lo = (__bf16)(x - (float)hi);
+// bf16 high part (round to nearest) and bf16 residual of two values, each
+// converted as a pair (a in the low half)
+typedef __bf16 bf16x2v __attribute__((ext_vector_type(2)));
+typedef float floatx2v __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ void split_pk(float a, float b, uint32_t &hi, uint32_t &lo) {
+    hi = __builtin_bit_cast(uint32_t, __builtin_convertvector(floatx2v{a, b}, bf16x2v));
+    const float ah = __uint_as_float(hi << 16), bh = __uint_as_float(hi & 0xffff0000u);
+    lo = __builtin_bit_cast(uint32_t, __builtin_convertvector(floatx2v{a - ah, b - bh}, bf16x2v));
+}
+// split of four values into short4v operands
+__device__ __forceinline__ void split4v(float x0, float x1, float x2, float x3, short4v &hi,
+                                        short4v &lo) {
+    uint32_t h0, l0, h1, l1;
+    split_pk(x0, x1, h0, l0);
+    split_pk(x2, x3, h1, l1);
+    hi = __builtin_bit_cast(short4v, make_uint2(h0, h1));
+    lo = __builtin_bit_cast(short4v, make_uint2(l0, l1));
 }
 // Wait for this wave's outstanding vector-memory operations (the direct
 // HBM -> LDS transfers among them).  Issued through the builtin so that the
@@ -543,26 +556,19 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
                            bf16x8 (&wlo)[IT / 2 > 0 ? IT / 2 : 1], short4v &w16hi,
                            short4v &w16lo) {
         if constexpr (DK == 16) {
-#pragma unroll
-            for (int m = 0; m < 4; ++m) {
-                __bf16 hi, lo;
-                split(W[0][m], hi, lo);
-                w16hi[m] = bf16_bits(hi);
-                w16lo[m] = bf16_bits(lo);
-            }
+            split4v(W[0][0], W[0][1], W[0][2], W[0][3], w16hi, w16lo);
         } else {
 #pragma unroll
-            for (int s = 0; s < DK / 32; ++s)
-#pragma unroll
-                for (int m = 0; m < 4; ++m) {
-                    __bf16 hi, lo;
-                    split(W[2 * s][m], hi, lo);
-                    whi[s][m] = hi;
-                    wlo[s][m] = lo;
-                    split(W[2 * s + 1][m], hi, lo);
-                    whi[s][4 + m] = hi;
-                    wlo[s][4 + m] = lo;
-                }
+            for (int s = 0; s < DK / 32; ++s) {
+                // elements m = 0..3 from W[2 s], 4..7 from W[2 s + 1]
+                uint32_t h[4], l[4];
+                split_pk(W[2 * s][0], W[2 * s][1], h[0], l[0]);
+                split_pk(W[2 * s][2], W[2 * s][3], h[1], l[1]);
+                split_pk(W[2 * s + 1][0], W[2 * s + 1][1], h[2], l[2]);
+                split_pk(W[2 * s + 1][2], W[2 * s + 1][3], h[3], l[3]);
+                whi[s] = __builtin_bit_cast(bf16x8, make_uint4(h[0], h[1], h[2], h[3]));
+                wlo[s] = __builtin_bit_cast(bf16x8, make_uint4(l[0], l[1], l[2], l[3]));
+            }
         }
     };
     // acc += (rows of tile) x S, with S split as above
@@ -902,13 +908,8 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
         // exactly the A operand of tril(A_m) C_m, A_m = Q_m K_m^T
         const floatx4 at = gram(sm.k[rs], sm.q[rs]);
         short4v ahi, alo;
-#pragma unroll
-        for (int mm = 0; mm < 4; ++mm) {
-            __bf16 hi, lo;
-            split(4 * lg + mm <= tl ? at[mm] : 0.f, hi, lo);
-            ahi[mm] = bf16_bits(hi);
-            alo[mm] = bf16_bits(lo);
-        }
+        split4v(4 * lg <= tl ? at[0] : 0.f, 4 * lg + 1 <= tl ? at[1] : 0.f,
+                4 * lg + 2 <= tl ? at[2] : 0.f, 4 * lg + 3 <= tl ? at[3] : 0.f, ahi, alo);
         Yacc = mfma16(ahi, chi, Yacc);
         Yacc = mfma16(ahi, clo, Yacc);
         Yacc = mfma16(alo, chi, Yacc);
