@@ -98,6 +98,25 @@ __device__ __forceinline__ floatx4 mm3(const S4 &a, const S4 &b, floatx4 acc) {
     acc = mfma16(a.lo, b.hi, acc);
     return acc;
 }
+// The same over two 16-wide k tiles at once (a0 b0 + a1 b1), on the 32-deep
+// instruction: a lane's eight k elements are its four of tile 0, then its four
+// of tile 1, in both operands.
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+__device__ __forceinline__ bf16x8 join8(short4v x, short4v y) {
+    return __builtin_bit_cast(bf16x8, make_uint4(__builtin_bit_cast(uint2, x).x,
+                                                 __builtin_bit_cast(uint2, x).y,
+                                                 __builtin_bit_cast(uint2, y).x,
+                                                 __builtin_bit_cast(uint2, y).y));
+}
+__device__ __forceinline__ floatx4 mm3x2(const S4 &a0, const S4 &a1, const S4 &b0, const S4 &b1,
+                                         floatx4 acc) {
+    const bf16x8 ah = join8(a0.hi, a1.hi), al = join8(a0.lo, a1.lo);
+    const bf16x8 bh = join8(b0.hi, b1.hi), bl = join8(b0.lo, b1.lo);
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bh, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bl, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, bh, acc, 0, 0, 0);
+    return acc;
+}
 
 __device__ __forceinline__ float bf(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
 
@@ -197,15 +216,45 @@ __global__ __launch_bounds__(512) void scan_gated_chunk_kernel(LayerArgs a) {
         bool deep_n = false, deep_n1 = false;   // chunk n, n+1 past the factorised Gram products
 
         // E^-1 (or, in a deep chunk, L) and E_C of chunk m for component tj from
-        // its decay logits (lane: key indices lane, lane + 64, ...); returns
-        // whether the chunk is deep.
+        // its decay logits (lane: key index lane, or 2 lane and 2 lane + 1 when
+        // Dk = 128); returns whether the chunk is deep.
         auto log_gates = [&](int m) {
             const int nt = min(kGC, T - m * kGC);
             bool deep = false;
+            if constexpr (DK == 128) {
+                // two adjacent key indices per lane
+                const int i = 2 * lane;
+                uint32_t x[kGC];
 #pragma unroll
-            for (int i0 = 0; i0 < DK; i0 += 64) {
-                // every lane loads its column first (idle lanes column 0), then multiplies
-                const int i = i0 + lane, ic = DK >= 64 || i < DK ? i : 0;
+                for (int t = 0; t < kGC; ++t)
+                    x[t] = *reinterpret_cast<const uint32_t *>(&sm.g[t][tj * DK + i]);
+                float c0 = 1.0f, c1 = 1.0f;
+#pragma unroll
+                for (int t = 0; t < kGC; ++t) {
+                    const float f0 = 1.0f + __builtin_amdgcn_exp2f(-kLog2e * __uint_as_float(x[t] << 16));
+                    const float f1 =
+                        1.0f + __builtin_amdgcn_exp2f(-kLog2e * __uint_as_float(x[t] & 0xffff0000u));
+                    c0 *= t < nt ? f0 : 1.0f;
+                    c1 *= t < nt ? f1 : 1.0f;
+                    *reinterpret_cast<float2 *>(&EI[t][i]) = make_float2(c0, c1);
+                }
+                *reinterpret_cast<float2 *>(&sm.ec[m & 1][tj][i]) = make_float2(rcp_fast(c0), rcp_fast(c1));
+                deep = !(c0 <= kGramEinv) || !(c1 <= kGramEinv);
+                if (__any(deep) == 0) return false;
+                // deep chunk: L = the running sum of log sigmoid, in place of E^-1
+                float l0 = 0.0f, l1 = 0.0f;
+#pragma unroll
+                for (int t = 0; t < kGC; ++t) {
+                    l0 += t < nt ? log_sigmoid(__uint_as_float(x[t] << 16)) : 0.0f;
+                    l1 += t < nt ? log_sigmoid(__uint_as_float(x[t] & 0xffff0000u)) : 0.0f;
+                    *reinterpret_cast<float2 *>(&EI[t][i]) = make_float2(l0, l1);
+                }
+                *reinterpret_cast<float2 *>(&sm.ec[m & 1][tj][i]) =
+                    make_float2(__builtin_amdgcn_exp2f(kLog2e * l0), __builtin_amdgcn_exp2f(kLog2e * l1));
+                return true;
+            } else {
+                // one key index per lane (lanes past Dk idle)
+                const int i = lane, ic = DK >= 64 || i < DK ? i : 0;
                 float x[kGC];
 #pragma unroll
                 for (int t = 0; t < kGC; ++t) x[t] = bf(sm.g[t][tj * DK + ic]);
@@ -222,25 +271,20 @@ __global__ __launch_bounds__(512) void scan_gated_chunk_kernel(LayerArgs a) {
 #pragma unroll
                     for (int t = 0; t < kGC; ++t) EI[t][i] = e[t];
                     sm.ec[m & 1][tj][i] = rcp_fast(cum);
-                    deep = deep || !(cum <= kGramEinv);
+                    deep = !(cum <= kGramEinv);
                 }
-            }
-            if (__any(deep) == 0) return false;
-            // deep chunk: L = the running sum of log sigmoid, in place of E^-1
-#pragma unroll
-            for (int i0 = 0; i0 < DK; i0 += 64) {
-                const int i = i0 + lane;
+                if (__any(deep) == 0) return false;
                 if (DK >= 64 || i < DK) {
-                    float cum = 0.0f;
+                    float l = 0.0f;
 #pragma unroll
                     for (int t = 0; t < kGC; ++t) {
-                        cum += t < nt ? log_sigmoid(bf(sm.g[t][tj * DK + i])) : 0.0f;
-                        EI[t][i] = cum;
+                        l += t < nt ? log_sigmoid(x[t]) : 0.0f;
+                        EI[t][i] = l;
                     }
-                    sm.ec[m & 1][tj][i] = __builtin_amdgcn_exp2f(kLog2e * cum);
+                    sm.ec[m & 1][tj][i] = __builtin_amdgcn_exp2f(kLog2e * l);
                 }
+                return true;
             }
-            return true;
         };
 
         // four bf16 of row tl of X, key indices 16 it + 4 lg .. + 3, times f
@@ -265,16 +309,26 @@ __global__ __launch_bounds__(512) void scan_gated_chunk_kernel(LayerArgs a) {
             const int s3 = m % 3;
             floatx4 g = floatx4{0.f, 0.f, 0.f, 0.f}, qg = floatx4{0.f, 0.f, 0.f, 0.f};
             if (!pair) {
-#pragma unroll
-                for (int it = 0; it < IT; ++it) {
-                    // E^-1 and E at rows tl, key indices 16 it + 4 lg .. + 3
+                // E^-1 and E at rows tl, key indices 16 it + 4 lg .. + 3; K (.) E^-1
+                // at rows s = tl
+                auto operands = [&](int it) {
                     const float4 x = *reinterpret_cast<const float4 *>(&EI[tl][16 * it + 4 * lg]);
                     const float4 er = make_float4(rcp_fast(x.x), rcp_fast(x.y), rcp_fast(x.z), rcp_fast(x.w));
                     Kp[it] = row4(sm.k[s3], it, er);
                     Qe[it] = row4(sm.q[s3], it, er);
-                    const S4 kinv = row4(sm.k[s3], it, x);   // K (.) E^-1, rows s = tl
-                    g = mm3(Kp[it], kinv, g);      // D[t = 4 lg + r][s = tl] = G_ts
-                    qg = mm3(kinv, Qe[it], qg);    // D[s = 4 lg + r][t = tl] = QG_ts
+                    return row4(sm.k[s3], it, x);
+                };
+                if constexpr (IT == 1) {
+                    const S4 kinv = operands(0);
+                    g = mm3(Kp[0], kinv, g);      // D[t = 4 lg + r][s = tl] = G_ts
+                    qg = mm3(kinv, Qe[0], qg);    // D[s = 4 lg + r][t = tl] = QG_ts
+                } else {
+#pragma unroll
+                    for (int it = 0; it < IT; it += 2) {
+                        const S4 k0 = operands(it), k1 = operands(it + 1);
+                        g = mm3x2(Kp[it], Kp[it + 1], k0, k1, g);
+                        qg = mm3x2(k0, k1, Qe[it], Qe[it + 1], qg);
+                    }
                 }
                 // lane (tl, lg) holds QG[t = tl][s = 4 lg + r]: the A operand of the retrieval
 #pragma unroll
@@ -307,11 +361,17 @@ __global__ __launch_bounds__(512) void scan_gated_chunk_kernel(LayerArgs a) {
         // for the sequential wave, in its units, and Q S (Y0q)
         auto predict = [&]() {
             floatx4 pacc = floatx4{0.f, 0.f, 0.f, 0.f}, y0 = floatx4{0.f, 0.f, 0.f, 0.f};
+            if constexpr (IT == 1) {
+                const S4 ws = split4(W[0]);
+                pacc = mm3(Kp[0], ws, pacc);   // D[t][col]
+                y0 = mm3(Qe[0], ws, y0);
+            } else {
 #pragma unroll
-            for (int it = 0; it < IT; ++it) {
-                const S4 ws = split4(W[it]);
-                pacc = mm3(Kp[it], ws, pacc);   // D[t][col]
-                y0 = mm3(Qe[it], ws, y0);
+                for (int it = 0; it < IT; it += 2) {
+                    const S4 w0 = split4(W[it]), w1 = split4(W[it + 1]);
+                    pacc = mm3x2(Kp[it], Kp[it + 1], w0, w1, pacc);
+                    y0 = mm3x2(Qe[it], Qe[it + 1], w0, w1, y0);
+                }
             }
             if (tvalid)
                 *reinterpret_cast<float4 *>(&sm.p[tcol][4 * lg]) =
