@@ -42,21 +42,21 @@ PEAK_MFMA_BF16 = 2.5e15    # FLOP/s, MI355X dense bf16 matrix
 # source, the workload it ran and the digest of the source at measurement.
 MEASURED_TRAFFIC = {
     ("scan_pipe.hip", "forward B=8 H=16 T=4096 Dk=Dv=128 J=4",
-     "6fc333fc19bb03e99649a170bb3cd97a9e6defdfb8a4d7f4e5967378ea424437"): 2189939206,
+     "1279d1e40d80d9581b39a017448a74ccd9c96fb369185c3126ebcc1d49dbcecf"): 2184251513,
     ("scan_pipe.hip", "forward B=4 H=8 T=2048 Dk=Dv=64 J=4",
-     "6fc333fc19bb03e99649a170bb3cd97a9e6defdfb8a4d7f4e5967378ea424437"): 136863294,
+     "1279d1e40d80d9581b39a017448a74ccd9c96fb369185c3126ebcc1d49dbcecf"): 136703396,
     ("scan_pipe.hip", "forward B=2 H=8 T=16384 Dk=Dv=128 J=8",
-     "6fc333fc19bb03e99649a170bb3cd97a9e6defdfb8a4d7f4e5967378ea424437"): 2534394415,
+     "1279d1e40d80d9581b39a017448a74ccd9c96fb369185c3126ebcc1d49dbcecf"): 1965727865,
     ("scan_pipe_temporal.hip", "temporal B=8 H=16 T=4096 Dk=Dv=128 J=4",
-     "cccc3565bc93a77d940c00ec22e392f9d5416ecb56469aaedb8c4fd185fdd548"): 2450704072,
-    ("scan_direct_dk128.hip", "gated B=8 H=16 T=4096 Dk=Dv=128 J=4",
-     "39988c61ffdc92c542a18091834b55f6a71977a11a0302fd3f9580181595ad2b"): 2718134140,
+     "6fcab140baddad3d29cdadda05b27e194601b259bba7afca4f0c99301dca8916"): 2451508642,
+    ("scan_gated_chunk.hip", "gated B=8 H=16 T=4096 Dk=Dv=128 J=4",
+     "cbd5ed2709e891b062a157630c2fb89d518e8158aef25b074c5155fb3b0d766e"): 2721113447,
     ("scan_direct_dk16.hip", "forward B=1 H=1 T=64 Dk=Dv=16 J=2",
-     "11dc94a786728640b929d058f8600bf4e3c032bd82c288ad3136a45bdd77cb84"): 67583,
+     "11dc94a786728640b929d058f8600bf4e3c032bd82c288ad3136a45bdd77cb84"): 67711,
     ("decode.hip", "decode B=256 H=16 Dk=Dv=128 J=4",
-     "885219bbb8497010b554af973a0d14b02c80037d8cb73ffd4fa2afb165c828d7"): 2165212629,
+     "885219bbb8497010b554af973a0d14b02c80037d8cb73ffd4fa2afb165c828d7"): 2165183583,
     ("scan_gated_chunk.hip", "gated B=4 H=8 T=2048 Dk=Dv=64 J=4",
-     "facc5a996b3a946a524b86831f86bc7f517c8906e403536001a496d93ad0d4d6"): 179186388,
+     "cbd5ed2709e891b062a157630c2fb89d518e8158aef25b074c5155fb3b0d766e"): 170709923,
 }
 
 
