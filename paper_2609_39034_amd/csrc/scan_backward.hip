@@ -68,9 +68,59 @@ constexpr int chunk_tile_dims() { return J == 1 ? 16 : J == 3 ? 8 : 32 / J; }
 // the Gram products K K^T, K Q^T and the base K E + triu(K Q^T) Y in parallel;
 // one wave then runs the chunk's tokens in reverse, one lane per column (all J
 // components of DB output dims, J lanes adjacent), with the later tokens'
-// dpred folded in as deferred updates; last E += Q^T Y + K^T P.  Every product
-// is fp32 on the vector ALUs.
+// dpred folded in as deferred updates; last E += Q^T Y + K^T P.  With fp32
+// inputs every product is fp32 on the vector ALUs.  With bf16 inputs the
+// products run on the matrix cores: K and Q are exact in bf16, so K K^T and
+// K Q^T are single products; E, Y, P and the Gram values are fp32, split into
+// a bf16 high part and a bf16 residual (about 2^-17 relative per operand,
+// fp32 accumulation).
 constexpr int kRC = 16;   // tokens per chunk of the reverse scan
+
+typedef short short4v __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2v __attribute__((ext_vector_type(2)));
+typedef float floatx2v __attribute__((ext_vector_type(2)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+// two fp32 values to packed bf16 (round to nearest; a in the low half), and
+// their residuals
+__device__ __forceinline__ uint32_t pk_bf16(float a, float b) {
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(floatx2v{a, b}, bf16x2v));
+}
+__device__ __forceinline__ void split_pk(float a, float b, uint32_t &hi, uint32_t &lo) {
+    hi = pk_bf16(a, b);
+    lo = pk_bf16(a - __uint_as_float(hi << 16), b - __uint_as_float(hi & 0xffff0000u));
+}
+// The k operand of a lane: M values (4 for the 16-deep product, 8 for the
+// 32-deep one) as bf16, or as high parts and residuals
+template <int M>
+struct KOp {
+    uint32_t hi[M / 2], lo[M / 2];
+};
+template <int M>
+__device__ __forceinline__ KOp<M> kop_exact(const float *x) {
+    KOp<M> o;
+#pragma unroll
+    for (int m = 0; m < M / 2; ++m) o.hi[m] = pk_bf16(x[2 * m], x[2 * m + 1]), o.lo[m] = 0u;
+    return o;
+}
+template <int M>
+__device__ __forceinline__ KOp<M> kop_split(const float *x) {
+    KOp<M> o;
+#pragma unroll
+    for (int m = 0; m < M / 2; ++m) split_pk(x[2 * m], x[2 * m + 1], o.hi[m], o.lo[m]);
+    return o;
+}
+__device__ __forceinline__ floatx4 mma(const uint32_t (&a)[2], const uint32_t (&b)[2], floatx4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(short4v, make_uint2(a[0], a[1])),
+                                                     __builtin_bit_cast(short4v, make_uint2(b[0], b[1])),
+                                                     c, 0, 0, 0);
+}
+__device__ __forceinline__ floatx4 mma(const uint32_t (&a)[4], const uint32_t (&b)[4], floatx4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+        __builtin_bit_cast(bf16x8, make_uint4(a[0], a[1], a[2], a[3])),
+        __builtin_bit_cast(bf16x8, make_uint4(b[0], b[1], b[2], b[3])), c, 0, 0, 0);
+}
 
 template <int DK, int J, int DB>
 __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a) {
@@ -95,6 +145,10 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
 
     const LayerArgs &f = a.f;
     const int tid = threadIdx.x, lane = tid % 64;
+    // matrix-core lane coordinates: row / column tl, k slot lg
+    const int wv = __builtin_amdgcn_readfirstlane(tid / 64), tl = lane % 16, lg = lane / 16;
+    constexpr int NTC = (N + 15) / 16;    // 16-column tiles
+    constexpr int KM = DK >= 32 ? 8 : 4;  // k values per lane: 32- or 16-deep products
     const int H = f.H, T = f.T, Dv = f.Dv;
     // Workgroups go to the eight XCDs (each with its own L2) round-robin by
     // index; every column block of a head is placed on the same XCD, so that
@@ -264,8 +318,27 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
         }
         block_sync_lds();
         if (n > 0) fetch(n - 1);   // lands while this chunk computes
-        // Gram products of the chunk: one (t, s) pair per thread
-        {
+        // Gram products of the chunk: on the matrix cores (bf16 inputs; wave 0
+        // K K^T, wave 1 K Q^T), else one (t, s) pair per thread
+        if (ibf) {
+            if (wv < 2) {
+                // D[row][col] = sum_i A[row][i] K[col][i], A = K (D[t][s]) or Q
+                // (D[s][t] = k_t . q_s); lane: row / col tl, k slot lg
+                const float (*A)[KP] = wv == 0 ? sK : sQ;
+                floatx4 acc = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int i0 = 0; i0 < DK; i0 += KM * 4) {
+                    const KOp<KM> a8 = kop_exact<KM>(&A[tl][i0 + KM * lg]);
+                    const KOp<KM> b8 = kop_exact<KM>(&sK[tl][i0 + KM * lg]);
+                    acc = mma(a8.hi, b8.hi, acc);
+                }
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    if (wv == 0) sGkk[4 * lg + r][tl] = acc[r];
+                    else sGkqT[4 * lg + r][tl] = acc[r];
+                }
+            }
+        } else {
             const int t = tid / kRC, s2 = tid % kRC;
             float gkk = 0.0f, gkq = 0.0f;
 #pragma unroll 4
@@ -280,7 +353,41 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
             sGkqT[s2][t] = gkq;
         }
         block_sync_lds();
-        // base_t = k_t . E + sum_{s>=t} (k_t . q_s) dy_s: four tokens per thread
+        // base_t = k_t . E + sum_{s>=t} (k_t . q_s) dy_s: a 16-column tile per
+        // wave on the matrix cores (bf16 inputs), else four tokens per thread
+        if (ibf) {
+            for (int ct = wv; ct < NTC; ct += kThreads / 64) {
+                const int col = 16 * ct + tl;
+                const bool cv = col < N;
+                floatx4 acc = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int i0 = 0; i0 < DK; i0 += KM * 4) {
+                    const KOp<KM> a8 = kop_exact<KM>(&sK[tl][i0 + KM * lg]);   // K[t = tl][i]
+                    float ev[KM];
+#pragma unroll
+                    for (int m = 0; m < KM; ++m) ev[m] = cv ? sE[i0 + KM * lg + m][col] : 0.0f;
+                    const KOp<KM> b8 = kop_split<KM>(ev);
+                    acc = mma(a8.hi, b8.hi, acc);
+                    acc = mma(a8.hi, b8.lo, acc);
+                }
+                // triu: A[t = tl][s = 4 lg + m] = k_t . q_s for s >= t, B = dy[s][col]
+                float gv[4], yv[4];
+#pragma unroll
+                for (int m = 0; m < 4; ++m) {
+                    const int s2 = 4 * lg + m;
+                    gv[m] = s2 >= tl ? sGkqT[s2][tl] : 0.0f;
+                    yv[m] = cv ? sY[s2][col] : 0.0f;
+                }
+                const KOp<4> ga = kop_split<4>(gv), yb = kop_split<4>(yv);
+                acc = mma(ga.hi, yb.hi, acc);
+                acc = mma(ga.hi, yb.lo, acc);
+                acc = mma(ga.lo, yb.hi, acc);
+                if (cv) {
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) sBase[4 * lg + r][col] = acc[r];
+                }
+            }
+        } else
         for (int e = tid; e < (kRC / 4) * N; e += kThreads) {
             const int t4 = (e / N) * 4, col = e % N;
             float acc[4] = {0.f, 0.f, 0.f, 0.f};
@@ -362,7 +469,36 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
         }
         block_sync_lds();
         // E += Q^T Y + K^T P (E now from the tokens after the previous chunk):
-        // four columns per thread
+        // 16 x 16 tiles of E on the matrix cores (bf16 inputs), else four
+        // columns per thread
+        if (ibf) {
+            for (int tile = wv; tile < (DK / 16) * NTC; tile += kThreads / 64) {
+                const int ti = tile / NTC, ct = tile % NTC;
+                const int col = 16 * ct + tl;
+                const bool cv = col < N;
+                floatx4 acc;
+#pragma unroll
+                for (int r = 0; r < 4; ++r) acc[r] = cv ? sE[16 * ti + 4 * lg + r][col] : 0.0f;
+                // A = Q^T, K^T: rows i = 16 ti + tl, k = t = 4 lg .. + 3
+                const KOp<4> qa = kop_exact<4>(&sQt[16 * ti + tl][4 * lg]);
+                const KOp<4> ka = kop_exact<4>(&sKt[16 * ti + tl][4 * lg]);
+                float yv[4], pv[4];
+#pragma unroll
+                for (int m = 0; m < 4; ++m) {
+                    yv[m] = cv ? sY[4 * lg + m][col] : 0.0f;
+                    pv[m] = cv ? sP[4 * lg + m][col] : 0.0f;
+                }
+                const KOp<4> yb = kop_split<4>(yv), pb = kop_split<4>(pv);
+                acc = mma(qa.hi, yb.hi, acc);
+                acc = mma(qa.hi, yb.lo, acc);
+                acc = mma(ka.hi, pb.hi, acc);
+                acc = mma(ka.hi, pb.lo, acc);
+                if (cv) {
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) sE[16 * ti + 4 * lg + r][col] = acc[r];
+                }
+            }
+        } else
         for (int e = tid; e < DK * (N / 4); e += kThreads) {
             const int i = e / (N / 4), c4 = (e % (N / 4)) * 4;
             float4 acc = *reinterpret_cast<const float4 *>(&sE[i][c4]);
