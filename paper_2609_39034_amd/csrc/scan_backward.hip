@@ -49,6 +49,11 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kCB = kBwdChunk;    // tokens per chunk of the chunk pass
 
+template <bool B>
+struct BTag {
+    static constexpr bool value = B;
+};
+
 // The kernels below order only LDS traffic at their barriers (block_sync_lds):
 // a full __syncthreads would also wait for every global load in flight, and
 // with it for the next chunk's prefetch.  Their staging loads raw bits
@@ -122,7 +127,9 @@ __device__ __forceinline__ floatx4 mma(const uint32_t (&a)[4], const uint32_t (&
         __builtin_bit_cast(bf16x8, make_uint4(b[0], b[1], b[2], b[3])), c, 0, 0, 0);
 }
 
-template <int DK, int J, int DB>
+// IBF: bf16 inputs (the input dtype is fixed per instantiation, so that the
+// prefetch has one load variant; dL/do's dtype stays a run-time choice)
+template <int DK, int J, int DB, bool IBF>
 __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a) {
     constexpr int JP = J == 3 ? 4 : J;   // lanes per output dim (J = 3 padded)
     constexpr int N = J * DB;            // columns, col = j * DB + dd
@@ -165,7 +172,8 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
         db = L % NDB;
     }
     const int d0 = db * DB, h = hh % H, b = hh / H;
-    const bool ibf = f.in_bf16, obf = f.out_bf16;
+    constexpr bool ibf = IBF;
+    const bool obf = f.out_bf16;
     const int NCH = (T + kRC - 1) / kRC;
     const int NC2 = (T + kBwdChunk - 1) / kBwdChunk;
     constexpr int R2 = kBwdChunk / kRC;   // reverse chunks per checkpoint interval
@@ -183,46 +191,61 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
 
     // Each chunk's HBM inputs are fetched into registers while the previous
     // (later) chunk computes: K and Q rows as float4, and per (token, output
-    // dim) the J errors and logits and dL/do.
+    // dim) the J errors and logits and dL/do.  Every thread loads every item it
+    // owns, from a clamped row (the chunk's last token, the last item), with
+    // the input dtype fixed at compile time: no load sits behind a branch
+    // (a load there is waited for at the join); staging zeroes what lies past
+    // the end.
     constexpr int NKQ = (kRC * (DK / 4) + kThreads - 1) / kThreads;
     constexpr int NSC = (kRC * DB + kThreads - 1) / kThreads;
-    uint4 pk[NKQ], pq[NKQ];
+    uint4 pk[NKQ] = {}, pq[NKQ] = {};   // (bf16: halves x and y)
     float pdl[NSC][J];
     uint32_t plk[NSC][J], plq[NSC][J], plb[NSC][J], pdo[NSC];
-    auto fetch = [&](int n) {
+    auto fetch_as = [&](int n, auto otag) {
+        constexpr bool BF = IBF, OBF = decltype(otag)::value;
         const int t0 = n * kRC, nt = min(kRC, T - t0);
 #pragma unroll
         for (int x = 0; x < NKQ; ++x) {
-            const int e = tid + kThreads * x, t = e / (DK / 4), i = (e % (DK / 4)) * 4;
-            pk[x] = pq[x] = make_uint4(0u, 0u, 0u, 0u);
-            if (e < kRC * (DK / 4) && t < nt) {
-                const size_t off = ((size_t)(b * T + t0 + t) * H + h) * DK + i;
-                pk[x] = raw4(f.k, off, ibf);
-                pq[x] = raw4(f.q, off, ibf);
+            const int e = min(tid + kThreads * x, kRC * (DK / 4) - 1);
+            const int t = min(e / (DK / 4), nt - 1), i = (e % (DK / 4)) * 4;
+            const size_t off = ((size_t)(b * T + t0 + t) * H + h) * DK + i;
+            if constexpr (BF) {
+                const uint2 kk = *reinterpret_cast<const uint2 *>(static_cast<const uint16_t *>(f.k) + off);
+                const uint2 qq = *reinterpret_cast<const uint2 *>(static_cast<const uint16_t *>(f.q) + off);
+                pk[x].x = kk.x, pk[x].y = kk.y;
+                pq[x].x = qq.x, pq[x].y = qq.y;
+            } else {
+                pk[x] = *reinterpret_cast<const uint4 *>(static_cast<const float *>(f.k) + off);
+                pq[x] = *reinterpret_cast<const uint4 *>(static_cast<const float *>(f.q) + off);
             }
         }
 #pragma unroll
         for (int x = 0; x < NSC; ++x) {
-            const int e = tid + kThreads * x, t = e / DB, dd = e % DB;
-            pdo[x] = 0u;
+            const int e = min(tid + kThreads * x, kRC * DB - 1);
+            const int t = min(e / DB, nt - 1), dd = e % DB;
+            const size_t row = (size_t)(b * T + t0 + t) * H + h;
+            // dL/do has the output dtype
+            if constexpr (OBF) pdo[x] = static_cast<const uint16_t *>(a.grad_o)[row * Dv + d0 + dd];
+            else pdo[x] = static_cast<const uint32_t *>(a.grad_o)[row * Dv + d0 + dd];
 #pragma unroll
             for (int j = 0; j < J; ++j) {
-                pdl[x][j] = 0.0f;
-                plk[x][j] = plq[x][j] = plb[x][j] = 0u;
-            }
-            if (e < kRC * DB && t < nt) {
-                const size_t row = (size_t)(b * T + t0 + t) * H + h;
-                pdo[x] = raw1(a.grad_o, row * Dv + d0 + dd, obf);
-#pragma unroll
-                for (int j = 0; j < J; ++j) {
-                    const size_t idx = (row * J + j) * Dv + d0 + dd;
-                    pdl[x][j] = a.delta[idx];
-                    plk[x][j] = raw1(f.lk, idx, ibf);
-                    plq[x][j] = raw1(f.lq, idx, ibf);
-                    plb[x][j] = raw1(f.lb, idx, ibf);
+                const size_t idx = (row * J + j) * Dv + d0 + dd;
+                pdl[x][j] = a.delta[idx];
+                if constexpr (BF) {
+                    plk[x][j] = static_cast<const uint16_t *>(f.lk)[idx];
+                    plq[x][j] = static_cast<const uint16_t *>(f.lq)[idx];
+                    plb[x][j] = static_cast<const uint16_t *>(f.lb)[idx];
+                } else {
+                    plk[x][j] = static_cast<const uint32_t *>(f.lk)[idx];
+                    plq[x][j] = static_cast<const uint32_t *>(f.lq)[idx];
+                    plb[x][j] = static_cast<const uint32_t *>(f.lb)[idx];
                 }
             }
         }
+    };
+    auto fetch = [&](int n) {
+        if (obf) fetch_as(n, BTag<true>{});
+        else fetch_as(n, BTag<false>{});
     };
     // The chunk pass's operands, in its tile order [b, h, interval, tile, token,
     // dd, j]: the rows of one tile and consecutive tokens are contiguous, so each
@@ -264,7 +287,8 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
         for (int x = 0; x < NKQ; ++x) {
             const int e = tid + kThreads * x, t = e / (DK / 4), i = (e % (DK / 4)) * 4;
             if (e >= kRC * (DK / 4)) break;
-            const float4 kv = cvt4(pk[x], ibf), qv = cvt4(pq[x], ibf);
+            float4 kv = cvt4(pk[x], ibf), qv = cvt4(pq[x], ibf);
+            if (t >= nt) kv.x = kv.y = kv.z = kv.w = qv.x = qv.y = qv.z = qv.w = 0.0f;
             *reinterpret_cast<float4 *>(&sK[t][i]) = kv;
             *reinterpret_cast<float4 *>(&sQ[t][i]) = qv;
             sKt[i][t] = kv.x, sKt[i + 1][t] = kv.y, sKt[i + 2][t] = kv.z, sKt[i + 3][t] = kv.w;
@@ -830,9 +854,13 @@ hipError_t launch_reverse(const BackwardArgs &a, hipStream_t stream) {
     if constexpr ((J == 3 ? 4 : J) * DB > 64) {
         return hipErrorInvalidValue;
     } else {
-        hipLaunchKernelGGL((reverse_chunk_kernel<DK, J, DB>),
-                           dim3((unsigned)((a.f.Dv / DB) * a.f.H * a.f.B)), dim3(kThreads), 0,
-                           stream, a);
+        const dim3 grid((unsigned)((a.f.Dv / DB) * a.f.H * a.f.B));
+        if (a.f.in_bf16)
+            hipLaunchKernelGGL((reverse_chunk_kernel<DK, J, DB, true>), grid, dim3(kThreads), 0,
+                               stream, a);
+        else
+            hipLaunchKernelGGL((reverse_chunk_kernel<DK, J, DB, false>), grid, dim3(kThreads), 0,
+                               stream, a);
         return hipGetLastError();
     }
 }

@@ -90,6 +90,29 @@ def test_backward(B, H, T, Dk, Dv, J, dtype, std, gs):
     assert all(v <= tol for v in e.values()), e
 
 
+@pytest.mark.parametrize("dtype,go_dtype", [("bf16", "f32"), ("f32", "bf16")])
+def test_backward_grad_o_dtype_differs(dtype, go_dtype):
+    """dL/do in the other dtype than the inputs (it carries the forward's output
+    dtype): the gradients against the oracle fed the same rounded dL/do."""
+    import torch
+    import paper_2609_39034_amd as sw
+    B, H, T, Dk, Dv, J = 2, 2, 37, 64, 32, 4
+    inp = workloads.iid_inputs(B, H, T, Dk, Dv, J, dtype=dtype, seed=731, state_std=0.1)
+    dev = to_device(inp, dtype)
+    rng = np.random.default_rng(732)
+    go_dev = torch.from_numpy(rng.standard_normal((B, T, H, Dv)).astype(np.float32)).to(
+        "cuda", torch_dtype(go_dtype))
+    go = go_dev.float().cpu().numpy().astype(np.float64)
+    res = sw.backward(*(dev[n] for n in NAMES), dev["state"], go_dev, None)
+    torch.cuda.synchronize()
+    got = dict(zip(GRADS + ("state",), (x.cpu().numpy().astype(np.float64) for x in res)))
+    ref = ob.backward(*(inp[n] for n in NAMES), inp["state"], go, None)
+    e = _errs(got, ref)
+    tol = tol_for(dtype)
+    print(" ".join("%s %.2e" % kv for kv in e.items()), "(tol %.0e)" % tol)
+    assert all(v <= tol for v in e.values()), e
+
+
 def test_backward_empty_sequence():
     """T = 0: dL/dW_0 = dL/dW_T; nothing else is written."""
     import torch
