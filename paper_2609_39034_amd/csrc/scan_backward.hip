@@ -691,48 +691,76 @@ __global__ __launch_bounds__(kThreads) void bwd_chunk_kernel(BackwardArgs a) {
 
     // checkpoints of this chunk, [Dv][J][DK]
     const size_t ck0 = (((size_t)b * H + h) * NCH + n) * Dv * J * DK;
+    // A tile's HBM operands are loaded into registers while the previous tile
+    // computes: its state checkpoints S and E, and its per-(token, column)
+    // operands, contiguous in the reverse scan's tile order [token][dd][j].
+    // Every thread loads every item it owns (tokens past the end from the
+    // chunk's last row); the store to LDS zeroes them.
+    constexpr int NSE4 = DT * J * (DK / 4);                  // float4 of S (and of E)
+    constexpr int NSE = (NSE4 + kThreads - 1) / kThreads;
+    constexpr int NOP = (kCB * DT + kThreads - 1) / kThreads;
+    floatx4 rS[NSE], rE[NSE];   // (native vectors: an array of float4 went to scratch memory)
+    float rc[NOP][J], rp[NOP][J], rq[NOP][J], rd[NOP];
+    auto fetch_tile = [&](int dt0) {
+#pragma unroll
+        for (int x = 0; x < NSE; ++x) {
+            const size_t src = ck0 + (size_t)dt0 * J * DK + 4 * min(tid + kThreads * x, NSE4 - 1);
+            rS[x] = *reinterpret_cast<const floatx4 *>(a.wck + src);
+            rE[x] = *reinterpret_cast<const floatx4 *>(a.eck + src);
+        }
+        const size_t tb = ((((size_t)b * H + h) * NCH + n) * (Dv / DT) + dt0 / DT) * kCB;
+#pragma unroll
+        for (int x = 0; x < NOP; ++x) {
+            const int g = min(tid + kThreads * x, kCB * DT - 1);
+            const int t = min(g / DT, nt - 1), dd = g % DT;
+            const size_t row = (tb + t) * DT + dd;
+            lds_row<J>(a.cpk + row * J, rc[x]);
+            lds_row<J>(a.ppk + row * J, rp[x]);
+            lds_row<J>(a.qpk + row * J, rq[x]);
+            rd[x] = a.dopk[row];
+        }
+    };
+    fetch_tile(0);
     for (int dt0 = 0; dt0 < Dv; dt0 += DT) {
         block_sync_lds();   // the previous tile is consumed
-        for (int g = tid; g < DT * J * (DK / 4); g += kThreads) {
-            const int e = 4 * g;
+#pragma unroll
+        for (int x = 0; x < NSE; ++x) {
+            const int e = 4 * (tid + kThreads * x);
             const int dd = e / (J * DK), j = (e / DK) % J, i = e % DK;
-            const size_t src = ck0 + (size_t)dt0 * J * DK + e;
-            *reinterpret_cast<float4 *>(&sS[j * DT + dd][i]) =
-                *reinterpret_cast<const float4 *>(a.wck + src);
-            *reinterpret_cast<float4 *>(&sE[j * DT + dd][i]) =
-                *reinterpret_cast<const float4 *>(a.eck + src);
-        }
-        // this tile's per-(token, column) operands, contiguous in the reverse
-        // scan's tile order: [token][dd][j]
-        const size_t tb = ((((size_t)b * H + h) * NCH + n) * (Dv / DT) + dt0 / DT) * kCB;
-        for (int g = tid; g < kCB * DT; g += kThreads) {
-            const int t = g / DT, dd = g % DT;
-            float c[J], p[J], y[J], pq[J], dov = 0.0f;
-            if (t < nt) {
-                const size_t row = (tb + t) * DT + dd;
-                lds_row<J>(a.cpk + row * J, c);
-                lds_row<J>(a.ppk + row * J, p);
-                lds_row<J>(a.qpk + row * J, pq);
-                dov = a.dopk[row];
-#pragma unroll
-                for (int j = 0; j < J; ++j) y[j] = dov * pq[j];
-            } else {
-#pragma unroll
-                for (int j = 0; j < J; ++j) c[j] = p[j] = y[j] = pq[j] = 0.0f;
+            if (NSE4 % kThreads == 0 || e < 4 * NSE4) {
+                *reinterpret_cast<floatx4 *>(&sS[j * DT + dd][i]) = rS[x];
+                *reinterpret_cast<floatx4 *>(&sE[j * DT + dd][i]) = rE[x];
             }
-            sDo[t][dd] = dov;
+        }
+#pragma unroll
+        for (int x = 0; x < NOP; ++x) {
+            const int g = tid + kThreads * x;
+            const int t = g / DT, dd = g % DT;
+            const bool in = t < nt;
+            const float dov = in ? rd[x] : 0.0f;
+            float c[J], p[J], pq[J];
 #pragma unroll
             for (int j = 0; j < J; ++j) {
-                const int cc = j * DT + dd;
-                sC[t][cc] = c[j];
-                sP[t][cc] = p[j];
-                sY[t][cc] = y[j];
-                sCt[cc][t] = c[j];
-                sPt[cc][t] = p[j];
-                sPq[t][cc] = pq[j];
+                c[j] = in ? rc[x][j] : 0.0f;
+                p[j] = in ? rp[x][j] : 0.0f;
+                pq[j] = in ? rq[x][j] : 0.0f;
+            }
+            if ((kCB * DT) % kThreads == 0 || g < kCB * DT) {
+                sDo[t][dd] = dov;
+#pragma unroll
+                for (int j = 0; j < J; ++j) {
+                    const int cc = j * DT + dd;
+                    sC[t][cc] = c[j];
+                    sP[t][cc] = p[j];
+                    sY[t][cc] = dov * pq[j];
+                    sCt[cc][t] = c[j];
+                    sPt[cc][t] = p[j];
+                    sPq[t][cc] = pq[j];
+                }
             }
         }
         block_sync_lds();
+        if (dt0 + DT < Dv) fetch_tile(dt0 + DT);   // lands while this tile computes
 
         // dq += Y S; dk += P S + C E (this tile's columns)
 #pragma unroll 4
