@@ -128,7 +128,19 @@ __device__ __forceinline__ floatx4 mma(const uint32_t (&a)[4], const uint32_t (&
 }
 
 // IBF: bf16 inputs (the input dtype is fixed per instantiation, so that the
-// prefetch has one load variant; dL/do's dtype stays a run-time choice)
+// prefetch has one load variant; dL/do's dtype stays a run-time choice).
+//
+// Schedule.  fp32 inputs: per chunk, every thread stages the chunk, then the
+// Gram products, the base, the sequential wave's tokens (the other waves store
+// the chunk pass's operands meanwhile), and the update of E, each step between
+// block barriers.  bf16 inputs: the staged inputs have two slots (chunk m in
+// slot m & 1) and three barriers per chunk:
+//   A  the sequential wave runs chunk n's tokens; the other waves store its
+//      operands for the chunk pass, stage chunk n-1 into the other slot from
+//      registers and issue the loads of chunk n-2
+//   B  E += Q_n^T Y_n + K_n^T P_n, chunk n's outputs, the Gram products of
+//      chunk n-1
+//   C  the base of chunk n-1 from the new E.
 template <int DK, int J, int DB, bool IBF>
 __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a) {
     constexpr int JP = J == 3 ? 4 : J;   // lanes per output dim (J = 3 padded)
@@ -139,16 +151,18 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
     static_assert(NL <= 64 && kBwdChunk % kRC == 0 && N % 4 == 0, "one sequential wave");
     static_assert(DB % chunk_tile_dims<J>() == 0 || chunk_tile_dims<J>() % DB == 0,
                   "a block covers whole tiles of the chunk pass, or a part of one");
+    constexpr int NS = IBF ? 2 : 1;      // slots of the staged inputs
+    constexpr int KT = IBF ? 1 : DK;     // rows of K and Q transposed (fp32 products only)
 
     __shared__ __align__(16) float sE[DK][CP];
-    __shared__ __align__(16) float sK[kRC][KP], sQ[kRC][KP];    // rows t
-    __shared__ __align__(16) float sKt[DK][GP], sQt[DK][GP];    // the same, [i][t]
-    __shared__ __align__(16) float sGkk[kRC][GP];               // k_t . k_s (symmetric)
-    __shared__ __align__(16) float sGkqT[kRC][GP];              // [s][t] = k_t . q_s
-    __shared__ __align__(16) float sBase[kRC][CP], sY[kRC][CP], sP[kRC][CP];
-    __shared__ float sDelta[kRC][CP], sBeta[kRC][CP], sR[kRC][CP];
+    __shared__ __align__(16) float sK[NS][kRC][KP], sQ[NS][kRC][KP];   // rows t
+    __shared__ __align__(16) float sKt[KT][GP], sQt[KT][GP];           // the same, [i][t]
+    __shared__ __align__(16) float sGkk[kRC][GP];                      // k_t . k_s (symmetric)
+    __shared__ __align__(16) float sGkqT[kRC][GP];                     // [s][t] = k_t . q_s
+    __shared__ __align__(16) float sBase[kRC][CP], sY[NS][kRC][CP], sP[kRC][CP];
+    __shared__ float sDelta[NS][kRC][CP], sBeta[NS][kRC][CP], sR[NS][kRC][CP];
     __shared__ float sDlb[kRC][CP], sDlk[kRC][CP], sDv[kRC][DB];
-    __shared__ float sPq[kRC][CP], sDo[kRC][DB];                // pi^q, dL/do
+    __shared__ float sPq[NS][kRC][CP], sDo[NS][kRC][DB];               // pi^q, dL/do
 
     const LayerArgs &f = a.f;
     const int tid = threadIdx.x, lane = tid % 64;
@@ -189,24 +203,26 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
     const bool sact = tid < 64 && lane < NL && sj < J;
     const int scol = sact ? sj * DB + sdd : 0;
 
-    // Each chunk's HBM inputs are fetched into registers while the previous
-    // (later) chunk computes: K and Q rows as float4, and per (token, output
-    // dim) the J errors and logits and dL/do.  Every thread loads every item it
-    // owns, from a clamped row (the chunk's last token, the last item), with
-    // the input dtype fixed at compile time: no load sits behind a branch
-    // (a load there is waited for at the join); staging zeroes what lies past
-    // the end.
-    constexpr int NKQ = (kRC * (DK / 4) + kThreads - 1) / kThreads;
-    constexpr int NSC = (kRC * DB + kThreads - 1) / kThreads;
+    // Each chunk's HBM inputs are fetched into registers while a later chunk
+    // computes: K and Q rows as float4, and per (token, output dim) the J
+    // errors and logits and dL/do.  The staging threads (F0 .. kThreads - 1)
+    // load them and later stage them.  Every such thread loads every item it
+    // owns, from a clamped row (the chunk's last token, the last item), with the
+    // input dtype fixed at compile time: no load sits behind a branch (a load
+    // there is waited for at the join); staging zeroes what lies past the end.
+    constexpr int F0 = IBF ? 64 : 0, FT = kThreads - F0;
+    constexpr int NKQ = (kRC * (DK / 4) + FT - 1) / FT;
+    constexpr int NSC = (kRC * DB + FT - 1) / FT;
     uint4 pk[NKQ] = {}, pq[NKQ] = {};   // (bf16: halves x and y)
     float pdl[NSC][J];
     uint32_t plk[NSC][J], plq[NSC][J], plb[NSC][J], pdo[NSC];
+    const int ft = tid - F0;   // index among the staging threads (when >= 0)
     auto fetch_as = [&](int n, auto otag) {
         constexpr bool BF = IBF, OBF = decltype(otag)::value;
         const int t0 = n * kRC, nt = min(kRC, T - t0);
 #pragma unroll
         for (int x = 0; x < NKQ; ++x) {
-            const int e = min(tid + kThreads * x, kRC * (DK / 4) - 1);
+            const int e = min(ft + FT * x, kRC * (DK / 4) - 1);
             const int t = min(e / (DK / 4), nt - 1), i = (e % (DK / 4)) * 4;
             const size_t off = ((size_t)(b * T + t0 + t) * H + h) * DK + i;
             if constexpr (BF) {
@@ -221,7 +237,7 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
         }
 #pragma unroll
         for (int x = 0; x < NSC; ++x) {
-            const int e = min(tid + kThreads * x, kRC * DB - 1);
+            const int e = min(ft + FT * x, kRC * DB - 1);
             const int t = min(e / DB, nt - 1), dd = e % DB;
             const size_t row = (size_t)(b * T + t0 + t) * H + h;
             // dL/do has the output dtype
@@ -247,59 +263,30 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
         if (obf) fetch_as(n, BTag<true>{});
         else fetch_as(n, BTag<false>{});
     };
-    // The chunk pass's operands, in its tile order [b, h, interval, tile, token,
-    // dd, j]: the rows of one tile and consecutive tokens are contiguous, so each
-    // store run covers whole lines.  This block's dims cover TW dims of each tile
-    // it touches (all of them, or a part when the block is narrower than a
-    // tile).  Threads first .. first + nthr - 1 store X[t][col] for the chunk's
-    // tokens (trip counts and divisors compile-time; tokens past the end skipped).
-    constexpr int CT = chunk_tile_dims<J>();
-    constexpr int TW = DB < CT ? DB : CT;
-    auto pack_index = [&](int t0, int t, int d) {
-        const size_t pbase = ((size_t)b * H + h) * NC2 + t0 / kBwdChunk;
-        return ((pbase * (Dv / CT) + d / CT) * kBwdChunk + t0 % kBwdChunk + t) * CT + d % CT;
-    };
-    auto pack_store = [&](float *dst, const float (*X)[CP], int t0, int nt, int first, int nthr) {
-        constexpr int NE = kRC * J * DB;
-        for (int e = tid - first; e < NE; e += nthr) {
-            const int j = e % J, w = (e / J) % TW, t = (e / (J * TW)) % kRC,
-                      kk = e / (J * TW * kRC);
-            const int dd = kk * TW + w;
-            if (t < nt) dst[pack_index(t0, t, d0 + dd) * J + j] = X[t][j * DB + dd];
-        }
-    };
-    fetch(NCH - 1);
-
-    for (int n = NCH - 1; n >= 0; --n) {
+    // chunk n's registers to slot sl: K, Q (and their transposes for the fp32
+    // products), delta, r, beta, pi^q, dy = dL/do pi^q and dL/do
+    auto stage = [&](int n, int sl) {
         const int t0 = n * kRC, nt = min(kRC, T - t0);
-        block_sync_lds();   // E is complete; the previous chunk's staging is consumed
-        // E_m (the gradient from the tokens after checkpoint interval m) before
-        // the interval's last reverse chunk runs: [.., m, d, j, i]
-        if (n % R2 == R2 - 1 || n == NCH - 1) {
-            const int m = n / R2;
-            float *ck = a.eck + (((size_t)b * H + h) * NC2 + m) * Dv * J * DK;
-            for (int e = tid; e < DB * J * DK; e += kThreads) {
-                const int dd = e / (J * DK), j = (e / DK) % J, i = e % DK;
-                ck[(size_t)(d0 + dd) * J * DK + j * DK + i] = sE[i][j * DB + dd];
+#pragma unroll
+        for (int x = 0; x < NKQ; ++x) {
+            const int e = ft + FT * x, t = e / (DK / 4), i = (e % (DK / 4)) * 4;
+            if ((kRC * (DK / 4)) % FT == 0 || e < kRC * (DK / 4)) {
+                float4 kv = cvt4(pk[x], ibf), qv = cvt4(pq[x], ibf);
+                if (t >= nt) kv.x = kv.y = kv.z = kv.w = qv.x = qv.y = qv.z = qv.w = 0.0f;
+                *reinterpret_cast<float4 *>(&sK[sl][t][i]) = kv;
+                *reinterpret_cast<float4 *>(&sQ[sl][t][i]) = qv;
+                if constexpr (!IBF) {
+                    sKt[i][t] = kv.x, sKt[i + 1][t] = kv.y, sKt[i + 2][t] = kv.z, sKt[i + 3][t] = kv.w;
+                    sQt[i][t] = qv.x, sQt[i + 1][t] = qv.y, sQt[i + 2][t] = qv.z, sQt[i + 3][t] = qv.w;
+                }
             }
         }
 #pragma unroll
-        for (int x = 0; x < NKQ; ++x) {
-            const int e = tid + kThreads * x, t = e / (DK / 4), i = (e % (DK / 4)) * 4;
-            if (e >= kRC * (DK / 4)) break;
-            float4 kv = cvt4(pk[x], ibf), qv = cvt4(pq[x], ibf);
-            if (t >= nt) kv.x = kv.y = kv.z = kv.w = qv.x = qv.y = qv.z = qv.w = 0.0f;
-            *reinterpret_cast<float4 *>(&sK[t][i]) = kv;
-            *reinterpret_cast<float4 *>(&sQ[t][i]) = qv;
-            sKt[i][t] = kv.x, sKt[i + 1][t] = kv.y, sKt[i + 2][t] = kv.z, sKt[i + 3][t] = kv.w;
-            sQt[i][t] = qv.x, sQt[i + 1][t] = qv.y, sQt[i + 2][t] = qv.z, sQt[i + 3][t] = qv.w;
-        }
-#pragma unroll
         for (int x = 0; x < NSC; ++x) {
-            const int e = tid + kThreads * x, t = e / DB, dd = e % DB;
-            if (e >= kRC * DB) break;
+            const int e = ft + FT * x, t = e / DB, dd = e % DB;
+            if ((kRC * DB) % FT != 0 && e >= kRC * DB) continue;
             float dl[J], ee[J], lq[J], be[J];
-            const float dov = cvt1(pdo[x], obf);
+            const float dov = t < nt ? cvt1(pdo[x], obf) : 0.0f;
             if (t < nt) {
                 float m = -INFINITY, mq = -INFINITY;
 #pragma unroll
@@ -332,28 +319,71 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
 #pragma unroll
             for (int j = 0; j < J; ++j) {
                 const int col = j * DB + dd;
-                sDelta[t][col] = dl[j];
-                sR[t][col] = ee[j];
-                sBeta[t][col] = be[j];
-                sY[t][col] = dov * lq[j];
-                sPq[t][col] = lq[j];
+                sDelta[sl][t][col] = dl[j];
+                sR[sl][t][col] = ee[j];
+                sBeta[sl][t][col] = be[j];
+                sY[sl][t][col] = dov * lq[j];
+                sPq[sl][t][col] = lq[j];
             }
-            sDo[t][dd] = dov;
+            sDo[sl][t][dd] = dov;
         }
-        block_sync_lds();
-        if (n > 0) fetch(n - 1);   // lands while this chunk computes
-        // Gram products of the chunk: on the matrix cores (bf16 inputs; wave 0
-        // K K^T, wave 1 K Q^T), else one (t, s) pair per thread
-        if (ibf) {
+    };
+    // The chunk pass's operands, in its tile order [b, h, interval, tile, token,
+    // dd, j]: the rows of one tile and consecutive tokens are contiguous, so each
+    // store run covers whole lines.  This block's dims cover TW dims of each tile
+    // it touches (all of them, or a part when the block is narrower than a
+    // tile).  Threads first .. first + nthr - 1 store X[t][col] for the chunk's
+    // tokens (trip counts and divisors compile-time; tokens past the end skipped).
+    constexpr int CT = chunk_tile_dims<J>();
+    constexpr int TW = DB < CT ? DB : CT;
+    auto pack_index = [&](int t0, int t, int d) {
+        const size_t pbase = ((size_t)b * H + h) * NC2 + t0 / kBwdChunk;
+        return ((pbase * (Dv / CT) + d / CT) * kBwdChunk + t0 % kBwdChunk + t) * CT + d % CT;
+    };
+    auto pack_store = [&](float *dst, const float (*X)[CP], int t0, int nt, int first, int nthr) {
+        constexpr int NE = kRC * J * DB;
+        for (int e = tid - first; e < NE; e += nthr) {
+            const int j = e % J, w = (e / J) % TW, t = (e / (J * TW)) % kRC,
+                      kk = e / (J * TW * kRC);
+            const int dd = kk * TW + w;
+            if (t < nt) dst[pack_index(t0, t, d0 + dd) * J + j] = X[t][j * DB + dd];
+        }
+    };
+    // pi^q and dL/do of chunk n for the chunk pass, by threads 64 .. kThreads - 1
+    // (the sequential wave stores c = beta r delta and dpred)
+    auto packs = [&](int n, int sl) {
+        const int t0 = n * kRC, nt = min(kRC, T - t0);
+        pack_store(a.qpk, sPq[sl], t0, nt, 64, kThreads - 64);
+        for (int e = tid - 64; e < kRC * DB; e += kThreads - 64) {
+            const int w = e % TW, t = (e / TW) % kRC, kk = e / (TW * kRC);
+            if (t < nt) a.dopk[pack_index(t0, t, d0 + kk * TW + w)] = sDo[sl][t][kk * TW + w];
+        }
+    };
+    // E_m (the gradient from the tokens after checkpoint interval m) before
+    // the interval's last reverse chunk runs: [.., m, d, j, i]
+    auto checkpoint = [&](int n, int first, int nthr) {
+        if (n % R2 == R2 - 1 || n == NCH - 1) {
+            const int m = n / R2;
+            float *ck = a.eck + (((size_t)b * H + h) * NC2 + m) * Dv * J * DK;
+            for (int e = tid - first; e < DB * J * DK; e += nthr) {
+                const int dd = e / (J * DK), j = (e / DK) % J, i = e % DK;
+                ck[(size_t)(d0 + dd) * J * DK + j * DK + i] = sE[i][j * DB + dd];
+            }
+        }
+    };
+    // Gram products of the chunk in slot sl: on the matrix cores (bf16 inputs;
+    // wave 0 K K^T, wave 1 K Q^T), else one (t, s) pair per thread
+    auto gram = [&](int sl) {
+        if constexpr (IBF) {
             if (wv < 2) {
                 // D[row][col] = sum_i A[row][i] K[col][i], A = K (D[t][s]) or Q
                 // (D[s][t] = k_t . q_s); lane: row / col tl, k slot lg
-                const float (*A)[KP] = wv == 0 ? sK : sQ;
+                const float (*A)[KP] = wv == 0 ? sK[sl] : sQ[sl];
                 floatx4 acc = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                 for (int i0 = 0; i0 < DK; i0 += KM * 4) {
                     const KOp<KM> a8 = kop_exact<KM>(&A[tl][i0 + KM * lg]);
-                    const KOp<KM> b8 = kop_exact<KM>(&sK[tl][i0 + KM * lg]);
+                    const KOp<KM> b8 = kop_exact<KM>(&sK[sl][tl][i0 + KM * lg]);
                     acc = mma(a8.hi, b8.hi, acc);
                 }
 #pragma unroll
@@ -367,26 +397,28 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
             float gkk = 0.0f, gkq = 0.0f;
 #pragma unroll 4
             for (int i = 0; i < DK; i += 4) {
-                const float4 kt = *reinterpret_cast<const float4 *>(&sK[t][i]);
-                const float4 ks = *reinterpret_cast<const float4 *>(&sK[s2][i]);
-                const float4 qs = *reinterpret_cast<const float4 *>(&sQ[s2][i]);
+                const float4 kt = *reinterpret_cast<const float4 *>(&sK[sl][t][i]);
+                const float4 ks = *reinterpret_cast<const float4 *>(&sK[sl][s2][i]);
+                const float4 qs = *reinterpret_cast<const float4 *>(&sQ[sl][s2][i]);
                 gkk = fmaf(kt.x, ks.x, fmaf(kt.y, ks.y, fmaf(kt.z, ks.z, fmaf(kt.w, ks.w, gkk))));
                 gkq = fmaf(kt.x, qs.x, fmaf(kt.y, qs.y, fmaf(kt.z, qs.z, fmaf(kt.w, qs.w, gkq))));
             }
             sGkk[t][s2] = gkk;
             sGkqT[s2][t] = gkq;
         }
-        block_sync_lds();
-        // base_t = k_t . E + sum_{s>=t} (k_t . q_s) dy_s: a 16-column tile per
-        // wave on the matrix cores (bf16 inputs), else four tokens per thread
-        if (ibf) {
+    };
+    // base_t = k_t . E + sum_{s>=t} (k_t . q_s) dy_s for the chunk in slot sl: a
+    // 16-column tile per wave on the matrix cores (bf16 inputs), else four
+    // tokens per thread
+    auto base = [&](int sl) {
+        if constexpr (IBF) {
             for (int ct = wv; ct < NTC; ct += kThreads / 64) {
                 const int col = 16 * ct + tl;
                 const bool cv = col < N;
                 floatx4 acc = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                 for (int i0 = 0; i0 < DK; i0 += KM * 4) {
-                    const KOp<KM> a8 = kop_exact<KM>(&sK[tl][i0 + KM * lg]);   // K[t = tl][i]
+                    const KOp<KM> a8 = kop_exact<KM>(&sK[sl][tl][i0 + KM * lg]);   // K[t = tl][i]
                     float ev[KM];
 #pragma unroll
                     for (int m = 0; m < KM; ++m) ev[m] = cv ? sE[i0 + KM * lg + m][col] : 0.0f;
@@ -400,7 +432,7 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
                 for (int m = 0; m < 4; ++m) {
                     const int s2 = 4 * lg + m;
                     gv[m] = s2 >= tl ? sGkqT[s2][tl] : 0.0f;
-                    yv[m] = cv ? sY[s2][col] : 0.0f;
+                    yv[m] = cv ? sY[sl][s2][col] : 0.0f;
                 }
                 const KOp<4> ga = kop_split<4>(gv), yb = kop_split<4>(yv);
                 acc = mma(ga.hi, yb.hi, acc);
@@ -411,91 +443,85 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
                     for (int r = 0; r < 4; ++r) sBase[4 * lg + r][col] = acc[r];
                 }
             }
-        } else
-        for (int e = tid; e < (kRC / 4) * N; e += kThreads) {
-            const int t4 = (e / N) * 4, col = e % N;
-            float acc[4] = {0.f, 0.f, 0.f, 0.f};
+        } else {
+            for (int e = tid; e < (kRC / 4) * N; e += kThreads) {
+                const int t4 = (e / N) * 4, col = e % N;
+                float acc[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll 8
-            for (int i = 0; i < DK; ++i) {
-                const float4 kv = *reinterpret_cast<const float4 *>(&sKt[i][t4]);
-                const float ev = sE[i][col];
-                acc[0] = fmaf(kv.x, ev, acc[0]);
-                acc[1] = fmaf(kv.y, ev, acc[1]);
-                acc[2] = fmaf(kv.z, ev, acc[2]);
-                acc[3] = fmaf(kv.w, ev, acc[3]);
-            }
-            for (int s2 = t4; s2 < kRC; ++s2) {
-                const float4 gq = *reinterpret_cast<const float4 *>(&sGkqT[s2][t4]);
-                const float yv = sY[s2][col];
-                // only s >= t: token t4 + x takes s2 >= t4 + x
-                acc[0] = fmaf(gq.x, yv, acc[0]);
-                if (s2 >= t4 + 1) acc[1] = fmaf(gq.y, yv, acc[1]);
-                if (s2 >= t4 + 2) acc[2] = fmaf(gq.z, yv, acc[2]);
-                if (s2 >= t4 + 3) acc[3] = fmaf(gq.w, yv, acc[3]);
-            }
-#pragma unroll
-            for (int x = 0; x < 4; ++x) sBase[t4 + x][col] = acc[x];
-        }
-        block_sync_lds();
-        if (tid >= 64) {
-            // while the sequential wave runs (it stores c = beta r delta and dpred
-            // for the chunk pass), the other waves store pi^q and dL/do
-            pack_store(a.qpk, sPq, t0, nt, 64, kThreads - 64);
-            for (int e = tid - 64; e < kRC * DB; e += kThreads - 64) {
-                const int w = e % TW, t = (e / TW) % kRC, kk = e / (TW * kRC);
-                if (t < nt) a.dopk[pack_index(t0, t, d0 + kk * TW + w)] = sDo[t][kk * TW + w];
-            }
-        }
-        if (tid < 64) {
-            // the chunk's tokens in reverse; dfr[u] collects sum_{s>u} (k_u . k_s) dpred_s
-            float dfr[kRC], vb[kRC], vd[kRC], vbe[kRC], vr[kRC];
-            // this lane's column in the chunk pass's tile order: token t of the
-            // chunk at t * CT * J floats on (tokens past the end land in the
-            // padding of the last interval, inside the buffer)
-            const size_t pl = pack_index(t0, 0, d0 + sdd) * J + sj;
-            float *const cl = a.cpk + pl, *const plp = a.ppk + pl;
-#pragma unroll
-            for (int u = 0; u < kRC; ++u) {
-                dfr[u] = 0.0f;
-                vb[u] = sact ? sBase[u][scol] : 0.0f;
-                vd[u] = sact ? sDelta[u][scol] : 0.0f;
-                vbe[u] = sact ? sBeta[u][scol] : 0.0f;
-                vr[u] = sact ? sR[u][scol] : 0.0f;
-            }
-#pragma unroll
-            for (int t = kRC - 1; t >= 0; --t) {
-                float grow[kRC];   // row t of K K^T (= column t), the part u < t
-#pragma unroll
-                for (int u4 = 0; u4 < (t + 3) / 4; ++u4) {
-                    const float4 x = *reinterpret_cast<const float4 *>(&sGkk[t][4 * u4]);
-                    grow[4 * u4] = x.x, grow[4 * u4 + 1] = x.y;
-                    grow[4 * u4 + 2] = x.z, grow[4 * u4 + 3] = x.w;
+                for (int i = 0; i < DK; ++i) {
+                    const float4 kv = *reinterpret_cast<const float4 *>(&sKt[i][t4]);
+                    const float ev = sE[i][col];
+                    acc[0] = fmaf(kv.x, ev, acc[0]);
+                    acc[1] = fmaf(kv.y, ev, acc[1]);
+                    acc[2] = fmaf(kv.z, ev, acc[2]);
+                    acc[3] = fmaf(kv.w, ev, acc[3]);
                 }
-                const float dc = vb[t] + dfr[t];
-                const float dl = vd[t], be = vbe[t], r = vr[t];
-                const float dr = dc * be * dl;
-                const float sdr = group_sum<JP>(r * dr);
-                const float da = J == 1 ? 0.0f : r * (dr - sdr);
-                const float ddelta = dc * be * r - dl * da;
-                const float dvv = group_sum<JP>(ddelta);
-                const float dpred = -ddelta;
-#pragma unroll
-                for (int u = 0; u < t; ++u) dfr[u] = fmaf(grow[u], dpred, dfr[u]);
-                if (sact) {
-                    sP[t][scol] = dpred;
-                    sDlb[t][scol] = dc * r * dl * be * (1.0f - be);
-                    sDlk[t][scol] = da;
-                    if (sj == 0) sDv[t][sdd] = dvv;
-                    cl[t * CT * J] = be * r * dl;
-                    plp[t * CT * J] = dpred;
+                for (int s2 = t4; s2 < kRC; ++s2) {
+                    const float4 gq = *reinterpret_cast<const float4 *>(&sGkqT[s2][t4]);
+                    const float yv = sY[sl][s2][col];
+                    // only s >= t: token t4 + x takes s2 >= t4 + x
+                    acc[0] = fmaf(gq.x, yv, acc[0]);
+                    if (s2 >= t4 + 1) acc[1] = fmaf(gq.y, yv, acc[1]);
+                    if (s2 >= t4 + 2) acc[2] = fmaf(gq.z, yv, acc[2]);
+                    if (s2 >= t4 + 3) acc[3] = fmaf(gq.w, yv, acc[3]);
                 }
+#pragma unroll
+                for (int x = 0; x < 4; ++x) sBase[t4 + x][col] = acc[x];
             }
         }
-        block_sync_lds();
-        // E += Q^T Y + K^T P (E now from the tokens after the previous chunk):
-        // 16 x 16 tiles of E on the matrix cores (bf16 inputs), else four
-        // columns per thread
-        if (ibf) {
+    };
+    // the chunk's tokens in reverse, by the sequential wave (tid < 64)
+    auto tokens = [&](int n, int sl) {
+        const int t0 = n * kRC;
+        // dfr[u] collects sum_{s>u} (k_u . k_s) dpred_s
+        float dfr[kRC], vb[kRC], vd[kRC], vbe[kRC], vr[kRC];
+        // this lane's column in the chunk pass's tile order: token t of the
+        // chunk at t * CT * J floats on (tokens past the end land in the
+        // padding of the last interval, inside the buffer)
+        const size_t pl = pack_index(t0, 0, d0 + sdd) * J + sj;
+        float *const cl = a.cpk + pl, *const plp = a.ppk + pl;
+#pragma unroll
+        for (int u = 0; u < kRC; ++u) {
+            dfr[u] = 0.0f;
+            vb[u] = sact ? sBase[u][scol] : 0.0f;
+            vd[u] = sact ? sDelta[sl][u][scol] : 0.0f;
+            vbe[u] = sact ? sBeta[sl][u][scol] : 0.0f;
+            vr[u] = sact ? sR[sl][u][scol] : 0.0f;
+        }
+#pragma unroll
+        for (int t = kRC - 1; t >= 0; --t) {
+            float grow[kRC];   // row t of K K^T (= column t), the part u < t
+#pragma unroll
+            for (int u4 = 0; u4 < (t + 3) / 4; ++u4) {
+                const float4 x = *reinterpret_cast<const float4 *>(&sGkk[t][4 * u4]);
+                grow[4 * u4] = x.x, grow[4 * u4 + 1] = x.y;
+                grow[4 * u4 + 2] = x.z, grow[4 * u4 + 3] = x.w;
+            }
+            const float dc = vb[t] + dfr[t];
+            const float dl = vd[t], be = vbe[t], r = vr[t];
+            const float dr = dc * be * dl;
+            const float sdr = group_sum<JP>(r * dr);
+            const float da = J == 1 ? 0.0f : r * (dr - sdr);
+            const float ddelta = dc * be * r - dl * da;
+            const float dvv = group_sum<JP>(ddelta);
+            const float dpred = -ddelta;
+#pragma unroll
+            for (int u = 0; u < t; ++u) dfr[u] = fmaf(grow[u], dpred, dfr[u]);
+            if (sact) {
+                sP[t][scol] = dpred;
+                sDlb[t][scol] = dc * r * dl * be * (1.0f - be);
+                sDlk[t][scol] = da;
+                if (sj == 0) sDv[t][sdd] = dvv;
+                cl[t * CT * J] = be * r * dl;
+                plp[t * CT * J] = dpred;
+            }
+        }
+    };
+    // E += Q^T Y + K^T P for the chunk in slot sl (E then holds the gradient
+    // from the tokens after the previous chunk): 16 x 16 tiles of E on the
+    // matrix cores (bf16 inputs), else four columns per thread
+    auto update_e = [&](int sl) {
+        if constexpr (IBF) {
             for (int tile = wv; tile < (DK / 16) * NTC; tile += kThreads / 64) {
                 const int ti = tile / NTC, ct = tile % NTC;
                 const int col = 16 * ct + tl;
@@ -504,14 +530,15 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
 #pragma unroll
                 for (int r = 0; r < 4; ++r) acc[r] = cv ? sE[16 * ti + 4 * lg + r][col] : 0.0f;
                 // A = Q^T, K^T: rows i = 16 ti + tl, k = t = 4 lg .. + 3
-                const KOp<4> qa = kop_exact<4>(&sQt[16 * ti + tl][4 * lg]);
-                const KOp<4> ka = kop_exact<4>(&sKt[16 * ti + tl][4 * lg]);
-                float yv[4], pv[4];
+                float qv[4], kv[4], yv[4], pv[4];
 #pragma unroll
                 for (int m = 0; m < 4; ++m) {
-                    yv[m] = cv ? sY[4 * lg + m][col] : 0.0f;
+                    qv[m] = sQ[sl][4 * lg + m][16 * ti + tl];
+                    kv[m] = sK[sl][4 * lg + m][16 * ti + tl];
+                    yv[m] = cv ? sY[sl][4 * lg + m][col] : 0.0f;
                     pv[m] = cv ? sP[4 * lg + m][col] : 0.0f;
                 }
+                const KOp<4> qa = kop_exact<4>(qv), ka = kop_exact<4>(kv);
                 const KOp<4> yb = kop_split<4>(yv), pb = kop_split<4>(pv);
                 acc = mma(qa.hi, yb.hi, acc);
                 acc = mma(qa.hi, yb.lo, acc);
@@ -522,28 +549,32 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
                     for (int r = 0; r < 4; ++r) sE[16 * ti + 4 * lg + r][col] = acc[r];
                 }
             }
-        } else
-        for (int e = tid; e < DK * (N / 4); e += kThreads) {
-            const int i = e / (N / 4), c4 = (e % (N / 4)) * 4;
-            float4 acc = *reinterpret_cast<const float4 *>(&sE[i][c4]);
+        } else {
+            for (int e = tid; e < DK * (N / 4); e += kThreads) {
+                const int i = e / (N / 4), c4 = (e % (N / 4)) * 4;
+                float4 acc = *reinterpret_cast<const float4 *>(&sE[i][c4]);
 #pragma unroll
-            for (int t4 = 0; t4 < kRC; t4 += 4) {
-                const float4 qv = *reinterpret_cast<const float4 *>(&sQt[i][t4]);
-                const float4 kv = *reinterpret_cast<const float4 *>(&sKt[i][t4]);
-                const float qa[4] = {qv.x, qv.y, qv.z, qv.w}, ka[4] = {kv.x, kv.y, kv.z, kv.w};
+                for (int t4 = 0; t4 < kRC; t4 += 4) {
+                    const float4 qv = *reinterpret_cast<const float4 *>(&sQt[i][t4]);
+                    const float4 kv = *reinterpret_cast<const float4 *>(&sKt[i][t4]);
+                    const float qa[4] = {qv.x, qv.y, qv.z, qv.w}, ka[4] = {kv.x, kv.y, kv.z, kv.w};
 #pragma unroll
-                for (int x = 0; x < 4; ++x) {
-                    const float4 y = *reinterpret_cast<const float4 *>(&sY[t4 + x][c4]);
-                    const float4 p = *reinterpret_cast<const float4 *>(&sP[t4 + x][c4]);
-                    acc.x = fmaf(qa[x], y.x, fmaf(ka[x], p.x, acc.x));
-                    acc.y = fmaf(qa[x], y.y, fmaf(ka[x], p.y, acc.y));
-                    acc.z = fmaf(qa[x], y.z, fmaf(ka[x], p.z, acc.z));
-                    acc.w = fmaf(qa[x], y.w, fmaf(ka[x], p.w, acc.w));
+                    for (int x = 0; x < 4; ++x) {
+                        const float4 y = *reinterpret_cast<const float4 *>(&sY[sl][t4 + x][c4]);
+                        const float4 p = *reinterpret_cast<const float4 *>(&sP[t4 + x][c4]);
+                        acc.x = fmaf(qa[x], y.x, fmaf(ka[x], p.x, acc.x));
+                        acc.y = fmaf(qa[x], y.y, fmaf(ka[x], p.y, acc.y));
+                        acc.z = fmaf(qa[x], y.z, fmaf(ka[x], p.z, acc.z));
+                        acc.w = fmaf(qa[x], y.w, fmaf(ka[x], p.w, acc.w));
+                    }
                 }
+                *reinterpret_cast<float4 *>(&sE[i][c4]) = acc;
             }
-            *reinterpret_cast<float4 *>(&sE[i][c4]) = acc;
         }
-        // the chunk's per-token outputs, coalesced over output dims
+    };
+    // the chunk's per-token outputs, coalesced over output dims
+    auto outputs = [&](int n) {
+        const int t0 = n * kRC, nt = min(kRC, T - t0);
         for (int e = tid; e < nt * J * DB; e += kThreads) {
             const int t = e / (J * DB), j = (e / DB) % J, dd = e % DB;
             const int col = j * DB + dd;
@@ -554,6 +585,59 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
         for (int e = tid; e < nt * DB; e += kThreads) {
             const int t = e / DB, dd = e % DB;
             a.dv[((size_t)(b * T + t0 + t) * H + h) * Dv + d0 + dd] = sDv[t][dd];
+        }
+    };
+
+    if constexpr (IBF) {
+        if (NCH > 0) {
+            const int n0 = NCH - 1;
+            if (tid >= F0) {
+                fetch(n0);
+                stage(n0, n0 & 1);
+                if (n0 > 0) fetch(n0 - 1);
+            }
+            block_sync_lds();
+            gram(n0 & 1);
+            block_sync_lds();
+            base(n0 & 1);
+            for (int n = n0; n >= 0; --n) {
+                const int sl = n & 1;
+                block_sync_lds();   // A: the base of chunk n and E are complete
+                if (tid < 64) {
+                    tokens(n, sl);
+                } else {
+                    checkpoint(n, 64, kThreads - 64);
+                    packs(n, sl);
+                    if (n > 0) {
+                        stage(n - 1, sl ^ 1);
+                        if (n > 1) fetch(n - 2);   // lands during chunks n and n - 1
+                    }
+                }
+                block_sync_lds();   // B: chunk n's dpred published
+                update_e(sl);
+                outputs(n);
+                if (n > 0) gram(sl ^ 1);
+                block_sync_lds();   // C: E now from the tokens after chunk n - 1
+                if (n > 0) base(sl ^ 1);
+            }
+        }
+    } else {
+        if (NCH > 0) fetch(NCH - 1);
+        for (int n = NCH - 1; n >= 0; --n) {
+            block_sync_lds();   // E is complete; the previous chunk's staging is consumed
+            checkpoint(n, 0, kThreads);
+            stage(n, 0);
+            block_sync_lds();
+            if (n > 0) fetch(n - 1);   // lands while this chunk computes
+            gram(0);
+            block_sync_lds();
+            base(0);
+            block_sync_lds();
+            if (tid >= 64) packs(n, 0);
+            if (tid < 64) tokens(n, 0);
+            block_sync_lds();
+            update_e(0);
+            outputs(n);
         }
     }
     block_sync_lds();
