@@ -161,7 +161,7 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
     __shared__ __align__(16) float sGkqT[kRC][GP];                     // [s][t] = k_t . q_s
     __shared__ __align__(16) float sBase[kRC][CP], sY[NS][kRC][CP], sP[kRC][CP];
     __shared__ float sDelta[NS][kRC][CP], sBeta[NS][kRC][CP], sR[NS][kRC][CP];
-    __shared__ float sDlb[kRC][CP], sDlk[kRC][CP], sDv[kRC][DB];
+    __shared__ float sDlb[kRC][CP], sDlk[kRC][CP], sDv[kRC][DB + 1];
     __shared__ float sPq[NS][kRC][CP], sDo[NS][kRC][DB];               // pi^q, dL/do
 
     const LayerArgs &f = a.f;
@@ -480,6 +480,7 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
         // padding of the last interval, inside the buffer)
         const size_t pl = pack_index(t0, 0, d0 + sdd) * J + sj;
         float *const cl = a.cpk + pl, *const plp = a.ppk + pl;
+        const int scw = sact ? scol : N, sdw = sact && sj == 0 ? sdd : DB;
 #pragma unroll
         for (int u = 0; u < kRC; ++u) {
             dfr[u] = 0.0f;
@@ -507,11 +508,14 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
             const float dpred = -ddelta;
 #pragma unroll
             for (int u = 0; u < t; ++u) dfr[u] = fmaf(grow[u], dpred, dfr[u]);
+            // every lane stores to LDS (idle lanes to a padding column), so that
+            // no branch hides from the compiler how many LDS operations are in
+            // flight when the next row of K K^T is waited for
+            sP[t][scw] = dpred;
+            sDlb[t][scw] = dc * r * dl * be * (1.0f - be);
+            sDlk[t][scw] = da;
+            sDv[t][sdw] = dvv;
             if (sact) {
-                sP[t][scol] = dpred;
-                sDlb[t][scol] = dc * r * dl * be * (1.0f - be);
-                sDlk[t][scol] = da;
-                if (sj == 0) sDv[t][sdd] = dvv;
                 cl[t * CT * J] = be * r * dl;
                 plp[t * CT * J] = dpred;
             }
