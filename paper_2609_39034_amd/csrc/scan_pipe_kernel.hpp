@@ -129,6 +129,39 @@ struct IntTag {
 
 __device__ __forceinline__ void wait_vm() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
+// Padding rows after each component's block of DB columns in a column-major
+// [column][token] staging array of PITCH floats a row.  The sequential wave's
+// lane l holds column (l % JP) DB + (l / JP) % DB: the J components of an
+// output dim are DB rows apart, and with DB * PITCH a multiple of 64 floats
+// their 16-byte accesses would all start in one bank.  Over paddings 0 .. 15,
+// the one with the fewest sequential lanes of a 16-lane group starting in one
+// four-bank group (64 banks of 4 bytes), then the fewest of a tile wave's 16
+// consecutive columns, then the smallest.
+template <int DB, int J, int JP, int N, int PITCH>
+constexpr int skew_ways(int x, bool seq) {
+    int worst = 0;
+    for (int g = 0; g < (seq ? 4 : N / 16); ++g) {
+        int cnt[16] = {};
+        for (int u = 0; u < 16; ++u) {
+            const int l = 16 * g + u, bj = l % JP, bdl = (l / JP) % DB;
+            if (seq && (l >= DB * JP || bj >= J)) continue;   // idle lanes: no access of their own
+            const int col = seq ? bj * DB + bdl : l;
+            const int grp = ((col + x * (col / DB)) * PITCH % 64) / 4;
+            worst = ++cnt[grp] > worst ? cnt[grp] : worst;
+        }
+    }
+    return worst;
+}
+template <int DB, int J, int JP, int N, int PITCH>
+constexpr int skew_rows() {
+    int best = 0, bs = 64, bt = 64;
+    for (int x = 0; x < 16; ++x) {
+        const int s = skew_ways<DB, J, JP, N, PITCH>(x, true), t = skew_ways<DB, J, JP, N, PITCH>(x, false);
+        if (s < bs || (s == bs && t < bt)) best = x, bs = s, bt = t;
+    }
+    return best;
+}
+
 template <int DK, int J, int DB>
 struct PCfg {
     static constexpr int N = J * DB;
@@ -145,6 +178,13 @@ struct PCfg {
     static constexpr int PPIECES = kC * N / 4;    // fp32 predictions of a chunk (Newton)
     static_assert(N % 16 == 0 && N <= 64 && DB % 8 == 0, "column block");
     static_assert(DB * JP <= 64, "one sequential wave");
+    // rows of the column-major arrays: p and c (kTP floats a row), sq (kC + 2
+    // float2), with the padding of skew_rows after each component's block
+    static constexpr int XP = skew_rows<DB, J, JP, N, kTP>();
+    static constexpr int XS = skew_rows<DB, J, JP, N, 2 * (kC + 2)>();
+    static constexpr int NRP = N + J * XP, NRS = N + J * XS;
+    __device__ static constexpr int prow(int col) { return col + XP * (col / DB); }
+    __device__ static constexpr int srow(int col) { return col + XS * (col / DB); }
 };
 
 // MD: 0 exact scan, 1 Newton sweeps (App. D), 2 exact scan of Temporal SwiLA
@@ -166,7 +206,7 @@ struct PSmem {
         // exact: {beta, log2(e) key-prior logit}, [column][token]; a column's
         // 16 tokens are 128 contiguous bytes, padded so that the sequential
         // wave's 16-byte reads of adjacent columns fall in distinct banks
-        alignas(16) float2 sq[2][C::N][kC + 2];
+        alignas(16) float2 sq[2][C::NRS][kC + 2];
         struct {
             float beta[2][kC][C::NP];   // Newton: g (before the clamp)
             float lks[2][kC][C::NP];    // Newton: beta r delta
@@ -177,8 +217,10 @@ struct PSmem {
     float gqs[TP ? 3 : 1][kC][TP ? DB : 1];                  // temporal: g^q, [token][dim]
     float pq[TP ? 3 : 2][kC][C::NP];    // query prior (temporal: the running prior, 3 slots)
     alignas(16) float g[2][kC][kC + 4];    // K_n K_n^T, for the sequential wave
-    float p[2][C::N][kTP];     // chunk-start predictions, [column][token]
-    float c[2][C::N + 1][kTP];  // coefficients, [column][token] (column N: idle lanes)
+    // chunk-start predictions and coefficients, [C::prow(column)][token]
+    // (C::prow(N): the idle lanes' row of c)
+    float p[2][C::NRP][kTP];
+    float c[2][C::NRP + 1][kTP];
     float r[NT ? 1 : 2][kC][C::NP];  // responsibilities (exact mode)
     float py[2][kC][C::NP];    // pi^q * retrieval
     int flag;                  // Newton: this sweep met the tolerance
@@ -656,7 +698,7 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
                     const float gz = g * rcp_fast(zk[u]);
 #pragma unroll
                     for (int j = 0; j < J; ++j)
-                        sm.sq[pr][j * DB + dl + u][t] =
+                        sm.sq[pr][C::srow(j * DB + dl + u)][t] =
                             make_float2(ok ? sigmoid(lbj[j][u]) : 0.f, gz * lkj[j][u]);
                     sm.gs[pr][dl + u][t] = 1.f - g;
                     sm.vs[pr][dl + u][t] = kS * vv[u];
@@ -679,7 +721,7 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
             bf16_row<4>(sm.lk[rs], e4, lkv);
 #pragma unroll
             for (int u = 0; u < 4; ++u)
-                sm.sq[pr][cc + u][t] = make_float2(ok ? sigmoid(lbv[u]) : 0.f, lkv[u] * kLog2e);
+                sm.sq[pr][C::srow(cc + u)][t] = make_float2(ok ? sigmoid(lbv[u]) : 0.f, lkv[u] * kLog2e);
           }
 #pragma unroll
           for (int i_ = 0; i_ < ceil_div(kC * DB / 4, NBT); ++i_) {
@@ -976,7 +1018,7 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
             }
             auto fetch_inputs = [&](int prn) {
                 // 16-byte reads: few enough to be in flight together
-                const float4 *sq4 = reinterpret_cast<const float4 *>(sm.sq[prn][bcol]);
+                const float4 *sq4 = reinterpret_cast<const float4 *>(sm.sq[prn][C::srow(bcol)]);
                 const float4 *vs4 = reinterpret_cast<const float4 *>(sm.vs[prn][bdl]);
                 const float4 *g4 = reinterpret_cast<const float4 *>(sm.g[prn][0]);
 #pragma unroll
@@ -1034,7 +1076,7 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
                     auto load_pred = [&]() {
 #pragma unroll
                         for (int t = 0; t < kC; t += 4) {
-                            const float4 p4 = *reinterpret_cast<const float4 *>(&sm.p[pr][bcol][t]);
+                            const float4 p4 = *reinterpret_cast<const float4 *>(&sm.p[pr][C::prow(bcol)][t]);
                             P[t] = p4.x, P[t + 1] = p4.y, P[t + 2] = p4.z, P[t + 3] = p4.w;
                         }
                     };
@@ -1109,7 +1151,7 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
                             const float cs = bdex * iz;                  // s c
                             cb[t & 3] = cs;
                             if ((t & 3) == 3)
-                                *reinterpret_cast<float4 *>(&sm.c[pr][bsto][t - 3]) =
+                                *reinterpret_cast<float4 *>(&sm.c[pr][C::prow(bsto)][t - 3]) =
                                     make_float4(cb[0], cb[1], cb[2], cb[3]);
                             if constexpr (R) {
                                 const float rt = ex * iz;
@@ -1147,7 +1189,7 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
                                 const float cs = (bd * ex) * iz;
 #pragma unroll
                                 for (int u = t + 1; u < kC; ++u) P[u] = fmaf(grow[u], cs, P[u]);
-                                sm.c[pr][bsto][t] = cs;
+                                sm.c[pr][C::prow(bsto)][t] = cs;
                                 if constexpr (R) {
                                     const float rt = ex * iz;
                                     sm.r[pr][t][bsto] = dmode ? kInvWS * d : rt;
@@ -1169,7 +1211,7 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
                     const float glo_t = na.clamp ? 0.f : -INFINITY;
 #pragma unroll
                     for (int t = 0; t < kC; ++t) {
-                        P[t] = sm.p[pr][bcol][t];
+                        P[t] = sm.p[pr][C::prow(bcol)][t];
                         const float ghi_t = na.clamp ? 2.f * rcp_fast(sm.g[pr][t][t]) : INFINITY;
                         gc[t] = fminf(fmaxf(sm.beta[pr][t][bcol], glo_t), ghi_t);
                         bb[t] = sm.lks[pr][t][bcol];
@@ -1184,7 +1226,7 @@ void scan_pipe_kernel(LayerArgs a, NewtonArgs na) {
                         const float x = fmaf(gc[t], pold[t] - pt, bb[t]);
 #pragma unroll
                         for (int u = t + 1; u < kC; ++u) P[u] = fmaf(grow[u], x, P[u]);
-                        sm.c[pr][bsto][t] = x;
+                        sm.c[pr][C::prow(bsto)][t] = x;
                         const int tok = n * kC + t;
                         if (bact) {
                             pred[(size_t)tok * N + bcol] = pt;
