@@ -42,21 +42,21 @@ PEAK_MFMA_BF16 = 2.5e15    # FLOP/s, MI355X dense bf16 matrix
 # source, the workload it ran and the digest of the source at measurement.
 MEASURED_TRAFFIC = {
     ("scan_pipe.hip", "forward B=8 H=16 T=4096 Dk=Dv=128 J=4",
-     "1279d1e40d80d9581b39a017448a74ccd9c96fb369185c3126ebcc1d49dbcecf"): 2184251513,
+     "478522f9a30133cca34325343278e425f9bd2f91afb87ce8f5741641f6f7d101"): 2185643894,
     ("scan_pipe.hip", "forward B=4 H=8 T=2048 Dk=Dv=64 J=4",
-     "1279d1e40d80d9581b39a017448a74ccd9c96fb369185c3126ebcc1d49dbcecf"): 136703396,
+     "478522f9a30133cca34325343278e425f9bd2f91afb87ce8f5741641f6f7d101"): 136693175,
     ("scan_pipe.hip", "forward B=2 H=8 T=16384 Dk=Dv=128 J=8",
-     "1279d1e40d80d9581b39a017448a74ccd9c96fb369185c3126ebcc1d49dbcecf"): 1965727865,
+     "478522f9a30133cca34325343278e425f9bd2f91afb87ce8f5741641f6f7d101"): 3416643008,
     ("scan_pipe_temporal.hip", "temporal B=8 H=16 T=4096 Dk=Dv=128 J=4",
-     "6fcab140baddad3d29cdadda05b27e194601b259bba7afca4f0c99301dca8916"): 2451508642,
+     "f81abc0500e68902e00ce6a028c736ac30cedba669d7e5bfb0868fe335be5b3e"): 2450477142,
     ("scan_gated_chunk.hip", "gated B=8 H=16 T=4096 Dk=Dv=128 J=4",
-     "cbd5ed2709e891b062a157630c2fb89d518e8158aef25b074c5155fb3b0d766e"): 2721113447,
+     "cbd5ed2709e891b062a157630c2fb89d518e8158aef25b074c5155fb3b0d766e"): 2720590625,
     ("scan_direct_dk16.hip", "forward B=1 H=1 T=64 Dk=Dv=16 J=2",
      "11dc94a786728640b929d058f8600bf4e3c032bd82c288ad3136a45bdd77cb84"): 67711,
     ("decode.hip", "decode B=256 H=16 Dk=Dv=128 J=4",
-     "885219bbb8497010b554af973a0d14b02c80037d8cb73ffd4fa2afb165c828d7"): 2165183583,
+     "885219bbb8497010b554af973a0d14b02c80037d8cb73ffd4fa2afb165c828d7"): 2166513399,
     ("scan_gated_chunk.hip", "gated B=4 H=8 T=2048 Dk=Dv=64 J=4",
-     "cbd5ed2709e891b062a157630c2fb89d518e8158aef25b074c5155fb3b0d766e"): 170709923,
+     "cbd5ed2709e891b062a157630c2fb89d518e8158aef25b074c5155fb3b0d766e"): 171481254,
 }
 
 
