@@ -653,20 +653,9 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
     }
 }
 
-template <int N>
-__device__ __forceinline__ void lds_vec(const float *p, float (&v)[N]) {
-    if constexpr (N == 4) {
-        const float4 x = *reinterpret_cast<const float4 *>(p);
-        v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
-    } else {
-        const float2 x = *reinterpret_cast<const float2 *>(p);
-        v[0] = x.x; v[1] = x.y;
-    }
-}
-
 // J consecutive floats from global memory (16-byte loads where J allows).
 template <int J>
-__device__ __forceinline__ void lds_row(const float *p, float (&v)[J]) {
+__device__ __forceinline__ void ld_row(const float *p, float (&v)[J]) {
     if constexpr (J % 4 == 0) {
 #pragma unroll
         for (int x = 0; x < J; x += 4) {
@@ -682,33 +671,65 @@ __device__ __forceinline__ void lds_row(const float *p, float (&v)[J]) {
     }
 }
 
+// fp32 product on the matrix cores, D (16 x 16) += A (16 x 4) B (4 x 16): lane l
+// supplies A[l % 16][l / 16] and B[l / 16][l % 16], and holds D[4 (l / 16) + r][l % 16]
+// in element r.  Over a 16-deep block the lane group g = l / 16 supplies depth
+// index 4 g + s at step s, so that an operand stored depth-contiguous is read
+// with one 16-byte load per lane and block (a4), one stored depth-major with
+// four 4-byte loads (b4).
+__device__ __forceinline__ floatx4 mma4(float a, float b, floatx4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ floatx4 a4(const float *row, int k0, int g) {
+    return *reinterpret_cast<const floatx4 *>(row + k0 + 4 * g);
+}
+template <int P>
+__device__ __forceinline__ floatx4 b4(const float (*m)[P], int k0, int g, int col) {
+    const int k = k0 + 4 * g;
+    return floatx4{m[k][col], m[k + 1][col], m[k + 2][col], m[k + 3][col]};
+}
+__device__ __forceinline__ floatx4 mma16(floatx4 a, floatx4 b, floatx4 c) {
+    c = mma4(a[0], b[0], c);
+    c = mma4(a[1], b[1], c);
+    c = mma4(a[2], b[2], c);
+    return mma4(a[3], b[3], c);
+}
+
+// Chunk pass on the matrix cores (fp32 products, fp32 accumulation; one
+// instantiation for both input dtypes).  The chunk's 32 tokens are two 16-token
+// halves; every product is a set of 16 x 16 output tiles spread over the four
+// waves:
+//   dq, dk (tokens x key indices): per wave both token halves of key block w
+//     (and w + 4, ...), accumulated over all column tiles and the intra-chunk
+//     terms; with Dk = 32 one tile per wave, with Dk = 16 waves 0 and 1 only
+//   the column Gram products Y_t.C_s (needed for s <= t) and C_t.P_s (s >= t):
+//     three 16 x 16 tiles each, accumulated over the column tiles
+//   the retrievals (Q S + tril(Q K^T) C), per column tile.
 template <int DK, int J>
 __global__ __launch_bounds__(kThreads) void bwd_chunk_kernel(BackwardArgs a) {
     constexpr int DT = chunk_tile_dims<J>();
-    constexpr int NCT = J * DT;               // columns per tile
-    constexpr int NO = kCB * DK / kThreads;   // (token, key index) outputs per thread
-    constexpr int TN = NO < 4 ? NO : 4;       // consecutive key indices per thread
-    constexpr int TM = NO / TN;               // tokens per thread
-    constexpr int NIB = DK / TN;
-    static_assert(TN >= 2 && NIB * (kCB / TM) == kThreads, "thread tiling");
-    static_assert(kCB * kCB == 4 * kThreads, "Gram tiling: 4 entries per thread");
-    constexpr int KP = DK + 4, GP = kCB + 4, CP = NCT + 1;   // row pitches (16-byte rows)
+    constexpr int NCT = J * DT;                  // columns per tile: 16, 24 or 32
+    constexpr int NCP = (NCT + 15) / 16 * 16;    // columns held (J = 3: 8 zero columns)
+    constexpr int NIB = DK / 16;                 // 16-wide key-index blocks
+    constexpr int NTH = NIB >= 4 ? 2 : 1;        // token halves per wave (dq, dk)
+    constexpr int NIW = NIB >= 4 ? NIB / 4 : 1;  // key blocks per wave
+    constexpr int KP = DK + 4, CP = NCP + 4, GP = kCB + 4;   // row pitches (16-byte rows)
+    static_assert(kCB == 32 && kThreads == 256, "two token halves, four waves");
 
     __shared__ __align__(16) float sK[kCB][KP];
     __shared__ __align__(16) float sQ[kCB][KP];
-    __shared__ float sQK[kCB][GP];                 // q_t . k_s
+    __shared__ __align__(16) float sQK[kCB][GP];   // tril(Q K^T)
     // The column tiles' buffers and the final coefficient matrices are never
-    // live together: they share LDS, which keeps two blocks per compute unit.
+    // live together: they share LDS, which keeps two blocks per compute unit
+    // up to Dk = 64.
     struct TileBufs {
-        alignas(16) float S[NCT][KP], E[NCT][KP];
-        float C[kCB][CP], P[kCB][CP], Y[kCB][CP];
-        alignas(16) float Ct[NCT][GP], Pt[NCT][GP];   // C and P transposed: [column][token]
-        float Pq[kCB][CP], Yv[kCB][CP];               // pi^q and the retrievals y
+        alignas(16) float S[NCP][KP], E[NCP][KP];                // [column][key index]
+        alignas(16) float C[kCB][CP], P[kCB][CP], Y[kCB][CP];    // [token][column]
+        float Pq[kCB][CP], Yv[kCB][CP];                          // pi^q and the retrievals y
         float Do[kCB][DT];
     };
     struct EndBufs {
-        float A[kCB][GP], B[kCB][GP];
-        alignas(16) float M[3][kCB][GP];              // masked intra-chunk coefficients
+        alignas(16) float M[3][kCB][GP];   // masked intra-chunk coefficients
     };
     __shared__ union {
         TileBufs t;
@@ -719,28 +740,23 @@ __global__ __launch_bounds__(kThreads) void bwd_chunk_kernel(BackwardArgs a) {
     auto &sC = lds.t.C;
     auto &sP = lds.t.P;
     auto &sY = lds.t.Y;
-    auto &sCt = lds.t.Ct;
-    auto &sPt = lds.t.Pt;
     auto &sPq = lds.t.Pq;
     auto &sYv = lds.t.Yv;
     auto &sDo = lds.t.Do;
-    auto &sA = lds.e.A;
-    auto &sB = lds.e.B;
     auto &sM = lds.e.M;
 
     const LayerArgs &f = a.f;
     const int n = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
     const int tid = threadIdx.x;
+    const int w = __builtin_amdgcn_readfirstlane(tid / 64);
+    const int lr = tid % 16, g = (tid % 64) / 16;   // MFMA lane row/column and depth group
     const int H = f.H, T = f.T, Dv = f.Dv;
     const int NCH = (T + kCB - 1) / kCB;
     const int t0 = n * kCB, nt = min(kCB, T - t0);
     const bool ibf = f.in_bf16;
-    const int i0 = (tid % NIB) * TN, tA = (tid / NIB) * TM;   // this thread's outputs
-    const int gt = tid / 8, gs = (tid % 8) * 4;               // its Gram entries
-    const int gt8 = tid % 8;                                  // its retrieval columns
 
-    for (int g = tid; g < kCB * (DK / 4); g += kThreads) {
-        const int t = g / (DK / 4), i = (g % (DK / 4)) * 4;
+    for (int e = tid; e < kCB * (DK / 4); e += kThreads) {
+        const int t = e / (DK / 4), i = (e % (DK / 4)) * 4;
         uint4 kr = make_uint4(0u, 0u, 0u, 0u), qr = kr;
         if (t < nt) {
             const size_t off = ((size_t)(b * T + t0 + t) * H + h) * DK + i;
@@ -750,32 +766,56 @@ __global__ __launch_bounds__(kThreads) void bwd_chunk_kernel(BackwardArgs a) {
         *reinterpret_cast<float4 *>(&sK[t][i]) = cvt4(kr, ibf);
         *reinterpret_cast<float4 *>(&sQ[t][i]) = cvt4(qr, ibf);
     }
-    block_sync_lds();
-    {   // Q K^T: row gt, columns gt8 + 8 x
-        float qk[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll 4
-        for (int i = 0; i < DK; i += 4) {
-            float qv[4];
-            lds_vec<4>(&sQ[gt][i], qv);
-#pragma unroll
-            for (int x = 0; x < 4; ++x) {
-                float kv[4];
-                lds_vec<4>(&sK[gt8 + 8 * x][i], kv);
-#pragma unroll
-                for (int z = 0; z < 4; ++z) qk[x] = fmaf(qv[z], kv[z], qk[x]);
+    if constexpr (NCP > NCT) {   // the padding columns stay zero
+        for (int e = tid; e < (NCP - NCT) * (kCB + DK); e += kThreads) {
+            const int c = NCT + e % (NCP - NCT), r = e / (NCP - NCT);
+            if (r < kCB) {
+                sC[r][c] = 0.0f;
+                sP[r][c] = 0.0f;
+                sY[r][c] = 0.0f;
+            } else {
+                sS[c][r - kCB] = 0.0f;
+                sE[c][r - kCB] = 0.0f;
             }
         }
+    }
+    block_sync_lds();
+    if constexpr (J > 1) {   // tril(Q K^T): wave w has tile (w / 2, w % 2)
+        const int th = w >> 1, sh = w & 1;
+        floatx4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+        if (sh <= th) {
+#pragma unroll 4
+            for (int k0 = 0; k0 < DK; k0 += 16)
+                acc = mma16(a4(sQ[16 * th + lr], k0, g), a4(sK[16 * sh + lr], k0, g), acc);
+        }
 #pragma unroll
-        for (int x = 0; x < 4; ++x) sQK[gt][gt8 + 8 * x] = qk[x];
+        for (int r = 0; r < 4; ++r) {
+            const int t = 16 * th + 4 * g + r, s = 16 * sh + lr;
+            sQK[t][s] = s <= t ? acc[r] : 0.0f;
+        }
     }
 
-    float dq[TM][TN], dk[TM][TN], ga[4], gb[4];
+    // this wave's dq and dk tiles: (token half, key block) = (x, w + 4 y) for
+    // Dk >= 64, (w / 2, w % 2) for Dk = 32, (w, 0) on waves 0 and 1 for Dk = 16
+    const bool dwave = NIB >= 2 || w < 2;
+    auto tile_th = [&](int x) { return NIB >= 4 ? x : NIB == 2 ? w >> 1 : w; };
+    auto tile_ib = [&](int y) { return NIB >= 4 ? w + 4 * y : NIB == 2 ? (w & 1) : 0; };
+    floatx4 dq[NTH][NIW], dk[NTH][NIW];
+    // Gram tiles: index w and w + 4 of ga(0,0), gb(0,0), ga(1,0), gb(0,1), ga(1,1),
+    // gb(1,1); ga = Y_t.C_s, gb = C_t.P_s
+    floatx4 gr[2];
 #pragma unroll
-    for (int m = 0; m < TM; ++m)
+    for (int x = 0; x < NTH; ++x)
 #pragma unroll
-        for (int x = 0; x < TN; ++x) dq[m][x] = dk[m][x] = 0.0f;
-#pragma unroll
-    for (int x = 0; x < 4; ++x) ga[x] = gb[x] = 0.0f;
+        for (int y = 0; y < NIW; ++y) dq[x][y] = dk[x][y] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
+    gr[0] = gr[1] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
+    auto gram_tile = [&](int slot, int &kind, int &th, int &sh) {
+        const int idx = w + 4 * slot, pos = idx >> 1;
+        kind = idx & 1;
+        th = kind ? pos == 2 : pos > 0;
+        sh = kind ? pos > 0 : pos == 2;
+        return idx < 6;
+    };
 
     // checkpoints of this chunk, [Dv][J][DK]
     const size_t ck0 = (((size_t)b * H + h) * NCH + n) * Dv * J * DK;
@@ -799,12 +839,12 @@ __global__ __launch_bounds__(kThreads) void bwd_chunk_kernel(BackwardArgs a) {
         const size_t tb = ((((size_t)b * H + h) * NCH + n) * (Dv / DT) + dt0 / DT) * kCB;
 #pragma unroll
         for (int x = 0; x < NOP; ++x) {
-            const int g = min(tid + kThreads * x, kCB * DT - 1);
-            const int t = min(g / DT, nt - 1), dd = g % DT;
+            const int e = min(tid + kThreads * x, kCB * DT - 1);
+            const int t = min(e / DT, nt - 1), dd = e % DT;
             const size_t row = (tb + t) * DT + dd;
-            lds_row<J>(a.cpk + row * J, rc[x]);
-            lds_row<J>(a.ppk + row * J, rp[x]);
-            lds_row<J>(a.qpk + row * J, rq[x]);
+            ld_row<J>(a.cpk + row * J, rc[x]);
+            ld_row<J>(a.ppk + row * J, rp[x]);
+            ld_row<J>(a.qpk + row * J, rq[x]);
             rd[x] = a.dopk[row];
         }
     };
@@ -822,28 +862,20 @@ __global__ __launch_bounds__(kThreads) void bwd_chunk_kernel(BackwardArgs a) {
         }
 #pragma unroll
         for (int x = 0; x < NOP; ++x) {
-            const int g = tid + kThreads * x;
-            const int t = g / DT, dd = g % DT;
+            const int e = tid + kThreads * x;
+            const int t = e / DT, dd = e % DT;
             const bool in = t < nt;
             const float dov = in ? rd[x] : 0.0f;
-            float c[J], p[J], pq[J];
-#pragma unroll
-            for (int j = 0; j < J; ++j) {
-                c[j] = in ? rc[x][j] : 0.0f;
-                p[j] = in ? rp[x][j] : 0.0f;
-                pq[j] = in ? rq[x][j] : 0.0f;
-            }
-            if ((kCB * DT) % kThreads == 0 || g < kCB * DT) {
+            if ((kCB * DT) % kThreads == 0 || e < kCB * DT) {
                 sDo[t][dd] = dov;
 #pragma unroll
                 for (int j = 0; j < J; ++j) {
                     const int cc = j * DT + dd;
-                    sC[t][cc] = c[j];
-                    sP[t][cc] = p[j];
-                    sY[t][cc] = dov * pq[j];
-                    sCt[cc][t] = c[j];
-                    sPt[cc][t] = p[j];
-                    sPq[t][cc] = pq[j];
+                    const float pq = in ? rq[x][j] : 0.0f;
+                    sC[t][cc] = in ? rc[x][j] : 0.0f;
+                    sP[t][cc] = in ? rp[x][j] : 0.0f;
+                    sY[t][cc] = dov * pq;
+                    sPq[t][cc] = pq;
                 }
             }
         }
@@ -851,64 +883,64 @@ __global__ __launch_bounds__(kThreads) void bwd_chunk_kernel(BackwardArgs a) {
         if (dt0 + DT < Dv) fetch_tile(dt0 + DT);   // lands while this tile computes
 
         // dq += Y S; dk += P S + C E (this tile's columns)
-#pragma unroll 4
-        for (int cc = 0; cc < NCT; ++cc) {
-            float sv[TN], ev[TN];
-            lds_vec<TN>(&sS[cc][i0], sv);
-            lds_vec<TN>(&sE[cc][i0], ev);
+        if (dwave) {
 #pragma unroll
-            for (int m = 0; m < TM; ++m) {
-                const float yv = sY[tA + m][cc], pv = sP[tA + m][cc], cv = sC[tA + m][cc];
+            for (int k0 = 0; k0 < NCP; k0 += 16) {
+                floatx4 ya[NTH], pa[NTH], ca[NTH], sb[NIW], eb[NIW];
 #pragma unroll
-                for (int x = 0; x < TN; ++x) {
-                    dq[m][x] = fmaf(yv, sv[x], dq[m][x]);
-                    dk[m][x] = fmaf(pv, sv[x], fmaf(cv, ev[x], dk[m][x]));
+                for (int x = 0; x < NTH; ++x) {
+                    const int row = 16 * tile_th(x) + lr;
+                    ya[x] = a4(sY[row], k0, g);
+                    pa[x] = a4(sP[row], k0, g);
+                    ca[x] = a4(sC[row], k0, g);
                 }
-            }
-        }
-        // Gram products over the columns: ga = Y_t . C_s, gb = C_t . P_s
-#pragma unroll 4
-        for (int cc = 0; cc < NCT; ++cc) {
-            float ct[4], pt[4];
-            lds_vec<4>(&sCt[cc][gs], ct);
-            lds_vec<4>(&sPt[cc][gs], pt);
-            const float yv = sY[gt][cc], cv = sC[gt][cc];
 #pragma unroll
-            for (int x = 0; x < 4; ++x) {
-                ga[x] = fmaf(yv, ct[x], ga[x]);
-                gb[x] = fmaf(cv, pt[x], gb[x]);
+                for (int y = 0; y < NIW; ++y) {
+                    sb[y] = b4(sS, k0, g, 16 * tile_ib(y) + lr);
+                    eb[y] = b4(sE, k0, g, 16 * tile_ib(y) + lr);
+                }
+#pragma unroll
+                for (int x = 0; x < NTH; ++x)
+#pragma unroll
+                    for (int y = 0; y < NIW; ++y) {
+                        dq[x][y] = mma16(ya[x], sb[y], dq[x][y]);
+                        dk[x][y] = mma16(pa[x], sb[y], dk[x][y]);
+                        dk[x][y] = mma16(ca[x], eb[y], dk[x][y]);
+                    }
             }
         }
-        // retrievals y = Q S + tril(Q K^T) C: row gt, columns gt8 + 8 x
+        // the Gram tiles of this wave
+#pragma unroll
+        for (int slot = 0; slot < 2; ++slot) {
+            int kind, th, sh;
+            if (gram_tile(slot, kind, th, sh)) {
+                const float *ar = kind ? sC[16 * th + lr] : sY[16 * th + lr];
+                const float *br = kind ? sP[16 * sh + lr] : sC[16 * sh + lr];
+#pragma unroll
+                for (int k0 = 0; k0 < NCP; k0 += 16)
+                    gr[slot] = mma16(a4(ar, k0, g), a4(br, k0, g), gr[slot]);
+            }
+        }
+        // retrievals y = Q S + tril(Q K^T) C: tile (token half, column block)
+        // (w / 2, w % 2) for 32 columns, (w - 2, 0) on waves 2 and 3 for 16
         if constexpr (J > 1) {
-            constexpr int NY = NCT / 8;
-            float yr[NY];
-#pragma unroll
-            for (int x = 0; x < NY; ++x) yr[x] = 0.0f;
+            constexpr int NCB = NCP / 16;
+            const int th = NCB == 2 ? w >> 1 : w - 2, cb = NCB == 2 ? (w & 1) : 0;
+            if (th >= 0) {
+                floatx4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll 4
-            for (int i = 0; i < DK; i += 4) {
-                float qv[4];
-                lds_vec<4>(&sQ[gt][i], qv);
+                for (int k0 = 0; k0 < DK; k0 += 16)
+                    acc = mma16(a4(sQ[16 * th + lr], k0, g), a4(sS[16 * cb + lr], k0, g), acc);
+                for (int s0 = 0; s0 <= 16 * th; s0 += 16)
+                    acc = mma16(a4(sQK[16 * th + lr], s0, g), b4(sC, s0, g, 16 * cb + lr), acc);
 #pragma unroll
-                for (int x = 0; x < NY; ++x) {
-                    float sv[4];
-                    lds_vec<4>(&sS[gt8 + 8 * x][i], sv);
-#pragma unroll
-                    for (int z = 0; z < 4; ++z) yr[x] = fmaf(qv[z], sv[z], yr[x]);
-                }
+                for (int r = 0; r < 4; ++r) sYv[16 * th + 4 * g + r][16 * cb + lr] = acc[r];
             }
-            for (int s2 = 0; s2 <= gt; ++s2) {
-                const float qk = sQK[gt][s2];
-#pragma unroll
-                for (int x = 0; x < NY; ++x) yr[x] = fmaf(qk, sC[s2][gt8 + 8 * x], yr[x]);
-            }
-#pragma unroll
-            for (int x = 0; x < NY; ++x) sYv[gt][gt8 + 8 * x] = yr[x];
         }
         block_sync_lds();
         // dL/dlq_j = pi^q_j do (y_j - sum_i pi^q_i y_i); zero for one component
-        for (int g = tid; g < nt * DT; g += kThreads) {
-            const int t = g / DT, dd = g % DT;
+        for (int e = tid; e < nt * DT; e += kThreads) {
+            const int t = e / DT, dd = e % DT;
             const size_t row = (size_t)(b * T + t0 + t) * H + h;
             float mean = 0.0f;
 #pragma unroll
@@ -921,47 +953,69 @@ __global__ __launch_bounds__(kThreads) void bwd_chunk_kernel(BackwardArgs a) {
         }
     }
 
-    // the intra-chunk terms, as three masked C x C coefficient matrices (in the
-    // tile buffers' LDS: the last tile is consumed first)
+    // The intra-chunk terms as three masked C x C coefficient matrices (in the
+    // tile buffers' LDS: the last tile is consumed first):
+    //   M0[t][s] = (Y_t.C_s) for s <= t          (dq, times k_s)
+    //   M1[t][s] = (C_t.P_s) for s > t, (P_t.C_s) for s < t   (dk, times k_s)
+    //   M2[t][s] = (C_t.Y_s) for s >= t          (dk, times q_s)
+    // A ga element (t, s) with s <= t gives M0[t][s] and M2[s][t]; a gb element
+    // with s > t gives M1[t][s] and M1[s][t].  M0's upper and M2's lower
+    // off-diagonal blocks are zero.
     block_sync_lds();
-#pragma unroll
-    for (int x = 0; x < 4; ++x) {
-        sA[gt][gs + x] = ga[x];
-        sB[gt][gs + x] = gb[x];
+    for (int e = tid; e < 16 * 16; e += kThreads) {
+        sM[0][e / 16][16 + e % 16] = 0.0f;
+        sM[2][16 + e / 16][e % 16] = 0.0f;
     }
-    block_sync_lds();
-    for (int g = tid; g < kCB * kCB; g += kThreads) {
-        const int t = g / kCB, s = g % kCB;
-        sM[0][t][s] = s <= t ? sA[t][s] : 0.0f;                          // (Y_t . C_s) k_s
-        sM[1][t][s] = s > t ? sB[t][s] : (s < t ? sB[s][t] : 0.0f);      // (C_t.P_s), (P_t.C_s) k_s
-        sM[2][t][s] = s >= t ? sA[s][t] : 0.0f;                          // (C_t . Y_s) q_s
-    }
-    block_sync_lds();
-#pragma unroll 4
-    for (int s = 0; s < kCB; ++s) {
-        float kv[TN], qv[TN];
-        lds_vec<TN>(&sK[s][i0], kv);
-        lds_vec<TN>(&sQ[s][i0], qv);
 #pragma unroll
-        for (int m = 0; m < TM; ++m) {
-            const float mq = sM[0][tA + m][s], m1 = sM[1][tA + m][s], m2 = sM[2][tA + m][s];
+    for (int slot = 0; slot < 2; ++slot) {
+        int kind, th, sh;
+        if (gram_tile(slot, kind, th, sh)) {
 #pragma unroll
-            for (int x = 0; x < TN; ++x) {
-                dq[m][x] = fmaf(mq, kv[x], dq[m][x]);
-                dk[m][x] = fmaf(m1, kv[x], fmaf(m2, qv[x], dk[m][x]));
+            for (int r = 0; r < 4; ++r) {
+                const int t = 16 * th + 4 * g + r, s = 16 * sh + lr;
+                const float v = gr[slot][r];
+                if (kind == 0) {
+                    sM[0][t][s] = s <= t ? v : 0.0f;
+                    sM[2][s][t] = s <= t ? v : 0.0f;
+                } else if (s >= t) {
+                    sM[1][t][s] = s > t ? v : 0.0f;
+                    sM[1][s][t] = s > t ? v : 0.0f;
+                }
             }
         }
     }
+    block_sync_lds();
+    if (dwave) {
+        // dq += M0 K (s up to the end of the token half); dk += M1 K + M2 Q
+        // (M2 from the token half's start)
 #pragma unroll
-    for (int m = 0; m < TM; ++m) {
-        const int t = tA + m;
-        if (t >= nt) continue;
-        const size_t off = ((size_t)(b * T + t0 + t) * H + h) * DK + i0;
+        for (int x = 0; x < NTH; ++x) {
+            const int th = tile_th(x), row = 16 * th + lr;
 #pragma unroll
-        for (int x = 0; x < TN; ++x) {
-            a.dq[off + x] = dq[m][x];
-            a.dk[off + x] = dk[m][x];
+            for (int y = 0; y < NIW; ++y) {
+                const int col = 16 * tile_ib(y) + lr;
+                for (int s0 = 0; s0 < kCB; s0 += 16) {
+                    const floatx4 kb = b4(sK, s0, g, col);
+                    if (s0 <= 16 * th) dq[x][y] = mma16(a4(sM[0][row], s0, g), kb, dq[x][y]);
+                    dk[x][y] = mma16(a4(sM[1][row], s0, g), kb, dk[x][y]);
+                    if (s0 >= 16 * th)
+                        dk[x][y] = mma16(a4(sM[2][row], s0, g), b4(sQ, s0, g, col), dk[x][y]);
+                }
+            }
         }
+#pragma unroll
+        for (int x = 0; x < NTH; ++x)
+#pragma unroll
+            for (int y = 0; y < NIW; ++y)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int t = 16 * tile_th(x) + 4 * g + r;
+                    if (t >= nt) continue;
+                    const size_t off =
+                        ((size_t)(b * T + t0 + t) * H + h) * DK + 16 * tile_ib(y) + lr;
+                    a.dq[off] = dq[x][y][r];
+                    a.dk[off] = dk[x][y][r];
+                }
     }
 }
 
