@@ -53,6 +53,10 @@ template <bool B>
 struct BTag {
     static constexpr bool value = B;
 };
+template <int N>
+struct ITag {
+    static constexpr int value = N;
+};
 
 // The kernels below order only LDS traffic at their barriers (block_sync_lds):
 // a full __syncthreads would also wait for every global load in flight, and
@@ -159,9 +163,10 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
     __shared__ __align__(16) float sKt[KT][GP], sQt[KT][GP];           // the same, [i][t]
     __shared__ __align__(16) float sGkk[kRC][GP];                      // k_t . k_s (symmetric)
     __shared__ __align__(16) float sGkqT[kRC][GP];                     // [s][t] = k_t . q_s
-    __shared__ __align__(16) float sBase[kRC][CP], sY[NS][kRC][CP], sP[kRC][CP];
+    __shared__ __align__(16) float sBase[kRC][CP], sY[NS][kRC][CP], sP[NS][kRC][CP];
     __shared__ float sDelta[NS][kRC][CP], sBeta[NS][kRC][CP], sR[NS][kRC][CP];
-    __shared__ float sDlb[kRC][CP], sDlk[kRC][CP], sDv[kRC][DB + 1];
+    __shared__ float sDc[kRC][CP], sDlk[kRC][CP], sDv[kRC][DB + 1];   // dc, da, dv
+    __shared__ float sCv[NS][kRC][CP];                                 // c = beta r delta
     __shared__ float sPq[NS][kRC][CP], sDo[NS][kRC][DB];               // pi^q, dL/do
 
     const LayerArgs &f = a.f;
@@ -340,34 +345,66 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
         const size_t pbase = ((size_t)b * H + h) * NC2 + t0 / kBwdChunk;
         return ((pbase * (Dv / CT) + d / CT) * kBwdChunk + t0 % kBwdChunk + t) * CT + d % CT;
     };
-    auto pack_store = [&](float *dst, const float (*X)[CP], int t0, int nt, int first, int nthr) {
-        constexpr int NE = kRC * J * DB;
-        for (int e = tid - first; e < NE; e += nthr) {
-            const int j = e % J, w = (e / J) % TW, t = (e / (J * TW)) % kRC,
-                      kk = e / (J * TW * kRC);
-            const int dd = kk * TW + w;
-            if (t < nt) dst[pack_index(t0, t, d0 + dd) * J + j] = X[t][j * DB + dd];
+    // dst[(tile row of (t, d)) * JJ + j] = val(t, j, dd) for the chunk's tokens,
+    // by threads first .. first + nthr - 1 (compile-time: the loop is unrolled
+    // and every LDS read is issued before the first store)
+    auto pack_store = [&](float *dst, auto jj, auto val, int t0, int nt, auto first, auto nthr) {
+        constexpr int JJ = decltype(jj)::value, F = decltype(first)::value;
+        constexpr int NT = decltype(nthr)::value, NE = kRC * JJ * DB, NI = (NE + NT - 1) / NT;
+        float v[NI];
+#pragma unroll
+        for (int x = 0; x < NI; ++x) {
+            const int e = min(tid - F + NT * x, NE - 1);
+            const int j = e % JJ, w = (e / JJ) % TW, t = (e / (JJ * TW)) % kRC,
+                      kk = e / (JJ * TW * kRC);
+            v[x] = val(t, j, kk * TW + w);
+        }
+#pragma unroll
+        for (int x = 0; x < NI; ++x) {
+            const int e = tid - F + NT * x;
+            const int j = e % JJ, w = (e / JJ) % TW, t = (e / (JJ * TW)) % kRC,
+                      kk = e / (JJ * TW * kRC);
+            if ((NE % NT == 0 || e < NE) && t < nt)
+                dst[pack_index(t0, t, d0 + kk * TW + w) * JJ + j] = v[x];
         }
     };
-    // pi^q and dL/do of chunk n for the chunk pass, by threads 64 .. kThreads - 1
-    // (the sequential wave stores c = beta r delta and dpred)
-    auto packs = [&](int n, int sl) {
+    // pi^q and dL/do of chunk n for the chunk pass (staged inputs in slot sl)
+    auto packs = [&](int n, int sl, auto first, auto nthr) {
         const int t0 = n * kRC, nt = min(kRC, T - t0);
-        pack_store(a.qpk, sPq[sl], t0, nt, 64, kThreads - 64);
-        for (int e = tid - 64; e < kRC * DB; e += kThreads - 64) {
-            const int w = e % TW, t = (e / TW) % kRC, kk = e / (TW * kRC);
-            if (t < nt) a.dopk[pack_index(t0, t, d0 + kk * TW + w)] = sDo[sl][t][kk * TW + w];
-        }
+        pack_store(a.qpk, ITag<J>{}, [&](int t, int j, int dd) { return sPq[sl][t][j * DB + dd]; },
+                   t0, nt, first, nthr);
+        pack_store(a.dopk, ITag<1>{}, [&](int t, int, int dd) { return sDo[sl][t][dd]; }, t0, nt,
+                   first, nthr);
+    };
+    // c = beta r delta and dpred of chunk n (its tokens' results in slot sl)
+    auto packs_cp = [&](int n, int sl, auto first, auto nthr) {
+        const int t0 = n * kRC, nt = min(kRC, T - t0);
+        pack_store(a.cpk, ITag<J>{}, [&](int t, int j, int dd) { return sCv[sl][t][j * DB + dd]; },
+                   t0, nt, first, nthr);
+        pack_store(a.ppk, ITag<J>{}, [&](int t, int j, int dd) { return sP[sl][t][j * DB + dd]; },
+                   t0, nt, first, nthr);
     };
     // E_m (the gradient from the tokens after checkpoint interval m) before
-    // the interval's last reverse chunk runs: [.., m, d, j, i]
-    auto checkpoint = [&](int n, int first, int nthr) {
+    // the interval's last reverse chunk runs: [.., m, d, j, i], four key indices
+    // per store, all LDS reads issued first
+    auto checkpoint = [&](int n, auto first, auto nthr) {
+        constexpr int F = decltype(first)::value, NT = decltype(nthr)::value;
+        constexpr int NE4 = DB * J * DK / 4, NI = (NE4 + NT - 1) / NT;
         if (n % R2 == R2 - 1 || n == NCH - 1) {
             const int m = n / R2;
-            float *ck = a.eck + (((size_t)b * H + h) * NC2 + m) * Dv * J * DK;
-            for (int e = tid - first; e < DB * J * DK; e += nthr) {
-                const int dd = e / (J * DK), j = (e / DK) % J, i = e % DK;
-                ck[(size_t)(d0 + dd) * J * DK + j * DK + i] = sE[i][j * DB + dd];
+            float *ck = a.eck + ((((size_t)b * H + h) * NC2 + m) * Dv + d0) * J * DK;
+            float4 v[NI];
+#pragma unroll
+            for (int x = 0; x < NI; ++x) {
+                const int e = min(tid - F + NT * x, NE4 - 1);
+                const int dd = e / (J * DK / 4), j = (e / (DK / 4)) % J, i = (e % (DK / 4)) * 4;
+                const int col = j * DB + dd;
+                v[x] = make_float4(sE[i][col], sE[i + 1][col], sE[i + 2][col], sE[i + 3][col]);
+            }
+#pragma unroll
+            for (int x = 0; x < NI; ++x) {
+                const int e = tid - F + NT * x;
+                if (NE4 % NT == 0 || e < NE4) reinterpret_cast<float4 *>(ck)[e] = v[x];
             }
         }
     };
@@ -471,15 +508,9 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
         }
     };
     // the chunk's tokens in reverse, by the sequential wave (tid < 64)
-    auto tokens = [&](int n, int sl) {
-        const int t0 = n * kRC;
+    auto tokens = [&](int sl) {
         // dfr[u] collects sum_{s>u} (k_u . k_s) dpred_s
         float dfr[kRC], vb[kRC], vd[kRC], vbe[kRC], vr[kRC];
-        // this lane's column in the chunk pass's tile order: token t of the
-        // chunk at t * CT * J floats on (tokens past the end land in the
-        // padding of the last interval, inside the buffer)
-        const size_t pl = pack_index(t0, 0, d0 + sdd) * J + sj;
-        float *const cl = a.cpk + pl, *const plp = a.ppk + pl;
         const int scw = sact ? scol : N, sdw = sact && sj == 0 ? sdd : DB;
 #pragma unroll
         for (int u = 0; u < kRC; ++u) {
@@ -489,15 +520,24 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
             vbe[u] = sact ? sBeta[sl][u][scol] : 0.0f;
             vr[u] = sact ? sR[sl][u][scol] : 0.0f;
         }
+        // rows of K K^T (= columns), the part u < t: row t - 1 is read while
+        // token t runs, a token ahead of its use
+        float grow[2][kRC];
+#pragma unroll
+        for (int u4 = 0; u4 < kRC / 4; ++u4) {
+            const float4 x = *reinterpret_cast<const float4 *>(&sGkk[kRC - 1][4 * u4]);
+            float *g = grow[(kRC - 1) & 1];
+            g[4 * u4] = x.x, g[4 * u4 + 1] = x.y, g[4 * u4 + 2] = x.z, g[4 * u4 + 3] = x.w;
+        }
 #pragma unroll
         for (int t = kRC - 1; t >= 0; --t) {
-            float grow[kRC];   // row t of K K^T (= column t), the part u < t
 #pragma unroll
-            for (int u4 = 0; u4 < (t + 3) / 4; ++u4) {
-                const float4 x = *reinterpret_cast<const float4 *>(&sGkk[t][4 * u4]);
-                grow[4 * u4] = x.x, grow[4 * u4 + 1] = x.y;
-                grow[4 * u4 + 2] = x.z, grow[4 * u4 + 3] = x.w;
+            for (int u4 = 0; u4 < (t + 2) / 4; ++u4) {   // row t - 1
+                const float4 x = *reinterpret_cast<const float4 *>(&sGkk[t - 1][4 * u4]);
+                float *g = grow[(t - 1) & 1];
+                g[4 * u4] = x.x, g[4 * u4 + 1] = x.y, g[4 * u4 + 2] = x.z, g[4 * u4 + 3] = x.w;
             }
+            __builtin_amdgcn_sched_barrier(0);   // (the scheduler would sink these loads to their use)
             const float dc = vb[t] + dfr[t];
             const float dl = vd[t], be = vbe[t], r = vr[t];
             const float dr = dc * be * dl;
@@ -507,18 +547,15 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
             const float dvv = group_sum<JP>(ddelta);
             const float dpred = -ddelta;
 #pragma unroll
-            for (int u = 0; u < t; ++u) dfr[u] = fmaf(grow[u], dpred, dfr[u]);
+            for (int u = 0; u < t; ++u) dfr[u] = fmaf(grow[t & 1][u], dpred, dfr[u]);
             // every lane stores to LDS (idle lanes to a padding column), so that
             // no branch hides from the compiler how many LDS operations are in
             // flight when the next row of K K^T is waited for
-            sP[t][scw] = dpred;
-            sDlb[t][scw] = dc * r * dl * be * (1.0f - be);
+            sP[sl][t][scw] = dpred;
+            sCv[sl][t][scw] = be * r * dl;
+            sDc[t][scw] = dc;
             sDlk[t][scw] = da;
             sDv[t][sdw] = dvv;
-            if (sact) {
-                cl[t * CT * J] = be * r * dl;
-                plp[t * CT * J] = dpred;
-            }
         }
     };
     // E += Q^T Y + K^T P for the chunk in slot sl (E then holds the gradient
@@ -540,7 +577,7 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
                     qv[m] = sQ[sl][4 * lg + m][16 * ti + tl];
                     kv[m] = sK[sl][4 * lg + m][16 * ti + tl];
                     yv[m] = cv ? sY[sl][4 * lg + m][col] : 0.0f;
-                    pv[m] = cv ? sP[4 * lg + m][col] : 0.0f;
+                    pv[m] = cv ? sP[sl][4 * lg + m][col] : 0.0f;
                 }
                 const KOp<4> qa = kop_exact<4>(qv), ka = kop_exact<4>(kv);
                 const KOp<4> yb = kop_split<4>(yv), pb = kop_split<4>(pv);
@@ -565,7 +602,7 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
 #pragma unroll
                     for (int x = 0; x < 4; ++x) {
                         const float4 y = *reinterpret_cast<const float4 *>(&sY[sl][t4 + x][c4]);
-                        const float4 p = *reinterpret_cast<const float4 *>(&sP[t4 + x][c4]);
+                        const float4 p = *reinterpret_cast<const float4 *>(&sP[sl][t4 + x][c4]);
                         acc.x = fmaf(qa[x], y.x, fmaf(ka[x], p.x, acc.x));
                         acc.y = fmaf(qa[x], y.y, fmaf(ka[x], p.y, acc.y));
                         acc.z = fmaf(qa[x], y.z, fmaf(ka[x], p.z, acc.z));
@@ -576,21 +613,48 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
             }
         }
     };
-    // the chunk's per-token outputs, coalesced over output dims
-    auto outputs = [&](int n) {
+    // chunk n's per-token outputs, coalesced over output dims: dL/dlb and dL/dlk
+    // (from the tokens' dc and da and the staged inputs in slot sl) and dv; all
+    // LDS reads are issued before the stores
+    auto outputs = [&](int n, int sl) {
         const int t0 = n * kRC, nt = min(kRC, T - t0);
-        for (int e = tid; e < nt * J * DB; e += kThreads) {
-            const int t = e / (J * DB), j = (e / DB) % J, dd = e % DB;
-            const int col = j * DB + dd;
-            const size_t idx = (((size_t)(b * T + t0 + t) * H + h) * J + j) * Dv + d0 + dd;
-            a.dlb[idx] = sDlb[t][col];
-            a.dlk[idx] = sDlk[t][col];
+        constexpr int NE = kRC * J * DB, NI = (NE + kThreads - 1) / kThreads;
+        constexpr int NV = (kRC * DB + kThreads - 1) / kThreads;
+        float vb[NI], vk[NI], vv[NV];
+#pragma unroll
+        for (int x = 0; x < NI; ++x) {
+            const int e = min(tid + kThreads * x, NE - 1);
+            const int t = e / (J * DB), col = e % (J * DB);
+            const float be = sBeta[sl][t][col];
+            vb[x] = sDc[t][col] * sR[sl][t][col] * sDelta[sl][t][col] * be * (1.0f - be);
+            vk[x] = sDlk[t][col];
         }
-        for (int e = tid; e < nt * DB; e += kThreads) {
-            const int t = e / DB, dd = e % DB;
-            a.dv[((size_t)(b * T + t0 + t) * H + h) * Dv + d0 + dd] = sDv[t][dd];
+#pragma unroll
+        for (int x = 0; x < NV; ++x) {
+            const int e = min(tid + kThreads * x, kRC * DB - 1);
+            vv[x] = sDv[e / DB][e % DB];
+        }
+#pragma unroll
+        for (int x = 0; x < NI; ++x) {
+            const int e = tid + kThreads * x;
+            const int t = e / (J * DB), j = (e / DB) % J, dd = e % DB;
+            if ((NE % kThreads == 0 || e < NE) && t < nt) {
+                const size_t idx = (((size_t)(b * T + t0 + t) * H + h) * J + j) * Dv + d0 + dd;
+                a.dlb[idx] = vb[x];
+                a.dlk[idx] = vk[x];
+            }
+        }
+#pragma unroll
+        for (int x = 0; x < NV; ++x) {
+            const int e = tid + kThreads * x, t = e / DB, dd = e % DB;
+            if (((kRC * DB) % kThreads == 0 || e < kRC * DB) && t < nt)
+                a.dv[((size_t)(b * T + t0 + t) * H + h) * Dv + d0 + dd] = vv[x];
         }
     };
+    constexpr ITag<64> kF1{};               // the staging threads of the bf16 schedule
+    constexpr ITag<kThreads - 64> kN1{};
+    constexpr ITag<0> kF0{};                // every thread
+    constexpr ITag<kThreads> kN0{};
 
     if constexpr (IBF) {
         if (NCH > 0) {
@@ -608,10 +672,11 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
                 const int sl = n & 1;
                 block_sync_lds();   // A: the base of chunk n and E are complete
                 if (tid < 64) {
-                    tokens(n, sl);
+                    tokens(sl);
                 } else {
-                    checkpoint(n, 64, kThreads - 64);
-                    packs(n, sl);
+                    checkpoint(n, kF1, kN1);
+                    packs(n, sl, kF1, kN1);
+                    if (n < n0) packs_cp(n + 1, sl ^ 1, kF1, kN1);
                     if (n > 0) {
                         stage(n - 1, sl ^ 1);
                         if (n > 1) fetch(n - 2);   // lands during chunks n and n - 1
@@ -619,17 +684,18 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
                 }
                 block_sync_lds();   // B: chunk n's dpred published
                 update_e(sl);
-                outputs(n);
+                outputs(n, sl);
                 if (n > 0) gram(sl ^ 1);
                 block_sync_lds();   // C: E now from the tokens after chunk n - 1
                 if (n > 0) base(sl ^ 1);
             }
+            packs_cp(0, 0, kF0, kN0);   // chunk 0's tokens ended before the last barrier B
         }
     } else {
         if (NCH > 0) fetch(NCH - 1);
         for (int n = NCH - 1; n >= 0; --n) {
             block_sync_lds();   // E is complete; the previous chunk's staging is consumed
-            checkpoint(n, 0, kThreads);
+            checkpoint(n, kF0, kN0);
             stage(n, 0);
             block_sync_lds();
             if (n > 0) fetch(n - 1);   // lands while this chunk computes
@@ -637,11 +703,12 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
             block_sync_lds();
             base(0);
             block_sync_lds();
-            if (tid >= 64) packs(n, 0);
-            if (tid < 64) tokens(n, 0);
+            if (tid >= 64) packs(n, 0, kF1, kN1);
+            if (tid < 64) tokens(0);
             block_sync_lds();
             update_e(0);
-            outputs(n);
+            outputs(n, 0);
+            packs_cp(n, 0, kF0, kN0);
         }
     }
     block_sync_lds();
