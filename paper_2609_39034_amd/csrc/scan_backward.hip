@@ -166,7 +166,6 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
     __shared__ __align__(16) float sBase[kRC][CP], sY[NS][kRC][CP], sP[NS][kRC][CP];
     __shared__ float sDelta[NS][kRC][CP], sBeta[NS][kRC][CP], sR[NS][kRC][CP];
     __shared__ float sDc[kRC][CP], sDlk[kRC][CP], sDv[kRC][DB + 1];   // dc, da, dv
-    __shared__ float sCv[NS][kRC][CP];                                 // c = beta r delta
     __shared__ float sPq[NS][kRC][CP], sDo[NS][kRC][DB];               // pi^q, dL/do
 
     const LayerArgs &f = a.f;
@@ -368,19 +367,22 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
                 dst[pack_index(t0, t, d0 + kk * TW + w) * JJ + j] = v[x];
         }
     };
-    // pi^q and dL/do of chunk n for the chunk pass (staged inputs in slot sl)
+    // pi^q, c = beta r delta and dL/do of chunk n for the chunk pass (staged
+    // inputs in slot sl)
     auto packs = [&](int n, int sl, auto first, auto nthr) {
         const int t0 = n * kRC, nt = min(kRC, T - t0);
         pack_store(a.qpk, ITag<J>{}, [&](int t, int j, int dd) { return sPq[sl][t][j * DB + dd]; },
                    t0, nt, first, nthr);
+        pack_store(a.cpk, ITag<J>{}, [&](int t, int j, int dd) {
+            const int col = j * DB + dd;
+            return sBeta[sl][t][col] * sR[sl][t][col] * sDelta[sl][t][col];
+        }, t0, nt, first, nthr);
         pack_store(a.dopk, ITag<1>{}, [&](int t, int, int dd) { return sDo[sl][t][dd]; }, t0, nt,
                    first, nthr);
     };
-    // c = beta r delta and dpred of chunk n (its tokens' results in slot sl)
-    auto packs_cp = [&](int n, int sl, auto first, auto nthr) {
+    // dpred of chunk n (its tokens' results in slot sl)
+    auto packs_dpred = [&](int n, int sl, auto first, auto nthr) {
         const int t0 = n * kRC, nt = min(kRC, T - t0);
-        pack_store(a.cpk, ITag<J>{}, [&](int t, int j, int dd) { return sCv[sl][t][j * DB + dd]; },
-                   t0, nt, first, nthr);
         pack_store(a.ppk, ITag<J>{}, [&](int t, int j, int dd) { return sP[sl][t][j * DB + dd]; },
                    t0, nt, first, nthr);
     };
@@ -508,14 +510,20 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
         }
     };
     // the chunk's tokens in reverse, by the sequential wave (tid < 64)
+    // With c_j = beta_j r_j delta_j and sdr = sum_i c_i dc_i over the token's J
+    // components, the per-token step above reads
+    //   da_j = c_j dc_j - r_j sdr
+    //   ddelta_j = beta_j r_j (1 - delta_j^2) dc_j + r_j delta_j sdr
+    // (one component: ddelta = beta dc), so that the dependent chain from one
+    // token's dc to the next is a product, the J-lane sum and two fused
+    // multiply-adds.
     auto tokens = [&](int sl) {
-        // dfr[u] collects sum_{s>u} (k_u . k_s) dpred_s
-        float dfr[kRC], vb[kRC], vd[kRC], vbe[kRC], vr[kRC];
+        // dfr[u] starts at base_u and collects sum_{s>u} (k_u . k_s) dpred_s: dc_u
+        float dfr[kRC], vd[kRC], vbe[kRC], vr[kRC];
         const int scw = sact ? scol : N, sdw = sact && sj == 0 ? sdd : DB;
 #pragma unroll
         for (int u = 0; u < kRC; ++u) {
-            dfr[u] = 0.0f;
-            vb[u] = sact ? sBase[u][scol] : 0.0f;
+            dfr[u] = sact ? sBase[u][scol] : 0.0f;
             vd[u] = sact ? sDelta[sl][u][scol] : 0.0f;
             vbe[u] = sact ? sBeta[sl][u][scol] : 0.0f;
             vr[u] = sact ? sR[sl][u][scol] : 0.0f;
@@ -537,22 +545,28 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
                 float *g = grow[(t - 1) & 1];
                 g[4 * u4] = x.x, g[4 * u4 + 1] = x.y, g[4 * u4 + 2] = x.z, g[4 * u4 + 3] = x.w;
             }
-            __builtin_amdgcn_sched_barrier(0);   // (the scheduler would sink these loads to their use)
-            const float dc = vb[t] + dfr[t];
-            const float dl = vd[t], be = vbe[t], r = vr[t];
-            const float dr = dc * be * dl;
-            const float sdr = group_sum<JP>(r * dr);
-            const float da = J == 1 ? 0.0f : r * (dr - sdr);
-            const float ddelta = dc * be * r - dl * da;
+            // (the scheduler would sink these loads to their use: no LDS read may
+            // cross here; arithmetic and LDS writes may)
+            __builtin_amdgcn_sched_barrier(0x207);
+            const float dc = dfr[t];
+            const float dl = vd[t], br = vbe[t] * vr[t], r = vr[t];
+            float da = 0.0f, ddelta = br * dc;
+            if constexpr (J > 1) {
+                const float c = br * dl, g = fmaf(-c, dl, br);   // beta r (1 - delta^2)
+                const float cdc = c * dc;
+                const float sdr = group_sum<JP>(cdc);
+                da = fmaf(-r, sdr, cdc);
+                ddelta = fmaf(r * dl, sdr, g * dc);
+            }
             const float dvv = group_sum<JP>(ddelta);
             const float dpred = -ddelta;
+            // (the next token's dc first: it is on the dependent chain)
 #pragma unroll
-            for (int u = 0; u < t; ++u) dfr[u] = fmaf(grow[t & 1][u], dpred, dfr[u]);
+            for (int u = t - 1; u >= 0; --u) dfr[u] = fmaf(grow[t & 1][u], dpred, dfr[u]);
             // every lane stores to LDS (idle lanes to a padding column), so that
             // no branch hides from the compiler how many LDS operations are in
             // flight when the next row of K K^T is waited for
             sP[sl][t][scw] = dpred;
-            sCv[sl][t][scw] = be * r * dl;
             sDc[t][scw] = dc;
             sDlk[t][scw] = da;
             sDv[t][sdw] = dvv;
@@ -676,7 +690,7 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
                 } else {
                     checkpoint(n, kF1, kN1);
                     packs(n, sl, kF1, kN1);
-                    if (n < n0) packs_cp(n + 1, sl ^ 1, kF1, kN1);
+                    if (n < n0) packs_dpred(n + 1, sl ^ 1, kF1, kN1);
                     if (n > 0) {
                         stage(n - 1, sl ^ 1);
                         if (n > 1) fetch(n - 2);   // lands during chunks n and n - 1
@@ -689,7 +703,7 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
                 block_sync_lds();   // C: E now from the tokens after chunk n - 1
                 if (n > 0) base(sl ^ 1);
             }
-            packs_cp(0, 0, kF0, kN0);   // chunk 0's tokens ended before the last barrier B
+            packs_dpred(0, 0, kF0, kN0);   // chunk 0's tokens ended before the last barrier B
         }
     } else {
         if (NCH > 0) fetch(NCH - 1);
@@ -708,7 +722,7 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
             block_sync_lds();
             update_e(0);
             outputs(n, 0);
-            packs_cp(n, 0, kF0, kN0);
+            packs_dpred(n, 0, kF0, kN0);
         }
     }
     block_sync_lds();
