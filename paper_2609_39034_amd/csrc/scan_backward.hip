@@ -36,10 +36,10 @@
 //    chunk-sized operands.  The query-prior logit gradient needs the
 //    retrievals y_{tjd} = w_{t,jd} . q_t = (Q S + tril(Q K^T) C)_{t,col}:
 //    dlq_j = pi^q_j do (y_j - sum_i pi^q_i y_i).  Column tiles of all J
-//    components of DT output dims stream through LDS; each thread accumulates a
-//    TM x TN block of (token, key index) outputs in registers, and the
-//    intra-chunk sums become three masked C x C coefficient matrices applied to
-//    the chunk's K and Q at the end.
+//    components of DT output dims stream through LDS; every product runs on the
+//    matrix cores in fp32 (16 x 16 output tiles spread over the four waves),
+//    and the intra-chunk sums become three masked C x C coefficient matrices
+//    applied to the chunk's K and Q at the end.
 #include "device_common.hpp"
 #include "launch.hpp"
 
