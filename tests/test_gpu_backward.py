@@ -78,7 +78,7 @@ CASES = [
     (1, 2, 130, 64, 64, 4, "f32", 0.1, True),      # five chunks, two staging rounds each
     (1, 2, 45, 32, 16, 1, "f32", 0.2, True),       # reverse blocks of 8 dims, half a tile
     (2, 1, 70, 64, 16, 2, "bf16", 0.1, False),     # the same with two components
-    (1, 2, 75, 64, 48, 3, "bf16", 0.2, True),      # J = 3 on the matrix cores: padded columns
+    (1, 2, 75, 64, 32, 3, "bf16", 0.2, True),      # J = 3 on the matrix cores: padded columns
     (2, 1, 40, 16, 32, 4, "bf16", 0.0, True),      # Dk = 16: dq, dk tiles on two waves
 ]
 
