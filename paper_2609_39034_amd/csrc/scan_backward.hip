@@ -139,12 +139,15 @@ __device__ __forceinline__ floatx4 mma(const uint32_t (&a)[4], const uint32_t (&
 // the chunk pass's operands meanwhile), and the update of E, each step between
 // block barriers.  bf16 inputs: the staged inputs have two slots (chunk m in
 // slot m & 1) and three barriers per chunk:
-//   A  the sequential wave runs chunk n's tokens; the other waves store its
-//      operands for the chunk pass, stage chunk n-1 into the other slot from
-//      registers and issue the loads of chunk n-2
-//   B  E += Q_n^T Y_n + K_n^T P_n, chunk n's outputs, the Gram products of
+//   A  the sequential wave runs chunk n's tokens; the other waves store the
+//      chunk pass's operands (chunk n's pi^q, c and dL/do, chunk n+1's dpred),
+//      stage chunk n-1 into the other slot from registers and issue the loads
+//      of chunk n-2
+//   B  E += Q_n^T Y_n + K_n^T P_n; waves 2 and 3 also the Gram products of
 //      chunk n-1
-//   C  the base of chunk n-1 from the new E.
+//   C  the base of chunk n-1 from the new E (one wave per 16-column tile);
+//      chunk n's outputs on waves 2 and 3 when there are two tiles or fewer,
+//      else in B.
 template <int DK, int J, int DB, bool IBF>
 __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a) {
     constexpr int JP = J == 3 ? 4 : J;   // lanes per output dim (J = 3 padded)
@@ -411,13 +414,13 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
         }
     };
     // Gram products of the chunk in slot sl: on the matrix cores (bf16 inputs;
-    // wave 0 K K^T, wave 1 K Q^T), else one (t, s) pair per thread
+    // wave 2 K K^T, wave 3 K Q^T), else one (t, s) pair per thread
     auto gram = [&](int sl) {
         if constexpr (IBF) {
-            if (wv < 2) {
+            if (wv >= 2) {
                 // D[row][col] = sum_i A[row][i] K[col][i], A = K (D[t][s]) or Q
                 // (D[s][t] = k_t . q_s); lane: row / col tl, k slot lg
-                const float (*A)[KP] = wv == 0 ? sK[sl] : sQ[sl];
+                const float (*A)[KP] = wv == 2 ? sK[sl] : sQ[sl];
                 floatx4 acc = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                 for (int i0 = 0; i0 < DK; i0 += KM * 4) {
@@ -427,7 +430,7 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
                 }
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
-                    if (wv == 0) sGkk[4 * lg + r][tl] = acc[r];
+                    if (wv == 2) sGkk[4 * lg + r][tl] = acc[r];
                     else sGkqT[4 * lg + r][tl] = acc[r];
                 }
             }
@@ -577,31 +580,50 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
     // matrix cores (bf16 inputs), else four columns per thread
     auto update_e = [&](int sl) {
         if constexpr (IBF) {
-            for (int tile = wv; tile < (DK / 16) * NTC; tile += kThreads / 64) {
-                const int ti = tile / NTC, ct = tile % NTC;
-                const int col = 16 * ct + tl;
-                const bool cv = col < N;
-                floatx4 acc;
+            // tiles wv, wv + 4, ..., two at a time with every LDS read of both
+            // issued before their products (a clamped duplicate past the end
+            // is computed and not stored)
+            constexpr int NTL = (DK / 16) * NTC, NU = (NTL + 3) / 4;
 #pragma unroll
-                for (int r = 0; r < 4; ++r) acc[r] = cv ? sE[16 * ti + 4 * lg + r][col] : 0.0f;
-                // A = Q^T, K^T: rows i = 16 ti + tl, k = t = 4 lg .. + 3
-                float qv[4], kv[4], yv[4], pv[4];
+            for (int u0 = 0; u0 < NU; u0 += 2) {
+                constexpr int NP2 = NU > 1 ? 2 : 1;
+                floatx4 acc[NP2];
+                KOp<4> qa[NP2], ka[NP2], yb[NP2], pb[NP2];
 #pragma unroll
-                for (int m = 0; m < 4; ++m) {
-                    qv[m] = sQ[sl][4 * lg + m][16 * ti + tl];
-                    kv[m] = sK[sl][4 * lg + m][16 * ti + tl];
-                    yv[m] = cv ? sY[sl][4 * lg + m][col] : 0.0f;
-                    pv[m] = cv ? sP[sl][4 * lg + m][col] : 0.0f;
+                for (int x = 0; x < NP2; ++x) {
+                    const int tile = min(wv + 4 * (u0 + x), NTL - 1);
+                    const int ti = tile / NTC, col = 16 * (tile % NTC) + tl;
+                    const bool cv = col < N;
+                    const int cc = cv ? col : 0;
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) acc[x][r] = cv ? sE[16 * ti + 4 * lg + r][cc] : 0.0f;
+                    // A = Q^T, K^T: rows i = 16 ti + tl, k = t = 4 lg .. + 3
+                    float qv[4], kv[4], yv[4], pv[4];
+#pragma unroll
+                    for (int m = 0; m < 4; ++m) {
+                        qv[m] = sQ[sl][4 * lg + m][16 * ti + tl];
+                        kv[m] = sK[sl][4 * lg + m][16 * ti + tl];
+                        yv[m] = cv ? sY[sl][4 * lg + m][cc] : 0.0f;
+                        pv[m] = cv ? sP[sl][4 * lg + m][cc] : 0.0f;
+                    }
+                    qa[x] = kop_exact<4>(qv), ka[x] = kop_exact<4>(kv);
+                    yb[x] = kop_split<4>(yv), pb[x] = kop_split<4>(pv);
                 }
-                const KOp<4> qa = kop_exact<4>(qv), ka = kop_exact<4>(kv);
-                const KOp<4> yb = kop_split<4>(yv), pb = kop_split<4>(pv);
-                acc = mma(qa.hi, yb.hi, acc);
-                acc = mma(qa.hi, yb.lo, acc);
-                acc = mma(ka.hi, pb.hi, acc);
-                acc = mma(ka.hi, pb.lo, acc);
-                if (cv) {
 #pragma unroll
-                    for (int r = 0; r < 4; ++r) sE[16 * ti + 4 * lg + r][col] = acc[r];
+                for (int x = 0; x < NP2; ++x) {
+                    acc[x] = mma(qa[x].hi, yb[x].hi, acc[x]);
+                    acc[x] = mma(qa[x].hi, yb[x].lo, acc[x]);
+                    acc[x] = mma(ka[x].hi, pb[x].hi, acc[x]);
+                    acc[x] = mma(ka[x].hi, pb[x].lo, acc[x]);
+                }
+#pragma unroll
+                for (int x = 0; x < NP2; ++x) {
+                    const int tile = wv + 4 * (u0 + x);
+                    const int ti = tile / NTC, col = 16 * (tile % NTC) + tl;
+                    if (u0 + x < NU && tile < NTL && col < N) {
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) sE[16 * ti + 4 * lg + r][col] = acc[x][r];
+                    }
                 }
             }
         } else {
@@ -628,16 +650,18 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
         }
     };
     // chunk n's per-token outputs, coalesced over output dims: dL/dlb and dL/dlk
-    // (from the tokens' dc and da and the staged inputs in slot sl) and dv; all
-    // LDS reads are issued before the stores
-    auto outputs = [&](int n, int sl) {
-        const int t0 = n * kRC, nt = min(kRC, T - t0);
-        constexpr int NE = kRC * J * DB, NI = (NE + kThreads - 1) / kThreads;
-        constexpr int NV = (kRC * DB + kThreads - 1) / kThreads;
+    // (from the tokens' dc and da and the staged inputs in slot sl) and dv, by
+    // threads first .. first + nthr - 1; all LDS reads are issued before the
+    // stores
+    auto outputs = [&](int n, int sl, auto first, auto nthr) {
+        constexpr int F = decltype(first)::value, NT = decltype(nthr)::value;
+        const int t0 = n * kRC, nt = min(kRC, T - t0), lt = tid - F;
+        constexpr int NE = kRC * J * DB, NI = (NE + NT - 1) / NT;
+        constexpr int NV = (kRC * DB + NT - 1) / NT;
         float vb[NI], vk[NI], vv[NV];
 #pragma unroll
         for (int x = 0; x < NI; ++x) {
-            const int e = min(tid + kThreads * x, NE - 1);
+            const int e = min(lt + NT * x, NE - 1);
             const int t = e / (J * DB), col = e % (J * DB);
             const float be = sBeta[sl][t][col];
             vb[x] = sDc[t][col] * sR[sl][t][col] * sDelta[sl][t][col] * be * (1.0f - be);
@@ -645,14 +669,14 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
         }
 #pragma unroll
         for (int x = 0; x < NV; ++x) {
-            const int e = min(tid + kThreads * x, kRC * DB - 1);
+            const int e = min(lt + NT * x, kRC * DB - 1);
             vv[x] = sDv[e / DB][e % DB];
         }
 #pragma unroll
         for (int x = 0; x < NI; ++x) {
-            const int e = tid + kThreads * x;
+            const int e = lt + NT * x;
             const int t = e / (J * DB), j = (e / DB) % J, dd = e % DB;
-            if ((NE % kThreads == 0 || e < NE) && t < nt) {
+            if ((NE % NT == 0 || e < NE) && t < nt) {
                 const size_t idx = (((size_t)(b * T + t0 + t) * H + h) * J + j) * Dv + d0 + dd;
                 a.dlb[idx] = vb[x];
                 a.dlk[idx] = vk[x];
@@ -660,8 +684,8 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
         }
 #pragma unroll
         for (int x = 0; x < NV; ++x) {
-            const int e = tid + kThreads * x, t = e / DB, dd = e % DB;
-            if (((kRC * DB) % kThreads == 0 || e < kRC * DB) && t < nt)
+            const int e = lt + NT * x, t = e / DB, dd = e % DB;
+            if (((kRC * DB) % NT == 0 || e < kRC * DB) && t < nt)
                 a.dv[((size_t)(b * T + t0 + t) * H + h) * Dv + d0 + dd] = vv[x];
         }
     };
@@ -669,6 +693,9 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
     constexpr ITag<kThreads - 64> kN1{};
     constexpr ITag<0> kF0{};                // every thread
     constexpr ITag<kThreads> kN0{};
+    constexpr ITag<128> kF2{};              // waves 2 and 3
+    constexpr ITag<kThreads - 128> kN2{};
+
 
     if constexpr (IBF) {
         if (NCH > 0) {
@@ -698,10 +725,14 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
                 }
                 block_sync_lds();   // B: chunk n's dpred published
                 update_e(sl);
-                outputs(n, sl);
-                if (n > 0) gram(sl ^ 1);
+                if (n > 0) gram(sl ^ 1);   // waves 2 and 3
+                if constexpr (NTC > 2) outputs(n, sl, kF0, kN0);
                 block_sync_lds();   // C: E now from the tokens after chunk n - 1
-                if (n > 0) base(sl ^ 1);
+                if (n > 0) base(sl ^ 1);   // waves 0 .. NTC - 1
+                // (with two column tiles, waves 2 and 3 store the outputs meanwhile)
+                if constexpr (NTC <= 2) {
+                    if (wv >= 2) outputs(n, sl, kF2, kN2);
+                }
             }
             packs_dpred(0, 0, kF0, kN0);   // chunk 0's tokens ended before the last barrier B
         }
@@ -721,7 +752,7 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
             if (tid < 64) tokens(0);
             block_sync_lds();
             update_e(0);
-            outputs(n, 0);
+            outputs(n, 0, kF0, kN0);
             packs_dpred(n, 0, kF0, kN0);
         }
     }
