@@ -131,18 +131,32 @@ __device__ __forceinline__ floatx4 mma(const uint32_t (&a)[4], const uint32_t (&
         __builtin_bit_cast(bf16x8, make_uint4(b[0], b[1], b[2], b[3])), c, 0, 0, 0);
 }
 
+// J consecutive floats to global memory (16-byte stores where J allows).
+template <int J>
+__device__ __forceinline__ void st_row(float *p, const float (&v)[J]) {
+    if constexpr (J % 4 == 0) {
+#pragma unroll
+        for (int x = 0; x < J; x += 4)
+            *reinterpret_cast<float4 *>(p + x) = make_float4(v[x], v[x + 1], v[x + 2], v[x + 3]);
+    } else if constexpr (J == 2) {
+        *reinterpret_cast<float2 *>(p) = make_float2(v[0], v[1]);
+    } else {
+#pragma unroll
+        for (int x = 0; x < J; ++x) p[x] = v[x];
+    }
+}
+
 // IBF: bf16 inputs (the input dtype is fixed per instantiation, so that the
 // prefetch has one load variant; dL/do's dtype stays a run-time choice).
 //
 // Schedule.  fp32 inputs: per chunk, every thread stages the chunk, then the
-// Gram products, the base, the sequential wave's tokens (the other waves store
-// the chunk pass's operands meanwhile), and the update of E, each step between
-// block barriers.  bf16 inputs: the staged inputs have two slots (chunk m in
+// Gram products, the base, the sequential wave's tokens, and the update of E,
+// each step between block barriers.  bf16 inputs: the staged inputs have two slots (chunk m in
 // slot m & 1) and three barriers per chunk:
 //   A  the sequential wave runs chunk n's tokens; the other waves store the
-//      chunk pass's operands (chunk n's pi^q, c and dL/do, chunk n+1's dpred),
-//      stage chunk n-1 into the other slot from registers and issue the loads
-//      of chunk n-2
+//      chunk pass's dpred of chunk n+1,
+//      stage chunk n-1 into the other slot from registers (storing its pi^q, c
+//      and dL/do for the chunk pass) and issue the loads of chunk n-2
 //   B  E += Q_n^T Y_n + K_n^T P_n; waves 2 and 3 also the Gram products of
 //      chunk n-1
 //   C  the base of chunk n-1 from the new E (one wave per 16-column tile);
@@ -169,7 +183,6 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
     __shared__ __align__(16) float sBase[kRC][CP], sY[NS][kRC][CP], sP[NS][kRC][CP];
     __shared__ float sDelta[NS][kRC][CP], sBeta[NS][kRC][CP], sR[NS][kRC][CP];
     __shared__ float sDc[kRC][CP], sDlk[kRC][CP], sDv[kRC][DB + 1];   // dc, da, dv
-    __shared__ float sPq[NS][kRC][CP], sDo[NS][kRC][DB];               // pi^q, dL/do
 
     const LayerArgs &f = a.f;
     const int tid = threadIdx.x, lane = tid % 64;
@@ -270,8 +283,22 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
         if (obf) fetch_as(n, BTag<true>{});
         else fetch_as(n, BTag<false>{});
     };
+    // The chunk pass's operands, in its tile order [b, h, interval, tile, token,
+    // dd, j]: the rows of one tile and consecutive tokens are contiguous, so each
+    // store run covers whole lines.  This block's dims cover TW dims of each tile
+    // it touches (all of them, or a part when the block is narrower than a
+    // tile).  Threads first .. first + nthr - 1 store X[t][col] for the chunk's
+    // tokens (trip counts and divisors compile-time; tokens past the end skipped).
+    constexpr int CT = chunk_tile_dims<J>();
+    constexpr int TW = DB < CT ? DB : CT;
+    auto pack_index = [&](int t0, int t, int d) {
+        const size_t pbase = ((size_t)b * H + h) * NC2 + t0 / kBwdChunk;
+        return ((pbase * (Dv / CT) + d / CT) * kBwdChunk + t0 % kBwdChunk + t) * CT + d % CT;
+    };
     // chunk n's registers to slot sl: K, Q (and their transposes for the fp32
-    // products), delta, r, beta, pi^q, dy = dL/do pi^q and dL/do
+    // products), delta, r, beta and dy = dL/do pi^q; and, from the same
+    // registers, the chunk pass's operands pi^q, c = beta r delta and dL/do (a
+    // thread's J components are adjacent there)
     auto stage = [&](int n, int sl) {
         const int t0 = n * kRC, nt = min(kRC, T - t0);
 #pragma unroll
@@ -330,22 +357,17 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
                 sR[sl][t][col] = ee[j];
                 sBeta[sl][t][col] = be[j];
                 sY[sl][t][col] = dov * lq[j];
-                sPq[sl][t][col] = lq[j];
             }
-            sDo[sl][t][dd] = dov;
+            if (t < nt) {
+                const size_t pr = pack_index(t0, t, d0 + dd);
+                float cv[J];
+#pragma unroll
+                for (int j = 0; j < J; ++j) cv[j] = be[j] * ee[j] * dl[j];
+                st_row<J>(a.qpk + pr * J, lq);
+                st_row<J>(a.cpk + pr * J, cv);
+                a.dopk[pr] = dov;
+            }
         }
-    };
-    // The chunk pass's operands, in its tile order [b, h, interval, tile, token,
-    // dd, j]: the rows of one tile and consecutive tokens are contiguous, so each
-    // store run covers whole lines.  This block's dims cover TW dims of each tile
-    // it touches (all of them, or a part when the block is narrower than a
-    // tile).  Threads first .. first + nthr - 1 store X[t][col] for the chunk's
-    // tokens (trip counts and divisors compile-time; tokens past the end skipped).
-    constexpr int CT = chunk_tile_dims<J>();
-    constexpr int TW = DB < CT ? DB : CT;
-    auto pack_index = [&](int t0, int t, int d) {
-        const size_t pbase = ((size_t)b * H + h) * NC2 + t0 / kBwdChunk;
-        return ((pbase * (Dv / CT) + d / CT) * kBwdChunk + t0 % kBwdChunk + t) * CT + d % CT;
     };
     // dst[(tile row of (t, d)) * JJ + j] = val(t, j, dd) for the chunk's tokens,
     // by threads first .. first + nthr - 1 (compile-time: the loop is unrolled
@@ -369,19 +391,6 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
             if ((NE % NT == 0 || e < NE) && t < nt)
                 dst[pack_index(t0, t, d0 + kk * TW + w) * JJ + j] = v[x];
         }
-    };
-    // pi^q, c = beta r delta and dL/do of chunk n for the chunk pass (staged
-    // inputs in slot sl)
-    auto packs = [&](int n, int sl, auto first, auto nthr) {
-        const int t0 = n * kRC, nt = min(kRC, T - t0);
-        pack_store(a.qpk, ITag<J>{}, [&](int t, int j, int dd) { return sPq[sl][t][j * DB + dd]; },
-                   t0, nt, first, nthr);
-        pack_store(a.cpk, ITag<J>{}, [&](int t, int j, int dd) {
-            const int col = j * DB + dd;
-            return sBeta[sl][t][col] * sR[sl][t][col] * sDelta[sl][t][col];
-        }, t0, nt, first, nthr);
-        pack_store(a.dopk, ITag<1>{}, [&](int t, int, int dd) { return sDo[sl][t][dd]; }, t0, nt,
-                   first, nthr);
     };
     // dpred of chunk n (its tokens' results in slot sl)
     auto packs_dpred = [&](int n, int sl, auto first, auto nthr) {
@@ -716,7 +725,6 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
                     tokens(sl);
                 } else {
                     checkpoint(n, kF1, kN1);
-                    packs(n, sl, kF1, kN1);
                     if (n < n0) packs_dpred(n + 1, sl ^ 1, kF1, kN1);
                     if (n > 0) {
                         stage(n - 1, sl ^ 1);
@@ -748,7 +756,6 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
             block_sync_lds();
             base(0);
             block_sync_lds();
-            if (tid >= 64) packs(n, 0, kF1, kN1);
             if (tid < 64) tokens(0);
             block_sync_lds();
             update_e(0);
