@@ -153,8 +153,8 @@ __device__ __forceinline__ void st_row(float *p, const float (&v)[J]) {
 // Gram products, the base, the sequential wave's tokens, and the update of E,
 // each step between block barriers.  bf16 inputs: the staged inputs have two slots (chunk m in
 // slot m & 1) and three barriers per chunk:
-//   A  the sequential wave runs chunk n's tokens; the other waves store the
-//      chunk pass's dpred of chunk n+1,
+//   A  the sequential wave runs chunk n's tokens; the other waves store
+//      chunk n+1's dv and the chunk pass's dpred of chunk n+1,
 //      stage chunk n-1 into the other slot from registers (storing its pi^q, c
 //      and dL/do for the chunk pass) and issue the loads of chunk n-2
 //   B  E += Q_n^T Y_n + K_n^T P_n; waves 2 and 3 also the Gram products of
@@ -182,7 +182,7 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
     __shared__ __align__(16) float sGkqT[kRC][GP];                     // [s][t] = k_t . q_s
     __shared__ __align__(16) float sBase[kRC][CP], sY[NS][kRC][CP], sP[NS][kRC][CP];
     __shared__ float sDelta[NS][kRC][CP], sBeta[NS][kRC][CP], sR[NS][kRC][CP];
-    __shared__ float sDc[kRC][CP], sDlk[kRC][CP], sDv[kRC][DB + 1];   // dc, da, dv
+    __shared__ float sDc[kRC][CP], sDlk[kRC][CP];   // dc, da
 
     const LayerArgs &f = a.f;
     const int tid = threadIdx.x, lane = tid % 64;
@@ -392,6 +392,32 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
                 dst[pack_index(t0, t, d0 + kk * TW + w) * JJ + j] = v[x];
         }
     };
+    // dv of chunk n = -(sum over j of its dpred, slot sl), summed in the pairs
+    // of a J-lane reduction, by threads first .. first + nthr - 1
+    auto dv_store = [&](int n, int sl, auto first, auto nthr) {
+        constexpr int F = decltype(first)::value, NT = decltype(nthr)::value;
+        constexpr int NE = kRC * DB, NI = (NE + NT - 1) / NT;
+        const int t0 = n * kRC, nt = min(kRC, T - t0);
+        float v[NI];
+#pragma unroll
+        for (int x = 0; x < NI; ++x) {
+            const int e = min(tid - F + NT * x, NE - 1), t = e / DB, dd = e % DB;
+            float p[JP];
+#pragma unroll
+            for (int j = 0; j < JP; ++j) p[j] = j < J ? sP[sl][t][j * DB + dd] : 0.0f;
+#pragma unroll
+            for (int w = 1; w < JP; w *= 2)
+#pragma unroll
+                for (int j = 0; j < JP; j += 2 * w) p[j] += p[j + w];
+            v[x] = -p[0];
+        }
+#pragma unroll
+        for (int x = 0; x < NI; ++x) {
+            const int e = tid - F + NT * x, t = e / DB, dd = e % DB;
+            if ((NE % NT == 0 || e < NE) && t < nt)
+                a.dv[((size_t)(b * T + t0 + t) * H + h) * Dv + d0 + dd] = v[x];
+        }
+    };
     // dpred of chunk n (its tokens' results in slot sl)
     auto packs_dpred = [&](int n, int sl, auto first, auto nthr) {
         const int t0 = n * kRC, nt = min(kRC, T - t0);
@@ -532,7 +558,7 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
     auto tokens = [&](int sl) {
         // dfr[u] starts at base_u and collects sum_{s>u} (k_u . k_s) dpred_s: dc_u
         float dfr[kRC], vd[kRC], vbe[kRC], vr[kRC];
-        const int scw = sact ? scol : N, sdw = sact && sj == 0 ? sdd : DB;
+        const int scw = sact ? scol : N;
 #pragma unroll
         for (int u = 0; u < kRC; ++u) {
             dfr[u] = sact ? sBase[u][scol] : 0.0f;
@@ -570,7 +596,6 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
                 da = fmaf(-r, sdr, cdc);
                 ddelta = fmaf(r * dl, sdr, g * dc);
             }
-            const float dvv = group_sum<JP>(ddelta);
             const float dpred = -ddelta;
             // (the next token's dc first: it is on the dependent chain)
 #pragma unroll
@@ -581,7 +606,6 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
             sP[sl][t][scw] = dpred;
             sDc[t][scw] = dc;
             sDlk[t][scw] = da;
-            sDv[t][sdw] = dvv;
         }
     };
     // E += Q^T Y + K^T P for the chunk in slot sl (E then holds the gradient
@@ -659,15 +683,13 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
         }
     };
     // chunk n's per-token outputs, coalesced over output dims: dL/dlb and dL/dlk
-    // (from the tokens' dc and da and the staged inputs in slot sl) and dv, by
-    // threads first .. first + nthr - 1; all LDS reads are issued before the
-    // stores
+    // (from the tokens' dc and da and the staged inputs in slot sl), by threads
+    // first .. first + nthr - 1; all LDS reads are issued before the stores
     auto outputs = [&](int n, int sl, auto first, auto nthr) {
         constexpr int F = decltype(first)::value, NT = decltype(nthr)::value;
         const int t0 = n * kRC, nt = min(kRC, T - t0), lt = tid - F;
         constexpr int NE = kRC * J * DB, NI = (NE + NT - 1) / NT;
-        constexpr int NV = (kRC * DB + NT - 1) / NT;
-        float vb[NI], vk[NI], vv[NV];
+        float vb[NI], vk[NI];
 #pragma unroll
         for (int x = 0; x < NI; ++x) {
             const int e = min(lt + NT * x, NE - 1);
@@ -675,11 +697,6 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
             const float be = sBeta[sl][t][col];
             vb[x] = sDc[t][col] * sR[sl][t][col] * sDelta[sl][t][col] * be * (1.0f - be);
             vk[x] = sDlk[t][col];
-        }
-#pragma unroll
-        for (int x = 0; x < NV; ++x) {
-            const int e = min(lt + NT * x, kRC * DB - 1);
-            vv[x] = sDv[e / DB][e % DB];
         }
 #pragma unroll
         for (int x = 0; x < NI; ++x) {
@@ -690,12 +707,6 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
                 a.dlb[idx] = vb[x];
                 a.dlk[idx] = vk[x];
             }
-        }
-#pragma unroll
-        for (int x = 0; x < NV; ++x) {
-            const int e = lt + NT * x, t = e / DB, dd = e % DB;
-            if (((kRC * DB) % NT == 0 || e < kRC * DB) && t < nt)
-                a.dv[((size_t)(b * T + t0 + t) * H + h) * Dv + d0 + dd] = vv[x];
         }
     };
     constexpr ITag<64> kF1{};               // the staging threads of the bf16 schedule
@@ -725,7 +736,10 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
                     tokens(sl);
                 } else {
                     checkpoint(n, kF1, kN1);
-                    if (n < n0) packs_dpred(n + 1, sl ^ 1, kF1, kN1);
+                    if (n < n0) {
+                        packs_dpred(n + 1, sl ^ 1, kF1, kN1);
+                        dv_store(n + 1, sl ^ 1, kF1, kN1);
+                    }
                     if (n > 0) {
                         stage(n - 1, sl ^ 1);
                         if (n > 1) fetch(n - 2);   // lands during chunks n and n - 1
@@ -742,7 +756,9 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
                     if (wv >= 2) outputs(n, sl, kF2, kN2);
                 }
             }
-            packs_dpred(0, 0, kF0, kN0);   // chunk 0's tokens ended before the last barrier B
+            // chunk 0's tokens ended before the last barrier B
+            packs_dpred(0, 0, kF0, kN0);
+            dv_store(0, 0, kF0, kN0);
         }
     } else {
         if (NCH > 0) fetch(NCH - 1);
@@ -761,6 +777,7 @@ __global__ __launch_bounds__(kThreads) void reverse_chunk_kernel(BackwardArgs a)
             update_e(0);
             outputs(n, 0, kF0, kN0);
             packs_dpred(n, 0, kF0, kN0);
+            dv_store(n, 0, kF0, kN0);
         }
     }
     block_sync_lds();
