@@ -30,8 +30,10 @@
  *                            weight i of component j for output dimension d,
  *                            i.e. (W_j)_{d,i} in the paper's notation (App. B.4)
  *   - q, k, v and the logits share one dtype (opts->in_dtype); o has
- *     opts->out_dtype; the state and all arithmetic are fp32.  bf16 values are
- *     widened exactly; o is rounded to nearest-even when it is bf16.
+ *     opts->out_dtype; the state, the scalar recurrence and every accumulation
+ *     are fp32 (the matrix-core forms multiply fp32 operands as a bf16 high part
+ *     and a bf16 residual, see swila_algo).  bf16 values are widened exactly; o
+ *     is rounded to nearest-even when it is bf16.
  *   - stream is a hipStream_t (NULL = the null stream).  Work is enqueued and
  *     the call returns; device faults surface at the caller's next sync.
  *   - Return value: SWILA_OK, or a negative status.  Argument errors are found
@@ -311,7 +313,10 @@ int swila_decode_step_gated(const swila_shape *shape, const swila_opts *opts,
  * eq. responsibility, eq. retrieval, with the logits of App. B.2): the exact
  * gradient of a scalar loss L through the forward, for training.  The paper
  * trains through the sequential evaluation and gives no backward formulas;
- * this is the chain rule of that forward, evaluated in fp32.
+ * this is the chain rule of that forward, evaluated with fp32 values and
+ * accumulation (with bf16 inputs the reverse scan's Dk-long products take fp32
+ * operands as a bf16 high part and residual on the matrix cores; the final
+ * pass multiplies in fp32 on the matrix cores).
  *   q, k, v, beta_logit, prior_k_logit, prior_q_logit, state_in: the forward's
  *              inputs, as in swila_forward (state_in NULL = zeros).
  *   grad_o:    dL/do [B,T,H,Dv], out_dtype; required when T > 0.
