@@ -149,12 +149,14 @@ def test_backward_frozen_state():
     assert float(dq.abs().max()) > 0.0
 
 
-def test_backward_config2_sampled_heads():
+def test_backward_config2_every_head():
     """The standard bf16 training batch (B=4 H=8 T=2048 Dk=Dv=64 J=4, zero initial
-    state) as the benchmark runs it; the oracle on sampled heads."""
+    state) as the benchmark runs it; the oracle on every (b, h), one after another
+    (about 0.7 s each), the worst error over the heads per gradient."""
     c = workloads.CONFIGS[2]
+    heads = [(b, h) for b in range(c["B"]) for h in range(c["H"])]
     errs = _run(c["B"], c["H"], c["T"], c["Dk"], c["Dv"], c["J"], "bf16", 0.0, False,
-                seed=1002, heads=[(0, 0), (3, 7), (2, 4)])
+                seed=1002, heads=heads)
     print(" ".join("%s %.2e" % kv for kv in errs.items()))
     assert all(v <= 2e-2 for v in errs.values()), errs
 

@@ -1,11 +1,12 @@
-"""Oracle parity on every head of the largest configurations, in the launch
-shape the benchmark times, through the C ABI.
+"""Oracle parity on every head of the standard and the largest configurations,
+in the launch shape the benchmark times, through the C ABI.
 
+  c2  B=4  H=8  T=2048  Dk=Dv=64  J=4  the standard training batch
   c3  B=8  H=16 T=4096  Dk=Dv=128 J=4  LM-shaped projections
   c5  B=2  H=8  T=16384 Dk=Dv=128 J=8  recall-shaped long context
   c4  B=256 H=16 Dk=Dv=128 J=4, 512 in-place decode steps from N(0, 0.1^2)
 
-For c3 and c5: the plain forward (outputs, final state, responsibilities), the
+For c2, c3 and c5: the plain forward (outputs, final state, responsibilities), the
 App. D form run to convergence (its fixed point is the sequential trajectory,
 App. D.1), the temporal form (App. B.3; gate logits N(0,1)) and the gated form
 (App. B.4; decay logits N(2,1)), each against the fp64 oracle on the whole
@@ -55,7 +56,7 @@ def _report(cfg, form, **errs):
         assert e <= TOL_BF16, (name, e)
 
 
-@pytest.mark.parametrize("cfg", [3, 5])
+@pytest.mark.parametrize("cfg", [2, 3, 5])
 class TestEveryHead:
     def test_plain(self, cfg):
         import torch
