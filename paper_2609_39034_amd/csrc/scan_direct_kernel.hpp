@@ -59,7 +59,10 @@ constexpr int max_cols(int L, int J, bool tp) {
     return n;
 }
 
-template <int DK, int J, int S, bool TP, bool GT, bool AX>
+// IBF: bf16 inputs.  The input dtype is fixed per instantiation, so that every
+// staging load has one form and none sits in a branch on it (a load in one arm
+// of a branch is waited for where the arms join).
+template <int DK, int J, int S, bool TP, bool GT, bool AX, bool IBF>
 __global__ __launch_bounds__(kThreads) void scan_direct_kernel(LayerArgs a, int ncol) {
     static_assert(kBwdChunk % kTC == 0, "checkpoints fall on round starts");
     constexpr int L = DK / S;             // lanes per output column
@@ -95,7 +98,8 @@ __global__ __launch_bounds__(kThreads) void scan_direct_kernel(LayerArgs a, int 
     const int h = hh % gridDim.y, b = hh / gridDim.y;
     const int H = a.H, T = a.T, Dv = a.Dv;
     const int d = d0 + dl;
-    const bool ibf = a.in_bf16, obf = a.out_bf16;
+    constexpr bool ibf = IBF;
+    const bool obf = a.out_bf16;
 
     float w[J][S];
     const size_t sbase = ((size_t)b * H + h) * J * DK * Dv;
@@ -176,43 +180,45 @@ __global__ __launch_bounds__(kThreads) void scan_direct_kernel(LayerArgs a, int 
         j = rem / (DK / 4), i = (rem % (DK / 4)) * 4;
         return g < un * J * (DK / 4);
     };
+    // Every thread loads every item it may own, from a clamped index (the
+    // round's last item past the end), with no branch around the load: a load
+    // behind a branch is waited for where the branch joins, which would put the
+    // HBM latency of each load back on the sequential path.  commit stores only
+    // the items that exist.
     auto issue = [&](int u0) {   // the raw loads of the round that starts at token u0
         const int un = min(kTC, T - u0);
 #pragma unroll
         for (int x = 0; x < NKQ; ++x) {
-            const int g = tid + x * nthr;
-            if (g < un * (DK / 4)) {
-                const size_t off = ((size_t)(b * T + u0 + g / (DK / 4)) * H + h) * DK +
-                                   (g % (DK / 4)) * 4;
-                pk[x] = raw4(a.k, off, ibf);
-                pq[x] = raw4(a.q, off, ibf);
-            }
+            const int g = min(tid + x * nthr, un * (DK / 4) - 1);
+            const size_t off = ((size_t)(b * T + u0 + g / (DK / 4)) * H + h) * DK +
+                               (g % (DK / 4)) * 4;
+            pk[x] = raw4(a.k, off, ibf);
+            pq[x] = raw4(a.q, off, ibf);
         }
 #pragma unroll
         for (int x = 0; x < NI; ++x) {
-            const int g = tid + x * nthr;
-            if (g < un * ncol) {
-                const int tt = g / ncol, c = g % ncol;
-                const size_t row = (size_t)(b * T + u0 + tt) * H + h;
-                pv[x] = raw1(a.v, row * Dv + d0 + c, ibf);
+            const int g = min(tid + x * nthr, un * ncol - 1);
+            const int tt = g / ncol, c = g % ncol;
+            const size_t row = (size_t)(b * T + u0 + tt) * H + h;
+            pv[x] = raw1(a.v, row * Dv + d0 + c, ibf);
 #pragma unroll
-                for (int j = 0; j < J; ++j) {
-                    const size_t idx = (row * J + j) * Dv + d0 + c;
-                    pb[x][j] = raw1(a.lb, idx, ibf);
-                    plk[x][j] = raw1(a.lk, idx, ibf);
-                    plq[x][j] = raw1(a.lq, idx, ibf);
-                }
-                if constexpr (TP) {
-                    pgk[x] = raw1(a.gk, row * Dv + d0 + c, ibf);
-                    pgq[x] = raw1(a.gq, row * Dv + d0 + c, ibf);
-                }
+            for (int j = 0; j < J; ++j) {
+                const size_t idx = (row * J + j) * Dv + d0 + c;
+                pb[x][j] = raw1(a.lb, idx, ibf);
+                plk[x][j] = raw1(a.lk, idx, ibf);
+                plq[x][j] = raw1(a.lq, idx, ibf);
+            }
+            if constexpr (TP) {
+                pgk[x] = raw1(a.gk, row * Dv + d0 + c, ibf);
+                pgq[x] = raw1(a.gq, row * Dv + d0 + c, ibf);
             }
         }
 #pragma unroll
         for (int x = 0; x < ND; ++x) {
-            int tt, j, i;
-            if (dpiece_n(x, un, tt, j, i))
-                pd[x] = raw4(a.decay, (((size_t)(b * T + u0 + tt) * H + h) * J + j) * DK + i, ibf);
+            const int g = min(tid + x * nthr, un * J * (DK / 4) - 1);
+            const int tt = g / (J * (DK / 4)), rem = g % (J * (DK / 4));
+            const int j = rem / (DK / 4), i = (rem % (DK / 4)) * 4;
+            pd[x] = raw4(a.decay, (((size_t)(b * T + u0 + tt) * H + h) * J + j) * DK + i, ibf);
         }
     };
     auto commit = [&](int u0) {   // convert the issued round and store it to LDS
@@ -477,7 +483,12 @@ hipError_t launch_s(const LayerArgs &a, hipStream_t stream) {
     const int ncol = a.Dv < max_cols(L, J, TP) ? a.Dv : max_cols(L, J, TP);
     dim3 grid(a.Dv / ncol, a.H, a.B);
     dim3 block(ncol * L);
-    hipLaunchKernelGGL((scan_direct_kernel<DK, J, S, TP, GT, AX>), grid, block, 0, stream, a, ncol);
+    if (a.in_bf16)
+        hipLaunchKernelGGL((scan_direct_kernel<DK, J, S, TP, GT, AX, true>), grid, block, 0, stream, a,
+                           ncol);
+    else
+        hipLaunchKernelGGL((scan_direct_kernel<DK, J, S, TP, GT, AX, false>), grid, block, 0, stream, a,
+                           ncol);
     return hipGetLastError();
 }
 
