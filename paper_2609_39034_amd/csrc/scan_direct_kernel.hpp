@@ -248,8 +248,41 @@ __global__ __launch_bounds__(kThreads) void scan_direct_kernel(LayerArgs a, int 
             }
         }
     };
+    // The token loop leaves each token's output in sO and, where they are
+    // asked for, r in the token's beta slot and delta in its key-prior slot,
+    // both read for the last time by that token.  They go to HBM at the top
+    // of the next round (and after the last one), so that the token loop
+    // holds no global store: with one in it, the compiler waits for every
+    // load in flight before the loop starts, the next round's prefetch
+    // included.  A thread writes out the items g = tid + x nthr, which are
+    // the ones it also stages, so none is overwritten before it is read.
+    auto flush = [&](int u0, int un) {
+        for (int g = tid; g < un * ncol; g += nthr) {
+            const int tt = g / ncol, c = g % ncol;
+            const size_t row = (size_t)(b * T + u0 + tt) * H + h;
+            if constexpr (!AX) store1(a.o, row * Dv + d0 + c, sO[tt][c], obf);
+            if (a.resp) {
+#pragma unroll
+                for (int j = 0; j < J; ++j) a.resp[(row * J + j) * Dv + d0 + c] = sBeta[tt][j][c];
+            }
+            if constexpr (AX) {
+#pragma unroll
+                for (int j = 0; j < J; ++j) a.delta_out[(row * J + j) * Dv + d0 + c] = sLk[tt][j][c];
+            }
+        }
+    };
     if constexpr (PF) {
         if (T > 0) issue(0);
+    }
+    // The state (and the temporal priors) must have landed before the first
+    // token; waiting for them here, behind the first round's loads, keeps the
+    // compiler from placing a wait for every load in flight inside the token
+    // loop, where the next round's prefetch would be waited for.
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+#pragma unroll
+        for (int s = 0; s < S; ++s) asm volatile("" : "+v"(w[j][s]));
+        if constexpr (TP) asm volatile("" : "+v"(rprev[j]), "+v"(rho[j]));
     }
 
     for (int t0 = 0; t0 < T; t0 += kTC) {
@@ -267,12 +300,7 @@ __global__ __launch_bounds__(kThreads) void scan_direct_kernel(LayerArgs a, int 
             }
         }
         block_sync_lds();
-        if (!AX && t0 > 0) {  // outputs of the previous (full) round
-            for (int g = tid; g < kTC * ncol; g += nthr) {
-                const int tt = g / ncol, c = g % ncol;
-                store1(a.o, ((size_t)(b * T + t0 - kTC + tt) * H + h) * Dv + d0 + c, sO[tt][c], obf);
-            }
-        }
+        if (t0 > 0) flush(t0 - kTC, kTC);   // the previous (full) round
         // Staging issues every load of a batch before it converts anything:
         // loading and converting element by element would make each load wait
         // for its data before the next one is issued.  The block barriers order
@@ -441,23 +469,19 @@ __global__ __launch_bounds__(kThreads) void scan_direct_kernel(LayerArgs a, int 
                     pq = rho[j];
                 }
                 o = fmaf(pq, fmaf(c, kq, y[j]), o);
-                if (a.resp && l == 0)
-                    a.resp[(((size_t)(b * T + t0 + tt) * H + h) * J + j) * Dv + d] = r;
-                if (AX && l == 0)
-                    a.delta_out[(((size_t)(b * T + t0 + tt) * H + h) * J + j) * Dv + d] = delta[j];
+                // r and delta wait in slots that this token has read for the last
+                // time (every lane of the column writes the same value)
+                sBeta[tt][j][dl] = r;
+                if constexpr (AX) sLk[tt][j][dl] = delta[j];
             }
             if (l == 0) sO[tt][dl] = o;
         }
     }
 
     block_sync_lds();
-    if (!AX && T > 0) {
+    if (T > 0) {
         const int tl = ((T - 1) / kTC) * kTC;
-        const int nt = T - tl;
-        for (int g = tid; g < nt * ncol; g += nthr) {
-            const int tt = g / ncol, c = g % ncol;
-            store1(a.o, ((size_t)(b * T + tl + tt) * H + h) * Dv + d0 + c, sO[tt][c], obf);
-        }
+        flush(tl, T - tl);
     }
     if (a.state_out) {
 #pragma unroll
